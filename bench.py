@@ -1,0 +1,326 @@
+"""Benchmark of the RaBitQCache decode hot path on one MI355X.
+
+A step is one pass of the whole path over the 128K-context GQA workload
+(batch 1, 32 query / 8 KV heads, head_dim 128, bf16 K/V, 130,816 indexed keys
+plus a 256-key local window): query quantisation -> binary x INT4 scoring of
+every indexed key -> Top-p selection -> sparse attention over the selection and
+the window -> lazy flush (re-encoding the 256 window keys into the index).
+Inputs are resident in HBM before timing; several replicas of the cache and
+index rotate between steps so that a step does not find the previous step's
+data in the 256 MB Infinity Cache.
+
+One JSON line is printed (rank 0, N = 1). `value` = proxy-scored (query head,
+key) pairs per second over the whole step; `ms_per_step` is the sparse decode
+step latency at 128K, compared against dense bf16 decode at the same shape
+(this library's split-K kernel and torch SDPA, the faster of the two).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import subprocess
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def _git_sha():
+    try:
+        return subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"], capture_output=True,
+                              text=True).stdout.strip() or None
+    except Exception:
+        return None
+
+
+def _clone_state(st, pipeline):
+    import torch
+    c = pipeline.DecodeState(st.B, st.Hq, st.Hkv, st.D, st.cap, st.n, st.w, st.K.clone(), st.V.clone(), st.q,
+                             st.P, st.c_q, st.device)
+    for name in ("c_k", "codes", "kfac"):
+        getattr(c, name).copy_(getattr(st, name))
+    torch.cuda.synchronize()
+    return c
+
+
+def _stage_bytes(st, p_counts):
+    """Algorithmic HBM bytes of each stage for one step (the minimum each must move)."""
+    B, Hq, Hkv, D, n, w = st.B, st.Hq, st.Hkv, st.D, st.n, st.w
+    sel_total = float(p_counts["sel_total"])
+    union_rows = float(p_counts["union_rows"])
+    return {
+        "quantize": B * Hq * D * 4 + D * D * 4 + B * Hq * (64 + 32),
+        "score": B * Hkv * n * (D // 8 + 8) + B * Hq * n * 4,
+        "topp": B * Hq * n * 4 + sel_total * 4,
+        "sparse_decode": union_rows * 2 * D * 2 + B * Hkv * w * 2 * D * 2 + sel_total * 4 + B * Hq * D * 4,
+        "flush": B * Hkv * w * (D * 2 + D // 8 + 8),
+    }
+
+
+def _union_rows(st):
+    """Distinct indexed rows gathered per KV group (the sparse decode's K/V reads)."""
+    sel = st.sel_idx.cpu().numpy()
+    cnt = st.sel_count.cpu().numpy()
+    G = st.Hq // st.Hkv
+    tot = 0
+    for b in range(st.B):
+        for hk in range(st.Hkv):
+            rows = [sel[b, h, :cnt[b, h]] for h in range(hk * G, (hk + 1) * G)]
+            tot += np.unique(np.concatenate(rows)).size if rows else 0
+    return tot, int(cnt.sum())
+
+
+def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
+    """The oracle (fp64 NumPy), untuned, on a bounded sample of the same workload:
+    whole KV groups (G query heads over all indexed keys) through one decode step
+    each (quantise, score, Top-p, sparse attention, flush), until ~budget_s."""
+    from oracle import rbq_oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = 1
+    n, w, G, D = wl.n_index, wl.w, wl.G, wl.D
+    tau = 1.0 / math.sqrt(D)
+    done_keys, t_total, groups = 0, 0.0, 0
+    for hk in range(wl.Hkv):
+        K = wl.K_f32(0, hk).astype(np.float64)
+        V = wl.V_f32(0, hk).astype(np.float64)
+        enc = orc.encode_keys(K[:n], wl.P, c_q=wl.c_q[0, hk])          # index build: not part of a step
+        t0 = time.perf_counter()
+        for g in range(G):
+            h = hk * G + g
+            qq = orc.quantize_query(wl.q[0, h], wl.P, wl.c_q[0, hk], enc["c_k"])
+            est = orc.estimate_scores(enc, qq)
+            sel = orc.topp_select(est["S"], wl.p, tau)
+            orc.sparse_decode(wl.q[0, h], K[:n], V[:n], sel["idx"], K[n:n + w], V[n:n + w], tau)
+        orc.encode_keys(K[n:n + w], wl.P, c_k=enc["c_k"], c_q=wl.c_q[0, hk])   # lazy flush
+        t_total += time.perf_counter() - t0
+        done_keys += G * n
+        groups += 1
+        if t_total >= budget_s:
+            break
+    return {"value": done_keys / t_total, "unit": "keys/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{groups} of {wl.Hkv} KV groups of the 128K workload, one decode step each "
+                      f"({G} query heads x {n} keys per group; index build excluded), {t_total:.1f} s"}
+
+
+def time_scan_c5(pipeline, gen, torch, steps, warmup, replicas=4):
+    """Standalone rbq_score scan on the wide-head workload (batch 4 x 128K, 64/8 heads)."""
+    wl = gen.config5()
+    st = pipeline.DecodeState.from_workload(wl)
+    st.build_index()
+    st.quantize()
+    torch.cuda.synchronize()
+    reps = [st]
+    for _ in range(replicas - 1):
+        c = pipeline.DecodeState.__new__(pipeline.DecodeState)
+        c.__dict__.update(st.__dict__)
+        c.codes, c.kfac, c.scores = st.codes.clone(), st.kfac.clone(), torch.empty_like(st.scores)
+        reps.append(c)
+    del wl
+    for i in range(warmup):
+        reps[i % replicas].score()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for i in range(steps):
+        evs[i][0].record()
+        reps[i % replicas].score()
+        evs[i][1].record()
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    B, Hq, Hkv, D, n = st.B, st.Hq, st.Hkv, st.D, st.n
+    nbytes = B * Hkv * n * (D // 8 + 8) + B * Hq * n * 4
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"workload": "gqa 64q/8kv ctx=128K b=4 bf16 student-t", "kernel": "score_kernel",
+            "ms": ms, "keys_per_s": B * Hq * n / (ms * 1e-3), "kv_keys_per_s": B * Hkv * n / (ms * 1e-3),
+            "bytes": nbytes, "GBps": gbs, "frac_hbm": gbs / HBM_PEAK_GBS}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--p", type=float, default=0.95)
+    ap.add_argument("--replicas", type=int, default=4)
+    ap.add_argument("--no-scan", action="store_true", help="skip the standalone wide-head scan")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--sweep", action="store_true", help="also time p = 0.8 / 0.9 / 0.99")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this path is built and measured "
+              f"on a single MI355X. Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_31519_amd import pipeline
+    from workloads import gen
+
+    torch.cuda.set_device(0)
+    t_gen = time.perf_counter()
+    wl = gen.config3()
+    t_gen = time.perf_counter() - t_gen
+    st0 = pipeline.DecodeState.from_workload(wl)
+    st0.build_index()
+    torch.cuda.synchronize()
+    reps = [st0] + [_clone_state(st0, pipeline) for _ in range(args.replicas - 1)]
+    p = args.p
+
+    stages = ["quantize", "score", "topp", "sparse_decode", "flush"]
+
+    def run_step(st, evs=None):
+        if evs is not None:
+            evs[0].record()
+        st.quantize()
+        if evs is not None:
+            evs[1].record()
+        st.score()
+        if evs is not None:
+            evs[2].record()
+        st.select(p)
+        if evs is not None:
+            evs[3].record()
+        st.sparse_decode()
+        if evs is not None:
+            evs[4].record()
+        st.flush_window()
+        if evs is not None:
+            evs[5].record()
+
+    for i in range(args.warmup):
+        run_step(reps[i % len(reps)])
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(args.steps):
+        run_step(reps[i % len(reps)], evs[i])
+    t1.record()
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    stage_ms = {s: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs])) for k, s in enumerate(stages)}
+
+    union_rows, sel_total = _union_rows(st0)
+    sbytes = _stage_bytes(st0, {"sel_total": sel_total, "union_rows": union_rows})
+
+    # dense bf16 decode at the same shape: this library's kernel, then torch SDPA
+    dense_out = torch.empty_like(st0.out)
+    dense_lse = torch.empty_like(st0.lse)
+    for i in range(args.warmup):
+        reps[i % len(reps)].dense_decode(dense_out, dense_lse)
+    torch.cuda.synchronize()
+    d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    d0.record()
+    for i in range(args.steps):
+        reps[i % len(reps)].dense_decode(dense_out, dense_lse)
+    d1.record()
+    torch.cuda.synchronize()
+    dense_ms = d0.elapsed_time(d1) / args.steps
+    sdpa_ms = None
+    try:
+        N = st0.n + st0.w
+        qs = [r.q.view(1, r.Hq, 1, r.D).to(torch.bfloat16) for r in reps]
+        for i in range(args.warmup):
+            r = reps[i % len(reps)]
+            torch.nn.functional.scaled_dot_product_attention(qs[i % len(reps)], r.K[:, :, :N], r.V[:, :, :N],
+                                                             enable_gqa=True)
+        torch.cuda.synchronize()
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for i in range(args.steps):
+            r = reps[i % len(reps)]
+            torch.nn.functional.scaled_dot_product_attention(qs[i % len(reps)], r.K[:, :, :N], r.V[:, :, :N],
+                                                             enable_gqa=True)
+        s1.record()
+        torch.cuda.synchronize()
+        sdpa_ms = s0.elapsed_time(s1) / args.steps
+    except Exception as e:  # noqa: BLE001
+        print(f"torch SDPA baseline unavailable: {e}", file=sys.stderr)
+    dense_best = min(x for x in (dense_ms, sdpa_ms) if x is not None)
+    dense_bytes = st0.B * st0.Hkv * (st0.n + st0.w) * 2 * st0.D * 2
+
+    sweep = {}
+    if args.sweep:
+        for pp in (0.8, 0.9, 0.95, 0.99):
+            for i in range(args.warmup):
+                st = reps[i % len(reps)]
+                st.step(pp)
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for i in range(args.steps):
+                reps[i % len(reps)].step(pp)
+            b.record()
+            torch.cuda.synchronize()
+            cnt = st0.sel_count.cpu().numpy()
+            sweep[str(pp)] = {"ms_per_step": a.elapsed_time(b) / args.steps,
+                              "budget_mean": float(cnt.mean()), "budget_min": int(cnt.min()),
+                              "budget_max": int(cnt.max())}
+        st0.step(p)
+        torch.cuda.synchronize()
+
+    # roofline of the dominant kernel(s) of the step
+    kern = {}
+    for s in stages:
+        gbs = sbytes[s] / (stage_ms[s] * 1e-3) / 1e9
+        kern[s] = {"ms": stage_ms[s], "bytes": float(sbytes[s]), "GBps": gbs, "frac_hbm": gbs / HBM_PEAK_GBS}
+    dom = max(stages, key=lambda s: stage_ms[s])
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": kern[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": kern[dom]["GBps"] / HBM_PEAK_GBS, "traffic": None,
+                "algorithmic_bytes_per_launch": float(sbytes[dom])}
+
+    scan = None
+    if not args.no_scan:
+        del reps
+        torch.cuda.empty_cache()
+        scan = time_scan_c5(pipeline, gen, torch, args.steps, args.warmup)
+
+    cpu = None if args.no_cpu else cpu_baseline(wl)
+    cnt = st0.sel_count.cpu().numpy()
+    keys_scored = st0.B * st0.Hq * st0.n
+    line = {
+        "metric": "proxy-scored keys/s of the Top-p sparse decode step at 128K context",
+        "value": keys_scored / (ms_step * 1e-3),
+        "unit": "keys/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32 codes x int4 / f32 scores / bf16 KV, f32 accumulate",
+        "data": "synthetic (seeded; shapes of LLaMA-3.1-8B GQA decode)",
+        "config": {"workload": "gqa 32q/8kv ctx=128K (130816 indexed + 256 window) b=1 bf16, lazy flush of 256 keys",
+                   "p": p, "batch": st0.B, "heads_q": st0.Hq, "heads_kv": st0.Hkv, "head_dim": st0.D,
+                   "context": st0.n + st0.w, "replicas": args.replicas},
+        "dense_decode_ms": dense_ms,
+        "sdpa_decode_ms": sdpa_ms,
+        "speedup_vs_dense": dense_best / ms_step,
+        "dense_GBps": dense_bytes / (dense_ms * 1e-3) / 1e9,
+        "budget": {"mean": float(cnt.mean()), "min": int(cnt.min()), "max": int(cnt.max()),
+                   "union_rows_per_kv_head": union_rows / (st0.B * st0.Hkv)},
+        "stages": kern,
+        "roofline": roofline,
+        "scan_wide_heads": scan,
+        "p_sweep": sweep or None,
+        "cpu_baseline": cpu,
+        "gen_s": t_gen,
+        "git": _git_sha(),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,91 @@
+// Internal declarations shared by the library's translation units.
+// Host-side argument checks live in validate.cpp (plain C++, no HIP calls);
+// each *.hip file holds one stage's kernels and its launcher.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/rbq.h"
+
+namespace rbq {
+
+constexpr int kHeadDim = 128;        // the head_dim this build's kernels are written for
+constexpr int kWords = kHeadDim / 32;
+
+// ---------------------------------------------------------------- validation
+rbq_status check_heads(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim);
+rbq_status check_encode(int32_t batch, int32_t heads_kv, int32_t head_dim, const void* keys, int32_t keys_dtype,
+                        int64_t keys_ld, int32_t n_new, int32_t offset, int32_t cap, const float* P,
+                        const float* c_k, const uint32_t* codes, const float* kfac, uint32_t flags,
+                        const void* ws, size_t ws_bytes);
+rbq_status check_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                          const float* P, const float* c_k, const uint32_t* qplanes, const float* qscal);
+rbq_status check_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
+                       const uint32_t* codes, const void* kfac, const uint32_t* qplanes, const void* qscal,
+                       const void* out);
+rbq_status check_topp(int32_t batch, int32_t heads_q, int32_t n, const float* scores, float p, float sm_scale,
+                      const int32_t* sel_idx, const int32_t* sel_count, const void* ws, size_t ws_bytes);
+rbq_status check_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                        const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n, bool sparse,
+                        const int32_t* sel_idx, const int32_t* sel_count, const void* K_loc, const void* V_loc,
+                        int64_t loc_ld, int32_t w, float sm_scale, const float* out, const void* ws,
+                        size_t ws_bytes);
+
+// ---------------------------------------------------------------- workspace layouts
+// Top-p: per row, the scores are cut into chunks of kToppChunk; three radix
+// levels of 12, 12 and 8 bits of the order-preserving score key.
+constexpr int kToppThreads = 256;
+constexpr int kToppPerThread = 16;
+constexpr int kToppChunk = kToppThreads * kToppPerThread;   // 4096 scores per block
+constexpr int kBins1 = 4096, kBins2 = 4096, kBins3 = 256;
+constexpr int kHistPerRow = kBins1 + kBins2 + kBins3;         // uint64 counters per row
+constexpr int kToppStateWords = 8;                          // per-row uint32 state
+
+struct ToppWorkspace {
+  float* chunk_max;             // [rows][chunks]
+  unsigned long long* hist;     // [rows][kHistPerRow]
+  int32_t* chunk_cnt;           // [rows][chunks]
+  uint32_t* state;              // [rows][kToppStateWords]
+  size_t bytes;
+};
+ToppWorkspace topp_workspace(void* base, int64_t rows, int32_t n);
+
+// Decode: split-K over chunks of the indexed rows and of the window.
+constexpr int kDecodeChunk = 2048;        // indexed positions per block
+constexpr int kDecodeWinChunk = 256;      // window rows per block
+struct DecodeSplits {
+  int32_t chunk;            // indexed positions per split (<= kDecodeChunk)
+  int32_t idx_splits;
+  int32_t win_splits;
+  int32_t total() const { return idx_splits + win_splits; }
+};
+DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w);
+size_t decode_workspace_bytes(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
+                              int32_t w);
+
+// Encode: centroid partial sums over chunks of kCentroidChunk keys.
+constexpr int kCentroidChunk = 1024;
+size_t encode_workspace_bytes(int32_t batch, int32_t heads_kv, int32_t head_dim, int32_t n_new);
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------- launchers (HIP)
+rbq_status launch_encode(int32_t batch, int32_t heads_kv, const void* keys, int32_t keys_dtype, int64_t keys_ld,
+                         int32_t n_new, int32_t offset, int32_t cap, const float* P, const float* c_q, float* c_k,
+                         uint32_t* codes, float* kfac, uint32_t flags, float* alpha_out, void* ws,
+                         float* rot_out, hipStream_t stream);
+rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
+                           const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
+                           hipStream_t stream);
+rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
+                        const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
+                        float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream);
+rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,
+                       int32_t* sel_count, void* ws, hipStream_t stream);
+rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const void* K,
+                         const void* V, int32_t kv_dtype, int32_t cap, int32_t n, const int32_t* sel_idx,
+                         const int32_t* sel_count, const void* K_loc, const void* V_loc, int64_t loc_ld, int32_t w,
+                         float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream);
+
+}  // namespace rbq

@@ -1,0 +1,114 @@
+"""Device buffers of one decode workload and the calls of one decode step.
+
+The KV cache of a (sequence, KV head) holds `cap` rows: rows [0, n) are
+indexed (Algorithm 1), rows [n, n + w) are the local window of newest keys
+that decode attends in full precision and that a lazy flush later appends to
+the index (Section 3.4). torch only allocates memory and supplies the stream;
+every step of the method runs in librbq.so's kernels.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+from . import rbq
+
+
+def to_device_kv(arr: np.ndarray, kv_dtype: str, device) -> torch.Tensor:
+    """Upload keys/values given as float32 or as bf16 bit patterns (uint16)."""
+    if kv_dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).to(device)
+    t = torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).to(device)
+    return t.view(torch.bfloat16)
+
+
+class DecodeState:
+    """Index + cache + per-step buffers for B sequences x Hkv KV heads."""
+
+    def __init__(self, B, Hq, Hkv, D, cap, n, w, K, V, q, P, c_q=None, device="cuda"):
+        self.B, self.Hq, self.Hkv, self.D = B, Hq, Hkv, D
+        self.cap, self.n, self.w = cap, n, w
+        self.device = device
+        self.K, self.V = K, V                       # [B][Hkv][cap][D]
+        self.q = q                                  # [B][Hq][D] fp32
+        self.P = P                                  # [D][D] fp32
+        self.c_q = c_q                              # [B][Hkv][D] fp32 or None
+        f32 = dict(dtype=torch.float32, device=device)
+        self.c_k = torch.zeros(B, Hkv, D, **f32)
+        self.codes = torch.zeros(B, Hkv, cap, D // 32, dtype=torch.int32, device=device)
+        self.kfac = torch.zeros(B, Hkv, cap, 2, **f32)
+        self.qplanes = torch.zeros(B, Hq, 4, D // 32, dtype=torch.int32, device=device)
+        self.qscal = torch.zeros(B, Hq, rbq.QSCAL_STRIDE, **f32)
+        self.scores = torch.zeros(B, Hq, max(n, 1), **f32)
+        self.sel_idx = torch.zeros(B, Hq, max(n, 1), dtype=torch.int32, device=device)
+        self.sel_count = torch.zeros(B, Hq, dtype=torch.int32, device=device)
+        self.out = torch.zeros(B, Hq, D, **f32)
+        self.lse = torch.zeros(B, Hq, **f32)
+        self.ws_encode = rbq.workspace(rbq.RBQ_OP_ENCODE, B, Hq, Hkv, D, max(n, w, 1), 0, device)
+        self.ws_topp = rbq.workspace(rbq.RBQ_OP_TOPP, B, Hq, Hkv, D, n, 0, device)
+        self.ws_decode = rbq.workspace(rbq.RBQ_OP_SPARSE_DECODE, B, Hq, Hkv, D, n, w, device)
+        self.sm_scale = 1.0 / math.sqrt(D)
+
+    @classmethod
+    def from_workload(cls, wl, device="cuda", c_q: bool = True):
+        K = to_device_kv(wl.K, wl.kv_dtype, device)
+        V = to_device_kv(wl.V, wl.kv_dtype, device)
+        q = torch.from_numpy(np.ascontiguousarray(wl.q)).to(device)
+        P = torch.from_numpy(np.ascontiguousarray(wl.P)).to(device)
+        cq = torch.from_numpy(np.ascontiguousarray(wl.c_q)).to(device) if c_q else None
+        return cls(wl.B, wl.Hq, wl.Hkv, wl.D, wl.N, wl.n_index, wl.w, K, V, q, P, cq, device)
+
+    # ---------------------------------------------------------------- the five calls
+    def build_index(self, stream=None, rot_out=None, alpha_out=None):
+        """Prefill index construction over rows [0, n), setting c_k (Algorithm 1)."""
+        rbq.rbq_encode_keys(self.B, self.Hkv, self.D, self.K, self.cap, self.n, 0, self.cap, self.P, self.c_q,
+                            self.c_k, self.codes, self.kfac, rbq.RBQ_ENCODE_SET_CENTROID, alpha_out,
+                            self.ws_encode, stream, rot_out=rot_out)
+
+    def flush_window(self, stream=None):
+        """Lazy update: encode the w window rows into index rows [n, n + w) with
+        the prefill centroid (Section 3.4). The index size used by scoring is
+        left at n, so repeated steps stay identical."""
+        if self.w == 0:
+            return
+        K_win = self.K[:, :, self.n:]
+        rbq.rbq_encode_keys(self.B, self.Hkv, self.D, K_win, self.cap, self.w, self.n, self.cap, self.P, self.c_q,
+                            self.c_k, self.codes, self.kfac, 0, None, None, stream)
+
+    def quantize(self, stream=None, qrot_out=None):
+        rbq.rbq_quantize_query(self.B, self.Hq, self.Hkv, self.D, self.q, self.P, self.c_q, self.c_k,
+                               self.qplanes, self.qscal, stream, qrot_out=qrot_out)
+
+    def score(self, stream=None):
+        rbq.rbq_score(self.B, self.Hq, self.Hkv, self.D, self.n, self.cap, self.codes, self.kfac, self.qplanes,
+                      self.qscal, self.scores, stream)
+
+    def select(self, p, stream=None):
+        rbq.rbq_topp_select(self.B, self.Hq, self.n, self.scores, p, self.sm_scale, self.sel_idx, self.sel_count,
+                            self.ws_topp, stream)
+
+    def sparse_decode(self, stream=None):
+        K_loc = self.K[:, :, self.n:] if self.w else None
+        V_loc = self.V[:, :, self.n:] if self.w else None
+        rbq.rbq_sparse_decode(self.B, self.Hq, self.Hkv, self.D, self.q, self.K, self.V, self.cap, self.n,
+                              self.sel_idx, self.sel_count, K_loc, V_loc, self.cap, self.w, self.sm_scale, self.out,
+                              self.lse, self.ws_decode, stream)
+
+    def dense_decode(self, out=None, lse=None, stream=None):
+        K_loc = self.K[:, :, self.n:] if self.w else None
+        V_loc = self.V[:, :, self.n:] if self.w else None
+        rbq.rbq_dense_decode(self.B, self.Hq, self.Hkv, self.D, self.q, self.K, self.V, self.cap, self.n, K_loc,
+                             V_loc, self.cap, self.w, self.sm_scale, self.out if out is None else out,
+                             self.lse if lse is None else lse, self.ws_decode, stream)
+
+    def step(self, p, stream=None, flush=True):
+        """One decode step of the whole path: quantize -> score -> Top-p -> sparse
+        attention (index selection + window), then the lazy flush of the window."""
+        self.quantize(stream)
+        self.score(stream)
+        self.select(p, stream)
+        self.sparse_decode(stream)
+        if flush:
+            self.flush_window(stream)

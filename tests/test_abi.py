@@ -1,0 +1,118 @@
+"""The C ABI without a GPU: the library loads, exports every declared entry
+point, and rejects invalid arguments on the host before enqueuing anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rbq.h")
+LIB = os.path.join(ROOT, "paper_2606_31519_amd", "librbq.so")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_2606_31519_amd import build
+        build.build()
+    from paper_2606_31519_amd import rbq
+    return rbq
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:rbq_status|size_t|const char\*|int32_t)\s+(rbq_\w+)\(", text, re.M)))
+
+
+def test_header_declares_the_five_calls():
+    names = declared_symbols()
+    for n in ("rbq_encode_keys", "rbq_quantize_query", "rbq_score", "rbq_topp_select", "rbq_sparse_decode"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    cdll = ctypes.CDLL(LIB)
+    for n in declared_symbols():
+        assert hasattr(cdll, n), n
+    assert set(declared_symbols()) <= set(lib.EXPORTED)
+
+
+def test_status_strings_and_version(lib):
+    assert lib.status_string(0) == "ok"
+    assert lib.status_string(1) == "invalid argument"
+    assert lib.rbq_version() >= 100
+
+
+def test_index_footprint_matches_the_space_model(lib):
+    # Appendix C: eta = (D/8 + B_alpha) / (2 D B_data); with FP16 alpha and FP16
+    # KV at D = 128 the paper states 18/512 ~ 3.5 %. This layout stores 8 bytes of
+    # factors per key instead of B_alpha = 2.
+    D, B_data = 128, 2
+    assert abs((D / 8 + 2) / (2 * D * B_data) - 0.035) < 0.001
+    per_key = lib.rbq_index_bytes(1, 1, D, 1)
+    assert per_key == D // 8 + 8
+    assert abs(per_key / (2 * D * B_data) - 0.046875) < 1e-12
+    assert lib.rbq_index_bytes(4, 8, D, 131072) == 4 * 8 * 131072 * 24
+
+
+def test_workspace_sizes(lib):
+    assert lib.rbq_workspace_bytes(lib.RBQ_OP_TOPP, 1, 32, 8, 128, 131072) > 32 * 8448 * 8
+    assert lib.rbq_workspace_bytes(lib.RBQ_OP_SPARSE_DECODE, 1, 32, 8, 128, 130816, 256) > 0
+    assert lib.rbq_workspace_bytes(lib.RBQ_OP_ENCODE, 1, 8, 8, 128, 4096, 0) >= 8 * 4 * 128 * 4
+    assert lib.rbq_workspace_bytes(99, 1, 32, 8, 128, 100) == 0
+    assert lib.rbq_workspace_bytes(lib.RBQ_OP_TOPP, 0, 32, 8, 128, 100) == 0
+
+
+FAKE = 1 << 40   # never dereferenced: every call below fails validation first
+
+
+def _status(fn, *args):
+    return fn(*args)
+
+
+def test_invalid_arguments_are_rejected_on_the_host(lib):
+    L = lib.lib
+    EINVAL, EUNSUP = lib.RBQ_EINVAL, lib.RBQ_EUNSUPPORTED
+    # encode: offset + n_new > cap, null P, bad flags, centroid of zero keys, bad dtype, D unsupported
+    enc = lambda **k: L.rbq_encode_keys(k.get("B", 1), k.get("H", 1), k.get("D", 128), FAKE, k.get("dt", 1),
+                                        k.get("ld", 10), k.get("n", 10), k.get("off", 0), k.get("cap", 10),
+                                        k.get("P", FAKE), None, FAKE, FAKE, FAKE, k.get("flags", 0), None,
+                                        k.get("ws", FAKE), k.get("wsb", 1 << 20), 0)
+    assert enc(off=1) == EINVAL
+    assert enc(P=None) == EINVAL
+    assert enc(flags=4) == EINVAL
+    assert enc(n=0, flags=1) == EINVAL
+    assert enc(flags=1, ws=None) == EINVAL
+    assert enc(flags=1, wsb=16) == EINVAL
+    assert enc(dt=7) == EUNSUP
+    assert enc(D=64) == EUNSUP
+    assert enc(D=100) == EINVAL
+    assert enc(ld=5) == EINVAL
+    assert enc(B=0) == EINVAL
+    # quantize: Hq not a multiple of Hkv, null c_k
+    assert L.rbq_quantize_query(1, 6, 4, 128, FAKE, FAKE, None, FAKE, FAKE, FAKE, 0) == EINVAL
+    assert L.rbq_quantize_query(1, 8, 4, 128, FAKE, FAKE, None, None, FAKE, FAKE, 0) == EINVAL
+    # score: n > cap
+    assert L.rbq_score(1, 8, 4, 128, 11, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EINVAL
+    assert L.rbq_score(1, 8, 4, 128, -1, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EINVAL
+    # top-p: p outside (0, 1], non-finite or non-positive scale, short workspace
+    tp = lambda p=0.9, s=0.1, wsb=1 << 30: L.rbq_topp_select(1, 8, 100, FAKE, p, s, FAKE, FAKE, FAKE, wsb, 0)
+    assert tp(p=0.0) == EINVAL
+    assert tp(p=1.5) == EINVAL
+    assert tp(p=float("nan")) == EINVAL
+    assert tp(s=float("inf")) == EINVAL
+    assert tp(s=-1.0) == EINVAL
+    assert tp(wsb=8) == EINVAL
+    # decode: window above the limit, window without buffers, G not a power of two, n > cap
+    dec = lambda **k: L.rbq_sparse_decode(1, k.get("Hq", 8), 4 if k.get("Hq", 8) % 4 == 0 else 3, 128, FAKE, FAKE,
+                                          FAKE, 1, k.get("cap", 100), k.get("n", 100), FAKE, FAKE,
+                                          k.get("kl", FAKE), FAKE, k.get("ld", 300), k.get("w", 10), 0.1, FAKE,
+                                          None, FAKE, 1 << 30, 0)
+    assert dec(w=5000, ld=5000) == EINVAL
+    assert dec(kl=None) == EINVAL
+    assert dec(ld=5) == EINVAL
+    assert dec(n=101) == EINVAL
+    assert dec(Hq=12) == EUNSUP
+    assert L.rbq_dense_decode(1, 8, 4, 128, FAKE, FAKE, FAKE, 3, 100, 100, None, None, 0, 0, 0.1, FAKE, None,
+                              FAKE, 1 << 30, 0) == EUNSUP

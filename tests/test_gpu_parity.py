@@ -1,0 +1,331 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, stage by stage.
+
+Every test feeds both sides the same seeded inputs; the comparison rules are
+in parity_util. Sizes span several tiles with ragged tails; the full-size
+workloads are checked on sampled (sequence, head) groups.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import rbq_oracle as orc
+from workloads import gen
+import parity_util as pu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def R():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2606_31519_amd import rbq
+    return rbq
+
+
+@pytest.fixture(scope="module")
+def pipeline(R):
+    from paper_2606_31519_amd import pipeline as pl
+    return pl
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+# ---------------------------------------------------------------- integer path
+@pytest.mark.parametrize("B,Hkv,G,cap,n", [(2, 2, 4, 700, 650), (1, 1, 1, 64, 64), (1, 2, 8, 300, 257)])
+def test_score_integers_bit_exact(R, B, Hkv, G, cap, n):
+    rng = np.random.default_rng(n)
+    Hq = Hkv * G
+    codes = rng.integers(0, 2 ** 32, (B, Hkv, cap, 4), dtype=np.uint64).astype(np.uint32)
+    codes[0, 0, 0] = 0xFFFFFFFF
+    codes[0, 0, 1] = 0
+    qcodes = rng.integers(0, 16, (B, Hq, 128))
+    qcodes[0, 0] = 15
+    planes = np.stack([np.stack([orc.query_bit_planes(qcodes[b, h]) for h in range(Hq)]) for b in range(B)])
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int32)).cuda()
+    ip = torch.full((B, Hq, n), -1, dtype=torch.int32, device="cuda")
+    pc = torch.full((B, Hkv, n), -1, dtype=torch.int32, device="cuda")
+    R.rbq_score_ints(B, Hq, Hkv, 128, n, cap, dev(codes), dev(planes), ip, pc)
+    torch.cuda.synchronize()
+    ip, pc = _np(ip), _np(pc)
+    for b in range(B):
+        for hk in range(Hkv):
+            bits = orc.unpack_bits(codes[b, hk, :n], 128)
+            for g in range(G):
+                ref_ip, ref_pc = orc.int_dot(bits, qcodes[b, hk * G + g])
+                assert np.array_equal(ip[b, hk * G + g], ref_ip)
+                assert np.array_equal(pc[b, hk], ref_pc)
+
+
+# ---------------------------------------------------------------- query quantisation
+@pytest.mark.parametrize("case", ["plain", "centred", "degenerate"])
+def test_quantize_query_stagewise(R, pipeline, case):
+    w = gen.random_case(2, 8, 2, 64, seed=11, kv_dtype="f32", c_q_scale=0.0 if case == "plain" else 0.7)
+    if case == "degenerate":
+        w.q[0, 0] = w.c_q[0, 0]          # q == c_q: A = 0
+        w.q[1, 3] = 0.0
+    st = pipeline.DecodeState.from_workload(w)
+    st.c_k.copy_(torch.randn(2, 2, 128, generator=torch.Generator().manual_seed(1)).cuda())
+    qrot = torch.empty(2, 8, 128, device="cuda")
+    st.quantize(qrot_out=qrot)
+    torch.cuda.synchronize()
+    planes = pu.u32(st.qplanes)
+    qs, qr, ck = _np(st.qscal), _np(qrot), _np(st.c_k)
+    for b in range(2):
+        for h in range(8):
+            hk = h // 4
+            z = orc.uniform_quantize(qr[b, h], dtype=np.float32)      # the decision in fp32, from the GPU's q'
+            assert np.array_equal(pu.planes_to_codes(planes[b, h]), z["codes"])
+            assert qs[b, h, 0] == np.float32(z["ql"]) and qs[b, h, 1] == np.float32(z["delta"])
+            assert qs[b, h, 2] == z["s_u"]
+            ref = orc.quantize_query(w.q[b, h], w.P, w.c_q[b, hk], ck[b, hk])
+            assert abs(qs[b, h, 3] - ref["A"]) <= 1e-5 * ref["A"] + 1e-6
+            assert abs(qs[b, h, 4] - ref["B0"]) <= 1e-5 * (np.abs(w.q[b, h]) @ np.abs(ck[b, hk])) + 1e-6
+            assert np.abs(qr[b, h] - ref["qrot"]).max() <= 1e-5
+            # end to end the codes may differ only where the oracle's value sits on a rounding edge
+            t = (ref["qrot"] - ref["ql"]) / ref["delta"] if ref["delta"] > 0 else np.zeros(128)
+            off = np.nonzero(pu.planes_to_codes(planes[b, h]) != ref["codes"])[0]
+            assert np.all(np.abs(t[off] - np.floor(t[off]) - 0.5) <= 1e-4)
+
+
+# ---------------------------------------------------------------- index construction
+def _check_encode_group(st, w, b, hk, n, rot, alpha, c_k_given=None):
+    K = w.K_f32(b, hk, slice(0, n)).astype(np.float64)
+    ck_gpu = _np(st.c_k[b, hk]).astype(np.float64)
+    if c_k_given is None:
+        ck_ref = orc.key_centroid(K)
+        assert np.abs(ck_gpu - ck_ref).max() <= 1e-5 * (np.abs(K).mean() + 1.0)
+    enc = orc.encode_keys(K, w.P, c_k=ck_gpu, c_q=w.c_q[b, hk])
+    codes = pu.u32(st.codes[b, hk, :n])
+    kfac = _np(st.kfac[b, hk, :n]).astype(np.float64)
+    nrm = enc["norm"]
+    if rot is not None:
+        r = _np(rot[b, hk]).astype(np.float64)
+        assert np.array_equal(codes, orc.pack_bits(orc.sign_bits(r)))        # stage-wise exact
+        assert np.all(np.abs(r - enc["R"]) <= 1e-5 * nrm[:, None] + 1e-30)
+    diff = orc.unpack_bits(codes, 128) != enc["bits"]
+    assert np.all(np.abs(enc["R"][diff]) <= 1e-5 * np.broadcast_to(nrm[:, None], diff.shape)[diff])
+    assert np.all(np.abs(kfac[:, 0] - enc["f"]) <= 1e-5 * np.abs(enc["f"]) + 1e-6)
+    gscale = np.abs(w.c_q[b, hk]).sum() * np.abs(enc["X"]).max(axis=1)
+    assert np.all(np.abs(kfac[:, 1] - enc["g"]) <= 1e-5 * gscale + 1e-6)
+    if alpha is not None:
+        a = _np(alpha[b, hk]).astype(np.float64)
+        assert np.all(np.abs(a - enc["alpha"]) <= 1e-5 * enc["alpha"] + 1e-7)
+    return int(diff.sum())
+
+
+@pytest.mark.parametrize("kv_dtype,n", [("bf16", 1000), ("f32", 257), ("bf16", 1), ("f32", 128)])
+def test_encode_stagewise(R, pipeline, kv_dtype, n):
+    w = gen.random_case(2, 4, 2, n, seed=n, kv_dtype=kv_dtype, c_q_scale=0.5, key_offset=2.0)
+    st = pipeline.DecodeState.from_workload(w)
+    rot = torch.empty(2, 2, n, 128, device="cuda")
+    alpha = torch.empty(2, 2, n, device="cuda")
+    st.build_index(rot_out=rot, alpha_out=alpha)
+    torch.cuda.synchronize()
+    for b in range(2):
+        for hk in range(2):
+            _check_encode_group(st, w, b, hk, n, rot, alpha)
+
+
+def test_encode_degenerate_key_and_lazy_append(R, pipeline):
+    n1, n2 = 300, 77
+    w = gen.random_case(1, 4, 1, n1 + n2, seed=5, kv_dtype="bf16", c_q_scale=0.3)
+    st = pipeline.DecodeState.from_workload(w)
+    st.n = n1
+    st.build_index()
+    torch.cuda.synchronize()
+    ck = _np(st.c_k[0, 0])
+    before = pu.u32(st.codes[0, 0, :n1]).copy()
+    # lazy append: rows [n1, n1 + n2) encoded with the prefill centroid at offset n1
+    R.rbq_encode_keys(1, 1, 128, st.K[:, :, n1:], st.cap, n2, n1, st.cap, st.P, st.c_q, st.c_k, st.codes, st.kfac,
+                      0, None, None)
+    torch.cuda.synchronize()
+    assert np.array_equal(pu.u32(st.codes[0, 0, :n1]), before)
+    assert np.array_equal(_np(st.c_k[0, 0]), ck)
+    K2 = w.K_f32(0, 0, slice(n1, n1 + n2)).astype(np.float64)
+    enc = orc.encode_keys(K2, w.P, c_k=ck.astype(np.float64), c_q=w.c_q[0, 0])
+    diff = orc.unpack_bits(pu.u32(st.codes[0, 0, n1:n1 + n2]), 128) != enc["bits"]
+    assert np.all(np.abs(enc["R"][diff]) <= 1e-5 * np.broadcast_to(enc["norm"][:, None], diff.shape)[diff])
+    # a key equal to the centroid: no bits, f = 0, g = 0
+    Kc = torch.from_numpy(np.tile(ck, (3, 1))).to(torch.bfloat16).float().cuda()
+    ck_exact = Kc[0].clone()
+    st.c_k[0, 0] = ck_exact
+    R.rbq_encode_keys(1, 1, 128, Kc, 3, 3, 0, st.cap, st.P, st.c_q, st.c_k, st.codes, st.kfac, 0, None, None)
+    torch.cuda.synchronize()
+    assert np.all(pu.u32(st.codes[0, 0, :3]) == 0)
+    assert np.all(_np(st.kfac[0, 0, :3]) == 0)
+
+
+# ---------------------------------------------------------------- scores
+@pytest.mark.parametrize("B,Hq,Hkv,n,cq", [(1, 4, 1, 4097, 0.0), (2, 8, 1, 31, 0.5), (1, 32, 8, 1000, 0.0),
+                                            (2, 16, 2, 1, 0.2), (1, 64, 8, 2500, 0.3)])
+def test_score_parity(R, pipeline, B, Hq, Hkv, n, cq):
+    w = gen.random_case(B, Hq, Hkv, n, seed=Hq + n, kv_dtype="bf16", c_q_scale=cq, key_offset=1.0)
+    st = pipeline.DecodeState.from_workload(w)
+    st.build_index()
+    st.quantize()
+    st.score()
+    torch.cuda.synchronize()
+    S, codes, kfac = _np(st.scores), pu.u32(st.codes), _np(st.kfac)
+    planes, qs = pu.u32(st.qplanes), _np(st.qscal)
+    G = Hq // Hkv
+    for b in range(B):
+        for h in range(Hq):
+            pu.check_scores(S[b, h, :n], codes[b, h // G, :n], kfac[b, h // G, :n], planes[b, h], qs[b, h])
+
+
+# ---------------------------------------------------------------- Top-p
+def _topp_rows(R, S: np.ndarray, p: float, sm_scale: float):
+    rows, n = S.shape
+    dS = torch.from_numpy(np.ascontiguousarray(S, dtype=np.float32)).cuda()
+    sel = torch.full((rows, max(n, 1)), -7, dtype=torch.int32, device="cuda")
+    cnt = torch.full((rows,), -7, dtype=torch.int32, device="cuda")
+    ws = R.workspace(R.RBQ_OP_TOPP, 1, rows, rows, 128, n)
+    R.rbq_topp_select(1, rows, n, dS, p, sm_scale, sel, cnt, ws)
+    torch.cuda.synchronize()
+    return _np(sel), _np(cnt)
+
+
+@pytest.mark.parametrize("n", [1, 31, 4096, 4097, 20000, 70001])
+@pytest.mark.parametrize("p", [0.5, 0.9, 0.95, 0.99, 1.0])
+def test_topp_parity_random(R, n, p):
+    rng = np.random.default_rng(n)
+    S = np.stack([rng.standard_normal(n) * 6.0,                         # spread
+                  rng.standard_normal(n) * 0.3,                         # near uniform
+                  np.round(rng.standard_normal(n) * 4.0) / 2.0,         # many exact ties
+                  np.where(rng.random(n) < 0.01, 30.0, 0.0) + rng.standard_normal(n)])   # peaky
+    sel, cnt = _topp_rows(R, S, p, 1 / math.sqrt(128) * 8)
+    for r in range(S.shape[0]):
+        assert 0 <= cnt[r] <= n
+        got = sel[r, :cnt[r]]
+        if p >= 1.0:
+            assert np.array_equal(got, np.arange(n))
+        else:
+            pu.check_topp(S[r].astype(np.float32), p, 1 / math.sqrt(128) * 8, got)
+
+
+def test_topp_degenerate_rows(R):
+    n = 5000
+    S = np.stack([np.full(n, 0.25), np.full(n, -3.0), np.where(np.arange(n) % 2 == 0, 0.0, -0.0),
+                  np.where(np.arange(n) == 1234, 100.0, -100.0)])
+    sel, cnt = _topp_rows(R, S, 0.9, 1.0)
+    assert cnt[0] == n and cnt[1] == n and cnt[2] == n       # all tied: everything
+    assert cnt[3] == 1 and sel[3, 0] == 1234
+    sel, cnt = _topp_rows(R, np.zeros((3, 0)), 0.9, 1.0)
+    assert np.all(cnt == 0)
+
+
+# ---------------------------------------------------------------- attention
+def _rand_sel(rng, n, frac, Hq):
+    out = []
+    for _ in range(Hq):
+        k = int(round(frac * n))
+        out.append(np.sort(rng.choice(n, size=k, replace=False)) if n else np.zeros(0, np.int64))
+    return out
+
+
+@pytest.mark.parametrize("kv_dtype,G,n,w,frac", [("bf16", 4, 5000, 17, 0.05), ("f32", 1, 3000, 0, 0.3),
+                                                 ("bf16", 8, 2049, 256, 0.5), ("bf16", 4, 0, 100, 0.0),
+                                                 ("bf16", 2, 700, 0, 0.0), ("bf16", 4, 131, 5, 1.0)])
+def test_sparse_decode_parity(R, pipeline, kv_dtype, G, n, w, frac):
+    B, Hkv = 2, 2
+    Hq = G * Hkv
+    wl = gen.random_case(B, Hq, Hkv, n, seed=n + w, kv_dtype=kv_dtype, w=w)
+    st = pipeline.DecodeState.from_workload(wl)
+    rng = np.random.default_rng(3)
+    sels = [_rand_sel(rng, n, frac, Hq) for _ in range(B)]
+    idx = np.zeros((B, Hq, max(n, 1)), np.int32)
+    cnt = np.zeros((B, Hq), np.int32)
+    for b in range(B):
+        for h in range(Hq):
+            idx[b, h, :len(sels[b][h])] = sels[b][h]
+            cnt[b, h] = len(sels[b][h])
+    st.sel_idx.copy_(torch.from_numpy(idx))
+    st.sel_count.copy_(torch.from_numpy(cnt))
+    st.sparse_decode()
+    torch.cuda.synchronize()
+    out, lse = _np(st.out), _np(st.lse)
+    for b in range(B):
+        for h in range(Hq):
+            hk = h // G
+            K, V = wl.K_f32(b, hk), wl.V_f32(b, hk)
+            pu.check_attention(out[b, h], lse[b, h], wl.q[b, h], K[:n], V[:n], sels[b][h], K[n:n + w], V[n:n + w],
+                               st.sm_scale)
+    # dense: every indexed row plus the window
+    st.dense_decode()
+    torch.cuda.synchronize()
+    out, lse = _np(st.out), _np(st.lse)
+    for b in range(B):
+        for h in range(Hq):
+            hk = h // G
+            K, V = wl.K_f32(b, hk), wl.V_f32(b, hk)
+            pu.check_attention(out[b, h], lse[b, h], wl.q[b, h], K[:n], V[:n], np.arange(n), K[n:n + w],
+                               V[n:n + w], st.sm_scale)
+
+
+# ---------------------------------------------------------------- end to end
+def _end_to_end(R, pipeline, wl, p, groups, rows_per_group=None, flush=False):
+    st = pipeline.DecodeState.from_workload(wl)
+    st.build_index()
+    st.step(p, flush=flush)
+    torch.cuda.synchronize()
+    n, w, G = wl.n_index, wl.w, wl.G
+    S, codes, kfac = _np(st.scores), pu.u32(st.codes), _np(st.kfac)
+    planes, qs, ck = pu.u32(st.qplanes), _np(st.qscal), _np(st.c_k)
+    sel, cnt, out, lse = _np(st.sel_idx), _np(st.sel_count), _np(st.out), _np(st.lse)
+    report = []
+    for (b, hk) in groups:
+        K, V = wl.K_f32(b, hk), wl.V_f32(b, hk)
+        _check_encode_group(st, wl, b, hk, n, None, None)
+        heads = range(hk * G, (hk + 1) * G) if rows_per_group is None else [hk * G + g for g in rows_per_group]
+        for h in heads:
+            ref = orc.quantize_query(wl.q[b, h], wl.P, wl.c_q[b, hk], ck[b, hk])
+            qc = pu.planes_to_codes(planes[b, h])
+            t = (ref["qrot"] - ref["ql"]) / ref["delta"]
+            off = np.nonzero(qc != ref["codes"])[0]
+            assert np.all(np.abs(t[off] - np.floor(t[off]) - 0.5) <= 1e-4)
+            pu.check_scores(S[b, h, :n], codes[b, hk, :n], kfac[b, hk, :n], planes[b, h], qs[b, h])
+            got = sel[b, h, :cnt[b, h]]
+            res = pu.check_topp(S[b, h, :n], p, st.sm_scale, got)
+            pu.check_attention(out[b, h], lse[b, h], wl.q[b, h], K[:n], V[:n], got, K[n:n + w], V[n:n + w],
+                               st.sm_scale)
+            recall = orc.attention_recall(wl.q[b, h], K[:n], got, st.sm_scale)
+            report.append((b, h, int(cnt[b, h]), res["diff"], recall))
+    return st, report
+
+
+def test_end_to_end_config1(R, pipeline):
+    wl = gen.config1()
+    st, rep = _end_to_end(R, pipeline, wl, wl.p, [(0, 0)])
+    print("config1 (b, h, budget, set diff, recall):", rep)
+
+
+def test_end_to_end_config2(R, pipeline):
+    wl = gen.config2()
+    st, rep = _end_to_end(R, pipeline, wl, wl.p, [(0, hk) for hk in range(8)])
+    budgets = [r[2] for r in rep]
+    print(f"config2 budget mean {np.mean(budgets):.0f} of {wl.n_index}, recall mean {np.mean([r[4] for r in rep]):.3f}")
+
+
+@pytest.mark.slow
+def test_end_to_end_config3_full_size_sampled(R, pipeline):
+    wl = gen.config3()
+    for p in wl.p_sweep:
+        st, rep = _end_to_end(R, pipeline, wl, p, [(0, 0), (0, 5)], rows_per_group=[0, 3], flush=True)
+        print(f"config3 p={p}: budgets {[r[2] for r in rep]} recall {[round(r[4], 3) for r in rep]}")
+
+
+def test_step_is_deterministic(R, pipeline):
+    wl = gen.config2(N=8192)
+    st = pipeline.DecodeState.from_workload(wl)
+    st.build_index()
+    outs = []
+    for _ in range(2):
+        st.step(0.95)
+        torch.cuda.synchronize()
+        outs.append([_np(t).copy() for t in (st.scores, st.sel_idx, st.sel_count, st.out, st.lse)])
+    for a, b in zip(*outs):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
