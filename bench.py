@@ -112,10 +112,40 @@ def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
                       f"({G} query heads x {n} keys per group; index build excluded), {t_total:.1f} s"}
 
 
+def _graph(torch, fn):
+    """Capture fn() (library launches on the capturing stream) into a HIP graph."""
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()                      # warm the path once outside the graph
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    return g
+
+
+def _time_graphs(torch, graphs, steps, warmup):
+    """Replay the graphs round-robin; mean ms per replay between two HIP events."""
+    for i in range(warmup):
+        graphs[i % len(graphs)].replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for i in range(steps):
+        graphs[i % len(graphs)].replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
+
+
 def time_scan_c5(pipeline, gen, torch, steps, warmup, replicas=4):
     """Standalone rbq_score scan on the wide-head workload (batch 4 x 128K, 64/8 heads)."""
     wl = gen.config5()
     st = pipeline.DecodeState.from_workload(wl)
+    del wl
     st.build_index()
     st.quantize()
     torch.cuda.synchronize()
@@ -125,17 +155,8 @@ def time_scan_c5(pipeline, gen, torch, steps, warmup, replicas=4):
         c.__dict__.update(st.__dict__)
         c.codes, c.kfac, c.scores = st.codes.clone(), st.kfac.clone(), torch.empty_like(st.scores)
         reps.append(c)
-    del wl
-    for i in range(warmup):
-        reps[i % replicas].score()
-    torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for i in range(steps):
-        evs[i][0].record()
-        reps[i % replicas].score()
-        evs[i][1].record()
-    torch.cuda.synchronize()
-    ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    graphs = [_graph(torch, r.score) for r in reps]
+    ms = _time_graphs(torch, graphs, steps, warmup)
     B, Hq, Hkv, D, n = st.B, st.Hq, st.Hkv, st.D, st.n
     nbytes = B * Hkv * n * (D // 8 + 8) + B * Hq * n * 4
     gbs = nbytes / (ms * 1e-3) / 1e9
@@ -176,40 +197,25 @@ def main():
     p = args.p
 
     stages = ["quantize", "score", "topp", "sparse_decode", "flush"]
+    stage_fn = {"quantize": lambda r: r.quantize(), "score": lambda r: r.score(),
+                "topp": lambda r: r.select(p), "sparse_decode": lambda r: r.sparse_decode(),
+                "flush": lambda r: r.flush_window()}
 
-    def run_step(st, evs=None):
-        if evs is not None:
-            evs[0].record()
-        st.quantize()
-        if evs is not None:
-            evs[1].record()
-        st.score()
-        if evs is not None:
-            evs[2].record()
-        st.select(p)
-        if evs is not None:
-            evs[3].record()
-        st.sparse_decode()
-        if evs is not None:
-            evs[4].record()
-        st.flush_window()
-        if evs is not None:
-            evs[5].record()
-
-    for i in range(args.warmup):
-        run_step(reps[i % len(reps)])
+    # the whole step, one HIP graph per replica
+    step_graphs = [_graph(torch, lambda r=r: r.step(p)) for r in reps]
+    ms_step = _time_graphs(torch, step_graphs, args.steps, args.warmup)
+    # each stage on its own: one graph runs it REPS times back-to-back over the replicas, so the
+    # graph launch is amortised and the time per run is that of the stage's kernels plus launch gaps
+    REPS = 16
+    stage_ms = {}
+    for sname in stages:
+        f = stage_fn[sname]
+        g = _graph(torch, lambda f=f: [f(reps[i % len(reps)]) for i in range(REPS)])
+        stage_ms[sname] = _time_graphs(torch, [g], max(2, args.steps // 4), 2) / REPS
+        del g
+    for r in reps:       # leave every replica in the state of a full step
+        r.step(p)
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0.record()
-    for i in range(args.steps):
-        run_step(reps[i % len(reps)], evs[i])
-    t1.record()
-    torch.cuda.synchronize()
-    ms_step = t0.elapsed_time(t1) / args.steps
-    stage_ms = {s: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs])) for k, s in enumerate(stages)}
 
     union_rows, sel_total = _union_rows(st0)
     sbytes = _stage_bytes(st0, {"sel_total": sel_total, "union_rows": union_rows})
@@ -217,31 +223,22 @@ def main():
     # dense bf16 decode at the same shape: this library's kernel, then torch SDPA
     dense_out = torch.empty_like(st0.out)
     dense_lse = torch.empty_like(st0.lse)
-    for i in range(args.warmup):
-        reps[i % len(reps)].dense_decode(dense_out, dense_lse)
-    torch.cuda.synchronize()
-    d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    d0.record()
-    for i in range(args.steps):
-        reps[i % len(reps)].dense_decode(dense_out, dense_lse)
-    d1.record()
-    torch.cuda.synchronize()
-    dense_ms = d0.elapsed_time(d1) / args.steps
+    dense_graphs = [_graph(torch, lambda r=r: r.dense_decode(dense_out, dense_lse)) for r in reps]
+    dense_ms = _time_graphs(torch, dense_graphs, args.steps, args.warmup)
+    del dense_graphs
     sdpa_ms = None
     try:
         N = st0.n + st0.w
         qs = [r.q.view(1, r.Hq, 1, r.D).to(torch.bfloat16) for r in reps]
+        sdpa = lambda i: torch.nn.functional.scaled_dot_product_attention(
+            qs[i], reps[i].K[:, :, :N], reps[i].V[:, :, :N], enable_gqa=True)
         for i in range(args.warmup):
-            r = reps[i % len(reps)]
-            torch.nn.functional.scaled_dot_product_attention(qs[i % len(reps)], r.K[:, :, :N], r.V[:, :, :N],
-                                                             enable_gqa=True)
+            sdpa(i % len(reps))
         torch.cuda.synchronize()
         s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         s0.record()
         for i in range(args.steps):
-            r = reps[i % len(reps)]
-            torch.nn.functional.scaled_dot_product_attention(qs[i % len(reps)], r.K[:, :, :N], r.V[:, :, :N],
-                                                             enable_gqa=True)
+            sdpa(i % len(reps))
         s1.record()
         torch.cuda.synchronize()
         sdpa_ms = s0.elapsed_time(s1) / args.steps
@@ -253,19 +250,11 @@ def main():
     sweep = {}
     if args.sweep:
         for pp in (0.8, 0.9, 0.95, 0.99):
-            for i in range(args.warmup):
-                st = reps[i % len(reps)]
-                st.step(pp)
-            torch.cuda.synchronize()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            for i in range(args.steps):
-                reps[i % len(reps)].step(pp)
-            b.record()
-            torch.cuda.synchronize()
+            gs = [_graph(torch, lambda r=r, pp=pp: r.step(pp)) for r in reps]
+            ms = _time_graphs(torch, gs, args.steps, args.warmup)
+            del gs
             cnt = st0.sel_count.cpu().numpy()
-            sweep[str(pp)] = {"ms_per_step": a.elapsed_time(b) / args.steps,
-                              "budget_mean": float(cnt.mean()), "budget_min": int(cnt.min()),
+            sweep[str(pp)] = {"ms_per_step": ms, "budget_mean": float(cnt.mean()), "budget_min": int(cnt.min()),
                               "budget_max": int(cnt.max())}
         st0.step(p)
         torch.cuda.synchronize()
@@ -282,7 +271,7 @@ def main():
 
     scan = None
     if not args.no_scan:
-        del reps
+        del reps, step_graphs
         torch.cuda.empty_cache()
         scan = time_scan_c5(pipeline, gen, torch, args.steps, args.warmup)
 

@@ -10,8 +10,11 @@
 // (a per-entry head mask keeps each head's softmax over its own set only).
 // Each wave takes tiles of 64 gathered rows:
 //   logits: lane = row, the 256-byte K row against the G queries (LDS broadcast)
-//   online softmax per head in the log2 domain (wave max / sum)
+//   online softmax per head in the log2 domain (DPP / swizzle wave reductions)
 //   values: lane = 2 dimensions, V rows read coalesced, accumulated in fp32.
+// The kernel is occupancy-bound: keeping ~75 VGPRs (6 waves per SIMD) beats
+// issuing more loads per wave (measured on MI355X: a 16-load K prefetch or a
+// deeper V unroll doubles the registers and runs ~1.5x slower).
 // Waves merge in LDS; the block writes (m, l, acc[D]) per head; a combine
 // kernel merges the splits in fixed order (bitwise deterministic).
 #include <cmath>
@@ -26,6 +29,8 @@ constexpr int kDWaves = 4;
 constexpr int kDThreads = kDWaves * kWave;
 constexpr int kBmWords = kDecodeChunk / 32;
 constexpr float kLn2 = 0.69314718055994531f;
+__device__ __forceinline__ float wmax64(float v) { v = max32(v); return fmaxf(v, __shfl_xor(v, 32, kWave)); }
+__device__ __forceinline__ float wsum64(float v) { v = sum32(v); return v + __shfl_xor(v, 32, kWave); }
 
 __device__ __forceinline__ int lower_bound_i32(const int32_t* a, int cnt, int x) {
   int lo = 0, hi = cnt;
@@ -216,13 +221,13 @@ __global__ __launch_bounds__(kDThreads) void decode_partial_kernel(
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const float lg = (valid && ((mk >> g) & 1u)) ? dot[g] : -INFINITY;
-      const float tmax = wave_max(lg);
+      const float tmax = wmax64(lg);
       float pr = 0.f;
       if (tmax != -INFINITY) {
         const float mn = fmaxf(m[g], tmax);
         const float corr = m[g] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[g] - mn);
         pr = lg == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(lg - mn);
-        l[g] = fmaf(l[g], corr, wave_sum(pr));
+        l[g] = fmaf(l[g], corr, wsum64(pr));
         acc[g] = acc[g] * corr;
         m[g] = mn;
       }
@@ -278,25 +283,56 @@ __global__ __launch_bounds__(kDThreads) void decode_partial_kernel(
   }
 }
 
-__global__ __launch_bounds__(kHeadDim) void decode_combine_kernel(const float* __restrict__ part, int splits,
-                                                                  float* __restrict__ out, float* __restrict__ lse) {
+// Merge the splits of one query head: 8 groups of 128 threads, each group
+// folds a fixed residue class of splits, then the groups are added in order.
+constexpr int kCombGroups = 8;
+constexpr int kCombThreads = kCombGroups * kHeadDim;
+constexpr int kMaxSplits = 4096;
+
+__global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(const float* __restrict__ part, int splits,
+                                                                      float* __restrict__ out,
+                                                                      float* __restrict__ lse) {
+  __shared__ float wsc[kMaxSplits];
+  __shared__ float red[kCombThreads / kWave];
+  __shared__ float po[kCombGroups][kHeadDim];
+  __shared__ float pl[kCombGroups];
   const int row = blockIdx.x;
-  const int d = threadIdx.x;
   const float* pr = part + int64_t(row) * splits * (kHeadDim + 2);
   float M = -INFINITY;
-  for (int s = 0; s < splits; ++s) M = fmaxf(M, pr[s * (kHeadDim + 2)]);
-  float L = 0.f, o = 0.f;
-  if (M != -INFINITY) {
-    for (int s = 0; s < splits; ++s) {
-      const float ms = pr[s * (kHeadDim + 2)];
-      if (ms == -INFINITY) continue;
-      const float sc = __builtin_amdgcn_exp2f(ms - M);
-      L = fmaf(pr[s * (kHeadDim + 2) + 1], sc, L);
-      o = fmaf(pr[s * (kHeadDim + 2) + 2 + d], sc, o);
-    }
+  for (int s = threadIdx.x; s < splits; s += kCombThreads) M = fmaxf(M, pr[int64_t(s) * (kHeadDim + 2)]);
+  M = wave_max(M);
+  if (lane_id() == 0) red[threadIdx.x / kWave] = M;
+  __syncthreads();
+  M = red[0];
+#pragma unroll
+  for (int i = 1; i < kCombThreads / kWave; ++i) M = fmaxf(M, red[i]);
+  for (int s = threadIdx.x; s < splits; s += kCombThreads) {
+    const float ms = pr[int64_t(s) * (kHeadDim + 2)];
+    wsc[s] = (M == -INFINITY || ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - M);
   }
-  out[int64_t(row) * kHeadDim + d] = L > 0.f ? o / L : 0.f;
-  if (lse && d == 0) lse[row] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+  __syncthreads();
+  const int grp = threadIdx.x / kHeadDim, d = threadIdx.x % kHeadDim;
+  float o = 0.f, L = 0.f;
+#pragma unroll 4
+  for (int s = grp; s < splits; s += kCombGroups) {
+    const float sc = wsc[s];
+    const float* ps_ = pr + int64_t(s) * (kHeadDim + 2);
+    o = fmaf(ps_[2 + d], sc, o);
+    if (d == 0) L = fmaf(ps_[1], sc, L);
+  }
+  po[grp][d] = o;
+  if (d == 0) pl[grp] = L;
+  __syncthreads();
+  if (threadIdx.x < kHeadDim) {
+    float oo = 0.f, LL = 0.f;
+#pragma unroll
+    for (int g = 0; g < kCombGroups; ++g) {
+      oo += po[g][threadIdx.x];
+      LL += pl[g];
+    }
+    out[int64_t(row) * kHeadDim + threadIdx.x] = LL > 0.f ? oo / LL : 0.f;
+    if (lse && threadIdx.x == 0) lse[row] = LL > 0.f ? (M + log2f(LL)) * kLn2 : -INFINITY;
+  }
 }
 
 template <int DT, bool SPARSE>
@@ -351,7 +387,7 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                                            heads_q, heads_kv);
   }
   if (st != RBQ_OK) return st;
-  decode_combine_kernel<<<batch * heads_q, kHeadDim, 0, stream>>>(part, sp.total(), out, lse);
+  decode_combine_kernel<<<batch * heads_q, kCombThreads, 0, stream>>>(part, sp.total(), out, lse);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

@@ -4,15 +4,17 @@
 //   alpha' = sum_j |r_j| / ||x||,  f = ||x|| / alpha',  g = <c_q, x>
 //
 // The rotation is the only dense contraction on the path, so it runs on the
-// matrix cores: each wave rotates 32 keys with v_mfma_f32_32x32x2_f32
-// (fp32 in, fp32 accumulate: the sign decisions need fp32 accuracy, bf16
-// products of P would flip signs of small components). P (64 KB fp32) and
-// the wave's 32 centred keys are staged in LDS. In the 32x32 accumulator
-// layout lane l holds output column l % 32, so one wave ballot of (r > 0)
-// over a register yields two packed 32-bit code words directly.
+// matrix cores with v_mfma_f32_32x32x2_f32 (fp32 in, fp32 accumulate: the sign
+// decisions need fp32 accuracy, bf16 products of P would flip signs of small
+// components). P (64 KB fp32) and a tile of 32 centred keys are staged in LDS.
+// In the 32x32 accumulator layout lane l holds output column l % 32, so one
+// wave ballot of (r > 0) over a register yields two packed 32-bit code words
+// directly.
 //
 // With RBQ_ENCODE_SET_CENTROID a two-pass deterministic column mean over the
 // new keys first sets c_k (fixed-order partial sums, no atomics).
+#include <algorithm>
+
 #include "rbq_device.h"
 #include "rbq_internal.h"
 
@@ -21,10 +23,7 @@ namespace {
 
 constexpr int kEncWaves = 4;
 constexpr int kEncThreads = kEncWaves * kWave;
-constexpr int kKeysPerWave = 32;
-constexpr int kKeysPerBlock = kEncWaves * kKeysPerWave;
 constexpr int kXStride = kHeadDim + 1;        // padded LDS row of a staged key
-constexpr int kRedStride = 33;                // padded LDS row of the |r| partial sums
 
 // ---------------------------------------------------------------- centroid
 template <int DT>
@@ -74,22 +73,29 @@ __global__ __launch_bounds__(kHeadDim) void centroid_final_kernel(const float* _
 }
 
 // ---------------------------------------------------------------- encode
+// A block of 4 waves loops over tiles of 32 keys. The tile's centred keys are
+// staged once in LDS; wave w rotates them onto output dimensions [32 w, 32 w + 32)
+// with 64 dependent MFMAs, so all four matrix cores of the CU work on one tile.
+// P stays in LDS across the block's tiles.
+constexpr int kTileKeys = 32;
+
 template <int DT, bool ROT>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(
     const void* __restrict__ keys, int64_t keys_ld, int n_new, int offset, int cap, const float* __restrict__ P,
     const float* __restrict__ c_q, const float* __restrict__ c_k, uint32_t* __restrict__ codes,
     float* __restrict__ kfac, float* __restrict__ alpha_out, float* __restrict__ rot_out) {
-  __shared__ float Ps[kHeadDim * kHeadDim];                       // 64 KB
-  __shared__ float Xs[kEncWaves][kKeysPerWave * kXStride];        // 66 KB (reused for the |r| sums)
+  __shared__ __attribute__((aligned(16))) float Ps[kHeadDim * kHeadDim];   // 64 KB
+  __shared__ float Xs[kTileKeys * kXStride];                                // the tile's centred keys
   __shared__ float ck_s[kHeadDim], cq_s[kHeadDim];
-  __shared__ uint32_t code_s[kEncWaves][kKeysPerWave][kWords];
+  __shared__ uint32_t code_s[kTileKeys][kWords];
+  __shared__ float abs_s[kEncWaves][kTileKeys];
+  __shared__ float ng_s[2][kTileKeys];
 
   const int bh = blockIdx.y;
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = lane_id();
-  const int key0 = blockIdx.x * kKeysPerBlock + wave * kKeysPerWave;
+  const int mk = lane % 32, half = lane / 32;
 
-  // stage P and the centroids
   for (int e = threadIdx.x * 4; e < kHeadDim * kHeadDim; e += kEncThreads * 4)
     *reinterpret_cast<f32x4*>(Ps + e) = *reinterpret_cast<const f32x4*>(P + e);
   if (threadIdx.x < kHeadDim) {
@@ -98,94 +104,110 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
   }
   __syncthreads();
 
-  // stage this wave's 32 centred keys: lane l holds dims 2l, 2l + 1 of each row
-  float* X = Xs[wave];
-  for (int m = 0; m < kKeysPerWave; ++m) {
-    const int key = key0 + m;
-    float x0 = 0.f, x1 = 0.f;
-    if (key < n_new) {
-      const int64_t e = (int64_t(bh) * keys_ld + key) * kHeadDim + 2 * lane;
+  const int tiles = (n_new + kTileKeys - 1) / kTileKeys;
+  for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const int key0 = tile * kTileKeys;
+    // ---- stage the tile: 16-byte pieces, consecutive threads on consecutive pieces
+    constexpr int kElemBytes = DT == RBQ_BF16 ? 2 : 4;
+    constexpr int kPiecesPerRow = kHeadDim * kElemBytes / 16;            // 16 (bf16) or 32 (fp32)
+    constexpr int kPer = kTileKeys * kPiecesPerRow / kEncThreads;         // 2 or 4 per thread
+    u32x4 pc[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int pidx = j * kEncThreads + threadIdx.x;
+      const int row = pidx / kPiecesPerRow, piece = pidx % kPiecesPerRow;
+      const int key = key0 + row;
+      pc[j] = key < n_new ? *reinterpret_cast<const u32x4*>(static_cast<const char*>(keys) +
+                                                           ((int64_t(bh) * keys_ld + key) * kHeadDim) * kElemBytes +
+                                                           piece * 16)
+                          : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int pidx = j * kEncThreads + threadIdx.x;
+      const int row = pidx / kPiecesPerRow, piece = pidx % kPiecesPerRow;
+      const bool in = key0 + row < n_new;
+      float* xr = Xs + row * kXStride;
       if (DT == RBQ_BF16) {
-        const uint32_t v = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(keys) + e);
-        x0 = bf16_lo(v) - ck_s[2 * lane];
-        x1 = bf16_hi(v) - ck_s[2 * lane + 1];
+        const int d = piece * 8;
+        const uint32_t wv[4] = {pc[j].x, pc[j].y, pc[j].z, pc[j].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          xr[d + 2 * e] = in ? bf16_lo(wv[e]) - ck_s[d + 2 * e] : 0.f;
+          xr[d + 2 * e + 1] = in ? bf16_hi(wv[e]) - ck_s[d + 2 * e + 1] : 0.f;
+        }
       } else {
-        const f32x2 v = *reinterpret_cast<const f32x2*>(static_cast<const float*>(keys) + e);
-        x0 = v.x - ck_s[2 * lane];
-        x1 = v.y - ck_s[2 * lane + 1];
+        const int d = piece * 4;
+        xr[d] = in ? __uint_as_float(pc[j].x) - ck_s[d] : 0.f;
+        xr[d + 1] = in ? __uint_as_float(pc[j].y) - ck_s[d + 1] : 0.f;
+        xr[d + 2] = in ? __uint_as_float(pc[j].z) - ck_s[d + 2] : 0.f;
+        xr[d + 3] = in ? __uint_as_float(pc[j].w) - ck_s[d + 3] : 0.f;
       }
     }
-    X[m * kXStride + 2 * lane] = x0;
-    X[m * kXStride + 2 * lane + 1] = x1;
-  }
-  __syncthreads();
+    __syncthreads();
 
-  // ||x||^2 and <c_q, x>: lane l takes key l % 32, half (l / 32) of the dims
-  const int mk = lane % 32;
-  const int half = lane / 32;
-  float nn = 0.f, gg = 0.f;
-  for (int d = half * 64; d < half * 64 + 64; ++d) {
-    const float x = X[mk * kXStride + d];
-    nn = fmaf(x, x, nn);
-    gg = fmaf(cq_s[d], x, gg);
-  }
-  nn += __shfl_xor(nn, 32, kWave);
-  gg += __shfl_xor(gg, 32, kWave);
-
-  // r = x P on the matrix cores: A = X (32 keys x 2 dims per step), B = P rows
-  f32x16 acc[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) acc[t] = f32x16{0.f};
-  for (int s = 0; s < kHeadDim / 2; ++s) {
-    const int k = 2 * s + half;
-    const float a = X[mk * kXStride + k];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const float b = Ps[k * kHeadDim + 32 * t + mk];
-      acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[t], 0, 0, 0);
+    // ---- ||x||^2 and <c_q, x>: threads 0..127, key t / 4, a quarter of the dims each
+    if (threadIdx.x < 4 * kTileKeys) {
+      const int kk = threadIdx.x / 4, qd = threadIdx.x % 4;
+      float nn = 0.f, gg = 0.f;
+#pragma unroll 8
+      for (int d = qd * 32; d < qd * 32 + 32; ++d) {
+        const float x = Xs[kk * kXStride + d];
+        nn = fmaf(x, x, nn);
+        gg = fmaf(cq_s[d], x, gg);
+      }
+      nn += RBQ_DPP(nn, 0xB1);
+      nn += RBQ_DPP(nn, 0x4E);
+      gg += RBQ_DPP(gg, 0xB1);
+      gg += RBQ_DPP(gg, 0x4E);
+      if (qd == 0) {
+        ng_s[0][kk] = nn;
+        ng_s[1][kk] = gg;
+      }
     }
-  }
-  __syncthreads();   // every wave is done reading X before it is reused
 
-  // acc[t][r] at lane l: key 8 (r / 4) + 4 (l / 32) + r % 4, dimension 32 t + l % 32
-  float* red = X;    // [32 keys][kRedStride]
+    // ---- r = x P for output dimensions [32 wave, 32 wave + 32): A = X rows, B = P rows
+    f32x16 acc = f32x16{0.f};
+    for (int s2 = 0; s2 < kHeadDim / 2; ++s2) {
+      const int k = 2 * s2 + half;
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(Xs[mk * kXStride + k], Ps[k * kHeadDim + 32 * wave + mk], acc, 0,
+                                                 0, 0);
+    }
+    // acc[r] at lane l: key 8 (r / 4) + 4 (l / 32) + r % 4, dimension 32 wave + l % 32
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int key_r = 8 * (r / 4) + 4 * half + (r % 4);
-    float a = 0.f;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const float v = acc[t][r];
-      a += fabsf(v);
+    for (int r = 0; r < 16; ++r) {
+      const float v = acc[r];
       const uint64_t bal = __ballot(v > 0.f);
+      const float a = sum32(fabsf(v));
+      const int key_a = 8 * (r / 4) + (r % 4);
       if (lane == 0) {
-        code_s[wave][8 * (r / 4) + (r % 4)][t] = uint32_t(bal);
-        code_s[wave][8 * (r / 4) + 4 + (r % 4)][t] = uint32_t(bal >> 32);
+        code_s[key_a][wave] = uint32_t(bal);
+        code_s[key_a + 4][wave] = uint32_t(bal >> 32);
+        abs_s[wave][key_a] = a;
       }
+      if (lane == 32) abs_s[wave][key_a + 4] = a;
       if (ROT) {
-        const int key = key0 + key_r;
-        if (key < n_new) rot_out[(int64_t(bh) * n_new + key) * kHeadDim + 32 * t + mk] = v;
+        const int key = key0 + key_a + 4 * half;
+        if (key < n_new) rot_out[(int64_t(bh) * n_new + key) * kHeadDim + 32 * wave + mk] = v;
       }
     }
-    red[key_r * kRedStride + mk] = a;
-  }
-  __syncthreads();
+    __syncthreads();
 
-  if (lane < kKeysPerWave) {
-    const int key = key0 + lane;
-    float absum = 0.f;
-#pragma unroll
-    for (int t = 0; t < 32; ++t) absum += red[lane * kRedStride + t];
-    const float nrm = sqrtf(nn);
-    const float alpha_p = nrm > 0.f ? absum / nrm : 0.f;
-    const float f = alpha_p > 0.f ? nrm / alpha_p : 0.f;
-    if (key < n_new) {
-      const int64_t o = int64_t(bh) * cap + offset + key;
-      *reinterpret_cast<u32x4*>(codes + o * kWords) =
-          u32x4{code_s[wave][lane][0], code_s[wave][lane][1], code_s[wave][lane][2], code_s[wave][lane][3]};
-      *reinterpret_cast<f32x2*>(kfac + o * 2) = f32x2{f, gg};
-      if (alpha_out) alpha_out[int64_t(bh) * n_new + key] = alpha_p * 0.08838834764831845f;   // 1/sqrt(128)
+    if (threadIdx.x < kTileKeys) {
+      const int t = threadIdx.x;
+      const int key = key0 + t;
+      const float absum = (abs_s[0][t] + abs_s[1][t]) + (abs_s[2][t] + abs_s[3][t]);
+      const float nrm = sqrtf(ng_s[0][t]);
+      const float alpha_p = nrm > 0.f ? absum / nrm : 0.f;
+      const float f = alpha_p > 0.f ? nrm / alpha_p : 0.f;
+      if (key < n_new) {
+        const int64_t o = int64_t(bh) * cap + offset + key;
+        *reinterpret_cast<u32x4*>(codes + o * kWords) = u32x4{code_s[t][0], code_s[t][1], code_s[t][2], code_s[t][3]};
+        *reinterpret_cast<f32x2*>(kfac + o * 2) = f32x2{f, ng_s[1][t]};
+        if (alpha_out) alpha_out[int64_t(bh) * n_new + key] = alpha_p * 0.08838834764831845f;   // 1/sqrt(128)
+      }
     }
+    __syncthreads();   // the tile buffers are refilled next
   }
 }
 
@@ -200,7 +222,10 @@ rbq_status launch_dt(int32_t batch, int32_t heads_kv, const void* keys, int64_t 
     centroid_partial_kernel<DT><<<dim3(chunks, bhs), 256, 0, stream>>>(keys, keys_ld, n_new, partial, chunks);
     centroid_final_kernel<<<bhs, kHeadDim, 0, stream>>>(partial, chunks, n_new, c_k);
   }
-  const dim3 grid((n_new + kKeysPerBlock - 1) / kKeysPerBlock, bhs);
+  // enough blocks to cover the CUs a few times; each loops over its tiles with P kept in LDS
+  const int tiles = (n_new + kTileKeys - 1) / kTileKeys;
+  const int per_head = std::max(1, std::min(tiles, 2048 / std::max(1, bhs)));
+  const dim3 grid(per_head, bhs);
   if (rot_out)
     encode_kernel<DT, true><<<grid, kEncThreads, 0, stream>>>(keys, keys_ld, n_new, offset, cap, P, c_q, c_k, codes,
                                                              kfac, alpha_out, rot_out);

@@ -1,7 +1,8 @@
 // rbq_quantize_query: query pre-processing and INT4 quantisation
 // (Algorithm 2 step 1; Section 3.3 "Query Quantization"; Appendix A.3.2).
 //
-// One block of D = 128 threads per query head, one thread per dimension:
+// One block per query head; 4 x 128 threads share the 128 x 128 product (all
+// loads of a thread in flight at once), then 128 threads, one per dimension:
 //   y = q - c_q, A = ||y||, u = y / A, q'[j] = sum_d P[d][j] u[d]   (q' = P^T u)
 //   q_l = min q', q_r = max q', Delta = (q_r - q_l) / 15,
 //   q_u = clamp(floor((q' - q_l) / Delta + 1/2), 0, 15)
@@ -16,14 +17,17 @@
 namespace rbq {
 namespace {
 
-constexpr int kQThreads = kHeadDim;   // one thread per dimension
+constexpr int kQThreads = kHeadDim;   // one thread per output dimension in the epilogue
 constexpr int kQWaves = kQThreads / kWave;
+constexpr int kQParts = 4;            // the matrix-vector product is split over 4 thread groups
+constexpr int kQAll = kQParts * kQThreads;
 
+// reductions over the first kQWaves waves (the other waves take part in the barriers only)
 __device__ __forceinline__ float block_sum(float v, float* red) {
   v = wave_sum(v);
   const int w = threadIdx.x / kWave;
   __syncthreads();
-  if (lane_id() == 0) red[w] = v;
+  if (lane_id() == 0 && w < kQWaves) red[w] = v;
   __syncthreads();
   float s = 0.f;
 #pragma unroll
@@ -31,11 +35,24 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return s;
 }
 
+// sum over all kQAll threads of the block
+__device__ __forceinline__ float block_sum_all(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x / kWave;
+  __syncthreads();
+  if (lane_id() == 0) red[w] = v;
+  __syncthreads();
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kQAll / kWave; ++i) s += red[i];
+  return s;
+}
+
 __device__ __forceinline__ float block_min(float v, float* red) {
   v = wave_min(v);
   const int w = threadIdx.x / kWave;
   __syncthreads();
-  if (lane_id() == 0) red[w] = v;
+  if (lane_id() == 0 && w < kQWaves) red[w] = v;
   __syncthreads();
   float s = red[0];
 #pragma unroll
@@ -47,7 +64,7 @@ __device__ __forceinline__ float block_max(float v, float* red) {
   v = wave_max(v);
   const int w = threadIdx.x / kWave;
   __syncthreads();
-  if (lane_id() == 0) red[w] = v;
+  if (lane_id() == 0 && w < kQWaves) red[w] = v;
   __syncthreads();
   float s = red[0];
 #pragma unroll
@@ -65,37 +82,54 @@ __device__ __forceinline__ int quant_code(float x, float ql, float delta) {
   return int(r);
 }
 
-__global__ __launch_bounds__(kQThreads) void quantize_kernel(const float* __restrict__ q, const float* __restrict__ P,
+__global__ __launch_bounds__(kQAll) void quantize_kernel(const float* __restrict__ q, const float* __restrict__ P,
                                                              const float* __restrict__ c_q,
                                                              const float* __restrict__ c_k,
                                                              uint32_t* __restrict__ qplanes,
                                                              float* __restrict__ qscal, float* __restrict__ qrot_out,
                                                              int Hq, int Hkv) {
   __shared__ float u_s[kHeadDim];
-  __shared__ float red[4 * kQWaves];
+  __shared__ float part_s[kQParts][kHeadDim];
+  __shared__ float red[2 * (kQAll / kWave) + 2 * kQWaves];
   const int row = blockIdx.x;                  // b * Hq + h
   const int b = row / Hq;
   const int h = row - b * Hq;
   const int grp = b * Hkv + h / (Hq / Hkv);    // (b, kv head)
-  const int j = threadIdx.x;
+  const int j = threadIdx.x % kHeadDim;        // output dimension
+  const int part = threadIdx.x / kHeadDim;     // which quarter of the input dimensions
 
-  const float qj = q[int64_t(row) * kHeadDim + j];
-  const float cq = c_q ? c_q[int64_t(grp) * kHeadDim + j] : 0.f;
-  const float ck = c_k[int64_t(grp) * kHeadDim + j];
-  const float y = qj - cq;
-  const float A = sqrtf(block_sum(y * y, red));
-  const float B0 = block_sum(qj * ck, red + kQWaves);
-  u_s[j] = A > 0.f ? y / A : 0.f;
+  float qj = 0.f, y = 0.f, ck = 0.f;
+  if (part == 0) {
+    qj = q[int64_t(row) * kHeadDim + j];
+    const float cq = c_q ? c_q[int64_t(grp) * kHeadDim + j] : 0.f;
+    ck = c_k[int64_t(grp) * kHeadDim + j];
+    y = qj - cq;
+  }
+  // the first two waves hold the vector; the block sums include zeros from the others
+  const float A = sqrtf(block_sum_all(y * y, red));
+  const float B0 = block_sum_all(qj * ck, red + kQAll / kWave);
+  if (part == 0) u_s[j] = A > 0.f ? y / A : 0.f;
   __syncthreads();
 
-  // q'[j] = sum_d P[d][j] u[d]: threads read row d of P together (coalesced)
+  // q'[j] = sum_d P[d][j] u[d]: each group takes 32 rows of P, all loads in flight at once
   float acc = 0.f;
-#pragma unroll 8
-  for (int d = 0; d < kHeadDim; ++d) acc = fmaf(P[d * kHeadDim + j], u_s[d], acc);
-  if (qrot_out) qrot_out[int64_t(row) * kHeadDim + j] = acc;
+  {
+    constexpr int kRows = kHeadDim / kQParts;
+    float pv[kRows];
+#pragma unroll
+    for (int k = 0; k < kRows; ++k) pv[k] = P[(part * kRows + k) * kHeadDim + j];
+#pragma unroll
+    for (int k = 0; k < kRows; ++k) acc = fmaf(pv[k], u_s[part * kRows + k], acc);
+  }
+  part_s[part][j] = acc;
+  __syncthreads();
+  // every thread computes the sum; only the first 128 (two waves) use it
+  acc = (part_s[0][j] + part_s[1][j]) + (part_s[2][j] + part_s[3][j]);
+  const bool lead = part == 0;
+  if (qrot_out && lead) qrot_out[int64_t(row) * kHeadDim + j] = acc;
 
-  const float ql = block_min(acc, red + 2 * kQWaves);
-  const float qr = block_max(acc, red + 3 * kQWaves);
+  const float ql = block_min(acc, red + 2 * (kQAll / kWave));
+  const float qr = block_max(acc, red + 2 * (kQAll / kWave) + kQWaves);
   float delta;
   {
 #pragma clang fp contract(off)
@@ -110,12 +144,12 @@ __global__ __launch_bounds__(kQThreads) void quantize_kernel(const float* __rest
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
     const uint64_t bal = __ballot((code >> m) & 1);
-    if (lane_id() == 0) {
+    if (lead && lane_id() == 0) {
       planes[m * kWords + 2 * w] = uint32_t(bal);
       planes[m * kWords + 2 * w + 1] = uint32_t(bal >> 32);
     }
   }
-  if (j < RBQ_QSCAL_STRIDE) {
+  if (lead && j < RBQ_QSCAL_STRIDE) {
     float v = 0.f;
     if (j == 0) v = ql;
     else if (j == 1) v = delta;
@@ -132,7 +166,7 @@ __global__ __launch_bounds__(kQThreads) void quantize_kernel(const float* __rest
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
                            hipStream_t stream) {
-  quantize_kernel<<<batch * heads_q, kQThreads, 0, stream>>>(q, P, c_q, c_k, qplanes, qscal, qrot_out, heads_q,
+  quantize_kernel<<<batch * heads_q, kQAll, 0, stream>>>(q, P, c_q, c_k, qplanes, qscal, qrot_out, heads_q,
                                                              heads_kv);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }

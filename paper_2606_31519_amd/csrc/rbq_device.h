@@ -37,6 +37,28 @@ __device__ __forceinline__ int wave_sum_int(int v) {
   return v;
 }
 
+// Reductions over each group of 32 lanes (both halves of the wave reduce
+// independently): DPP within 16-lane rows, then a swizzle across row pairs.
+#define RBQ_DPP(v, ctrl) \
+  __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, (v)), (ctrl), 0xF, 0xF, false))
+__device__ __forceinline__ float swap16(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+}
+__device__ __forceinline__ float max32(float v) {
+  v = fmaxf(v, RBQ_DPP(v, 0xB1));    // quad_perm [1,0,3,2]
+  v = fmaxf(v, RBQ_DPP(v, 0x4E));    // quad_perm [2,3,0,1]
+  v = fmaxf(v, RBQ_DPP(v, 0x141));   // row_half_mirror
+  v = fmaxf(v, RBQ_DPP(v, 0x140));   // row_mirror
+  return fmaxf(v, swap16(v));
+}
+__device__ __forceinline__ float sum32(float v) {
+  v += RBQ_DPP(v, 0xB1);
+  v += RBQ_DPP(v, 0x4E);
+  v += RBQ_DPP(v, 0x141);
+  v += RBQ_DPP(v, 0x140);
+  return v + swap16(v);
+}
+
 // bf16 bit patterns packed two per 32-bit word: low half is the lower index.
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -49,5 +71,11 @@ __device__ __forceinline__ uint32_t score_key(float s) {
 }
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Raw buffer resource over `bytes` bytes from `base` (gfx9 descriptor word 3):
+// loads through it are range-checked by the hardware and return 0 past the end.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), 0x00020000);
+}
 
 }  // namespace rbq

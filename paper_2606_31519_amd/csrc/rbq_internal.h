@@ -45,14 +45,15 @@ constexpr int kToppStateWords = 8;                          // per-row uint32 st
 struct ToppWorkspace {
   float* chunk_max;             // [rows][chunks]
   unsigned long long* hist;     // [rows][kHistPerRow]
-  int32_t* chunk_cnt;           // [rows][chunks]
+  int32_t* chunk_cnt;           // [rows][chunks][1 + kBins3]: keys above the final bin, then
+                                // suffix counts of the final bin's 256 sub-bins
   uint32_t* state;              // [rows][kToppStateWords]
   size_t bytes;
 };
 ToppWorkspace topp_workspace(void* base, int64_t rows, int32_t n);
 
 // Decode: split-K over chunks of the indexed rows and of the window.
-constexpr int kDecodeChunk = 2048;        // indexed positions per block
+constexpr int kDecodeChunk = 1024;        // indexed positions per block (at most)
 constexpr int kDecodeWinChunk = 256;      // window rows per block
 struct DecodeSplits {
   int32_t chunk;            // indexed positions per split (<= kDecodeChunk)

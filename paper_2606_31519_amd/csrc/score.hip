@@ -86,7 +86,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         const float s = fmaf(fg[u].x, y, B0 + fg[u].y);
-        if (i < n) __builtin_nontemporal_store(s, out + i);
+        if (i < n) out[i] = s;   // cached store: the Top-p passes read the scores next
       }
     }
   }

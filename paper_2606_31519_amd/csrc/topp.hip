@@ -15,13 +15,21 @@
 // each) and fp32 exp (~1 ulp) leave the decision within ~1e-6 of the exact
 // cumulative mass.
 //
-// Kernels, each over grid (chunks of 4096 scores, rows):
+// Kernels, each over grid (chunks of 4096 scores, rows). The crossing searches
+// are repeated by every block of a row (a parallel scan over the row's bins,
+// read from L2), which costs less than an extra launch and needs neither
+// cross-block waiting nor device-wide fences:
 //   1 max        per-chunk max; clears the row's histograms
-//   2 level 1    global max; 4096-bin histogram of key bits 31..20
-//   3 level 2    find the crossing bin b1; histogram of bits 19..8 inside b1
-//   4 level 3    find b2; histogram of bits 7..0 inside (b1, b2)
-//   5 count      find b3, K* = (b1, b2, b3); per-chunk count of keys >= K*
-//   6 write      prefix over chunk counts; ascending compaction
+//   2 level 1    row max; 4096-bin histogram of key bits 31..20
+//   3 level 2    total mass Z, target T = ceil(p Z), crossing bin b1;
+//                histogram of bits 19..8 inside b1
+//   4 level 3    crossing b2; histogram of bits 7..0 inside (b1, b2); per
+//                chunk: the count of keys above that 24-bit bin and the suffix
+//                counts of its 256 sub-bins
+//   5 write      crossing b3 and K*; offset = sum over the earlier chunks of
+//                (count above + suffix count at b3); ascending compaction
+// Every pass issues its 16 loads per thread up front (indices clamped, the
+// out-of-range values masked), so a pass costs one memory round trip.
 #include <cmath>
 
 #include "rbq_device.h"
@@ -34,6 +42,7 @@ typedef unsigned long long u64;
 constexpr int kT = kToppThreads;
 constexpr int kPT = kToppPerThread;
 constexpr int kChunk = kToppChunk;
+constexpr int kTW = kT / kWave;            // waves per block
 constexpr float kFix = 1099511627776.0f;   // 2^40
 
 // softmax mass of one score in 2^-40 units; every pass evaluates it with the
@@ -43,71 +52,99 @@ __device__ __forceinline__ u64 fixed_mass(float s, float m, float scale_log2e) {
   return u64(__fmul_rn(e, kFix));
 }
 
-__device__ __forceinline__ float load_row_max(const float* chunk_max, int chunks, float* red) {
-  float m = -INFINITY;
-  for (int c = threadIdx.x; c < chunks; c += kT) m = fmaxf(m, chunk_max[c]);
+__device__ __forceinline__ u64 shfl_down_u64(u64 v, int o) {
+  const uint32_t lo = __shfl_down(uint32_t(v), o, kWave);
+  const uint32_t hi = __shfl_down(uint32_t(v >> 32), o, kWave);
+  return (u64(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ float block_max(float m, float* red) {
   m = wave_max(m);
   __syncthreads();
   if (lane_id() == 0) red[threadIdx.x / kWave] = m;
   __syncthreads();
-  m = red[0];
+  float r = red[0];
 #pragma unroll
-  for (int w = 1; w < kT / kWave; ++w) m = fmaxf(m, red[w]);
-  return m;
+  for (int w = 1; w < kTW; ++w) r = fmaxf(r, red[w]);
+  return r;
 }
 
-// Among `nbins` global bins (mass counters), find the highest bin b whose
-// suffix mass sum_{b' >= b} reaches T. Writes b and the mass still needed from
-// inside b (T - sum_{b' > b}) to *out (visible after the trailing barrier).
+// Crossing search over `nbins` counters of one row (bins ordered by key): the
+// highest bin b with sum_{b' >= b} hist[b'] >= T. With `frac` > 0 the target
+// is T = ceil(frac * total). Returns b and the mass needed inside it,
+// T - sum_{b' > b}, in *out (valid after the trailing barrier). Exactly one
+// thread matches, because the suffix sums grow monotonically from 0 to the
+// total and 1 <= T <= total.
 struct Crossing {
   uint32_t bin;
+  uint32_t pad;
   u64 need;
 };
-__device__ void find_crossing(const u64* __restrict__ hist, int nbins, u64 T, u64* scan, Crossing* out) {
-  const int bpt = nbins / kT;   // bins per thread: 16 or 1
-  const int t = threadIdx.x;
-  u64 local = 0;
-  for (int k = 0; k < bpt; ++k) local += hist[t * bpt + k];
-  // inclusive suffix scan over threads: scan[t] = sum_{t' >= t} local_t'
-  scan[t] = local;
-  __syncthreads();
-  for (int off = 1; off < kT; off <<= 1) {
-    const u64 add = (t + off < kT) ? scan[t + off] : 0;
-    __syncthreads();
-    scan[t] += add;
-    __syncthreads();
+template <int BPT>
+__device__ void find_crossing(const u64* __restrict__ hist, u64 T, float frac, u64* wtot, Crossing* out) {
+  const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  u64 h[BPT];
+  u64 s = 0;
+#pragma unroll
+  for (int k = 0; k < BPT; ++k) {
+    h[k] = hist[t * BPT + k];
+    s += h[k];
   }
-  u64 cum = (t + 1 < kT) ? scan[t + 1] : 0;   // mass strictly above this thread's bins
-  for (int k = bpt - 1; k >= 0; --k) {
-    const u64 h = hist[t * bpt + k];
-    if (cum < T && cum + h >= T) {
-      out->bin = uint32_t(t * bpt + k);
+  // inclusive suffix sum inside the wave (higher lanes hold higher bins)
+  u64 x = s;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const u64 y = shfl_down_u64(x, o);
+    if (lane + o < kWave) x += y;
+  }
+  __syncthreads();   // wtot may still be read by a previous search
+  if (lane == 0) wtot[w] = x;
+  __syncthreads();
+  u64 above = x - s;                        // strictly above this thread's bins, inside the wave
+  u64 total = 0;
+#pragma unroll
+  for (int v = 0; v < kTW; ++v) {
+    total += wtot[v];
+    if (v > w) above += wtot[v];
+  }
+  if (frac > 0.f) T = u64(ceil(double(frac) * double(total)));
+  u64 cum = above;
+#pragma unroll
+  for (int k = BPT - 1; k >= 0; --k) {
+    if (cum < T && cum + h[k] >= T) {
+      out->bin = uint32_t(t * BPT + k);
       out->need = T - cum;
     }
-    cum += h;
+    cum += h[k];
   }
   __syncthreads();
+}
+
+// the thread's kPT scores of chunk c (element c * kChunk + k * kT + tid), all loads in flight
+__device__ __forceinline__ void load_chunk(const float* __restrict__ s, int n, int c, float* v) {
+#pragma unroll
+  for (int k = 0; k < kPT; ++k) v[k] = s[min(c * kChunk + k * kT + int(threadIdx.x), n - 1)];
+}
+__device__ __forceinline__ bool in_row(int n, int c, int k) { return c * kChunk + k * kT + int(threadIdx.x) < n; }
+
+__device__ __forceinline__ float row_max(const float* __restrict__ chunk_max, int chunks, float* red) {
+  float m = -INFINITY;
+  for (int k = threadIdx.x; k < chunks; k += kT) m = fmaxf(m, chunk_max[k]);
+  return block_max(m, red);
 }
 
 __global__ __launch_bounds__(kT) void topp_max_kernel(const float* __restrict__ scores, int n, int chunks,
                                                       float* __restrict__ chunk_max, u64* __restrict__ hist) {
-  __shared__ float red[kT / kWave];
+  __shared__ float red[kTW];
   const int row = blockIdx.y, c = blockIdx.x;
-  const float* s = scores + int64_t(row) * n;
+  float v[kPT];
+  load_chunk(scores + int64_t(row) * n, n, c, v);
   float m = -INFINITY;
 #pragma unroll
-  for (int k = 0; k < kPT; ++k) {
-    const int i = c * kChunk + k * kT + threadIdx.x;
-    if (i < n) m = fmaxf(m, s[i]);
-  }
-  m = wave_max(m);
-  if (lane_id() == 0) red[threadIdx.x / kWave] = m;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float r = red[0];
-    for (int w = 1; w < kT / kWave; ++w) r = fmaxf(r, red[w]);
-    chunk_max[int64_t(row) * chunks + c] = r;
-  }
+  for (int k = 0; k < kPT; ++k)
+    if (in_row(n, c, k)) m = fmaxf(m, v[k]);
+  m = block_max(m, red);
+  if (threadIdx.x == 0) chunk_max[int64_t(row) * chunks + c] = m;
   // this block's share of the row's histogram counters
   const int per = (kHistPerRow + chunks - 1) / chunks;
   const int e0 = c * per, e1 = min(kHistPerRow, e0 + per);
@@ -119,67 +156,57 @@ __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict
                                                          const float* __restrict__ chunk_max, float scale_log2e,
                                                          u64* __restrict__ hist) {
   __shared__ u64 h[kBins1];
-  __shared__ float red[kT / kWave];
+  __shared__ float red[kTW];
   const int row = blockIdx.y, c = blockIdx.x;
   for (int b = threadIdx.x; b < kBins1; b += kT) h[b] = 0;
-  const float m = load_row_max(chunk_max + int64_t(row) * chunks, chunks, red);   // has barriers
-  const float* s = scores + int64_t(row) * n;
-#pragma unroll 4
-  for (int k = 0; k < kPT; ++k) {
-    const int i = c * kChunk + k * kT + threadIdx.x;
-    if (i < n) {
-      const float v = s[i];
-      atomicAdd(&h[score_key(v) >> 20], fixed_mass(v, m, scale_log2e));
-    }
-  }
+  float v[kPT];
+  load_chunk(scores + int64_t(row) * n, n, c, v);
+  const float m = row_max(chunk_max + int64_t(row) * chunks, chunks, red);   // barriers: h is clear after it
+#pragma unroll
+  for (int k = 0; k < kPT; ++k)
+    if (in_row(n, c, k)) atomicAdd(&h[score_key(v[k]) >> 20], fixed_mass(v[k], m, scale_log2e));
   __syncthreads();
   u64* g = hist + int64_t(row) * kHistPerRow;
   for (int b = threadIdx.x; b < kBins1; b += kT)
     if (h[b]) atomicAdd(&g[b], h[b]);
 }
 
-// Level 2 (LEVEL == 2) or level 3 (LEVEL == 3) histogram inside the crossing bin(s).
+// Level 2 (LEVEL == 2) or level 3 (LEVEL == 3): find the previous level's
+// crossing, then histogram the keys inside it.
 template <int LEVEL>
 __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict__ scores, int n, int chunks,
                                                         const float* __restrict__ chunk_max, float scale_log2e,
                                                         float p, u64* __restrict__ hist,
-                                                        uint32_t* __restrict__ state) {
+                                                        uint32_t* __restrict__ state,
+                                                        int32_t* __restrict__ chunk_cnt) {
   constexpr int kBins = LEVEL == 2 ? kBins2 : kBins3;
   __shared__ u64 h[kBins];
-  __shared__ u64 scan[kT];
-  __shared__ float red[kT / kWave];
+  __shared__ uint32_t cnt_s[LEVEL == 3 ? kBins3 + 1 : 1];
+  __shared__ int red2[kTW];
+  if (LEVEL == 3)
+    for (int b = threadIdx.x; b <= kBins3; b += kT) cnt_s[b] = 0;
+  __shared__ u64 wtot[kTW];
+  __shared__ float red[kTW];
   __shared__ Crossing cr;
   const int row = blockIdx.y, c = blockIdx.x;
   u64* rh = hist + int64_t(row) * kHistPerRow;
   uint32_t* st = state + int64_t(row) * kToppStateWords;
   for (int b = threadIdx.x; b < kBins; b += kT) h[b] = 0;
-  const float m = load_row_max(chunk_max + int64_t(row) * chunks, chunks, red);
-
-  // state words: [0..2] = level-1 bin and the mass still needed inside it
-  // (written by level 2), [3..5] = the same for level 2 (written by level 3),
-  // [6] = K* (written by count). A kernel never rewrites what it reads.
-  uint32_t prefix;   // key bits fixed so far
+  float v[kPT];
+  load_chunk(scores + int64_t(row) * n, n, c, v);
+  const float m = row_max(chunk_max + int64_t(row) * chunks, chunks, red);
+  uint32_t prefix;
   if (LEVEL == 2) {
-    // total mass and target from the level-1 histogram
-    u64 local = 0;
-    for (int b = threadIdx.x; b < kBins1; b += kT) local += rh[b];
-    scan[threadIdx.x] = local;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      u64 z = 0;
-      for (int t = 0; t < kT; ++t) z += scan[t];
-      scan[0] = u64(ceil(double(p) * double(z)));   // mass to reach, >= 1
-    }
-    __syncthreads();
-    const u64 T = scan[0];
-    __syncthreads();
-    find_crossing(rh, kBins1, T, scan, &cr);
+    find_crossing<kBins1 / kT>(rh, 0, p, wtot, &cr);
     prefix = cr.bin;
   } else {
     const u64 T = (u64(st[2]) << 32) | st[1];
-    find_crossing(rh + kBins1, kBins2, T, scan, &cr);
+    find_crossing<kBins2 / kT>(rh + kBins1, T, 0.f, wtot, &cr);
     prefix = (st[0] << 12) | cr.bin;
   }
+  // state words: [0..2] = level-1 bin and the mass still needed inside it
+  // (written by level 2), [3..5] = the same for level 2 (written by level 3);
+  // a kernel never rewrites what it reads
   if (c == 0 && threadIdx.x == 0) {
     const int o = LEVEL == 2 ? 0 : 3;
     st[o] = prefix;
@@ -187,79 +214,79 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
     st[o + 2] = uint32_t(cr.need >> 32);
   }
   const int shift_hi = LEVEL == 2 ? 20 : 8;
-  const float* s = scores + int64_t(row) * n;
-#pragma unroll 4
+  int above = 0;   // level 3: keys above the 24-bit bin, certainly selected
+#pragma unroll
   for (int k = 0; k < kPT; ++k) {
-    const int i = c * kChunk + k * kT + threadIdx.x;
-    if (i < n) {
-      const float v = s[i];
-      const uint32_t key = score_key(v);
-      if ((key >> shift_hi) == prefix) {
-        const uint32_t bin = LEVEL == 2 ? ((key >> 8) & 0xfffu) : (key & 0xffu);
-        atomicAdd(&h[bin], fixed_mass(v, m, scale_log2e));
-      }
+    if (!in_row(n, c, k)) continue;
+    const uint32_t key = score_key(v[k]);
+    if ((key >> shift_hi) == prefix) {
+      const uint32_t bin = LEVEL == 2 ? ((key >> 8) & 0xfffu) : (key & 0xffu);
+      atomicAdd(&h[bin], fixed_mass(v[k], m, scale_log2e));
+      if (LEVEL == 3) atomicAdd(&cnt_s[bin], 1u);
+    } else if (LEVEL == 3 && (key >> 8) > prefix) {
+      ++above;
     }
+  }
+  if (LEVEL == 3) {
+    above = wave_sum_int(above);
+    if (lane_id() == 0) atomicAdd(&cnt_s[kBins3], uint32_t(above));
   }
   __syncthreads();
   u64* g = rh + (LEVEL == 2 ? kBins1 : kBins1 + kBins2);
   for (int b = threadIdx.x; b < kBins; b += kT)
     if (h[b]) atomicAdd(&g[b], h[b]);
-}
-
-__global__ __launch_bounds__(kT) void topp_count_kernel(const float* __restrict__ scores, int n, int chunks,
-                                                        const u64* __restrict__ hist, uint32_t* __restrict__ state,
-                                                        int32_t* __restrict__ chunk_cnt) {
-  __shared__ u64 scan[kT];
-  __shared__ int red[kT / kWave];
-  __shared__ Crossing cr;
-  const int row = blockIdx.y, c = blockIdx.x;
-  uint32_t* st = state + int64_t(row) * kToppStateWords;
-  const u64 T = (u64(st[5]) << 32) | st[4];
-  const uint32_t prefix = st[3];
-  find_crossing(hist + int64_t(row) * kHistPerRow + kBins1 + kBins2, kBins3, T, scan, &cr);
-  const uint32_t kstar = (prefix << 8) | cr.bin;
-  if (c == 0 && threadIdx.x == 0) st[6] = kstar;
-  const float* s = scores + int64_t(row) * n;
-  int cnt = 0;
-#pragma unroll 4
-  for (int k = 0; k < kPT; ++k) {
-    const int i = c * kChunk + k * kT + threadIdx.x;
-    if (i < n && score_key(s[i]) >= kstar) ++cnt;
-  }
-  cnt = wave_sum_int(cnt);
-  if (lane_id() == 0) red[threadIdx.x / kWave] = cnt;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int tot = 0;
-    for (int w = 0; w < kT / kWave; ++w) tot += red[w];
-    chunk_cnt[int64_t(row) * chunks + c] = tot;
+  if (LEVEL == 3) {
+    // this chunk's count above the bin, then suffix counts of the 256 sub-bins
+    static_assert(kBins3 == kT, "one sub-bin per thread");
+    int32_t* cc = chunk_cnt + (int64_t(row) * chunks + c) * (1 + kBins3);
+    const int t = threadIdx.x, ln = lane_id(), wv = t / kWave;
+    int x = int(cnt_s[t]);
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {   // inclusive suffix sum inside the wave
+      const int y = __shfl_down(x, o, kWave);
+      if (ln + o < kWave) x += y;
+    }
+    if (ln == 0) red2[wv] = x;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kTW; ++u)
+      if (u > wv) x += red2[u];
+    cc[1 + t] = x;
+    if (t == 0) cc[0] = int32_t(cnt_s[kBins3]);
   }
 }
 
 __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict__ scores, int n, int chunks,
-                                                        const uint32_t* __restrict__ state,
+                                                        const u64* __restrict__ hist, uint32_t* __restrict__ state,
                                                         const int32_t* __restrict__ chunk_cnt,
                                                         int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_count) {
-  __shared__ int red[kT / kWave];
-  __shared__ int wcnt[kT / kWave];
+  __shared__ u64 wtot[kTW];
+  __shared__ int red[kTW];
+  __shared__ int wcnt[kTW];
+  __shared__ Crossing cr;
   const int row = blockIdx.y, c = blockIdx.x;
   const int wave = threadIdx.x / kWave, lane = lane_id();
-  const uint32_t kstar = state[int64_t(row) * kToppStateWords + 6];
-  // offset of this chunk = sum of the counts of the chunks before it
+  uint32_t* st = state + int64_t(row) * kToppStateWords;
+  float v[kPT];
+  load_chunk(scores + int64_t(row) * n, n, c, v);
+  const u64 T = (u64(st[5]) << 32) | st[4];
+  find_crossing<kBins3 / kT>(hist + int64_t(row) * kHistPerRow + kBins1 + kBins2, T, 0.f, wtot, &cr);
+  const uint32_t kstar = (st[3] << 8) | cr.bin;
+  // offset of this chunk = selected keys of the chunks before it
+  const int32_t* cc = chunk_cnt + int64_t(row) * chunks * (1 + kBins3);
   int before = 0;
-  for (int k = threadIdx.x; k < c; k += kT) before += chunk_cnt[int64_t(row) * chunks + k];
+  for (int k = threadIdx.x; k < c; k += kT) before += cc[k * (1 + kBins3)] + cc[k * (1 + kBins3) + 1 + cr.bin];
   before = wave_sum_int(before);
   if (lane == 0) red[wave] = before;
   __syncthreads();
   int offset = 0;
 #pragma unroll
-  for (int w = 0; w < kT / kWave; ++w) offset += red[w];
+  for (int w = 0; w < kTW; ++w) offset += red[w];
 
-  const float* s = scores + int64_t(row) * n;
   int32_t* out = sel_idx + int64_t(row) * n;
   for (int k = 0; k < kPT; ++k) {
     const int i = c * kChunk + k * kT + threadIdx.x;
-    const bool f = i < n && score_key(s[i]) >= kstar;
+    const bool f = in_row(n, c, k) && score_key(v[k]) >= kstar;
     const uint64_t bal = __ballot(f);
     const int pre = __builtin_amdgcn_mbcnt_hi(uint32_t(bal >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal), 0u));
     __syncthreads();
@@ -267,7 +294,7 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
     __syncthreads();
     int woff = 0, tot = 0;
 #pragma unroll
-    for (int w = 0; w < kT / kWave; ++w) {
+    for (int w = 0; w < kTW; ++w) {
       woff += w < wave ? wcnt[w] : 0;
       tot += wcnt[w];
     }
@@ -301,10 +328,11 @@ rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, fl
   const dim3 grid(chunks, rows);
   topp_max_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, w.hist);
   topp_level1_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, scale_log2e, w.hist);
-  topp_level_kernel<2><<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, scale_log2e, p, w.hist, w.state);
-  topp_level_kernel<3><<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, scale_log2e, p, w.hist, w.state);
-  topp_count_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.hist, w.state, w.chunk_cnt);
-  topp_write_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.state, w.chunk_cnt, sel_idx, sel_count);
+  topp_level_kernel<2><<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, scale_log2e, p, w.hist, w.state,
+                                               w.chunk_cnt);
+  topp_level_kernel<3><<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, scale_log2e, p, w.hist, w.state,
+                                               w.chunk_cnt);
+  topp_write_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.hist, w.state, w.chunk_cnt, sel_idx, sel_count);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

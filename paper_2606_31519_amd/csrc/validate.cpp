@@ -77,7 +77,7 @@ ToppWorkspace topp_workspace(void* base, int64_t rows, int32_t n) {
   w.chunk_max = reinterpret_cast<float*>(b + off);
   off = align_up(off + size_t(rows) * chunks * sizeof(float), 256);
   w.chunk_cnt = reinterpret_cast<int32_t*>(b + off);
-  off = align_up(off + size_t(rows) * chunks * sizeof(int32_t), 256);
+  off = align_up(off + size_t(rows) * chunks * (1 + kBins3) * sizeof(int32_t), 256);
   w.state = reinterpret_cast<uint32_t*>(b + off);
   off = align_up(off + size_t(rows) * kToppStateWords * sizeof(uint32_t), 256);
   w.bytes = off;
@@ -133,6 +133,9 @@ rbq_status check_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
   if (n > 0 && (bad_ptr(K) || bad_ptr(V))) return RBQ_EINVAL;
   if (sparse && (bad_ptr(sel_count) || (n > 0 && bad_ptr(sel_idx)))) return RBQ_EINVAL;
   if (w > 0 && (bad_ptr(K_loc) || bad_ptr(V_loc) || loc_ld < w || loc_ld >= kMaxRows)) return RBQ_EINVAL;
+  // rows of one (sequence, KV head) are addressed with 32-bit byte offsets
+  const int64_t row_bytes = int64_t(head_dim) * (kv_dtype == RBQ_BF16 ? 2 : 4);
+  if (int64_t(n) * row_bytes >= (int64_t(1) << 31) || int64_t(w) * row_bytes >= (int64_t(1) << 31)) return RBQ_EINVAL;
   if (bad_ptr(ws) || ws_bytes < decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w)) return RBQ_EINVAL;
   return RBQ_OK;
 }
