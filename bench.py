@@ -30,6 +30,52 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sparse_decode_128k_traffic.txt")
+DECODE_SRC = os.path.join(ROOT, "paper_2606_31519_amd", "csrc", "decode.hip")
+
+
+def _sha256(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def _measured_traffic():
+    """HBM bytes per rbq_sparse_decode call from the committed rocprofv3 --pmc summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by the copy-kernel calibration), or None when the
+    decode source has changed since the counters were taken."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as f:
+            for ln in f:
+                if ":" in ln and not ln.startswith("#"):
+                    k, v = ln.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("decode_source_sha256") != _sha256(DECODE_SRC):
+            return None
+        return float(kv["hbm_bytes_per_call"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_probe(torch, steps):
+    """A plain elementwise copy of known size (1 GiB read + 1 GiB written, fp32): the
+    calibration run for the FETCH_SIZE / WRITE_SIZE counters."""
+    n = 1 << 28
+    src = torch.randn(n, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        torch.mul(src, 1.0, out=dst)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    print(json.dumps({"copy_probe": {"bytes_read": n * 4, "bytes_written": n * 4, "ms": ms,
+                                     "GBps": 2 * n * 4 / (ms * 1e-3) / 1e9}}), flush=True)
 
 
 def _git_sha():
@@ -175,6 +221,8 @@ def main():
     ap.add_argument("--no-scan", action="store_true", help="skip the standalone wide-head scan")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--sweep", action="store_true", help="also time p = 0.8 / 0.9 / 0.99")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this path is built and measured "
@@ -182,6 +230,10 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_probe:
+        copy_probe(torch, args.steps)
+        return
 
     from paper_2606_31519_amd import pipeline
     from workloads import gen
@@ -259,15 +311,17 @@ def main():
         st0.step(p)
         torch.cuda.synchronize()
 
-    # roofline of the dominant kernel(s) of the step
+    # roofline of the dominant call of the step: rbq_sparse_decode (split pass + combine),
+    # algorithmic bytes per call / its mean duration between HIP events on the launch stream
     kern = {}
     for s in stages:
         gbs = sbytes[s] / (stage_ms[s] * 1e-3) / 1e9
         kern[s] = {"ms": stage_ms[s], "bytes": float(sbytes[s]), "GBps": gbs, "frac_hbm": gbs / HBM_PEAK_GBS}
     dom = max(stages, key=lambda s: stage_ms[s])
+    traffic = _measured_traffic() if dom == "sparse_decode" else None
     roofline = {"bound": "hbm", "kernel": dom, "achieved": kern[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": kern[dom]["GBps"] / HBM_PEAK_GBS, "traffic": None,
-                "algorithmic_bytes_per_launch": float(sbytes[dom])}
+                "frac": kern[dom]["GBps"] / HBM_PEAK_GBS, "traffic": traffic,
+                "algorithmic_bytes_per_launch": float(sbytes[dom]), "ms_per_launch": stage_ms[dom]}
 
     scan = None
     if not args.no_scan:

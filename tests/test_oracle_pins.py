@@ -99,6 +99,32 @@ def test_packing_bit_order_and_roundtrip():
     assert np.array_equal((c > 0).astype(np.uint8), b)
 
 
+def _golden(name):
+    import os
+    kv = {}
+    with open(os.path.join(os.path.dirname(__file__), "golden", name)) as f:
+        for ln in f:
+            if ln.strip() and not ln.startswith("#"):
+                k, v = ln.split(":", 1)
+                kv[k.strip()] = float(v)
+    return kv
+
+
+def test_index_size_matches_appendix_c_case_study():
+    """Appendix C prints eta = (D/8 + B_alpha) / (2 D B_data) = 18/512 ~ 3.5 % at D = 128 (FP16):
+    the oracle's packed sign codes take exactly D/8 bytes per key."""
+    g = _golden("index_overhead_fp16.txt")
+    D = int(g["head_dim"])
+    rng = np.random.default_rng(3)
+    enc = orc.encode_keys(rng.standard_normal((5, D)), _haar(D, 3))
+    code_bytes = enc["codes"].astype(np.uint32).nbytes // 5
+    assert code_bytes == D // 8
+    index = code_bytes + g["bytes_per_alpha"]
+    kv = 2 * D * g["bytes_per_kv_element"]
+    assert index == g["index_bytes_per_key_per_head"] and kv == g["kv_bytes_per_key_per_head"]
+    assert round(100 * index / kv, 1) == g["eta_percent_printed"]
+
+
 # ---------------------------------------------------------------- correction factor
 def test_alpha_special_cases():
     D = 16
