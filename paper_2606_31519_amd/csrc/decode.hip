@@ -3,18 +3,28 @@
 //
 // Split-K over the key axis: block (split, b * Hkv + kv head) owns a chunk of
 // indexed positions (or of window rows) for all G query heads of the KV group.
-// For the sparse call it intersects each head's ascending selection list with
-// the chunk (two binary searches), marks the selected positions in per-head LDS
-// bitmaps and compacts their union: every K/V row selected by any head of the
-// group is gathered from HBM once and used by the heads that selected it
-// (a per-entry head mask keeps each head's softmax over its own set only).
-// Each wave takes tiles of 64 gathered rows:
-//   logits: lane = row, the 256-byte K row against the G queries (LDS broadcast)
-//   online softmax per head in the log2 domain (DPP / swizzle wave reductions)
-//   values: lane = 2 dimensions, V rows read coalesced, accumulated in fp32.
-// The kernel is occupancy-bound: keeping ~75 VGPRs (6 waves per SIMD) beats
-// issuing more loads per wave (measured on MI355X: a 16-load K prefetch or a
-// deeper V unroll doubles the registers and runs ~1.5x slower).
+// For the sparse call it finds each head's part of its ascending selection list
+// (a 64-way search per wave: three dependent loads for 128K entries), marks the
+// selected positions in per-head LDS bitmaps and compacts their union: every
+// K/V row selected by any head of the group is gathered from HBM once and used
+// by the heads that selected it (a per-entry head mask keeps each head's
+// softmax over its own set only).
+//
+// bf16 K/V (decode_mfma_kernel): each wave takes groups of 16 gathered rows and
+// runs both products on the matrix cores, straight from the loaded registers:
+//   logits  v_mfma_f32_16x16x32_bf16: A = 16 K rows (lane = row, 64 contiguous
+//           bytes per lane), B = the queries as hi + mid + lo bf16 parts (the
+//           three parts carry all 24 bits of the fp32 query; products of bf16
+//           values are exact in fp32), C lane (head h, quarter j) = rows 4j..4j+3
+//   softmax online per head in the log2 domain; C's layout is already the A
+//           layout of the next product, so the probabilities stay in registers
+//           (split into hi + lo bf16 parts)
+//   values  v_mfma_f32_16x16x16bf16_1k: B = V (each lane loads 16 contiguous
+//           bytes of 4 rows and pairs rows with v_perm), 8 column blocks of 16
+//           dimensions, accumulated in fp32.
+// The next group's loads are issued before the current group is computed.
+// fp32 K/V (decode_vec_kernel, small workloads): the same split with vector
+// ALU dots (lane = row for the logits, lane = 2 dimensions for the values).
 // Waves merge in LDS; the block writes (m, l, acc[D]) per head; a combine
 // kernel merges the splits in fixed order (bitwise deterministic).
 #include <cmath>
@@ -32,14 +42,81 @@ constexpr float kLn2 = 0.69314718055994531f;
 __device__ __forceinline__ float wmax64(float v) { v = max32(v); return fmaxf(v, __shfl_xor(v, 32, kWave)); }
 __device__ __forceinline__ float wsum64(float v) { v = sum32(v); return v + __shfl_xor(v, 32, kWave); }
 
-__device__ __forceinline__ int lower_bound_i32(const int32_t* a, int cnt, int x) {
-  int lo = 0, hi = cnt;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (a[mid] < x) lo = mid + 1;
-    else hi = mid;
+// First index of the ascending a[0, cnt) whose value is >= x, found by one
+// wave: each round probes 64 evenly spaced entries and keeps the gap where the
+// answer lies (cnt = 2^17 takes three rounds). Every lane returns the answer.
+__device__ __forceinline__ int wave_lower_bound(const int32_t* __restrict__ a, int cnt, int x) {
+  const int lane = lane_id();
+  int lo = 0, hi = cnt;                     // the answer lies in [lo, hi]
+  while (hi > lo) {
+    const int step = (hi - lo + kWave - 1) / kWave;
+    const int pos = lo + lane * step;
+    const bool lt = pos < hi && a[pos] < x;
+    const int k = __popcll(__ballot(lt));   // the first k probes are below x
+    if (k == 0) break;                      // a[lo] >= x
+    lo += (k - 1) * step + 1;
+    hi = min(hi, lo - 1 + step);
   }
   return lo;
+}
+
+// Per-block row list of a sparse split: the union over the G heads of the
+// group of the positions in [c0, c1) that each head selected, in ascending
+// order, with a bit mask of the heads that selected each entry. Returns the
+// number of entries (block-uniform). All threads of the block must call it.
+template <int G, int kThreads>
+__device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count, int row0,
+                                int n, int c0, int c1, uint32_t (*bm)[kBmWords], int32_t* lst, uint16_t* hmask,
+                                int* rng_lo, int* rng_hi, int* wcnt, int* ucount) {
+  constexpr int kWaves = kThreads / kWave;
+  const int wave = threadIdx.x / kWave;
+  for (int g = wave; g < G; g += kWaves) {
+    const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
+    const int cnt = min(max(sel_count[row0 + g], 0), n);
+    const int lo = wave_lower_bound(sel, cnt, c0);
+    const int hi = wave_lower_bound(sel, cnt, c1);
+    if (lane_id() == 0) {
+      rng_lo[g] = lo;
+      rng_hi[g] = hi;
+    }
+  }
+  for (int e = threadIdx.x; e < G * kBmWords; e += kThreads) bm[e / kBmWords][e % kBmWords] = 0u;
+  __syncthreads();
+  for (int g = 0; g < G; ++g) {
+    const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
+    for (int e = rng_lo[g] + threadIdx.x; e < rng_hi[g]; e += kThreads) {
+      const int pos = sel[e] - c0;
+      if (pos >= 0 && pos < c1 - c0) atomicOr(&bm[g][pos >> 5], 1u << (pos & 31));
+    }
+  }
+  __syncthreads();
+  // union of the G bitmaps, compacted in ascending position order
+  const int nw = (c1 - c0 + 31) / 32;
+  uint32_t uw = 0u;
+  if (threadIdx.x < kBmWords && int(threadIdx.x) < nw) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) uw |= bm[g][threadIdx.x];
+  }
+  if (threadIdx.x < kBmWords) wcnt[threadIdx.x] = __popc(uw);
+  __syncthreads();
+  if (threadIdx.x < kBmWords) {
+    int off = 0;
+    for (int k = 0; k < int(threadIdx.x); ++k) off += wcnt[k];
+    if (threadIdx.x == kBmWords - 1) *ucount = off + wcnt[threadIdx.x];
+    uint32_t bits = uw;
+    while (bits) {
+      const int bit = __ffs(bits) - 1;
+      bits &= bits - 1u;
+      uint16_t mk = 0;
+#pragma unroll
+      for (int g = 0; g < G; ++g) mk |= uint16_t(((bm[g][threadIdx.x] >> bit) & 1u) << g);
+      lst[off] = c0 + 32 * threadIdx.x + bit;
+      hmask[off] = mk;
+      ++off;
+    }
+  }
+  __syncthreads();
+  return *ucount;
 }
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -96,14 +173,14 @@ __device__ __forceinline__ f32x2 load_v2(const void* rowp, int lane) {
 }
 
 template <int DT, bool SPARSE, int G>
-__global__ __launch_bounds__(kDThreads) void decode_partial_kernel(
+__global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     const float* __restrict__ q, const void* __restrict__ K, const void* __restrict__ V, int cap, int n,
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count, const void* __restrict__ K_loc,
     const void* __restrict__ V_loc, int64_t loc_ld, int w, int chunk, int idx_splits, int total_splits,
     float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
   constexpr int kElem = DT == RBQ_BF16 ? 2 : 4;
   __shared__ float qs[G][kHeadDim];
-  __shared__ uint32_t bm[SPARSE ? G : 1][kBmWords];
+  __shared__ uint32_t bm[G][kBmWords];
   __shared__ int32_t lst[SPARSE ? kDecodeChunk : 1];
   __shared__ uint16_t hmask[SPARSE ? kDecodeChunk : 1];
   __shared__ int rng_lo[G], rng_hi[G];
@@ -139,50 +216,8 @@ __global__ __launch_bounds__(kDThreads) void decode_partial_kernel(
   const bool use_list = SPARSE && !window;
   int U;
   if (use_list) {
-    if (threadIdx.x < G) {
-      const int g = threadIdx.x;
-      const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
-      const int cnt = min(max(sel_count[row0 + g], 0), n);
-      rng_lo[g] = lower_bound_i32(sel, cnt, c0);
-      rng_hi[g] = lower_bound_i32(sel, cnt, c1);
-    }
-    for (int e = threadIdx.x; e < G * kBmWords; e += kDThreads) bm[e / kBmWords][e % kBmWords] = 0u;
-    __syncthreads();
-    for (int g = 0; g < G; ++g) {
-      const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
-      for (int e = rng_lo[g] + threadIdx.x; e < rng_hi[g]; e += kDThreads) {
-        const int pos = sel[e] - c0;
-        if (pos >= 0 && pos < c1 - c0) atomicOr(&bm[g][pos >> 5], 1u << (pos & 31));
-      }
-    }
-    __syncthreads();
-    // union of the G bitmaps, compacted in ascending position order
-    const int nw = (c1 - c0 + 31) / 32;
-    uint32_t uw = 0u;
-    if (threadIdx.x < kBmWords && threadIdx.x < nw) {
-#pragma unroll
-      for (int g = 0; g < G; ++g) uw |= bm[g][threadIdx.x];
-    }
-    if (threadIdx.x < kBmWords) wcnt[threadIdx.x] = __popc(uw);
-    __syncthreads();
-    if (threadIdx.x < kBmWords) {
-      int off = 0;
-      for (int k = 0; k < int(threadIdx.x); ++k) off += wcnt[k];
-      if (threadIdx.x == kBmWords - 1) ucount = off + wcnt[threadIdx.x];
-      uint32_t bits = uw;
-      while (bits) {
-        const int bit = __ffs(bits) - 1;
-        bits &= bits - 1u;
-        uint16_t mk = 0;
-#pragma unroll
-        for (int g = 0; g < G; ++g) mk |= uint16_t(((bm[g][threadIdx.x] >> bit) & 1u) << g);
-        lst[off] = c0 + 32 * threadIdx.x + bit;
-        hmask[off] = mk;
-        ++off;
-      }
-    }
-    __syncthreads();
-    U = ucount;
+    U = build_union_list<G, kDThreads>(sel_idx, sel_count, row0, n, c0, c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
+                                       &ucount);
   } else {
     __syncthreads();
     U = max(c1 - c0, 0);
@@ -283,6 +318,305 @@ __global__ __launch_bounds__(kDThreads) void decode_partial_kernel(
   }
 }
 
+// ---------------------------------------------------------------- bf16 K/V on the matrix cores
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kGroupRows = 16;   // rows per MFMA group
+constexpr int kQParts = 3;       // the query as hi + mid + lo bf16 parts
+
+// round-to-nearest-even bf16 bit pattern of a finite float, and its value
+__device__ __forceinline__ uint32_t bf16_bits(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ float bf16_val(uint32_t b) { return __uint_as_float(b << 16); }
+
+// The loads of one group of 16 rows, as one lane sees them (lane = 16 * j + x):
+//   k[kb]: K row x of the group, dimensions 32j + 8kb .. +8 (A operand of kb)
+//   v[i] : V row 4j + i of the group, dimensions 8x .. 8x + 8
+//   mk   : bit i set when row 4j + i is valid and selected by head x
+struct GroupLoads {
+  u32x4 k[4];
+  u32x4 v[4];
+  uint32_t mk;
+};
+
+// Loads go through buffer resources over the (sequence, KV head)'s rows: a
+// load that has nothing to fetch (no next group) gets an offset past the end
+// and is dropped by the hardware, so every path issues the same instructions
+// and the compiler's wait counts stay exact.
+constexpr int kSkipOffset = 0x7FFFFF00;
+
+template <bool SPARSE>
+__device__ __forceinline__ int row_at(int e, bool list, int c0, const int32_t* lst) {
+  if constexpr (SPARSE) {
+    const int lv = lst[e];
+    return list ? lv : c0 + e;
+  }
+  return c0 + e;
+}
+
+template <bool SPARSE>
+__device__ __forceinline__ void load_group_k(GroupLoads& d, int grp, bool skip, int U, int c0, bool list,
+                                             const int32_t* lst, __amdgpu_buffer_rsrc_t Kr, int x, int j) {
+  const int e0 = grp * kGroupRows;
+  const int ek = e0 + x < U ? e0 + x : e0;
+  const int pk = row_at<SPARSE>(ek, list, c0, lst);
+  const int off = skip ? kSkipOffset : pk * (kHeadDim * 2) + 64 * j;
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 16 * kb, 0, 0);
+}
+
+template <bool SPARSE, int G>
+__device__ __forceinline__ void load_group_v(GroupLoads& d, int grp, bool skip, int U, int c0, bool list,
+                                             const int32_t* lst, const uint16_t* hmask,
+                                             __amdgpu_buffer_rsrc_t Vr, int x, int j) {
+  const int e0 = grp * kGroupRows;
+  uint32_t mk = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = e0 + 4 * j + i;
+    const bool valid = e < U;
+    const int ev = valid ? e : e0;
+    const int pv = row_at<SPARSE>(ev, list, c0, lst);
+    const int off = skip ? kSkipOffset : pv * (kHeadDim * 2) + 16 * x;
+    d.v[i] = __builtin_amdgcn_raw_buffer_load_b128(Vr, off, 0, 0);
+    bool on = valid && x < G;
+    if constexpr (SPARSE) on = on & (!list | bool((hmask[ev] >> x) & 1u));
+    mk |= uint32_t(on) << i;
+  }
+  d.mk = mk;
+}
+
+template <bool SPARSE, int G>
+__global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
+    const float* __restrict__ q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V, int cap, int n,
+    const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count, const uint16_t* __restrict__ K_loc,
+    const uint16_t* __restrict__ V_loc, int64_t loc_ld, int w, int chunk, int idx_splits, int total_splits,
+    float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
+  static_assert(G >= 1 && G <= 16, "the MFMA tiles hold at most 16 heads");
+  constexpr bool kPackedQ = kQParts * G <= 16;
+  constexpr int kQOps = kPackedQ ? 1 : kQParts;
+  __shared__ u32x4 qB[4][kQOps][kWave];           // B operands of the logits product
+  __shared__ uint32_t bm[G][kBmWords];
+  __shared__ int32_t lst[SPARSE ? kDecodeChunk : 1];
+  __shared__ uint16_t hmask[SPARSE ? kDecodeChunk : 1];
+  __shared__ int rng_lo[G], rng_hi[G];
+  __shared__ int wcnt[kBmWords];
+  __shared__ int ucount;
+  __shared__ float sm[kDWaves][G], sl[kDWaves][G];
+  __shared__ float sacc[kDWaves][G][kHeadDim];
+
+  const int split = blockIdx.x;
+  const int bh = blockIdx.y;
+  const int b = bh / Hkv, hk = bh - b * Hkv;
+  const int row0 = b * Hq + hk * G;
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int x = lane & 15, j = lane >> 4;
+  const bool window = split >= idx_splits;
+  int c0, c1;
+  if (!window) {
+    c0 = split * chunk;
+    c1 = min(n, c0 + chunk);
+  } else {
+    c0 = (split - idx_splits) * kDecodeWinChunk;
+    c1 = min(w, c0 + kDecodeWinChunk);
+  }
+  const uint16_t* Kb = window ? K_loc + int64_t(bh) * loc_ld * kHeadDim : K + int64_t(bh) * cap * kHeadDim;
+  const uint16_t* Vb = window ? V_loc + int64_t(bh) * loc_ld * kHeadDim : V + int64_t(bh) * cap * kHeadDim;
+  const uint32_t region = uint32_t(window ? w : n) * uint32_t(kHeadDim * 2);   // < 2^31, checked on the host
+  const __amdgpu_buffer_rsrc_t Kr = make_rsrc(Kb, region);
+  const __amdgpu_buffer_rsrc_t Vr = make_rsrc(Vb, region);
+
+  // query operands, lane (column c, quarter jj) of k-block kb = dims 32 jj + 8 kb .. +8.
+  // G <= 4: one operand per k-block, column c = part * G + head; otherwise one
+  // operand per (k-block, part), column c = head.
+  for (int e = threadIdx.x; e < 4 * kQOps * kWave; e += kDThreads) {
+    const int kb = e / (kQOps * kWave), op = (e / kWave) % kQOps, ln = e % kWave;
+    const int c = ln & 15, jj = ln >> 4;
+    const int h = kPackedQ ? c % G : c;
+    const int prt = kPackedQ ? c / G : op;
+    uint32_t wds[4] = {0u, 0u, 0u, 0u};
+    if (h < G && prt < kQParts) {
+      const float* qp = q + int64_t(row0 + h) * kHeadDim + 32 * jj + 8 * kb;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        float r = qp[i] * scale_log2e;
+        uint32_t bits = 0u;
+        for (int t = 0; t <= prt; ++t) {
+          bits = bf16_bits(r);
+          r -= bf16_val(bits);
+        }
+        wds[i >> 1] |= bits << (16 * (i & 1));
+      }
+    }
+    qB[kb][op][ln] = u32x4{wds[0], wds[1], wds[2], wds[3]};
+  }
+
+  int U;
+  if (SPARSE && !window) {
+    U = build_union_list<G, kDThreads>(sel_idx, sel_count, row0, n, c0, c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
+                                       &ucount);
+  } else {
+    __syncthreads();
+    U = max(c1 - c0, 0);
+  }
+  const bool list = SPARSE && !window;
+
+  float m = -INFINITY, lsum = 0.f;      // head x's running max (uniform over j) and this lane's partial sum
+  f32x4 acc[4][2];                      // lane (x, j), reg i: head 4j + i, dimension 8x + 2t + par
+#pragma unroll
+  for (int t = 0; t < 4; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int ngroups = (U + kGroupRows - 1) / kGroupRows;
+  // One group's registers are reused for the next: its K rows are requested
+  // as soon as the logits are done, its V rows as soon as the values are.
+  GroupLoads cur;
+  int grp = wave;
+  if (grp < ngroups) {
+    load_group_k<SPARSE>(cur, grp, false, U, c0, list, lst, Kr, x, j);
+    load_group_v<SPARSE, G>(cur, grp, false, U, c0, list, lst, hmask, Vr, x, j);
+  }
+  while (grp < ngroups) {
+    const int nxt = grp + kDWaves;
+    const bool last = nxt >= ngroups;
+    // logits of 16 rows x 16 columns; the query operands are re-read from LDS
+    // every group (an opaque pointer keeps the compiler from holding them all
+    // in registers, which would cost waves per SIMD)
+    int qoff = lane;
+    asm volatile("" : "+v"(qoff));
+    const u32x4* qp = &qB[0][0][0] + qoff;
+    f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const bf16x8 a = __builtin_bit_cast(bf16x8, cur.k[kb]);
+#pragma unroll
+      for (int op = 0; op < kQOps; ++op)
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, qp[(kb * kQOps + op) * kWave]), s,
+                                                    0, 0, 0);
+    }
+    load_group_k<SPARSE>(cur, last ? grp : nxt, last, U, c0, list, lst, Kr, x, j);
+    if constexpr (kPackedQ) {
+      // column h + G and h + 2G hold the mid and lo parts of head h's logits
+      // (each element goes through an opaque copy first: hipcc 7.2 miscompiles
+      // update_dpp applied directly to the elements of an MFMA result vector,
+      // reading one element's register for all four)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float sv = s[i];
+        asm volatile("" : "+v"(sv));
+        const int v = __builtin_bit_cast(int, sv);
+        const float mid = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, v, 0x100 + G, 0xF, 0xF, false));
+        const float lo = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, v, 0x100 + 2 * G, 0xF, 0xF, false));
+        s[i] = (sv + mid) + lo;
+      }
+    }
+    // online softmax of head x over rows 4j .. 4j + 3 (log2 domain)
+    float lg[4];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      lg[i] = ((cur.mk >> i) & 1u) ? s[i] : -INFINITY;
+      tmax = fmaxf(tmax, lg[i]);
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
+    const float mn = fmaxf(m, tmax);
+    float corr = 1.f, pr[4];
+    if (mn == -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pr[i] = 0.f;
+    } else {
+      corr = __builtin_amdgcn_exp2f(m - mn);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pr[i] = lg[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(lg[i] - mn);
+    }
+    m = mn;
+    lsum = fmaf(lsum, corr, (pr[0] + pr[1]) + (pr[2] + pr[3]));
+    if (__ballot(corr != 1.f)) {
+      float cr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cr[i] = __shfl(corr, 4 * j + i, kWave);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          acc[t][0][i] *= cr[i];
+          acc[t][1][i] *= cr[i];
+        }
+      }
+    }
+    // probabilities as hi + lo bf16 parts: A operand (row = head x, k = rows 4j .. 4j + 3)
+    uint32_t ph[4], pl[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ph[i] = bf16_bits(pr[i]);
+      pl[i] = bf16_bits(pr[i] - bf16_val(ph[i]));
+    }
+    const s16x4 a_hi = __builtin_bit_cast(s16x4, u32x2{ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16)});
+    const s16x4 a_lo = __builtin_bit_cast(s16x4, u32x2{pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16)});
+    // values: column x of block (t, par) is dimension 8x + 2t + par; k = rows 4j .. 4j + 3
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int par = 0; par < 2; ++par) {
+        const uint32_t sel = par ? 0x07060302u : 0x05040100u;
+        const uint32_t b0 = __builtin_amdgcn_perm(cur.v[1][t], cur.v[0][t], sel);
+        const uint32_t b1 = __builtin_amdgcn_perm(cur.v[3][t], cur.v[2][t], sel);
+        const s16x4 bv = __builtin_bit_cast(s16x4, u32x2{b0, b1});
+        acc[t][par] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a_hi, bv, acc[t][par], 0, 0, 0);
+        acc[t][par] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a_lo, bv, acc[t][par], 0, 0, 0);
+      }
+    }
+    load_group_v<SPARSE, G>(cur, last ? grp : nxt, last, U, c0, list, lst, hmask, Vr, x, j);
+    grp = nxt;
+  }
+
+  // ---- merge the waves, write this split's partial state per head
+  lsum += __shfl_xor(lsum, 16, kWave);
+  lsum += __shfl_xor(lsum, 32, kWave);
+  if (j == 0 && x < G) {
+    sm[wave][x] = m;
+    sl[wave][x] = lsum;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int h = 4 * j + i;
+    if (h < G) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        sacc[wave][h][8 * x + 2 * t] = acc[t][0][i];
+        sacc[wave][h][8 * x + 2 * t + 1] = acc[t][1][i];
+      }
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < G * (kHeadDim + 2); e += kDThreads) {
+    const int g = e / (kHeadDim + 2);
+    const int k = e - g * (kHeadDim + 2);
+    float M = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < kDWaves; ++v) M = fmaxf(M, sm[v][g]);
+    float r;
+    if (k == 0) {
+      r = M;
+    } else {
+      r = 0.f;
+      if (M != -INFINITY) {
+#pragma unroll
+        for (int v = 0; v < kDWaves; ++v) {
+          if (sm[v][g] != -INFINITY) {
+            const float sc = __builtin_amdgcn_exp2f(sm[v][g] - M);
+            r = fmaf(k == 1 ? sl[v][g] : sacc[v][g][k - 2], sc, r);
+          }
+        }
+      }
+    }
+    part[(int64_t(row0 + g) * total_splits + split) * (kHeadDim + 2) + k] = r;
+  }
+}
+
 // Merge the splits of one query head: 8 groups of 128 threads, each group
 // folds a fixed residue class of splits, then the groups are added in order.
 constexpr int kCombGroups = 8;
@@ -340,11 +674,17 @@ rbq_status launch_g(int G, dim3 grid, hipStream_t stream, const float* q, const 
                     int n, const int32_t* sel_idx, const int32_t* sel_count, const void* K_loc, const void* V_loc,
                     int64_t loc_ld, int w, int chunk, int idx_splits, int total, float scale_log2e, float* part,
                     int Hq, int Hkv) {
-#define RBQ_DECODE_CASE(GG)                                                                                  \
-  case GG:                                                                                                   \
-    decode_partial_kernel<DT, SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                   \
-        q, K, V, cap, n, sel_idx, sel_count, K_loc, V_loc, loc_ld, w, chunk, idx_splits, total, scale_log2e, \
-        part, Hq, Hkv);                                                                                      \
+#define RBQ_DECODE_CASE(GG)                                                                                    \
+  case GG:                                                                                                     \
+    if (DT == RBQ_BF16)                                                                                        \
+      decode_mfma_kernel<SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                          \
+          q, static_cast<const uint16_t*>(K), static_cast<const uint16_t*>(V), cap, n, sel_idx, sel_count,     \
+          static_cast<const uint16_t*>(K_loc), static_cast<const uint16_t*>(V_loc), loc_ld, w, chunk,          \
+          idx_splits, total, scale_log2e, part, Hq, Hkv);                                                      \
+    else                                                                                                       \
+      decode_vec_kernel<DT, SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                       \
+          q, K, V, cap, n, sel_idx, sel_count, K_loc, V_loc, loc_ld, w, chunk, idx_splits, total, scale_log2e, \
+          part, Hq, Hkv);                                                                                      \
     break;
   switch (G) {
     RBQ_DECODE_CASE(1)

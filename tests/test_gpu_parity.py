@@ -229,7 +229,9 @@ def _rand_sel(rng, n, frac, Hq):
 
 @pytest.mark.parametrize("kv_dtype,G,n,w,frac", [("bf16", 4, 5000, 17, 0.05), ("f32", 1, 3000, 0, 0.3),
                                                  ("bf16", 8, 2049, 256, 0.5), ("bf16", 4, 0, 100, 0.0),
-                                                 ("bf16", 2, 700, 0, 0.0), ("bf16", 4, 131, 5, 1.0)])
+                                                 ("bf16", 2, 700, 0, 0.0), ("bf16", 4, 131, 5, 1.0),
+                                                 ("bf16", 16, 1500, 40, 0.2), ("bf16", 1, 2500, 3, 0.1),
+                                                 ("bf16", 4, 4100, 300, 0.02)])
 def test_sparse_decode_parity(R, pipeline, kv_dtype, G, n, w, frac):
     B, Hkv = 2, 2
     Hq = G * Hkv
