@@ -12,8 +12,9 @@
 //
 // bf16 K/V (decode_mfma_kernel): each wave takes groups of 16 gathered rows and
 // runs both products on the matrix cores, straight from the loaded registers:
-//   logits  v_mfma_f32_16x16x32_bf16: A = 16 K rows (lane = row, 64 contiguous
-//           bytes per lane), B = the queries as hi + mid + lo bf16 parts (the
+//   logits  v_mfma_f32_16x16x32_bf16: A = 16 K rows (lane = row; per load the
+//           4 lanes of a row read 64 contiguous bytes), B = the queries as
+//           hi + mid + lo bf16 parts (the
 //           three parts carry all 24 bits of the fp32 query; products of bf16
 //           values are exact in fp32), C lane (head h, quarter j) = rows 4j..4j+3
 //   softmax online per head in the log2 domain; C's layout is already the A
@@ -42,79 +43,131 @@ constexpr float kLn2 = 0.69314718055994531f;
 __device__ __forceinline__ float wmax64(float v) { v = max32(v); return fmaxf(v, __shfl_xor(v, 32, kWave)); }
 __device__ __forceinline__ float wsum64(float v) { v = sum32(v); return v + __shfl_xor(v, 32, kWave); }
 
-// First index of the ascending a[0, cnt) whose value is >= x, found by one
-// wave: each round probes 64 evenly spaced entries and keeps the gap where the
-// answer lies (cnt = 2^17 takes three rounds). Every lane returns the answer.
-__device__ __forceinline__ int wave_lower_bound(const int32_t* __restrict__ a, int cnt, int x) {
+// Lower bounds of x0 and x1 in the ascending a[0, cnt) (first index whose
+// value is >= x), found together by one wave: each round probes 64 evenly
+// spaced entries per search and keeps the gap where the answer lies, so a list
+// of 2^17 entries takes three rounds of loads for both. Every lane returns both.
+__device__ __forceinline__ void wave_lower_bounds(const int32_t* __restrict__ a, int cnt, int x0, int x1, int& r0,
+                                                  int& r1) {
   const int lane = lane_id();
-  int lo = 0, hi = cnt;                     // the answer lies in [lo, hi]
-  while (hi > lo) {
-    const int step = (hi - lo + kWave - 1) / kWave;
-    const int pos = lo + lane * step;
-    const bool lt = pos < hi && a[pos] < x;
-    const int k = __popcll(__ballot(lt));   // the first k probes are below x
-    if (k == 0) break;                      // a[lo] >= x
-    lo += (k - 1) * step + 1;
-    hi = min(hi, lo - 1 + step);
+  int lo0 = 0, hi0 = cnt, lo1 = 0, hi1 = cnt;   // each answer lies in [lo, hi]
+  while (hi0 > lo0 || hi1 > lo1) {
+    const int st0 = (hi0 - lo0 + kWave - 1) / kWave, st1 = (hi1 - lo1 + kWave - 1) / kWave;
+    const int p0 = lo0 + lane * st0, p1 = lo1 + lane * st1;
+    const bool lt0 = p0 < hi0 && a[p0] < x0;
+    const bool lt1 = p1 < hi1 && a[p1] < x1;
+    const int k0 = __popcll(__ballot(lt0)), k1 = __popcll(__ballot(lt1));   // the first k probes are below x
+    if (hi0 > lo0) {
+      if (k0 == 0) {
+        hi0 = lo0;
+      } else {
+        lo0 += (k0 - 1) * st0 + 1;
+        hi0 = min(hi0, lo0 - 1 + st0);
+      }
+    }
+    if (hi1 > lo1) {
+      if (k1 == 0) {
+        hi1 = lo1;
+      } else {
+        lo1 += (k1 - 1) * st1 + 1;
+        hi1 = min(hi1, lo1 - 1 + st1);
+      }
+    }
   }
-  return lo;
+  r0 = lo0;
+  r1 = lo1;
 }
 
 // Per-block row list of a sparse split: the union over the G heads of the
 // group of the positions in [c0, c1) that each head selected, in ascending
 // order, with a bit mask of the heads that selected each entry. Returns the
 // number of entries (block-uniform). All threads of the block must call it.
+// Each wave finds the part [lower bound of c0, lower bound of c1) of its
+// heads' selection lists; the entries are then loaded all at once and marked
+// in per-head LDS bitmaps, and the union is compacted with wave ballots.
 template <int G, int kThreads>
 __device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count, int row0,
                                 int n, int c0, int c1, uint32_t (*bm)[kBmWords], int32_t* lst, uint16_t* hmask,
                                 int* rng_lo, int* rng_hi, int* wcnt, int* ucount) {
   constexpr int kWaves = kThreads / kWave;
-  const int wave = threadIdx.x / kWave;
+  const int t = threadIdx.x, wave = t / kWave, lane = lane_id();
   for (int g = wave; g < G; g += kWaves) {
     const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
     const int cnt = min(max(sel_count[row0 + g], 0), n);
-    const int lo = wave_lower_bound(sel, cnt, c0);
-    const int hi = wave_lower_bound(sel, cnt, c1);
-    if (lane_id() == 0) {
+    int lo, hi;
+    wave_lower_bounds(sel, cnt, c0, c1, lo, hi);
+    if (lane == 0) {
       rng_lo[g] = lo;
       rng_hi[g] = hi;
     }
   }
-  for (int e = threadIdx.x; e < G * kBmWords; e += kThreads) bm[e / kBmWords][e % kBmWords] = 0u;
+  for (int e = t; e < G * kBmWords; e += kThreads) bm[e / kBmWords][e % kBmWords] = 0u;
   __syncthreads();
-  for (int g = 0; g < G; ++g) {
-    const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
-    for (int e = rng_lo[g] + threadIdx.x; e < rng_hi[g]; e += kThreads) {
-      const int pos = sel[e] - c0;
-      if (pos >= 0 && pos < c1 - c0) atomicOr(&bm[g][pos >> 5], 1u << (pos & 31));
-    }
-  }
-  __syncthreads();
-  // union of the G bitmaps, compacted in ascending position order
-  const int nw = (c1 - c0 + 31) / 32;
-  uint32_t uw = 0u;
-  if (threadIdx.x < kBmWords && int(threadIdx.x) < nw) {
+  // mark the selected positions: every entry's load first, then the LDS bit sets
+  constexpr int kPer = kDecodeChunk / kThreads;            // entries per thread per head (a split has <= chunk)
+  constexpr int kHB = G < 4 ? G : 4;                      // heads per batch of loads
 #pragma unroll
-    for (int g = 0; g < G; ++g) uw |= bm[g][threadIdx.x];
+  for (int g0 = 0; g0 < G; g0 += kHB) {
+    int pv[kHB][kPer];
+#pragma unroll
+    for (int gg = 0; gg < kHB; ++gg) {
+      const int g = g0 + gg;
+      const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
+      const int lo = rng_lo[g], hi = rng_hi[g];
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int e = lo + u * kThreads + t;
+        pv[gg][u] = e < hi ? sel[e] - c0 : -1;
+      }
+    }
+#pragma unroll
+    for (int gg = 0; gg < kHB; ++gg)
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int pos = pv[gg][u];
+        if (pos >= 0 && pos < c1 - c0) atomicOr(&bm[g0 + gg][pos >> 5], 1u << (pos & 31));
+      }
   }
-  if (threadIdx.x < kBmWords) wcnt[threadIdx.x] = __popc(uw);
   __syncthreads();
-  if (threadIdx.x < kBmWords) {
-    int off = 0;
-    for (int k = 0; k < int(threadIdx.x); ++k) off += wcnt[k];
-    if (threadIdx.x == kBmWords - 1) *ucount = off + wcnt[threadIdx.x];
-    uint32_t bits = uw;
-    while (bits) {
-      const int bit = __ffs(bits) - 1;
-      bits &= bits - 1u;
+  // union of the G bitmaps, compacted in ascending position order: position
+  // r * kThreads + t in round r, ranked by wave ballots
+  constexpr int kRounds = kDecodeChunk / kThreads;
+  bool f[kRounds];
+  uint64_t bal[kRounds];
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    const int pos = r * kThreads + t;
+    uint32_t any = 0u;
+#pragma unroll
+    for (int g = 0; g < G; ++g) any |= bm[g][pos >> 5];
+    f[r] = pos < c1 - c0 && ((any >> (pos & 31)) & 1u);
+    bal[r] = __ballot(f[r]);
+    if (lane == 0) wcnt[r * kWaves + wave] = __popcll(bal[r]);
+  }
+  __syncthreads();
+  int base = 0;
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    int woff = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const int cw = wcnt[r * kWaves + w];
+      woff += w < wave ? cw : 0;
+      tot += cw;
+    }
+    if (f[r]) {
+      const int pos = r * kThreads + t;
+      const int o = base + woff + __builtin_amdgcn_mbcnt_hi(uint32_t(bal[r] >> 32),
+                                                            __builtin_amdgcn_mbcnt_lo(uint32_t(bal[r]), 0u));
       uint16_t mk = 0;
 #pragma unroll
-      for (int g = 0; g < G; ++g) mk |= uint16_t(((bm[g][threadIdx.x] >> bit) & 1u) << g);
-      lst[off] = c0 + 32 * threadIdx.x + bit;
-      hmask[off] = mk;
-      ++off;
+      for (int g = 0; g < G; ++g) mk |= uint16_t(((bm[g][pos >> 5] >> (pos & 31)) & 1u) << g);
+      lst[o] = c0 + pos;
+      hmask[o] = mk;
     }
+    base += tot;
   }
+  if (t == 0) *ucount = base;
   __syncthreads();
   return *ucount;
 }
@@ -333,7 +386,8 @@ __device__ __forceinline__ uint32_t bf16_bits(float x) {
 __device__ __forceinline__ float bf16_val(uint32_t b) { return __uint_as_float(b << 16); }
 
 // The loads of one group of 16 rows, as one lane sees them (lane = 16 * j + x):
-//   k[kb]: K row x of the group, dimensions 32j + 8kb .. +8 (A operand of kb)
+//   k[kb]: K row x of the group, dimensions 32kb + 8j .. +8 (A operand of kb);
+//          the four lanes of a row read 64 contiguous bytes per instruction
 //   v[i] : V row 4j + i of the group, dimensions 8x .. 8x + 8
 //   mk   : bit i set when row 4j + i is valid and selected by head x
 struct GroupLoads {
@@ -363,9 +417,9 @@ __device__ __forceinline__ void load_group_k(GroupLoads& d, int grp, bool skip, 
   const int e0 = grp * kGroupRows;
   const int ek = e0 + x < U ? e0 + x : e0;
   const int pk = row_at<SPARSE>(ek, list, c0, lst);
-  const int off = skip ? kSkipOffset : pk * (kHeadDim * 2) + 64 * j;
+  const int off = skip ? kSkipOffset : pk * (kHeadDim * 2) + 16 * j;
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 16 * kb, 0, 0);
+  for (int kb = 0; kb < 4; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 64 * kb, 0, 0);
 }
 
 template <bool SPARSE, int G>
@@ -429,7 +483,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   const __amdgpu_buffer_rsrc_t Kr = make_rsrc(Kb, region);
   const __amdgpu_buffer_rsrc_t Vr = make_rsrc(Vb, region);
 
-  // query operands, lane (column c, quarter jj) of k-block kb = dims 32 jj + 8 kb .. +8.
+  // query operands, lane (column c, quarter jj) of k-block kb = dims 32 kb + 8 jj .. +8.
   // G <= 4: one operand per k-block, column c = part * G + head; otherwise one
   // operand per (k-block, part), column c = head.
   for (int e = threadIdx.x; e < 4 * kQOps * kWave; e += kDThreads) {
@@ -439,7 +493,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     const int prt = kPackedQ ? c / G : op;
     uint32_t wds[4] = {0u, 0u, 0u, 0u};
     if (h < G && prt < kQParts) {
-      const float* qp = q + int64_t(row0 + h) * kHeadDim + 32 * jj + 8 * kb;
+      const float* qp = q + int64_t(row0 + h) * kHeadDim + 32 * kb + 8 * jj;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         float r = qp[i] * scale_log2e;
@@ -617,55 +671,57 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   }
 }
 
-// Merge the splits of one query head: 8 groups of 128 threads, each group
-// folds a fixed residue class of splits, then the groups are added in order.
-constexpr int kCombGroups = 8;
-constexpr int kCombThreads = kCombGroups * kHeadDim;
-constexpr int kMaxSplits = 4096;
+// Merge the splits of one query head. Block (head, slice) produces 32 output
+// dimensions: 8 groups of 32 threads each fold a fixed residue class of the
+// splits with running (max, sum, acc) rescaling, all of a group's loads issued
+// together; the 8 groups are then merged in order (bitwise deterministic).
+constexpr int kCombThreads = 256;
+constexpr int kSliceDims = kHeadDim / kCombSlices;               // 32
+constexpr int kCombGroups = kCombThreads / kSliceDims;           // 8
+constexpr int kCombBatch = 16;                                   // splits per thread per round
+
+__device__ __forceinline__ void lse_merge(float& m, float& l, float& o, float ms, float ls, float os) {
+  if (ms == -INFINITY) return;
+  const float mn = fmaxf(m, ms);
+  const float a = __builtin_amdgcn_exp2f(m - mn);   // 0 when m is -inf
+  const float b = __builtin_amdgcn_exp2f(ms - mn);
+  l = fmaf(l, a, ls * b);
+  o = fmaf(o, a, os * b);
+  m = mn;
+}
 
 __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(const float* __restrict__ part, int splits,
                                                                       float* __restrict__ out,
                                                                       float* __restrict__ lse) {
-  __shared__ float wsc[kMaxSplits];
-  __shared__ float red[kCombThreads / kWave];
-  __shared__ float po[kCombGroups][kHeadDim];
-  __shared__ float pl[kCombGroups];
-  const int row = blockIdx.x;
+  __shared__ float gm[kCombGroups][kSliceDims], gl[kCombGroups][kSliceDims], go[kCombGroups][kSliceDims];
+  const int row = blockIdx.x, slice = blockIdx.y;
+  const int dl = threadIdx.x % kSliceDims, grp = threadIdx.x / kSliceDims;
+  const int d = slice * kSliceDims + dl;
   const float* pr = part + int64_t(row) * splits * (kHeadDim + 2);
-  float M = -INFINITY;
-  for (int s = threadIdx.x; s < splits; s += kCombThreads) M = fmaxf(M, pr[int64_t(s) * (kHeadDim + 2)]);
-  M = wave_max(M);
-  if (lane_id() == 0) red[threadIdx.x / kWave] = M;
-  __syncthreads();
-  M = red[0];
+  float m = -INFINITY, l = 0.f, o = 0.f;
+  for (int s0 = grp; s0 < splits; s0 += kCombGroups * kCombBatch) {
+    float ms[kCombBatch], ls[kCombBatch], os[kCombBatch];
 #pragma unroll
-  for (int i = 1; i < kCombThreads / kWave; ++i) M = fmaxf(M, red[i]);
-  for (int s = threadIdx.x; s < splits; s += kCombThreads) {
-    const float ms = pr[int64_t(s) * (kHeadDim + 2)];
-    wsc[s] = (M == -INFINITY || ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - M);
-  }
-  __syncthreads();
-  const int grp = threadIdx.x / kHeadDim, d = threadIdx.x % kHeadDim;
-  float o = 0.f, L = 0.f;
-#pragma unroll 4
-  for (int s = grp; s < splits; s += kCombGroups) {
-    const float sc = wsc[s];
-    const float* ps_ = pr + int64_t(s) * (kHeadDim + 2);
-    o = fmaf(ps_[2 + d], sc, o);
-    if (d == 0) L = fmaf(ps_[1], sc, L);
-  }
-  po[grp][d] = o;
-  if (d == 0) pl[grp] = L;
-  __syncthreads();
-  if (threadIdx.x < kHeadDim) {
-    float oo = 0.f, LL = 0.f;
-#pragma unroll
-    for (int g = 0; g < kCombGroups; ++g) {
-      oo += po[g][threadIdx.x];
-      LL += pl[g];
+    for (int k = 0; k < kCombBatch; ++k) {
+      const int s = s0 + kCombGroups * k;
+      const bool ok = s < splits;
+      const float* ps = pr + int64_t(ok ? s : 0) * (kHeadDim + 2);
+      ms[k] = ok ? ps[0] : -INFINITY;
+      ls[k] = ps[1];
+      os[k] = ps[2 + d];
     }
-    out[int64_t(row) * kHeadDim + threadIdx.x] = LL > 0.f ? oo / LL : 0.f;
-    if (lse && threadIdx.x == 0) lse[row] = LL > 0.f ? (M + log2f(LL)) * kLn2 : -INFINITY;
+#pragma unroll
+    for (int k = 0; k < kCombBatch; ++k) lse_merge(m, l, o, ms[k], ls[k], os[k]);
+  }
+  gm[grp][dl] = m;
+  gl[grp][dl] = l;
+  go[grp][dl] = o;
+  __syncthreads();
+  if (grp == 0) {
+#pragma unroll
+    for (int g = 1; g < kCombGroups; ++g) lse_merge(m, l, o, gm[g][dl], gl[g][dl], go[g][dl]);
+    out[int64_t(row) * kHeadDim + d] = l > 0.f ? o / l : 0.f;
+    if (lse && slice == 0 && dl == 0) lse[row] = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
   }
 }
 
@@ -727,7 +783,8 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                                            heads_q, heads_kv);
   }
   if (st != RBQ_OK) return st;
-  decode_combine_kernel<<<batch * heads_q, kCombThreads, 0, stream>>>(part, sp.total(), out, lse);
+  decode_combine_kernel<<<dim3(batch * heads_q, kCombSlices), kCombThreads, 0, stream>>>(part, sp.total(), out,
+                                                                                           lse);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

@@ -39,7 +39,8 @@ constexpr int kToppThreads = 256;
 constexpr int kToppPerThread = 16;
 constexpr int kToppChunk = kToppThreads * kToppPerThread;   // 4096 scores per block
 constexpr int kBins1 = 4096, kBins2 = 4096, kBins3 = 256;
-constexpr int kHistPerRow = kBins1 + kBins2 + kBins3;         // uint64 counters per row
+constexpr int kCoarse = 64;                                   // coarse bins (of 64 fine bins) of levels 1 and 2
+constexpr int kHistPerRow = kBins1 + kBins2 + kBins3 + 2 * kCoarse;   // uint64 counters per row
 constexpr int kToppStateWords = 8;                          // per-row uint32 state
 
 struct ToppWorkspace {
@@ -54,6 +55,8 @@ ToppWorkspace topp_workspace(void* base, int64_t rows, int32_t n);
 
 // Decode: split-K over chunks of the indexed rows and of the window.
 constexpr int kDecodeChunk = 1024;        // indexed positions per block (at most)
+constexpr int kDecodeMinBlocks = 1024;    // the chunk is halved (down to 256) until the grid has this many blocks
+constexpr int kCombSlices = 4;            // combine blocks per query head (32 output dimensions each)
 constexpr int kDecodeWinChunk = 256;      // window rows per block
 struct DecodeSplits {
   int32_t chunk;            // indexed positions per split (<= kDecodeChunk)

@@ -16,9 +16,10 @@
 // cumulative mass.
 //
 // Kernels, each over grid (chunks of 4096 scores, rows). The crossing searches
-// are repeated by every block of a row (a parallel scan over the row's bins,
-// read from L2), which costs less than an extra launch and needs neither
-// cross-block waiting nor device-wide fences:
+// are repeated by every block of a row, which costs less than an extra launch
+// and needs neither cross-block waiting nor device-wide fences; levels 1 and 2
+// also keep 64 coarse bins (sums of 64 fine bins), so a search reads 64 coarse
+// then 64 fine counters (one wave, two dependent loads) instead of 4096:
 //   1 max        per-chunk max; clears the row's histograms
 //   2 level 1    row max; 4096-bin histogram of key bits 31..20
 //   3 level 2    total mass Z, target T = ceil(p Z), crossing bin b1;
@@ -81,15 +82,11 @@ struct Crossing {
   u64 need;
 };
 template <int BPT>
-__device__ void find_crossing(const u64* __restrict__ hist, u64 T, float frac, u64* wtot, Crossing* out) {
+__device__ void find_crossing(const u64* h, u64 T, float frac, u64* wtot, Crossing* out) {
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
-  u64 h[BPT];
   u64 s = 0;
 #pragma unroll
-  for (int k = 0; k < BPT; ++k) {
-    h[k] = hist[t * BPT + k];
-    s += h[k];
-  }
+  for (int k = 0; k < BPT; ++k) s += h[k];
   // inclusive suffix sum inside the wave (higher lanes hold higher bins)
   u64 x = s;
 #pragma unroll
@@ -118,6 +115,56 @@ __device__ void find_crossing(const u64* __restrict__ hist, u64 T, float frac, u
     cum += h[k];
   }
   __syncthreads();
+}
+
+// The same search over 4096 fine bins with their 64 coarse sums, by wave 0:
+// the coarse crossing first, then the fine crossing inside it.
+// `c` is coarse[lane] for the threads of wave 0 (loaded by the caller together
+// with its other independent loads, so the search costs one more round trip).
+__device__ void find_crossing_2lvl(const u64* __restrict__ fine, u64 c, u64 T, float frac, Crossing* out) {
+  static_assert(kCoarse == kWave && kBins1 == kCoarse * kWave && kBins2 == kBins1, "one coarse bin per lane");
+  if (threadIdx.x < kWave) {
+    const int lane = lane_id();
+    u64 x = c;                                   // inclusive suffix sum (higher lanes hold higher bins)
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const u64 y = shfl_down_u64(x, o);
+      if (lane + o < kWave) x += y;
+    }
+    const uint32_t tlo = __shfl(uint32_t(x), 0, kWave), thi = __shfl(uint32_t(x >> 32), 0, kWave);
+    const u64 total = (u64(thi) << 32) | tlo;
+    if (frac > 0.f) T = u64(ceil(double(frac) * double(total)));
+    const u64 above = x - c;
+    const uint64_t hit = __ballot(above < T && x >= T);
+    const int g = __builtin_ctzll(hit);          // exactly one lane: suffix sums grow from 0 to total >= T >= 1
+    const uint32_t nlo = __shfl(uint32_t(T - above), g, kWave), nhi = __shfl(uint32_t((T - above) >> 32), g, kWave);
+    const u64 need = (u64(nhi) << 32) | nlo;
+    const u64 f = fine[g * kWave + lane];
+    u64 z = f;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const u64 y = shfl_down_u64(z, o);
+      if (lane + o < kWave) z += y;
+    }
+    const u64 above2 = z - f;
+    if (above2 < need && z >= need) {
+      out->bin = uint32_t(g * kWave + lane);
+      out->need = need - above2;
+    }
+  }
+  __syncthreads();
+}
+
+// Coarse sums of a block's LDS histogram of 4096 bins, added to the row's
+// 64 global coarse counters (one atomic per non-empty coarse bin).
+__device__ __forceinline__ void flush_coarse(const u64* h, u64* __restrict__ gcoarse) {
+  constexpr int kPer = kBins1 / kT;             // 16 fine bins per thread, 4 threads per coarse bin
+  u64 s = 0;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) s += h[threadIdx.x * kPer + k];
+  s += shfl_down_u64(s, 1);
+  s += shfl_down_u64(s, 2);
+  if ((threadIdx.x & 3) == 0 && s) atomicAdd(&gcoarse[threadIdx.x / 4], s);
 }
 
 // the thread's kPT scores of chunk c (element c * kChunk + k * kT + tid), all loads in flight
@@ -163,12 +210,15 @@ __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict
   load_chunk(scores + int64_t(row) * n, n, c, v);
   const float m = row_max(chunk_max + int64_t(row) * chunks, chunks, red);   // barriers: h is clear after it
 #pragma unroll
-  for (int k = 0; k < kPT; ++k)
-    if (in_row(n, c, k)) atomicAdd(&h[score_key(v[k]) >> 20], fixed_mass(v[k], m, scale_log2e));
+  for (int k = 0; k < kPT; ++k) {
+    const u64 ms = fixed_mass(v[k], m, scale_log2e);
+    if (in_row(n, c, k) && ms) atomicAdd(&h[score_key(v[k]) >> 20], ms);
+  }
   __syncthreads();
   u64* g = hist + int64_t(row) * kHistPerRow;
   for (int b = threadIdx.x; b < kBins1; b += kT)
     if (h[b]) atomicAdd(&g[b], h[b]);
+  flush_coarse(h, g + kBins1 + kBins2 + kBins3);
 }
 
 // Level 2 (LEVEL == 2) or level 3 (LEVEL == 3): find the previous level's
@@ -185,23 +235,24 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   __shared__ int red2[kTW];
   if (LEVEL == 3)
     for (int b = threadIdx.x; b <= kBins3; b += kT) cnt_s[b] = 0;
-  __shared__ u64 wtot[kTW];
   __shared__ float red[kTW];
   __shared__ Crossing cr;
   const int row = blockIdx.y, c = blockIdx.x;
   u64* rh = hist + int64_t(row) * kHistPerRow;
   uint32_t* st = state + int64_t(row) * kToppStateWords;
   for (int b = threadIdx.x; b < kBins; b += kT) h[b] = 0;
+  u64* coarse = rh + kBins1 + kBins2 + kBins3;
+  const u64 cpre = threadIdx.x < kWave ? coarse[(LEVEL == 2 ? 0 : kCoarse) + threadIdx.x] : 0;
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
   const float m = row_max(chunk_max + int64_t(row) * chunks, chunks, red);
   uint32_t prefix;
   if (LEVEL == 2) {
-    find_crossing<kBins1 / kT>(rh, 0, p, wtot, &cr);
+    find_crossing_2lvl(rh, cpre, 0, p, &cr);
     prefix = cr.bin;
   } else {
     const u64 T = (u64(st[2]) << 32) | st[1];
-    find_crossing<kBins2 / kT>(rh + kBins1, T, 0.f, wtot, &cr);
+    find_crossing_2lvl(rh + kBins1, cpre, T, 0.f, &cr);
     prefix = (st[0] << 12) | cr.bin;
   }
   // state words: [0..2] = level-1 bin and the mass still needed inside it
@@ -221,7 +272,8 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
     const uint32_t key = score_key(v[k]);
     if ((key >> shift_hi) == prefix) {
       const uint32_t bin = LEVEL == 2 ? ((key >> 8) & 0xfffu) : (key & 0xffu);
-      atomicAdd(&h[bin], fixed_mass(v[k], m, scale_log2e));
+      const u64 ms = fixed_mass(v[k], m, scale_log2e);
+      if (ms) atomicAdd(&h[bin], ms);
       if (LEVEL == 3) atomicAdd(&cnt_s[bin], 1u);
     } else if (LEVEL == 3 && (key >> 8) > prefix) {
       ++above;
@@ -235,6 +287,7 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   u64* g = rh + (LEVEL == 2 ? kBins1 : kBins1 + kBins2);
   for (int b = threadIdx.x; b < kBins; b += kT)
     if (h[b]) atomicAdd(&g[b], h[b]);
+  if (LEVEL == 2) flush_coarse(h, coarse + kCoarse);
   if (LEVEL == 3) {
     // this chunk's count above the bin, then suffix counts of the 256 sub-bins
     static_assert(kBins3 == kT, "one sub-bin per thread");
@@ -262,15 +315,17 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
                                                         int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_count) {
   __shared__ u64 wtot[kTW];
   __shared__ int red[kTW];
-  __shared__ int wcnt[kTW];
+  __shared__ int kcnt[kPT][kTW];
   __shared__ Crossing cr;
   const int row = blockIdx.y, c = blockIdx.x;
   const int wave = threadIdx.x / kWave, lane = lane_id();
   uint32_t* st = state + int64_t(row) * kToppStateWords;
+  static_assert(kBins3 == kT, "one final-level bin per thread");
+  const u64 hv = hist[int64_t(row) * kHistPerRow + kBins1 + kBins2 + threadIdx.x];
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
   const u64 T = (u64(st[5]) << 32) | st[4];
-  find_crossing<kBins3 / kT>(hist + int64_t(row) * kHistPerRow + kBins1 + kBins2, T, 0.f, wtot, &cr);
+  find_crossing<1>(&hv, T, 0.f, wtot, &cr);
   const uint32_t kstar = (st[3] << 8) | cr.bin;
   // offset of this chunk = selected keys of the chunks before it
   const int32_t* cc = chunk_cnt + int64_t(row) * chunks * (1 + kBins3);
@@ -283,22 +338,28 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
 #pragma unroll
   for (int w = 0; w < kTW; ++w) offset += red[w];
 
+  // ascending compaction: element (k, thread) has index c*kChunk + k*kT + thread, so the
+  // order is k-major, then wave, then lane; all kPT ballots first, one barrier
   int32_t* out = sel_idx + int64_t(row) * n;
+  uint64_t bal[kPT];
+#pragma unroll
   for (int k = 0; k < kPT; ++k) {
-    const int i = c * kChunk + k * kT + threadIdx.x;
-    const bool f = in_row(n, c, k) && score_key(v[k]) >= kstar;
-    const uint64_t bal = __ballot(f);
-    const int pre = __builtin_amdgcn_mbcnt_hi(uint32_t(bal >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal), 0u));
-    __syncthreads();
-    if (lane == 0) wcnt[wave] = __popcll(bal);
-    __syncthreads();
+    bal[k] = __ballot(in_row(n, c, k) && score_key(v[k]) >= kstar);
+    if (lane == 0) kcnt[k][wave] = __popcll(bal[k]);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kPT; ++k) {
     int woff = 0, tot = 0;
 #pragma unroll
     for (int w = 0; w < kTW; ++w) {
-      woff += w < wave ? wcnt[w] : 0;
-      tot += wcnt[w];
+      woff += w < wave ? kcnt[k][w] : 0;
+      tot += kcnt[k][w];
     }
-    if (f) out[offset + woff + pre] = i;
+    if ((bal[k] >> lane) & 1u) {
+      const int pre = __builtin_amdgcn_mbcnt_hi(uint32_t(bal[k] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal[k]), 0u));
+      out[offset + woff + pre] = c * kChunk + k * kT + int(threadIdx.x);
+    }
     offset += tot;
   }
   if (c == chunks - 1 && threadIdx.x == 0) sel_count[row] = offset;

@@ -100,10 +100,10 @@ rbq_status check_topp(int32_t batch, int32_t heads_q, int32_t n, const float* sc
 
 DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w) {
   DecodeSplits s;
-  // halve the chunk until the grid has >= 1024 blocks (4 per CU) or the chunk is 256
+  // halve the chunk until the grid has kDecodeMinBlocks blocks or the chunk is 256
   const int64_t groups = int64_t(batch) * heads_kv;
   s.chunk = kDecodeChunk;
-  while (s.chunk > 256 && groups * ((int64_t(n) + s.chunk - 1) / s.chunk) < 1024) s.chunk /= 2;
+  while (s.chunk > 256 && groups * ((int64_t(n) + s.chunk - 1) / s.chunk) < kDecodeMinBlocks) s.chunk /= 2;
   s.idx_splits = n > 0 ? (n + s.chunk - 1) / s.chunk : 0;
   s.win_splits = w > 0 ? (w + kDecodeWinChunk - 1) / kDecodeWinChunk : 0;
   if (s.total() == 0) s.win_splits = 1;   // one empty split keeps the combine step uniform

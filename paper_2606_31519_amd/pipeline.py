@@ -105,7 +105,10 @@ class DecodeState:
 
     def step(self, p, stream=None, flush=True):
         """One decode step of the whole path: quantize -> score -> Top-p -> sparse
-        attention (index selection + window), then the lazy flush of the window."""
+        attention (index selection + window), then the lazy flush of the window.
+        (The flush writes index rows [n, n + w), which this step's scoring does
+        not read; running it on a second stream was measured slower on MI355X:
+        the fork/join costs more than the flush itself.)"""
         self.quantize(stream)
         self.score(stream)
         self.select(p, stream)
