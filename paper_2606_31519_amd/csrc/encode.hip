@@ -96,6 +96,27 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
   const int lane = lane_id();
   const int mk = lane % 32, half = lane / 32;
 
+  // the tile's keys in 16-byte pieces, consecutive threads on consecutive pieces;
+  // the first tile is requested before P is staged, each next one during the current tile
+  constexpr int kElemBytes = DT == RBQ_BF16 ? 2 : 4;
+  constexpr int kPiecesPerRow = kHeadDim * kElemBytes / 16;            // 16 (bf16) or 32 (fp32)
+  constexpr int kPer = kTileKeys * kPiecesPerRow / kEncThreads;         // 2 or 4 per thread
+  const int tiles = (n_new + kTileKeys - 1) / kTileKeys;
+  u32x4 pc[kPer];
+  auto load_tile = [&](int tl) {
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int pidx = j * kEncThreads + threadIdx.x;
+      const int row = pidx / kPiecesPerRow, piece = pidx % kPiecesPerRow;
+      const int key = tl * kTileKeys + row;
+      pc[j] = key < n_new ? *reinterpret_cast<const u32x4*>(static_cast<const char*>(keys) +
+                                                           ((int64_t(bh) * keys_ld + key) * kHeadDim) * kElemBytes +
+                                                           piece * 16)
+                          : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  if (int(blockIdx.x) < tiles) load_tile(blockIdx.x);
+
   for (int e = threadIdx.x * 4; e < kHeadDim * kHeadDim; e += kEncThreads * 4)
     *reinterpret_cast<f32x4*>(Ps + e) = *reinterpret_cast<const f32x4*>(P + e);
   if (threadIdx.x < kHeadDim) {
@@ -104,24 +125,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
   }
   __syncthreads();
 
-  const int tiles = (n_new + kTileKeys - 1) / kTileKeys;
   for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
     const int key0 = tile * kTileKeys;
-    // ---- stage the tile: 16-byte pieces, consecutive threads on consecutive pieces
-    constexpr int kElemBytes = DT == RBQ_BF16 ? 2 : 4;
-    constexpr int kPiecesPerRow = kHeadDim * kElemBytes / 16;            // 16 (bf16) or 32 (fp32)
-    constexpr int kPer = kTileKeys * kPiecesPerRow / kEncThreads;         // 2 or 4 per thread
-    u32x4 pc[kPer];
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      const int pidx = j * kEncThreads + threadIdx.x;
-      const int row = pidx / kPiecesPerRow, piece = pidx % kPiecesPerRow;
-      const int key = key0 + row;
-      pc[j] = key < n_new ? *reinterpret_cast<const u32x4*>(static_cast<const char*>(keys) +
-                                                           ((int64_t(bh) * keys_ld + key) * kHeadDim) * kElemBytes +
-                                                           piece * 16)
-                          : u32x4{0u, 0u, 0u, 0u};
-    }
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int pidx = j * kEncThreads + threadIdx.x;
@@ -144,6 +149,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
         xr[d + 3] = in ? __uint_as_float(pc[j].w) - ck_s[d + 3] : 0.f;
       }
     }
+    if (tile + int(gridDim.x) < tiles) load_tile(tile + gridDim.x);   // lands while this tile is rotated
     __syncthreads();
 
     // ---- ||x||^2 and <c_q, x>: threads 0..127, key t / 4, a quarter of the dims each
@@ -167,12 +173,15 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
     }
 
     // ---- r = x P for output dimensions [32 wave, 32 wave + 32): A = X rows, B = P rows
-    f32x16 acc = f32x16{0.f};
-    for (int s2 = 0; s2 < kHeadDim / 2; ++s2) {
+    f32x16 acc = f32x16{0.f}, acc2 = f32x16{0.f};   // two chains over alternate k-steps, added at the end
+    for (int s2 = 0; s2 < kHeadDim / 2; s2 += 2) {
       const int k = 2 * s2 + half;
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(Xs[mk * kXStride + k], Ps[k * kHeadDim + 32 * wave + mk], acc, 0,
                                                  0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x2f32(Xs[mk * kXStride + k + 2], Ps[(k + 2) * kHeadDim + 32 * wave + mk],
+                                                  acc2, 0, 0, 0);
     }
+    acc += acc2;
     // acc[r] at lane l: key 8 (r / 4) + 4 (l / 32) + r % 4, dimension 32 wave + l % 32
 #pragma unroll
     for (int r = 0; r < 16; ++r) {

@@ -98,6 +98,12 @@ __global__ __launch_bounds__(kQAll) void quantize_kernel(const float* __restrict
   const int j = threadIdx.x % kHeadDim;        // output dimension
   const int part = threadIdx.x / kHeadDim;     // which quarter of the input dimensions
 
+  // this group's 32 rows of P, requested before anything else (they do not depend on q)
+  constexpr int kRows = kHeadDim / kQParts;
+  float pv[kRows];
+#pragma unroll
+  for (int k = 0; k < kRows; ++k) pv[k] = P[(part * kRows + k) * kHeadDim + j];
+
   float qj = 0.f, y = 0.f, ck = 0.f;
   if (part == 0) {
     qj = q[int64_t(row) * kHeadDim + j];
@@ -111,16 +117,10 @@ __global__ __launch_bounds__(kQAll) void quantize_kernel(const float* __restrict
   if (part == 0) u_s[j] = A > 0.f ? y / A : 0.f;
   __syncthreads();
 
-  // q'[j] = sum_d P[d][j] u[d]: each group takes 32 rows of P, all loads in flight at once
+  // q'[j] = sum_d P[d][j] u[d]: each group takes 32 rows of P (loaded above)
   float acc = 0.f;
-  {
-    constexpr int kRows = kHeadDim / kQParts;
-    float pv[kRows];
 #pragma unroll
-    for (int k = 0; k < kRows; ++k) pv[k] = P[(part * kRows + k) * kHeadDim + j];
-#pragma unroll
-    for (int k = 0; k < kRows; ++k) acc = fmaf(pv[k], u_s[part * kRows + k], acc);
-  }
+  for (int k = 0; k < kRows; ++k) acc = fmaf(pv[k], u_s[part * kRows + k], acc);
   part_s[part][j] = acc;
   __syncthreads();
   // every thread computes the sum; only the first 128 (two waves) use it

@@ -12,8 +12,13 @@
 //   X = Delta (2 ip - S_u) + q_l (2 pc - D)   ( = 2 Delta ip + 2 q_l pc - Delta S_u - D q_l )
 //   S = A f X + B0 + g,
 // which avoids the cancellation between 2 Delta ip and Delta S_u in fp32.
-// The kernel streams codes + factors once (24 B per KV key) and writes 4 B per
-// (key, head): HBM-bound at G = 4 and close to the VALU limit at G = 8.
+// Per (key, head) that is 16 AND + 16 v_bcnt_u32_b32 (the popcount-and-add,
+// chained by Horner over the planes) + 3 shifts, then 5 float ops. The kernel
+// streams codes + factors once (24 B per KV key, non-temporal) and writes 4 B
+// per (key, head) with non-temporal stores (measured faster for the whole
+// decode step too, although the Top-p passes read the scores next). Blocks
+// that lie wholly inside [0, n) take a path without per-key guards. At G = 4 it
+// is HBM-bound; at G = 8 the integer work adds ~25 % over a memory-only pass.
 #include "rbq_device.h"
 #include "rbq_internal.h"
 
@@ -21,6 +26,27 @@ namespace rbq {
 namespace {
 
 constexpr int kScoreThreads = 256;
+
+// acc + popcount(x), one v_bcnt_u32_b32 (kept as a chain: the compiler would
+// otherwise re-associate the sums into extra adds)
+__device__ __forceinline__ uint32_t bcnt_acc(uint32_t x, uint32_t acc) {
+  uint32_t r;
+  asm("v_bcnt_u32_b32 %0, %1, %2" : "=v"(r) : "v"(x), "v"(acc));
+  return r;
+}
+// ip = sum_j 2^j popcount(c AND plane_j) by Horner over the planes, 16 AND + 16 BCNT + 3 shifts
+__device__ __forceinline__ uint32_t binary_int4_dot(const u32x4 c, const uint32_t* q) {
+  uint32_t a = 0u;
+#pragma unroll
+  for (int j = 3; j >= 0; --j) {
+    a <<= 1;
+    a = bcnt_acc(c.x & q[4 * j + 0], a);
+    a = bcnt_acc(c.y & q[4 * j + 1], a);
+    a = bcnt_acc(c.z & q[4 * j + 2], a);
+    a = bcnt_acc(c.w & q[4 * j + 3], a);
+  }
+  return a;
+}
 
 template <int KPT, bool INTS>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(
@@ -32,20 +58,16 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   const int hk = bh - b * Hkv;
   const int64_t kbase = int64_t(bh) * cap;
   const int i0 = blockIdx.x * (kScoreThreads * KPT) + threadIdx.x;
+  const bool full = (blockIdx.x + 1) * (kScoreThreads * KPT) <= n;   // block-uniform: no key past n
 
   u32x4 c[KPT];
   f32x2 fg[KPT];
   int pcm[KPT];   // 2 popcount(code) - D, exact
 #pragma unroll
   for (int u = 0; u < KPT; ++u) {
-    const int i = i0 + u * kScoreThreads;
-    if (i < n) {
-      c[u] = __builtin_nontemporal_load(codes + kbase + i);
-      if (!INTS) fg[u] = __builtin_nontemporal_load(kfac + kbase + i);
-    } else {
-      c[u] = u32x4{0u, 0u, 0u, 0u};
-      fg[u] = f32x2{0.f, 0.f};
-    }
+    const int i = min(i0 + u * kScoreThreads, n - 1);    // keys past n are computed but never stored
+    c[u] = __builtin_nontemporal_load(codes + kbase + i);
+    if (!INTS) fg[u] = __builtin_nontemporal_load(kfac + kbase + i);
   }
 #pragma unroll
   for (int u = 0; u < KPT; ++u) {
@@ -57,8 +79,30 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     }
   }
 
+  const int row0 = b * Hq + hk * G;
+  if (full && !INTS) {
+    for (int g = 0; g < G; ++g) {
+      const int row = row0 + g;
+      const uint32_t* Q = qplanes + int64_t(row) * 16;
+      uint32_t qp[16];
+#pragma unroll
+      for (int t = 0; t < 16; ++t) qp[t] = Q[t];
+      const float* qs = qscal + int64_t(row) * RBQ_QSCAL_STRIDE;
+      const float ql = qs[0], delta = qs[1], A = qs[3], B0 = qs[4];
+      const int su = int(qs[2]);
+      const float a_delta = A * delta, a_ql = A * ql;
+      float* out = scores + int64_t(row) * n;
+#pragma unroll
+      for (int u = 0; u < KPT; ++u) {
+        const int ip = int(binary_int4_dot(c[u], qp));
+        const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
+        __builtin_nontemporal_store(fmaf(fg[u].x, y, B0 + fg[u].y), out + i0 + u * kScoreThreads);
+      }
+    }
+    return;
+  }
   for (int g = 0; g < G; ++g) {
-    const int row = b * Hq + hk * G + g;
+    const int row = row0 + g;
     const uint32_t* Q = qplanes + int64_t(row) * 16;   // [plane][word]
     uint32_t qp[16];
 #pragma unroll
@@ -71,22 +115,14 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
 #pragma unroll
     for (int u = 0; u < KPT; ++u) {
       const int i = i0 + u * kScoreThreads;
-      unsigned p0 = __popc(c[u].x & qp[0]) + __popc(c[u].y & qp[1]) + __popc(c[u].z & qp[2]) +
-                    __popc(c[u].w & qp[3]);
-      unsigned p1 = __popc(c[u].x & qp[4]) + __popc(c[u].y & qp[5]) + __popc(c[u].z & qp[6]) +
-                    __popc(c[u].w & qp[7]);
-      unsigned p2 = __popc(c[u].x & qp[8]) + __popc(c[u].y & qp[9]) + __popc(c[u].z & qp[10]) +
-                    __popc(c[u].w & qp[11]);
-      unsigned p3 = __popc(c[u].x & qp[12]) + __popc(c[u].y & qp[13]) + __popc(c[u].z & qp[14]) +
-                    __popc(c[u].w & qp[15]);
-      const int ip = int(p0 + 2u * p1 + 4u * p2 + 8u * p3);
+      const int ip = int(binary_int4_dot(c[u], qp));
       if (INTS) {
         if (i < n) ip_out[int64_t(row) * n + i] = ip;
       } else {
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
-        const float s = fmaf(fg[u].x, y, B0 + fg[u].y);
-        if (i < n) out[i] = s;   // cached store: the Top-p passes read the scores next
+        const float sc = fmaf(fg[u].x, y, B0 + fg[u].y);
+        if (i < n) __builtin_nontemporal_store(sc, out + i);
       }
     }
   }
