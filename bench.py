@@ -12,7 +12,10 @@ data in the 256 MB Infinity Cache.
 One JSON line is printed (rank 0, N = 1). `value` = proxy-scored (query head,
 key) pairs per second over the whole step; `ms_per_step` is the sparse decode
 step latency at 128K, compared against dense bf16 decode at the same shape
-(this library's split-K kernel and torch SDPA, the faster of the two).
+(this library's split-K kernel and torch SDPA, the faster of the two). The line
+also carries the per-stage times, the roofline of the dominant call, the Top-p
+sweep (p = 0.8 / 0.9 / 0.95 / 0.99: step time, budget, KV-group union), the
+standalone score scan of the wide-head workload, and the oracle's CPU rate.
 """
 from __future__ import annotations
 
@@ -220,7 +223,7 @@ def main():
     ap.add_argument("--replicas", type=int, default=4)
     ap.add_argument("--no-scan", action="store_true", help="skip the standalone wide-head scan")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
-    ap.add_argument("--sweep", action="store_true", help="also time p = 0.8 / 0.9 / 0.99")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the Top-p sweep (p = 0.8 / 0.9 / 0.95 / 0.99)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
@@ -299,15 +302,21 @@ def main():
     dense_best = min(x for x in (dense_ms, sdpa_ms) if x is not None)
     dense_bytes = st0.B * st0.Hkv * (st0.n + st0.w) * 2 * st0.D * 2
 
+    # Top-p sweep of the 128K workload: step time, selected budget and KV-group union per p
     sweep = {}
-    if args.sweep:
-        for pp in (0.8, 0.9, 0.95, 0.99):
+    if not args.no_sweep:
+        for pp in wl.p_sweep or (0.8, 0.9, 0.95, 0.99):
             gs = [_graph(torch, lambda r=r, pp=pp: r.step(pp)) for r in reps]
             ms = _time_graphs(torch, gs, args.steps, args.warmup)
             del gs
+            st0.step(pp)
+            torch.cuda.synchronize()
+            u_rows, _ = _union_rows(st0)
             cnt = st0.sel_count.cpu().numpy()
-            sweep[str(pp)] = {"ms_per_step": ms, "budget_mean": float(cnt.mean()), "budget_min": int(cnt.min()),
-                              "budget_max": int(cnt.max())}
+            sweep[str(pp)] = {"ms_per_step": ms, "speedup_vs_dense": dense_best / ms,
+                              "budget_mean": float(cnt.mean()), "budget_frac": float(cnt.mean()) / st0.n,
+                              "budget_min": int(cnt.min()), "budget_max": int(cnt.max()),
+                              "union_frac": u_rows / (st0.B * st0.Hkv * st0.n)}
         st0.step(p)
         torch.cuda.synchronize()
 
