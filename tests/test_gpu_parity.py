@@ -320,6 +320,23 @@ def test_end_to_end_config3_full_size_sampled(R, pipeline):
         print(f"config3 p={p}: budgets {[r[2] for r in rep]} recall {[round(r[4], 3) for r in rep]}")
 
 
+def test_end_to_end_config4_batched_varied_sparsity_sampled(R, pipeline):
+    """Batch 16 x 32K with per-sequence planted fractions: one launch covers every
+    sequence's budget; sampled (sequence, KV head) groups are checked in full."""
+    wl = gen.config4()
+    st, rep = _end_to_end(R, pipeline, wl, wl.p, [(0, 0), (5, 3), (11, 7), (15, 2)], rows_per_group=[0, 2])
+    print("config4 (b, h, budget, set diff, recall):", rep)
+
+
+@pytest.mark.slow
+def test_end_to_end_config5_wide_heads_sampled(R, pipeline):
+    """64 query / 8 KV heads, batch 4 x 128K, Student-t keys: the launch shape of
+    the standalone scan in the bench; sampled groups and heads checked in full."""
+    wl = gen.config5()
+    st, rep = _end_to_end(R, pipeline, wl, wl.p, [(0, 0), (3, 6)], rows_per_group=[0, 7])
+    print("config5 (b, h, budget, set diff, recall):", rep)
+
+
 def test_step_is_deterministic(R, pipeline):
     wl = gen.config2(N=8192)
     st = pipeline.DecodeState.from_workload(wl)

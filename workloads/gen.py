@@ -193,25 +193,39 @@ def _student_t_keys(rng, N: int, D: int, nu: float = 3.0) -> np.ndarray:
 
 def _planted_gqa(name, B, Hq, Hkv, D, N, n_index, w, seed, p, key_fn, frac_fn, rho=0.9,
                  p_sweep=()) -> Workload:
+    """Each (sequence, KV head) group draws from its own generator, spawned from
+    `seed` in group order, so the groups can be generated by parallel threads
+    (numpy releases the GIL while it fills arrays) with a result that does not
+    depend on the thread count or scheduling."""
+    import concurrent.futures
+    import os
+
     rng = np.random.default_rng(seed)
     G = Hq // Hkv
+    fracs = [frac_fn(rng, b) for b in range(B)]
+    children = np.random.SeedSequence(seed).spawn(B * Hkv)
     K = np.empty((B, Hkv, N, D), dtype=np.uint16)
     V = np.empty((B, Hkv, N, D), dtype=np.uint16)
     q = np.empty((B, Hq, D), dtype=np.float32)
-    planted = []
-    for b in range(B):
-        frac = frac_fn(rng, b)
-        for hk in range(Hkv):
-            Kg = key_fn(rng, N, D)
-            dirs, sets = _plant_group(rng, Kg, G, frac, N)
-            K[b, hk] = f32_to_bf16_bits(Kg)
-            V[b, hk] = f32_to_bf16_bits(rng.standard_normal((N, D), dtype=np.float32))
-            kw = bf16_bits_to_f32(K[b, hk]).astype(np.float64)
-            for g in range(G):
-                s = kw @ dirs[g]
-                gamma = _calibrate_gamma(s, sets[g], rho, D)
-                q[b, hk * G + g] = (gamma * dirs[g]).astype(np.float32)
-                planted.append(sets[g])
+    planted = [None] * (B * Hq)
+
+    def group(idx):
+        b, hk = divmod(idx, Hkv)
+        grng = np.random.default_rng(children[idx])
+        Kg = key_fn(grng, N, D)
+        dirs, sets = _plant_group(grng, Kg, G, fracs[b], N)
+        K[b, hk] = f32_to_bf16_bits(Kg)
+        V[b, hk] = f32_to_bf16_bits(grng.standard_normal((N, D), dtype=np.float32))
+        kw = bf16_bits_to_f32(K[b, hk]).astype(np.float64)
+        for g in range(G):
+            s = kw @ dirs[g]
+            gamma = _calibrate_gamma(s, sets[g], rho, D)
+            q[b, hk * G + g] = (gamma * dirs[g]).astype(np.float32)
+            planted[b * Hq + hk * G + g] = sets[g]
+
+    workers = max(1, min(16, len(os.sched_getaffinity(0)), B * Hkv))
+    with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(group, range(B * Hkv)))
     return Workload(name=name, B=B, Hq=Hq, Hkv=Hkv, D=D, N=N, n_index=n_index, w=w, kv_dtype="bf16",
                     K=K, V=V, q=q, c_q=np.zeros((B, Hkv, D), np.float32), P=haar_rotation(D),
                     p=p, planted=planted, p_sweep=tuple(p_sweep))
