@@ -35,6 +35,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sparse_decode_128k_traffic.txt")
 DECODE_SRC = os.path.join(ROOT, "paper_2606_31519_amd", "csrc", "decode.hip")
+SCAN_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_scan_wide_heads_traffic.txt")
+SCORE_SRC = os.path.join(ROOT, "paper_2606_31519_amd", "csrc", "score.hip")
 
 
 def _sha256(path):
@@ -43,18 +45,19 @@ def _sha256(path):
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def _measured_traffic():
-    """HBM bytes per rbq_sparse_decode call from the committed rocprofv3 --pmc summary
-    (FETCH_SIZE + WRITE_SIZE, scaled by the copy-kernel calibration), or None when the
-    decode source has changed since the counters were taken."""
+def _measured_traffic(path=TRAFFIC_FILE, src=DECODE_SRC, sha_key="decode_source_sha256"):
+    """HBM bytes per call from a committed rocprofv3 --pmc summary (FETCH_SIZE +
+    WRITE_SIZE, scaled by the copy-kernel calibration): rbq_sparse_decode by
+    default, the wide-head rbq_score scan with the scan file. None when the
+    kernel's source has changed since the counters were taken."""
     try:
         kv = {}
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             for ln in f:
                 if ":" in ln and not ln.startswith("#"):
                     k, v = ln.split(":", 1)
                     kv[k.strip()] = v.strip()
-        if kv.get("decode_source_sha256") != _sha256(DECODE_SRC):
+        if kv.get(sha_key) != _sha256(src):
             return None
         return float(kv["hbm_bytes_per_call"])
     except (OSError, KeyError, ValueError):
@@ -211,7 +214,8 @@ def time_scan_c5(pipeline, gen, torch, steps, warmup, replicas=4):
     gbs = nbytes / (ms * 1e-3) / 1e9
     return {"workload": "gqa 64q/8kv ctx=128K b=4 bf16 student-t", "kernel": "score_kernel",
             "ms": ms, "keys_per_s": B * Hq * n / (ms * 1e-3), "kv_keys_per_s": B * Hkv * n / (ms * 1e-3),
-            "bytes": nbytes, "GBps": gbs, "frac_hbm": gbs / HBM_PEAK_GBS}
+            "bytes": nbytes, "GBps": gbs, "frac_hbm": gbs / HBM_PEAK_GBS,
+            "traffic": _measured_traffic(SCAN_TRAFFIC_FILE, SCORE_SRC, "score_source_sha256")}
 
 
 def main():

@@ -3,22 +3,25 @@
 // Eq. decomposition).
 //
 // One lane owns one key: a 128-bit load brings its whole D = 128 sign code,
-// a 64-bit load its factors (f, g). The G query heads of the KV group are
-// wave-uniform, so their four bit-planes (16 words per head) and scalars come
-// through scalar loads into SGPRs, and
-//   ip = sum_j 2^j popcount(code AND plane_j)
-// is 16 AND + 16 popcount-accumulate per (key, head) in registers. The fp32
-// reconstruction uses the exact integers 2 ip - S_u and 2 pc - D first,
+// a 64-bit load its factors (f, g). The integer part
+//   ip = sum_d bit_d q_d   (q_d in [0, 15], the INT4 query)
+// runs on v_dot8_u32_u4, which multiplies eight 4-bit pairs and accumulates:
+// the code is spread once per key to one bit per nibble (word 4 w + s holds
+// the bits of dimensions 32 w + 4 k + s, k = 0..7; 28 shift/AND ops), and the
+// query's four bit-planes are turned once per block into the matching nibble
+// words by a 4x4 bit transpose (kept in LDS). One (key, head) pair then costs
+// 16 dot8 ops, under half of the 16 AND + 16 popcount + 3 shift of the
+// bit-plane form, and the spread code is shared by the G query heads of the
+// KV group. The fp32 reconstruction uses the exact integers 2 ip - S_u and
+// 2 pc - D first,
 //   X = Delta (2 ip - S_u) + q_l (2 pc - D)   ( = 2 Delta ip + 2 q_l pc - Delta S_u - D q_l )
 //   S = A f X + B0 + g,
-// which avoids the cancellation between 2 Delta ip and Delta S_u in fp32.
-// Per (key, head) that is 16 AND + 16 v_bcnt_u32_b32 (the popcount-and-add,
-// chained by Horner over the planes) + 3 shifts, then 5 float ops. The kernel
-// streams codes + factors once (24 B per KV key, non-temporal) and writes 4 B
-// per (key, head) with non-temporal stores (measured faster for the whole
-// decode step too, although the Top-p passes read the scores next). Blocks
-// that lie wholly inside [0, n) take a path without per-key guards. At G = 4 it
-// is HBM-bound; at G = 8 the integer work adds ~25 % over a memory-only pass.
+// which avoids the cancellation between 2 Delta ip and Delta S_u in fp32. The
+// kernel streams codes + factors once (24 B per KV key, non-temporal) and
+// writes 4 B per (key, head) with non-temporal stores (measured faster for the
+// whole decode step too, although the Top-p passes read the scores next).
+// Blocks that lie wholly inside [0, n) take a path without per-key guards.
+// The scan is HBM-bound at G = 4 and at G = 8.
 #include "rbq_device.h"
 #include "rbq_internal.h"
 
@@ -26,26 +29,42 @@ namespace rbq {
 namespace {
 
 constexpr int kScoreThreads = 256;
+constexpr int kMaxGroup = 16;   // query heads per KV head handled by the kernels
 
-// acc + popcount(x), one v_bcnt_u32_b32 (kept as a chain: the compiler would
-// otherwise re-associate the sums into extra adds)
-__device__ __forceinline__ uint32_t bcnt_acc(uint32_t x, uint32_t acc) {
-  uint32_t r;
-  asm("v_bcnt_u32_b32 %0, %1, %2" : "=v"(r) : "v"(x), "v"(acc));
+// Nibble-packed query: word 4 w + s holds, in nibble k, the 4-bit value of
+// dimension 32 w + 4 k + s. Built from the four bit-planes of word w by a 4x4
+// bit transpose inside every nibble (plane j, bit s -> word s, bit j).
+__device__ __forceinline__ void planes_to_nibbles(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3,
+                                                  uint32_t* out) {
+  uint32_t t;
+  t = ((a0 >> 2) ^ a2) & 0x33333333u; a2 ^= t; a0 ^= t << 2;
+  t = ((a1 >> 2) ^ a3) & 0x33333333u; a3 ^= t; a1 ^= t << 2;
+  t = ((a0 >> 1) ^ a1) & 0x55555555u; a1 ^= t; a0 ^= t << 1;
+  t = ((a2 >> 1) ^ a3) & 0x55555555u; a3 ^= t; a2 ^= t << 1;
+  out[0] = a0; out[1] = a1; out[2] = a2; out[3] = a3;
+}
+
+// The sign code spread to one bit per nibble: word 4 w + s holds, in nibble k,
+// the sign bit of dimension 32 w + 4 k + s.
+struct Spread { uint32_t e[16]; };
+__device__ __forceinline__ Spread spread_code(const u32x4 c) {
+  Spread r;
+  const uint32_t cw[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+  for (int w = 0; w < 4; ++w)
+#pragma unroll
+    for (int s = 0; s < 4; ++s) r.e[4 * w + s] = (cw[w] >> s) & 0x11111111u;
   return r;
 }
-// ip = sum_j 2^j popcount(c AND plane_j) by Horner over the planes, 16 AND + 16 BCNT + 3 shifts
-__device__ __forceinline__ uint32_t binary_int4_dot(const u32x4 c, const uint32_t* q) {
-  uint32_t a = 0u;
+// ip = sum_d bit_d q_d: 16 v_dot8_u32_u4 (8 dimensions x 4 query bits each)
+__device__ __forceinline__ uint32_t binary_int4_dot(const Spread& e, const uint32_t* qn) {
+  uint32_t a = 0u, b = 0u;
 #pragma unroll
-  for (int j = 3; j >= 0; --j) {
-    a <<= 1;
-    a = bcnt_acc(c.x & q[4 * j + 0], a);
-    a = bcnt_acc(c.y & q[4 * j + 1], a);
-    a = bcnt_acc(c.z & q[4 * j + 2], a);
-    a = bcnt_acc(c.w & q[4 * j + 3], a);
+  for (int t = 0; t < 16; t += 2) {
+    a = __builtin_amdgcn_udot8(e.e[t], qn[t], a, false);
+    b = __builtin_amdgcn_udot8(e.e[t + 1], qn[t + 1], b, false);
   }
-  return a;
+  return a + b;
 }
 
 template <int KPT, bool INTS>
@@ -53,40 +72,53 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const u32x4* __restrict__ codes, const f32x2* __restrict__ kfac, const uint32_t* __restrict__ qplanes,
     const float* __restrict__ qscal, float* __restrict__ scores, int32_t* __restrict__ ip_out,
     int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G) {
+  __shared__ uint32_t qn_s[kMaxGroup][16];
   const int bh = blockIdx.y;                 // b * Hkv + kv head
   const int b = bh / Hkv;
   const int hk = bh - b * Hkv;
   const int64_t kbase = int64_t(bh) * cap;
   const int i0 = blockIdx.x * (kScoreThreads * KPT) + threadIdx.x;
   const bool full = (blockIdx.x + 1) * (kScoreThreads * KPT) <= n;   // block-uniform: no key past n
+  const int row0 = b * Hq + hk * G;
 
   u32x4 c[KPT];
   f32x2 fg[KPT];
-  int pcm[KPT];   // 2 popcount(code) - D, exact
 #pragma unroll
   for (int u = 0; u < KPT; ++u) {
     const int i = min(i0 + u * kScoreThreads, n - 1);    // keys past n are computed but never stored
     c[u] = __builtin_nontemporal_load(codes + kbase + i);
     if (!INTS) fg[u] = __builtin_nontemporal_load(kfac + kbase + i);
   }
+  if (threadIdx.x < 4 * G) {                  // one lane per (head, word)
+    const int h = threadIdx.x >> 2, w = threadIdx.x & 3;
+    const uint32_t* Q = qplanes + int64_t(row0 + h) * 16 + w;   // [plane][word]
+    uint32_t o[4];
+    planes_to_nibbles(Q[0], Q[4], Q[8], Q[12], o);
+    *reinterpret_cast<u32x4*>(&qn_s[h][4 * w]) = u32x4{o[0], o[1], o[2], o[3]};
+  }
+  int pcm[KPT];   // 2 popcount(code) - D, exact
+  Spread e[KPT];
 #pragma unroll
   for (int u = 0; u < KPT; ++u) {
     const int pc = __popc(c[u].x) + __popc(c[u].y) + __popc(c[u].z) + __popc(c[u].w);
     pcm[u] = 2 * pc - kHeadDim;
+    e[u] = spread_code(c[u]);
     if (INTS) {
       const int i = i0 + u * kScoreThreads;
       if (i < n) pc_out[int64_t(bh) * n + i] = pc;
     }
   }
+  __syncthreads();
 
-  const int row0 = b * Hq + hk * G;
   if (full && !INTS) {
     for (int g = 0; g < G; ++g) {
       const int row = row0 + g;
-      const uint32_t* Q = qplanes + int64_t(row) * 16;
-      uint32_t qp[16];
+      uint32_t qn[16];
 #pragma unroll
-      for (int t = 0; t < 16; ++t) qp[t] = Q[t];
+      for (int t = 0; t < 4; ++t) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(&qn_s[g][4 * t]);
+        qn[4 * t] = v.x; qn[4 * t + 1] = v.y; qn[4 * t + 2] = v.z; qn[4 * t + 3] = v.w;
+      }
       const float* qs = qscal + int64_t(row) * RBQ_QSCAL_STRIDE;
       const float ql = qs[0], delta = qs[1], A = qs[3], B0 = qs[4];
       const int su = int(qs[2]);
@@ -94,7 +126,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       float* out = scores + int64_t(row) * n;
 #pragma unroll
       for (int u = 0; u < KPT; ++u) {
-        const int ip = int(binary_int4_dot(c[u], qp));
+        const int ip = int(binary_int4_dot(e[u], qn));
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         __builtin_nontemporal_store(fmaf(fg[u].x, y, B0 + fg[u].y), out + i0 + u * kScoreThreads);
       }
@@ -103,10 +135,9 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   }
   for (int g = 0; g < G; ++g) {
     const int row = row0 + g;
-    const uint32_t* Q = qplanes + int64_t(row) * 16;   // [plane][word]
-    uint32_t qp[16];
+    uint32_t qn[16];
 #pragma unroll
-    for (int t = 0; t < 16; ++t) qp[t] = Q[t];
+    for (int t = 0; t < 16; ++t) qn[t] = qn_s[g][t];
     const float* qs = qscal + int64_t(row) * RBQ_QSCAL_STRIDE;
     const float ql = qs[0], delta = qs[1], A = qs[3], B0 = qs[4];
     const int su = int(qs[2]);
@@ -115,7 +146,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
 #pragma unroll
     for (int u = 0; u < KPT; ++u) {
       const int i = i0 + u * kScoreThreads;
-      const int ip = int(binary_int4_dot(c[u], qp));
+      const int ip = int(binary_int4_dot(e[u], qn));
       if (INTS) {
         if (i < n) ip_out[int64_t(row) * n + i] = ip;
       } else {
