@@ -65,6 +65,7 @@ typedef enum rbq_dtype { RBQ_F32 = 0, RBQ_BF16 = 1 } rbq_dtype;
 #define RBQ_OP_TOPP 2
 #define RBQ_OP_SPARSE_DECODE 3
 #define RBQ_OP_DENSE_DECODE 4
+#define RBQ_OP_DECODE_STEP 5
 
 #define RBQ_QSCAL_STRIDE 8   /* floats per query head in qscal */
 #define RBQ_MAX_WINDOW 4096  /* largest local window accepted by the decode calls */
@@ -186,6 +187,38 @@ rbq_status rbq_dense_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, in
                             int32_t cap, int32_t n, const void* K_loc, const void* V_loc,
                             int64_t loc_ld, int32_t w, float sm_scale, float* out, float* lse,
                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * rbq_decode_step -- one decode step of Algorithm 2 (steps 1 to 4) followed by
+ * the lazy index update of Section 3.4, in one call. The local window is the
+ * tail of the cache: rows [n, n + w) of K and V (n + w <= cap). The outputs
+ * are bitwise identical to those of the sequence
+ *   rbq_quantize_query(B, Hq, Hkv, D, q, P, c_q, c_k, qplanes, qscal)
+ *   rbq_score(B, Hq, Hkv, D, n, cap, codes, kfac, qplanes, qscal, scores)
+ *   rbq_topp_select(B, Hq, n, scores, p, sm_scale, sel_idx, sel_count)
+ *   rbq_sparse_decode(B, Hq, Hkv, D, q, K, V, kv_dtype, cap, n, sel_idx, sel_count,
+ *                     K + n*D, V + n*D, cap, w, sm_scale, out, lse)
+ *   if (flush) rbq_encode_keys(B, Hkv, D, K + n*D, kv_dtype, cap, w, n, cap,
+ *                              P, c_q, c_k, codes, kfac, 0, NULL)
+ * (K + n*D: row n of every (b, kv-head) block, rows `cap` apart), with fewer
+ * launches: the query quantisation and the window encode share one launch
+ * (the encode writes index rows [n, n + w), which nothing else in the step
+ * reads); the score pass also writes per-block maxima of every query head
+ * and clears the selection's counters, so the selection starts from the
+ * histogram; the selection also writes per-head bitmaps of the selected keys,
+ * from which the sparse attention builds its row lists without searching
+ * sel_idx. Every argument means what it means in those calls; qplanes, qscal,
+ * scores, sel_idx and sel_count are written as they would be.
+ *   flush: nonzero to run the window encode (codes / kfac rows [n, n + w)).
+ *   ws: at least rbq_workspace_bytes(RBQ_OP_DECODE_STEP, B, Hq, Hkv, D, n, w) bytes.
+ */
+rbq_status rbq_decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                           const float* q, const float* P, const float* c_q, const float* c_k,
+                           const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n,
+                           int32_t w, uint32_t* codes, float* kfac, int32_t flush, float p,
+                           float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
+                           int32_t* sel_idx, int32_t* sel_count, float* out, float* lse,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Workspace bytes needed by `op` (one of RBQ_OP_*) for these sizes; 0 for an
  * unknown op or invalid sizes. Host-only, never touches the device. */

@@ -91,4 +91,50 @@ rbq_status rbq_dense_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, in
                        sm_scale, out, lse, ws, false, stream);
 }
 
+rbq_status rbq_decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                           const float* P, const float* c_q, const float* c_k, const void* K, const void* V,
+                           int32_t kv_dtype, int32_t cap, int32_t n, int32_t w, uint32_t* codes, float* kfac,
+                           int32_t flush, float p, float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
+                           int32_t* sel_idx, int32_t* sel_count, float* out, float* lse, void* ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
+  if (s != RBQ_OK) return s;
+  if (n < 0 || w < 0 || cap < 0 || int64_t(n) + w > cap) return RBQ_EINVAL;
+  const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
+  if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
+  const size_t elem = kv_dtype == RBQ_BF16 ? 2 : 4;
+  const void* K_loc = K ? static_cast<const char*>(K) + size_t(n) * head_dim * elem : nullptr;
+  const void* V_loc = V ? static_cast<const char*>(V) + size_t(n) * head_dim * elem : nullptr;
+  const size_t dec_bytes = decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w);
+  const bool do_flush = flush != 0 && w > 0;
+  if ((s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal)) != RBQ_OK) return s;
+  if ((s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores)) != RBQ_OK)
+    return s;
+  if ((s = check_topp(batch, heads_q, n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, sw.topp_bytes)) != RBQ_OK)
+    return s;
+  if ((s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, true, sel_idx, sel_count,
+                        K_loc, V_loc, cap, w, sm_scale, out, sw.decode, dec_bytes)) != RBQ_OK)
+    return s;
+  if (do_flush && (s = check_encode(batch, heads_kv, head_dim, K_loc, kv_dtype, cap, w, n, cap, P, c_k, codes, kfac,
+                                    0u, nullptr, 0)) != RBQ_OK)
+    return s;
+
+  const int64_t rows = int64_t(batch) * heads_q;
+  if (do_flush)
+    s = launch_quantize_flush(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, K_loc, kv_dtype, cap, w, n,
+                              cap, codes, kfac, stream);
+  else
+    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
+  if (s != RBQ_OK) return s;
+  const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
+  s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
+                   sw.slot_max, tw.hist, rows * kHistPerRow);
+  if (s != RBQ_OK) return s;
+  s = launch_topp(int32_t(rows), n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
+                  score_blocks_per_row(batch, heads_kv, n), sw.masks);
+  if (s != RBQ_OK) return s;
+  return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, cap, w,
+                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n));
+}
+
 }  // extern "C"

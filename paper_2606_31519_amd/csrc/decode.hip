@@ -85,12 +85,28 @@ __device__ __forceinline__ void wave_lower_bounds(const int32_t* __restrict__ a,
 // Each wave finds the part [lower bound of c0, lower bound of c1) of its
 // heads' selection lists; the entries are then loaded all at once and marked
 // in per-head LDS bitmaps, and the union is compacted with wave ballots.
+//
+// With selection bitmaps (sel_mask != NULL, [rows][mask_words] words of 64
+// keys, c0 a multiple of 64) the per-head bitmaps are loaded directly instead.
 template <int G, int kThreads>
-__device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count, int row0,
+__device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
+                                const unsigned long long* __restrict__ sel_mask, int mask_words, int row0,
                                 int n, int c0, int c1, uint32_t (*bm)[kBmWords], int32_t* lst, uint16_t* hmask,
                                 int* rng_lo, int* rng_hi, int* wcnt, int* ucount) {
   constexpr int kWaves = kThreads / kWave;
   const int t = threadIdx.x, wave = t / kWave, lane = lane_id();
+  if (sel_mask) {
+    constexpr int kMw = kBmWords / 2;   // 64-key words per split
+    static_assert(G * kMw <= kThreads, "one word per thread");
+    if (t < G * kMw) {
+      const int g = t / kMw, wd = t % kMw;
+      const unsigned long long v =
+          c0 + 64 * wd < c1 ? sel_mask[int64_t(row0 + g) * mask_words + c0 / 64 + wd] : 0ull;
+      bm[g][2 * wd] = uint32_t(v);
+      bm[g][2 * wd + 1] = uint32_t(v >> 32);
+    }
+    __syncthreads();
+  } else {
   for (int g = wave; g < G; g += kWaves) {
     const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
     const int cnt = min(max(sel_count[row0 + g], 0), n);
@@ -129,6 +145,7 @@ __device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32
       }
   }
   __syncthreads();
+  }
   // union of the G bitmaps, compacted in ascending position order: position
   // r * kThreads + t in round r, ranked by wave ballots
   constexpr int kRounds = kDecodeChunk / kThreads;
@@ -228,7 +245,8 @@ __device__ __forceinline__ f32x2 load_v2(const void* rowp, int lane) {
 template <int DT, bool SPARSE, int G>
 __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     const float* __restrict__ q, const void* __restrict__ K, const void* __restrict__ V, int cap, int n,
-    const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count, const void* __restrict__ K_loc,
+    const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
+    const unsigned long long* __restrict__ sel_mask, int mask_words, const void* __restrict__ K_loc,
     const void* __restrict__ V_loc, int64_t loc_ld, int w, int chunk, int idx_splits, int total_splits,
     float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
   constexpr int kElem = DT == RBQ_BF16 ? 2 : 4;
@@ -269,7 +287,7 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   const bool use_list = SPARSE && !window;
   int U;
   if (use_list) {
-    U = build_union_list<G, kDThreads>(sel_idx, sel_count, row0, n, c0, c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
+    U = build_union_list<G, kDThreads>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
                                        &ucount);
   } else {
     __syncthreads();
@@ -446,7 +464,8 @@ __device__ __forceinline__ void load_group_v(GroupLoads& d, int grp, bool skip, 
 template <bool SPARSE, int G>
 __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     const float* __restrict__ q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V, int cap, int n,
-    const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count, const uint16_t* __restrict__ K_loc,
+    const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
+    const unsigned long long* __restrict__ sel_mask, int mask_words, const uint16_t* __restrict__ K_loc,
     const uint16_t* __restrict__ V_loc, int64_t loc_ld, int w, int chunk, int idx_splits, int total_splits,
     float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
   static_assert(G >= 1 && G <= 16, "the MFMA tiles hold at most 16 heads");
@@ -510,7 +529,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
 
   int U;
   if (SPARSE && !window) {
-    U = build_union_list<G, kDThreads>(sel_idx, sel_count, row0, n, c0, c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
+    U = build_union_list<G, kDThreads>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
                                        &ucount);
   } else {
     __syncthreads();
@@ -727,20 +746,20 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(const floa
 
 template <int DT, bool SPARSE>
 rbq_status launch_g(int G, dim3 grid, hipStream_t stream, const float* q, const void* K, const void* V, int cap,
-                    int n, const int32_t* sel_idx, const int32_t* sel_count, const void* K_loc, const void* V_loc,
-                    int64_t loc_ld, int w, int chunk, int idx_splits, int total, float scale_log2e, float* part,
-                    int Hq, int Hkv) {
-#define RBQ_DECODE_CASE(GG)                                                                                    \
-  case GG:                                                                                                     \
-    if (DT == RBQ_BF16)                                                                                        \
-      decode_mfma_kernel<SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                          \
-          q, static_cast<const uint16_t*>(K), static_cast<const uint16_t*>(V), cap, n, sel_idx, sel_count,     \
-          static_cast<const uint16_t*>(K_loc), static_cast<const uint16_t*>(V_loc), loc_ld, w, chunk,          \
-          idx_splits, total, scale_log2e, part, Hq, Hkv);                                                      \
-    else                                                                                                       \
-      decode_vec_kernel<DT, SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                       \
-          q, K, V, cap, n, sel_idx, sel_count, K_loc, V_loc, loc_ld, w, chunk, idx_splits, total, scale_log2e, \
-          part, Hq, Hkv);                                                                                      \
+                    int n, const int32_t* sel_idx, const int32_t* sel_count, const unsigned long long* sel_mask,
+                    int mask_words, const void* K_loc, const void* V_loc, int64_t loc_ld, int w, int chunk,
+                    int idx_splits, int total, float scale_log2e, float* part, int Hq, int Hkv) {
+#define RBQ_DECODE_CASE(GG)                                                                                       \
+  case GG:                                                                                                        \
+    if (DT == RBQ_BF16)                                                                                           \
+      decode_mfma_kernel<SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                             \
+          q, static_cast<const uint16_t*>(K), static_cast<const uint16_t*>(V), cap, n, sel_idx, sel_count,        \
+          sel_mask, mask_words, static_cast<const uint16_t*>(K_loc), static_cast<const uint16_t*>(V_loc), loc_ld, \
+          w, chunk, idx_splits, total, scale_log2e, part, Hq, Hkv);                                               \
+    else                                                                                                          \
+      decode_vec_kernel<DT, SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                          \
+          q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, loc_ld, w, chunk, idx_splits,  \
+          total, scale_log2e, part, Hq, Hkv);                                                                     \
     break;
   switch (G) {
     RBQ_DECODE_CASE(1)
@@ -760,28 +779,22 @@ rbq_status launch_g(int G, dim3 grid, hipStream_t stream, const float* q, const 
 rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const void* K,
                          const void* V, int32_t kv_dtype, int32_t cap, int32_t n, const int32_t* sel_idx,
                          const int32_t* sel_count, const void* K_loc, const void* V_loc, int64_t loc_ld, int32_t w,
-                         float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream) {
+                         float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream,
+                         const unsigned long long* sel_mask, int32_t mask_words) {
   const int G = heads_q / heads_kv;
   const DecodeSplits sp = decode_splits(batch, heads_kv, n, w);
   const dim3 grid(sp.total(), batch * heads_kv);
   float* part = static_cast<float*>(ws);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
   rbq_status st;
-  if (kv_dtype == RBQ_BF16) {
-    st = sparse ? launch_g<RBQ_BF16, true>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, K_loc, V_loc,
-                                           loc_ld, w, sp.chunk, sp.idx_splits, sp.total(), scale_log2e, part,
-                                           heads_q, heads_kv)
-                : launch_g<RBQ_BF16, false>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, K_loc, V_loc,
-                                            loc_ld, w, sp.chunk, sp.idx_splits, sp.total(), scale_log2e, part,
-                                            heads_q, heads_kv);
-  } else {
-    st = sparse ? launch_g<RBQ_F32, true>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, K_loc, V_loc,
-                                          loc_ld, w, sp.chunk, sp.idx_splits, sp.total(), scale_log2e, part,
-                                          heads_q, heads_kv)
-                : launch_g<RBQ_F32, false>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, K_loc, V_loc,
-                                           loc_ld, w, sp.chunk, sp.idx_splits, sp.total(), scale_log2e, part,
-                                           heads_q, heads_kv);
-  }
+#define RBQ_DECODE_LAUNCH(DT, SP)                                                                                  \
+  launch_g<DT, SP>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, loc_ld, \
+                   w, sp.chunk, sp.idx_splits, sp.total(), scale_log2e, part, heads_q, heads_kv)
+  if (kv_dtype == RBQ_BF16)
+    st = sparse ? RBQ_DECODE_LAUNCH(RBQ_BF16, true) : RBQ_DECODE_LAUNCH(RBQ_BF16, false);
+  else
+    st = sparse ? RBQ_DECODE_LAUNCH(RBQ_F32, true) : RBQ_DECODE_LAUNCH(RBQ_F32, false);
+#undef RBQ_DECODE_LAUNCH
   if (st != RBQ_OK) return st;
   decode_combine_kernel<<<dim3(batch * heads_q, kCombSlices), kCombThreads, 0, stream>>>(part, sp.total(), out,
                                                                                            lse);

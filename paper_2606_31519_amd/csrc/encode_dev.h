@@ -1,0 +1,191 @@
+// The tile encoder of rbq_encode_keys (Algorithm 1; Section 3.2; Appendix A.2),
+// shared by the standalone encode kernel and the fused decode step.
+#pragma once
+
+#include "rbq_device.h"
+#include "rbq_internal.h"
+
+namespace rbq {
+
+constexpr int kEncWaves = 4;
+constexpr int kEncThreads = kEncWaves * kWave;
+constexpr int kXStride = kHeadDim + 1;        // padded LDS row of a staged key
+
+// ---------------------------------------------------------------- encode
+// A block of 4 waves loops over tiles of 32 keys. The tile's centred keys are
+// staged once in LDS; wave w rotates them onto output dimensions [32 w, 32 w + 32)
+// with 64 MFMAs in two chains, so all four matrix cores of the CU work on one
+// tile. The wave's columns of P stay in registers across the block's tiles.
+// Keys past n_new are loaded clamped to the last key (their rows of the
+// product are independent of the others and never stored), so no load is
+// conditional and the waits stay exact.
+constexpr int kTileKeys = 32;
+
+struct EncodeArgs {
+  const void* keys;        // blocks of keys_ld rows per (b, kv-head)
+  int64_t keys_ld;
+  int n_new, offset, cap;
+  const float* P;
+  const float* c_q;        // or NULL
+  const float* c_k;
+  uint32_t* codes;
+  float* kfac;
+  float* alpha_out;        // or NULL
+  float* rot_out;          // or NULL
+};
+
+// Blocks per (b, kv-head) of an encode over n_new keys: enough to cover the
+// CUs a few times; each block loops over its tiles.
+inline int encode_blocks_per_head(int n_new, int bhs) {
+  const int tiles = (n_new + kTileKeys - 1) / kTileKeys;
+  const int cap_blocks = 2048 / (bhs > 0 ? bhs : 1);
+  const int b = tiles < cap_blocks ? tiles : cap_blocks;
+  return b > 0 ? b : 1;
+}
+
+// The tiles bx, bx + gx, ... of (b, kv-head) bh, by the 256 threads of the calling block.
+template <int DT, bool ROT>
+__device__ __forceinline__ void encode_tiles(const EncodeArgs& ea, int bh, int bx, int gx) {
+  const void* __restrict__ keys = ea.keys;
+  const int64_t keys_ld = ea.keys_ld;
+  const int n_new = ea.n_new, offset = ea.offset, cap = ea.cap;
+  const float* __restrict__ P = ea.P;
+  const float* __restrict__ c_q = ea.c_q;
+  const float* __restrict__ c_k = ea.c_k;
+  uint32_t* __restrict__ codes = ea.codes;
+  float* __restrict__ kfac = ea.kfac;
+  float* __restrict__ alpha_out = ea.alpha_out;
+  float* __restrict__ rot_out = ea.rot_out;
+  __shared__ float Xs[kTileKeys * kXStride];                                // the tile's centred keys
+  __shared__ float ck_s[kHeadDim], cq_s[kHeadDim];
+  __shared__ uint32_t code_s[kTileKeys][kWords];
+  __shared__ float abs_s[kEncWaves][kTileKeys];
+  __shared__ float ng_s[2][kTileKeys];
+
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int lane = lane_id();
+  const int mk = lane % 32, half = lane / 32;
+
+  // the tile's keys in 16-byte pieces, consecutive threads on consecutive pieces;
+  // the first tile is requested before P is staged, each next one during the current tile
+  constexpr int kElemBytes = DT == RBQ_BF16 ? 2 : 4;
+  constexpr int kPiecesPerRow = kHeadDim * kElemBytes / 16;            // 16 (bf16) or 32 (fp32)
+  constexpr int kPer = kTileKeys * kPiecesPerRow / kEncThreads;         // 2 or 4 per thread
+  const int tiles = (n_new + kTileKeys - 1) / kTileKeys;
+  u32x4 pc[kPer];
+  auto load_tile = [&](int tl) {
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int pidx = j * kEncThreads + threadIdx.x;
+      const int row = pidx / kPiecesPerRow, piece = pidx % kPiecesPerRow;
+      const int key = min(tl * kTileKeys + row, n_new - 1);
+      pc[j] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(keys) +
+                                              ((int64_t(bh) * keys_ld + key) * kHeadDim) * kElemBytes + piece * 16);
+    }
+  };
+  if (bx < tiles) load_tile(bx);
+
+  // B operands of this wave: pb[i] = P[2 i + half][32 wave + mk]
+  float pb[kHeadDim / 2];
+#pragma unroll
+  for (int i = 0; i < kHeadDim / 2; ++i) pb[i] = P[(2 * i + half) * kHeadDim + 32 * wave + mk];
+  if (threadIdx.x < kHeadDim) {
+    ck_s[threadIdx.x] = c_k[int64_t(bh) * kHeadDim + threadIdx.x];
+    cq_s[threadIdx.x] = c_q ? c_q[int64_t(bh) * kHeadDim + threadIdx.x] : 0.f;
+  }
+  __syncthreads();
+
+  for (int tile = bx; tile < tiles; tile += gx) {
+    const int key0 = tile * kTileKeys;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int pidx = j * kEncThreads + threadIdx.x;
+      const int row = pidx / kPiecesPerRow, piece = pidx % kPiecesPerRow;
+      float* xr = Xs + row * kXStride;
+      if (DT == RBQ_BF16) {
+        const int d = piece * 8;
+        const uint32_t wv[4] = {pc[j].x, pc[j].y, pc[j].z, pc[j].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          xr[d + 2 * e] = bf16_lo(wv[e]) - ck_s[d + 2 * e];
+          xr[d + 2 * e + 1] = bf16_hi(wv[e]) - ck_s[d + 2 * e + 1];
+        }
+      } else {
+        const int d = piece * 4;
+        xr[d] = __uint_as_float(pc[j].x) - ck_s[d];
+        xr[d + 1] = __uint_as_float(pc[j].y) - ck_s[d + 1];
+        xr[d + 2] = __uint_as_float(pc[j].z) - ck_s[d + 2];
+        xr[d + 3] = __uint_as_float(pc[j].w) - ck_s[d + 3];
+      }
+    }
+    if (tile + gx < tiles) load_tile(tile + gx);   // lands while this tile is rotated
+    __syncthreads();
+
+    // ---- ||x||^2 and <c_q, x>: threads 0..127, key t / 4, a quarter of the dims each
+    if (threadIdx.x < 4 * kTileKeys) {
+      const int kk = threadIdx.x / 4, qd = threadIdx.x % 4;
+      float nn = 0.f, gg = 0.f;
+#pragma unroll 8
+      for (int d = qd * 32; d < qd * 32 + 32; ++d) {
+        const float x = Xs[kk * kXStride + d];
+        nn = fmaf(x, x, nn);
+        gg = fmaf(cq_s[d], x, gg);
+      }
+      nn += RBQ_DPP(nn, 0xB1);
+      nn += RBQ_DPP(nn, 0x4E);
+      gg += RBQ_DPP(gg, 0xB1);
+      gg += RBQ_DPP(gg, 0x4E);
+      if (qd == 0) {
+        ng_s[0][kk] = nn;
+        ng_s[1][kk] = gg;
+      }
+    }
+
+    // ---- r = x P for output dimensions [32 wave, 32 wave + 32): A = X rows, B = P rows
+    f32x16 acc = f32x16{0.f}, acc2 = f32x16{0.f};   // two chains over alternate k-steps, added at the end
+#pragma unroll
+    for (int s2 = 0; s2 < kHeadDim / 2; s2 += 2) {
+      const int k = 2 * s2 + half;
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(Xs[mk * kXStride + k], pb[s2], acc, 0, 0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x2f32(Xs[mk * kXStride + k + 2], pb[s2 + 1], acc2, 0, 0, 0);
+    }
+    acc += acc2;
+    // acc[r] at lane l: key 8 (r / 4) + 4 (l / 32) + r % 4, dimension 32 wave + l % 32
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float v = acc[r];
+      const uint64_t bal = __ballot(v > 0.f);
+      const float a = sum32(fabsf(v));
+      const int key_a = 8 * (r / 4) + (r % 4);
+      if (lane == 0) {
+        code_s[key_a][wave] = uint32_t(bal);
+        code_s[key_a + 4][wave] = uint32_t(bal >> 32);
+        abs_s[wave][key_a] = a;
+      }
+      if (lane == 32) abs_s[wave][key_a + 4] = a;
+      if (ROT) {
+        const int key = key0 + key_a + 4 * half;
+        if (key < n_new) rot_out[(int64_t(bh) * n_new + key) * kHeadDim + 32 * wave + mk] = v;
+      }
+    }
+    __syncthreads();
+
+    if (threadIdx.x < kTileKeys) {
+      const int t = threadIdx.x;
+      const int key = key0 + t;
+      const float absum = (abs_s[0][t] + abs_s[1][t]) + (abs_s[2][t] + abs_s[3][t]);
+      const float nrm = sqrtf(ng_s[0][t]);
+      const float alpha_p = nrm > 0.f ? absum / nrm : 0.f;
+      const float f = alpha_p > 0.f ? nrm / alpha_p : 0.f;
+      if (key < n_new) {
+        const int64_t o = int64_t(bh) * cap + offset + key;
+        *reinterpret_cast<u32x4*>(codes + o * kWords) = u32x4{code_s[t][0], code_s[t][1], code_s[t][2], code_s[t][3]};
+        *reinterpret_cast<f32x2*>(kfac + o * 2) = f32x2{f, ng_s[1][t]};
+        if (alpha_out) alpha_out[int64_t(bh) * n_new + key] = alpha_p * 0.08838834764831845f;   // 1/sqrt(128)
+      }
+    }
+    __syncthreads();   // the tile buffers are refilled next
+  }
+}
+
+}  // namespace rbq

@@ -1,7 +1,7 @@
 // rbq_quantize_query: query pre-processing and INT4 quantisation
 // (Algorithm 2 step 1; Section 3.3 "Query Quantization"; Appendix A.3.2).
 //
-// One block per query head; 4 x 128 threads share the 128 x 128 product (all
+// One block per query head; 2 x 128 threads share the 128 x 128 product (all
 // loads of a thread in flight at once), then 128 threads, one per dimension:
 //   y = q - c_q, A = ||y||, u = y / A, q'[j] = sum_d P[d][j] u[d]   (q' = P^T u)
 //   q_l = min q', q_r = max q', Delta = (q_r - q_l) / 15,
@@ -11,6 +11,7 @@
 // decision exactly from the same q'. Bit-plane j of the codes is one wave
 // ballot per 64 dimensions. The cost is one 128 x 128 matrix-vector product
 // per head, amortised over all keys (Section 3.1).
+#include "encode_dev.h"
 #include "rbq_device.h"
 #include "rbq_internal.h"
 
@@ -19,7 +20,7 @@ namespace {
 
 constexpr int kQThreads = kHeadDim;   // one thread per output dimension in the epilogue
 constexpr int kQWaves = kQThreads / kWave;
-constexpr int kQParts = 4;            // the matrix-vector product is split over 4 thread groups
+constexpr int kQParts = 2;            // the matrix-vector product is split over 2 thread groups
 constexpr int kQAll = kQParts * kQThreads;
 
 // reductions over the first kQWaves waves (the other waves take part in the barriers only)
@@ -82,23 +83,37 @@ __device__ __forceinline__ int quant_code(float x, float ql, float delta) {
   return int(r);
 }
 
-__global__ __launch_bounds__(kQAll) void quantize_kernel(const float* __restrict__ q, const float* __restrict__ P,
-                                                             const float* __restrict__ c_q,
-                                                             const float* __restrict__ c_k,
-                                                             uint32_t* __restrict__ qplanes,
-                                                             float* __restrict__ qscal, float* __restrict__ qrot_out,
-                                                             int Hq, int Hkv) {
+struct QuantArgs {
+  const float* q;
+  const float* P;
+  const float* c_q;      // or NULL
+  const float* c_k;
+  uint32_t* qplanes;
+  float* qscal;
+  float* qrot_out;       // or NULL
+  int Hq, Hkv;
+};
+
+// query head `row` (= b * Hq + h), by the kQAll threads of the calling block
+__device__ __forceinline__ void quantize_row(const QuantArgs& qa, int row) {
+  const float* __restrict__ q = qa.q;
+  const float* __restrict__ P = qa.P;
+  const float* __restrict__ c_q = qa.c_q;
+  const float* __restrict__ c_k = qa.c_k;
+  uint32_t* __restrict__ qplanes = qa.qplanes;
+  float* __restrict__ qscal = qa.qscal;
+  float* __restrict__ qrot_out = qa.qrot_out;
+  const int Hq = qa.Hq, Hkv = qa.Hkv;
   __shared__ float u_s[kHeadDim];
   __shared__ float part_s[kQParts][kHeadDim];
   __shared__ float red[2 * (kQAll / kWave) + 2 * kQWaves];
-  const int row = blockIdx.x;                  // b * Hq + h
   const int b = row / Hq;
   const int h = row - b * Hq;
   const int grp = b * Hkv + h / (Hq / Hkv);    // (b, kv head)
   const int j = threadIdx.x % kHeadDim;        // output dimension
   const int part = threadIdx.x / kHeadDim;     // which quarter of the input dimensions
 
-  // this group's 32 rows of P, requested before anything else (they do not depend on q)
+  // this group's 64 rows of P, requested before anything else (they do not depend on q)
   constexpr int kRows = kHeadDim / kQParts;
   float pv[kRows];
 #pragma unroll
@@ -117,14 +132,14 @@ __global__ __launch_bounds__(kQAll) void quantize_kernel(const float* __restrict
   if (part == 0) u_s[j] = A > 0.f ? y / A : 0.f;
   __syncthreads();
 
-  // q'[j] = sum_d P[d][j] u[d]: each group takes 32 rows of P (loaded above)
+  // q'[j] = sum_d P[d][j] u[d]: each group takes 64 rows of P (loaded above)
   float acc = 0.f;
 #pragma unroll
   for (int k = 0; k < kRows; ++k) acc = fmaf(pv[k], u_s[part * kRows + k], acc);
   part_s[part][j] = acc;
   __syncthreads();
   // every thread computes the sum; only the first 128 (two waves) use it
-  acc = (part_s[0][j] + part_s[1][j]) + (part_s[2][j] + part_s[3][j]);
+  acc = part_s[0][j] + part_s[1][j];
   const bool lead = part == 0;
   if (qrot_out && lead) qrot_out[int64_t(row) * kHeadDim + j] = acc;
 
@@ -161,13 +176,48 @@ __global__ __launch_bounds__(kQAll) void quantize_kernel(const float* __restrict
   }
 }
 
+__global__ __launch_bounds__(kQAll) void quantize_kernel(QuantArgs qa) { quantize_row(qa, blockIdx.x); }
+
+// One launch for the query quantisation and the lazy index update of the
+// decode step (they are independent): blocks [0, rows) quantise one query
+// head each, the others encode the window keys as encode_kernel would.
+static_assert(kQAll == kEncThreads, "both roles run on blocks of the same size");
+template <int DT>
+__global__ __launch_bounds__(kQAll) void quantize_flush_kernel(QuantArgs qa, EncodeArgs ea, int rows, int per_head) {
+  const int blk = blockIdx.x;
+  if (blk < rows) {
+    quantize_row(qa, blk);
+  } else {
+    const int e = blk - rows;
+    encode_tiles<DT, false>(ea, e / per_head, e % per_head, per_head);
+  }
+}
+
 }  // namespace
 
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
                            hipStream_t stream) {
-  quantize_kernel<<<batch * heads_q, kQAll, 0, stream>>>(q, P, c_q, c_k, qplanes, qscal, qrot_out, heads_q,
-                                                             heads_kv);
+  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, qrot_out, heads_q, heads_kv};
+  quantize_kernel<<<batch * heads_q, kQAll, 0, stream>>>(qa);
+  return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
+}
+
+rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
+                                 const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal,
+                                 const void* keys, int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset,
+                                 int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream) {
+  if (n_new == 0)
+    return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
+  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, nullptr, heads_q, heads_kv};
+  const EncodeArgs ea{keys, keys_ld, n_new, offset, cap, P, c_q, c_k, codes, kfac, nullptr, nullptr};
+  const int rows = batch * heads_q, bhs = batch * heads_kv;
+  const int per_head = encode_blocks_per_head(n_new, bhs);
+  const int blocks = rows + per_head * bhs;
+  if (keys_dtype == RBQ_BF16)
+    quantize_flush_kernel<RBQ_BF16><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+  else
+    quantize_flush_kernel<RBQ_F32><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

@@ -68,6 +68,24 @@ DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w
 size_t decode_workspace_bytes(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
                               int32_t w);
 
+// Score: blocks of kScoreThreads lanes, 1, 2 or 4 keys per lane.
+constexpr int kScoreThreads = 256;
+int score_keys_per_lane(int32_t batch, int32_t heads_kv, int32_t n);
+int score_blocks_per_row(int32_t batch, int32_t heads_kv, int32_t n);
+int topp_mask_words(int32_t n);   // 64-key words of a row's selection bitmap
+
+// Fused decode step: the workspaces of its stages side by side.
+struct StepWorkspace {
+  void* decode;                     // decode_workspace_bytes()
+  void* topp;                       // topp_workspace().bytes
+  float* slot_max;                  // [B * Hq][score_blocks_per_row()]
+  unsigned long long* masks;        // [B * Hq][topp_mask_words(n)]
+  size_t topp_bytes;
+  size_t bytes;
+};
+StepWorkspace step_workspace(void* base, int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                             int32_t n, int32_t w);
+
 // Encode: centroid partial sums over chunks of kCentroidChunk keys.
 constexpr int kCentroidChunk = 1024;
 size_t encode_workspace_bytes(int32_t batch, int32_t heads_kv, int32_t head_dim, int32_t n_new);
@@ -82,14 +100,28 @@ rbq_status launch_encode(int32_t batch, int32_t heads_kv, const void* keys, int3
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
                            hipStream_t stream);
+// query quantisation and, in the same launch, the lazy encode of n_new window
+// keys into index rows [offset, offset + n_new) with the existing c_k
+rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
+                                 const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal,
+                                 const void* keys, int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset,
+                                 int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream);
+// slot_max (fused decode step): [B * Hq][score_blocks_per_row()] block maxima of the
+// scores, with hist[0, hist_words) zeroed by the same launch; NULL otherwise
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
-                        float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream);
+                        float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream,
+                        float* slot_max = nullptr, unsigned long long* hist = nullptr, int64_t hist_words = 0);
+// slot_max / nslots: per-row partial maxima written by launch_score together with
+// the zeroing of the workspace's counters (the max pass is skipped); masks:
+// optional [rows][topp_mask_words(n)] selection bitmaps (bit i of word k = key 64 k + i)
 rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,
-                       int32_t* sel_count, void* ws, hipStream_t stream);
+                       int32_t* sel_count, void* ws, hipStream_t stream, const float* slot_max = nullptr,
+                       int32_t nslots = 0, unsigned long long* masks = nullptr);
 rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const void* K,
                          const void* V, int32_t kv_dtype, int32_t cap, int32_t n, const int32_t* sel_idx,
                          const int32_t* sel_count, const void* K_loc, const void* V_loc, int64_t loc_ld, int32_t w,
-                         float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream);
+                         float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream,
+                         const unsigned long long* sel_mask = nullptr, int32_t mask_words = 0);
 
 }  // namespace rbq

@@ -28,7 +28,6 @@
 namespace rbq {
 namespace {
 
-constexpr int kScoreThreads = 256;
 constexpr int kMaxGroup = 16;   // query heads per KV head handled by the kernels
 
 // Nibble-packed query: word 4 w + s holds, in nibble k, the 4-bit value of
@@ -67,12 +66,33 @@ __device__ __forceinline__ uint32_t binary_int4_dot(const Spread& e, const uint3
   return a + b;
 }
 
-template <int KPT, bool INTS>
+// block maximum of each of the G heads from the per-wave maxima
+__device__ __forceinline__ void write_slots(float (*mx_s)[kScoreThreads / kWave], int row0, int G, float* slot_max) {
+  __syncthreads();
+  if (int(threadIdx.x) < G) {
+    float m = mx_s[threadIdx.x][0];
+#pragma unroll
+    for (int w = 1; w < kScoreThreads / kWave; ++w) m = fmaxf(m, mx_s[threadIdx.x][w]);
+    slot_max[int64_t(row0 + threadIdx.x) * gridDim.x + blockIdx.x] = m;
+  }
+}
+
+// Extra outputs of the fused decode step: the maximum score of every (query
+// head, block) in slot_max[row][blockIdx.x], and the zeroing of the Top-p
+// histogram counters that the selection accumulates into next.
+struct ScoreSlots {
+  float* slot_max;                 // [B * Hq][gridDim.x] or NULL
+  unsigned long long* hist;        // counters to zero
+  int64_t hist_words;
+};
+
+template <int KPT, bool INTS, bool SLOTS>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const u32x4* __restrict__ codes, const f32x2* __restrict__ kfac, const uint32_t* __restrict__ qplanes,
     const float* __restrict__ qscal, float* __restrict__ scores, int32_t* __restrict__ ip_out,
-    int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G) {
+    int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl) {
   __shared__ uint32_t qn_s[kMaxGroup][16];
+  __shared__ float mx_s[SLOTS ? kMaxGroup : 1][kScoreThreads / kWave];
   const int bh = blockIdx.y;                 // b * Hkv + kv head
   const int b = bh / Hkv;
   const int hk = bh - b * Hkv;
@@ -88,6 +108,12 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const int i = min(i0 + u * kScoreThreads, n - 1);    // keys past n are computed but never stored
     c[u] = __builtin_nontemporal_load(codes + kbase + i);
     if (!INTS) fg[u] = __builtin_nontemporal_load(kfac + kbase + i);
+  }
+  if (SLOTS) {   // this block's share of the counters
+    const int64_t nb = int64_t(gridDim.x) * gridDim.y, lb = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
+    const int64_t per = (sl.hist_words + nb - 1) / nb;
+    const int64_t e1 = min(sl.hist_words, (lb + 1) * per);
+    for (int64_t e = lb * per + threadIdx.x; e < e1; e += kScoreThreads) sl.hist[e] = 0ull;
   }
   if (threadIdx.x < 4 * G) {                  // one lane per (head, word)
     const int h = threadIdx.x >> 2, w = threadIdx.x & 3;
@@ -124,13 +150,21 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       const int su = int(qs[2]);
       const float a_delta = A * delta, a_ql = A * ql;
       float* out = scores + int64_t(row) * n;
+      float mx = -INFINITY;
 #pragma unroll
       for (int u = 0; u < KPT; ++u) {
         const int ip = int(binary_int4_dot(e[u], qn));
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
-        __builtin_nontemporal_store(fmaf(fg[u].x, y, B0 + fg[u].y), out + i0 + u * kScoreThreads);
+        const float sc = fmaf(fg[u].x, y, B0 + fg[u].y);
+        if (SLOTS) mx = fmaxf(mx, sc);
+        __builtin_nontemporal_store(sc, out + i0 + u * kScoreThreads);
+      }
+      if (SLOTS) {
+        mx = wave_max(mx);
+        if (lane_id() == 0) mx_s[g][threadIdx.x / kWave] = mx;
       }
     }
+    if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
     return;
   }
   for (int g = 0; g < G; ++g) {
@@ -143,6 +177,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const int su = int(qs[2]);
     const float a_delta = A * delta, a_ql = A * ql;
     float* out = scores + int64_t(row) * n;
+    float mx = -INFINITY;
 #pragma unroll
     for (int u = 0; u < KPT; ++u) {
       const int i = i0 + u * kScoreThreads;
@@ -153,30 +188,38 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         const float sc = fmaf(fg[u].x, y, B0 + fg[u].y);
-        if (i < n) __builtin_nontemporal_store(sc, out + i);
+        if (i < n) {
+          if (SLOTS) mx = fmaxf(mx, sc);
+          __builtin_nontemporal_store(sc, out + i);
+        }
       }
     }
+    if (SLOTS) {
+      mx = wave_max(mx);
+      if (lane_id() == 0) mx_s[g][threadIdx.x / kWave] = mx;
+    }
   }
+  if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
 }
 
-template <bool INTS>
+template <bool INTS, bool SLOTS>
 rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
                       const uint32_t* qplanes, const float* qscal, float* scores, int32_t* ip_out,
-                      int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G) {
+                      int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl) {
   const u32x4* c4 = reinterpret_cast<const u32x4*>(codes);
   const f32x2* f2 = reinterpret_cast<const f32x2*>(kfac);
   switch (kpt) {
     case 4:
-      score_kernel<4, INTS><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out, n,
-                                                               cap, Hq, Hkv, G);
+      score_kernel<4, INTS, SLOTS><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
+                                                                       n, cap, Hq, Hkv, G, sl);
       break;
     case 2:
-      score_kernel<2, INTS><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out, n,
-                                                               cap, Hq, Hkv, G);
+      score_kernel<2, INTS, SLOTS><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
+                                                                       n, cap, Hq, Hkv, G, sl);
       break;
     default:
-      score_kernel<1, INTS><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out, n,
-                                                               cap, Hq, Hkv, G);
+      score_kernel<1, INTS, SLOTS><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
+                                                                       n, cap, Hq, Hkv, G, sl);
       break;
   }
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
@@ -186,22 +229,21 @@ rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* co
 
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
-                        float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream) {
+                        float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, float* slot_max,
+                        unsigned long long* hist, int64_t hist_words) {
   if (n == 0) return RBQ_OK;
   const int G = heads_q / heads_kv;
-  // Keys per lane: enough blocks to cover the 256 CUs several times over,
-  // as many keys in flight per lane as that allows.
-  const int64_t kv_keys = int64_t(batch) * heads_kv * n;
-  int kpt = 1;
-  if (kv_keys >= int64_t(kScoreThreads) * 4 * 2048) kpt = 4;
-  else if (kv_keys >= int64_t(kScoreThreads) * 2 * 1024) kpt = 2;
-  const int per_block = kScoreThreads * kpt;
-  dim3 grid((n + per_block - 1) / per_block, batch * heads_kv);
+  const int kpt = score_keys_per_lane(batch, heads_kv, n);
+  dim3 grid(score_blocks_per_row(batch, heads_kv, n), batch * heads_kv);
+  const ScoreSlots sl{slot_max, hist, hist_words};
   if (ip_out != nullptr)
-    return launch_kpt<true>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap,
-                            heads_q, heads_kv, G);
-  return launch_kpt<false>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap,
-                           heads_q, heads_kv, G);
+    return launch_kpt<true, false>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap,
+                                   heads_q, heads_kv, G, sl);
+  if (slot_max != nullptr)
+    return launch_kpt<false, true>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap,
+                                   heads_q, heads_kv, G, sl);
+  return launch_kpt<false, false>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap,
+                                  heads_q, heads_kv, G, sl);
 }
 
 }  // namespace rbq

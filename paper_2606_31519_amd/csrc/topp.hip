@@ -174,9 +174,9 @@ __device__ __forceinline__ void load_chunk(const float* __restrict__ s, int n, i
 }
 __device__ __forceinline__ bool in_row(int n, int c, int k) { return c * kChunk + k * kT + int(threadIdx.x) < n; }
 
-__device__ __forceinline__ float row_max(const float* __restrict__ chunk_max, int chunks, float* red) {
+__device__ __forceinline__ float row_max(const float* __restrict__ part_max, int nmax, float* red) {
   float m = -INFINITY;
-  for (int k = threadIdx.x; k < chunks; k += kT) m = fmaxf(m, chunk_max[k]);
+  for (int k = threadIdx.x; k < nmax; k += kT) m = fmaxf(m, part_max[k]);
   return block_max(m, red);
 }
 
@@ -199,8 +199,10 @@ __global__ __launch_bounds__(kT) void topp_max_kernel(const float* __restrict__ 
   for (int e = e0 + threadIdx.x; e < e1; e += kT) h[e] = 0;
 }
 
+// The row maximum comes from nmax partial maxima per row: the max kernel's per
+// chunk, or (fused decode step) the score kernel's per block.
 __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict__ scores, int n, int chunks,
-                                                         const float* __restrict__ chunk_max, float scale_log2e,
+                                                         const float* __restrict__ rmax, int nmax, float scale_log2e,
                                                          u64* __restrict__ hist) {
   __shared__ u64 h[kBins1];
   __shared__ float red[kTW];
@@ -208,7 +210,7 @@ __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict
   for (int b = threadIdx.x; b < kBins1; b += kT) h[b] = 0;
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
-  const float m = row_max(chunk_max + int64_t(row) * chunks, chunks, red);   // barriers: h is clear after it
+  const float m = row_max(rmax + int64_t(row) * nmax, nmax, red);   // barriers: h is clear after it
 #pragma unroll
   for (int k = 0; k < kPT; ++k) {
     const u64 ms = fixed_mass(v[k], m, scale_log2e);
@@ -225,7 +227,7 @@ __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict
 // crossing, then histogram the keys inside it.
 template <int LEVEL>
 __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict__ scores, int n, int chunks,
-                                                        const float* __restrict__ chunk_max, float scale_log2e,
+                                                        const float* __restrict__ rmax, int nmax, float scale_log2e,
                                                         float p, u64* __restrict__ hist,
                                                         uint32_t* __restrict__ state,
                                                         int32_t* __restrict__ chunk_cnt) {
@@ -245,7 +247,7 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   const u64 cpre = threadIdx.x < kWave ? coarse[(LEVEL == 2 ? 0 : kCoarse) + threadIdx.x] : 0;
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
-  const float m = row_max(chunk_max + int64_t(row) * chunks, chunks, red);
+  const float m = row_max(rmax + int64_t(row) * nmax, nmax, red);
   uint32_t prefix;
   if (LEVEL == 2) {
     find_crossing_2lvl(rh, cpre, 0, p, &cr);
@@ -312,7 +314,8 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
 __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict__ scores, int n, int chunks,
                                                         const u64* __restrict__ hist, uint32_t* __restrict__ state,
                                                         const int32_t* __restrict__ chunk_cnt,
-                                                        int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_count) {
+                                                        int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_count,
+                                                        u64* __restrict__ masks) {
   __shared__ u64 wtot[kTW];
   __shared__ int red[kTW];
   __shared__ int kcnt[kPT][kTW];
@@ -345,7 +348,11 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
 #pragma unroll
   for (int k = 0; k < kPT; ++k) {
     bal[k] = __ballot(in_row(n, c, k) && score_key(v[k]) >= kstar);
-    if (lane == 0) kcnt[k][wave] = __popcll(bal[k]);
+    if (lane == 0) {
+      kcnt[k][wave] = __popcll(bal[k]);
+      // keys c*kChunk + k*kT + 64 wave + [0, 64) of the row's selection bitmap
+      if (masks) masks[int64_t(row) * chunks * (kChunk / 64) + c * (kChunk / 64) + k * kTW + wave] = bal[k];
+    }
   }
   __syncthreads();
 #pragma unroll
@@ -366,34 +373,49 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
 }
 
 __global__ __launch_bounds__(kT) void topp_all_kernel(int n, int32_t* __restrict__ sel_idx,
-                                                      int32_t* __restrict__ sel_count) {
+                                                      int32_t* __restrict__ sel_count, u64* __restrict__ masks,
+                                                      int mask_words) {
   const int row = blockIdx.y;
   const int i = blockIdx.x * kT + threadIdx.x;
   if (i < n) sel_idx[int64_t(row) * n + i] = i;
   if (blockIdx.x == 0 && threadIdx.x == 0) sel_count[row] = n;
+  if (masks && (i & 63) == 0 && i / 64 < mask_words) {
+    const int left = n - i;   // keys [i, i + 64) that exist
+    masks[int64_t(row) * mask_words + i / 64] = left >= 64 ? ~0ull : left > 0 ? (1ull << left) - 1 : 0ull;
+  }
 }
 
 }  // namespace
 
 rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,
-                       int32_t* sel_count, void* ws, hipStream_t stream) {
+                       int32_t* sel_count, void* ws, hipStream_t stream, const float* slot_max, int32_t nslots,
+                       unsigned long long* masks) {
+  const int mask_words = topp_mask_words(n);
   if (n == 0 || p >= 1.0f) {
     // every key (or none) is selected
-    const dim3 grid(n > 0 ? (n + kT - 1) / kT : 1, rows);
-    topp_all_kernel<<<grid, kT, 0, stream>>>(n, sel_idx, sel_count);
+    const int cover = masks ? mask_words * 64 : n;
+    const dim3 grid(cover > 0 ? (cover + kT - 1) / kT : 1, rows);
+    topp_all_kernel<<<grid, kT, 0, stream>>>(n, sel_idx, sel_count, masks, mask_words);
     return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
   }
   const int chunks = (n + kChunk - 1) / kChunk;
   ToppWorkspace w = topp_workspace(ws, rows, n);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
   const dim3 grid(chunks, rows);
-  topp_max_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, w.hist);
-  topp_level1_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, scale_log2e, w.hist);
-  topp_level_kernel<2><<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, scale_log2e, p, w.hist, w.state,
+  const float* rmax = slot_max;
+  int nmax = nslots;
+  if (slot_max == nullptr) {   // otherwise the score launch has written the maxima and cleared the counters
+    topp_max_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, w.hist);
+    rmax = w.chunk_max;
+    nmax = chunks;
+  }
+  topp_level1_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, w.hist);
+  topp_level_kernel<2><<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, p, w.hist, w.state,
                                                w.chunk_cnt);
-  topp_level_kernel<3><<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, scale_log2e, p, w.hist, w.state,
+  topp_level_kernel<3><<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, p, w.hist, w.state,
                                                w.chunk_cnt);
-  topp_write_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.hist, w.state, w.chunk_cnt, sel_idx, sel_count);
+  topp_write_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.hist, w.state, w.chunk_cnt, sel_idx, sel_count,
+                                             masks);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

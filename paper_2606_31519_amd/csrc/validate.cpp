@@ -140,6 +140,39 @@ rbq_status check_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
   return RBQ_OK;
 }
 
+// Keys per lane of the score kernel: enough blocks to cover the 256 CUs
+// several times over, as many keys in flight per lane as that allows.
+int score_keys_per_lane(int32_t batch, int32_t heads_kv, int32_t n) {
+  const int64_t kv_keys = int64_t(batch) * heads_kv * n;
+  if (kv_keys >= int64_t(kScoreThreads) * 4 * 2048) return 4;
+  if (kv_keys >= int64_t(kScoreThreads) * 2 * 1024) return 2;
+  return 1;
+}
+int score_blocks_per_row(int32_t batch, int32_t heads_kv, int32_t n) {
+  const int per_block = kScoreThreads * score_keys_per_lane(batch, heads_kv, n);
+  return (n + per_block - 1) / per_block;
+}
+int topp_mask_words(int32_t n) { return n > 0 ? (n + kToppChunk - 1) / kToppChunk * (kToppChunk / 64) : 0; }
+
+StepWorkspace step_workspace(void* base, int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                             int32_t n, int32_t w) {
+  StepWorkspace s{};
+  const int64_t rows = int64_t(batch) * heads_q;
+  char* b = static_cast<char*>(base);
+  size_t off = 0;
+  s.decode = b + off;
+  off = align_up(off + decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w), 256);
+  s.topp = b + off;
+  s.topp_bytes = topp_workspace(nullptr, rows, n).bytes;
+  off = align_up(off + s.topp_bytes, 256);
+  s.slot_max = reinterpret_cast<float*>(b + off);
+  off = align_up(off + size_t(rows) * score_blocks_per_row(batch, heads_kv, n) * sizeof(float), 256);
+  s.masks = reinterpret_cast<unsigned long long*>(b + off);
+  off = align_up(off + size_t(rows) * topp_mask_words(n) * sizeof(unsigned long long), 256);
+  s.bytes = off;
+  return s;
+}
+
 }  // namespace rbq
 
 extern "C" {
@@ -155,6 +188,9 @@ size_t rbq_workspace_bytes(int32_t op, int32_t batch, int32_t heads_q, int32_t h
     case RBQ_OP_SPARSE_DECODE:
     case RBQ_OP_DENSE_DECODE:
       return rbq::decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w);
+    case RBQ_OP_DECODE_STEP:
+      if (heads_q % heads_kv != 0) return 0;
+      return rbq::step_workspace(nullptr, batch, heads_q, heads_kv, head_dim, n, w).bytes;
     default:
       return 0;
   }

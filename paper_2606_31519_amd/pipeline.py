@@ -49,6 +49,7 @@ class DecodeState:
         self.ws_encode = rbq.workspace(rbq.RBQ_OP_ENCODE, B, Hq, Hkv, D, max(n, w, 1), 0, device)
         self.ws_topp = rbq.workspace(rbq.RBQ_OP_TOPP, B, Hq, Hkv, D, n, 0, device)
         self.ws_decode = rbq.workspace(rbq.RBQ_OP_SPARSE_DECODE, B, Hq, Hkv, D, n, w, device)
+        self.ws_step = rbq.workspace(rbq.RBQ_OP_DECODE_STEP, B, Hq, Hkv, D, n, w, device)
         self.sm_scale = 1.0 / math.sqrt(D)
 
     @classmethod
@@ -104,11 +105,17 @@ class DecodeState:
                              self.lse if lse is None else lse, self.ws_decode, stream)
 
     def step(self, p, stream=None, flush=True):
-        """One decode step of the whole path: quantize -> score -> Top-p -> sparse
-        attention (index selection + window), then the lazy flush of the window.
-        (The flush writes index rows [n, n + w), which this step's scoring does
-        not read; running it on a second stream was measured slower on MI355X:
-        the fork/join costs more than the flush itself.)"""
+        """One decode step of the whole path with rbq_decode_step: quantize ->
+        score -> Top-p -> sparse attention (index selection + window), and the
+        lazy flush of the window into index rows [n, n + w) (which this step's
+        scoring does not read), in one call with fewer launches."""
+        rbq.rbq_decode_step(self.B, self.Hq, self.Hkv, self.D, self.q, self.P, self.c_q, self.c_k, self.K, self.V,
+                            self.cap, self.n, self.w, self.codes, self.kfac, flush, p, self.sm_scale, self.qplanes,
+                            self.qscal, self.scores, self.sel_idx, self.sel_count, self.out, self.lse, self.ws_step,
+                            stream)
+
+    def step_calls(self, p, stream=None, flush=True):
+        """The same step as the five separate calls (bitwise the same outputs)."""
         self.quantize(stream)
         self.score(stream)
         self.select(p, stream)

@@ -18,12 +18,12 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librbq.so")
 RBQ_OK, RBQ_EINVAL, RBQ_EUNSUPPORTED, RBQ_EDEVICE = 0, 1, 2, 3
 RBQ_F32, RBQ_BF16 = 0, 1
 RBQ_ENCODE_SET_CENTROID = 1
-RBQ_OP_ENCODE, RBQ_OP_TOPP, RBQ_OP_SPARSE_DECODE, RBQ_OP_DENSE_DECODE = 1, 2, 3, 4
+RBQ_OP_ENCODE, RBQ_OP_TOPP, RBQ_OP_SPARSE_DECODE, RBQ_OP_DENSE_DECODE, RBQ_OP_DECODE_STEP = 1, 2, 3, 4, 5
 QSCAL_STRIDE = 8
 
 EXPORTED = [
     "rbq_encode_keys", "rbq_quantize_query", "rbq_score", "rbq_topp_select", "rbq_sparse_decode",
-    "rbq_dense_decode", "rbq_workspace_bytes", "rbq_index_bytes", "rbq_status_string", "rbq_version",
+    "rbq_dense_decode", "rbq_decode_step", "rbq_workspace_bytes", "rbq_index_bytes", "rbq_status_string", "rbq_version",
     "rbq_encode_keys_debug", "rbq_quantize_query_debug", "rbq_score_ints",
 ]
 
@@ -53,6 +53,8 @@ def _load():
                               vp, sz, vp],
         "rbq_dense_decode": [i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, i64, i32, f32, vp, vp, vp, sz,
                              vp],
+        "rbq_decode_step": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, i32, f32, f32,
+                            vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -172,3 +174,13 @@ def rbq_dense_decode(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, K_loc,
     _check("rbq_dense_decode", lib.rbq_dense_decode(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n, _ptr(K_loc),
         _ptr(V_loc), loc_ld, w, sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def rbq_decode_step(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, cap, n, w, codes, kfac, flush, p,
+                    sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws, stream=None):
+    ws_bytes = ws.numel() * ws.element_size()
+    _check("rbq_decode_step", lib.rbq_decode_step(
+        batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_q), _ptr(c_k), _ptr(K), _ptr(V),
+        kv_dtype_code(K), cap, n, w, _ptr(codes), _ptr(kfac), int(bool(flush)), p, sm_scale, _ptr(qplanes),
+        _ptr(qscal), _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _ptr(out), _ptr(lse), _ptr(ws), ws_bytes,
+        _stream(stream)))

@@ -1,0 +1,104 @@
+"""rbq_decode_step (the whole decode step in one call) against the five
+separate calls it replaces: same inputs, bitwise the same outputs, also when
+the call is repeated on the same workspace and when it is replayed from a HIP
+graph. The separate calls are checked against the oracle elsewhere; the
+end-to-end oracle tests run the fused step."""
+import numpy as np
+import pytest
+import torch
+
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+# (B, Hq, Hkv, n, w, kv dtype, p, flush, seed)
+CASES = [
+    (1, 32, 8, 5000, 256, "bf16", 0.95, True, 1),     # the 8B-model GQA shape, ragged n
+    (2, 8, 2, 3000, 40, "bf16", 0.9, True, 2),
+    (1, 16, 1, 2049, 0, "bf16", 0.8, False, 3),       # G = 16, no window
+    (1, 1, 1, 700, 33, "f32", 0.9, True, 4),          # fp32 K/V, one head
+    (2, 8, 8, 4100, 300, "bf16", 1.0, True, 5),       # p = 1 selects every key
+    (1, 8, 2, 0, 64, "bf16", 0.9, True, 6),           # no indexed key: the window only
+    (1, 4, 1, 10000, 17, "bf16", 0.5, True, 7),
+]
+
+
+@pytest.fixture(scope="module")
+def pipeline():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2606_31519_amd import pipeline as pl
+    return pl
+
+
+def _state(pipeline, case):
+    B, Hq, Hkv, n, w, dt, p, flush, seed = case
+    wl = gen.random_case(B, Hq, Hkv, n, seed=seed, kv_dtype=dt, w=w, c_q_scale=0.5)
+    st = pipeline.DecodeState.from_workload(wl)
+    if n > 0:                 # (a centroid of no keys is undefined: c_k stays zero)
+        st.build_index()
+    return st
+
+
+def _outputs(st):
+    torch.cuda.synchronize()
+    n = st.n
+    cnt = st.sel_count.cpu().numpy()
+    sel = st.sel_idx.cpu().numpy()
+    o = {name: getattr(st, name).cpu().numpy().copy() for name in
+         ("qplanes", "qscal", "sel_count", "out", "lse", "codes", "kfac")}
+    o["scores"] = st.scores[:, :, :n].cpu().numpy().copy()
+    o["sel"] = [sel[b, h, :cnt[b, h]].copy() for b in range(st.B) for h in range(st.Hq)]
+    return o
+
+
+def _same(a, b):
+    assert a.keys() == b.keys()
+    for k in a:
+        if k == "sel":
+            assert len(a[k]) == len(b[k]) and all(np.array_equal(x, y) for x, y in zip(a[k], b[k])), k
+        else:
+            assert a[k].shape == b[k].shape and np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"B{c[0]}-Hq{c[1]}-Hkv{c[2]}-n{c[3]}-w{c[4]}-{c[5]}-p{c[6]}")
+def test_fused_step_matches_separate_calls(pipeline, case):
+    p, flush = case[6], case[7]
+    print("case", case, flush=True)
+    ref = _state(pipeline, case)
+    ref.step_calls(p, flush=flush)
+    want = _outputs(ref)
+    st = _state(pipeline, case)
+    st.step(p, flush=flush)
+    _same(_outputs(st), want)
+    if case[3] > 0:
+        assert want["sel_count"].min() >= 1
+    # the same workspace again: nothing is left over from the first call
+    st.step(p, flush=flush)
+    _same(_outputs(st), want)
+
+
+def test_fused_step_graph_replays(pipeline):
+    case = CASES[0]
+    p = case[6]
+    ref = _state(pipeline, case)
+    ref.step_calls(p)
+    want = _outputs(ref)
+    st = _state(pipeline, case)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        st.step(p)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            st.step(p)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        st.out.zero_()
+        st.sel_count.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        _same(_outputs(st), want)
+        st.step(p)            # eager work between the replays
+        _same(_outputs(st), want)
