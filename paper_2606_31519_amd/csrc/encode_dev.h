@@ -43,6 +43,34 @@ inline int encode_blocks_per_head(int n_new, int bhs) {
   return b > 0 ? b : 1;
 }
 
+// sum over each group of 16 lanes (a DPP row), in every lane of the group
+__device__ __forceinline__ float sum16(float v) {
+  v += RBQ_DPP(v, 0xB1);    // quad_perm [1,0,3,2]
+  v += RBQ_DPP(v, 0x4E);    // quad_perm [2,3,0,1]
+  v += RBQ_DPP(v, 0x141);   // row_half_mirror
+  v += RBQ_DPP(v, 0x140);   // row_mirror
+  return v;
+}
+// the value of lane ^ (1 << BIT) (BIT < 4)
+template <int BIT>
+__device__ __forceinline__ float xor_lane(float v) {
+  if constexpr (BIT == 0) return RBQ_DPP(v, 0xB1);
+  if constexpr (BIT == 1) return RBQ_DPP(v, 0x4E);
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), ((1 << BIT) << 10) | 0x1F));
+}
+// One step of the transpose-reduction: registers 2i and 2i + 1 become register
+// i, the lane whose bit BIT is set keeping the odd one, summed with its partner.
+template <int C, int BIT>
+__device__ __forceinline__ void fold_lanes(float* v, int lane) {
+  const bool hi = (lane >> BIT) & 1;
+#pragma unroll
+  for (int i = 0; i < C / 2; ++i) {
+    const float keep = hi ? v[2 * i + 1] : v[2 * i];
+    const float send = hi ? v[2 * i] : v[2 * i + 1];
+    v[i] = keep + xor_lane<BIT>(send);
+  }
+}
+
 // The tiles bx, bx + gx, ... of (b, kv-head) bh, by the 256 threads of the calling block.
 template <int DT, bool ROT>
 __device__ __forceinline__ void encode_tiles(const EncodeArgs& ea, int bh, int bx, int gx) {
@@ -97,49 +125,47 @@ __device__ __forceinline__ void encode_tiles(const EncodeArgs& ea, int bh, int b
 
   for (int tile = bx; tile < tiles; tile += gx) {
     const int key0 = tile * kTileKeys;
+    // stage the centred keys; ||x||^2 and <c_q, x> of each key are summed on
+    // the way, over the kPiecesPerRow consecutive lanes that hold its pieces
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int pidx = j * kEncThreads + threadIdx.x;
       const int row = pidx / kPiecesPerRow, piece = pidx % kPiecesPerRow;
       float* xr = Xs + row * kXStride;
+      float nn = 0.f, gg = 0.f;
       if (DT == RBQ_BF16) {
         const int d = piece * 8;
         const uint32_t wv[4] = {pc[j].x, pc[j].y, pc[j].z, pc[j].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          xr[d + 2 * e] = bf16_lo(wv[e]) - ck_s[d + 2 * e];
-          xr[d + 2 * e + 1] = bf16_hi(wv[e]) - ck_s[d + 2 * e + 1];
+          const float x0 = bf16_lo(wv[e]) - ck_s[d + 2 * e], x1 = bf16_hi(wv[e]) - ck_s[d + 2 * e + 1];
+          xr[d + 2 * e] = x0;
+          xr[d + 2 * e + 1] = x1;
+          nn = fmaf(x1, x1, fmaf(x0, x0, nn));
+          gg = fmaf(cq_s[d + 2 * e + 1], x1, fmaf(cq_s[d + 2 * e], x0, gg));
         }
+        nn = sum16(nn);
+        gg = sum16(gg);
       } else {
         const int d = piece * 4;
-        xr[d] = __uint_as_float(pc[j].x) - ck_s[d];
-        xr[d + 1] = __uint_as_float(pc[j].y) - ck_s[d + 1];
-        xr[d + 2] = __uint_as_float(pc[j].z) - ck_s[d + 2];
-        xr[d + 3] = __uint_as_float(pc[j].w) - ck_s[d + 3];
+        const float x[4] = {__uint_as_float(pc[j].x) - ck_s[d], __uint_as_float(pc[j].y) - ck_s[d + 1],
+                            __uint_as_float(pc[j].z) - ck_s[d + 2], __uint_as_float(pc[j].w) - ck_s[d + 3]};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          xr[d + e] = x[e];
+          nn = fmaf(x[e], x[e], nn);
+          gg = fmaf(cq_s[d + e], x[e], gg);
+        }
+        nn = sum32(nn);
+        gg = sum32(gg);
+      }
+      if (piece == 0) {
+        ng_s[0][row] = nn;
+        ng_s[1][row] = gg;
       }
     }
     if (tile + gx < tiles) load_tile(tile + gx);   // lands while this tile is rotated
     __syncthreads();
-
-    // ---- ||x||^2 and <c_q, x>: threads 0..127, key t / 4, a quarter of the dims each
-    if (threadIdx.x < 4 * kTileKeys) {
-      const int kk = threadIdx.x / 4, qd = threadIdx.x % 4;
-      float nn = 0.f, gg = 0.f;
-#pragma unroll 8
-      for (int d = qd * 32; d < qd * 32 + 32; ++d) {
-        const float x = Xs[kk * kXStride + d];
-        nn = fmaf(x, x, nn);
-        gg = fmaf(cq_s[d], x, gg);
-      }
-      nn += RBQ_DPP(nn, 0xB1);
-      nn += RBQ_DPP(nn, 0x4E);
-      gg += RBQ_DPP(gg, 0xB1);
-      gg += RBQ_DPP(gg, 0x4E);
-      if (qd == 0) {
-        ng_s[0][kk] = nn;
-        ng_s[1][kk] = gg;
-      }
-    }
 
     // ---- r = x P for output dimensions [32 wave, 32 wave + 32): A = X rows, B = P rows
     f32x16 acc = f32x16{0.f}, acc2 = f32x16{0.f};   // two chains over alternate k-steps, added at the end
@@ -150,24 +176,34 @@ __device__ __forceinline__ void encode_tiles(const EncodeArgs& ea, int bh, int b
       acc2 = __builtin_amdgcn_mfma_f32_32x32x2f32(Xs[mk * kXStride + k + 2], pb[s2 + 1], acc2, 0, 0, 0);
     }
     acc += acc2;
-    // acc[r] at lane l: key 8 (r / 4) + 4 (l / 32) + r % 4, dimension 32 wave + l % 32
+    // acc[r] at lane l: key 8 (r / 4) + 4 (l / 32) + r % 4, dimension 32 wave + l % 32.
+    // Sign bits: one ballot per register. sum |r| over the wave's 32 dimensions
+    // of every key: a transpose-reduction that halves the registers while
+    // folding lane bits 0..3 (afterwards lane l holds register l & 15), then
+    // bit 4 completes the 32-lane sums.
+    uint64_t bal[16];
+    float v[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float v = acc[r];
-      const uint64_t bal = __ballot(v > 0.f);
-      const float a = sum32(fabsf(v));
-      const int key_a = 8 * (r / 4) + (r % 4);
-      if (lane == 0) {
-        code_s[key_a][wave] = uint32_t(bal);
-        code_s[key_a + 4][wave] = uint32_t(bal >> 32);
-        abs_s[wave][key_a] = a;
-      }
-      if (lane == 32) abs_s[wave][key_a + 4] = a;
+      bal[r] = __ballot(acc[r] > 0.f);
+      v[r] = fabsf(acc[r]);
       if (ROT) {
-        const int key = key0 + key_a + 4 * half;
-        if (key < n_new) rot_out[(int64_t(bh) * n_new + key) * kHeadDim + 32 * wave + mk] = v;
+        const int key = key0 + 8 * (r / 4) + (r % 4) + 4 * half;
+        if (key < n_new) rot_out[(int64_t(bh) * n_new + key) * kHeadDim + 32 * wave + mk] = acc[r];
       }
     }
+    fold_lanes<16, 0>(v, lane);
+    fold_lanes<8, 1>(v, lane);
+    fold_lanes<4, 2>(v, lane);
+    fold_lanes<2, 3>(v, lane);
+    const float asum = v[0] + swap16(v[0]);
+    const int rr = lane & 15;
+    const int key_a = 8 * (rr / 4) + (rr % 4);
+    if ((lane & 16) == 0) abs_s[wave][key_a + 4 * half] = asum;
+    uint64_t mine = bal[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mine = rr == r ? bal[r] : mine;
+    if (lane < 32) code_s[key_a + 4 * (lane >> 4)][wave] = (lane & 16) ? uint32_t(mine >> 32) : uint32_t(mine);
     __syncthreads();
 
     if (threadIdx.x < kTileKeys) {

@@ -67,12 +67,14 @@ __device__ __forceinline__ uint32_t binary_int4_dot(const Spread& e, const uint3
 }
 
 // block maximum of each of the G heads from the per-wave maxima
-__device__ __forceinline__ void write_slots(float (*mx_s)[kScoreThreads / kWave], int row0, int G, float* slot_max) {
+// (maxima of every 32-lane half-wave, reduced by DPP in the head loop)
+constexpr int kHalfWaves = 2 * kScoreThreads / kWave;
+__device__ __forceinline__ void write_slots(float (*mx_s)[kHalfWaves], int row0, int G, float* slot_max) {
   __syncthreads();
   if (int(threadIdx.x) < G) {
     float m = mx_s[threadIdx.x][0];
 #pragma unroll
-    for (int w = 1; w < kScoreThreads / kWave; ++w) m = fmaxf(m, mx_s[threadIdx.x][w]);
+    for (int w = 1; w < kHalfWaves; ++w) m = fmaxf(m, mx_s[threadIdx.x][w]);
     slot_max[int64_t(row0 + threadIdx.x) * gridDim.x + blockIdx.x] = m;
   }
 }
@@ -92,7 +94,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const float* __restrict__ qscal, float* __restrict__ scores, int32_t* __restrict__ ip_out,
     int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl) {
   __shared__ uint32_t qn_s[kMaxGroup][16];
-  __shared__ float mx_s[SLOTS ? kMaxGroup : 1][kScoreThreads / kWave];
+  __shared__ float mx_s[SLOTS ? kMaxGroup : 1][kHalfWaves];
   const int bh = blockIdx.y;                 // b * Hkv + kv head
   const int b = bh / Hkv;
   const int hk = bh - b * Hkv;
@@ -160,8 +162,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
         __builtin_nontemporal_store(sc, out + i0 + u * kScoreThreads);
       }
       if (SLOTS) {
-        mx = wave_max(mx);
-        if (lane_id() == 0) mx_s[g][threadIdx.x / kWave] = mx;
+        mx = max32(mx);
+        if ((lane_id() & 31) == 0) mx_s[g][threadIdx.x / 32] = mx;
       }
     }
     if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
@@ -195,8 +197,8 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       }
     }
     if (SLOTS) {
-      mx = wave_max(mx);
-      if (lane_id() == 0) mx_s[g][threadIdx.x / kWave] = mx;
+      mx = max32(mx);
+      if ((lane_id() & 31) == 0) mx_s[g][threadIdx.x / 32] = mx;
     }
   }
   if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
