@@ -38,7 +38,10 @@ namespace {
 
 constexpr int kDWaves = 4;
 constexpr int kDThreads = kDWaves * kWave;
-constexpr int kBmWords = kDecodeChunk / 32;
+constexpr int kBmWords = kDecodeChunk / 32;                       // words of the indexed positions
+constexpr int kListRounds = (kDecodeChunk + kDecodeFoldMax + kDThreads - 1) / kDThreads;
+constexpr int kListCap = kListRounds * kDThreads;                 // list positions (indexed + folded window)
+constexpr int kBmAll = kListCap / 32;
 constexpr float kLn2 = 0.69314718055994531f;
 __device__ __forceinline__ float wmax64(float v) { v = max32(v); return fmaxf(v, __shfl_xor(v, 32, kWave)); }
 __device__ __forceinline__ float wsum64(float v) { v = sum32(v); return v + __shfl_xor(v, 32, kWave); }
@@ -78,9 +81,25 @@ __device__ __forceinline__ void wave_lower_bounds(const int32_t* __restrict__ a,
   r1 = lo1;
 }
 
+// This thread's word of the split's selection bitmaps (thread t < G * 16: head
+// t / 16, 64-key word t % 16); for small groups it is requested at the start
+// of the kernel so that the load overlaps the query staging.
+template <int G>
+__device__ __forceinline__ unsigned long long load_mask_word(const unsigned long long* __restrict__ sel_mask,
+                                                             int mask_words, int row0, int c0, int c1) {
+  constexpr int kMw = kBmWords / 2;   // 64-key words per split
+  static_assert(G * kMw <= kDThreads, "one word per thread");
+  const int t = threadIdx.x;
+  if (sel_mask == nullptr || t >= G * kMw) return 0ull;
+  const int g = t / kMw, wd = t % kMw;
+  return c0 + 64 * wd < c1 ? sel_mask[int64_t(row0 + g) * mask_words + c0 / 64 + wd] : 0ull;
+}
+
 // Per-block row list of a sparse split: the union over the G heads of the
 // group of the positions in [c0, c1) that each head selected, in ascending
-// order, with a bit mask of the heads that selected each entry. Returns the
+// order, with a bit mask of the heads that selected each entry, followed by
+// the nwin window rows folded into the split (every head; list positions
+// c1 - c0 + i, rows c1 + wshift + i). Returns the
 // number of entries (block-uniform). All threads of the block must call it.
 // Each wave finds the part [lower bound of c0, lower bound of c1) of its
 // heads' selection lists; the entries are then loaded all at once and marked
@@ -88,23 +107,25 @@ __device__ __forceinline__ void wave_lower_bounds(const int32_t* __restrict__ a,
 //
 // With selection bitmaps (sel_mask != NULL, [rows][mask_words] words of 64
 // keys, c0 a multiple of 64) the per-head bitmaps are loaded directly instead.
-template <int G, int kThreads>
+template <int G, int kThreads, bool PRE>
 __device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
                                 const unsigned long long* __restrict__ sel_mask, int mask_words, int row0,
-                                int n, int c0, int c1, uint32_t (*bm)[kBmWords], int32_t* lst, uint16_t* hmask,
-                                int* rng_lo, int* rng_hi, int* wcnt, int* ucount) {
+                                int n, int c0, int c1, int nwin, int wshift, uint32_t (*bm)[kBmAll], int32_t* lst,
+                                uint16_t* hmask, int* rng_lo, int* rng_hi, int* wcnt, int* ucount,
+                                unsigned long long mword) {
   constexpr int kWaves = kThreads / kWave;
   const int t = threadIdx.x, wave = t / kWave, lane = lane_id();
-  if (sel_mask) {
-    constexpr int kMw = kBmWords / 2;   // 64-key words per split
-    static_assert(G * kMw <= kThreads, "one word per thread");
+  if (sel_mask) {   // mword: this thread's word, from load_mask_word (when preloaded)
+    constexpr int kMw = kBmWords / 2;
+    static_assert(kThreads == kDThreads, "load_mask_word assigns the words");
+    if (!PRE) mword = load_mask_word<G>(sel_mask, mask_words, row0, c0, c1);
     if (t < G * kMw) {
       const int g = t / kMw, wd = t % kMw;
-      const unsigned long long v =
-          c0 + 64 * wd < c1 ? sel_mask[int64_t(row0 + g) * mask_words + c0 / 64 + wd] : 0ull;
-      bm[g][2 * wd] = uint32_t(v);
-      bm[g][2 * wd + 1] = uint32_t(v >> 32);
+      bm[g][2 * wd] = uint32_t(mword);
+      bm[g][2 * wd + 1] = uint32_t(mword >> 32);
     }
+    constexpr int kExtra = kBmAll - kBmWords;   // the folded window's words
+    for (int e = t; e < G * kExtra; e += kThreads) bm[e / kExtra][kBmWords + e % kExtra] = 0u;
     __syncthreads();
   } else {
   for (int g = wave; g < G; g += kWaves) {
@@ -117,7 +138,7 @@ __device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32
       rng_hi[g] = hi;
     }
   }
-  for (int e = t; e < G * kBmWords; e += kThreads) bm[e / kBmWords][e % kBmWords] = 0u;
+  for (int e = t; e < G * kBmAll; e += kThreads) bm[e / kBmAll][e % kBmAll] = 0u;
   __syncthreads();
   // mark the selected positions: every entry's load first, then the LDS bit sets
   constexpr int kPer = kDecodeChunk / kThreads;            // entries per thread per head (a split has <= chunk)
@@ -146,9 +167,17 @@ __device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32
   }
   __syncthreads();
   }
+  // the folded window rows are marked in the first head's bitmap
+  // (their head masks are set to every head below)
+  const int ce = c1 + nwin;   // list positions end at ce - c0
+  if (nwin > 0) {
+    for (int e = c1 - c0 + t; e < ce - c0; e += kThreads) atomicOr(&bm[0][e >> 5], 1u << (e & 31));
+    __syncthreads();
+  }
   // union of the G bitmaps, compacted in ascending position order: position
   // r * kThreads + t in round r, ranked by wave ballots
-  constexpr int kRounds = kDecodeChunk / kThreads;
+  constexpr int kRounds = kListRounds;
+  static_assert(kThreads == kDThreads, "list sizes assume the decode block");
   bool f[kRounds];
   uint64_t bal[kRounds];
 #pragma unroll
@@ -157,7 +186,7 @@ __device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32
     uint32_t any = 0u;
 #pragma unroll
     for (int g = 0; g < G; ++g) any |= bm[g][pos >> 5];
-    f[r] = pos < c1 - c0 && ((any >> (pos & 31)) & 1u);
+    f[r] = pos < ce - c0 && ((any >> (pos & 31)) & 1u);
     bal[r] = __ballot(f[r]);
     if (lane == 0) wcnt[r * kWaves + wave] = __popcll(bal[r]);
   }
@@ -176,10 +205,11 @@ __device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32
       const int pos = r * kThreads + t;
       const int o = base + woff + __builtin_amdgcn_mbcnt_hi(uint32_t(bal[r] >> 32),
                                                             __builtin_amdgcn_mbcnt_lo(uint32_t(bal[r]), 0u));
-      uint16_t mk = 0;
+      uint32_t mk32 = 0u;
 #pragma unroll
-      for (int g = 0; g < G; ++g) mk |= uint16_t(((bm[g][pos >> 5] >> (pos & 31)) & 1u) << g);
-      lst[o] = c0 + pos;
+      for (int g = 0; g < G; ++g) mk32 |= ((bm[g][pos >> 5] >> (pos & 31)) & 1u) << g;
+      const uint16_t mk = uint16_t(pos >= c1 - c0 ? (1u << G) - 1u : mk32);   // window rows: every head
+      lst[o] = c0 + pos + (pos >= c1 - c0 ? wshift : 0);
       hmask[o] = mk;
     }
     base += tot;
@@ -247,15 +277,15 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     const float* __restrict__ q, const void* __restrict__ K, const void* __restrict__ V, int cap, int n,
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
     const unsigned long long* __restrict__ sel_mask, int mask_words, const void* __restrict__ K_loc,
-    const void* __restrict__ V_loc, int64_t loc_ld, int w, int chunk, int idx_splits, int total_splits,
-    float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
+    const void* __restrict__ V_loc, int64_t loc_ld, int w, int chunk, int idx_splits, int total_splits, int fold_s0,
+    int fold_wq, float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
   constexpr int kElem = DT == RBQ_BF16 ? 2 : 4;
   __shared__ float qs[G][kHeadDim];
-  __shared__ uint32_t bm[G][kBmWords];
-  __shared__ int32_t lst[SPARSE ? kDecodeChunk : 1];
-  __shared__ uint16_t hmask[SPARSE ? kDecodeChunk : 1];
+  __shared__ uint32_t bm[G][kBmAll];
+  __shared__ int32_t lst[SPARSE ? kListCap : 1];
+  __shared__ uint16_t hmask[SPARSE ? kListCap : 1];
   __shared__ int rng_lo[G], rng_hi[G];
-  __shared__ int wcnt[kBmWords];
+  __shared__ int wcnt[kBmAll];
   __shared__ int ucount;
   __shared__ float ps[kDWaves][G][kWave];
   __shared__ float sm[kDWaves][G], sl[kDWaves][G];
@@ -267,10 +297,16 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   const int row0 = b * Hq + hk * G;     // first query head of the group
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const bool window = split >= idx_splits;
-  int c0, c1;
+  // indexed rows [c0, c1), then nwin folded window rows from row wrow0 (same buffer)
+  int c0, c1, nwin = 0, wrow0 = 0;
   if (!window) {
     c0 = split * chunk;
     c1 = min(n, c0 + chunk);
+    if (fold_wq > 0 && split >= fold_s0) {
+      const int k = split - fold_s0;
+      nwin = min(max(w - k * fold_wq, 0), fold_wq);
+      wrow0 = n + k * fold_wq;
+    }
   } else {
     c0 = (split - idx_splits) * kDecodeWinChunk;
     c1 = min(w, c0 + kDecodeWinChunk);
@@ -280,6 +316,9 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   const char* Vbase = window ? static_cast<const char*>(V_loc) + int64_t(bh) * loc_ld * kHeadDim * kElem
                              : static_cast<const char*>(V) + int64_t(bh) * cap * kHeadDim * kElem;
 
+  constexpr bool kPreMask = G <= 4;   // (for larger groups the early load costs registers)
+  const unsigned long long mword =
+      kPreMask && SPARSE && !window ? load_mask_word<G>(sel_mask, mask_words, row0, c0, c1) : 0ull;
   for (int e = threadIdx.x; e < G * kHeadDim; e += kDThreads)
     qs[e / kHeadDim][e % kHeadDim] = q[int64_t(row0) * kHeadDim + e] * scale_log2e;
 
@@ -287,11 +326,11 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   const bool use_list = SPARSE && !window;
   int U;
   if (use_list) {
-    U = build_union_list<G, kDThreads>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
-                                       &ucount);
+    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
+                                       &ucount, mword);
   } else {
     __syncthreads();
-    U = max(c1 - c0, 0);
+    U = max(c1 - c0, 0) + nwin;   // (dense: the window is folded only right after the last rows)
   }
 
   // ---- online softmax over tiles of 64 rows, one wave per tile
@@ -467,16 +506,16 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
     const unsigned long long* __restrict__ sel_mask, int mask_words, const uint16_t* __restrict__ K_loc,
     const uint16_t* __restrict__ V_loc, int64_t loc_ld, int w, int chunk, int idx_splits, int total_splits,
-    float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
+    int fold_s0, int fold_wq, float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
   static_assert(G >= 1 && G <= 16, "the MFMA tiles hold at most 16 heads");
   constexpr bool kPackedQ = kQParts * G <= 16;
   constexpr int kQOps = kPackedQ ? 1 : kQParts;
   __shared__ u32x4 qB[4][kQOps][kWave];           // B operands of the logits product
-  __shared__ uint32_t bm[G][kBmWords];
-  __shared__ int32_t lst[SPARSE ? kDecodeChunk : 1];
-  __shared__ uint16_t hmask[SPARSE ? kDecodeChunk : 1];
+  __shared__ uint32_t bm[G][kBmAll];
+  __shared__ int32_t lst[SPARSE ? kListCap : 1];
+  __shared__ uint16_t hmask[SPARSE ? kListCap : 1];
   __shared__ int rng_lo[G], rng_hi[G];
-  __shared__ int wcnt[kBmWords];
+  __shared__ int wcnt[kBmAll];
   __shared__ int ucount;
   __shared__ float sm[kDWaves][G], sl[kDWaves][G];
   __shared__ float sacc[kDWaves][G][kHeadDim];
@@ -488,19 +527,28 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const int x = lane & 15, j = lane >> 4;
   const bool window = split >= idx_splits;
-  int c0, c1;
+  // indexed rows [c0, c1), then nwin folded window rows from row wrow0 (same buffer)
+  int c0, c1, nwin = 0, wrow0 = 0;
   if (!window) {
     c0 = split * chunk;
     c1 = min(n, c0 + chunk);
+    if (fold_wq > 0 && split >= fold_s0) {
+      const int k = split - fold_s0;
+      nwin = min(max(w - k * fold_wq, 0), fold_wq);
+      wrow0 = n + k * fold_wq;
+    }
   } else {
     c0 = (split - idx_splits) * kDecodeWinChunk;
     c1 = min(w, c0 + kDecodeWinChunk);
   }
   const uint16_t* Kb = window ? K_loc + int64_t(bh) * loc_ld * kHeadDim : K + int64_t(bh) * cap * kHeadDim;
   const uint16_t* Vb = window ? V_loc + int64_t(bh) * loc_ld * kHeadDim : V + int64_t(bh) * cap * kHeadDim;
-  const uint32_t region = uint32_t(window ? w : n) * uint32_t(kHeadDim * 2);   // < 2^31, checked on the host
+  const uint32_t region = uint32_t(window ? w : n + (fold_wq > 0 ? w : 0)) * uint32_t(kHeadDim * 2);   // < 2^31
   const __amdgpu_buffer_rsrc_t Kr = make_rsrc(Kb, region);
   const __amdgpu_buffer_rsrc_t Vr = make_rsrc(Vb, region);
+  constexpr bool kPreMask = kPackedQ;   // (for larger groups the early load costs registers)
+  const unsigned long long mword =
+      kPreMask && SPARSE && !window ? load_mask_word<G>(sel_mask, mask_words, row0, c0, c1) : 0ull;
 
   // query operands, lane (column c, quarter jj) of k-block kb = dims 32 kb + 8 jj .. +8.
   // G <= 4: one operand per k-block, column c = part * G + head; otherwise one
@@ -529,11 +577,11 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
 
   int U;
   if (SPARSE && !window) {
-    U = build_union_list<G, kDThreads>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
-                                       &ucount);
+    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
+                                       &ucount, mword);
   } else {
     __syncthreads();
-    U = max(c1 - c0, 0);
+    U = max(c1 - c0, 0) + nwin;   // (dense: the window is folded only right after the last rows)
   }
   const bool list = SPARSE && !window;
 
@@ -748,18 +796,19 @@ template <int DT, bool SPARSE>
 rbq_status launch_g(int G, dim3 grid, hipStream_t stream, const float* q, const void* K, const void* V, int cap,
                     int n, const int32_t* sel_idx, const int32_t* sel_count, const unsigned long long* sel_mask,
                     int mask_words, const void* K_loc, const void* V_loc, int64_t loc_ld, int w, int chunk,
-                    int idx_splits, int total, float scale_log2e, float* part, int Hq, int Hkv) {
+                    int idx_splits, int total, int fold_s0, int fold_wq, float scale_log2e, float* part, int Hq,
+                    int Hkv) {
 #define RBQ_DECODE_CASE(GG)                                                                                       \
   case GG:                                                                                                        \
     if (DT == RBQ_BF16)                                                                                           \
       decode_mfma_kernel<SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                             \
           q, static_cast<const uint16_t*>(K), static_cast<const uint16_t*>(V), cap, n, sel_idx, sel_count,        \
           sel_mask, mask_words, static_cast<const uint16_t*>(K_loc), static_cast<const uint16_t*>(V_loc), loc_ld, \
-          w, chunk, idx_splits, total, scale_log2e, part, Hq, Hkv);                                               \
+          w, chunk, idx_splits, total, fold_s0, fold_wq, scale_log2e, part, Hq, Hkv);                             \
     else                                                                                                          \
       decode_vec_kernel<DT, SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                          \
           q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, loc_ld, w, chunk, idx_splits,  \
-          total, scale_log2e, part, Hq, Hkv);                                                                     \
+          total, fold_s0, fold_wq, scale_log2e, part, Hq, Hkv);                                                   \
     break;
   switch (G) {
     RBQ_DECODE_CASE(1)
@@ -782,14 +831,21 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                          float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream,
                          const unsigned long long* sel_mask, int32_t mask_words) {
   const int G = heads_q / heads_kv;
-  const DecodeSplits sp = decode_splits(batch, heads_kv, n, w);
+  // the window rows are the cache tail when they sit right after the indexed rows of every (b, kv-head)
+  const size_t elem = kv_dtype == RBQ_BF16 ? 2 : 4;
+  const bool tail = n > 0 && w > 0 && loc_ld == cap &&
+                    static_cast<const char*>(K_loc) == static_cast<const char*>(K) + size_t(n) * kHeadDim * elem &&
+                    static_cast<const char*>(V_loc) == static_cast<const char*>(V) + size_t(n) * kHeadDim * elem &&
+                    (int64_t(n) + w) * kHeadDim * int64_t(elem) < (int64_t(1) << 31);
+  const DecodeSplits sp = decode_splits(batch, heads_kv, n, w, tail, sparse);
   const dim3 grid(sp.total(), batch * heads_kv);
   float* part = static_cast<float*>(ws);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
   rbq_status st;
 #define RBQ_DECODE_LAUNCH(DT, SP)                                                                                  \
   launch_g<DT, SP>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, loc_ld, \
-                   w, sp.chunk, sp.idx_splits, sp.total(), scale_log2e, part, heads_q, heads_kv)
+                   w, sp.chunk, sp.idx_splits, sp.total(), sp.fold_s0, sp.fold_wq, scale_log2e, part, heads_q,      \
+                   heads_kv)
   if (kv_dtype == RBQ_BF16)
     st = sparse ? RBQ_DECODE_LAUNCH(RBQ_BF16, true) : RBQ_DECODE_LAUNCH(RBQ_BF16, false);
   else

@@ -62,9 +62,18 @@ struct DecodeSplits {
   int32_t chunk;            // indexed positions per split (<= kDecodeChunk)
   int32_t idx_splits;
   int32_t win_splits;
+  int32_t fold_s0;          // window rows folded into the indexed splits: split s >= fold_s0
+  int32_t fold_wq;          // takes window rows [(s - fold_s0) * fold_wq, +fold_wq) (0: window splits)
   int32_t total() const { return idx_splits + win_splits; }
 };
-DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w);
+constexpr int kDecodeFoldMax = 64;        // window rows a sparse split may take beside its indexed rows
+// tail_window: the window rows are rows [n, n + w) of K / V (the cache tail).
+// Then they are folded into the indexed splits instead of splits of their own
+// (a grid of whole waves of resident blocks for the usual shapes): spread over
+// every split for the sparse call (they are dense, the indexed rows are not),
+// given to the last split, beside its rows, for the dense call.
+DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w, bool tail_window = false,
+                           bool sparse = false);
 size_t decode_workspace_bytes(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
                               int32_t w);
 

@@ -98,14 +98,29 @@ rbq_status check_topp(int32_t batch, int32_t heads_q, int32_t n, const float* sc
   return RBQ_OK;
 }
 
-DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w) {
+DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w, bool tail_window, bool sparse) {
   DecodeSplits s;
+  s.fold_s0 = 0;
+  s.fold_wq = 0;
   // halve the chunk until the grid has kDecodeMinBlocks blocks or the chunk is 256
   const int64_t groups = int64_t(batch) * heads_kv;
   s.chunk = kDecodeChunk;
   while (s.chunk > 256 && groups * ((int64_t(n) + s.chunk - 1) / s.chunk) < kDecodeMinBlocks) s.chunk /= 2;
   s.idx_splits = n > 0 ? (n + s.chunk - 1) / s.chunk : 0;
   s.win_splits = w > 0 ? (w + kDecodeWinChunk - 1) / kDecodeWinChunk : 0;
+  if (tail_window && s.idx_splits > 0 && w > 0) {
+    if (sparse) {
+      const int wq = (w + s.idx_splits - 1) / s.idx_splits;
+      if (wq <= kDecodeFoldMax) {
+        s.fold_wq = wq;
+        s.win_splits = 0;
+      }
+    } else if (n - (s.idx_splits - 1) * s.chunk + w <= s.chunk) {
+      s.fold_s0 = s.idx_splits - 1;
+      s.fold_wq = w;
+      s.win_splits = 0;
+    }
+  }
   if (s.total() == 0) s.win_splits = 1;   // one empty split keeps the combine step uniform
   return s;
 }

@@ -218,6 +218,21 @@ def test_topp_degenerate_rows(R):
     assert np.all(cnt == 0)
 
 
+def test_topp_large_crossing_bin(R):
+    """Rows whose level-1 crossing bin holds most of the keys (far more than the
+    candidates kept in registers): the final pass streams the candidate list."""
+    n = 70001
+    rng = np.random.default_rng(5)
+    spread = rng.standard_normal(n) * 5.0
+    S = np.stack([np.full(n, 1.5), np.where(rng.random(n) < 0.6, 2.0, spread),
+                  2.0 + rng.random(n) * 1e-3])              # one narrow band of distinct values
+    for p in (0.5, 0.9, 0.99):
+        sel, cnt = _topp_rows(R, S, p, 1.0)
+        assert cnt[0] == n
+        for r in (1, 2):
+            pu.check_topp(S[r].astype(np.float32), p, 1.0, sel[r, :cnt[r]])
+
+
 # ---------------------------------------------------------------- attention
 def _rand_sel(rng, n, frac, Hq):
     out = []
