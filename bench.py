@@ -11,9 +11,11 @@ data in the 256 MB Infinity Cache.
 
 One JSON line is printed (rank 0, N = 1). `value` = proxy-scored (query head,
 key) pairs per second over the whole step; `ms_per_step` is the sparse decode
-step latency at 128K, compared against dense bf16 decode at the same shape
-(this library's split-K kernel and torch SDPA, the faster of the two). The line
-also carries the per-stage times, the roofline of the dominant call, the Top-p
+step latency at 128K (one rbq_decode_step call; the same step as five separate
+calls is reported beside it), compared against dense bf16 decode at the same
+shape (this library's split-K kernel and torch SDPA, the faster of the two).
+The per-stage times come from the separate calls. The line also carries the
+roofline of the dominant call, the Top-p
 sweep (p = 0.8 / 0.9 / 0.95 / 0.99: step time, budget, KV-group union), the
 standalone score scan of the wide-head workload, and the oracle's CPU rate.
 """
@@ -263,8 +265,13 @@ def main():
                 "flush": lambda r: r.flush_window()}
 
     # the whole step, one HIP graph per replica
+    # the whole step (rbq_decode_step), one HIP graph per replica; then the same step
+    # as the five separate calls, for reference
     step_graphs = [_graph(torch, lambda r=r: r.step(p)) for r in reps]
     ms_step = _time_graphs(torch, step_graphs, args.steps, args.warmup)
+    call_graphs = [_graph(torch, lambda r=r: r.step_calls(p)) for r in reps]
+    ms_step_calls = _time_graphs(torch, call_graphs, args.steps, args.warmup)
+    del call_graphs
     # each stage on its own: one graph runs it REPS times back-to-back over the replicas, so the
     # graph launch is amortised and the time per run is that of the stage's kernels plus launch gaps
     REPS = 16
@@ -355,6 +362,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_five_calls": ms_step_calls,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
