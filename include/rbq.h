@@ -9,7 +9,8 @@
  * window of recent keys.
  *
  * Conventions shared by every call
- *   - Pointers are DEVICE pointers owned by the caller unless marked (host).
+ *   - Pointers are DEVICE pointers owned by the caller unless marked (host),
+ *     16-byte aligned (RBQ_EINVAL otherwise).
  *     The library never allocates, frees or synchronises: each call checks
  *     its arguments on the host, enqueues kernels on `stream` and returns.
  *   - Shapes: B = batch, Hq = query heads, Hkv = KV heads (Hq % Hkv == 0,

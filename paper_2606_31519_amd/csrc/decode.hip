@@ -560,14 +560,21 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     const int prt = kPackedQ ? c / G : op;
     uint32_t wds[4] = {0u, 0u, 0u, 0u};
     if (h < G && prt < kQParts) {
-      const float* qp = q + int64_t(row0 + h) * kHeadDim + 32 * kb + 8 * jj;
+      // both 16-byte loads are issued before any use (a loop over the part index
+      // with a run-time bound otherwise serialises one load per element)
+      const f32x4* qp = reinterpret_cast<const f32x4*>(q + int64_t(row0 + h) * kHeadDim + 32 * kb + 8 * jj);
+      const f32x4 qa = qp[0], qb = qp[1];
+      const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        float r = qp[i] * scale_log2e;
+        float r = qv[i] * scale_log2e;
         uint32_t bits = 0u;
-        for (int t = 0; t <= prt; ++t) {
-          bits = bf16_bits(r);
-          r -= bf16_val(bits);
+#pragma unroll
+        for (int t = 0; t < kQParts; ++t) {   // part prt = the residual after prt subtractions
+          if (t <= prt) {
+            bits = bf16_bits(r);
+            r -= bf16_val(bits);
+          }
         }
         wds[i >> 1] |= bits << (16 * (i & 1));
       }

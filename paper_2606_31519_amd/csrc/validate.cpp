@@ -9,7 +9,8 @@ namespace rbq {
 
 namespace {
 constexpr int64_t kMaxRows = int64_t(1) << 31;
-bool bad_ptr(const void* p) { return p == nullptr; }
+// a required device pointer: present, and 16-byte aligned (the kernels use 16-byte vector loads)
+bool bad_ptr(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 }  // namespace
 
 rbq_status check_heads(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim) {

@@ -116,3 +116,13 @@ def test_invalid_arguments_are_rejected_on_the_host(lib):
     assert dec(Hq=12) == EUNSUP
     assert L.rbq_dense_decode(1, 8, 4, 128, FAKE, FAKE, FAKE, 3, 100, 100, None, None, 0, 0, 0.1, FAKE, None,
                               FAKE, 1 << 30, 0) == EUNSUP
+    # device pointers must be 16-byte aligned (the kernels use 16-byte vector loads)
+    assert L.rbq_score(1, 8, 4, 128, 10, 10, FAKE + 4, FAKE, FAKE, FAKE, FAKE, 0) == EINVAL
+    assert L.rbq_quantize_query(1, 8, 4, 128, FAKE + 8, FAKE, None, FAKE, FAKE, FAKE, 0) == EINVAL
+    assert dec(kl=FAKE + 2) == EINVAL
+    # the fused step: n + w beyond the capacity, a short workspace
+    step = lambda **k: L.rbq_decode_step(1, 8, 4, 128, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1, k.get("cap", 200),
+                                         100, k.get("w", 10), FAKE, FAKE, 1, 0.9, 0.1, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                         FAKE, None, FAKE, k.get("wsb", 1 << 30), 0)
+    assert step(cap=105) == EINVAL
+    assert step(wsb=64) == EINVAL
