@@ -66,9 +66,8 @@ def _measured_traffic(path=TRAFFIC_FILE, src=DECODE_SRC, sha_key="decode_source_
         return None
 
 
-def copy_probe(torch, steps):
-    """A plain elementwise copy of known size (1 GiB read + 1 GiB written, fp32): the
-    calibration run for the FETCH_SIZE / WRITE_SIZE counters."""
+def _copy_rate(torch, steps):
+    """A plain elementwise copy of known size (1 GiB read + 1 GiB written, fp32)."""
     n = 1 << 28
     src = torch.randn(n, device="cuda")
     dst = torch.empty_like(src)
@@ -82,8 +81,14 @@ def copy_probe(torch, steps):
     b.record()
     torch.cuda.synchronize()
     ms = a.elapsed_time(b) / steps
-    print(json.dumps({"copy_probe": {"bytes_read": n * 4, "bytes_written": n * 4, "ms": ms,
-                                     "GBps": 2 * n * 4 / (ms * 1e-3) / 1e9}}), flush=True)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes_read": n * 4, "bytes_written": n * 4, "ms": ms, "GBps": 2 * n * 4 / (ms * 1e-3) / 1e9}
+
+
+def copy_probe(torch, steps):
+    """The calibration run for the FETCH_SIZE / WRITE_SIZE counters."""
+    print(json.dumps({"copy_probe": _copy_rate(torch, steps)}), flush=True)
 
 
 def _git_sha():
@@ -333,6 +338,9 @@ def main():
         st0.step(p)
         torch.cuda.synchronize()
 
+    # the box's own streaming rate (elementwise copy), a second reference beside the 8 TB/s peak
+    copy = _copy_rate(torch, 5)
+
     # roofline of the dominant call of the step: rbq_sparse_decode (split pass + combine),
     # algorithmic bytes per call / its mean duration between HIP events on the launch stream
     kern = {}
@@ -343,13 +351,15 @@ def main():
     traffic = _measured_traffic() if dom == "sparse_decode" else None
     roofline = {"bound": "hbm", "kernel": dom, "achieved": kern[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": kern[dom]["GBps"] / HBM_PEAK_GBS, "traffic": traffic,
-                "algorithmic_bytes_per_launch": float(sbytes[dom]), "ms_per_launch": stage_ms[dom]}
+                "algorithmic_bytes_per_launch": float(sbytes[dom]), "ms_per_launch": stage_ms[dom],
+                "copy_GBps": copy["GBps"], "frac_of_copy": kern[dom]["GBps"] / copy["GBps"]}
 
     scan = None
     if not args.no_scan:
         del reps, step_graphs
         torch.cuda.empty_cache()
         scan = time_scan_c5(pipeline, gen, torch, args.steps, args.warmup)
+        scan["frac_of_copy"] = scan["GBps"] / copy["GBps"]
 
     cpu = None if args.no_cpu else cpu_baseline(wl)
     cnt = st0.sel_count.cpu().numpy()
