@@ -203,7 +203,7 @@ __global__ __launch_bounds__(kT) void topp_max_kernel(const float* __restrict__ 
 // chunk, or (fused decode step) the score kernel's per block.
 __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict__ scores, int n, int chunks,
                                                          const float* __restrict__ rmax, int nmax, float scale_log2e,
-                                                         u64* __restrict__ hist) {
+                                                         u64* __restrict__ hist, uint32_t* __restrict__ state) {
   __shared__ u64 h[kBins1];
   __shared__ float red[kTW];
   const int row = blockIdx.y, c = blockIdx.x;
@@ -211,6 +211,7 @@ __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
   const float m = row_max(rmax + int64_t(row) * nmax, nmax, red);   // barriers: h is clear after it
+  if (c == 0 && threadIdx.x == 0) state[int64_t(row) * kToppStateWords + 6] = __float_as_uint(m);   // for the next passes
 #pragma unroll
   for (int k = 0; k < kPT; ++k) {
     const u64 ms = fixed_mass(v[k], m, scale_log2e);
@@ -227,8 +228,7 @@ __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict
 // crossing, then histogram the keys inside it.
 template <int LEVEL>
 __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict__ scores, int n, int chunks,
-                                                        const float* __restrict__ rmax, int nmax, float scale_log2e,
-                                                        float p, u64* __restrict__ hist,
+                                                        float scale_log2e, float p, u64* __restrict__ hist,
                                                         uint32_t* __restrict__ state,
                                                         int32_t* __restrict__ chunk_cnt) {
   constexpr int kBins = LEVEL == 2 ? kBins2 : kBins3;
@@ -237,7 +237,6 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   __shared__ int red2[kTW];
   if (LEVEL == 3)
     for (int b = threadIdx.x; b <= kBins3; b += kT) cnt_s[b] = 0;
-  __shared__ float red[kTW];
   __shared__ Crossing cr;
   const int row = blockIdx.y, c = blockIdx.x;
   u64* rh = hist + int64_t(row) * kHistPerRow;
@@ -247,7 +246,7 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   const u64 cpre = threadIdx.x < kWave ? coarse[(LEVEL == 2 ? 0 : kCoarse) + threadIdx.x] : 0;
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
-  const float m = row_max(rmax + int64_t(row) * nmax, nmax, red);
+  const float m = __uint_as_float(st[6]);   // the row max, from level 1 (h is clear after the search's barrier)
   uint32_t prefix;
   if (LEVEL == 2) {
     find_crossing_2lvl(rh, cpre, 0, p, &cr);
@@ -258,8 +257,8 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
     prefix = (st[0] << 12) | cr.bin;
   }
   // state words: [0..2] = level-1 bin and the mass still needed inside it
-  // (written by level 2), [3..5] = the same for level 2 (written by level 3);
-  // a kernel never rewrites what it reads
+  // (written by level 2), [3..5] = the same for level 2 (written by level 3),
+  // [6] = the row max (written by level 1); a kernel never rewrites what it reads
   if (c == 0 && threadIdx.x == 0) {
     const int o = LEVEL == 2 ? 0 : 3;
     st[o] = prefix;
@@ -409,10 +408,10 @@ rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, fl
     rmax = w.chunk_max;
     nmax = chunks;
   }
-  topp_level1_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, w.hist);
-  topp_level_kernel<2><<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, p, w.hist, w.state,
+  topp_level1_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, w.hist, w.state);
+  topp_level_kernel<2><<<grid, kT, 0, stream>>>(scores, n, chunks, scale_log2e, p, w.hist, w.state,
                                                w.chunk_cnt);
-  topp_level_kernel<3><<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, p, w.hist, w.state,
+  topp_level_kernel<3><<<grid, kT, 0, stream>>>(scores, n, chunks, scale_log2e, p, w.hist, w.state,
                                                w.chunk_cnt);
   topp_write_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.hist, w.state, w.chunk_cnt, sel_idx, sel_count,
                                              masks);
