@@ -221,6 +221,58 @@ rbq_status rbq_decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int
                            int32_t* sel_idx, int32_t* sel_count, float* out, float* lse,
                            void* ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Ragged batches -- the score, selection, attention and fused-step calls for a
+ * batch whose sequences hold different numbers of keys and use different p,
+ * as a serving batch does (Algorithm 2 run per sequence; Section 3.4 for the
+ * window). Every layout is the uniform call's, with n and w the LARGEST counts:
+ * n is the row stride of scores and sel_idx, and n and w size the launches.
+ * Sequence b (query heads b*Hq .. b*Hq + Hq - 1) uses
+ *   seq_n [B] int32 (device): its indexed keys, rows [0, seq_n[b]) of the index
+ *         and of K / V, clamped to [0, n];
+ *   seq_w [B] int32 (device) or NULL: its window rows, which are its cache
+ *         tail, rows [seq_n[b], seq_n[b] + seq_w[b]) of K / V, clamped to
+ *         [0, w]; NULL gives every sequence w rows;
+ *   seq_p [B] float (device): its p. A value >= 1 selects every key; a value
+ *         <= 0 or NaN acts as the smallest positive p (the top key and its ties).
+ * The results for sequence b are those of the uniform call with B = 1, n =
+ * seq_n[b], w = seq_w[b] and p = seq_p[b] (bitwise for scores and selections).
+ * Entries of scores and sel_idx past a sequence's count are unspecified. The
+ * device counts are not checked on the host: n + w <= cap keeps every row in
+ * the cache. Workspaces: as for the uniform op with the same n and w.
+ */
+rbq_status rbq_score_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                            int32_t n, int32_t cap, const int32_t* seq_n, const uint32_t* codes,
+                            const float* kfac, const uint32_t* qplanes, const float* qscal, float* scores,
+                            hipStream_t stream);
+rbq_status rbq_topp_select_varlen(int32_t batch, int32_t heads_q, int32_t n, const int32_t* seq_n,
+                                  const float* scores, const float* seq_p, float sm_scale,
+                                  int32_t* sel_idx, int32_t* sel_count, void* ws, size_t ws_bytes,
+                                  hipStream_t stream);
+/* ws: rbq_workspace_bytes(RBQ_OP_SPARSE_DECODE / RBQ_OP_DENSE_DECODE, B, Hq, Hkv, D, n, w). */
+rbq_status rbq_sparse_decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                    const float* q, const void* K, const void* V, int32_t kv_dtype,
+                                    int32_t cap, int32_t n, int32_t w, const int32_t* seq_n,
+                                    const int32_t* seq_w, const int32_t* sel_idx, const int32_t* sel_count,
+                                    float sm_scale, float* out, float* lse, void* ws, size_t ws_bytes,
+                                    hipStream_t stream);
+rbq_status rbq_dense_decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                   const float* q, const void* K, const void* V, int32_t kv_dtype,
+                                   int32_t cap, int32_t n, int32_t w, const int32_t* seq_n,
+                                   const int32_t* seq_w, float sm_scale, float* out, float* lse,
+                                   void* ws, size_t ws_bytes, hipStream_t stream);
+/* The fused step of a ragged batch: rbq_decode_step with the calls above; the
+ * flush encodes each sequence's window rows into index rows [seq_n[b],
+ * seq_n[b] + seq_w[b]). ws: rbq_workspace_bytes(RBQ_OP_DECODE_STEP, B, Hq, Hkv, D, n, w). */
+rbq_status rbq_decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                  const float* q, const float* P, const float* c_q, const float* c_k,
+                                  const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n,
+                                  int32_t w, const int32_t* seq_n, const int32_t* seq_w, uint32_t* codes,
+                                  float* kfac, int32_t flush, const float* seq_p, float sm_scale,
+                                  uint32_t* qplanes, float* qscal, float* scores, int32_t* sel_idx,
+                                  int32_t* sel_count, float* out, float* lse, void* ws, size_t ws_bytes,
+                                  hipStream_t stream);
+
 /* Workspace bytes needed by `op` (one of RBQ_OP_*) for these sizes; 0 for an
  * unknown op or invalid sizes. Host-only, never touches the device. */
 size_t rbq_workspace_bytes(int32_t op, int32_t batch, int32_t heads_q, int32_t heads_kv,

@@ -138,3 +138,119 @@ rbq_status rbq_decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int
 }
 
 }  // extern "C"
+
+namespace {
+
+// the checks of a ragged call beyond the uniform call's: the per-sequence
+// arrays, and room for every sequence's window at its cache tail
+rbq_status check_ragged(int32_t n, int32_t w, int32_t cap, const int32_t* seq_n, const int32_t* seq_w) {
+  auto misaligned = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; };
+  if (seq_n == nullptr || misaligned(seq_n) || (seq_w != nullptr && misaligned(seq_w))) return RBQ_EINVAL;
+  if (n < 0 || w < 0 || cap < 0 || int64_t(n) + w > cap) return RBQ_EINVAL;
+  return RBQ_OK;
+}
+
+rbq_status decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                         const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n, int32_t w,
+                         const int32_t* seq_n, const int32_t* seq_w, bool sparse, const int32_t* sel_idx,
+                         const int32_t* sel_count, float sm_scale, float* out, float* lse, void* ws, size_t ws_bytes,
+                         hipStream_t stream) {
+  rbq_status s = check_ragged(n, w, cap, seq_n, seq_w);
+  if (s != RBQ_OK) return s;
+  s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, sparse, sel_idx, sel_count, K, V,
+                   cap, w, sm_scale, out, ws, ws_bytes);
+  if (s != RBQ_OK) return s;
+  return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K, V, cap, w,
+                       sm_scale, out, lse, ws, sparse, stream, nullptr, 0, seq_n, seq_w);
+}
+
+}  // namespace
+
+extern "C" {
+
+rbq_status rbq_score_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
+                            int32_t cap, const int32_t* seq_n, const uint32_t* codes, const float* kfac,
+                            const uint32_t* qplanes, const float* qscal, float* scores, hipStream_t stream) {
+  rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores);
+  if (s != RBQ_OK) return s;
+  if ((s = check_ragged(n, 0, cap, seq_n, nullptr)) != RBQ_OK) return s;
+  return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr,
+                      stream, nullptr, nullptr, 0, seq_n);
+}
+
+rbq_status rbq_topp_select_varlen(int32_t batch, int32_t heads_q, int32_t n, const int32_t* seq_n,
+                                  const float* scores, const float* seq_p, float sm_scale, int32_t* sel_idx,
+                                  int32_t* sel_count, void* ws, size_t ws_bytes, hipStream_t stream) {
+  // (p = 0.5 stands for the device values: the workspace is needed whatever they are)
+  rbq_status s = check_topp(batch, heads_q, n, scores, 0.5f, sm_scale, sel_idx, sel_count, ws, ws_bytes);
+  if (s != RBQ_OK) return s;
+  if ((s = check_ragged(n, 0, n, seq_n, nullptr)) != RBQ_OK) return s;
+  if (seq_p == nullptr || (reinterpret_cast<uintptr_t>(seq_p) & 15u) != 0) return RBQ_EINVAL;
+  return launch_topp(batch * heads_q, n, scores, 0.5f, sm_scale, sel_idx, sel_count, ws, stream, nullptr, 0, nullptr,
+                     seq_n, seq_p, heads_q);
+}
+
+rbq_status rbq_sparse_decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                                    const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n, int32_t w,
+                                    const int32_t* seq_n, const int32_t* seq_w, const int32_t* sel_idx,
+                                    const int32_t* sel_count, float sm_scale, float* out, float* lse, void* ws,
+                                    size_t ws_bytes, hipStream_t stream) {
+  return decode_varlen(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, w, seq_n, seq_w, true, sel_idx,
+                       sel_count, sm_scale, out, lse, ws, ws_bytes, stream);
+}
+
+rbq_status rbq_dense_decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                                   const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n, int32_t w,
+                                   const int32_t* seq_n, const int32_t* seq_w, float sm_scale, float* out, float* lse,
+                                   void* ws, size_t ws_bytes, hipStream_t stream) {
+  return decode_varlen(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, w, seq_n, seq_w, false, nullptr,
+                       nullptr, sm_scale, out, lse, ws, ws_bytes, stream);
+}
+
+rbq_status rbq_decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                                  const float* P, const float* c_q, const float* c_k, const void* K, const void* V,
+                                  int32_t kv_dtype, int32_t cap, int32_t n, int32_t w, const int32_t* seq_n,
+                                  const int32_t* seq_w, uint32_t* codes, float* kfac, int32_t flush,
+                                  const float* seq_p, float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
+                                  int32_t* sel_idx, int32_t* sel_count, float* out, float* lse, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
+  if (s != RBQ_OK) return s;
+  if ((s = check_ragged(n, w, cap, seq_n, seq_w)) != RBQ_OK) return s;
+  if (seq_p == nullptr || (reinterpret_cast<uintptr_t>(seq_p) & 15u) != 0) return RBQ_EINVAL;
+  const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
+  if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
+  const size_t dec_bytes = decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w);
+  const bool do_flush = flush != 0 && w > 0;
+  if ((s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal)) != RBQ_OK) return s;
+  if ((s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores)) != RBQ_OK)
+    return s;
+  if ((s = check_topp(batch, heads_q, n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, sw.topp_bytes)) !=
+      RBQ_OK)
+    return s;
+  if ((s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, true, sel_idx, sel_count, K, V,
+                        cap, w, sm_scale, out, sw.decode, dec_bytes)) != RBQ_OK)
+    return s;
+  if (do_flush && (s = check_encode(batch, heads_kv, head_dim, K, kv_dtype, cap, w, n, cap, P, c_k, codes, kfac, 0u,
+                                    nullptr, 0)) != RBQ_OK)
+    return s;
+
+  const int64_t rows = int64_t(batch) * heads_q;
+  if (do_flush)   // window rows [seq_n[b], + seq_w[b]) of K into the same index rows
+    s = launch_quantize_flush(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, K, kv_dtype, cap, w, 0, cap,
+                              codes, kfac, stream, seq_n, seq_w, n);
+  else
+    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
+  if (s != RBQ_OK) return s;
+  const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
+  s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
+                   sw.slot_max, tw.hist, rows * kHistPerRow, seq_n);
+  if (s != RBQ_OK) return s;
+  s = launch_topp(int32_t(rows), n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
+                  score_blocks_per_row(batch, heads_kv, n), sw.masks, seq_n, seq_p, heads_q);
+  if (s != RBQ_OK) return s;
+  return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K, V, cap, w,
+                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), seq_n, seq_w);
+}
+
+}  // extern "C"

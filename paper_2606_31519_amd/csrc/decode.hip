@@ -28,6 +28,13 @@
 // ALU dots (lane = row for the logits, lane = 2 dimensions for the values).
 // Waves merge in LDS; the block writes (m, l, acc[D]) per head; a combine
 // kernel merges the splits in fixed order (bitwise deterministic).
+//
+// Ragged batches (seq_n != NULL, sparse only): sequence b has seq_n[b] indexed
+// rows (clamped to [0, n]) and seq_w[b] window rows (clamped to [0, w]; all w
+// when seq_w is NULL), the window being its cache tail, rows [seq_n[b],
+// seq_n[b] + seq_w[b]) of K / V (K_loc = K, loc_ld = cap). The grid is sized
+// by n and w; a split past a sequence's rows finds none and writes an empty
+// partial state.
 #include <cmath>
 
 #include "rbq_device.h"
@@ -45,6 +52,13 @@ constexpr int kBmAll = kListCap / 32;
 constexpr float kLn2 = 0.69314718055994531f;
 __device__ __forceinline__ float wmax64(float v) { v = max32(v); return fmaxf(v, __shfl_xor(v, 32, kWave)); }
 __device__ __forceinline__ float wsum64(float v) { v = sum32(v); return v + __shfl_xor(v, 32, kWave); }
+
+// Rows of a split without a list: [c0, c0 + cn), then the folded window rows,
+// which start wsh rows after c0 + cn (0 when they follow directly).
+struct RowMap {
+  int c0, cn, wsh;
+  __device__ __forceinline__ int at(int e) const { return c0 + e + (e >= cn ? wsh : 0); }
+};
 
 // Lower bounds of x0 and x1 in the ascending a[0, cnt) (first index whose
 // value is >= x), found together by one wave: each round probes 64 evenly
@@ -272,13 +286,14 @@ __device__ __forceinline__ f32x2 load_v2(const void* rowp, int lane) {
   return static_cast<const f32x2*>(rowp)[lane];
 }
 
-template <int DT, bool SPARSE, int G>
+template <int DT, bool SPARSE, int G, bool RAGGED>
 __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     const float* __restrict__ q, const void* __restrict__ K, const void* __restrict__ V, int cap, int n,
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
     const unsigned long long* __restrict__ sel_mask, int mask_words, const void* __restrict__ K_loc,
     const void* __restrict__ V_loc, int64_t loc_ld, int w, int chunk, int idx_splits, int total_splits, int fold_s0,
-    int fold_wq, float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
+    int fold_wq, float scale_log2e, float* __restrict__ part, int Hq, int Hkv, const int32_t* __restrict__ seq_n,
+    const int32_t* __restrict__ seq_w) {
   constexpr int kElem = DT == RBQ_BF16 ? 2 : 4;
   __shared__ float qs[G][kHeadDim];
   __shared__ uint32_t bm[G][kBmAll];
@@ -297,23 +312,27 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   const int row0 = b * Hq + hk * G;     // first query head of the group
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const bool window = split >= idx_splits;
+  // this sequence's indexed and window rows (the call's n and w unless ragged)
+  const int nb = RAGGED ? min(max(seq_n[b], 0), n) : n;
+  const int wb = RAGGED && seq_w ? min(max(seq_w[b], 0), w) : w;
+  const int64_t wbase = RAGGED ? nb : 0;   // first window row in K_loc / V_loc of this sequence
   // indexed rows [c0, c1), then nwin folded window rows from row wrow0 (same buffer)
   int c0, c1, nwin = 0, wrow0 = 0;
   if (!window) {
     c0 = split * chunk;
-    c1 = min(n, c0 + chunk);
+    c1 = RAGGED ? max(c0, min(nb, c0 + chunk)) : min(n, c0 + chunk);
     if (fold_wq > 0 && split >= fold_s0) {
       const int k = split - fold_s0;
-      nwin = min(max(w - k * fold_wq, 0), fold_wq);
-      wrow0 = n + k * fold_wq;
+      nwin = min(max(wb - k * fold_wq, 0), fold_wq);
+      wrow0 = nb + k * fold_wq;
     }
   } else {
     c0 = (split - idx_splits) * kDecodeWinChunk;
-    c1 = min(w, c0 + kDecodeWinChunk);
+    c1 = RAGGED ? max(c0, min(wb, c0 + kDecodeWinChunk)) : min(w, c0 + kDecodeWinChunk);
   }
-  const char* Kbase = window ? static_cast<const char*>(K_loc) + int64_t(bh) * loc_ld * kHeadDim * kElem
+  const char* Kbase = window ? static_cast<const char*>(K_loc) + (int64_t(bh) * loc_ld + wbase) * kHeadDim * kElem
                              : static_cast<const char*>(K) + int64_t(bh) * cap * kHeadDim * kElem;
-  const char* Vbase = window ? static_cast<const char*>(V_loc) + int64_t(bh) * loc_ld * kHeadDim * kElem
+  const char* Vbase = window ? static_cast<const char*>(V_loc) + (int64_t(bh) * loc_ld + wbase) * kHeadDim * kElem
                              : static_cast<const char*>(V) + int64_t(bh) * cap * kHeadDim * kElem;
 
   constexpr bool kPreMask = G <= 4;   // (for larger groups the early load costs registers)
@@ -330,8 +349,9 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
                                        &ucount, mword);
   } else {
     __syncthreads();
-    U = max(c1 - c0, 0) + nwin;   // (dense: the window is folded only right after the last rows)
+    U = (c1 - c0) + nwin;
   }
+  const RowMap rm{c0, c1 - c0, RAGGED && nwin > 0 ? wrow0 - c1 : 0};
 
   // ---- online softmax over tiles of 64 rows, one wave per tile
   float m[G], l[G];
@@ -353,7 +373,7 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
         pos = lst[e];
         mk = hmask[e];
       } else {
-        pos = c0 + e;
+        pos = rm.at(e);
       }
     }
     float dot[G];
@@ -460,27 +480,27 @@ struct GroupLoads {
 constexpr int kSkipOffset = 0x7FFFFF00;
 
 template <bool SPARSE>
-__device__ __forceinline__ int row_at(int e, bool list, int c0, const int32_t* lst) {
+__device__ __forceinline__ int row_at(int e, bool list, const RowMap& rm, const int32_t* lst) {
   if constexpr (SPARSE) {
     const int lv = lst[e];
-    return list ? lv : c0 + e;
+    return list ? lv : rm.at(e);
   }
-  return c0 + e;
+  return rm.at(e);
 }
 
 template <bool SPARSE>
-__device__ __forceinline__ void load_group_k(GroupLoads& d, int grp, bool skip, int U, int c0, bool list,
+__device__ __forceinline__ void load_group_k(GroupLoads& d, int grp, bool skip, int U, const RowMap& rm, bool list,
                                              const int32_t* lst, __amdgpu_buffer_rsrc_t Kr, int x, int j) {
   const int e0 = grp * kGroupRows;
   const int ek = e0 + x < U ? e0 + x : e0;
-  const int pk = row_at<SPARSE>(ek, list, c0, lst);
+  const int pk = row_at<SPARSE>(ek, list, rm, lst);
   const int off = skip ? kSkipOffset : pk * (kHeadDim * 2) + 16 * j;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 64 * kb, 0, 0);
 }
 
 template <bool SPARSE, int G>
-__device__ __forceinline__ void load_group_v(GroupLoads& d, int grp, bool skip, int U, int c0, bool list,
+__device__ __forceinline__ void load_group_v(GroupLoads& d, int grp, bool skip, int U, const RowMap& rm, bool list,
                                              const int32_t* lst, const uint16_t* hmask,
                                              __amdgpu_buffer_rsrc_t Vr, int x, int j) {
   const int e0 = grp * kGroupRows;
@@ -490,7 +510,7 @@ __device__ __forceinline__ void load_group_v(GroupLoads& d, int grp, bool skip, 
     const int e = e0 + 4 * j + i;
     const bool valid = e < U;
     const int ev = valid ? e : e0;
-    const int pv = row_at<SPARSE>(ev, list, c0, lst);
+    const int pv = row_at<SPARSE>(ev, list, rm, lst);
     const int off = skip ? kSkipOffset : pv * (kHeadDim * 2) + 16 * x;
     d.v[i] = __builtin_amdgcn_raw_buffer_load_b128(Vr, off, 0, 0);
     bool on = valid && x < G;
@@ -500,13 +520,14 @@ __device__ __forceinline__ void load_group_v(GroupLoads& d, int grp, bool skip, 
   d.mk = mk;
 }
 
-template <bool SPARSE, int G>
+template <bool SPARSE, int G, bool RAGGED>
 __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     const float* __restrict__ q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V, int cap, int n,
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
     const unsigned long long* __restrict__ sel_mask, int mask_words, const uint16_t* __restrict__ K_loc,
     const uint16_t* __restrict__ V_loc, int64_t loc_ld, int w, int chunk, int idx_splits, int total_splits,
-    int fold_s0, int fold_wq, float scale_log2e, float* __restrict__ part, int Hq, int Hkv) {
+    int fold_s0, int fold_wq, float scale_log2e, float* __restrict__ part, int Hq, int Hkv,
+    const int32_t* __restrict__ seq_n, const int32_t* __restrict__ seq_w) {
   static_assert(G >= 1 && G <= 16, "the MFMA tiles hold at most 16 heads");
   constexpr bool kPackedQ = kQParts * G <= 16;
   constexpr int kQOps = kPackedQ ? 1 : kQParts;
@@ -527,23 +548,27 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   const int wave = threadIdx.x / kWave, lane = lane_id();
   const int x = lane & 15, j = lane >> 4;
   const bool window = split >= idx_splits;
+  // this sequence's indexed and window rows (the call's n and w unless ragged)
+  const int nb = RAGGED ? min(max(seq_n[b], 0), n) : n;
+  const int wb = RAGGED && seq_w ? min(max(seq_w[b], 0), w) : w;
+  const int64_t wbase = RAGGED ? nb : 0;   // first window row in K_loc / V_loc of this sequence
   // indexed rows [c0, c1), then nwin folded window rows from row wrow0 (same buffer)
   int c0, c1, nwin = 0, wrow0 = 0;
   if (!window) {
     c0 = split * chunk;
-    c1 = min(n, c0 + chunk);
+    c1 = RAGGED ? max(c0, min(nb, c0 + chunk)) : min(n, c0 + chunk);
     if (fold_wq > 0 && split >= fold_s0) {
       const int k = split - fold_s0;
-      nwin = min(max(w - k * fold_wq, 0), fold_wq);
-      wrow0 = n + k * fold_wq;
+      nwin = min(max(wb - k * fold_wq, 0), fold_wq);
+      wrow0 = nb + k * fold_wq;
     }
   } else {
     c0 = (split - idx_splits) * kDecodeWinChunk;
-    c1 = min(w, c0 + kDecodeWinChunk);
+    c1 = RAGGED ? max(c0, min(wb, c0 + kDecodeWinChunk)) : min(w, c0 + kDecodeWinChunk);
   }
-  const uint16_t* Kb = window ? K_loc + int64_t(bh) * loc_ld * kHeadDim : K + int64_t(bh) * cap * kHeadDim;
-  const uint16_t* Vb = window ? V_loc + int64_t(bh) * loc_ld * kHeadDim : V + int64_t(bh) * cap * kHeadDim;
-  const uint32_t region = uint32_t(window ? w : n + (fold_wq > 0 ? w : 0)) * uint32_t(kHeadDim * 2);   // < 2^31
+  const uint16_t* Kb = window ? K_loc + (int64_t(bh) * loc_ld + wbase) * kHeadDim : K + int64_t(bh) * cap * kHeadDim;
+  const uint16_t* Vb = window ? V_loc + (int64_t(bh) * loc_ld + wbase) * kHeadDim : V + int64_t(bh) * cap * kHeadDim;
+  const uint32_t region = uint32_t(window ? wb : nb + (fold_wq > 0 ? wb : 0)) * uint32_t(kHeadDim * 2);   // < 2^31
   const __amdgpu_buffer_rsrc_t Kr = make_rsrc(Kb, region);
   const __amdgpu_buffer_rsrc_t Vr = make_rsrc(Vb, region);
   constexpr bool kPreMask = kPackedQ;   // (for larger groups the early load costs registers)
@@ -588,9 +613,10 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
                                        &ucount, mword);
   } else {
     __syncthreads();
-    U = max(c1 - c0, 0) + nwin;   // (dense: the window is folded only right after the last rows)
+    U = (c1 - c0) + nwin;
   }
   const bool list = SPARSE && !window;
+  const RowMap rm{c0, c1 - c0, RAGGED && nwin > 0 ? wrow0 - c1 : 0};
 
   float m = -INFINITY, lsum = 0.f;      // head x's running max (uniform over j) and this lane's partial sum
   f32x4 acc[4][2];                      // lane (x, j), reg i: head 4j + i, dimension 8x + 2t + par
@@ -603,8 +629,8 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   GroupLoads cur;
   int grp = wave;
   if (grp < ngroups) {
-    load_group_k<SPARSE>(cur, grp, false, U, c0, list, lst, Kr, x, j);
-    load_group_v<SPARSE, G>(cur, grp, false, U, c0, list, lst, hmask, Vr, x, j);
+    load_group_k<SPARSE>(cur, grp, false, U, rm, list, lst, Kr, x, j);
+    load_group_v<SPARSE, G>(cur, grp, false, U, rm, list, lst, hmask, Vr, x, j);
   }
   while (grp < ngroups) {
     const int nxt = grp + kDWaves;
@@ -624,7 +650,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, qp[(kb * kQOps + op) * kWave]), s,
                                                     0, 0, 0);
     }
-    load_group_k<SPARSE>(cur, last ? grp : nxt, last, U, c0, list, lst, Kr, x, j);
+    load_group_k<SPARSE>(cur, last ? grp : nxt, last, U, rm, list, lst, Kr, x, j);
     if constexpr (kPackedQ) {
       // column h + G and h + 2G hold the mid and lo parts of head h's logits
       // (each element goes through an opaque copy first: hipcc 7.2 miscompiles
@@ -697,7 +723,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
         acc[t][par] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a_lo, bv, acc[t][par], 0, 0, 0);
       }
     }
-    load_group_v<SPARSE, G>(cur, last ? grp : nxt, last, U, c0, list, lst, hmask, Vr, x, j);
+    load_group_v<SPARSE, G>(cur, last ? grp : nxt, last, U, rm, list, lst, hmask, Vr, x, j);
     grp = nxt;
   }
 
@@ -799,23 +825,23 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(const floa
   }
 }
 
-template <int DT, bool SPARSE>
+template <int DT, bool SPARSE, bool RAGGED>
 rbq_status launch_g(int G, dim3 grid, hipStream_t stream, const float* q, const void* K, const void* V, int cap,
                     int n, const int32_t* sel_idx, const int32_t* sel_count, const unsigned long long* sel_mask,
                     int mask_words, const void* K_loc, const void* V_loc, int64_t loc_ld, int w, int chunk,
                     int idx_splits, int total, int fold_s0, int fold_wq, float scale_log2e, float* part, int Hq,
-                    int Hkv) {
+                    int Hkv, const int32_t* seq_n, const int32_t* seq_w) {
 #define RBQ_DECODE_CASE(GG)                                                                                       \
   case GG:                                                                                                        \
-    if (DT == RBQ_BF16)                                                                                           \
-      decode_mfma_kernel<SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                             \
+    if constexpr (DT == RBQ_BF16)                                                                                 \
+      decode_mfma_kernel<SPARSE, GG, RAGGED><<<grid, kDThreads, 0, stream>>>(                                     \
           q, static_cast<const uint16_t*>(K), static_cast<const uint16_t*>(V), cap, n, sel_idx, sel_count,        \
           sel_mask, mask_words, static_cast<const uint16_t*>(K_loc), static_cast<const uint16_t*>(V_loc), loc_ld, \
-          w, chunk, idx_splits, total, fold_s0, fold_wq, scale_log2e, part, Hq, Hkv);                             \
+          w, chunk, idx_splits, total, fold_s0, fold_wq, scale_log2e, part, Hq, Hkv, seq_n, seq_w);               \
     else                                                                                                          \
-      decode_vec_kernel<DT, SPARSE, GG><<<grid, kDThreads, 0, stream>>>(                                          \
+      decode_vec_kernel<DT, SPARSE, GG, RAGGED><<<grid, kDThreads, 0, stream>>>(                                  \
           q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, loc_ld, w, chunk, idx_splits,  \
-          total, fold_s0, fold_wq, scale_log2e, part, Hq, Hkv);                                                   \
+          total, fold_s0, fold_wq, scale_log2e, part, Hq, Hkv, seq_n, seq_w);                                     \
     break;
   switch (G) {
     RBQ_DECODE_CASE(1)
@@ -836,27 +862,44 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                          const void* V, int32_t kv_dtype, int32_t cap, int32_t n, const int32_t* sel_idx,
                          const int32_t* sel_count, const void* K_loc, const void* V_loc, int64_t loc_ld, int32_t w,
                          float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream,
-                         const unsigned long long* sel_mask, int32_t mask_words) {
+                         const unsigned long long* sel_mask, int32_t mask_words, const int32_t* seq_n,
+                         const int32_t* seq_w) {
   const int G = heads_q / heads_kv;
-  // the window rows are the cache tail when they sit right after the indexed rows of every (b, kv-head)
   const size_t elem = kv_dtype == RBQ_BF16 ? 2 : 4;
+  if (seq_n) {   // ragged: every sequence's window is its own cache tail
+    K_loc = K;
+    V_loc = V;
+    loc_ld = cap;
+  } else {
+    seq_w = nullptr;
+  }
+  // the window rows are the cache tail when they sit right after the indexed rows of every (b, kv-head)
   const bool tail = n > 0 && w > 0 && loc_ld == cap &&
-                    static_cast<const char*>(K_loc) == static_cast<const char*>(K) + size_t(n) * kHeadDim * elem &&
-                    static_cast<const char*>(V_loc) == static_cast<const char*>(V) + size_t(n) * kHeadDim * elem &&
+                    (seq_n != nullptr ||
+                     (static_cast<const char*>(K_loc) == static_cast<const char*>(K) + size_t(n) * kHeadDim * elem &&
+                      static_cast<const char*>(V_loc) == static_cast<const char*>(V) + size_t(n) * kHeadDim * elem)) &&
                     (int64_t(n) + w) * kHeadDim * int64_t(elem) < (int64_t(1) << 31);
   const DecodeSplits sp = decode_splits(batch, heads_kv, n, w, tail, sparse);
   const dim3 grid(sp.total(), batch * heads_kv);
   float* part = static_cast<float*>(ws);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
   rbq_status st;
-#define RBQ_DECODE_LAUNCH(DT, SP)                                                                                  \
-  launch_g<DT, SP>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, loc_ld, \
+#define RBQ_DECODE_LAUNCH(DT, SP, RG)                                                                              \
+  launch_g<DT, SP, RG>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, loc_ld, \
                    w, sp.chunk, sp.idx_splits, sp.total(), sp.fold_s0, sp.fold_wq, scale_log2e, part, heads_q,      \
-                   heads_kv)
-  if (kv_dtype == RBQ_BF16)
-    st = sparse ? RBQ_DECODE_LAUNCH(RBQ_BF16, true) : RBQ_DECODE_LAUNCH(RBQ_BF16, false);
-  else
-    st = sparse ? RBQ_DECODE_LAUNCH(RBQ_F32, true) : RBQ_DECODE_LAUNCH(RBQ_F32, false);
+                   heads_kv, seq_n, seq_w)
+  const bool rg = seq_n != nullptr;
+  if (kv_dtype == RBQ_BF16) {
+    if (rg)
+      st = sparse ? RBQ_DECODE_LAUNCH(RBQ_BF16, true, true) : RBQ_DECODE_LAUNCH(RBQ_BF16, false, true);
+    else
+      st = sparse ? RBQ_DECODE_LAUNCH(RBQ_BF16, true, false) : RBQ_DECODE_LAUNCH(RBQ_BF16, false, false);
+  } else {
+    if (rg)
+      st = sparse ? RBQ_DECODE_LAUNCH(RBQ_F32, true, true) : RBQ_DECODE_LAUNCH(RBQ_F32, false, true);
+    else
+      st = sparse ? RBQ_DECODE_LAUNCH(RBQ_F32, true, false) : RBQ_DECODE_LAUNCH(RBQ_F32, false, false);
+  }
 #undef RBQ_DECODE_LAUNCH
   if (st != RBQ_OK) return st;
   decode_combine_kernel<<<dim3(batch * heads_q, kCombSlices), kCombThreads, 0, stream>>>(part, sp.total(), out,

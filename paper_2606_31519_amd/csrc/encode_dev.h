@@ -32,6 +32,12 @@ struct EncodeArgs {
   float* kfac;
   float* alpha_out;        // or NULL
   float* rot_out;          // or NULL
+  // Ragged batches (encode_tiles<..., true>): sequence b encodes min(seq_cnt[b], n_new)
+  // keys (n_new when seq_cnt is NULL) from row o = min(seq_off[b], off_max) of
+  // its block of `keys` into index rows [offset + o, ...); hkv maps (b, kv-head) to b.
+  const int32_t* seq_off;
+  const int32_t* seq_cnt;
+  int off_max, hkv;
 };
 
 // Blocks per (b, kv-head) of an encode over n_new keys: enough to cover the
@@ -72,11 +78,21 @@ __device__ __forceinline__ void fold_lanes(float* v, int lane) {
 }
 
 // The tiles bx, bx + gx, ... of (b, kv-head) bh, by the 256 threads of the calling block.
-template <int DT, bool ROT>
+template <int DT, bool ROT, bool RAGGED = false>
 __device__ __forceinline__ void encode_tiles(const EncodeArgs& ea, int bh, int bx, int gx) {
-  const void* __restrict__ keys = ea.keys;
   const int64_t keys_ld = ea.keys_ld;
-  const int n_new = ea.n_new, offset = ea.offset, cap = ea.cap;
+  int n_new = ea.n_new, offset = ea.offset;
+  const int cap = ea.cap;
+  int64_t krow0 = 0;   // first key row of this (b, kv-head) inside its block of `keys`
+  if (RAGGED) {
+    const int b = bh / ea.hkv;
+    const int o = min(max(ea.seq_off[b], 0), ea.off_max);
+    if (ea.seq_cnt) n_new = min(max(ea.seq_cnt[b], 0), n_new);
+    offset += o;
+    krow0 = o;
+  }
+  if (RAGGED && n_new == 0) return;   // block-uniform: nothing to encode for this (b, kv-head)
+  const char* __restrict__ keys = static_cast<const char*>(ea.keys) + krow0 * kHeadDim * (DT == RBQ_BF16 ? 2 : 4);
   const float* __restrict__ P = ea.P;
   const float* __restrict__ c_q = ea.c_q;
   const float* __restrict__ c_k = ea.c_k;
@@ -107,8 +123,8 @@ __device__ __forceinline__ void encode_tiles(const EncodeArgs& ea, int bh, int b
       const int pidx = j * kEncThreads + threadIdx.x;
       const int row = pidx / kPiecesPerRow, piece = pidx % kPiecesPerRow;
       const int key = min(tl * kTileKeys + row, n_new - 1);
-      pc[j] = *reinterpret_cast<const u32x4*>(static_cast<const char*>(keys) +
-                                              ((int64_t(bh) * keys_ld + key) * kHeadDim) * kElemBytes + piece * 16);
+      pc[j] = *reinterpret_cast<const u32x4*>(keys + ((int64_t(bh) * keys_ld + key) * kHeadDim) * kElemBytes +
+                                              piece * 16);
     }
   };
   if (bx < tiles) load_tile(bx);

@@ -182,14 +182,14 @@ __global__ __launch_bounds__(kQAll) void quantize_kernel(QuantArgs qa) { quantiz
 // decode step (they are independent): blocks [0, rows) quantise one query
 // head each, the others encode the window keys as encode_kernel would.
 static_assert(kQAll == kEncThreads, "both roles run on blocks of the same size");
-template <int DT>
+template <int DT, bool RAGGED>
 __global__ __launch_bounds__(kQAll) void quantize_flush_kernel(QuantArgs qa, EncodeArgs ea, int rows, int per_head) {
   const int blk = blockIdx.x;
   if (blk < rows) {
     quantize_row(qa, blk);
   } else {
     const int e = blk - rows;
-    encode_tiles<DT, false>(ea, e / per_head, e % per_head, per_head);
+    encode_tiles<DT, false, RAGGED>(ea, e / per_head, e % per_head, per_head);
   }
 }
 
@@ -206,18 +206,28 @@ rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, con
 rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                                  const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal,
                                  const void* keys, int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset,
-                                 int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream) {
+                                 int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream, const int32_t* seq_off,
+                                 const int32_t* seq_cnt, int32_t off_max) {
   if (n_new == 0)
     return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
   const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, nullptr, heads_q, heads_kv};
-  const EncodeArgs ea{keys, keys_ld, n_new, offset, cap, P, c_q, c_k, codes, kfac, nullptr, nullptr};
+  const EncodeArgs ea{keys,  keys_ld, n_new,   offset,  cap,     P,       c_q,     c_k,     codes,
+                      kfac,  nullptr, nullptr, seq_off, seq_cnt, off_max, heads_kv};
   const int rows = batch * heads_q, bhs = batch * heads_kv;
   const int per_head = encode_blocks_per_head(n_new, bhs);
   const int blocks = rows + per_head * bhs;
-  if (keys_dtype == RBQ_BF16)
-    quantize_flush_kernel<RBQ_BF16><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
-  else
-    quantize_flush_kernel<RBQ_F32><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+  const bool rg = seq_off != nullptr;
+  if (keys_dtype == RBQ_BF16) {
+    if (rg)
+      quantize_flush_kernel<RBQ_BF16, true><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+    else
+      quantize_flush_kernel<RBQ_BF16, false><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+  } else {
+    if (rg)
+      quantize_flush_kernel<RBQ_F32, true><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+    else
+      quantize_flush_kernel<RBQ_F32, false><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+  }
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

@@ -110,27 +110,39 @@ rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, con
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
                            hipStream_t stream);
 // query quantisation and, in the same launch, the lazy encode of n_new window
-// keys into index rows [offset, offset + n_new) with the existing c_k
+// keys into index rows [offset, offset + n_new) with the existing c_k (ragged,
+// seq_off != NULL: sequence b encodes min(seq_cnt[b], n_new) keys (n_new without
+// seq_cnt) from row min(seq_off[b], off_max) of its block of `keys` into index
+// rows offset + that row onwards)
 rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                                  const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal,
                                  const void* keys, int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset,
-                                 int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream);
+                                 int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream,
+                                 const int32_t* seq_off = nullptr, const int32_t* seq_cnt = nullptr,
+                                 int32_t off_max = 0);
 // slot_max (fused decode step): [B * Hq][score_blocks_per_row()] block maxima of the
-// scores, with hist[0, hist_words) zeroed by the same launch; NULL otherwise
+// scores, with hist[0, hist_words) zeroed by the same launch; NULL otherwise.
+// seq_n (ragged batches): [B] indexed keys per sequence, clamped to [0, n]; n is the row stride
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream,
-                        float* slot_max = nullptr, unsigned long long* hist = nullptr, int64_t hist_words = 0);
+                        float* slot_max = nullptr, unsigned long long* hist = nullptr, int64_t hist_words = 0,
+                        const int32_t* seq_n = nullptr);
 // slot_max / nslots: per-row partial maxima written by launch_score together with
 // the zeroing of the workspace's counters (the max pass is skipped); masks:
-// optional [rows][topp_mask_words(n)] selection bitmaps (bit i of word k = key 64 k + i)
+// optional [rows][topp_mask_words(n)] selection bitmaps (bit i of word k = key 64 k + i);
+// seq_n / seq_p (ragged batches): [B] keys and p per sequence, row r of sequence r / heads_q
 rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,
                        int32_t* sel_count, void* ws, hipStream_t stream, const float* slot_max = nullptr,
-                       int32_t nslots = 0, unsigned long long* masks = nullptr);
+                       int32_t nslots = 0, unsigned long long* masks = nullptr, const int32_t* seq_n = nullptr,
+                       const float* seq_p = nullptr, int32_t heads_q = 1);
 rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const void* K,
                          const void* V, int32_t kv_dtype, int32_t cap, int32_t n, const int32_t* sel_idx,
                          const int32_t* sel_count, const void* K_loc, const void* V_loc, int64_t loc_ld, int32_t w,
                          float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream,
-                         const unsigned long long* sel_mask = nullptr, int32_t mask_words = 0);
+                         const unsigned long long* sel_mask = nullptr, int32_t mask_words = 0,
+                         const int32_t* seq_n = nullptr, const int32_t* seq_w = nullptr);
+// (ragged: seq_n / seq_w [B] indexed and window rows per sequence, the window
+// being the sequence's cache tail; K_loc, V_loc and loc_ld are then ignored)
 
 }  // namespace rbq

@@ -22,6 +22,10 @@
 // whole decode step too, although the Top-p passes read the scores next).
 // Blocks that lie wholly inside [0, n) take a path without per-key guards.
 // The scan is HBM-bound at G = 4 and at G = 8.
+// Ragged batches (seq_n != NULL): sequence b has seq_n[b] indexed keys
+// (clamped to [0, n]); n is the row stride of the scores and bounds the grid.
+// Loads are clamped to n - 1, so the key count's load overlaps them (keys past
+// a sequence's count are computed from whatever the rows hold and never stored).
 #include "rbq_device.h"
 #include "rbq_internal.h"
 
@@ -88,11 +92,12 @@ struct ScoreSlots {
   int64_t hist_words;
 };
 
-template <int KPT, bool INTS, bool SLOTS>
+template <int KPT, bool INTS, bool SLOTS, bool RAGGED>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const u32x4* __restrict__ codes, const f32x2* __restrict__ kfac, const uint32_t* __restrict__ qplanes,
     const float* __restrict__ qscal, float* __restrict__ scores, int32_t* __restrict__ ip_out,
-    int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl) {
+    int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
+    const int32_t* __restrict__ seq_n) {
   __shared__ uint32_t qn_s[kMaxGroup][16];
   __shared__ float mx_s[SLOTS ? kMaxGroup : 1][kHalfWaves];
   const int bh = blockIdx.y;                 // b * Hkv + kv head
@@ -100,7 +105,6 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   const int hk = bh - b * Hkv;
   const int64_t kbase = int64_t(bh) * cap;
   const int i0 = blockIdx.x * (kScoreThreads * KPT) + threadIdx.x;
-  const bool full = (blockIdx.x + 1) * (kScoreThreads * KPT) <= n;   // block-uniform: no key past n
   const int row0 = b * Hq + hk * G;
 
   u32x4 c[KPT];
@@ -112,11 +116,17 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     if (!INTS) fg[u] = __builtin_nontemporal_load(kfac + kbase + i);
   }
   if (SLOTS) {   // this block's share of the counters
-    const int64_t nb = int64_t(gridDim.x) * gridDim.y, lb = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
-    const int64_t per = (sl.hist_words + nb - 1) / nb;
+    const int64_t nblk = int64_t(gridDim.x) * gridDim.y, lb = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
+    const int64_t per = (sl.hist_words + nblk - 1) / nblk;
     const int64_t e1 = min(sl.hist_words, (lb + 1) * per);
     for (int64_t e = lb * per + threadIdx.x; e < e1; e += kScoreThreads) sl.hist[e] = 0ull;
   }
+  const int nb = RAGGED ? min(max(seq_n[b], 0), n) : n;   // this sequence's indexed keys
+  if (RAGGED && int(blockIdx.x) * (kScoreThreads * KPT) >= nb) {   // block-uniform: no key of this block is indexed
+    if (SLOTS && int(threadIdx.x) < G) sl.slot_max[int64_t(row0 + threadIdx.x) * gridDim.x + blockIdx.x] = -INFINITY;
+    return;
+  }
+  const bool full = (blockIdx.x + 1) * (kScoreThreads * KPT) <= nb;   // block-uniform: no key past nb
   if (threadIdx.x < 4 * G) {                  // one lane per (head, word)
     const int h = threadIdx.x >> 2, w = threadIdx.x & 3;
     const uint32_t* Q = qplanes + int64_t(row0 + h) * 16 + w;   // [plane][word]
@@ -133,7 +143,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     e[u] = spread_code(c[u]);
     if (INTS) {
       const int i = i0 + u * kScoreThreads;
-      if (i < n) pc_out[int64_t(bh) * n + i] = pc;
+      if (i < nb) pc_out[int64_t(bh) * n + i] = pc;
     }
   }
   __syncthreads();
@@ -185,12 +195,12 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       const int i = i0 + u * kScoreThreads;
       const int ip = int(binary_int4_dot(e[u], qn));
       if (INTS) {
-        if (i < n) ip_out[int64_t(row) * n + i] = ip;
+        if (i < nb) ip_out[int64_t(row) * n + i] = ip;
       } else {
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         const float sc = fmaf(fg[u].x, y, B0 + fg[u].y);
-        if (i < n) {
+        if (i < nb) {
           if (SLOTS) mx = fmaxf(mx, sc);
           __builtin_nontemporal_store(sc, out + i);
         }
@@ -204,24 +214,25 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
 }
 
-template <bool INTS, bool SLOTS>
+template <bool INTS, bool SLOTS, bool RAGGED>
 rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
                       const uint32_t* qplanes, const float* qscal, float* scores, int32_t* ip_out,
-                      int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl) {
+                      int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
+                      const int32_t* seq_n) {
   const u32x4* c4 = reinterpret_cast<const u32x4*>(codes);
   const f32x2* f2 = reinterpret_cast<const f32x2*>(kfac);
   switch (kpt) {
     case 4:
-      score_kernel<4, INTS, SLOTS><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
-                                                                       n, cap, Hq, Hkv, G, sl);
+      score_kernel<4, INTS, SLOTS, RAGGED><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
+                                                                       n, cap, Hq, Hkv, G, sl, seq_n);
       break;
     case 2:
-      score_kernel<2, INTS, SLOTS><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
-                                                                       n, cap, Hq, Hkv, G, sl);
+      score_kernel<2, INTS, SLOTS, RAGGED><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
+                                                                       n, cap, Hq, Hkv, G, sl, seq_n);
       break;
     default:
-      score_kernel<1, INTS, SLOTS><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
-                                                                       n, cap, Hq, Hkv, G, sl);
+      score_kernel<1, INTS, SLOTS, RAGGED><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
+                                                                       n, cap, Hq, Hkv, G, sl, seq_n);
       break;
   }
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
@@ -232,20 +243,20 @@ rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* co
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, float* slot_max,
-                        unsigned long long* hist, int64_t hist_words) {
+                        unsigned long long* hist, int64_t hist_words, const int32_t* seq_n) {
   if (n == 0) return RBQ_OK;
   const int G = heads_q / heads_kv;
   const int kpt = score_keys_per_lane(batch, heads_kv, n);
   dim3 grid(score_blocks_per_row(batch, heads_kv, n), batch * heads_kv);
   const ScoreSlots sl{slot_max, hist, hist_words};
-  if (ip_out != nullptr)
-    return launch_kpt<true, false>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap,
-                                   heads_q, heads_kv, G, sl);
-  if (slot_max != nullptr)
-    return launch_kpt<false, true>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap,
-                                   heads_q, heads_kv, G, sl);
-  return launch_kpt<false, false>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap,
-                                  heads_q, heads_kv, G, sl);
+#define RBQ_SCORE_LAUNCH(I, S, R)                                                                            \
+  launch_kpt<I, S, R>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap, heads_q, \
+                      heads_kv, G, sl, seq_n)
+  if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false);   // (the integer hook is never ragged)
+  if (seq_n != nullptr)
+    return slot_max != nullptr ? RBQ_SCORE_LAUNCH(false, true, true) : RBQ_SCORE_LAUNCH(false, false, true);
+  return slot_max != nullptr ? RBQ_SCORE_LAUNCH(false, true, false) : RBQ_SCORE_LAUNCH(false, false, false);
+#undef RBQ_SCORE_LAUNCH
 }
 
 }  // namespace rbq

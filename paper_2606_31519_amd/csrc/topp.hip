@@ -31,6 +31,12 @@
 //                (count above + suffix count at b3); ascending compaction
 // Every pass issues its 16 loads per thread up front (indices clamped, the
 // out-of-range values masked), so a pass costs one memory round trip.
+//
+// Ragged batches (seq_n / seq_p != NULL): row r of sequence b = r / Hq has
+// seq_n[b] keys (clamped to [0, n]; n stays the row stride and sizes the grid)
+// and its own p = seq_p[b]. Blocks past a row's keys leave at once; rows whose
+// p is >= 1 (or that have no keys) skip the histogram passes, and the write
+// pass selects every key of them.
 #include <cmath>
 
 #include "rbq_device.h"
@@ -174,22 +180,44 @@ __device__ __forceinline__ void load_chunk(const float* __restrict__ s, int n, i
 }
 __device__ __forceinline__ bool in_row(int n, int c, int k) { return c * kChunk + k * kT + int(threadIdx.x) < n; }
 
+// A row's key count and p: the call's, or its sequence's in a ragged batch. A
+// p outside (0, 1] is clamped into it (<= 0 or NaN: the smallest positive p,
+// which keeps the top key and its ties).
+struct RowSel {
+  int n;
+  float p;
+};
+__device__ __forceinline__ RowSel row_sel(const int32_t* __restrict__ seq_n, const float* __restrict__ seq_p, int hq,
+                                          int row, int n, float p) {
+  RowSel r{n, p};
+  const int b = row / hq;
+  if (seq_n) r.n = min(max(seq_n[b], 0), n);
+  if (seq_p) {
+    const float v = seq_p[b];
+    r.p = v > 0.f ? fminf(v, 1.f) : 1e-30f;
+  }
+  return r;
+}
+
 __device__ __forceinline__ float row_max(const float* __restrict__ part_max, int nmax, float* red) {
   float m = -INFINITY;
   for (int k = threadIdx.x; k < nmax; k += kT) m = fmaxf(m, part_max[k]);
   return block_max(m, red);
 }
 
+template <bool RAGGED>
 __global__ __launch_bounds__(kT) void topp_max_kernel(const float* __restrict__ scores, int n, int chunks,
-                                                      float* __restrict__ chunk_max, u64* __restrict__ hist) {
+                                                      float* __restrict__ chunk_max, u64* __restrict__ hist,
+                                                      const int32_t* __restrict__ seq_n, int hq) {
   __shared__ float red[kTW];
   const int row = blockIdx.y, c = blockIdx.x;
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
+  const int nr = RAGGED ? row_sel(seq_n, nullptr, hq, row, n, 1.f).n : n;
   float m = -INFINITY;
 #pragma unroll
   for (int k = 0; k < kPT; ++k)
-    if (in_row(n, c, k)) m = fmaxf(m, v[k]);
+    if (in_row(nr, c, k)) m = fmaxf(m, v[k]);
   m = block_max(m, red);
   if (threadIdx.x == 0) chunk_max[int64_t(row) * chunks + c] = m;
   // this block's share of the row's histogram counters
@@ -201,21 +229,26 @@ __global__ __launch_bounds__(kT) void topp_max_kernel(const float* __restrict__ 
 
 // The row maximum comes from nmax partial maxima per row: the max kernel's per
 // chunk, or (fused decode step) the score kernel's per block.
+template <bool RAGGED>
 __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict__ scores, int n, int chunks,
                                                          const float* __restrict__ rmax, int nmax, float scale_log2e,
-                                                         u64* __restrict__ hist, uint32_t* __restrict__ state) {
+                                                         float p, u64* __restrict__ hist, uint32_t* __restrict__ state,
+                                                         const int32_t* __restrict__ seq_n,
+                                                         const float* __restrict__ seq_p, int hq) {
   __shared__ u64 h[kBins1];
   __shared__ float red[kTW];
   const int row = blockIdx.y, c = blockIdx.x;
   for (int b = threadIdx.x; b < kBins1; b += kT) h[b] = 0;
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
+  const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, row, n, p) : RowSel{n, p};
+  if (RAGGED && (c * kChunk >= rs.n || rs.p >= 1.f)) return;   // block-uniform: nothing of this row to histogram here
   const float m = row_max(rmax + int64_t(row) * nmax, nmax, red);   // barriers: h is clear after it
   if (c == 0 && threadIdx.x == 0) state[int64_t(row) * kToppStateWords + 6] = __float_as_uint(m);   // for the next passes
 #pragma unroll
   for (int k = 0; k < kPT; ++k) {
     const u64 ms = fixed_mass(v[k], m, scale_log2e);
-    if (in_row(n, c, k) && ms) atomicAdd(&h[score_key(v[k]) >> 20], ms);
+    if (in_row(rs.n, c, k) && ms) atomicAdd(&h[score_key(v[k]) >> 20], ms);
   }
   __syncthreads();
   u64* g = hist + int64_t(row) * kHistPerRow;
@@ -226,11 +259,13 @@ __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict
 
 // Level 2 (LEVEL == 2) or level 3 (LEVEL == 3): find the previous level's
 // crossing, then histogram the keys inside it.
-template <int LEVEL>
+template <int LEVEL, bool RAGGED>
 __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict__ scores, int n, int chunks,
                                                         float scale_log2e, float p, u64* __restrict__ hist,
                                                         uint32_t* __restrict__ state,
-                                                        int32_t* __restrict__ chunk_cnt) {
+                                                        int32_t* __restrict__ chunk_cnt,
+                                                        const int32_t* __restrict__ seq_n,
+                                                        const float* __restrict__ seq_p, int hq) {
   constexpr int kBins = LEVEL == 2 ? kBins2 : kBins3;
   __shared__ u64 h[kBins];
   __shared__ uint32_t cnt_s[LEVEL == 3 ? kBins3 + 1 : 1];
@@ -246,10 +281,12 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   const u64 cpre = threadIdx.x < kWave ? coarse[(LEVEL == 2 ? 0 : kCoarse) + threadIdx.x] : 0;
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
+  const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, row, n, p) : RowSel{n, p};
+  if (RAGGED && (c * kChunk >= rs.n || rs.p >= 1.f)) return;   // block-uniform (the write pass handles p >= 1)
   const float m = __uint_as_float(st[6]);   // the row max, from level 1 (h is clear after the search's barrier)
   uint32_t prefix;
   if (LEVEL == 2) {
-    find_crossing_2lvl(rh, cpre, 0, p, &cr);
+    find_crossing_2lvl(rh, cpre, 0, rs.p, &cr);
     prefix = cr.bin;
   } else {
     const u64 T = (u64(st[2]) << 32) | st[1];
@@ -269,7 +306,7 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   int above = 0;   // level 3: keys above the 24-bit bin, certainly selected
 #pragma unroll
   for (int k = 0; k < kPT; ++k) {
-    if (!in_row(n, c, k)) continue;
+    if (!in_row(rs.n, c, k)) continue;
     const uint32_t key = score_key(v[k]);
     if ((key >> shift_hi) == prefix) {
       const uint32_t bin = LEVEL == 2 ? ((key >> 8) & 0xfffu) : (key & 0xffu);
@@ -310,11 +347,13 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   }
 }
 
-__global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict__ scores, int n, int chunks,
+template <bool RAGGED>
+__global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict__ scores, int n, int chunks, float p,
                                                         const u64* __restrict__ hist, uint32_t* __restrict__ state,
                                                         const int32_t* __restrict__ chunk_cnt,
                                                         int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_count,
-                                                        u64* __restrict__ masks) {
+                                                        u64* __restrict__ masks, const int32_t* __restrict__ seq_n,
+                                                        const float* __restrict__ seq_p, int hq) {
   __shared__ u64 wtot[kTW];
   __shared__ int red[kTW];
   __shared__ int kcnt[kPT][kTW];
@@ -326,19 +365,29 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
   const u64 hv = hist[int64_t(row) * kHistPerRow + kBins1 + kBins2 + threadIdx.x];
   float v[kPT];
   load_chunk(scores + int64_t(row) * n, n, c, v);
-  const u64 T = (u64(st[5]) << 32) | st[4];
-  find_crossing<1>(&hv, T, 0.f, wtot, &cr);
-  const uint32_t kstar = (st[3] << 8) | cr.bin;
-  // offset of this chunk = selected keys of the chunks before it
-  const int32_t* cc = chunk_cnt + int64_t(row) * chunks * (1 + kBins3);
-  int before = 0;
-  for (int k = threadIdx.x; k < c; k += kT) before += cc[k * (1 + kBins3)] + cc[k * (1 + kBins3) + 1 + cr.bin];
-  before = wave_sum_int(before);
-  if (lane == 0) red[wave] = before;
-  __syncthreads();
-  int offset = 0;
+  const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, row, n, p) : RowSel{n, p};
+  if (RAGGED && c * kChunk >= rs.n) {   // block-uniform: no key of this row here (a row without keys selects none)
+    if (c == 0 && threadIdx.x == 0) sel_count[row] = 0;
+    return;
+  }
+  const bool all = RAGGED && rs.p >= 1.f;   // every key of the row (the histogram passes skipped it)
+  uint32_t kstar = 0u;            // keys >= kstar are selected (every key is >= 0)
+  int offset = c * kChunk;
+  if (!all) {
+    const u64 T = (u64(st[5]) << 32) | st[4];
+    find_crossing<1>(&hv, T, 0.f, wtot, &cr);
+    kstar = (st[3] << 8) | cr.bin;
+    // offset of this chunk = selected keys of the chunks before it
+    const int32_t* cc = chunk_cnt + int64_t(row) * chunks * (1 + kBins3);
+    int before = 0;
+    for (int k = threadIdx.x; k < c; k += kT) before += cc[k * (1 + kBins3)] + cc[k * (1 + kBins3) + 1 + cr.bin];
+    before = wave_sum_int(before);
+    if (lane == 0) red[wave] = before;
+    __syncthreads();
+    offset = 0;
 #pragma unroll
-  for (int w = 0; w < kTW; ++w) offset += red[w];
+    for (int w = 0; w < kTW; ++w) offset += red[w];
+  }
 
   // ascending compaction: element (k, thread) has index c*kChunk + k*kT + thread, so the
   // order is k-major, then wave, then lane; all kPT ballots first, one barrier
@@ -346,7 +395,7 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
   uint64_t bal[kPT];
 #pragma unroll
   for (int k = 0; k < kPT; ++k) {
-    bal[k] = __ballot(in_row(n, c, k) && score_key(v[k]) >= kstar);
+    bal[k] = __ballot(in_row(rs.n, c, k) && score_key(v[k]) >= kstar);
     if (lane == 0) {
       kcnt[k][wave] = __popcll(bal[k]);
       // keys c*kChunk + k*kT + 64 wave + [0, 64) of the row's selection bitmap
@@ -368,7 +417,7 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
     }
     offset += tot;
   }
-  if (c == chunks - 1 && threadIdx.x == 0) sel_count[row] = offset;
+  if (c == (RAGGED ? (rs.n - 1) / kChunk : chunks - 1) && threadIdx.x == 0) sel_count[row] = offset;   // its last chunk
 }
 
 __global__ __launch_bounds__(kT) void topp_all_kernel(int n, int32_t* __restrict__ sel_idx,
@@ -384,13 +433,35 @@ __global__ __launch_bounds__(kT) void topp_all_kernel(int n, int32_t* __restrict
   }
 }
 
+template <bool RAGGED>
+void topp_passes(dim3 grid, hipStream_t stream, int n, int chunks, const float* scores, float p, float scale_log2e,
+                 const ToppWorkspace& w, int32_t* sel_idx, int32_t* sel_count, const float* slot_max, int nslots,
+                 u64* masks, const int32_t* seq_n, const float* seq_p, int heads_q) {
+  const float* rmax = slot_max;
+  int nmax = nslots;
+  if (slot_max == nullptr) {   // otherwise the score launch has written the maxima and cleared the counters
+    topp_max_kernel<RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, w.hist, seq_n, heads_q);
+    rmax = w.chunk_max;
+    nmax = chunks;
+  }
+  topp_level1_kernel<RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, p, w.hist, w.state,
+                                                      seq_n, seq_p, heads_q);
+  topp_level_kernel<2, RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, scale_log2e, p, w.hist, w.state,
+                                                        w.chunk_cnt, seq_n, seq_p, heads_q);
+  topp_level_kernel<3, RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, scale_log2e, p, w.hist, w.state,
+                                                        w.chunk_cnt, seq_n, seq_p, heads_q);
+  topp_write_kernel<RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, p, w.hist, w.state, w.chunk_cnt, sel_idx,
+                                                     sel_count, masks, seq_n, seq_p, heads_q);
+}
+
 }  // namespace
 
 rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,
                        int32_t* sel_count, void* ws, hipStream_t stream, const float* slot_max, int32_t nslots,
-                       unsigned long long* masks) {
+                       unsigned long long* masks, const int32_t* seq_n, const float* seq_p, int32_t heads_q) {
   const int mask_words = topp_mask_words(n);
-  if (n == 0 || p >= 1.0f) {
+  const bool ragged = seq_n != nullptr || seq_p != nullptr;   // per-row counts / p: decided on the device
+  if (n == 0 || (p >= 1.0f && !ragged)) {
     // every key (or none) is selected
     const int cover = masks ? mask_words * 64 : n;
     const dim3 grid(cover > 0 ? (cover + kT - 1) / kT : 1, rows);
@@ -401,20 +472,12 @@ rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, fl
   ToppWorkspace w = topp_workspace(ws, rows, n);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
   const dim3 grid(chunks, rows);
-  const float* rmax = slot_max;
-  int nmax = nslots;
-  if (slot_max == nullptr) {   // otherwise the score launch has written the maxima and cleared the counters
-    topp_max_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, w.hist);
-    rmax = w.chunk_max;
-    nmax = chunks;
-  }
-  topp_level1_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, w.hist, w.state);
-  topp_level_kernel<2><<<grid, kT, 0, stream>>>(scores, n, chunks, scale_log2e, p, w.hist, w.state,
-                                               w.chunk_cnt);
-  topp_level_kernel<3><<<grid, kT, 0, stream>>>(scores, n, chunks, scale_log2e, p, w.hist, w.state,
-                                               w.chunk_cnt);
-  topp_write_kernel<<<grid, kT, 0, stream>>>(scores, n, chunks, w.hist, w.state, w.chunk_cnt, sel_idx, sel_count,
-                                             masks);
+  if (ragged)
+    topp_passes<true>(grid, stream, n, chunks, scores, p, scale_log2e, w, sel_idx, sel_count, slot_max, nslots, masks,
+                      seq_n, seq_p, heads_q);
+  else
+    topp_passes<false>(grid, stream, n, chunks, scores, p, scale_log2e, w, sel_idx, sel_count, slot_max, nslots,
+                       masks, nullptr, nullptr, heads_q);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

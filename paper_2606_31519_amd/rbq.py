@@ -25,6 +25,8 @@ EXPORTED = [
     "rbq_encode_keys", "rbq_quantize_query", "rbq_score", "rbq_topp_select", "rbq_sparse_decode",
     "rbq_dense_decode", "rbq_decode_step", "rbq_workspace_bytes", "rbq_index_bytes", "rbq_status_string", "rbq_version",
     "rbq_encode_keys_debug", "rbq_quantize_query_debug", "rbq_score_ints",
+    "rbq_score_varlen", "rbq_topp_select_varlen", "rbq_sparse_decode_varlen", "rbq_dense_decode_varlen",
+    "rbq_decode_step_varlen",
 ]
 
 
@@ -55,6 +57,14 @@ def _load():
                              vp],
         "rbq_decode_step": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, i32, f32, f32,
                             vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
+        "rbq_score_varlen": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp],
+        "rbq_topp_select_varlen": [i32, i32, i32, vp, vp, vp, f32, vp, vp, vp, sz, vp],
+        "rbq_sparse_decode_varlen": [i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp,
+                                     vp, vp, sz, vp],
+        "rbq_dense_decode_varlen": [i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, i32, vp, vp, f32, vp, vp, vp, sz,
+                                    vp],
+        "rbq_decode_step_varlen": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp,
+                                   i32, vp, f32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -184,3 +194,48 @@ def rbq_decode_step(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, ca
         kv_dtype_code(K), cap, n, w, _ptr(codes), _ptr(kfac), int(bool(flush)), p, sm_scale, _ptr(qplanes),
         _ptr(qscal), _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _ptr(out), _ptr(lse), _ptr(ws), ws_bytes,
         _stream(stream)))
+
+
+# ---- ragged batches: per-sequence key counts (seq_n), window rows (seq_w) and p (seq_p), device tensors
+
+
+def rbq_score_varlen(batch, heads_q, heads_kv, head_dim, n, cap, seq_n, codes, kfac, qplanes, qscal, scores,
+                     stream=None):
+    _check("rbq_score_varlen", lib.rbq_score_varlen(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(seq_n),
+                                                    _ptr(codes), _ptr(kfac), _ptr(qplanes), _ptr(qscal),
+                                                    _ptr(scores), _stream(stream)))
+
+
+def rbq_topp_select_varlen(batch, heads_q, n, seq_n, scores, seq_p, sm_scale, sel_idx, sel_count, ws, stream=None):
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("rbq_topp_select_varlen", lib.rbq_topp_select_varlen(
+        batch, heads_q, n, _ptr(seq_n), _ptr(scores), _ptr(seq_p), sm_scale, _ptr(sel_idx), _ptr(sel_count),
+        _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def rbq_sparse_decode_varlen(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, w, seq_n, seq_w, sel_idx,
+                             sel_count, sm_scale, out, lse, ws, stream=None):
+    ws_bytes = ws.numel() * ws.element_size()
+    _check("rbq_sparse_decode_varlen", lib.rbq_sparse_decode_varlen(
+        batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n, w, _ptr(seq_n),
+        _ptr(seq_w), _ptr(sel_idx), _ptr(sel_count), sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws_bytes,
+        _stream(stream)))
+
+
+def rbq_dense_decode_varlen(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, w, seq_n, seq_w, sm_scale, out,
+                            lse, ws, stream=None):
+    ws_bytes = ws.numel() * ws.element_size()
+    _check("rbq_dense_decode_varlen", lib.rbq_dense_decode_varlen(
+        batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n, w, _ptr(seq_n),
+        _ptr(seq_w), sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def rbq_decode_step_varlen(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, cap, n, w, seq_n, seq_w, codes,
+                           kfac, flush, seq_p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws,
+                           stream=None):
+    ws_bytes = ws.numel() * ws.element_size()
+    _check("rbq_decode_step_varlen", lib.rbq_decode_step_varlen(
+        batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_q), _ptr(c_k), _ptr(K), _ptr(V),
+        kv_dtype_code(K), cap, n, w, _ptr(seq_n), _ptr(seq_w), _ptr(codes), _ptr(kfac), int(bool(flush)),
+        _ptr(seq_p), sm_scale, _ptr(qplanes), _ptr(qscal), _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _ptr(out),
+        _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)))

@@ -126,3 +126,40 @@ def test_invalid_arguments_are_rejected_on_the_host(lib):
                                          FAKE, None, FAKE, k.get("wsb", 1 << 30), 0)
     assert step(cap=105) == EINVAL
     assert step(wsb=64) == EINVAL
+
+
+def test_ragged_calls_reject_invalid_arguments_on_the_host(lib):
+    L = lib.lib
+    EINVAL = lib.RBQ_EINVAL
+    # score: the per-sequence counts are required and aligned; n > cap
+    sc = lambda **k: L.rbq_score_varlen(1, 8, 4, 128, k.get("n", 10), k.get("cap", 10), k.get("sn", FAKE), FAKE,
+                                        FAKE, FAKE, FAKE, FAKE, 0)
+    assert sc(sn=None) == EINVAL
+    assert sc(sn=FAKE + 4) == EINVAL
+    assert sc(n=11) == EINVAL
+    # top-p: per-sequence p required; the workspace is needed whatever the device p values are
+    tp = lambda **k: L.rbq_topp_select_varlen(2, 8, 100, k.get("sn", FAKE), FAKE, k.get("sp", FAKE),
+                                              k.get("s", 0.1), FAKE, FAKE, FAKE, k.get("wsb", 1 << 30), 0)
+    assert tp(sp=None) == EINVAL
+    assert tp(sp=FAKE + 8) == EINVAL
+    assert tp(sn=None) == EINVAL
+    assert tp(s=0.0) == EINVAL
+    assert tp(wsb=8) == EINVAL
+    # decode: every sequence's window must fit at the tail (n + w <= cap); aligned seq_w when given
+    dec = lambda **k: L.rbq_sparse_decode_varlen(2, 8, 4, 128, FAKE, FAKE, FAKE, 1, k.get("cap", 200), 100,
+                                                 k.get("w", 10), k.get("sn", FAKE), k.get("sw", None), FAKE, FAKE,
+                                                 0.1, FAKE, None, FAKE, 1 << 30, 0)
+    assert dec(cap=105) == EINVAL
+    assert dec(sn=None) == EINVAL
+    assert dec(sw=FAKE + 4) == EINVAL
+    assert dec(w=5000, cap=10000) == EINVAL   # above the window limit
+    assert L.rbq_dense_decode_varlen(2, 8, 4, 128, FAKE, FAKE, FAKE, 1, 105, 100, 10, FAKE, None, 0.1, FAKE, None,
+                                     FAKE, 1 << 30, 0) == EINVAL
+    # the fused step: short workspace, missing p, window past the capacity
+    step = lambda **k: L.rbq_decode_step_varlen(2, 8, 4, 128, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1,
+                                                k.get("cap", 200), 100, 10, FAKE, None, FAKE, FAKE, 1,
+                                                k.get("sp", FAKE), 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                                FAKE, k.get("wsb", 1 << 30), 0)
+    assert step(cap=105) == EINVAL
+    assert step(sp=None) == EINVAL
+    assert step(wsb=64) == EINVAL

@@ -1,0 +1,192 @@
+"""Ragged batches through the C ABI: sequences of one batch with their own key
+counts, window rows and p.
+
+  * rbq_score_varlen / rbq_topp_select_varlen against the uniform calls run on
+    each sequence alone (B = 1, n = seq_n[b], p = seq_p[b]): bitwise the same
+    scores and selections (and the uniform calls are checked against the
+    oracle elsewhere);
+  * the Top-p sets against the oracle on the same scores;
+  * rbq_sparse_decode_varlen / rbq_dense_decode_varlen against the oracle's
+    attention over each sequence's selected (or all) rows plus its window, the
+    window being the sequence's cache tail;
+  * rbq_decode_step_varlen against the separate ragged calls followed by the
+    window encode of each sequence: bitwise the same outputs, codes and factors.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from workloads import gen
+import parity_util as pu
+
+pytestmark = pytest.mark.gpu
+
+# (Hq, Hkv, kv dtype, seq_n, seq_w, seq_p, n slack, seed)
+CASES = [
+    # G = 4 bf16: the largest sequence, one without indexed keys (window only), one a key past a
+    # Top-p chunk with p = 1, a short one
+    (8, 2, "bf16", [6000, 0, 4097, 1234], [48, 17, 0, 33], [0.9, 0.7, 1.0, 0.95], 0, 11),
+    # G = 1 fp32 K/V; n above every count; a sequence of one key
+    (4, 4, "f32", [700, 1500, 1], [5, 0, 9], [0.5, 0.99, 0.8], 300, 12),
+    # G = 16; p <= 0 and NaN act as the smallest positive p; a count above n is clamped to n
+    (16, 1, "bf16", [2049, 4096, 9000], [0, 64, 64], [-1.0, float("nan"), 0.9], 0, 13),
+    # no window anywhere, no indexed key anywhere but one sequence
+    (8, 2, "bf16", [0, 3000], [0, 0], [0.9, 0.8], 0, 14),
+]
+N_CAP = 8192   # largest n of the cases above (9000 is clamped to it)
+
+
+def _ids(c):
+    return f"Hq{c[0]}-Hkv{c[1]}-{c[2]}-n{'_'.join(map(str, c[3]))}"
+
+
+@pytest.fixture(scope="module")
+def R():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2606_31519_amd import rbq
+    return rbq
+
+
+@pytest.fixture(scope="module")
+def pipeline(R):
+    from paper_2606_31519_amd import pipeline as pl
+    return pl
+
+
+def _p_eff(p):
+    """A device p as the ragged calls read it: clamped into (0, 1]."""
+    p = float(np.float32(p))
+    return min(p, 1.0) if p > 0 else 1e-30
+
+
+def _setup(R, pipeline, case):
+    Hq, Hkv, dt, seq_n, seq_w, seq_p, slack, seed = case
+    B = len(seq_n)
+    n = min(max(seq_n), N_CAP) + slack
+    w = max(seq_w)
+    wl = gen.random_case(B, Hq, Hkv, n, seed=seed, kv_dtype=dt, w=w, c_q_scale=0.5)
+    st = pipeline.DecodeState.from_workload(wl)
+    nb = [min(max(x, 0), n) for x in seq_n]
+    for b in range(B):   # each sequence's index over its own rows (a centroid of no keys stays zero)
+        if nb[b] > 0:
+            R.rbq_encode_keys(1, Hkv, st.D, st.K[b:b + 1], st.cap, nb[b], 0, st.cap, st.P, st.c_q[b:b + 1],
+                              st.c_k[b:b + 1], st.codes[b:b + 1], st.kfac[b:b + 1], R.RBQ_ENCODE_SET_CENTROID, None,
+                              st.ws_encode)
+    dev = dict(device="cuda")
+    arrays = (torch.tensor(seq_n, dtype=torch.int32, **dev), torch.tensor(seq_w, dtype=torch.int32, **dev),
+              torch.tensor(seq_p, dtype=torch.float32, **dev))
+    return wl, st, nb, arrays
+
+
+def _varlen_calls(R, st, arrays, flush=False):
+    sn, sw, sp = arrays
+    B, Hq, Hkv, D, n, w, cap = st.B, st.Hq, st.Hkv, st.D, st.n, st.w, st.cap
+    R.rbq_quantize_query(B, Hq, Hkv, D, st.q, st.P, st.c_q, st.c_k, st.qplanes, st.qscal)
+    R.rbq_score_varlen(B, Hq, Hkv, D, n, cap, sn, st.codes, st.kfac, st.qplanes, st.qscal, st.scores)
+    R.rbq_topp_select_varlen(B, Hq, n, sn, st.scores, sp, st.sm_scale, st.sel_idx, st.sel_count, st.ws_topp)
+    R.rbq_sparse_decode_varlen(B, Hq, Hkv, D, st.q, st.K, st.V, cap, n, w, sn, sw, st.sel_idx, st.sel_count,
+                               st.sm_scale, st.out, st.lse, st.ws_decode)
+
+
+@pytest.mark.parametrize("case", CASES, ids=_ids)
+def test_ragged_calls_match_each_sequence_alone(R, pipeline, case):
+    print("case", case, flush=True)
+    wl, st, nb, arrays = _setup(R, pipeline, case)
+    _varlen_calls(R, st, arrays)
+    torch.cuda.synchronize()
+    Hq, Hkv, D, cap = st.Hq, st.Hkv, st.D, st.cap
+    seq_w, seq_p = case[4], case[5]
+    scores, sel, cnt = st.scores.cpu().numpy(), st.sel_idx.cpu().numpy(), st.sel_count.cpu().numpy()
+    out, lse = st.out.cpu().numpy(), st.lse.cpu().numpy()
+    f32 = dict(dtype=torch.float32, device="cuda")
+    for b in range(st.B):
+        n_b, w_b, p_b = nb[b], seq_w[b], _p_eff(seq_p[b])
+        # the uniform calls on this sequence alone
+        qp = torch.zeros(1, Hq, 4, D // 32, dtype=torch.int32, device="cuda")
+        qs = torch.zeros(1, Hq, 8, **f32)
+        R.rbq_quantize_query(1, Hq, Hkv, D, st.q[b:b + 1], st.P, st.c_q[b:b + 1], st.c_k[b:b + 1], qp, qs)
+        S1 = torch.zeros(1, Hq, max(n_b, 1), **f32)
+        R.rbq_score(1, Hq, Hkv, D, n_b, cap, st.codes[b:b + 1], st.kfac[b:b + 1], qp, qs, S1)
+        sel1 = torch.zeros(1, Hq, max(n_b, 1), dtype=torch.int32, device="cuda")
+        cnt1 = torch.zeros(1, Hq, dtype=torch.int32, device="cuda")
+        ws = R.workspace(R.RBQ_OP_TOPP, 1, Hq, Hkv, D, n_b)
+        R.rbq_topp_select(1, Hq, n_b, S1, p_b, st.sm_scale, sel1, cnt1, ws)
+        torch.cuda.synchronize()
+        S1, sel1, cnt1 = S1.cpu().numpy(), sel1.cpu().numpy(), cnt1.cpu().numpy()
+        assert np.array_equal(st.qplanes[b].cpu().numpy(), qp[0].cpu().numpy())
+        assert np.array_equal(scores[b, :, :n_b].view(np.uint32), S1[0, :, :n_b].view(np.uint32)), f"scores b={b}"
+        for h in range(Hq):
+            c = int(cnt[b, h])
+            assert c == int(cnt1[0, h]), (b, h, c, int(cnt1[0, h]))
+            assert np.array_equal(sel[b, h, :c], sel1[0, h, :c]), (b, h)
+            if n_b == 0:
+                assert c == 0
+            elif p_b >= 1.0:
+                assert c == n_b
+            else:
+                pu.check_topp(scores[b, h, :n_b], p_b, st.sm_scale, sel[b, h, :c])
+            # attention over the selected rows plus the sequence's cache tail
+            hk = h // (Hq // Hkv)
+            K = wl.K_f32(b, hk, slice(0, n_b))
+            V = wl.V_f32(b, hk, slice(0, n_b))
+            Kw = wl.K_f32(b, hk, slice(n_b, n_b + w_b))
+            Vw = wl.V_f32(b, hk, slice(n_b, n_b + w_b))
+            pu.check_attention(out[b, h], lse[b, h], wl.q[b, h], K, V, sel[b, h, :c], Kw, Vw, st.sm_scale)
+
+
+@pytest.mark.parametrize("case", [CASES[0], CASES[2]], ids=_ids)
+def test_ragged_dense_decode_matches_oracle(R, pipeline, case):
+    print("case", case, flush=True)
+    wl, st, nb, (sn, sw, _) = _setup(R, pipeline, case)
+    R.rbq_dense_decode_varlen(st.B, st.Hq, st.Hkv, st.D, st.q, st.K, st.V, st.cap, st.n, st.w, sn, sw, st.sm_scale,
+                              st.out, st.lse, st.ws_decode)
+    torch.cuda.synchronize()
+    out, lse = st.out.cpu().numpy(), st.lse.cpu().numpy()
+    for b in range(st.B):
+        n_b, w_b = nb[b], case[4][b]
+        for h in range(st.Hq):
+            hk = h // (st.Hq // st.Hkv)
+            pu.check_attention(out[b, h], lse[b, h], wl.q[b, h], wl.K_f32(b, hk, slice(0, n_b)),
+                               wl.V_f32(b, hk, slice(0, n_b)), np.arange(n_b),
+                               wl.K_f32(b, hk, slice(n_b, n_b + w_b)), wl.V_f32(b, hk, slice(n_b, n_b + w_b)),
+                               st.sm_scale)
+
+
+def _outputs(st, nb):
+    torch.cuda.synchronize()
+    o = {k: getattr(st, k).cpu().numpy().copy() for k in ("qplanes", "qscal", "sel_count", "out", "lse", "codes",
+                                                          "kfac")}
+    S, sel, cnt = st.scores.cpu().numpy(), st.sel_idx.cpu().numpy(), o["sel_count"]
+    o["scores"] = [S[b, :, :nb[b]].copy() for b in range(st.B)]
+    o["sel"] = [sel[b, h, :cnt[b, h]].copy() for b in range(st.B) for h in range(st.Hq)]
+    return o
+
+
+def _same(a, b):
+    for k in a:
+        if k in ("scores", "sel"):
+            assert all(np.array_equal(x.view(np.uint8), y.view(np.uint8)) for x, y in zip(a[k], b[k])), k
+        else:
+            assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
+
+
+@pytest.mark.parametrize("case", CASES, ids=_ids)
+def test_ragged_fused_step_matches_separate_calls(R, pipeline, case):
+    print("case", case, flush=True)
+    _, ref, nb, arrays = _setup(R, pipeline, case)
+    _varlen_calls(R, ref, arrays)
+    for b in range(ref.B):   # the window encode of each sequence: rows [n_b, n_b + w_b)
+        w_b = case[4][b]
+        if w_b:
+            R.rbq_encode_keys(1, ref.Hkv, ref.D, ref.K[b:b + 1, :, nb[b]:], ref.cap, w_b, nb[b], ref.cap, ref.P,
+                              ref.c_q[b:b + 1], ref.c_k[b:b + 1], ref.codes[b:b + 1], ref.kfac[b:b + 1], 0, None,
+                              None)
+    want = _outputs(ref, nb)
+    _, st, _, (sn, sw, sp) = _setup(R, pipeline, case)
+    for _ in range(2):   # the same workspace twice: nothing is left over from the first call
+        R.rbq_decode_step_varlen(st.B, st.Hq, st.Hkv, st.D, st.q, st.P, st.c_q, st.c_k, st.K, st.V, st.cap, st.n,
+                                 st.w, sn, sw, st.codes, st.kfac, 1, sp, st.sm_scale, st.qplanes, st.qscal,
+                                 st.scores, st.sel_idx, st.sel_count, st.out, st.lse, st.ws_step)
+        _same(_outputs(st, nb), want)
