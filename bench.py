@@ -17,7 +17,9 @@ shape (this library's split-K kernel and torch SDPA, the faster of the two).
 The per-stage times come from the separate calls. The line also carries the
 roofline of the dominant call, the Top-p
 sweep (p = 0.8 / 0.9 / 0.95 / 0.99: step time, budget, KV-group union), the
-standalone score scan of the wide-head workload, and the oracle's CPU rate.
+standalone score scan of the wide-head workload, a ragged serving batch (16
+sequences of mixed length, window and p) against its dense decode, and the
+oracle's CPU rate.
 """
 from __future__ import annotations
 
@@ -227,6 +229,64 @@ def time_scan_c5(pipeline, gen, torch, steps, warmup, replicas=4):
             "traffic": _measured_traffic(SCAN_TRAFFIC_FILE, SCORE_SRC, "score_source_sha256")}
 
 
+def time_ragged(pipeline, gen, torch, steps, warmup, seed=20260):
+    """A ragged serving batch: config 4's 16 sequences (32 query / 8 KV heads,
+    planted fraction per sequence ~ U(0.1 %, 10 %)) with per-sequence indexed
+    lengths ~ U(2048, 32512), window rows ~ U(0, 256) at each sequence's cache
+    tail and p ~ U(0.80, 0.95), through rbq_decode_step_varlen, against the
+    ragged dense decode of the same rows."""
+    wl = gen.config4()
+    rng = np.random.default_rng(seed)
+    B, w_max = wl.B, 256
+    n_max = wl.N - w_max
+    seq_n = rng.integers(2048, n_max + 1, B).astype(np.int32)
+    seq_w = rng.integers(0, w_max + 1, B).astype(np.int32)
+    seq_p = np.round(rng.uniform(0.80, 0.95, B), 2).astype(np.float32)
+    K = pipeline.to_device_kv(wl.K, wl.kv_dtype, "cuda")
+    V = pipeline.to_device_kv(wl.V, wl.kv_dtype, "cuda")
+    q = torch.from_numpy(np.ascontiguousarray(wl.q)).cuda()
+    P = torch.from_numpy(np.ascontiguousarray(wl.P)).cuda()
+    cq = torch.from_numpy(np.ascontiguousarray(wl.c_q)).cuda()
+    st = pipeline.DecodeState(B, wl.Hq, wl.Hkv, wl.D, wl.N, n_max, w_max, K, V, q, P, cq)
+    del wl
+    st.build_index_ragged(seq_n.tolist())
+    sn, sw, sp = (torch.from_numpy(a).cuda() for a in (seq_n, seq_w, seq_p))
+    torch.cuda.synchronize()
+    g = _graph(torch, lambda: st.step_ragged(sn, sw, sp))
+    ms_step = _time_graphs(torch, [g], steps, warmup)
+    del g
+    st.step_ragged(sn, sw, sp)
+    torch.cuda.synchronize()
+    # the sparse attention alone (on the step's selection) and the ragged dense decode
+    g = _graph(torch, lambda: st.sparse_decode_ragged(sn, sw))
+    ms_sparse = _time_graphs(torch, [g], steps, warmup)
+    del g
+    d_out, d_lse = torch.empty_like(st.out), torch.empty_like(st.lse)
+    g = _graph(torch, lambda: st.dense_decode_ragged(sn, sw, d_out, d_lse))
+    ms_dense = _time_graphs(torch, [g], steps, warmup)
+    del g
+    sel, cnt = st.sel_idx.cpu().numpy(), st.sel_count.cpu().numpy()
+    G = st.Hq // st.Hkv
+    union = sum(np.unique(np.concatenate([sel[b, h, :cnt[b, h]] for h in range(hk * G, (hk + 1) * G)])).size
+                for b in range(B) for hk in range(st.Hkv))
+    idx_rows = st.Hkv * int(seq_n.sum())
+    win_rows = st.Hkv * int(seq_w.sum())
+    row_bytes = 2 * st.D * 2   # K + V, bf16
+    sparse_bytes = (union + win_rows) * row_bytes + int(cnt.sum()) * 4 + B * st.Hq * st.D * 4
+    dense_bytes = (idx_rows + win_rows) * row_bytes
+    frac = cnt / np.repeat(seq_n, st.Hq).reshape(B, st.Hq)
+    return {"workload": "gqa 32q/8kv b=16 bf16 ragged: indexed keys ~ U(2048, 32512), window ~ U(0, 256), "
+                        "p ~ U(0.80, 0.95) per sequence; planted fraction ~ U(0.1 %, 10 %)",
+            "seq_n": seq_n.tolist(), "seq_w": seq_w.tolist(), "seq_p": [float(x) for x in seq_p],
+            "ms_per_step": ms_step, "keys_per_s": st.Hq * int(seq_n.sum()) / (ms_step * 1e-3),
+            "dense_decode_ms": ms_dense, "speedup_vs_dense": ms_dense / ms_step,
+            "dense_GBps": dense_bytes / (ms_dense * 1e-3) / 1e9,
+            "sparse_decode": {"ms": ms_sparse, "bytes": float(sparse_bytes),
+                              "GBps": sparse_bytes / (ms_sparse * 1e-3) / 1e9,
+                              "frac_hbm": sparse_bytes / (ms_sparse * 1e-3) / 1e9 / HBM_PEAK_GBS},
+            "budget_frac_mean": float(frac.mean()), "union_frac": union / idx_rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -237,6 +297,7 @@ def main():
     ap.add_argument("--no-scan", action="store_true", help="skip the standalone wide-head scan")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-sweep", action="store_true", help="skip the Top-p sweep (p = 0.8 / 0.9 / 0.95 / 0.99)")
+    ap.add_argument("--no-ragged", action="store_true", help="skip the ragged-batch step (16 sequences of mixed length)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
@@ -354,12 +415,14 @@ def main():
                 "algorithmic_bytes_per_launch": float(sbytes[dom]), "ms_per_launch": stage_ms[dom],
                 "copy_GBps": copy["GBps"], "frac_of_copy": kern[dom]["GBps"] / copy["GBps"]}
 
+    del reps, step_graphs
+    torch.cuda.empty_cache()
     scan = None
     if not args.no_scan:
-        del reps, step_graphs
-        torch.cuda.empty_cache()
         scan = time_scan_c5(pipeline, gen, torch, args.steps, args.warmup)
         scan["frac_of_copy"] = scan["GBps"] / copy["GBps"]
+        torch.cuda.empty_cache()
+    ragged = None if args.no_ragged else time_ragged(pipeline, gen, torch, args.steps, args.warmup)
 
     cpu = None if args.no_cpu else cpu_baseline(wl)
     cnt = st0.sel_count.cpu().numpy()
@@ -391,6 +454,7 @@ def main():
         "roofline": roofline,
         "scan_wide_heads": scan,
         "p_sweep": sweep or None,
+        "ragged": ragged,
         "cpu_baseline": cpu,
         "gen_s": t_gen,
         "git": _git_sha(),

@@ -330,6 +330,10 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     c0 = (split - idx_splits) * kDecodeWinChunk;
     c1 = RAGGED ? max(c0, min(wb, c0 + kDecodeWinChunk)) : min(w, c0 + kDecodeWinChunk);
   }
+  if (RAGGED && c1 == c0 && nwin == 0) {   // block-uniform: past this sequence's rows, an empty partial state
+    if (int(threadIdx.x) < G) part[(int64_t(row0 + threadIdx.x) * total_splits + split) * (kHeadDim + 2)] = -INFINITY;
+    return;
+  }
   const char* Kbase = window ? static_cast<const char*>(K_loc) + (int64_t(bh) * loc_ld + wbase) * kHeadDim * kElem
                              : static_cast<const char*>(K) + int64_t(bh) * cap * kHeadDim * kElem;
   const char* Vbase = window ? static_cast<const char*>(V_loc) + (int64_t(bh) * loc_ld + wbase) * kHeadDim * kElem
@@ -565,6 +569,10 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   } else {
     c0 = (split - idx_splits) * kDecodeWinChunk;
     c1 = RAGGED ? max(c0, min(wb, c0 + kDecodeWinChunk)) : min(w, c0 + kDecodeWinChunk);
+  }
+  if (RAGGED && c1 == c0 && nwin == 0) {   // block-uniform: past this sequence's rows, an empty partial state
+    if (int(threadIdx.x) < G) part[(int64_t(row0 + threadIdx.x) * total_splits + split) * (kHeadDim + 2)] = -INFINITY;
+    return;
   }
   const uint16_t* Kb = window ? K_loc + (int64_t(bh) * loc_ld + wbase) * kHeadDim : K + int64_t(bh) * cap * kHeadDim;
   const uint16_t* Vb = window ? V_loc + (int64_t(bh) * loc_ld + wbase) * kHeadDim : V + int64_t(bh) * cap * kHeadDim;

@@ -116,6 +116,7 @@ __device__ __forceinline__ void encode_tiles(const EncodeArgs& ea, int bh, int b
   constexpr int kPiecesPerRow = kHeadDim * kElemBytes / 16;            // 16 (bf16) or 32 (fp32)
   constexpr int kPer = kTileKeys * kPiecesPerRow / kEncThreads;         // 2 or 4 per thread
   const int tiles = (n_new + kTileKeys - 1) / kTileKeys;
+  if (RAGGED && bx >= tiles) return;   // block-uniform: this sequence has no tile for this block
   u32x4 pc[kPer];
   auto load_tile = [&](int tl) {
 #pragma unroll

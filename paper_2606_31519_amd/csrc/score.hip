@@ -22,10 +22,10 @@
 // whole decode step too, although the Top-p passes read the scores next).
 // Blocks that lie wholly inside [0, n) take a path without per-key guards.
 // The scan is HBM-bound at G = 4 and at G = 8.
-// Ragged batches (seq_n != NULL): sequence b has seq_n[b] indexed keys
+// Ragged batches (RAGGED, seq_n != NULL): sequence b has seq_n[b] indexed keys
 // (clamped to [0, n]); n is the row stride of the scores and bounds the grid.
-// Loads are clamped to n - 1, so the key count's load overlaps them (keys past
-// a sequence's count are computed from whatever the rows hold and never stored).
+// A block reads its sequence's count first and leaves at once when it lies
+// past it; loads are clamped to the sequence's last key.
 #include "rbq_device.h"
 #include "rbq_internal.h"
 
@@ -107,25 +107,29 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   const int i0 = blockIdx.x * (kScoreThreads * KPT) + threadIdx.x;
   const int row0 = b * Hq + hk * G;
 
+  auto clear_counters = [&]() {   // (fused step) this block's share of the counters
+    if (SLOTS) {
+      const int64_t nblk = int64_t(gridDim.x) * gridDim.y, lb = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
+      const int64_t per = (sl.hist_words + nblk - 1) / nblk;
+      const int64_t e1 = min(sl.hist_words, (lb + 1) * per);
+      for (int64_t e = lb * per + threadIdx.x; e < e1; e += kScoreThreads) sl.hist[e] = 0ull;
+    }
+  };
+  const int nb = RAGGED ? min(max(seq_n[b], 0), n) : n;   // this sequence's indexed keys
+  if (RAGGED && int(blockIdx.x) * (kScoreThreads * KPT) >= nb) {   // block-uniform: no key of this block is indexed
+    clear_counters();
+    if (SLOTS && int(threadIdx.x) < G) sl.slot_max[int64_t(row0 + threadIdx.x) * gridDim.x + blockIdx.x] = -INFINITY;
+    return;
+  }
   u32x4 c[KPT];
   f32x2 fg[KPT];
 #pragma unroll
   for (int u = 0; u < KPT; ++u) {
-    const int i = min(i0 + u * kScoreThreads, n - 1);    // keys past n are computed but never stored
+    const int i = min(i0 + u * kScoreThreads, nb - 1);    // keys past nb are computed but never stored
     c[u] = __builtin_nontemporal_load(codes + kbase + i);
     if (!INTS) fg[u] = __builtin_nontemporal_load(kfac + kbase + i);
   }
-  if (SLOTS) {   // this block's share of the counters
-    const int64_t nblk = int64_t(gridDim.x) * gridDim.y, lb = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
-    const int64_t per = (sl.hist_words + nblk - 1) / nblk;
-    const int64_t e1 = min(sl.hist_words, (lb + 1) * per);
-    for (int64_t e = lb * per + threadIdx.x; e < e1; e += kScoreThreads) sl.hist[e] = 0ull;
-  }
-  const int nb = RAGGED ? min(max(seq_n[b], 0), n) : n;   // this sequence's indexed keys
-  if (RAGGED && int(blockIdx.x) * (kScoreThreads * KPT) >= nb) {   // block-uniform: no key of this block is indexed
-    if (SLOTS && int(threadIdx.x) < G) sl.slot_max[int64_t(row0 + threadIdx.x) * gridDim.x + blockIdx.x] = -INFINITY;
-    return;
-  }
+  clear_counters();
   const bool full = (blockIdx.x + 1) * (kScoreThreads * KPT) <= nb;   // block-uniform: no key past nb
   if (threadIdx.x < 4 * G) {                  // one lane per (head, word)
     const int h = threadIdx.x >> 2, w = threadIdx.x & 3;

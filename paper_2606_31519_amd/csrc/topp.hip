@@ -15,28 +15,32 @@
 // each) and fp32 exp (~1 ulp) leave the decision within ~1e-6 of the exact
 // cumulative mass.
 //
-// Kernels, each over grid (chunks of 4096 scores, rows). The crossing searches
+// Kernels, each over grid (blocks, rows); a block takes spb consecutive
+// sub-chunks of 4096 scores of its row (spb = 1 unless the batch has more than
+// about a wave of sub-chunks). The crossing searches
 // are repeated by every block of a row, which costs less than an extra launch
 // and needs neither cross-block waiting nor device-wide fences; levels 1 and 2
 // also keep 64 coarse bins (sums of 64 fine bins), so a search reads 64 coarse
 // then 64 fine counters (one wave, two dependent loads) instead of 4096:
-//   1 max        per-chunk max; clears the row's histograms
+//   1 max        per-block max; clears the row's histograms
 //   2 level 1    row max; 4096-bin histogram of key bits 31..20
 //   3 level 2    total mass Z, target T = ceil(p Z), crossing bin b1;
 //                histogram of bits 19..8 inside b1
 //   4 level 3    crossing b2; histogram of bits 7..0 inside (b1, b2); per
-//                chunk: the count of keys above that 24-bit bin and the suffix
+//                block: the count of keys above that 24-bit bin and the suffix
 //                counts of its 256 sub-bins
-//   5 write      crossing b3 and K*; offset = sum over the earlier chunks of
+//   5 write      crossing b3 and K*; offset = sum over the earlier blocks of
 //                (count above + suffix count at b3); ascending compaction
 // Every pass issues its 16 loads per thread up front (indices clamped, the
-// out-of-range values masked), so a pass costs one memory round trip.
+// out-of-range values masked) and those of the next sub-chunk before working
+// on the current one, so a pass costs one memory round trip per block.
 //
 // Ragged batches (seq_n / seq_p != NULL): row r of sequence b = r / Hq has
 // seq_n[b] keys (clamped to [0, n]; n stays the row stride and sizes the grid)
 // and its own p = seq_p[b]. Blocks past a row's keys leave at once; rows whose
 // p is >= 1 (or that have no keys) skip the histogram passes, and the write
 // pass selects every key of them.
+#include <algorithm>
 #include <cmath>
 
 #include "rbq_device.h"
@@ -173,12 +177,13 @@ __device__ __forceinline__ void flush_coarse(const u64* h, u64* __restrict__ gco
   if ((threadIdx.x & 3) == 0 && s) atomicAdd(&gcoarse[threadIdx.x / 4], s);
 }
 
-// the thread's kPT scores of chunk c (element c * kChunk + k * kT + tid), all loads in flight
-__device__ __forceinline__ void load_chunk(const float* __restrict__ s, int n, int c, float* v) {
+// the thread's kPT scores of sub-chunk cs (element cs * kChunk + k * kT + tid), all
+// loads in flight; indices past the row's n keys are clamped (the values are masked)
+__device__ __forceinline__ void load_chunk(const float* __restrict__ s, int n, int cs, float* v) {
 #pragma unroll
-  for (int k = 0; k < kPT; ++k) v[k] = s[min(c * kChunk + k * kT + int(threadIdx.x), n - 1)];
+  for (int k = 0; k < kPT; ++k) v[k] = s[min(cs * kChunk + k * kT + int(threadIdx.x), n - 1)];
 }
-__device__ __forceinline__ bool in_row(int n, int c, int k) { return c * kChunk + k * kT + int(threadIdx.x) < n; }
+__device__ __forceinline__ bool in_row(int n, int cs, int k) { return cs * kChunk + k * kT + int(threadIdx.x) < n; }
 
 // A row's key count and p: the call's, or its sequence's in a ragged batch. A
 // p outside (0, 1] is clamped into it (<= 0 or NaN: the smallest positive p,
@@ -199,38 +204,60 @@ __device__ __forceinline__ RowSel row_sel(const int32_t* __restrict__ seq_n, con
   return r;
 }
 
+// Block c of a row takes the sub-chunks [c * spb, c * spb + spb) that hold keys
+// of the row (none for a block past a short row of a ragged batch). The host
+// sets spb so that a pass is about one wave of blocks whatever the batch: the
+// per-block work of a pass (clearing and flushing the LDS histogram, the
+// crossing searches, the launch) is then paid once per spb sub-chunks.
+// (MULTI = false: spb == 1, the kernels compile to a single sub-chunk per block)
+struct Span {
+  int cs0, cs1;
+};
+template <bool MULTI>
+__device__ __forceinline__ Span block_span(int c, int spb, int chunks, int nr) {
+  if (!MULTI) return Span{c, c * kChunk < nr ? c + 1 : c};
+  return Span{c * spb, min(min(c * spb + spb, chunks), (nr + kChunk - 1) / kChunk)};
+}
+
 __device__ __forceinline__ float row_max(const float* __restrict__ part_max, int nmax, float* red) {
   float m = -INFINITY;
   for (int k = threadIdx.x; k < nmax; k += kT) m = fmaxf(m, part_max[k]);
   return block_max(m, red);
 }
 
-template <bool RAGGED>
-__global__ __launch_bounds__(kT) void topp_max_kernel(const float* __restrict__ scores, int n, int chunks,
+template <bool RAGGED, bool MULTI>
+__global__ __launch_bounds__(kT) void topp_max_kernel(const float* __restrict__ scores, int n, int chunks, int spb,
                                                       float* __restrict__ chunk_max, u64* __restrict__ hist,
                                                       const int32_t* __restrict__ seq_n, int hq) {
   __shared__ float red[kTW];
   const int row = blockIdx.y, c = blockIdx.x;
-  float v[kPT];
-  load_chunk(scores + int64_t(row) * n, n, c, v);
   const int nr = RAGGED ? row_sel(seq_n, nullptr, hq, row, n, 1.f).n : n;
+  const Span sp = block_span<MULTI>(c, spb, chunks, nr);
+  const float* srow = scores + int64_t(row) * n;
   float m = -INFINITY;
+  float v[kPT], vn[kPT];
+  if (sp.cs0 < sp.cs1) load_chunk(srow, nr, sp.cs0, v);
+  for (int cs = sp.cs0; cs < sp.cs1; ++cs) {
+    if (MULTI && cs + 1 < sp.cs1) load_chunk(srow, nr, cs + 1, vn);   // the next sub-chunk lands meanwhile
 #pragma unroll
-  for (int k = 0; k < kPT; ++k)
-    if (in_row(nr, c, k)) m = fmaxf(m, v[k]);
+    for (int k = 0; k < kPT; ++k) {
+      if (in_row(nr, cs, k)) m = fmaxf(m, v[k]);
+      if (MULTI) v[k] = vn[k];
+    }
+  }
   m = block_max(m, red);
-  if (threadIdx.x == 0) chunk_max[int64_t(row) * chunks + c] = m;
+  if (threadIdx.x == 0) chunk_max[int64_t(row) * gridDim.x + c] = m;
   // this block's share of the row's histogram counters
-  const int per = (kHistPerRow + chunks - 1) / chunks;
+  const int per = (kHistPerRow + gridDim.x - 1) / gridDim.x;
   const int e0 = c * per, e1 = min(kHistPerRow, e0 + per);
   u64* h = hist + int64_t(row) * kHistPerRow;
   for (int e = e0 + threadIdx.x; e < e1; e += kT) h[e] = 0;
 }
 
 // The row maximum comes from nmax partial maxima per row: the max kernel's per
-// chunk, or (fused decode step) the score kernel's per block.
-template <bool RAGGED>
-__global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict__ scores, int n, int chunks,
+// block, or (fused decode step) the score kernel's per block.
+template <bool RAGGED, bool MULTI>
+__global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict__ scores, int n, int chunks, int spb,
                                                          const float* __restrict__ rmax, int nmax, float scale_log2e,
                                                          float p, u64* __restrict__ hist, uint32_t* __restrict__ state,
                                                          const int32_t* __restrict__ seq_n,
@@ -238,17 +265,23 @@ __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict
   __shared__ u64 h[kBins1];
   __shared__ float red[kTW];
   const int row = blockIdx.y, c = blockIdx.x;
-  for (int b = threadIdx.x; b < kBins1; b += kT) h[b] = 0;
-  float v[kPT];
-  load_chunk(scores + int64_t(row) * n, n, c, v);
   const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, row, n, p) : RowSel{n, p};
-  if (RAGGED && (c * kChunk >= rs.n || rs.p >= 1.f)) return;   // block-uniform: nothing of this row to histogram here
+  const Span sp = block_span<MULTI>(c, spb, chunks, rs.n);
+  if (RAGGED && (sp.cs1 <= sp.cs0 || rs.p >= 1.f)) return;   // block-uniform: nothing of this row to histogram here
+  for (int b = threadIdx.x; b < kBins1; b += kT) h[b] = 0;
+  const float* srow = scores + int64_t(row) * n;
+  float v[kPT], vn[kPT];
+  load_chunk(srow, rs.n, sp.cs0, v);
   const float m = row_max(rmax + int64_t(row) * nmax, nmax, red);   // barriers: h is clear after it
   if (c == 0 && threadIdx.x == 0) state[int64_t(row) * kToppStateWords + 6] = __float_as_uint(m);   // for the next passes
+  for (int cs = sp.cs0; cs < (MULTI ? sp.cs1 : sp.cs0 + 1); ++cs) {
+    if (MULTI && cs + 1 < sp.cs1) load_chunk(srow, rs.n, cs + 1, vn);
 #pragma unroll
-  for (int k = 0; k < kPT; ++k) {
-    const u64 ms = fixed_mass(v[k], m, scale_log2e);
-    if (in_row(rs.n, c, k) && ms) atomicAdd(&h[score_key(v[k]) >> 20], ms);
+    for (int k = 0; k < kPT; ++k) {
+      const u64 ms = fixed_mass(v[k], m, scale_log2e);
+      if (in_row(rs.n, cs, k) && ms) atomicAdd(&h[score_key(v[k]) >> 20], ms);
+      if (MULTI) v[k] = vn[k];
+    }
   }
   __syncthreads();
   u64* g = hist + int64_t(row) * kHistPerRow;
@@ -259,8 +292,8 @@ __global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict
 
 // Level 2 (LEVEL == 2) or level 3 (LEVEL == 3): find the previous level's
 // crossing, then histogram the keys inside it.
-template <int LEVEL, bool RAGGED>
-__global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict__ scores, int n, int chunks,
+template <int LEVEL, bool RAGGED, bool MULTI>
+__global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict__ scores, int n, int chunks, int spb,
                                                         float scale_log2e, float p, u64* __restrict__ hist,
                                                         uint32_t* __restrict__ state,
                                                         int32_t* __restrict__ chunk_cnt,
@@ -279,10 +312,12 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   for (int b = threadIdx.x; b < kBins; b += kT) h[b] = 0;
   u64* coarse = rh + kBins1 + kBins2 + kBins3;
   const u64 cpre = threadIdx.x < kWave ? coarse[(LEVEL == 2 ? 0 : kCoarse) + threadIdx.x] : 0;
-  float v[kPT];
-  load_chunk(scores + int64_t(row) * n, n, c, v);
   const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, row, n, p) : RowSel{n, p};
-  if (RAGGED && (c * kChunk >= rs.n || rs.p >= 1.f)) return;   // block-uniform (the write pass handles p >= 1)
+  const Span sp = block_span<MULTI>(c, spb, chunks, rs.n);
+  if (RAGGED && (sp.cs1 <= sp.cs0 || rs.p >= 1.f)) return;   // block-uniform (the write pass handles p >= 1)
+  const float* srow = scores + int64_t(row) * n;
+  float v[kPT], vn[kPT];
+  load_chunk(srow, rs.n, sp.cs0, v);
   const float m = __uint_as_float(st[6]);   // the row max, from level 1 (h is clear after the search's barrier)
   uint32_t prefix;
   if (LEVEL == 2) {
@@ -304,17 +339,22 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   }
   const int shift_hi = LEVEL == 2 ? 20 : 8;
   int above = 0;   // level 3: keys above the 24-bit bin, certainly selected
+  for (int cs = sp.cs0; cs < (MULTI ? sp.cs1 : sp.cs0 + 1); ++cs) {
+    if (MULTI && cs + 1 < sp.cs1) load_chunk(srow, rs.n, cs + 1, vn);
 #pragma unroll
-  for (int k = 0; k < kPT; ++k) {
-    if (!in_row(rs.n, c, k)) continue;
-    const uint32_t key = score_key(v[k]);
-    if ((key >> shift_hi) == prefix) {
-      const uint32_t bin = LEVEL == 2 ? ((key >> 8) & 0xfffu) : (key & 0xffu);
-      const u64 ms = fixed_mass(v[k], m, scale_log2e);
-      if (ms) atomicAdd(&h[bin], ms);
-      if (LEVEL == 3) atomicAdd(&cnt_s[bin], 1u);
-    } else if (LEVEL == 3 && (key >> 8) > prefix) {
-      ++above;
+    for (int k = 0; k < kPT; ++k) {
+      const uint32_t key = score_key(v[k]);
+      if (in_row(rs.n, cs, k)) {
+        if ((key >> shift_hi) == prefix) {
+          const uint32_t bin = LEVEL == 2 ? ((key >> 8) & 0xfffu) : (key & 0xffu);
+          const u64 ms = fixed_mass(v[k], m, scale_log2e);
+          if (ms) atomicAdd(&h[bin], ms);
+          if (LEVEL == 3) atomicAdd(&cnt_s[bin], 1u);
+        } else if (LEVEL == 3 && (key >> 8) > prefix) {
+          ++above;
+        }
+      }
+      if (MULTI) v[k] = vn[k];
     }
   }
   if (LEVEL == 3) {
@@ -327,9 +367,9 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
     if (h[b]) atomicAdd(&g[b], h[b]);
   if (LEVEL == 2) flush_coarse(h, coarse + kCoarse);
   if (LEVEL == 3) {
-    // this chunk's count above the bin, then suffix counts of the 256 sub-bins
+    // this block's count above the bin, then suffix counts of the 256 sub-bins
     static_assert(kBins3 == kT, "one sub-bin per thread");
-    int32_t* cc = chunk_cnt + (int64_t(row) * chunks + c) * (1 + kBins3);
+    int32_t* cc = chunk_cnt + (int64_t(row) * gridDim.x + c) * (1 + kBins3);
     const int t = threadIdx.x, ln = lane_id(), wv = t / kWave;
     int x = int(cnt_s[t]);
 #pragma unroll
@@ -347,9 +387,10 @@ __global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict_
   }
 }
 
-template <bool RAGGED>
-__global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict__ scores, int n, int chunks, float p,
-                                                        const u64* __restrict__ hist, uint32_t* __restrict__ state,
+template <bool RAGGED, bool MULTI>
+__global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict__ scores, int n, int chunks, int spb,
+                                                        float p, const u64* __restrict__ hist,
+                                                        uint32_t* __restrict__ state,
                                                         const int32_t* __restrict__ chunk_cnt,
                                                         int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_count,
                                                         u64* __restrict__ masks, const int32_t* __restrict__ seq_n,
@@ -362,23 +403,25 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
   const int wave = threadIdx.x / kWave, lane = lane_id();
   uint32_t* st = state + int64_t(row) * kToppStateWords;
   static_assert(kBins3 == kT, "one final-level bin per thread");
-  const u64 hv = hist[int64_t(row) * kHistPerRow + kBins1 + kBins2 + threadIdx.x];
-  float v[kPT];
-  load_chunk(scores + int64_t(row) * n, n, c, v);
   const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, row, n, p) : RowSel{n, p};
-  if (RAGGED && c * kChunk >= rs.n) {   // block-uniform: no key of this row here (a row without keys selects none)
+  const Span sp = block_span<MULTI>(c, spb, chunks, rs.n);
+  if (RAGGED && sp.cs1 <= sp.cs0) {   // block-uniform: no key of this row here (a row without keys selects none)
     if (c == 0 && threadIdx.x == 0) sel_count[row] = 0;
     return;
   }
+  const u64 hv = hist[int64_t(row) * kHistPerRow + kBins1 + kBins2 + threadIdx.x];
+  const float* srow = scores + int64_t(row) * n;
+  float v[kPT], vn[kPT];
+  load_chunk(srow, rs.n, sp.cs0, v);
   const bool all = RAGGED && rs.p >= 1.f;   // every key of the row (the histogram passes skipped it)
-  uint32_t kstar = 0u;            // keys >= kstar are selected (every key is >= 0)
-  int offset = c * kChunk;
+  uint32_t kstar = 0u;                      // keys >= kstar are selected (every key is >= 0)
+  int offset = sp.cs0 * kChunk;
   if (!all) {
     const u64 T = (u64(st[5]) << 32) | st[4];
     find_crossing<1>(&hv, T, 0.f, wtot, &cr);
     kstar = (st[3] << 8) | cr.bin;
-    // offset of this chunk = selected keys of the chunks before it
-    const int32_t* cc = chunk_cnt + int64_t(row) * chunks * (1 + kBins3);
+    // offset of this block = selected keys of the blocks before it
+    const int32_t* cc = chunk_cnt + int64_t(row) * gridDim.x * (1 + kBins3);
     int before = 0;
     for (int k = threadIdx.x; k < c; k += kT) before += cc[k * (1 + kBins3)] + cc[k * (1 + kBins3) + 1 + cr.bin];
     before = wave_sum_int(before);
@@ -389,35 +432,43 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
     for (int w = 0; w < kTW; ++w) offset += red[w];
   }
 
-  // ascending compaction: element (k, thread) has index c*kChunk + k*kT + thread, so the
-  // order is k-major, then wave, then lane; all kPT ballots first, one barrier
+  // ascending compaction, sub-chunk by sub-chunk: element (k, thread) of sub-chunk cs has
+  // index cs*kChunk + k*kT + thread, so the order is k-major, then wave, then lane
   int32_t* out = sel_idx + int64_t(row) * n;
-  uint64_t bal[kPT];
+  for (int cs = sp.cs0; cs < (MULTI ? sp.cs1 : sp.cs0 + 1); ++cs) {
+    if (MULTI && cs + 1 < sp.cs1) load_chunk(srow, rs.n, cs + 1, vn);
+    uint64_t bal[kPT];
 #pragma unroll
-  for (int k = 0; k < kPT; ++k) {
-    bal[k] = __ballot(in_row(rs.n, c, k) && score_key(v[k]) >= kstar);
-    if (lane == 0) {
-      kcnt[k][wave] = __popcll(bal[k]);
-      // keys c*kChunk + k*kT + 64 wave + [0, 64) of the row's selection bitmap
-      if (masks) masks[int64_t(row) * chunks * (kChunk / 64) + c * (kChunk / 64) + k * kTW + wave] = bal[k];
+    for (int k = 0; k < kPT; ++k) {
+      bal[k] = __ballot(in_row(rs.n, cs, k) && score_key(v[k]) >= kstar);
+      if (lane == 0) {
+        kcnt[k][wave] = __popcll(bal[k]);
+        // keys cs*kChunk + k*kT + 64 wave + [0, 64) of the row's selection bitmap
+        if (masks) masks[int64_t(row) * chunks * (kChunk / 64) + cs * (kChunk / 64) + k * kTW + wave] = bal[k];
+      }
+      if (MULTI) v[k] = vn[k];
     }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kPT; ++k) {
+      int woff = 0, tot = 0;
+#pragma unroll
+      for (int w = 0; w < kTW; ++w) {
+        woff += w < wave ? kcnt[k][w] : 0;
+        tot += kcnt[k][w];
+      }
+      if ((bal[k] >> lane) & 1u) {
+        const int pre =
+            __builtin_amdgcn_mbcnt_hi(uint32_t(bal[k] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal[k]), 0u));
+        out[offset + woff + pre] = cs * kChunk + k * kT + int(threadIdx.x);
+      }
+      offset += tot;
+    }
+    if (MULTI && cs + 1 < sp.cs1) __syncthreads();   // kcnt is rewritten for the next sub-chunk
   }
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < kPT; ++k) {
-    int woff = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < kTW; ++w) {
-      woff += w < wave ? kcnt[k][w] : 0;
-      tot += kcnt[k][w];
-    }
-    if ((bal[k] >> lane) & 1u) {
-      const int pre = __builtin_amdgcn_mbcnt_hi(uint32_t(bal[k] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal[k]), 0u));
-      out[offset + woff + pre] = c * kChunk + k * kT + int(threadIdx.x);
-    }
-    offset += tot;
-  }
-  if (c == (RAGGED ? (rs.n - 1) / kChunk : chunks - 1) && threadIdx.x == 0) sel_count[row] = offset;   // its last chunk
+  // the block holding the row's last key writes the count
+  const int last = RAGGED ? ((rs.n - 1) / kChunk) / spb : int(gridDim.x) - 1;
+  if (c == last && threadIdx.x == 0) sel_count[row] = offset;
 }
 
 __global__ __launch_bounds__(kT) void topp_all_kernel(int n, int32_t* __restrict__ sel_idx,
@@ -433,24 +484,28 @@ __global__ __launch_bounds__(kT) void topp_all_kernel(int n, int32_t* __restrict
   }
 }
 
-template <bool RAGGED>
-void topp_passes(dim3 grid, hipStream_t stream, int n, int chunks, const float* scores, float p, float scale_log2e,
-                 const ToppWorkspace& w, int32_t* sel_idx, int32_t* sel_count, const float* slot_max, int nslots,
-                 u64* masks, const int32_t* seq_n, const float* seq_p, int heads_q) {
+constexpr int kToppWaveBlocks = 1024;   // blocks per pass the sub-chunks are shared out to (about one wave)
+
+template <bool RAGGED, bool MULTI>
+void topp_passes(int rows, hipStream_t stream, int n, int chunks, int spb, const float* scores, float p,
+                 float scale_log2e, const ToppWorkspace& w, int32_t* sel_idx, int32_t* sel_count,
+                 const float* slot_max, int nslots, u64* masks, const int32_t* seq_n, const float* seq_p,
+                 int heads_q) {
+  const dim3 grid((chunks + spb - 1) / spb, rows);
   const float* rmax = slot_max;
   int nmax = nslots;
   if (slot_max == nullptr) {   // otherwise the score launch has written the maxima and cleared the counters
-    topp_max_kernel<RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, w.chunk_max, w.hist, seq_n, heads_q);
+    topp_max_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, w.chunk_max, w.hist, seq_n, heads_q);
     rmax = w.chunk_max;
-    nmax = chunks;
+    nmax = int(grid.x);
   }
-  topp_level1_kernel<RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, rmax, nmax, scale_log2e, p, w.hist, w.state,
-                                                      seq_n, seq_p, heads_q);
-  topp_level_kernel<2, RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, scale_log2e, p, w.hist, w.state,
+  topp_level1_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, rmax, nmax, scale_log2e, p, w.hist,
+                                                      w.state, seq_n, seq_p, heads_q);
+  topp_level_kernel<2, RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, scale_log2e, p, w.hist, w.state,
                                                         w.chunk_cnt, seq_n, seq_p, heads_q);
-  topp_level_kernel<3, RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, scale_log2e, p, w.hist, w.state,
+  topp_level_kernel<3, RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, scale_log2e, p, w.hist, w.state,
                                                         w.chunk_cnt, seq_n, seq_p, heads_q);
-  topp_write_kernel<RAGGED><<<grid, kT, 0, stream>>>(scores, n, chunks, p, w.hist, w.state, w.chunk_cnt, sel_idx,
+  topp_write_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, p, w.hist, w.state, w.chunk_cnt, sel_idx,
                                                      sel_count, masks, seq_n, seq_p, heads_q);
 }
 
@@ -471,13 +526,16 @@ rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, fl
   const int chunks = (n + kChunk - 1) / kChunk;
   ToppWorkspace w = topp_workspace(ws, rows, n);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
-  const dim3 grid(chunks, rows);
-  if (ragged)
-    topp_passes<true>(grid, stream, n, chunks, scores, p, scale_log2e, w, sel_idx, sel_count, slot_max, nslots, masks,
-                      seq_n, seq_p, heads_q);
-  else
-    topp_passes<false>(grid, stream, n, chunks, scores, p, scale_log2e, w, sel_idx, sel_count, slot_max, nslots,
-                       masks, nullptr, nullptr, heads_q);
+  const int spb = int(std::min<int64_t>(chunks, std::max<int64_t>(1, int64_t(rows) * chunks / kToppWaveBlocks)));
+#define RBQ_TOPP_PASSES(RG, MU)                                                                                  \
+  topp_passes<RG, MU>(rows, stream, n, chunks, spb, scores, p, scale_log2e, w, sel_idx, sel_count, slot_max,   \
+                      nslots, masks, RG ? seq_n : nullptr, RG ? seq_p : nullptr, heads_q)
+  if (ragged) {
+    if (spb > 1) RBQ_TOPP_PASSES(true, true); else RBQ_TOPP_PASSES(true, false);
+  } else {
+    if (spb > 1) RBQ_TOPP_PASSES(false, true); else RBQ_TOPP_PASSES(false, false);
+  }
+#undef RBQ_TOPP_PASSES
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

@@ -122,3 +122,36 @@ class DecodeState:
         self.sparse_decode(stream)
         if flush:
             self.flush_window(stream)
+
+    # ---------------------------------------------------------------- ragged batches
+    # seq_n / seq_w / seq_p: per-sequence indexed keys, window rows (the cache
+    # tail after them) and p, as int32 / int32 / float32 device tensors [B]; the
+    # state's n and w are the largest counts (n + w <= cap).
+    def build_index_ragged(self, seq_n_host, stream=None):
+        """Index construction of a ragged batch: sequence b over its rows
+        [0, seq_n_host[b]) with its own centroid (a sequence without keys keeps a
+        zero centroid)."""
+        for b, nb in enumerate(seq_n_host):
+            nb = min(int(nb), self.n)
+            if nb > 0:
+                rbq.rbq_encode_keys(1, self.Hkv, self.D, self.K[b:b + 1], self.cap, nb, 0, self.cap, self.P,
+                                    None if self.c_q is None else self.c_q[b:b + 1], self.c_k[b:b + 1],
+                                    self.codes[b:b + 1], self.kfac[b:b + 1], rbq.RBQ_ENCODE_SET_CENTROID, None,
+                                    self.ws_encode, stream)
+
+    def step_ragged(self, seq_n, seq_w, seq_p, stream=None, flush=True):
+        """One decode step of a ragged batch (rbq_decode_step_varlen)."""
+        rbq.rbq_decode_step_varlen(self.B, self.Hq, self.Hkv, self.D, self.q, self.P, self.c_q, self.c_k, self.K,
+                                   self.V, self.cap, self.n, self.w, seq_n, seq_w, self.codes, self.kfac, flush,
+                                   seq_p, self.sm_scale, self.qplanes, self.qscal, self.scores, self.sel_idx,
+                                   self.sel_count, self.out, self.lse, self.ws_step, stream)
+
+    def sparse_decode_ragged(self, seq_n, seq_w, stream=None):
+        rbq.rbq_sparse_decode_varlen(self.B, self.Hq, self.Hkv, self.D, self.q, self.K, self.V, self.cap, self.n,
+                                     self.w, seq_n, seq_w, self.sel_idx, self.sel_count, self.sm_scale, self.out,
+                                     self.lse, self.ws_decode, stream)
+
+    def dense_decode_ragged(self, seq_n, seq_w, out=None, lse=None, stream=None):
+        rbq.rbq_dense_decode_varlen(self.B, self.Hq, self.Hkv, self.D, self.q, self.K, self.V, self.cap, self.n,
+                                    self.w, seq_n, seq_w, self.sm_scale, self.out if out is None else out,
+                                    self.lse if lse is None else lse, self.ws_decode, stream)

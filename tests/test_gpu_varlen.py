@@ -23,23 +23,28 @@ import parity_util as pu
 
 pytestmark = pytest.mark.gpu
 
-# (Hq, Hkv, kv dtype, seq_n, seq_w, seq_p, n slack, seed)
+# (Hq, Hkv, kv dtype, seq_n, seq_w, seq_p, n (the largest count, the row stride), seed)
 CASES = [
     # G = 4 bf16: the largest sequence, one without indexed keys (window only), one a key past a
     # Top-p chunk with p = 1, a short one
-    (8, 2, "bf16", [6000, 0, 4097, 1234], [48, 17, 0, 33], [0.9, 0.7, 1.0, 0.95], 0, 11),
+    (8, 2, "bf16", [6000, 0, 4097, 1234], [48, 17, 0, 33], [0.9, 0.7, 1.0, 0.95], 6000, 11),
     # G = 1 fp32 K/V; n above every count; a sequence of one key
-    (4, 4, "f32", [700, 1500, 1], [5, 0, 9], [0.5, 0.99, 0.8], 300, 12),
+    (4, 4, "f32", [700, 1500, 1], [5, 0, 9], [0.5, 0.99, 0.8], 1800, 12),
     # G = 16; p <= 0 and NaN act as the smallest positive p; a count above n is clamped to n
-    (16, 1, "bf16", [2049, 4096, 9000], [0, 64, 64], [-1.0, float("nan"), 0.9], 0, 13),
+    (16, 1, "bf16", [2049, 4096, 9000], [0, 64, 64], [-1.0, float("nan"), 0.9], 8192, 13),
     # no window anywhere, no indexed key anywhere but one sequence
-    (8, 2, "bf16", [0, 3000], [0, 0], [0.9, 0.8], 0, 14),
+    (8, 2, "bf16", [0, 3000], [0, 0], [0.9, 0.8], 3000, 14),
+    # 256 rows x 10 Top-p sub-chunks: each selection block walks two of them (one when the
+    # sequence ends inside its span), counts on and next to sub-chunk boundaries
+    (16, 1, "bf16", [40000, 0, 4096, 4097, 8192, 12288, 12289, 20000, 1, 39999, 30000, 25000, 16384, 16385, 100,
+                     33333],
+     [0, 5, 64, 1, 0, 17, 33, 64, 2, 0, 9, 64, 50, 0, 64, 3],
+     [0.9, 0.8, 0.95, 1.0, 0.5, 0.99, 0.7, 0.9, 0.9, 0.85, 0.9, 0.92, 0.6, 0.9, 0.9, 0.9], 40000, 15),
 ]
-N_CAP = 8192   # largest n of the cases above (9000 is clamped to it)
 
 
 def _ids(c):
-    return f"Hq{c[0]}-Hkv{c[1]}-{c[2]}-n{'_'.join(map(str, c[3]))}"
+    return f"Hq{c[0]}-Hkv{c[1]}-{c[2]}-B{len(c[3])}-n{c[6]}-seed{c[7]}"
 
 
 @pytest.fixture(scope="module")
@@ -62,9 +67,8 @@ def _p_eff(p):
 
 
 def _setup(R, pipeline, case):
-    Hq, Hkv, dt, seq_n, seq_w, seq_p, slack, seed = case
+    Hq, Hkv, dt, seq_n, seq_w, seq_p, n, seed = case
     B = len(seq_n)
-    n = min(max(seq_n), N_CAP) + slack
     w = max(seq_w)
     wl = gen.random_case(B, Hq, Hkv, n, seed=seed, kv_dtype=dt, w=w, c_q_scale=0.5)
     st = pipeline.DecodeState.from_workload(wl)
