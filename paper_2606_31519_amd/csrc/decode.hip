@@ -29,12 +29,12 @@
 // Waves merge in LDS; the block writes (m, l, acc[D]) per head; a combine
 // kernel merges the splits in fixed order (bitwise deterministic).
 //
-// Ragged batches (seq_n != NULL, sparse only): sequence b has seq_n[b] indexed
-// rows (clamped to [0, n]) and seq_w[b] window rows (clamped to [0, w]; all w
-// when seq_w is NULL), the window being its cache tail, rows [seq_n[b],
-// seq_n[b] + seq_w[b]) of K / V (K_loc = K, loc_ld = cap). The grid is sized
-// by n and w; a split past a sequence's rows finds none and writes an empty
-// partial state.
+// Ragged batches (seq_n != NULL): sequence b has seq_n[b] indexed rows
+// (clamped to [0, n]) and seq_w[b] window rows (clamped to [0, w]; all w when
+// seq_w is NULL), the window being its cache tail, rows [seq_n[b], seq_n[b] +
+// seq_w[b]) of K / V (K_loc = K, loc_ld = cap). The grid is sized by n and w
+// and launched split-major; a sequence's window is spread over its own splits,
+// and a split past its rows writes an empty partial state and leaves.
 #include <cmath>
 
 #include "rbq_device.h"
@@ -48,6 +48,7 @@ constexpr int kDThreads = kDWaves * kWave;
 constexpr int kBmWords = kDecodeChunk / 32;                       // words of the indexed positions
 constexpr int kListRounds = (kDecodeChunk + kDecodeFoldMax + kDThreads - 1) / kDThreads;
 constexpr int kListCap = kListRounds * kDThreads;                 // list positions (indexed + folded window)
+static_assert(kListCap == kDecodeListCap, "the split sizing on the host assumes this list capacity");
 constexpr int kBmAll = kListCap / 32;
 constexpr float kLn2 = 0.69314718055994531f;
 __device__ __forceinline__ float wmax64(float v) { v = max32(v); return fmaxf(v, __shfl_xor(v, 32, kWave)); }
@@ -306,8 +307,9 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   __shared__ float sm[kDWaves][G], sl[kDWaves][G];
   __shared__ float sacc[kDWaves][G][kHeadDim];
 
-  const int split = blockIdx.x;
-  const int bh = blockIdx.y;
+  // (ragged grids are split-major, so the empty splits past short sequences come last)
+  const int split = RAGGED ? blockIdx.y : blockIdx.x;
+  const int bh = RAGGED ? blockIdx.x : blockIdx.y;
   const int b = bh / Hkv, hk = bh - b * Hkv;
   const int row0 = b * Hq + hk * G;     // first query head of the group
   const int wave = threadIdx.x / kWave, lane = lane_id();
@@ -321,7 +323,13 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   if (!window) {
     c0 = split * chunk;
     c1 = RAGGED ? max(c0, min(nb, c0 + chunk)) : min(n, c0 + chunk);
-    if (fold_wq > 0 && split >= fold_s0) {
+    if (RAGGED && fold_wq > 0) {
+      // this sequence's window spread over its own splits (fold_wq: the most one split takes)
+      const int sb = max((nb + chunk - 1) / chunk, (wb + fold_wq - 1) / fold_wq);
+      const int wq = sb > 0 ? (wb + sb - 1) / sb : 0;
+      nwin = min(max(wb - split * wq, 0), wq);
+      wrow0 = nb + split * wq;
+    } else if (fold_wq > 0 && split >= fold_s0) {
       const int k = split - fold_s0;
       nwin = min(max(wb - k * fold_wq, 0), fold_wq);
       wrow0 = nb + k * fold_wq;
@@ -545,8 +553,8 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   __shared__ float sm[kDWaves][G], sl[kDWaves][G];
   __shared__ float sacc[kDWaves][G][kHeadDim];
 
-  const int split = blockIdx.x;
-  const int bh = blockIdx.y;
+  const int split = RAGGED ? blockIdx.y : blockIdx.x;   // (ragged grids are split-major)
+  const int bh = RAGGED ? blockIdx.x : blockIdx.y;
   const int b = bh / Hkv, hk = bh - b * Hkv;
   const int row0 = b * Hq + hk * G;
   const int wave = threadIdx.x / kWave, lane = lane_id();
@@ -561,7 +569,13 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   if (!window) {
     c0 = split * chunk;
     c1 = RAGGED ? max(c0, min(nb, c0 + chunk)) : min(n, c0 + chunk);
-    if (fold_wq > 0 && split >= fold_s0) {
+    if (RAGGED && fold_wq > 0) {
+      // this sequence's window spread over its own splits (fold_wq: the most one split takes)
+      const int sb = max((nb + chunk - 1) / chunk, (wb + fold_wq - 1) / fold_wq);
+      const int wq = sb > 0 ? (wb + sb - 1) / sb : 0;
+      nwin = min(max(wb - split * wq, 0), wq);
+      wrow0 = nb + split * wq;
+    } else if (fold_wq > 0 && split >= fold_s0) {
       const int k = split - fold_s0;
       nwin = min(max(wb - k * fold_wq, 0), fold_wq);
       wrow0 = nb + k * fold_wq;
@@ -887,8 +901,8 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                      (static_cast<const char*>(K_loc) == static_cast<const char*>(K) + size_t(n) * kHeadDim * elem &&
                       static_cast<const char*>(V_loc) == static_cast<const char*>(V) + size_t(n) * kHeadDim * elem)) &&
                     (int64_t(n) + w) * kHeadDim * int64_t(elem) < (int64_t(1) << 31);
-  const DecodeSplits sp = decode_splits(batch, heads_kv, n, w, tail, sparse);
-  const dim3 grid(sp.total(), batch * heads_kv);
+  const DecodeSplits sp = decode_splits(batch, heads_kv, n, w, tail, sparse, seq_n != nullptr);
+  const dim3 grid = seq_n ? dim3(batch * heads_kv, sp.total()) : dim3(sp.total(), batch * heads_kv);
   float* part = static_cast<float*>(ws);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
   rbq_status st;

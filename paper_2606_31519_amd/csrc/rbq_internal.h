@@ -67,13 +67,17 @@ struct DecodeSplits {
   int32_t total() const { return idx_splits + win_splits; }
 };
 constexpr int kDecodeFoldMax = 64;        // window rows a sparse split may take beside its indexed rows
+constexpr int kDecodeListCap = 1280;      // row-list positions of a sparse split (indexed + folded window)
 // tail_window: the window rows are rows [n, n + w) of K / V (the cache tail).
 // Then they are folded into the indexed splits instead of splits of their own
 // (a grid of whole waves of resident blocks for the usual shapes): spread over
 // every split for the sparse call (they are dense, the indexed rows are not),
 // given to the last split, beside its rows, for the dense call.
+// ragged: each sequence's window is spread on the device over that sequence's
+// own splits, fold_wq then being the most a split may take (the list room left
+// by the chunk), provided every sequence's window fits its splits that way.
 DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w, bool tail_window = false,
-                           bool sparse = false);
+                           bool sparse = false, bool ragged = false);
 size_t decode_workspace_bytes(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
                               int32_t w);
 

@@ -99,7 +99,8 @@ rbq_status check_topp(int32_t batch, int32_t heads_q, int32_t n, const float* sc
   return RBQ_OK;
 }
 
-DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w, bool tail_window, bool sparse) {
+DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w, bool tail_window, bool sparse,
+                           bool ragged) {
   DecodeSplits s;
   s.fold_s0 = 0;
   s.fold_wq = 0;
@@ -110,7 +111,13 @@ DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w
   s.idx_splits = n > 0 ? (n + s.chunk - 1) / s.chunk : 0;
   s.win_splits = w > 0 ? (w + kDecodeWinChunk - 1) / kDecodeWinChunk : 0;
   if (tail_window && s.idx_splits > 0 && w > 0) {
-    if (sparse) {
+    if (ragged) {
+      const int cap = kDecodeListCap - s.chunk;   // window rows a split's list can still take
+      if ((w + cap - 1) / cap <= s.idx_splits) {
+        s.fold_wq = cap;
+        s.win_splits = 0;
+      }
+    } else if (sparse) {
       const int wq = (w + s.idx_splits - 1) / s.idx_splits;
       if (wq <= kDecodeFoldMax) {
         s.fold_wq = wq;
