@@ -298,6 +298,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-sweep", action="store_true", help="skip the Top-p sweep (p = 0.8 / 0.9 / 0.95 / 0.99)")
     ap.add_argument("--no-ragged", action="store_true", help="skip the ragged-batch step (16 sequences of mixed length)")
+    ap.add_argument("--ragged-only", action="store_true", help="only the ragged-batch step (for its kernel profile)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
@@ -316,6 +317,9 @@ def main():
     from workloads import gen
 
     torch.cuda.set_device(0)
+    if args.ragged_only:
+        print(json.dumps({"ragged": time_ragged(pipeline, gen, torch, args.steps, args.warmup)}), flush=True)
+        return
     t_gen = time.perf_counter()
     wl = gen.config3()
     t_gen = time.perf_counter() - t_gen
