@@ -18,8 +18,9 @@ The per-stage times come from the separate calls. The line also carries the
 roofline of the dominant call, the Top-p
 sweep (p = 0.8 / 0.9 / 0.95 / 0.99: step time, budget, KV-group union), the
 standalone score scan of the wide-head workload, a ragged serving batch (16
-sequences of mixed length, window and p) against its dense decode, and the
-oracle's CPU rate.
+sequences of mixed length, window and p) against its dense decode, the
+attention recall of the selections against exact and fixed-budget Top-k, and
+the oracle's CPU rate.
 """
 from __future__ import annotations
 
@@ -287,6 +288,89 @@ def time_ragged(pipeline, gen, torch, steps, warmup, seed=20260):
             "budget_frac_mean": float(frac.mean()), "union_frac": union / idx_rows}
 
 
+def quality(pipeline, torch, st, p_list, seed=20261):
+    """Attention recall (Table budget_recall_stats): the share of a head's exact
+    softmax attention over the indexed keys, softmax(K q tau), that a selected
+    set holds. For each p: the adaptive Top-p set chosen from the estimates (one
+    rbq_decode_step), the exact Top-k set of the same per-head budget (the best
+    any selector of that budget can do), and a fixed-budget Top-k on the
+    estimates (every head gets the mean budget). Then the re-centering
+    ablation of Section 5.4 at p = 0.95, with the index built around the key
+    centroid (Algorithm 1) or around 0: on the workload's keys, and on the same
+    keys moved by a common offset of twice their median norm (keys clustered
+    away from the origin; the softmax, hence the exact recall, is unchanged by
+    a common shift). Evaluation only: the exact softmax is plain fp32 tensor
+    work beside the timed path."""
+    from paper_2606_31519_amd import rbq
+    B, Hq, Hkv, D, n = st.B, st.Hq, st.Hkv, st.D, st.n
+    G = Hq // Hkv
+
+    def exact_pi(K):
+        pi = torch.empty(B, Hq, n, device="cuda")
+        for b in range(B):
+            for hk in range(Hkv):
+                Kf = K[b, hk, :n].float()                                         # [n][D]
+                Qg = st.q[b, hk * G:(hk + 1) * G].transpose(0, 1).contiguous()    # [D][G]
+                pi[b, hk * G:(hk + 1) * G] = torch.softmax((Kf @ Qg).transpose(0, 1) * st.sm_scale, dim=-1)
+        return pi
+
+    def measure(pi, scores, sel, cnt):
+        idx = sel[..., :n].long().clamp(0, n - 1)   # (entries past a row's count are masked below)
+        held = torch.arange(n, device="cuda").view(1, 1, n) < cnt.view(B, Hq, 1)
+        r_topp = (torch.gather(pi, -1, idx) * held).sum(-1)
+        cum = torch.sort(pi, dim=-1, descending=True).values.cumsum(-1)           # exact Top-k recall for every k
+        r_exact = torch.gather(cum, -1, (cnt.long() - 1).clamp(min=0).view(B, Hq, 1)).view(B, Hq)
+        k_fix = max(1, int(round(float(cnt.float().mean()))))
+        top_est = torch.topk(scores[..., :n], k_fix, dim=-1).indices
+        r_fixed = torch.gather(pi, -1, top_est).sum(-1)
+        return {"budget_frac": float(cnt.float().mean()) / n, "recall_topp": float(r_topp.mean()),
+                "recall_topp_min": float(r_topp.min()), "recall_exact_topk_same_budget": float(r_exact.mean()),
+                "recall_fixed_budget_topk_on_estimates": float(r_fixed.mean())}
+
+    pi = exact_pi(st.K)
+    out = {}
+    for p in p_list:
+        st.step(p)
+        torch.cuda.synchronize()
+        out[str(p)] = measure(pi, st.scores, st.sel_idx, st.sel_count)
+
+    # re-centering ablation at p = 0.95
+    p = 0.95
+    c_k = torch.empty_like(st.c_k)
+    codes, kfac = torch.empty_like(st.codes), torch.empty_like(st.kfac)
+    qp, qs = torch.empty_like(st.qplanes), torch.empty_like(st.qscal)
+    S, sel, cnt = torch.empty_like(st.scores), torch.empty_like(st.sel_idx), torch.empty_like(st.sel_count)
+    ws = rbq.workspace(rbq.RBQ_OP_ENCODE, B, Hq, Hkv, D, n)
+
+    def select(K, recenter):
+        if recenter:
+            rbq.rbq_encode_keys(B, Hkv, D, K, st.cap, n, 0, st.cap, st.P, st.c_q, c_k, codes, kfac,
+                                rbq.RBQ_ENCODE_SET_CENTROID, None, ws)
+        else:
+            c_k.zero_()
+            rbq.rbq_encode_keys(B, Hkv, D, K, st.cap, n, 0, st.cap, st.P, st.c_q, c_k, codes, kfac, 0)
+        rbq.rbq_quantize_query(B, Hq, Hkv, D, st.q, st.P, st.c_q, c_k, qp, qs)
+        rbq.rbq_score(B, Hq, Hkv, D, n, st.cap, codes, kfac, qp, qs, S)
+        rbq.rbq_topp_select(B, Hq, n, S, p, st.sm_scale, sel, cnt, st.ws_topp)
+        torch.cuda.synchronize()
+
+    for recenter in (True, False):
+        select(st.K, recenter)
+        out[f"{p}_{'recentered' if recenter else 'no_recentering'}"] = measure(pi, S, sel, cnt)
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    direction = torch.randn(D, generator=g)
+    scale = 2.0 * float(st.K[0, 0, :n].float().norm(dim=-1).median())
+    K_off = (st.K.float() + (scale * direction / direction.norm()).cuda()).to(st.K.dtype)
+    pi_off = exact_pi(K_off)
+    for recenter in (True, False):
+        select(K_off, recenter)
+        key = f"{p}_offset_keys_{'recentered' if recenter else 'no_recentering'}"
+        out[key] = measure(pi_off, S, sel, cnt)
+    del pi, pi_off, K_off
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -299,6 +383,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the Top-p sweep (p = 0.8 / 0.9 / 0.95 / 0.99)")
     ap.add_argument("--no-ragged", action="store_true", help="skip the ragged-batch step (16 sequences of mixed length)")
     ap.add_argument("--ragged-only", action="store_true", help="only the ragged-batch step (for its kernel profile)")
+    ap.add_argument("--no-quality", action="store_true", help="skip the attention-recall report")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
@@ -403,6 +488,13 @@ def main():
         st0.step(p)
         torch.cuda.synchronize()
 
+    # attention recall of the selections (evaluation, not timed)
+    recall = None
+    if not args.no_quality:
+        recall = quality(pipeline, torch, st0, [float(x) for x in (wl.p_sweep or (0.8, 0.9, 0.95, 0.99))])
+        st0.step(p)
+        torch.cuda.synchronize()
+
     # the box's own streaming rate (elementwise copy), a second reference beside the 8 TB/s peak
     copy = _copy_rate(torch, 5)
 
@@ -459,6 +551,7 @@ def main():
         "scan_wide_heads": scan,
         "p_sweep": sweep or None,
         "ragged": ragged,
+        "recall": recall,
         "cpu_baseline": cpu,
         "gen_s": t_gen,
         "git": _git_sha(),

@@ -1,0 +1,51 @@
+"""The attention-recall report of bench.py (Table budget_recall_stats) against
+the oracle's definition of recall, on the same GPU selections: the share of
+the exact softmax attention over the indexed keys that the Top-p set holds,
+and the best share any set of the same size can hold (the exact Top-k)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import rbq_oracle as orc
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def pipeline():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2606_31519_amd import pipeline as pl
+    return pl
+
+
+def test_recall_report_matches_oracle_definition(pipeline):
+    import bench
+    wl = gen.random_case(1, 8, 2, 6000, seed=21, kv_dtype="bf16", c_q_scale=0.0, q_scale=6.0)
+    st = pipeline.DecodeState.from_workload(wl)
+    st.build_index()
+    p = 0.9
+    rep = bench.quality(pipeline, torch, st, [p])
+    st.step(p)
+    torch.cuda.synchronize()
+    sel, cnt = st.sel_idx.cpu().numpy(), st.sel_count.cpu().numpy()
+    tau = 1.0 / math.sqrt(wl.D)
+    got, best = [], []
+    for h in range(wl.Hq):
+        K = wl.K_f32(0, h // wl.G, slice(0, wl.n_index)).astype(np.float64)
+        got.append(orc.attention_recall(wl.q[0, h], K, sel[0, h, :cnt[0, h]], tau))
+        pi = orc.softmax((K @ wl.q[0, h].astype(np.float64)) * tau)
+        best.append(float(np.sort(pi)[::-1][:cnt[0, h]].sum()))
+    r = rep[str(p)]
+    assert abs(r["recall_topp"] - np.mean(got)) < 1e-4, (r["recall_topp"], np.mean(got))
+    assert abs(r["recall_exact_topk_same_budget"] - np.mean(best)) < 1e-4
+    assert abs(r["budget_frac"] - cnt.mean() / wl.n_index) < 1e-9
+    # a set can hold no more than the exact Top-k of its size holds
+    assert r["recall_topp"] <= r["recall_exact_topk_same_budget"] + 1e-6
+    for key in ("0.95_recentered", "0.95_no_recentering", "0.95_offset_keys_recentered",
+                "0.95_offset_keys_no_recentering"):
+        assert 0.0 < rep[key]["recall_topp"] <= 1.0 + 1e-6
+    # re-centering makes the index blind to a common shift of the keys
+    assert abs(rep["0.95_offset_keys_recentered"]["budget_frac"] - rep["0.95_recentered"]["budget_frac"]) < 0.01
