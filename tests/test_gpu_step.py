@@ -102,3 +102,29 @@ def test_fused_step_graph_replays(pipeline):
         _same(_outputs(st), want)
         st.step(p)            # eager work between the replays
         _same(_outputs(st), want)
+
+
+def test_index_build_beside_prefill_attention(pipeline):
+    """The prefill index build on a second stream, started together with a
+    causal attention over the same context (as bench.py times it), writes the
+    same centroid, codes and factors as a build alone."""
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    case = (1, 8, 2, 4096, 0, "bf16", 0.9, False, 8)
+    ref = _state(pipeline, case)
+    torch.cuda.synchronize()
+    want = [t.cpu().numpy().copy() for t in (ref.c_k, ref.codes, ref.kfac)]
+    st = _state(pipeline, case)
+    for t in (st.c_k, st.codes, st.kfac):
+        t.zero_()
+    q = torch.randn(1, st.Hq, st.n, st.D, device="cuda", dtype=torch.bfloat16)
+    k = st.K[:, :, :st.n].repeat_interleave(st.Hq // st.Hkv, dim=1).contiguous()
+    side, main = torch.cuda.Stream(), torch.cuda.current_stream()
+    side.wait_stream(main)
+    with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+        torch.nn.functional.scaled_dot_product_attention(q, k, k, is_causal=True)
+    with torch.cuda.stream(side):
+        st.build_index()
+    main.wait_stream(side)
+    torch.cuda.synchronize()
+    for a, b in zip(want, (st.c_k, st.codes, st.kfac)):
+        assert np.array_equal(a.view(np.uint8), b.cpu().numpy().view(np.uint8))
