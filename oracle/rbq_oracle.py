@@ -128,21 +128,23 @@ def rotate_query(q: np.ndarray, P: np.ndarray, c_q: np.ndarray | None = None) ->
     return dict(A=A, u=u, qrot=rotate(u[None, :], P)[0])
 
 
-def uniform_quantize(qrot: np.ndarray, dtype=np.float64) -> dict:
-    """Uniform scalar quantiser of Appendix A.3.2 with B_q = 4.
+def uniform_quantize(qrot: np.ndarray, dtype=np.float64, bits: int = B_Q) -> dict:
+    """Uniform scalar quantiser of Appendix A.3.2 with B_q = `bits` (4 in the paper).
 
-    [q_l, q_r] is the value range of q', Delta = (q_r - q_l) / 15 and
+    [q_l, q_r] is the value range of q', Delta = (q_r - q_l) / (2^B_q - 1) and
     q_u = Round((q' - q_l) / Delta) with Round(t) = floor(t + 1/2), kept in
-    [0, 15]. Every operation is evaluated in `dtype`: float64 for the oracle's
-    own path, float32 where the decision has to be taken in the kernel's
-    precision (the quantised code is an integer decided by floating point).
+    [0, 2^B_q - 1]. Every operation is evaluated in `dtype`: float64 for the
+    oracle's own path, float32 where the decision has to be taken in the
+    kernel's precision (the quantised code is an integer decided by floating
+    point).
     """
+    levels = (1 << bits) - 1
     x = np.asarray(qrot, dtype=dtype)
     ql, qr = x.min(), x.max()
-    delta = dtype((qr - ql) / dtype(Q_LEVELS))
+    delta = dtype((qr - ql) / dtype(levels))
     if delta > 0:
         t = (x - ql) / delta + dtype(0.5)
-        codes = np.clip(np.floor(t), 0, Q_LEVELS).astype(np.int64)
+        codes = np.clip(np.floor(t), 0, levels).astype(np.int64)
     else:
         codes = np.zeros(x.shape, np.int64)
     return dict(ql=float(ql), qr=float(qr), delta=float(delta), codes=codes, s_u=int(codes.sum()))
@@ -153,14 +155,16 @@ def dequantize(codes: np.ndarray, ql: float, delta: float) -> np.ndarray:
     return delta * np.asarray(codes, np.float64) + ql
 
 
-def quantize_query(q: np.ndarray, P: np.ndarray, c_q: np.ndarray | None, c_k: np.ndarray) -> dict:
-    """Rotation, INT4 quantisation and the per-query constants of Eq. decomposition.
+def quantize_query(q: np.ndarray, P: np.ndarray, c_q: np.ndarray | None, c_k: np.ndarray,
+                   bits: int = B_Q) -> dict:
+    """Rotation, B_q-bit (INT4 by default) quantisation and the per-query
+    constants of Eq. decomposition.
 
     Returns A = ||q - c_q||, q', the quantiser (q_l, Delta, codes, S_u = sum q_u)
     and B0 = <q, c_k>.
     """
     rq = rotate_query(q, P, c_q)
-    qz = uniform_quantize(rq["qrot"])
+    qz = uniform_quantize(rq["qrot"], bits=bits)
     return dict(A=rq["A"], u=rq["u"], qrot=rq["qrot"], ql=qz["ql"], qr=qz["qr"], delta=qz["delta"],
                 codes=qz["codes"], s_u=qz["s_u"],
                 B0=float(np.asarray(q, np.float64) @ np.asarray(c_k, np.float64)))

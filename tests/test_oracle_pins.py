@@ -229,6 +229,49 @@ def test_quantizer_is_nearest_level_and_bounded(dtype):
         assert abs(signs @ (x - qbar)) <= D * qz["delta"] / 2
 
 
+@pytest.mark.parametrize("bits", [1, 2, 3])
+def test_quantizer_fewer_bits_is_nearest_level(bits):
+    """B_q below the paper's 4: codes span [0, 2^B_q - 1] and each is the
+    nearest of the 2^B_q levels (brute force), within Delta / 2."""
+    rng = np.random.default_rng(10 + bits)
+    D, top = 128, (1 << bits) - 1
+    for _ in range(20):
+        x = rng.standard_normal(D)
+        x /= np.linalg.norm(x)
+        qz = orc.uniform_quantize(x.astype(np.float32), dtype=np.float32, bits=bits)
+        c = qz["codes"]
+        assert c.min() == 0 and c.max() == top
+        levels = qz["ql"] + qz["delta"] * np.arange(top + 1)
+        brute = np.argmin(np.abs(x.astype(np.float32).astype(np.float64)[:, None] - levels[None, :]), axis=1)
+        assert np.array_equal(c, brute)
+        assert np.all(np.abs(orc.dequantize(c, qz["ql"], qz["delta"]) - x) <= qz["delta"] / 2 * (1 + 1e-6))
+
+
+def test_one_bit_quantizer_is_the_midpoint_sign():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(128)
+    qz = orc.uniform_quantize(x, bits=1)
+    assert np.array_equal(qz["codes"], (x >= (x.min() + x.max()) / 2).astype(np.int64))
+
+
+def test_quantization_error_scales_with_the_step():
+    """Theorem A.2: the quantisation error of <c_bar, q'> is a sum of D
+    near-uniform errors of width Delta = range / (2^B_q - 1), so going from
+    B_q = 2 to B_q = 4 divides it by (15 / 3) = 5."""
+    D = 128
+    rng = np.random.default_rng(6)
+    err = {2: [], 4: []}
+    for _ in range(400):
+        x = rng.standard_normal(D)
+        x /= np.linalg.norm(x)
+        cbar = rng.choice([-1.0, 1.0], D) / math.sqrt(D)
+        for b in err:
+            qz = orc.uniform_quantize(x, bits=b)
+            err[b].append(cbar @ (x - orc.dequantize(qz["codes"], qz["ql"], qz["delta"])))
+    ratio = np.std(err[2]) / np.std(err[4])
+    assert 4.0 < ratio < 6.0, ratio
+
+
 def test_quantizer_degenerate_query():
     qz = orc.uniform_quantize(np.zeros(128))
     assert qz["delta"] == 0 and qz["codes"].sum() == 0
