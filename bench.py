@@ -295,7 +295,8 @@ def quality(pipeline, torch, st, p_list, seed=20261):
     set holds. For each p: the adaptive Top-p set chosen from the estimates (one
     rbq_decode_step), the exact Top-k set of the same per-head budget (the best
     any selector of that budget can do), and a fixed-budget Top-k on the
-    estimates (every head gets the mean budget). Then the re-centering
+    estimates (every head gets the mean budget). At p = 0.95, the query
+    quantised to 1, 2 or 3 bits instead of 4 (Theorem A.2). Then the re-centering
     ablation of Section 5.4 at p = 0.95, with the index built around the key
     centroid (Algorithm 1) or around 0: on the workload's keys, and on the same
     keys moved by a common offset of twice their median norm (keys clustered
@@ -358,6 +359,13 @@ def quality(pipeline, torch, st, p_list, seed=20261):
     for recenter in (True, False):
         select(st.K, recenter)
         out[f"{p}_{'recentered' if recenter else 'no_recentering'}"] = measure(pi, S, sel, cnt)
+    # the query's quantisation bits (Theorem A.2; 4 in the method), on the workload's own index
+    for bits in (1, 2, 3):
+        rbq.rbq_quantize_query_bits(B, Hq, Hkv, D, st.q, st.P, st.c_q, st.c_k, bits, qp, qs)
+        rbq.rbq_score(B, Hq, Hkv, D, n, st.cap, st.codes, st.kfac, qp, qs, S)
+        rbq.rbq_topp_select(B, Hq, n, S, p, st.sm_scale, sel, cnt, st.ws_topp)
+        torch.cuda.synchronize()
+        out[f"{p}_query_bits_{bits}"] = measure(pi, S, sel, cnt)
     g = torch.Generator(device="cpu").manual_seed(seed)
     direction = torch.randn(D, generator=g)
     scale = 2.0 * float(st.K[0, 0, :n].float().norm(dim=-1).median())

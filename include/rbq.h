@@ -116,6 +116,19 @@ rbq_status rbq_quantize_query(int32_t batch, int32_t heads_q, int32_t heads_kv, 
                               uint32_t* qplanes, float* qscal, hipStream_t stream);
 
 /*
+ * rbq_quantize_query_bits -- rbq_quantize_query with B_q = `bits` quantisation
+ * bits instead of 4 (Theorem A.2 bounds the estimator's error for any B_q;
+ * Section 3.3 uses 4): Delta = (q_r - q_l) / (2^bits - 1), codes in
+ * [0, 2^bits - 1], bit-planes j >= bits zero. The output feeds rbq_score
+ * unchanged. bits in [1, 4]; 5..8: RBQ_EUNSUPPORTED (the scan multiplies
+ * 4-bit codes); otherwise RBQ_EINVAL. bits = 4 gives rbq_quantize_query's
+ * results bitwise.
+ */
+rbq_status rbq_quantize_query_bits(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                   const float* q, const float* P, const float* c_q, const float* c_k,
+                                   int32_t bits, uint32_t* qplanes, float* qscal, hipStream_t stream);
+
+/*
  * rbq_score -- the binary x INT4 score estimate for every indexed key,
  * Algorithm 2 step 2 with Eq. estimator_core, Eqs. kc_bar_dot_q_c2 /
  * estk_cq_c (Appendix A.3.2) and Eq. decomposition (Section 3.1).

@@ -42,6 +42,16 @@ rbq_status rbq_quantize_query(int32_t batch, int32_t heads_q, int32_t heads_kv, 
                                   stream);
 }
 
+rbq_status rbq_quantize_query_bits(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                   const float* q, const float* P, const float* c_q, const float* c_k, int32_t bits,
+                                   uint32_t* qplanes, float* qscal, hipStream_t stream) {
+  if (bits >= 5 && bits <= 8) return RBQ_EUNSUPPORTED;   // the scan multiplies 4-bit query codes
+  if (bits < 1 || bits > 8) return RBQ_EINVAL;
+  const rbq_status s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal);
+  if (s != RBQ_OK) return s;
+  return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, bits);
+}
+
 rbq_status rbq_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
                      const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                      float* scores, hipStream_t stream) {

@@ -4,8 +4,10 @@
 // One block per query head; 2 x 128 threads share the 128 x 128 product (all
 // loads of a thread in flight at once), then 128 threads, one per dimension:
 //   y = q - c_q, A = ||y||, u = y / A, q'[j] = sum_d P[d][j] u[d]   (q' = P^T u)
-//   q_l = min q', q_r = max q', Delta = (q_r - q_l) / 15,
-//   q_u = clamp(floor((q' - q_l) / Delta + 1/2), 0, 15)
+//   q_l = min q', q_r = max q', Delta = (q_r - q_l) / L,
+//   q_u = clamp(floor((q' - q_l) / Delta + 1/2), 0, L)
+// with L = 2^B_q - 1 levels above the lowest (B_q = 4, L = 15, unless the
+// caller asks for fewer bits).
 // The code of each dimension is decided in fp32 with every operation rounded
 // separately (no contraction; IEEE division), so the oracle can repeat the
 // decision exactly from the same q'. Bit-plane j of the codes is one wave
@@ -73,13 +75,13 @@ __device__ __forceinline__ float block_max(float v, float* red) {
   return s;
 }
 
-// The INT4 code of one rotated component, every operation rounded on its own.
-__device__ __forceinline__ int quant_code(float x, float ql, float delta) {
+// The code of one rotated component, every operation rounded on its own.
+__device__ __forceinline__ int quant_code(float x, float ql, float delta, float top) {
 #pragma clang fp contract(off)
   if (!(delta > 0.f)) return 0;
   const float t = __fdiv_rn(__fsub_rn(x, ql), delta);
   float r = floorf(__fadd_rn(t, 0.5f));
-  r = fminf(fmaxf(r, 0.f), 15.f);
+  r = fminf(fmaxf(r, 0.f), top);
   return int(r);
 }
 
@@ -92,6 +94,7 @@ struct QuantArgs {
   float* qscal;
   float* qrot_out;       // or NULL
   int Hq, Hkv;
+  int levels;            // 2^B_q - 1
 };
 
 // query head `row` (= b * Hq + h), by the kQAll threads of the calling block
@@ -148,9 +151,9 @@ __device__ __forceinline__ void quantize_row(const QuantArgs& qa, int row) {
   float delta;
   {
 #pragma clang fp contract(off)
-    delta = __fdiv_rn(__fsub_rn(qr, ql), 15.0f);
+    delta = __fdiv_rn(__fsub_rn(qr, ql), float(qa.levels));
   }
-  const int code = quant_code(acc, ql, delta);
+  const int code = quant_code(acc, ql, delta, float(qa.levels));
   const float su = block_sum(float(code), red);   // exact: integers below 2^24
 
   // bit-plane m, 64 dimensions per wave: low 32 lanes -> word 2w, high -> 2w + 1
@@ -197,8 +200,8 @@ __global__ __launch_bounds__(kQAll) void quantize_flush_kernel(QuantArgs qa, Enc
 
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
-                           hipStream_t stream) {
-  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, qrot_out, heads_q, heads_kv};
+                           hipStream_t stream, int32_t bits) {
+  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, qrot_out, heads_q, heads_kv, (1 << bits) - 1};
   quantize_kernel<<<batch * heads_q, kQAll, 0, stream>>>(qa);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
@@ -210,7 +213,7 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
                                  const int32_t* seq_cnt, int32_t off_max) {
   if (n_new == 0)
     return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
-  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, nullptr, heads_q, heads_kv};
+  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, nullptr, heads_q, heads_kv, 15};
   const EncodeArgs ea{keys,  keys_ld, n_new,   offset,  cap,     P,       c_q,     c_k,     codes,
                       kfac,  nullptr, nullptr, seq_off, seq_cnt, off_max, heads_kv};
   const int rows = batch * heads_q, bhs = batch * heads_kv;

@@ -110,9 +110,10 @@ rbq_status launch_encode(int32_t batch, int32_t heads_kv, const void* keys, int3
                          int32_t n_new, int32_t offset, int32_t cap, const float* P, const float* c_q, float* c_k,
                          uint32_t* codes, float* kfac, uint32_t flags, float* alpha_out, void* ws,
                          float* rot_out, hipStream_t stream);
+// bits: B_q, the query's quantisation bits (1..4)
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
-                           hipStream_t stream);
+                           hipStream_t stream, int32_t bits = 4);
 // query quantisation and, in the same launch, the lazy encode of n_new window
 // keys into index rows [offset, offset + n_new) with the existing c_k (ragged,
 // seq_off != NULL: sequence b encodes min(seq_cnt[b], n_new) keys (n_new without

@@ -26,7 +26,7 @@ EXPORTED = [
     "rbq_dense_decode", "rbq_decode_step", "rbq_workspace_bytes", "rbq_index_bytes", "rbq_status_string", "rbq_version",
     "rbq_encode_keys_debug", "rbq_quantize_query_debug", "rbq_score_ints",
     "rbq_score_varlen", "rbq_topp_select_varlen", "rbq_sparse_decode_varlen", "rbq_dense_decode_varlen",
-    "rbq_decode_step_varlen",
+    "rbq_decode_step_varlen", "rbq_quantize_query_bits",
 ]
 
 
@@ -57,6 +57,7 @@ def _load():
                              vp],
         "rbq_decode_step": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, i32, f32, f32,
                             vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
+        "rbq_quantize_query_bits": [i32, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp],
         "rbq_score_varlen": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp],
         "rbq_topp_select_varlen": [i32, i32, i32, vp, vp, vp, f32, vp, vp, vp, sz, vp],
         "rbq_sparse_decode_varlen": [i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, f32, vp,
@@ -151,6 +152,12 @@ def rbq_quantize_query(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, qplan
         _check("rbq_quantize_query", lib.rbq_quantize_query(*args, _stream(stream)))
     else:
         _check("rbq_quantize_query_debug", lib.rbq_quantize_query_debug(*args, _ptr(qrot_out), _stream(stream)))
+
+
+def rbq_quantize_query_bits(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, bits, qplanes, qscal, stream=None):
+    _check("rbq_quantize_query_bits", lib.rbq_quantize_query_bits(
+        batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_q), _ptr(c_k), bits, _ptr(qplanes), _ptr(qscal),
+        _stream(stream)))
 
 
 def rbq_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores, stream=None):

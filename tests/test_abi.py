@@ -163,3 +163,13 @@ def test_ragged_calls_reject_invalid_arguments_on_the_host(lib):
     assert step(cap=105) == EINVAL
     assert step(sp=None) == EINVAL
     assert step(wsb=64) == EINVAL
+
+
+def test_query_bits_range_is_checked_on_the_host(lib):
+    L = lib.lib
+    qb = lambda bits: L.rbq_quantize_query_bits(1, 8, 4, 128, FAKE, FAKE, None, FAKE, bits, FAKE, FAKE, 0)
+    assert qb(0) == lib.RBQ_EINVAL
+    assert qb(9) == lib.RBQ_EINVAL
+    assert qb(5) == lib.RBQ_EUNSUPPORTED
+    assert qb(8) == lib.RBQ_EUNSUPPORTED
+    assert L.rbq_quantize_query_bits(1, 8, 4, 128, FAKE, FAKE, None, None, 2, FAKE, FAKE, 0) == lib.RBQ_EINVAL

@@ -91,6 +91,36 @@ def test_quantize_query_stagewise(R, pipeline, case):
             assert np.all(np.abs(t[off] - np.floor(t[off]) - 0.5) <= 1e-4)
 
 
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+def test_quantize_query_bits_and_scores(R, pipeline, bits):
+    """rbq_quantize_query_bits: the B_q-bit codes decided in fp32 from the GPU's
+    rotated query (the same rotation as rbq_quantize_query), bit-exact; B_q = 4
+    is rbq_quantize_query bitwise; the scores from those planes match the oracle."""
+    w = gen.random_case(1, 8, 2, 3000, seed=12, kv_dtype="bf16", c_q_scale=0.5)
+    st = pipeline.DecodeState.from_workload(w)
+    st.build_index()
+    qrot = torch.empty(1, 8, 128, device="cuda")
+    st.quantize(qrot_out=qrot)
+    planes4, qs4 = pu.u32(st.qplanes).copy(), _np(st.qscal).copy()
+    qp = torch.zeros_like(st.qplanes)
+    qs = torch.zeros_like(st.qscal)
+    R.rbq_quantize_query_bits(1, 8, 2, 128, st.q, st.P, st.c_q, st.c_k, bits, qp, qs)
+    R.rbq_score(1, 8, 2, 128, st.n, st.cap, st.codes, st.kfac, qp, qs, st.scores)
+    torch.cuda.synchronize()
+    planes, qsb, qr = pu.u32(qp), _np(qs), _np(qrot)
+    if bits == 4:
+        assert np.array_equal(planes, planes4) and np.array_equal(qsb.view(np.uint32), qs4.view(np.uint32))
+    codes, kfac, S = pu.u32(st.codes), _np(st.kfac), _np(st.scores)
+    for h in range(8):
+        z = orc.uniform_quantize(qr[0, h], dtype=np.float32, bits=bits)
+        got = pu.planes_to_codes(planes[0, h])
+        assert np.array_equal(got, z["codes"]) and got.max() == (1 << bits) - 1
+        assert qsb[0, h, 0] == np.float32(z["ql"]) and qsb[0, h, 1] == np.float32(z["delta"])
+        assert qsb[0, h, 2] == z["s_u"]
+        pu.check_scores(S[0, h, :st.n], codes[0, h // 4, :st.n], kfac[0, h // 4, :st.n].astype(np.float64),
+                        planes[0, h], qsb[0, h])
+
+
 # ---------------------------------------------------------------- index construction
 def _check_encode_group(st, w, b, hk, n, rot, alpha, c_k_given=None):
     K = w.K_f32(b, hk, slice(0, n)).astype(np.float64)
