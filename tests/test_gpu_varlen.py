@@ -40,6 +40,12 @@ CASES = [
                      33333],
      [0, 5, 64, 1, 0, 17, 33, 64, 2, 0, 9, 64, 50, 0, 64, 3],
      [0.9, 0.8, 0.95, 1.0, 0.5, 0.99, 0.7, 0.9, 0.9, 0.85, 0.9, 0.92, 0.6, 0.9, 0.9, 0.9], 40000, 15),
+    # windows larger than a split's spare list room: spread over more splits than a short
+    # sequence has indexed chunks (window-only splits), beside a long sequence
+    (8, 2, "bf16", [6000, 100, 0], [1000, 900, 700], [0.9, 0.8, 0.9], 6000, 16),
+    # a window that cannot be folded at all (4096 rows, few splits): separate window splits,
+    # each starting at its own sequence's cache tail
+    (8, 2, "bf16", [500, 0, 300], [4096, 1000, 3], [0.9, 0.9, 0.95], 500, 17),
 ]
 
 
