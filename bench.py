@@ -20,6 +20,7 @@ sweep (p = 0.8 / 0.9 / 0.95 / 0.99: step time, budget, KV-group union), the
 standalone score scan of the wide-head workload, a ragged serving batch (16
 sequences of mixed length, window and p) against its dense decode, the
 attention recall of the selections against exact and fixed-budget Top-k, the
+same step with the K/V cache in host memory (read over PCIe), the
 time-to-first-token cost of the index build beside a prefill attention, and
 the oracle's CPU rate.
 """
@@ -380,6 +381,43 @@ def quality(pipeline, torch, st, p_list, seed=20261):
     return out
 
 
+def offload(pipeline, torch, st, p_list, steps, warmup):
+    """The same 128K step with the K/V cache in pinned host memory and the index
+    in HBM: the kernels read the cache over PCIe (rbq.MappedHost), so the sparse
+    attention moves only the selected and window rows across the bus, while the
+    dense decode moves all of them."""
+    from paper_2606_31519_amd import rbq
+    hostK = torch.empty(st.K.shape, dtype=st.K.dtype, pin_memory=True)
+    hostV = torch.empty(st.V.shape, dtype=st.V.dtype, pin_memory=True)
+    hostK.copy_(st.K)
+    hostV.copy_(st.V)
+    K, V = rbq.MappedHost(hostK), rbq.MappedHost(hostV)
+    off = pipeline.DecodeState(st.B, st.Hq, st.Hkv, st.D, st.cap, st.n, st.w, K, V, st.q, st.P, st.c_q)
+    for name in ("c_k", "codes", "kfac"):
+        getattr(off, name).copy_(getattr(st, name))
+    row = 2 * st.D * hostK.element_size()          # K + V bytes of one row
+    win = st.B * st.Hkv * st.w * row
+    out = {}
+    for p in p_list:
+        g = _graph(torch, lambda p=p: off.step(p))
+        ms = _time_graphs(torch, [g], steps, warmup)
+        del g
+        off.step(p)
+        torch.cuda.synchronize()
+        union, _ = _union_rows(off)
+        out[str(p)] = {"ms_per_step": ms, "bus_bytes": union * row + win,
+                       "bus_GBps": (union * row + win) / (ms * 1e-3) / 1e9}
+    d_out, d_lse = torch.empty_like(off.out), torch.empty_like(off.lse)
+    g = _graph(torch, lambda: off.dense_decode(d_out, d_lse))
+    ms_dense = _time_graphs(torch, [g], max(2, steps // 4), 1)
+    del g
+    dense_bytes = st.B * st.Hkv * (st.n + st.w) * row
+    for v in out.values():
+        v["speedup_vs_dense"] = ms_dense / v["ms_per_step"]
+    return {"workload": "the 128K step with K/V in pinned host memory, index in HBM (reads over PCIe)",
+            "dense_decode_ms": ms_dense, "dense_bus_GBps": dense_bytes / (ms_dense * 1e-3) / 1e9, "p": out}
+
+
 def prefill_overlap(torch, st, steps=3):
     """Time to first token with the index build (Algorithm 1 over the prefill
     keys: centroid + encode) beside a causal prefill attention over the same
@@ -449,6 +487,7 @@ def main():
     ap.add_argument("--ragged-only", action="store_true", help="only the ragged-batch step (for its kernel profile)")
     ap.add_argument("--no-quality", action="store_true", help="skip the attention-recall report")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-overlap (time to first token) report")
+    ap.add_argument("--no-offload", action="store_true", help="skip the step with the K/V cache in host memory")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
@@ -560,6 +599,12 @@ def main():
         st0.step(p)
         torch.cuda.synchronize()
 
+    # the step with the cache in host memory (reads over PCIe)
+    offloaded = None
+    if not args.no_offload:
+        offloaded = offload(pipeline, torch, st0, [0.8, 0.9, 0.95], args.steps, args.warmup)
+        torch.cuda.empty_cache()
+
     # the box's own streaming rate (elementwise copy), a second reference beside the 8 TB/s peak
     copy = _copy_rate(torch, 5)
 
@@ -626,6 +671,7 @@ def main():
         "ragged": ragged,
         "recall": recall,
         "prefill_overlap": prefill,
+        "kv_in_host_memory": offloaded,
         "cpu_baseline": cpu,
         "gen_s": t_gen,
         "git": _git_sha(),

@@ -61,6 +61,10 @@ class DecodeState:
         cq = torch.from_numpy(np.ascontiguousarray(wl.c_q)).to(device) if c_q else None
         return cls(wl.B, wl.Hq, wl.Hkv, wl.D, wl.N, wl.n_index, wl.w, K, V, q, P, cq, device)
 
+    def _window(self, t):
+        """Rows [n, cap) of a cache (the local window), in HBM or mapped host memory."""
+        return t.rows(self.n, self.D) if isinstance(t, rbq.MappedHost) else t[:, :, self.n:]
+
     # ---------------------------------------------------------------- the five calls
     def build_index(self, stream=None, rot_out=None, alpha_out=None):
         """Prefill index construction over rows [0, n), setting c_k (Algorithm 1)."""
@@ -74,7 +78,7 @@ class DecodeState:
         left at n, so repeated steps stay identical."""
         if self.w == 0:
             return
-        K_win = self.K[:, :, self.n:]
+        K_win = self._window(self.K)
         rbq.rbq_encode_keys(self.B, self.Hkv, self.D, K_win, self.cap, self.w, self.n, self.cap, self.P, self.c_q,
                             self.c_k, self.codes, self.kfac, 0, None, None, stream)
 
@@ -91,15 +95,15 @@ class DecodeState:
                             self.ws_topp, stream)
 
     def sparse_decode(self, stream=None):
-        K_loc = self.K[:, :, self.n:] if self.w else None
-        V_loc = self.V[:, :, self.n:] if self.w else None
+        K_loc = self._window(self.K) if self.w else None
+        V_loc = self._window(self.V) if self.w else None
         rbq.rbq_sparse_decode(self.B, self.Hq, self.Hkv, self.D, self.q, self.K, self.V, self.cap, self.n,
                               self.sel_idx, self.sel_count, K_loc, V_loc, self.cap, self.w, self.sm_scale, self.out,
                               self.lse, self.ws_decode, stream)
 
     def dense_decode(self, out=None, lse=None, stream=None):
-        K_loc = self.K[:, :, self.n:] if self.w else None
-        V_loc = self.V[:, :, self.n:] if self.w else None
+        K_loc = self._window(self.K) if self.w else None
+        V_loc = self._window(self.V) if self.w else None
         rbq.rbq_dense_decode(self.B, self.Hq, self.Hkv, self.D, self.q, self.K, self.V, self.cap, self.n, K_loc,
                              V_loc, self.cap, self.w, self.sm_scale, self.out if out is None else out,
                              self.lse if lse is None else lse, self.ws_decode, stream)

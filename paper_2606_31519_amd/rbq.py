@@ -108,6 +108,37 @@ def _check(name, st):
         raise RbqError(name, st)
 
 
+class MappedHost:
+    """A pinned host tensor handed to the kernels by its device address
+    (hipHostGetDevicePointer), so that they read it over PCIe: a K/V cache kept
+    in host memory while the index (codes, factors, centroids) stays in HBM.
+    Only the rows a call touches cross the bus (the selected and window rows for
+    the sparse attention). Usable wherever a call takes K / V (or a K_loc / V_loc
+    from rows()), with the dtype of the wrapped tensor."""
+
+    def __init__(self, t: torch.Tensor, _base=None, _offset=0):
+        if t.device.type != "cpu" or not t.is_pinned() or not t.is_contiguous():
+            raise ValueError("a host K/V buffer must be a contiguous pinned CPU tensor (pin_memory=True)")
+        if _base is None:
+            # the HIP runtime of this process (torch and librbq.so load the same one)
+            hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | ctypes.RTLD_GLOBAL)
+            hip.hipHostGetDevicePointer.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_void_p, ctypes.c_uint]
+            hip.hipHostGetDevicePointer.restype = ctypes.c_int
+            dev = ctypes.c_void_p()
+            st = hip.hipHostGetDevicePointer(ctypes.byref(dev), ctypes.c_void_p(t.data_ptr()), 0)
+            if st != 0 or not dev.value:
+                raise RuntimeError(f"hipHostGetDevicePointer failed ({st}): the buffer is not mapped for the device")
+            _base = dev.value
+        self.tensor, self.dtype, self._base, self._offset = t, t.dtype, _base, _offset
+
+    def data_ptr(self) -> int:
+        return self._base + self._offset
+
+    def rows(self, first_row: int, head_dim: int) -> "MappedHost":
+        """The same buffer from row `first_row` of every block on (K + n*D: a cache tail)."""
+        return MappedHost(self.tensor, self._base, self._offset + first_row * head_dim * self.tensor.element_size())
+
+
 def kv_dtype_code(t: torch.Tensor) -> int:
     if t.dtype == torch.bfloat16:
         return RBQ_BF16
