@@ -286,6 +286,54 @@ rbq_status rbq_decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_
                                   int32_t* sel_count, float* out, float* lse, void* ws, size_t ws_bytes,
                                   hipStream_t stream);
 
+/*
+ * The compact index -- the paper's storage of the per-key scalar in FP16
+ * (Appendix C, storage overhead: D/8 + 2 bytes per key and head, 18 at D = 128,
+ * about 3.5 % of a 16-bit KV cache), in place of kfac's two fp32 factors.
+ *   kfac16 [B][Hkv][cap] uint16: f = ||k - c_k|| / alpha' as IEEE binary16,
+ *          rounded to nearest (ties to even) from the fp32 value, and
+ *          saturated to 65504 (the largest finite value) above it.
+ * The compact index has no room for g = <c_q, k - c_k>, so it is built and
+ * read with the query centroid at zero: these calls take no c_q, and the
+ * query must be quantised with c_q = NULL. The score is then
+ *   S = A * f16_i * X + B0
+ * (rbq_score with g = 0 and f rounded to fp16). Each call behaves as its
+ * full-index form otherwise (same arguments, layouts, checks and errors);
+ * kfac16 must be 16-byte aligned like every other buffer.
+ */
+rbq_status rbq_encode_keys_f16(int32_t batch, int32_t heads_kv, int32_t head_dim,
+                               const void* keys, int32_t keys_dtype, int64_t keys_ld,
+                               int32_t n_new, int32_t offset, int32_t cap, const float* P, float* c_k,
+                               uint32_t* codes, uint16_t* kfac16, uint32_t flags,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
+rbq_status rbq_score_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                         int32_t n, int32_t cap, const uint32_t* codes, const uint16_t* kfac16,
+                         const uint32_t* qplanes, const float* qscal, float* scores, hipStream_t stream);
+/* rbq_decode_step on the compact index: its outputs are bitwise those of
+ * rbq_quantize_query (c_q = NULL), rbq_score_f16, rbq_topp_select,
+ * rbq_sparse_decode and (flush) rbq_encode_keys_f16 of the window rows. */
+rbq_status rbq_decode_step_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                               const float* q, const float* P, const float* c_k,
+                               const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n,
+                               int32_t w, uint32_t* codes, uint16_t* kfac16, int32_t flush, float p,
+                               float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
+                               int32_t* sel_idx, int32_t* sel_count, float* out, float* lse,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
+/* The ragged-batch forms on the compact index (semantics of rbq_score_varlen
+ * and rbq_decode_step_varlen). */
+rbq_status rbq_score_varlen_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                int32_t n, int32_t cap, const int32_t* seq_n, const uint32_t* codes,
+                                const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal,
+                                float* scores, hipStream_t stream);
+rbq_status rbq_decode_step_varlen_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                      const float* q, const float* P, const float* c_k,
+                                      const void* K, const void* V, int32_t kv_dtype, int32_t cap,
+                                      int32_t n, int32_t w, const int32_t* seq_n, const int32_t* seq_w,
+                                      uint32_t* codes, uint16_t* kfac16, int32_t flush, const float* seq_p,
+                                      float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
+                                      int32_t* sel_idx, int32_t* sel_count, float* out, float* lse,
+                                      void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Workspace bytes needed by `op` (one of RBQ_OP_*) for these sizes; 0 for an
  * unknown op or invalid sizes. Host-only, never touches the device. */
 size_t rbq_workspace_bytes(int32_t op, int32_t batch, int32_t heads_q, int32_t heads_kv,

@@ -26,6 +26,8 @@ Conventions (readings of the paper where it is silent or inconsistent):
     step (Appendix A.3.2); deterministic rounding floor(t + 1/2).
   * degenerate vectors: ||x|| = 0 gives f = 0; ||q - c_q|| = 0 gives u = 0,
     Delta = 0 and all codes 0.
+  * compact index: f stored as IEEE binary16, saturated at 65504, rounded
+    to nearest with ties to even; no g, hence c_q = 0 (Appendix C).
   * Top-p: the smallest prefix of keys sorted by estimated score whose
     softmax(S / sqrt(D)) mass reaches p, extended to every key tied with the
     last one; p >= 1 keeps every key.
@@ -112,6 +114,18 @@ def encode_keys(K: np.ndarray, P: np.ndarray, c_k: np.ndarray | None = None,
     g = X @ c_q                                       # <c_q, k> - <c_q, c_k>
     return dict(c_k=c_k, X=X, norm=norm, R=R, bits=bits, codes=pack_bits(bits) if D % 32 == 0 else None,
                 alpha_p=alpha_p, alpha=alpha_p / np.sqrt(D), f=f, g=g)
+
+
+def compact_factor(f) -> np.ndarray:
+    """The per-key factor f as the compact index keeps it: the paper stores the
+    one scalar per key and head in FP16 (Appendix C, the correction factor's
+    storage; B_alpha = 2 bytes). Saturated at 65504, the largest finite IEEE
+    binary16 value (a reading: the paper does not treat values beyond the
+    range), then rounded to the nearest binary16 value with ties to even
+    (NumPy's float64 -> float16 conversion); returned as float64. The compact
+    index keeps no g, so it goes with c_q = 0."""
+    f = np.minimum(np.asarray(f, np.float64), 65504.0)
+    return f.astype(np.float16).astype(np.float64)
 
 
 # ---------------------------------------------------------------------------

@@ -5,6 +5,58 @@
 
 using namespace rbq;
 
+namespace {
+// rbq_decode_step over either index form: kfac (f, g in fp32) or, when
+// kfac16 is non-NULL, the compact index's fp16 factors (kfac unused)
+rbq_status decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                       const float* P, const float* c_q, const float* c_k, const void* K, const void* V,
+                       int32_t kv_dtype, int32_t cap, int32_t n, int32_t w, uint32_t* codes, float* kfac,
+                       uint16_t* kfac16, int32_t flush, float p, float sm_scale, uint32_t* qplanes, float* qscal,
+                       float* scores, int32_t* sel_idx, int32_t* sel_count, float* out, float* lse, void* ws,
+                       size_t ws_bytes, hipStream_t stream) {
+  const void* fac = kfac16 != nullptr ? static_cast<const void*>(kfac16) : kfac;
+  rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
+  if (s != RBQ_OK) return s;
+  if (n < 0 || w < 0 || cap < 0 || int64_t(n) + w > cap) return RBQ_EINVAL;
+  const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
+  if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
+  const size_t elem = kv_dtype == RBQ_BF16 ? 2 : 4;
+  const void* K_loc = K ? static_cast<const char*>(K) + size_t(n) * head_dim * elem : nullptr;
+  const void* V_loc = V ? static_cast<const char*>(V) + size_t(n) * head_dim * elem : nullptr;
+  const size_t dec_bytes = decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w);
+  const bool do_flush = flush != 0 && w > 0;
+  if ((s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal)) != RBQ_OK) return s;
+  if ((s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, fac, qplanes, qscal, scores)) != RBQ_OK)
+    return s;
+  if ((s = check_topp(batch, heads_q, n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, sw.topp_bytes)) != RBQ_OK)
+    return s;
+  if ((s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, true, sel_idx, sel_count,
+                        K_loc, V_loc, cap, w, sm_scale, out, sw.decode, dec_bytes)) != RBQ_OK)
+    return s;
+  if (do_flush && (s = check_encode(batch, heads_kv, head_dim, K_loc, kv_dtype, cap, w, n, cap, P, c_k, codes, fac,
+                                    0u, nullptr, 0)) != RBQ_OK)
+    return s;
+
+  const int64_t rows = int64_t(batch) * heads_q;
+  if (do_flush)
+    s = launch_quantize_flush(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, K_loc, kv_dtype, cap, w, n,
+                              cap, codes, kfac, stream, nullptr, nullptr, 0, kfac16);
+  else
+    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
+  if (s != RBQ_OK) return s;
+  const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
+  s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
+                   sw.slot_max, tw.hist, rows * kHistPerRow, nullptr, kfac16);
+  if (s != RBQ_OK) return s;
+  s = launch_topp(int32_t(rows), n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
+                  score_blocks_per_row(batch, heads_kv, n), sw.masks);
+  if (s != RBQ_OK) return s;
+  return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, cap, w,
+                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n));
+}
+
+}  // namespace
+
 extern "C" {
 
 rbq_status rbq_encode_keys_debug(int32_t batch, int32_t heads_kv, int32_t head_dim, const void* keys,
@@ -61,6 +113,26 @@ rbq_status rbq_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t h
                       stream);
 }
 
+rbq_status rbq_encode_keys_f16(int32_t batch, int32_t heads_kv, int32_t head_dim, const void* keys,
+                               int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset, int32_t cap,
+                               const float* P, float* c_k, uint32_t* codes, uint16_t* kfac16, uint32_t flags,
+                               void* ws, size_t ws_bytes, hipStream_t stream) {
+  const rbq_status s = check_encode(batch, heads_kv, head_dim, keys, keys_dtype, keys_ld, n_new, offset, cap, P, c_k,
+                                    codes, kfac16, flags, ws, ws_bytes);
+  if (s != RBQ_OK) return s;
+  return launch_encode(batch, heads_kv, keys, keys_dtype, keys_ld, n_new, offset, cap, P, nullptr, c_k, codes,
+                       nullptr, flags, nullptr, ws, nullptr, stream, kfac16);
+}
+
+rbq_status rbq_score_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
+                         const uint32_t* codes, const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal,
+                         float* scores, hipStream_t stream) {
+  const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac16, qplanes, qscal, scores);
+  if (s != RBQ_OK) return s;
+  return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, qscal, scores, nullptr, nullptr,
+                      stream, nullptr, nullptr, 0, nullptr, kfac16);
+}
+
 rbq_status rbq_score_ints(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
                           const uint32_t* codes, const uint32_t* qplanes, int32_t* ip_out, int32_t* pc_out,
                           hipStream_t stream) {
@@ -107,44 +179,20 @@ rbq_status rbq_decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int
                            int32_t flush, float p, float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
                            int32_t* sel_idx, int32_t* sel_count, float* out, float* lse, void* ws, size_t ws_bytes,
                            hipStream_t stream) {
-  rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
-  if (s != RBQ_OK) return s;
-  if (n < 0 || w < 0 || cap < 0 || int64_t(n) + w > cap) return RBQ_EINVAL;
-  const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
-  if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
-  const size_t elem = kv_dtype == RBQ_BF16 ? 2 : 4;
-  const void* K_loc = K ? static_cast<const char*>(K) + size_t(n) * head_dim * elem : nullptr;
-  const void* V_loc = V ? static_cast<const char*>(V) + size_t(n) * head_dim * elem : nullptr;
-  const size_t dec_bytes = decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w);
-  const bool do_flush = flush != 0 && w > 0;
-  if ((s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal)) != RBQ_OK) return s;
-  if ((s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores)) != RBQ_OK)
-    return s;
-  if ((s = check_topp(batch, heads_q, n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, sw.topp_bytes)) != RBQ_OK)
-    return s;
-  if ((s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, true, sel_idx, sel_count,
-                        K_loc, V_loc, cap, w, sm_scale, out, sw.decode, dec_bytes)) != RBQ_OK)
-    return s;
-  if (do_flush && (s = check_encode(batch, heads_kv, head_dim, K_loc, kv_dtype, cap, w, n, cap, P, c_k, codes, kfac,
-                                    0u, nullptr, 0)) != RBQ_OK)
-    return s;
+  return decode_step(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, kv_dtype, cap, n, w, codes, kfac,
+                     nullptr, flush, p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws, ws_bytes,
+                     stream);
+}
 
-  const int64_t rows = int64_t(batch) * heads_q;
-  if (do_flush)
-    s = launch_quantize_flush(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, K_loc, kv_dtype, cap, w, n,
-                              cap, codes, kfac, stream);
-  else
-    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
-  if (s != RBQ_OK) return s;
-  const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
-  s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   sw.slot_max, tw.hist, rows * kHistPerRow);
-  if (s != RBQ_OK) return s;
-  s = launch_topp(int32_t(rows), n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
-                  score_blocks_per_row(batch, heads_kv, n), sw.masks);
-  if (s != RBQ_OK) return s;
-  return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, cap, w,
-                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n));
+rbq_status rbq_decode_step_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                               const float* P, const float* c_k, const void* K, const void* V, int32_t kv_dtype,
+                               int32_t cap, int32_t n, int32_t w, uint32_t* codes, uint16_t* kfac16, int32_t flush,
+                               float p, float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
+                               int32_t* sel_idx, int32_t* sel_count, float* out, float* lse, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  return decode_step(batch, heads_q, heads_kv, head_dim, q, P, nullptr, c_k, K, V, kv_dtype, cap, n, w, codes,
+                     nullptr, kfac16, flush, p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws,
+                     ws_bytes, stream);
 }
 
 }  // extern "C"
@@ -174,6 +222,55 @@ rbq_status decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32
                        sm_scale, out, lse, ws, sparse, stream, nullptr, 0, seq_n, seq_w);
 }
 
+
+// rbq_decode_step_varlen over either index form (kfac16 non-NULL: the compact index)
+rbq_status decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
+                              const float* P, const float* c_q, const float* c_k, const void* K, const void* V,
+                              int32_t kv_dtype, int32_t cap, int32_t n, int32_t w, const int32_t* seq_n,
+                              const int32_t* seq_w, uint32_t* codes, float* kfac, uint16_t* kfac16, int32_t flush,
+                              const float* seq_p, float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
+                              int32_t* sel_idx, int32_t* sel_count, float* out, float* lse, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
+  const void* fac = kfac16 != nullptr ? static_cast<const void*>(kfac16) : kfac;
+  rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
+  if (s != RBQ_OK) return s;
+  if ((s = check_ragged(n, w, cap, seq_n, seq_w)) != RBQ_OK) return s;
+  if (seq_p == nullptr || (reinterpret_cast<uintptr_t>(seq_p) & 15u) != 0) return RBQ_EINVAL;
+  const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
+  if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
+  const size_t dec_bytes = decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w);
+  const bool do_flush = flush != 0 && w > 0;
+  if ((s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal)) != RBQ_OK) return s;
+  if ((s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, fac, qplanes, qscal, scores)) != RBQ_OK)
+    return s;
+  if ((s = check_topp(batch, heads_q, n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, sw.topp_bytes)) !=
+      RBQ_OK)
+    return s;
+  if ((s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, true, sel_idx, sel_count, K, V,
+                        cap, w, sm_scale, out, sw.decode, dec_bytes)) != RBQ_OK)
+    return s;
+  if (do_flush && (s = check_encode(batch, heads_kv, head_dim, K, kv_dtype, cap, w, n, cap, P, c_k, codes, fac, 0u,
+                                    nullptr, 0)) != RBQ_OK)
+    return s;
+
+  const int64_t rows = int64_t(batch) * heads_q;
+  if (do_flush)   // window rows [seq_n[b], + seq_w[b]) of K into the same index rows
+    s = launch_quantize_flush(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, K, kv_dtype, cap, w, 0, cap,
+                              codes, kfac, stream, seq_n, seq_w, n, kfac16);
+  else
+    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
+  if (s != RBQ_OK) return s;
+  const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
+  s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
+                   sw.slot_max, tw.hist, rows * kHistPerRow, seq_n, kfac16);
+  if (s != RBQ_OK) return s;
+  s = launch_topp(int32_t(rows), n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
+                  score_blocks_per_row(batch, heads_kv, n), sw.masks, seq_n, seq_p, heads_q);
+  if (s != RBQ_OK) return s;
+  return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K, V, cap, w,
+                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), seq_n, seq_w);
+}
+
 }  // namespace
 
 extern "C" {
@@ -186,6 +283,16 @@ rbq_status rbq_score_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, in
   if ((s = check_ragged(n, 0, cap, seq_n, nullptr)) != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr,
                       stream, nullptr, nullptr, 0, seq_n);
+}
+
+rbq_status rbq_score_varlen_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
+                                int32_t cap, const int32_t* seq_n, const uint32_t* codes, const uint16_t* kfac16,
+                                const uint32_t* qplanes, const float* qscal, float* scores, hipStream_t stream) {
+  rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac16, qplanes, qscal, scores);
+  if (s != RBQ_OK) return s;
+  if ((s = check_ragged(n, 0, cap, seq_n, nullptr)) != RBQ_OK) return s;
+  return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, qscal, scores, nullptr, nullptr,
+                      stream, nullptr, nullptr, 0, seq_n, kfac16);
 }
 
 rbq_status rbq_topp_select_varlen(int32_t batch, int32_t heads_q, int32_t n, const int32_t* seq_n,
@@ -224,43 +331,21 @@ rbq_status rbq_decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_
                                   const float* seq_p, float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
                                   int32_t* sel_idx, int32_t* sel_count, float* out, float* lse, void* ws,
                                   size_t ws_bytes, hipStream_t stream) {
-  rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
-  if (s != RBQ_OK) return s;
-  if ((s = check_ragged(n, w, cap, seq_n, seq_w)) != RBQ_OK) return s;
-  if (seq_p == nullptr || (reinterpret_cast<uintptr_t>(seq_p) & 15u) != 0) return RBQ_EINVAL;
-  const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
-  if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
-  const size_t dec_bytes = decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w);
-  const bool do_flush = flush != 0 && w > 0;
-  if ((s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal)) != RBQ_OK) return s;
-  if ((s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores)) != RBQ_OK)
-    return s;
-  if ((s = check_topp(batch, heads_q, n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, sw.topp_bytes)) !=
-      RBQ_OK)
-    return s;
-  if ((s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, true, sel_idx, sel_count, K, V,
-                        cap, w, sm_scale, out, sw.decode, dec_bytes)) != RBQ_OK)
-    return s;
-  if (do_flush && (s = check_encode(batch, heads_kv, head_dim, K, kv_dtype, cap, w, n, cap, P, c_k, codes, kfac, 0u,
-                                    nullptr, 0)) != RBQ_OK)
-    return s;
+  return decode_step_varlen(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, kv_dtype, cap, n, w, seq_n, seq_w,
+                            codes, kfac, nullptr, flush, seq_p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count,
+                            out, lse, ws, ws_bytes, stream);
+}
 
-  const int64_t rows = int64_t(batch) * heads_q;
-  if (do_flush)   // window rows [seq_n[b], + seq_w[b]) of K into the same index rows
-    s = launch_quantize_flush(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, K, kv_dtype, cap, w, 0, cap,
-                              codes, kfac, stream, seq_n, seq_w, n);
-  else
-    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
-  if (s != RBQ_OK) return s;
-  const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
-  s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   sw.slot_max, tw.hist, rows * kHistPerRow, seq_n);
-  if (s != RBQ_OK) return s;
-  s = launch_topp(int32_t(rows), n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
-                  score_blocks_per_row(batch, heads_kv, n), sw.masks, seq_n, seq_p, heads_q);
-  if (s != RBQ_OK) return s;
-  return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K, V, cap, w,
-                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), seq_n, seq_w);
+rbq_status rbq_decode_step_varlen_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                      const float* q, const float* P, const float* c_k, const void* K, const void* V,
+                                      int32_t kv_dtype, int32_t cap, int32_t n, int32_t w, const int32_t* seq_n,
+                                      const int32_t* seq_w, uint32_t* codes, uint16_t* kfac16, int32_t flush,
+                                      const float* seq_p, float sm_scale, uint32_t* qplanes, float* qscal,
+                                      float* scores, int32_t* sel_idx, int32_t* sel_count, float* out, float* lse,
+                                      void* ws, size_t ws_bytes, hipStream_t stream) {
+  return decode_step_varlen(batch, heads_q, heads_kv, head_dim, q, P, nullptr, c_k, K, V, kv_dtype, cap, n, w, seq_n,
+                            seq_w, codes, nullptr, kfac16, flush, seq_p, sm_scale, qplanes, qscal, scores, sel_idx,
+                            sel_count, out, lse, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -79,7 +79,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(EncodeArgs ea) {
 template <int DT>
 rbq_status launch_dt(int32_t batch, int32_t heads_kv, const void* keys, int64_t keys_ld, int32_t n_new,
                      int32_t offset, int32_t cap, const float* P, const float* c_q, float* c_k, uint32_t* codes,
-                     float* kfac, uint32_t flags, float* alpha_out, void* ws, float* rot_out, hipStream_t stream) {
+                     float* kfac, uint32_t flags, float* alpha_out, void* ws, float* rot_out, hipStream_t stream,
+                     uint16_t* kfac16) {
   const int bhs = batch * heads_kv;
   if (flags & RBQ_ENCODE_SET_CENTROID) {
     const int chunks = (n_new + kCentroidChunk - 1) / kCentroidChunk;
@@ -88,7 +89,8 @@ rbq_status launch_dt(int32_t batch, int32_t heads_kv, const void* keys, int64_t 
     centroid_final_kernel<<<bhs, kHeadDim, 0, stream>>>(partial, chunks, n_new, c_k);
   }
   const dim3 grid(encode_blocks_per_head(n_new, bhs), bhs);
-  const EncodeArgs ea{keys, keys_ld, n_new, offset, cap, P, c_q, c_k, codes, kfac, alpha_out, rot_out};
+  EncodeArgs ea{keys, keys_ld, n_new, offset, cap, P, c_q, c_k, codes, kfac, alpha_out, rot_out};
+  ea.kfac16 = kfac16;
   if (rot_out)
     encode_kernel<DT, true><<<grid, kEncThreads, 0, stream>>>(ea);
   else
@@ -101,13 +103,13 @@ rbq_status launch_dt(int32_t batch, int32_t heads_kv, const void* keys, int64_t 
 rbq_status launch_encode(int32_t batch, int32_t heads_kv, const void* keys, int32_t keys_dtype, int64_t keys_ld,
                          int32_t n_new, int32_t offset, int32_t cap, const float* P, const float* c_q, float* c_k,
                          uint32_t* codes, float* kfac, uint32_t flags, float* alpha_out, void* ws,
-                         float* rot_out, hipStream_t stream) {
+                         float* rot_out, hipStream_t stream, uint16_t* kfac16) {
   if (n_new == 0) return RBQ_OK;
   if (keys_dtype == RBQ_BF16)
     return launch_dt<RBQ_BF16>(batch, heads_kv, keys, keys_ld, n_new, offset, cap, P, c_q, c_k, codes, kfac, flags,
-                               alpha_out, ws, rot_out, stream);
+                               alpha_out, ws, rot_out, stream, kfac16);
   return launch_dt<RBQ_F32>(batch, heads_kv, keys, keys_ld, n_new, offset, cap, P, c_q, c_k, codes, kfac, flags,
-                            alpha_out, ws, rot_out, stream);
+                            alpha_out, ws, rot_out, stream, kfac16);
 }
 
 }  // namespace rbq

@@ -38,7 +38,17 @@ struct EncodeArgs {
   const int32_t* seq_off;
   const int32_t* seq_cnt;
   int off_max, hkv;
+  // The compact index (the paper's storage: one fp16 factor per key): when
+  // non-NULL, f is written here as fp16 ([cap] per (b, kv-head), values above
+  // the largest finite fp16 saturate to 65504) instead of (f, g) into kfac.
+  uint16_t* kfac16;
 };
+
+// f as stored by the compact index: rounded to nearest fp16 (ties to even),
+// saturated to the largest finite value
+__device__ __forceinline__ uint16_t compact_factor(float f) {
+  return __builtin_bit_cast(uint16_t, static_cast<_Float16>(fminf(f, 65504.f)));
+}
 
 // Blocks per (b, kv-head) of an encode over n_new keys: enough to cover the
 // CUs a few times; each block loops over its tiles.
@@ -233,7 +243,10 @@ __device__ __forceinline__ void encode_tiles(const EncodeArgs& ea, int bh, int b
       if (key < n_new) {
         const int64_t o = int64_t(bh) * cap + offset + key;
         *reinterpret_cast<u32x4*>(codes + o * kWords) = u32x4{code_s[t][0], code_s[t][1], code_s[t][2], code_s[t][3]};
-        *reinterpret_cast<f32x2*>(kfac + o * 2) = f32x2{f, ng_s[1][t]};
+        if (ea.kfac16 != nullptr)
+          ea.kfac16[o] = compact_factor(f);
+        else
+          *reinterpret_cast<f32x2*>(kfac + o * 2) = f32x2{f, ng_s[1][t]};
         if (alpha_out) alpha_out[int64_t(bh) * n_new + key] = alpha_p * 0.08838834764831845f;   // 1/sqrt(128)
       }
     }

@@ -210,12 +210,12 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
                                  const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal,
                                  const void* keys, int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset,
                                  int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream, const int32_t* seq_off,
-                                 const int32_t* seq_cnt, int32_t off_max) {
+                                 const int32_t* seq_cnt, int32_t off_max, uint16_t* kfac16) {
   if (n_new == 0)
     return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
   const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, nullptr, heads_q, heads_kv, 15};
   const EncodeArgs ea{keys,  keys_ld, n_new,   offset,  cap,     P,       c_q,     c_k,     codes,
-                      kfac,  nullptr, nullptr, seq_off, seq_cnt, off_max, heads_kv};
+                      kfac,  nullptr, nullptr, seq_off, seq_cnt, off_max, heads_kv, kfac16};
   const int rows = batch * heads_q, bhs = batch * heads_kv;
   const int per_head = encode_blocks_per_head(n_new, bhs);
   const int blocks = rows + per_head * bhs;

@@ -17,7 +17,7 @@ constexpr int kWords = kHeadDim / 32;
 rbq_status check_heads(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim);
 rbq_status check_encode(int32_t batch, int32_t heads_kv, int32_t head_dim, const void* keys, int32_t keys_dtype,
                         int64_t keys_ld, int32_t n_new, int32_t offset, int32_t cap, const float* P,
-                        const float* c_k, const uint32_t* codes, const float* kfac, uint32_t flags,
+                        const float* c_k, const uint32_t* codes, const void* kfac, uint32_t flags,
                         const void* ws, size_t ws_bytes);
 rbq_status check_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
                           const float* P, const float* c_k, const uint32_t* qplanes, const float* qscal);
@@ -109,7 +109,8 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 rbq_status launch_encode(int32_t batch, int32_t heads_kv, const void* keys, int32_t keys_dtype, int64_t keys_ld,
                          int32_t n_new, int32_t offset, int32_t cap, const float* P, const float* c_q, float* c_k,
                          uint32_t* codes, float* kfac, uint32_t flags, float* alpha_out, void* ws,
-                         float* rot_out, hipStream_t stream);
+                         float* rot_out, hipStream_t stream, uint16_t* kfac16 = nullptr);
+// (kfac16: the compact index's fp16 factors, written instead of kfac when non-NULL)
 // bits: B_q, the query's quantisation bits (1..4)
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
@@ -124,7 +125,7 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
                                  const void* keys, int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset,
                                  int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream,
                                  const int32_t* seq_off = nullptr, const int32_t* seq_cnt = nullptr,
-                                 int32_t off_max = 0);
+                                 int32_t off_max = 0, uint16_t* kfac16 = nullptr);
 // slot_max (fused decode step): [B * Hq][score_blocks_per_row()] block maxima of the
 // scores, with hist[0, hist_words) zeroed by the same launch; NULL otherwise.
 // seq_n (ragged batches): [B] indexed keys per sequence, clamped to [0, n]; n is the row stride
@@ -132,7 +133,8 @@ rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream,
                         float* slot_max = nullptr, unsigned long long* hist = nullptr, int64_t hist_words = 0,
-                        const int32_t* seq_n = nullptr);
+                        const int32_t* seq_n = nullptr, const uint16_t* kfac16 = nullptr);
+// (kfac16: the compact index's fp16 factors [B][Hkv][cap], read instead of kfac when non-NULL; g = 0)
 // slot_max / nslots: per-row partial maxima written by launch_score together with
 // the zeroing of the workspace's counters (the max pass is skipped); masks:
 // optional [rows][topp_mask_words(n)] selection bitmaps (bit i of word k = key 64 k + i);

@@ -92,12 +92,13 @@ struct ScoreSlots {
   int64_t hist_words;
 };
 
-template <int KPT, bool INTS, bool SLOTS, bool RAGGED>
+// FAC16: the compact index, one fp16 factor f per key (g = 0) instead of (f, g) in fp32.
+template <int KPT, bool INTS, bool SLOTS, bool RAGGED, bool FAC16>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(
-    const u32x4* __restrict__ codes, const f32x2* __restrict__ kfac, const uint32_t* __restrict__ qplanes,
-    const float* __restrict__ qscal, float* __restrict__ scores, int32_t* __restrict__ ip_out,
-    int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
-    const int32_t* __restrict__ seq_n) {
+    const u32x4* __restrict__ codes, const f32x2* __restrict__ kfac, const uint16_t* __restrict__ kfac16,
+    const uint32_t* __restrict__ qplanes, const float* __restrict__ qscal, float* __restrict__ scores,
+    int32_t* __restrict__ ip_out, int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G,
+    ScoreSlots sl, const int32_t* __restrict__ seq_n) {
   __shared__ uint32_t qn_s[kMaxGroup][16];
   __shared__ float mx_s[SLOTS ? kMaxGroup : 1][kHalfWaves];
   const int bh = blockIdx.y;                 // b * Hkv + kv head
@@ -123,12 +124,19 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   }
   u32x4 c[KPT];
   f32x2 fg[KPT];
+  uint16_t fh[KPT];
 #pragma unroll
   for (int u = 0; u < KPT; ++u) {
     const int i = min(i0 + u * kScoreThreads, nb - 1);    // keys past nb are computed but never stored
     c[u] = __builtin_nontemporal_load(codes + kbase + i);
-    if (!INTS) fg[u] = __builtin_nontemporal_load(kfac + kbase + i);
+    if (!INTS && FAC16) fh[u] = __builtin_nontemporal_load(kfac16 + kbase + i);
+    if (!INTS && !FAC16) fg[u] = __builtin_nontemporal_load(kfac + kbase + i);
   }
+  // A f X + B0 + g for key slot u
+  auto assemble = [&](int u, float y, float B0) {
+    if (FAC16) return fmaf(float(__builtin_bit_cast(_Float16, fh[u])), y, B0);
+    return fmaf(fg[u].x, y, B0 + fg[u].y);
+  };
   clear_counters();
   const bool full = (blockIdx.x + 1) * (kScoreThreads * KPT) <= nb;   // block-uniform: no key past nb
   if (threadIdx.x < 4 * G) {                  // one lane per (head, word)
@@ -171,7 +179,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       for (int u = 0; u < KPT; ++u) {
         const int ip = int(binary_int4_dot(e[u], qn));
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
-        const float sc = fmaf(fg[u].x, y, B0 + fg[u].y);
+        const float sc = assemble(u, y, B0);
         if (SLOTS) mx = fmaxf(mx, sc);
         __builtin_nontemporal_store(sc, out + i0 + u * kScoreThreads);
       }
@@ -203,7 +211,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       } else {
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
-        const float sc = fmaf(fg[u].x, y, B0 + fg[u].y);
+        const float sc = assemble(u, y, B0);
         if (i < nb) {
           if (SLOTS) mx = fmaxf(mx, sc);
           __builtin_nontemporal_store(sc, out + i);
@@ -218,24 +226,24 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
 }
 
-template <bool INTS, bool SLOTS, bool RAGGED>
+template <bool INTS, bool SLOTS, bool RAGGED, bool FAC16 = false>
 rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
-                      const uint32_t* qplanes, const float* qscal, float* scores, int32_t* ip_out,
-                      int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
+                      const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal, float* scores,
+                      int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
                       const int32_t* seq_n) {
   const u32x4* c4 = reinterpret_cast<const u32x4*>(codes);
   const f32x2* f2 = reinterpret_cast<const f32x2*>(kfac);
   switch (kpt) {
     case 4:
-      score_kernel<4, INTS, SLOTS, RAGGED><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
+      score_kernel<4, INTS, SLOTS, RAGGED, FAC16><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
                                                                        n, cap, Hq, Hkv, G, sl, seq_n);
       break;
     case 2:
-      score_kernel<2, INTS, SLOTS, RAGGED><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
+      score_kernel<2, INTS, SLOTS, RAGGED, FAC16><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
                                                                        n, cap, Hq, Hkv, G, sl, seq_n);
       break;
     default:
-      score_kernel<1, INTS, SLOTS, RAGGED><<<grid, kScoreThreads, 0, stream>>>(c4, f2, qplanes, qscal, scores, ip_out, pc_out,
+      score_kernel<1, INTS, SLOTS, RAGGED, FAC16><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
                                                                        n, cap, Hq, Hkv, G, sl, seq_n);
       break;
   }
@@ -247,19 +255,21 @@ rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* co
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, float* slot_max,
-                        unsigned long long* hist, int64_t hist_words, const int32_t* seq_n) {
+                        unsigned long long* hist, int64_t hist_words, const int32_t* seq_n,
+                        const uint16_t* kfac16) {
   if (n == 0) return RBQ_OK;
   const int G = heads_q / heads_kv;
   const int kpt = score_keys_per_lane(batch, heads_kv, n);
   dim3 grid(score_blocks_per_row(batch, heads_kv, n), batch * heads_kv);
   const ScoreSlots sl{slot_max, hist, hist_words};
-#define RBQ_SCORE_LAUNCH(I, S, R)                                                                            \
-  launch_kpt<I, S, R>(kpt, grid, stream, codes, kfac, qplanes, qscal, scores, ip_out, pc_out, n, cap, heads_q, \
-                      heads_kv, G, sl, seq_n)
-  if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false);   // (the integer hook is never ragged)
-  if (seq_n != nullptr)
-    return slot_max != nullptr ? RBQ_SCORE_LAUNCH(false, true, true) : RBQ_SCORE_LAUNCH(false, false, true);
-  return slot_max != nullptr ? RBQ_SCORE_LAUNCH(false, true, false) : RBQ_SCORE_LAUNCH(false, false, false);
+#define RBQ_SCORE_LAUNCH(I, S, R, F)                                                                    \
+  launch_kpt<I, S, R, F>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, cap, \
+                         heads_q, heads_kv, G, sl, seq_n)
+#define RBQ_SCORE_FAC(S, R) (kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, S, R, true) : RBQ_SCORE_LAUNCH(false, S, R, false))
+  if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, false);   // (the integer hook is never ragged)
+  if (seq_n != nullptr) return slot_max != nullptr ? RBQ_SCORE_FAC(true, true) : RBQ_SCORE_FAC(false, true);
+  return slot_max != nullptr ? RBQ_SCORE_FAC(true, false) : RBQ_SCORE_FAC(false, false);
+#undef RBQ_SCORE_FAC
 #undef RBQ_SCORE_LAUNCH
 }
 

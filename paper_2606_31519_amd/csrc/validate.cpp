@@ -32,7 +32,7 @@ size_t encode_workspace_bytes(int32_t batch, int32_t heads_kv, int32_t head_dim,
 
 rbq_status check_encode(int32_t batch, int32_t heads_kv, int32_t head_dim, const void* keys, int32_t keys_dtype,
                         int64_t keys_ld, int32_t n_new, int32_t offset, int32_t cap, const float* P,
-                        const float* c_k, const uint32_t* codes, const float* kfac, uint32_t flags,
+                        const float* c_k, const uint32_t* codes, const void* kfac, uint32_t flags,
                         const void* ws, size_t ws_bytes) {
   rbq_status s = check_heads(batch, heads_kv, heads_kv, head_dim);
   if (s != RBQ_OK) return s;

@@ -27,7 +27,12 @@ def to_device_kv(arr: np.ndarray, kv_dtype: str, device) -> torch.Tensor:
 class DecodeState:
     """Index + cache + per-step buffers for B sequences x Hkv KV heads."""
 
-    def __init__(self, B, Hq, Hkv, D, cap, n, w, K, V, q, P, c_q=None, device="cuda"):
+    def __init__(self, B, Hq, Hkv, D, cap, n, w, K, V, q, P, c_q=None, device="cuda", compact=False):
+        """compact: the compact index (one fp16 factor per key in kfac16, no
+        query centroid) and the *_f16 calls instead of the fp32 (f, g) index."""
+        if compact and c_q is not None:
+            raise ValueError("the compact index is built and read without a query centroid")
+        self.compact = compact
         self.B, self.Hq, self.Hkv, self.D = B, Hq, Hkv, D
         self.cap, self.n, self.w = cap, n, w
         self.device = device
@@ -38,7 +43,8 @@ class DecodeState:
         f32 = dict(dtype=torch.float32, device=device)
         self.c_k = torch.zeros(B, Hkv, D, **f32)
         self.codes = torch.zeros(B, Hkv, cap, D // 32, dtype=torch.int32, device=device)
-        self.kfac = torch.zeros(B, Hkv, cap, 2, **f32)
+        self.kfac = None if compact else torch.zeros(B, Hkv, cap, 2, **f32)
+        self.kfac16 = torch.zeros(B, Hkv, cap, dtype=torch.float16, device=device) if compact else None
         self.qplanes = torch.zeros(B, Hq, 4, D // 32, dtype=torch.int32, device=device)
         self.qscal = torch.zeros(B, Hq, rbq.QSCAL_STRIDE, **f32)
         self.scores = torch.zeros(B, Hq, max(n, 1), **f32)
@@ -53,13 +59,13 @@ class DecodeState:
         self.sm_scale = 1.0 / math.sqrt(D)
 
     @classmethod
-    def from_workload(cls, wl, device="cuda", c_q: bool = True):
+    def from_workload(cls, wl, device="cuda", c_q: bool = True, compact: bool = False):
         K = to_device_kv(wl.K, wl.kv_dtype, device)
         V = to_device_kv(wl.V, wl.kv_dtype, device)
         q = torch.from_numpy(np.ascontiguousarray(wl.q)).to(device)
         P = torch.from_numpy(np.ascontiguousarray(wl.P)).to(device)
-        cq = torch.from_numpy(np.ascontiguousarray(wl.c_q)).to(device) if c_q else None
-        return cls(wl.B, wl.Hq, wl.Hkv, wl.D, wl.N, wl.n_index, wl.w, K, V, q, P, cq, device)
+        cq = torch.from_numpy(np.ascontiguousarray(wl.c_q)).to(device) if c_q and not compact else None
+        return cls(wl.B, wl.Hq, wl.Hkv, wl.D, wl.N, wl.n_index, wl.w, K, V, q, P, cq, device, compact)
 
     def _window(self, t):
         """Rows [n, cap) of a cache (the local window), in HBM or mapped host memory."""
@@ -68,6 +74,11 @@ class DecodeState:
     # ---------------------------------------------------------------- the five calls
     def build_index(self, stream=None, rot_out=None, alpha_out=None):
         """Prefill index construction over rows [0, n), setting c_k (Algorithm 1)."""
+        if self.compact:
+            rbq.rbq_encode_keys_f16(self.B, self.Hkv, self.D, self.K, self.cap, self.n, 0, self.cap, self.P,
+                                    self.c_k, self.codes, self.kfac16, rbq.RBQ_ENCODE_SET_CENTROID, self.ws_encode,
+                                    stream)
+            return
         rbq.rbq_encode_keys(self.B, self.Hkv, self.D, self.K, self.cap, self.n, 0, self.cap, self.P, self.c_q,
                             self.c_k, self.codes, self.kfac, rbq.RBQ_ENCODE_SET_CENTROID, alpha_out,
                             self.ws_encode, stream, rot_out=rot_out)
@@ -79,6 +90,10 @@ class DecodeState:
         if self.w == 0:
             return
         K_win = self._window(self.K)
+        if self.compact:
+            rbq.rbq_encode_keys_f16(self.B, self.Hkv, self.D, K_win, self.cap, self.w, self.n, self.cap, self.P,
+                                    self.c_k, self.codes, self.kfac16, 0, None, stream)
+            return
         rbq.rbq_encode_keys(self.B, self.Hkv, self.D, K_win, self.cap, self.w, self.n, self.cap, self.P, self.c_q,
                             self.c_k, self.codes, self.kfac, 0, None, None, stream)
 
@@ -87,6 +102,10 @@ class DecodeState:
                                self.qplanes, self.qscal, stream, qrot_out=qrot_out)
 
     def score(self, stream=None):
+        if self.compact:
+            rbq.rbq_score_f16(self.B, self.Hq, self.Hkv, self.D, self.n, self.cap, self.codes, self.kfac16,
+                              self.qplanes, self.qscal, self.scores, stream)
+            return
         rbq.rbq_score(self.B, self.Hq, self.Hkv, self.D, self.n, self.cap, self.codes, self.kfac, self.qplanes,
                       self.qscal, self.scores, stream)
 
@@ -113,6 +132,12 @@ class DecodeState:
         score -> Top-p -> sparse attention (index selection + window), and the
         lazy flush of the window into index rows [n, n + w) (which this step's
         scoring does not read), in one call with fewer launches."""
+        if self.compact:
+            rbq.rbq_decode_step_f16(self.B, self.Hq, self.Hkv, self.D, self.q, self.P, self.c_k, self.K, self.V,
+                                    self.cap, self.n, self.w, self.codes, self.kfac16, flush, p, self.sm_scale,
+                                    self.qplanes, self.qscal, self.scores, self.sel_idx, self.sel_count, self.out,
+                                    self.lse, self.ws_step, stream)
+            return
         rbq.rbq_decode_step(self.B, self.Hq, self.Hkv, self.D, self.q, self.P, self.c_q, self.c_k, self.K, self.V,
                             self.cap, self.n, self.w, self.codes, self.kfac, flush, p, self.sm_scale, self.qplanes,
                             self.qscal, self.scores, self.sel_idx, self.sel_count, self.out, self.lse, self.ws_step,
@@ -137,7 +162,11 @@ class DecodeState:
         zero centroid)."""
         for b, nb in enumerate(seq_n_host):
             nb = min(int(nb), self.n)
-            if nb > 0:
+            if nb > 0 and self.compact:
+                rbq.rbq_encode_keys_f16(1, self.Hkv, self.D, self.K[b:b + 1], self.cap, nb, 0, self.cap, self.P,
+                                        self.c_k[b:b + 1], self.codes[b:b + 1], self.kfac16[b:b + 1],
+                                        rbq.RBQ_ENCODE_SET_CENTROID, self.ws_encode, stream)
+            elif nb > 0:
                 rbq.rbq_encode_keys(1, self.Hkv, self.D, self.K[b:b + 1], self.cap, nb, 0, self.cap, self.P,
                                     None if self.c_q is None else self.c_q[b:b + 1], self.c_k[b:b + 1],
                                     self.codes[b:b + 1], self.kfac[b:b + 1], rbq.RBQ_ENCODE_SET_CENTROID, None,
@@ -145,6 +174,12 @@ class DecodeState:
 
     def step_ragged(self, seq_n, seq_w, seq_p, stream=None, flush=True):
         """One decode step of a ragged batch (rbq_decode_step_varlen)."""
+        if self.compact:
+            rbq.rbq_decode_step_varlen_f16(self.B, self.Hq, self.Hkv, self.D, self.q, self.P, self.c_k, self.K,
+                                           self.V, self.cap, self.n, self.w, seq_n, seq_w, self.codes, self.kfac16,
+                                           flush, seq_p, self.sm_scale, self.qplanes, self.qscal, self.scores,
+                                           self.sel_idx, self.sel_count, self.out, self.lse, self.ws_step, stream)
+            return
         rbq.rbq_decode_step_varlen(self.B, self.Hq, self.Hkv, self.D, self.q, self.P, self.c_q, self.c_k, self.K,
                                    self.V, self.cap, self.n, self.w, seq_n, seq_w, self.codes, self.kfac, flush,
                                    seq_p, self.sm_scale, self.qplanes, self.qscal, self.scores, self.sel_idx,

@@ -27,6 +27,7 @@ EXPORTED = [
     "rbq_encode_keys_debug", "rbq_quantize_query_debug", "rbq_score_ints",
     "rbq_score_varlen", "rbq_topp_select_varlen", "rbq_sparse_decode_varlen", "rbq_dense_decode_varlen",
     "rbq_decode_step_varlen", "rbq_quantize_query_bits",
+    "rbq_encode_keys_f16", "rbq_score_f16", "rbq_decode_step_f16", "rbq_score_varlen_f16", "rbq_decode_step_varlen_f16",
 ]
 
 
@@ -66,6 +67,14 @@ def _load():
                                     vp],
         "rbq_decode_step_varlen": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp,
                                    i32, vp, f32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
+        # the compact index (fp16 factors, no c_q)
+        "rbq_encode_keys_f16": [i32, i32, i32, vp, i32, i64, i32, i32, i32, vp, vp, vp, vp, u32, vp, sz, vp],
+        "rbq_score_f16": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp],
+        "rbq_decode_step_f16": [i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, i32, f32, f32,
+                                vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
+        "rbq_score_varlen_f16": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp],
+        "rbq_decode_step_varlen_f16": [i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp,
+                                       i32, vp, f32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -277,3 +286,46 @@ def rbq_decode_step_varlen(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K
         kv_dtype_code(K), cap, n, w, _ptr(seq_n), _ptr(seq_w), _ptr(codes), _ptr(kfac), int(bool(flush)),
         _ptr(seq_p), sm_scale, _ptr(qplanes), _ptr(qscal), _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _ptr(out),
         _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+# ---- the compact index: one fp16 factor per key ([B][Hkv][cap] torch.float16), built and read with c_q = 0
+
+
+def rbq_encode_keys_f16(batch, heads_kv, head_dim, keys, keys_ld, n_new, offset, cap, P, c_k, codes, kfac16, flags,
+                        ws=None, stream=None):
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("rbq_encode_keys_f16", lib.rbq_encode_keys_f16(
+        batch, heads_kv, head_dim, _ptr(keys), kv_dtype_code(keys), keys_ld, n_new, offset, cap, _ptr(P), _ptr(c_k),
+        _ptr(codes), _ptr(kfac16), flags, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def rbq_score_f16(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac16, qplanes, qscal, scores, stream=None):
+    _check("rbq_score_f16", lib.rbq_score_f16(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(codes), _ptr(kfac16),
+                                              _ptr(qplanes), _ptr(qscal), _ptr(scores), _stream(stream)))
+
+
+def rbq_decode_step_f16(batch, heads_q, heads_kv, head_dim, q, P, c_k, K, V, cap, n, w, codes, kfac16, flush, p,
+                        sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws, stream=None):
+    ws_bytes = ws.numel() * ws.element_size()
+    _check("rbq_decode_step_f16", lib.rbq_decode_step_f16(
+        batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_k), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n,
+        w, _ptr(codes), _ptr(kfac16), int(bool(flush)), p, sm_scale, _ptr(qplanes), _ptr(qscal), _ptr(scores),
+        _ptr(sel_idx), _ptr(sel_count), _ptr(out), _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def rbq_score_varlen_f16(batch, heads_q, heads_kv, head_dim, n, cap, seq_n, codes, kfac16, qplanes, qscal, scores,
+                         stream=None):
+    _check("rbq_score_varlen_f16", lib.rbq_score_varlen_f16(
+        batch, heads_q, heads_kv, head_dim, n, cap, _ptr(seq_n), _ptr(codes), _ptr(kfac16), _ptr(qplanes),
+        _ptr(qscal), _ptr(scores), _stream(stream)))
+
+
+def rbq_decode_step_varlen_f16(batch, heads_q, heads_kv, head_dim, q, P, c_k, K, V, cap, n, w, seq_n, seq_w, codes,
+                               kfac16, flush, seq_p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse,
+                               ws, stream=None):
+    ws_bytes = ws.numel() * ws.element_size()
+    _check("rbq_decode_step_varlen_f16", lib.rbq_decode_step_varlen_f16(
+        batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_k), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n,
+        w, _ptr(seq_n), _ptr(seq_w), _ptr(codes), _ptr(kfac16), int(bool(flush)), _ptr(seq_p), sm_scale,
+        _ptr(qplanes), _ptr(qscal), _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _ptr(out), _ptr(lse), _ptr(ws),
+        ws_bytes, _stream(stream)))

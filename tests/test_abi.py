@@ -173,3 +173,32 @@ def test_query_bits_range_is_checked_on_the_host(lib):
     assert qb(5) == lib.RBQ_EUNSUPPORTED
     assert qb(8) == lib.RBQ_EUNSUPPORTED
     assert L.rbq_quantize_query_bits(1, 8, 4, 128, FAKE, FAKE, None, None, 2, FAKE, FAKE, 0) == lib.RBQ_EINVAL
+
+
+def test_compact_index_calls_reject_invalid_arguments_on_the_host(lib):
+    L = lib.lib
+    EINVAL, EUNSUP = lib.RBQ_EINVAL, lib.RBQ_EUNSUPPORTED
+    enc = lambda **k: L.rbq_encode_keys_f16(1, 1, k.get("D", 128), FAKE, 1, 10, 10, k.get("off", 0), 10, FAKE,
+                                            FAKE, FAKE, k.get("kf", FAKE), k.get("flags", 0), FAKE, 1 << 20, 0)
+    assert enc(kf=None) == EINVAL
+    assert enc(kf=FAKE + 2) == EINVAL
+    assert enc(off=1) == EINVAL
+    assert enc(flags=4) == EINVAL
+    assert enc(D=64) == EUNSUP
+    sc = lambda n=10, kf=FAKE: L.rbq_score_f16(1, 8, 4, 128, n, 10, FAKE, kf, FAKE, FAKE, FAKE, 0)
+    assert sc(n=11) == EINVAL
+    assert sc(kf=None) == EINVAL
+    assert sc(kf=FAKE + 4) == EINVAL
+    assert sc(n=0, kf=None) == lib.RBQ_OK          # nothing to score: nothing read, nothing enqueued
+    step = lambda **k: L.rbq_decode_step_f16(1, 8, 4, 128, FAKE, FAKE, FAKE, FAKE, FAKE, 1, k.get("cap", 200), 100,
+                                             10, FAKE, k.get("kf", FAKE), 1, 0.9, 0.1, FAKE, FAKE, FAKE, FAKE,
+                                             FAKE, FAKE, None, FAKE, k.get("wsb", 1 << 30), 0)
+    assert step(cap=105) == EINVAL
+    assert step(wsb=64) == EINVAL
+    assert step(kf=None) == EINVAL
+    sv = L.rbq_score_varlen_f16(1, 8, 4, 128, 10, 10, None, FAKE, FAKE, FAKE, FAKE, FAKE, 0)
+    assert sv == EINVAL                              # seq_n is required
+    stv = L.rbq_decode_step_varlen_f16(1, 8, 4, 128, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 200, 100, 10, FAKE, None,
+                                       FAKE, None, 1, FAKE, 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                       1 << 30, 0)
+    assert stv == EINVAL                             # no factor array

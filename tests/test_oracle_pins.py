@@ -341,6 +341,80 @@ def test_score_paths_agree():
         assert np.allclose(alt["S"], est["S"], rtol=1e-12, atol=1e-12)
 
 
+# ---------------------------------------------------------------- the compact index (Appendix C)
+def _is_binary16(v):
+    """v (float64) lies in the IEEE binary16 set: 0, or |v| <= 65504 with an
+    11-bit significand (normal: 2^(e-10) steps for 2^e <= |v| < 2^(e+1),
+    e >= -14; subnormal: multiples of 2^-24)."""
+    a = np.abs(np.asarray(v, np.float64))
+    ok = a <= 65504.0
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    step = np.where(a >= 2.0 ** -14, 2.0 ** (e - 10), 2.0 ** -24)
+    return ok & ((a == 0) | (a / step == np.round(a / step)))
+
+
+def test_compact_factor_is_ieee_binary16_rounding():
+    """Cases worked from the binary16 definition (11-bit significand, round to
+    nearest, ties to the even significand), independent of NumPy's float16."""
+    u = 2.0 ** -10                       # spacing at [1, 2)
+    cases = [
+        (1.0, 1.0), (1.0 + u, 1.0 + u),
+        (1.0 + u / 2, 1.0),                          # tie -> even significand (1.0)
+        (1.0 + 3 * u / 2, 1.0 + 2 * u),              # tie between odd 1+u and even 1+2u
+        (1.0 + u / 2 + 2.0 ** -30, 1.0 + u),         # just above the tie
+        (2049.0, 2048.0), (2051.0, 2052.0),          # spacing 2 on [2048, 4096): ties to even
+        (2050.9, 2050.0), (2051.1, 2052.0),
+        (65504.0, 65504.0), (65519.0, 65504.0), (65520.0, 65504.0), (1e9, 65504.0),   # saturation
+        (0.0, 0.0), (2.0 ** -24, 2.0 ** -24),        # zero, the smallest subnormal
+        (2.0 ** -25, 0.0),                           # tie between 0 (even) and 2^-24 (odd)
+        (3 * 2.0 ** -25, 2.0 ** -23),                # tie between 2^-24 (odd) and 2^-23 (even)
+        (1.0 / 3.0, 1365 * 2.0 ** -12),              # 0x3555: 1.0101010101b x 2^-2
+    ]
+    for x, want in cases:
+        assert orc.compact_factor(np.array([x]))[0] == want, x
+    # random normal-range factors: in the binary16 set, within half a spacing (2^-11 relative)
+    rng = np.random.default_rng(8)
+    f = np.exp(rng.uniform(np.log(1e-3), np.log(6e4), 20000))
+    c = orc.compact_factor(f)
+    assert _is_binary16(c).all()
+    assert np.all(np.abs(c - f) <= 2.0 ** -11 * np.abs(f))
+    # nearest: no binary16 neighbour of c is closer to f
+    e = np.floor(np.log2(c))
+    step = 2.0 ** (e - 10)
+    assert (_is_binary16(c - step) & _is_binary16(c + step)).all()
+    for nb in (c - step, c - step / 2, c + step):   # neighbours below (half a step below a power of two) and above
+        ok = _is_binary16(nb) & (nb != c)
+        assert np.all(np.abs(nb - f)[ok] >= np.abs(c - f)[ok])
+
+
+def test_compact_index_scores_and_size():
+    """Appendix C's index: D/8 bytes of codes + one 2-byte factor per key and
+    head, 18 bytes at D = 128 (the printed eta = 18/512 ~ 3.5 %). Its scores
+    are the full estimate with g = 0 and f rounded to binary16, so each stays
+    within 2^-11 |A f X| of the fp64 estimate, and the Top-p sets stay close."""
+    g = _golden("index_overhead_fp16.txt")
+    D = int(g["head_dim"])
+    assert D // 8 + np.dtype(np.float16).itemsize == g["index_bytes_per_key_per_head"]
+    w = gen.random_case(1, 4, 1, 3000, seed=9, kv_dtype="f32", c_q_scale=0.0, key_offset=1.0, q_scale=6.0)
+    K = w.K_f32(0, 0)
+    enc = orc.encode_keys(K, w.P)
+    f16 = orc.compact_factor(enc["f"])
+    assert np.all(f16 > 0)
+    same = 0
+    for h in range(4):
+        qq = orc.quantize_query(w.q[0, h], w.P, None, enc["c_k"])
+        full = orc.scores_from_codes(enc["codes"], enc["f"], enc["g"], qq["codes"], qq["ql"], qq["delta"],
+                                     qq["s_u"], qq["A"], qq["B0"])
+        comp = orc.scores_from_codes(enc["codes"], f16, np.zeros_like(f16), qq["codes"], qq["ql"], qq["delta"],
+                                     qq["s_u"], qq["A"], qq["B0"])
+        bound = 2.0 ** -11 * np.abs(qq["A"] * enc["f"] * full["X"]) + 1e-12
+        assert np.all(np.abs(comp["S"] - full["S"]) <= bound)
+        a = orc.topp_select(full["S"], 0.9, 1 / np.sqrt(D))["idx"]
+        b = orc.topp_select(comp["S"], 0.9, 1 / np.sqrt(D))["idx"]
+        same += np.intersect1d(a, b).size / max(a.size, b.size)
+    assert same / 4 > 0.95
+
+
 def test_estimate_tracks_true_scores():
     """On keys shaped like an LLM's, the estimate correlates strongly with q . k."""
     w = gen.config1()
