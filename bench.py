@@ -223,13 +223,35 @@ def time_scan_c5(pipeline, gen, torch, steps, warmup, replicas=4):
     calls = 16
     g = _graph(torch, lambda: [reps[i % len(reps)].score() for i in range(calls)])
     ms = _time_graphs(torch, [g], max(2, steps // 2), warmup) / calls
+    del g
     B, Hq, Hkv, D, n = st.B, st.Hq, st.Hkv, st.D, st.n
     nbytes = B * Hkv * n * (D // 8 + 8) + B * Hq * n * 4
     gbs = nbytes / (ms * 1e-3) / 1e9
+    # the same scan on the compact index (D/8 + 2 bytes per key; the workload's query centroid is zero)
+    comp = []
+    for r in reps:
+        c = pipeline.DecodeState(B, Hq, Hkv, D, st.cap, n, st.w, st.K, st.V, st.q, st.P, None, compact=True)
+        c.c_k.copy_(st.c_k)
+        c.codes = r.codes
+        c.qplanes, c.qscal, c.scores = st.qplanes, st.qscal, r.scores
+        comp.append(c)
+    pipeline.rbq.rbq_encode_keys_f16(B, Hkv, D, st.K, st.cap, n, 0, st.cap, st.P, comp[0].c_k, comp[0].codes,
+                                     comp[0].kfac16, 0)
+    for c in comp[1:]:
+        c.kfac16.copy_(comp[0].kfac16)
+    del c
+    torch.cuda.synchronize()
+    g = _graph(torch, lambda: [comp[i % len(comp)].score() for i in range(calls)])
+    ms16 = _time_graphs(torch, [g], max(2, steps // 2), warmup) / calls
+    del g
+    nbytes16 = B * Hkv * n * (D // 8 + 2) + B * Hq * n * 4
+    gbs16 = nbytes16 / (ms16 * 1e-3) / 1e9
     return {"workload": "gqa 64q/8kv ctx=128K b=4 bf16 student-t", "kernel": "score_kernel",
             "ms": ms, "keys_per_s": B * Hq * n / (ms * 1e-3), "kv_keys_per_s": B * Hkv * n / (ms * 1e-3),
             "bytes": nbytes, "GBps": gbs, "frac_hbm": gbs / HBM_PEAK_GBS,
-            "traffic": _measured_traffic(SCAN_TRAFFIC_FILE, SCORE_SRC, "score_source_sha256")}
+            "traffic": _measured_traffic(SCAN_TRAFFIC_FILE, SCORE_SRC, "score_source_sha256"),
+            "compact_index": {"ms": ms16, "keys_per_s": B * Hq * n / (ms16 * 1e-3), "bytes": nbytes16,
+                              "GBps": gbs16, "frac_hbm": gbs16 / HBM_PEAK_GBS}}
 
 
 def time_ragged(pipeline, gen, torch, steps, warmup, seed=20260):
@@ -381,6 +403,45 @@ def quality(pipeline, torch, st, p_list, seed=20261):
     return out
 
 
+def compact_index(pipeline, torch, reps, p_list, steps, warmup, dense_ms):
+    """The 128K step on the compact index (one fp16 factor per key, no query
+    centroid; rbq_decode_step_f16) over the same replicas of the cache: step
+    time per p, the score call alone, and how far its Top-p sets move from the
+    full index's (mean Jaccard similarity per head)."""
+    comp = []
+    for r in reps:
+        c = pipeline.DecodeState(r.B, r.Hq, r.Hkv, r.D, r.cap, r.n, r.w, r.K, r.V, r.q, r.P, None, compact=True)
+        c.build_index()
+        comp.append(c)
+    torch.cuda.synchronize()
+    out = {}
+    for p in p_list:
+        gs = [_graph(torch, lambda c=c, p=p: c.step(p)) for c in comp]
+        ms = _time_graphs(torch, gs, steps, warmup)
+        del gs
+        comp[0].step(p)
+        reps[0].step(p)
+        torch.cuda.synchronize()
+        jac = []
+        sa, ca = comp[0].sel_idx.cpu().numpy(), comp[0].sel_count.cpu().numpy()
+        sb, cb = reps[0].sel_idx.cpu().numpy(), reps[0].sel_count.cpu().numpy()
+        for b in range(reps[0].B):
+            for h in range(reps[0].Hq):
+                x, y = sa[b, h, :ca[b, h]], sb[b, h, :cb[b, h]]
+                jac.append(np.intersect1d(x, y).size / max(1, np.union1d(x, y).size))
+        out[str(p)] = {"ms_per_step": ms, "speedup_vs_dense": dense_ms / ms, "budget_mean": float(ca.mean()),
+                       "jaccard_vs_full_index": float(np.mean(jac))}
+    REPS = 16
+    g = _graph(torch, lambda: [comp[i % len(comp)].score() for i in range(REPS)])
+    ms_score = _time_graphs(torch, [g], max(2, steps // 4), 2) / REPS
+    del g
+    st = comp[0]
+    nbytes = st.B * st.Hkv * st.n * (st.D // 8 + 2) + st.B * st.Hq * st.n * 4
+    return {"workload": "the 128K step on the compact index (fp16 factor, no query centroid)",
+            "index_bytes_per_key": st.D // 8 + 2, "p": out, "score_ms": ms_score, "score_bytes": nbytes,
+            "score_GBps": nbytes / (ms_score * 1e-3) / 1e9}
+
+
 def offload(pipeline, torch, st, p_list, steps, warmup):
     """The same 128K step with the K/V cache in pinned host memory and the index
     in HBM: the kernels read the cache over PCIe (rbq.MappedHost), so the sparse
@@ -488,6 +549,7 @@ def main():
     ap.add_argument("--no-quality", action="store_true", help="skip the attention-recall report")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-overlap (time to first token) report")
     ap.add_argument("--no-offload", action="store_true", help="skip the step with the K/V cache in host memory")
+    ap.add_argument("--no-compact", action="store_true", help="skip the step on the compact (fp16-factor) index")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
@@ -599,6 +661,13 @@ def main():
         st0.step(p)
         torch.cuda.synchronize()
 
+    # the same step on the compact index
+    compact = None
+    if not args.no_compact:
+        compact = compact_index(pipeline, torch, reps, [0.8, 0.9, 0.95], args.steps, args.warmup, dense_best)
+        st0.step(p)
+        torch.cuda.synchronize()
+
     # the step with the cache in host memory (reads over PCIe)
     offloaded = None
     if not args.no_offload:
@@ -672,6 +741,7 @@ def main():
         "recall": recall,
         "prefill_overlap": prefill,
         "kv_in_host_memory": offloaded,
+        "compact_index": compact,
         "cpu_baseline": cpu,
         "gen_s": t_gen,
         "git": _git_sha(),
