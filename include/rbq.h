@@ -119,10 +119,13 @@ rbq_status rbq_quantize_query(int32_t batch, int32_t heads_q, int32_t heads_kv, 
  * rbq_quantize_query_bits -- rbq_quantize_query with B_q = `bits` quantisation
  * bits instead of 4 (Theorem A.2 bounds the estimator's error for any B_q;
  * Section 3.3 uses 4): Delta = (q_r - q_l) / (2^bits - 1), codes in
- * [0, 2^bits - 1], bit-planes j >= bits zero. The output feeds rbq_score
- * unchanged. bits in [1, 4]; 5..8: RBQ_EUNSUPPORTED (the scan multiplies
- * 4-bit codes); otherwise RBQ_EINVAL. bits = 4 gives rbq_quantize_query's
- * results bitwise.
+ * [0, 2^bits - 1], bit-planes j >= bits zero. bits in [1, 8], RBQ_EINVAL
+ * otherwise.
+ *   bits 1..4: qplanes [B][Hq][4][D/32] as rbq_quantize_query writes it; the
+ *     output feeds rbq_score (and every call that reads qplanes) unchanged;
+ *     bits = 4 gives rbq_quantize_query's results bitwise.
+ *   bits 5..8: qplanes [B][Hq][8][D/32], eight bit-planes per head, read by
+ *     rbq_score_q8.
  */
 rbq_status rbq_quantize_query_bits(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
                                    const float* q, const float* P, const float* c_q, const float* c_k,
@@ -144,6 +147,18 @@ rbq_status rbq_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t h
                      int32_t n, int32_t cap, const uint32_t* codes, const float* kfac,
                      const uint32_t* qplanes, const float* qscal, float* scores,
                      hipStream_t stream);
+
+/*
+ * rbq_score_q8 -- rbq_score for queries quantised to up to 8 bits
+ * (rbq_quantize_query_bits with bits 5..8, Theorem A.2): qplanes8 is
+ * [B][Hq][8][D/32], ip = sum_{j < 8} 2^j popcount(code_i AND plane_j), the
+ * rest as in rbq_score. (The fused step and the ragged calls read 4-bit
+ * queries only.)
+ */
+rbq_status rbq_score_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                        int32_t n, int32_t cap, const uint32_t* codes, const float* kfac,
+                        const uint32_t* qplanes8, const float* qscal, float* scores,
+                        hipStream_t stream);
 
 /*
  * rbq_topp_select -- adaptive Top-p selection, Algorithm 2 step 3 and
@@ -355,7 +370,8 @@ int32_t rbq_version(void);
  *   rbq_quantize_query_debug: as rbq_quantize_query, plus qrot_out [B][Hq][D]
  *     float = the fp32 rotated unit query that was quantised.
  *   rbq_score_ints: ip_out [B][Hq][n] int32 = <c_b, q_u>, pc_out [B][Hkv][n]
- *     int32 = popcount(c_b), computed by the score kernel's integer path.
+ *     int32 = popcount(c_b), computed by the score kernel's integer path;
+ *     rbq_score_ints_q8 the same from 8-plane queries (rbq_score_q8's path).
  */
 rbq_status rbq_encode_keys_debug(int32_t batch, int32_t heads_kv, int32_t head_dim,
                                  const void* keys, int32_t keys_dtype, int64_t keys_ld,
@@ -371,6 +387,9 @@ rbq_status rbq_quantize_query_debug(int32_t batch, int32_t heads_q, int32_t head
 rbq_status rbq_score_ints(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
                           int32_t n, int32_t cap, const uint32_t* codes, const uint32_t* qplanes,
                           int32_t* ip_out, int32_t* pc_out, hipStream_t stream);
+rbq_status rbq_score_ints_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                             int32_t n, int32_t cap, const uint32_t* codes, const uint32_t* qplanes8,
+                             int32_t* ip_out, int32_t* pc_out, hipStream_t stream);
 
 #ifdef __cplusplus
 }

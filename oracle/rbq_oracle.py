@@ -184,10 +184,12 @@ def quantize_query(q: np.ndarray, P: np.ndarray, c_q: np.ndarray | None, c_k: np
                 B0=float(np.asarray(q, np.float64) @ np.asarray(c_k, np.float64)))
 
 
-def query_bit_planes(codes: np.ndarray) -> np.ndarray:
-    """Bit-plane j of the INT4 codes, packed like the key codes: [4][D/32] uint32."""
+def query_bit_planes(codes: np.ndarray, planes: int = B_Q) -> np.ndarray:
+    """Bit-plane j of the query codes, packed like the key codes: [planes][D/32]
+    uint32 (4 planes for the INT4 codes of Section 3.3; 8 hold codes of up to
+    8 bits)."""
     codes = np.asarray(codes, np.int64)
-    return np.stack([pack_bits(((codes >> j) & 1).astype(np.uint8)) for j in range(B_Q)])
+    return np.stack([pack_bits(((codes >> j) & 1).astype(np.uint8)) for j in range(planes)])
 
 
 # ---------------------------------------------------------------------------

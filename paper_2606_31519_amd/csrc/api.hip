@@ -97,7 +97,6 @@ rbq_status rbq_quantize_query(int32_t batch, int32_t heads_q, int32_t heads_kv, 
 rbq_status rbq_quantize_query_bits(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
                                    const float* q, const float* P, const float* c_q, const float* c_k, int32_t bits,
                                    uint32_t* qplanes, float* qscal, hipStream_t stream) {
-  if (bits >= 5 && bits <= 8) return RBQ_EUNSUPPORTED;   // the scan multiplies 4-bit query codes
   if (bits < 1 || bits > 8) return RBQ_EINVAL;
   const rbq_status s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal);
   if (s != RBQ_OK) return s;
@@ -131,6 +130,25 @@ rbq_status rbq_score_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32
   if (s != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, qscal, scores, nullptr, nullptr,
                       stream, nullptr, nullptr, 0, nullptr, kfac16);
+}
+
+rbq_status rbq_score_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
+                        const uint32_t* codes, const float* kfac, const uint32_t* qplanes8, const float* qscal,
+                        float* scores, hipStream_t stream) {
+  const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes8, qscal, scores);
+  if (s != RBQ_OK) return s;
+  return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes8, qscal, scores, nullptr, nullptr,
+                      stream, nullptr, nullptr, 0, nullptr, nullptr, 8);
+}
+
+rbq_status rbq_score_ints_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
+                             int32_t cap, const uint32_t* codes, const uint32_t* qplanes8, int32_t* ip_out,
+                             int32_t* pc_out, hipStream_t stream) {
+  const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, ip_out, qplanes8, pc_out,
+                                   ip_out);
+  if (s != RBQ_OK) return s;
+  return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes8, nullptr, nullptr, ip_out, pc_out,
+                      stream, nullptr, nullptr, 0, nullptr, nullptr, 8);
 }
 
 rbq_status rbq_score_ints(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,

@@ -95,6 +95,7 @@ struct QuantArgs {
   float* qrot_out;       // or NULL
   int Hq, Hkv;
   int levels;            // 2^B_q - 1
+  int planes;            // bit-planes written per head: 4 (B_q <= 4) or 8
 };
 
 // query head `row` (= b * Hq + h), by the kQAll threads of the calling block
@@ -158,9 +159,10 @@ __device__ __forceinline__ void quantize_row(const QuantArgs& qa, int row) {
 
   // bit-plane m, 64 dimensions per wave: low 32 lanes -> word 2w, high -> 2w + 1
   const int w = j / kWave;
-  uint32_t* planes = qplanes + int64_t(row) * 4 * kWords;
+  uint32_t* planes = qplanes + int64_t(row) * qa.planes * kWords;
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
+  for (int m = 0; m < 8; ++m) {
+    if (m >= qa.planes) break;
     const uint64_t bal = __ballot((code >> m) & 1);
     if (lead && lane_id() == 0) {
       planes[m * kWords + 2 * w] = uint32_t(bal);
@@ -201,7 +203,7 @@ __global__ __launch_bounds__(kQAll) void quantize_flush_kernel(QuantArgs qa, Enc
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
                            hipStream_t stream, int32_t bits) {
-  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, qrot_out, heads_q, heads_kv, (1 << bits) - 1};
+  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, qrot_out, heads_q, heads_kv, (1 << bits) - 1, bits > 4 ? 8 : 4};
   quantize_kernel<<<batch * heads_q, kQAll, 0, stream>>>(qa);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
@@ -213,7 +215,7 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
                                  const int32_t* seq_cnt, int32_t off_max, uint16_t* kfac16) {
   if (n_new == 0)
     return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
-  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, nullptr, heads_q, heads_kv, 15};
+  const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, nullptr, heads_q, heads_kv, 15, 4};
   const EncodeArgs ea{keys,  keys_ld, n_new,   offset,  cap,     P,       c_q,     c_k,     codes,
                       kfac,  nullptr, nullptr, seq_off, seq_cnt, off_max, heads_kv, kfac16};
   const int rows = batch * heads_q, bhs = batch * heads_kv;

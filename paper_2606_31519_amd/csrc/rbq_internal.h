@@ -111,7 +111,7 @@ rbq_status launch_encode(int32_t batch, int32_t heads_kv, const void* keys, int3
                          uint32_t* codes, float* kfac, uint32_t flags, float* alpha_out, void* ws,
                          float* rot_out, hipStream_t stream, uint16_t* kfac16 = nullptr);
 // (kfac16: the compact index's fp16 factors, written instead of kfac when non-NULL)
-// bits: B_q, the query's quantisation bits (1..4)
+// bits: B_q, the query's quantisation bits (1..8; 4 bit-planes per head up to 4 bits, 8 above)
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
                            hipStream_t stream, int32_t bits = 4);
@@ -133,8 +133,9 @@ rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream,
                         float* slot_max = nullptr, unsigned long long* hist = nullptr, int64_t hist_words = 0,
-                        const int32_t* seq_n = nullptr, const uint16_t* kfac16 = nullptr);
-// (kfac16: the compact index's fp16 factors [B][Hkv][cap], read instead of kfac when non-NULL; g = 0)
+                        const int32_t* seq_n = nullptr, const uint16_t* kfac16 = nullptr, int32_t planes = 4);
+// (kfac16: the compact index's fp16 factors [B][Hkv][cap], read instead of kfac when non-NULL; g = 0.
+//  planes: query bit-planes per head, 4 or 8 (8: B_q up to 8; uniform, unfused calls only))
 // slot_max / nslots: per-row partial maxima written by launch_score together with
 // the zeroing of the workspace's counters (the max pass is skipped); masks:
 // optional [rows][topp_mask_words(n)] selection bitmaps (bit i of word k = key 64 k + i);

@@ -70,6 +70,13 @@ __device__ __forceinline__ uint32_t binary_int4_dot(const Spread& e, const uint3
   return a + b;
 }
 
+// ip over QB bit-planes: the low nibbles, plus 16 x the high nibbles when QB = 8
+template <int QB>
+__device__ __forceinline__ uint32_t query_dot(const Spread& e, const uint32_t* qn) {
+  if (QB == 8) return binary_int4_dot(e, qn) + 16u * binary_int4_dot(e, qn + 16);
+  return binary_int4_dot(e, qn);
+}
+
 // block maximum of each of the G heads from the per-wave maxima
 // (maxima of every 32-lane half-wave, reduced by DPP in the head loop)
 constexpr int kHalfWaves = 2 * kScoreThreads / kWave;
@@ -93,13 +100,16 @@ struct ScoreSlots {
 };
 
 // FAC16: the compact index, one fp16 factor f per key (g = 0) instead of (f, g) in fp32.
-template <int KPT, bool INTS, bool SLOTS, bool RAGGED, bool FAC16>
+// QB: bit-planes per query head, 4 (B_q <= 4) or 8 (B_q <= 8: the code is split
+// into its low and high nibbles, ip = ip_lo + 16 ip_hi, two dot8 chains).
+template <int KPT, bool INTS, bool SLOTS, bool RAGGED, bool FAC16, int QB = 4>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const u32x4* __restrict__ codes, const f32x2* __restrict__ kfac, const uint16_t* __restrict__ kfac16,
     const uint32_t* __restrict__ qplanes, const float* __restrict__ qscal, float* __restrict__ scores,
     int32_t* __restrict__ ip_out, int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G,
     ScoreSlots sl, const int32_t* __restrict__ seq_n) {
-  __shared__ uint32_t qn_s[kMaxGroup][16];
+  constexpr int QW = 4 * QB;                 // nibble words per head
+  __shared__ uint32_t qn_s[kMaxGroup][QW];
   __shared__ float mx_s[SLOTS ? kMaxGroup : 1][kHalfWaves];
   const int bh = blockIdx.y;                 // b * Hkv + kv head
   const int b = bh / Hkv;
@@ -141,10 +151,14 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   const bool full = (blockIdx.x + 1) * (kScoreThreads * KPT) <= nb;   // block-uniform: no key past nb
   if (threadIdx.x < 4 * G) {                  // one lane per (head, word)
     const int h = threadIdx.x >> 2, w = threadIdx.x & 3;
-    const uint32_t* Q = qplanes + int64_t(row0 + h) * 16 + w;   // [plane][word]
+    const uint32_t* Q = qplanes + int64_t(row0 + h) * QW + w;   // [plane][word]
     uint32_t o[4];
     planes_to_nibbles(Q[0], Q[4], Q[8], Q[12], o);
     *reinterpret_cast<u32x4*>(&qn_s[h][4 * w]) = u32x4{o[0], o[1], o[2], o[3]};
+    if (QB == 8) {                              // planes 4..7: the high nibbles
+      planes_to_nibbles(Q[16], Q[20], Q[24], Q[28], o);
+      *reinterpret_cast<u32x4*>(&qn_s[h][16 + 4 * w]) = u32x4{o[0], o[1], o[2], o[3]};
+    }
   }
   int pcm[KPT];   // 2 popcount(code) - D, exact
   Spread e[KPT];
@@ -163,9 +177,9 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   if (full && !INTS) {
     for (int g = 0; g < G; ++g) {
       const int row = row0 + g;
-      uint32_t qn[16];
+      uint32_t qn[QW];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
+      for (int t = 0; t < QW / 4; ++t) {
         const u32x4 v = *reinterpret_cast<const u32x4*>(&qn_s[g][4 * t]);
         qn[4 * t] = v.x; qn[4 * t + 1] = v.y; qn[4 * t + 2] = v.z; qn[4 * t + 3] = v.w;
       }
@@ -177,7 +191,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       float mx = -INFINITY;
 #pragma unroll
       for (int u = 0; u < KPT; ++u) {
-        const int ip = int(binary_int4_dot(e[u], qn));
+        const int ip = int(query_dot<QB>(e[u], qn));
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         const float sc = assemble(u, y, B0);
         if (SLOTS) mx = fmaxf(mx, sc);
@@ -193,9 +207,9 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   }
   for (int g = 0; g < G; ++g) {
     const int row = row0 + g;
-    uint32_t qn[16];
+    uint32_t qn[QW];
 #pragma unroll
-    for (int t = 0; t < 16; ++t) qn[t] = qn_s[g][t];
+    for (int t = 0; t < QW; ++t) qn[t] = qn_s[g][t];
     const float* qs = qscal + int64_t(row) * RBQ_QSCAL_STRIDE;
     const float ql = qs[0], delta = qs[1], A = qs[3], B0 = qs[4];
     const int su = int(qs[2]);
@@ -205,7 +219,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
 #pragma unroll
     for (int u = 0; u < KPT; ++u) {
       const int i = i0 + u * kScoreThreads;
-      const int ip = int(binary_int4_dot(e[u], qn));
+      const int ip = int(query_dot<QB>(e[u], qn));
       if (INTS) {
         if (i < nb) ip_out[int64_t(row) * n + i] = ip;
       } else {
@@ -226,7 +240,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
 }
 
-template <bool INTS, bool SLOTS, bool RAGGED, bool FAC16 = false>
+template <bool INTS, bool SLOTS, bool RAGGED, bool FAC16 = false, int QB = 4>
 rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
                       const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal, float* scores,
                       int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
@@ -235,15 +249,15 @@ rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* co
   const f32x2* f2 = reinterpret_cast<const f32x2*>(kfac);
   switch (kpt) {
     case 4:
-      score_kernel<4, INTS, SLOTS, RAGGED, FAC16><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
+      score_kernel<4, INTS, SLOTS, RAGGED, FAC16, QB><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
                                                                        n, cap, Hq, Hkv, G, sl, seq_n);
       break;
     case 2:
-      score_kernel<2, INTS, SLOTS, RAGGED, FAC16><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
+      score_kernel<2, INTS, SLOTS, RAGGED, FAC16, QB><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
                                                                        n, cap, Hq, Hkv, G, sl, seq_n);
       break;
     default:
-      score_kernel<1, INTS, SLOTS, RAGGED, FAC16><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
+      score_kernel<1, INTS, SLOTS, RAGGED, FAC16, QB><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
                                                                        n, cap, Hq, Hkv, G, sl, seq_n);
       break;
   }
@@ -256,7 +270,7 @@ rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, float* slot_max,
                         unsigned long long* hist, int64_t hist_words, const int32_t* seq_n,
-                        const uint16_t* kfac16) {
+                        const uint16_t* kfac16, int32_t planes) {
   if (n == 0) return RBQ_OK;
   const int G = heads_q / heads_kv;
   const int kpt = score_keys_per_lane(batch, heads_kv, n);
@@ -266,6 +280,18 @@ rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
   launch_kpt<I, S, R, F>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, cap, \
                          heads_q, heads_kv, G, sl, seq_n)
 #define RBQ_SCORE_FAC(S, R) (kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, S, R, true) : RBQ_SCORE_LAUNCH(false, S, R, false))
+  if (planes == 8) {   // 8-plane queries: the standalone call only (integer hook included)
+    if (ip_out != nullptr)
+      return launch_kpt<true, false, false, false, 8>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores,
+                                                      ip_out, pc_out, n, cap, heads_q, heads_kv, G, sl, seq_n);
+    return kfac16 != nullptr
+               ? launch_kpt<false, false, false, true, 8>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal,
+                                                          scores, ip_out, pc_out, n, cap, heads_q, heads_kv, G, sl,
+                                                          seq_n)
+               : launch_kpt<false, false, false, false, 8>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal,
+                                                           scores, ip_out, pc_out, n, cap, heads_q, heads_kv, G, sl,
+                                                           seq_n);
+  }
   if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, false);   // (the integer hook is never ragged)
   if (seq_n != nullptr) return slot_max != nullptr ? RBQ_SCORE_FAC(true, true) : RBQ_SCORE_FAC(false, true);
   return slot_max != nullptr ? RBQ_SCORE_FAC(true, false) : RBQ_SCORE_FAC(false, false);

@@ -27,6 +27,7 @@ EXPORTED = [
     "rbq_encode_keys_debug", "rbq_quantize_query_debug", "rbq_score_ints",
     "rbq_score_varlen", "rbq_topp_select_varlen", "rbq_sparse_decode_varlen", "rbq_dense_decode_varlen",
     "rbq_decode_step_varlen", "rbq_quantize_query_bits",
+    "rbq_score_q8", "rbq_score_ints_q8",
     "rbq_encode_keys_f16", "rbq_score_f16", "rbq_decode_step_f16", "rbq_score_varlen_f16", "rbq_decode_step_varlen_f16",
 ]
 
@@ -67,6 +68,8 @@ def _load():
                                     vp],
         "rbq_decode_step_varlen": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp,
                                    i32, vp, f32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
+        "rbq_score_q8": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp],
+        "rbq_score_ints_q8": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp],
         # the compact index (fp16 factors, no c_q)
         "rbq_encode_keys_f16": [i32, i32, i32, vp, i32, i64, i32, i32, i32, vp, vp, vp, vp, u32, vp, sz, vp],
         "rbq_score_f16": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp],
@@ -203,6 +206,17 @@ def rbq_quantize_query_bits(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, 
 def rbq_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores, stream=None):
     _check("rbq_score", lib.rbq_score(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(codes), _ptr(kfac),
                                       _ptr(qplanes), _ptr(qscal), _ptr(scores), _stream(stream)))
+
+
+def rbq_score_q8(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes8, qscal, scores, stream=None):
+    """rbq_score for queries of up to 8 bits (eight bit-planes per head)."""
+    _check("rbq_score_q8", lib.rbq_score_q8(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(codes), _ptr(kfac),
+                                            _ptr(qplanes8), _ptr(qscal), _ptr(scores), _stream(stream)))
+
+
+def rbq_score_ints_q8(batch, heads_q, heads_kv, head_dim, n, cap, codes, qplanes8, ip_out, pc_out, stream=None):
+    _check("rbq_score_ints_q8", lib.rbq_score_ints_q8(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(codes),
+                                                      _ptr(qplanes8), _ptr(ip_out), _ptr(pc_out), _stream(stream)))
 
 
 def rbq_score_ints(batch, heads_q, heads_kv, head_dim, n, cap, codes, qplanes, ip_out, pc_out, stream=None):

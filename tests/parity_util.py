@@ -36,9 +36,9 @@ def u32(t) -> np.ndarray:
 
 
 def planes_to_codes(planes: np.ndarray) -> np.ndarray:
-    """[4][D/32] uint32 bit-planes -> [D] INT4 codes."""
+    """[planes][D/32] uint32 bit-planes (4, or 8 for B_q > 4) -> [D] query codes."""
     D = planes.shape[-1] * 32
-    return sum(orc.unpack_bits(planes[j], D).astype(np.int64) << j for j in range(4))
+    return sum(orc.unpack_bits(planes[j], D).astype(np.int64) << j for j in range(planes.shape[0]))
 
 
 def score_tolerance(codes, f, g, qcodes, qs, D=128):

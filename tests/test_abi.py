@@ -170,8 +170,11 @@ def test_query_bits_range_is_checked_on_the_host(lib):
     qb = lambda bits: L.rbq_quantize_query_bits(1, 8, 4, 128, FAKE, FAKE, None, FAKE, bits, FAKE, FAKE, 0)
     assert qb(0) == lib.RBQ_EINVAL
     assert qb(9) == lib.RBQ_EINVAL
-    assert qb(5) == lib.RBQ_EUNSUPPORTED
-    assert qb(8) == lib.RBQ_EUNSUPPORTED
+    for bits in (5, 8):   # in range, then rejected for the missing c_k before anything is launched
+        assert L.rbq_quantize_query_bits(1, 8, 4, 128, FAKE, FAKE, None, None, bits, FAKE, FAKE, 0) == lib.RBQ_EINVAL
+    assert L.rbq_score_q8(1, 8, 4, 128, 11, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == lib.RBQ_EINVAL
+    assert L.rbq_score_q8(1, 8, 4, 128, 10, 10, FAKE, FAKE, FAKE + 4, FAKE, FAKE, 0) == lib.RBQ_EINVAL
+    assert L.rbq_score_ints_q8(1, 8, 4, 128, 10, 10, FAKE, None, FAKE, FAKE, 0) == lib.RBQ_EINVAL
     assert L.rbq_quantize_query_bits(1, 8, 4, 128, FAKE, FAKE, None, None, 2, FAKE, FAKE, 0) == lib.RBQ_EINVAL
 
 

@@ -91,21 +91,31 @@ def test_quantize_query_stagewise(R, pipeline, case):
             assert np.all(np.abs(t[off] - np.floor(t[off]) - 0.5) <= 1e-4)
 
 
-@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5, 6, 7, 8])
 def test_quantize_query_bits_and_scores(R, pipeline, bits):
     """rbq_quantize_query_bits: the B_q-bit codes decided in fp32 from the GPU's
     rotated query (the same rotation as rbq_quantize_query), bit-exact; B_q = 4
-    is rbq_quantize_query bitwise; the scores from those planes match the oracle."""
+    is rbq_quantize_query bitwise; the scores from those planes match the oracle
+    (B_q > 4: eight planes through rbq_score_q8, whose integer dot products are
+    bit-exact)."""
+    print("query bits", bits, flush=True)
     w = gen.random_case(1, 8, 2, 3000, seed=12, kv_dtype="bf16", c_q_scale=0.5)
     st = pipeline.DecodeState.from_workload(w)
     st.build_index()
     qrot = torch.empty(1, 8, 128, device="cuda")
     st.quantize(qrot_out=qrot)
     planes4, qs4 = pu.u32(st.qplanes).copy(), _np(st.qscal).copy()
-    qp = torch.zeros_like(st.qplanes)
+    nplanes = 8 if bits > 4 else 4
+    qp = torch.zeros(1, 8, nplanes, 4, dtype=torch.int32, device="cuda")
     qs = torch.zeros_like(st.qscal)
     R.rbq_quantize_query_bits(1, 8, 2, 128, st.q, st.P, st.c_q, st.c_k, bits, qp, qs)
-    R.rbq_score(1, 8, 2, 128, st.n, st.cap, st.codes, st.kfac, qp, qs, st.scores)
+    if bits > 4:
+        R.rbq_score_q8(1, 8, 2, 128, st.n, st.cap, st.codes, st.kfac, qp, qs, st.scores)
+        ip = torch.zeros(1, 8, st.n, dtype=torch.int32, device="cuda")
+        pc = torch.zeros(1, 2, st.n, dtype=torch.int32, device="cuda")
+        R.rbq_score_ints_q8(1, 8, 2, 128, st.n, st.cap, st.codes, qp, ip, pc)
+    else:
+        R.rbq_score(1, 8, 2, 128, st.n, st.cap, st.codes, st.kfac, qp, qs, st.scores)
     torch.cuda.synchronize()
     planes, qsb, qr = pu.u32(qp), _np(qs), _np(qrot)
     if bits == 4:
@@ -117,6 +127,9 @@ def test_quantize_query_bits_and_scores(R, pipeline, bits):
         assert np.array_equal(got, z["codes"]) and got.max() == (1 << bits) - 1
         assert qsb[0, h, 0] == np.float32(z["ql"]) and qsb[0, h, 1] == np.float32(z["delta"])
         assert qsb[0, h, 2] == z["s_u"]
+        if bits > 4:
+            ip_or, pc_or = orc.int_dot(orc.unpack_bits(codes[0, h // 4, :st.n], 128), got)
+            assert np.array_equal(_np(ip)[0, h], ip_or) and np.array_equal(_np(pc)[0, h // 4], pc_or)
         pu.check_scores(S[0, h, :st.n], codes[0, h // 4, :st.n], kfac[0, h // 4, :st.n].astype(np.float64),
                         planes[0, h], qsb[0, h])
 

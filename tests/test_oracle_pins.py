@@ -229,10 +229,10 @@ def test_quantizer_is_nearest_level_and_bounded(dtype):
         assert abs(signs @ (x - qbar)) <= D * qz["delta"] / 2
 
 
-@pytest.mark.parametrize("bits", [1, 2, 3])
+@pytest.mark.parametrize("bits", [1, 2, 3, 5, 6, 7, 8])
 def test_quantizer_fewer_bits_is_nearest_level(bits):
-    """B_q below the paper's 4: codes span [0, 2^B_q - 1] and each is the
-    nearest of the 2^B_q levels (brute force), within Delta / 2."""
+    """B_q other than the paper's 4 (Theorem A.2): codes span [0, 2^B_q - 1] and
+    each is the nearest of the 2^B_q levels (brute force), within Delta / 2."""
     rng = np.random.default_rng(10 + bits)
     D, top = 128, (1 << bits) - 1
     for _ in range(20):
@@ -317,6 +317,14 @@ def test_integer_dot_and_reconstruction():
                 acc += (1 << j) * bin(int(words[i, w]) & int(planes[j, w])).count("1")
         assert acc == ip[i]
     assert np.array_equal(sum((orc.unpack_bits(planes[j], D).astype(np.int64) << j) for j in range(4)), codes)
+    # eight planes hold 8-bit codes: ip = sum_{j < 8} 2^j popcount(word & plane_j)
+    codes8 = rng.integers(0, 256, D)
+    planes8 = orc.query_bit_planes(codes8, planes=8)
+    ip8, _ = orc.int_dot(bits, codes8)
+    for i in range(9):
+        acc = sum((1 << j) * bin(int(words[i, w]) & int(planes8[j, w])).count("1")
+                  for j in range(8) for w in range(D // 32))
+        assert acc == ip8[i] == sum(int(bits[i, d]) * int(codes8[d]) for d in range(D))
     # the reconstruction equals <2 c_b - 1, Delta q_u + q_l 1> evaluated directly
     ql, delta = -0.21, 0.028
     X = orc.reconstruct(ip, pc, ql, delta, int(codes.sum()), D)
