@@ -319,7 +319,7 @@ def quality(pipeline, torch, st, p_list, seed=20261):
     rbq_decode_step), the exact Top-k set of the same per-head budget (the best
     any selector of that budget can do), and a fixed-budget Top-k on the
     estimates (every head gets the mean budget). At p = 0.95, the query
-    quantised to 1, 2 or 3 bits instead of 4 (Theorem A.2). Then the re-centering
+    quantised to 1, 2, 3 or 5 to 8 bits instead of 4 (Theorem A.2). Then the re-centering
     ablation of Section 5.4 at p = 0.95, with the index built around the key
     centroid (Algorithm 1) or around 0: on the workload's keys, and on the same
     keys moved by a common offset of twice their median norm (keys clustered
@@ -383,9 +383,14 @@ def quality(pipeline, torch, st, p_list, seed=20261):
         select(st.K, recenter)
         out[f"{p}_{'recentered' if recenter else 'no_recentering'}"] = measure(pi, S, sel, cnt)
     # the query's quantisation bits (Theorem A.2; 4 in the method), on the workload's own index
-    for bits in (1, 2, 3):
-        rbq.rbq_quantize_query_bits(B, Hq, Hkv, D, st.q, st.P, st.c_q, st.c_k, bits, qp, qs)
-        rbq.rbq_score(B, Hq, Hkv, D, n, st.cap, st.codes, st.kfac, qp, qs, S)
+    qp8 = torch.empty(B, Hq, 8, D // 32, dtype=torch.int32, device=st.qplanes.device)
+    for bits in (1, 2, 3, 5, 6, 7, 8):
+        if bits > 4:
+            rbq.rbq_quantize_query_bits(B, Hq, Hkv, D, st.q, st.P, st.c_q, st.c_k, bits, qp8, qs)
+            rbq.rbq_score_q8(B, Hq, Hkv, D, n, st.cap, st.codes, st.kfac, qp8, qs, S)
+        else:
+            rbq.rbq_quantize_query_bits(B, Hq, Hkv, D, st.q, st.P, st.c_q, st.c_k, bits, qp, qs)
+            rbq.rbq_score(B, Hq, Hkv, D, n, st.cap, st.codes, st.kfac, qp, qs, S)
         rbq.rbq_topp_select(B, Hq, n, S, p, st.sm_scale, sel, cnt, st.ws_topp)
         torch.cuda.synchronize()
         out[f"{p}_query_bits_{bits}"] = measure(pi, S, sel, cnt)

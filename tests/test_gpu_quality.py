@@ -45,7 +45,8 @@ def test_recall_report_matches_oracle_definition(pipeline):
     # a set can hold no more than the exact Top-k of its size holds
     assert r["recall_topp"] <= r["recall_exact_topk_same_budget"] + 1e-6
     for key in ("0.95_recentered", "0.95_no_recentering", "0.95_offset_keys_recentered",
-                "0.95_offset_keys_no_recentering", "0.95_query_bits_1", "0.95_query_bits_2", "0.95_query_bits_3"):
+                "0.95_offset_keys_no_recentering", "0.95_query_bits_1", "0.95_query_bits_2", "0.95_query_bits_3",
+                "0.95_query_bits_5", "0.95_query_bits_8"):
         assert 0.0 < rep[key]["recall_topp"] <= 1.0 + 1e-6
     # re-centering makes the index blind to a common shift of the keys
     assert abs(rep["0.95_offset_keys_recentered"]["budget_frac"] - rep["0.95_recentered"]["budget_frac"]) < 0.01
