@@ -17,6 +17,7 @@ rbq_status decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
   const void* fac = kfac16 != nullptr ? static_cast<const void*>(kfac16) : kfac;
   rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
   if (s != RBQ_OK) return s;
+  if (head_dim != kHeadDim && kfac16 != nullptr) return RBQ_EUNSUPPORTED;   // (the compact index is D = 128 only)
   if (n < 0 || w < 0 || cap < 0 || int64_t(n) + w > cap) return RBQ_EINVAL;
   const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
   if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
@@ -40,19 +41,20 @@ rbq_status decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
   const int64_t rows = int64_t(batch) * heads_q;
   if (do_flush)
     s = launch_quantize_flush(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, K_loc, kv_dtype, cap, w, n,
-                              cap, codes, kfac, stream, nullptr, nullptr, 0, kfac16);
+                              cap, codes, kfac, stream, nullptr, nullptr, 0, kfac16, head_dim);
   else
-    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
+    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, 4, head_dim);
   if (s != RBQ_OK) return s;
   const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
   s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   sw.slot_max, tw.hist, rows * kHistPerRow, nullptr, kfac16);
+                   sw.slot_max, tw.hist, rows * kHistPerRow, nullptr, kfac16, 4, head_dim);
   if (s != RBQ_OK) return s;
   s = launch_topp(int32_t(rows), n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
                   score_blocks_per_row(batch, heads_kv, n), sw.masks);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, cap, w,
-                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n));
+                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), nullptr, nullptr,
+                       head_dim);
 }
 
 }  // namespace
@@ -68,7 +70,7 @@ rbq_status rbq_encode_keys_debug(int32_t batch, int32_t heads_kv, int32_t head_d
                                     codes, kfac, flags, ws, ws_bytes);
   if (s != RBQ_OK) return s;
   return launch_encode(batch, heads_kv, keys, keys_dtype, keys_ld, n_new, offset, cap, P, c_q, c_k, codes, kfac,
-                       flags, alpha_out, ws, rot_out, stream);
+                       flags, alpha_out, ws, rot_out, stream, nullptr, head_dim);
 }
 
 rbq_status rbq_encode_keys(int32_t batch, int32_t heads_kv, int32_t head_dim, const void* keys, int32_t keys_dtype,
@@ -84,7 +86,7 @@ rbq_status rbq_quantize_query_debug(int32_t batch, int32_t heads_q, int32_t head
                                     uint32_t* qplanes, float* qscal, float* qrot_out, hipStream_t stream) {
   const rbq_status s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal);
   if (s != RBQ_OK) return s;
-  return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, qrot_out, stream);
+  return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, qrot_out, stream, 4, head_dim);
 }
 
 rbq_status rbq_quantize_query(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
@@ -100,7 +102,7 @@ rbq_status rbq_quantize_query_bits(int32_t batch, int32_t heads_q, int32_t heads
   if (bits < 1 || bits > 8) return RBQ_EINVAL;
   const rbq_status s = check_quantize(batch, heads_q, heads_kv, head_dim, q, P, c_k, qplanes, qscal);
   if (s != RBQ_OK) return s;
-  return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, bits);
+  return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, bits, head_dim);
 }
 
 rbq_status rbq_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
@@ -109,7 +111,7 @@ rbq_status rbq_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t h
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores);
   if (s != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr,
-                      stream);
+                      stream, nullptr, nullptr, 0, nullptr, nullptr, 4, head_dim);
 }
 
 rbq_status rbq_encode_keys_f16(int32_t batch, int32_t heads_kv, int32_t head_dim, const void* keys,
@@ -119,6 +121,7 @@ rbq_status rbq_encode_keys_f16(int32_t batch, int32_t heads_kv, int32_t head_dim
   const rbq_status s = check_encode(batch, heads_kv, head_dim, keys, keys_dtype, keys_ld, n_new, offset, cap, P, c_k,
                                     codes, kfac16, flags, ws, ws_bytes);
   if (s != RBQ_OK) return s;
+  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_encode(batch, heads_kv, keys, keys_dtype, keys_ld, n_new, offset, cap, P, nullptr, c_k, codes,
                        nullptr, flags, nullptr, ws, nullptr, stream, kfac16);
 }
@@ -128,6 +131,7 @@ rbq_status rbq_score_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32
                          float* scores, hipStream_t stream) {
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac16, qplanes, qscal, scores);
   if (s != RBQ_OK) return s;
+  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, qscal, scores, nullptr, nullptr,
                       stream, nullptr, nullptr, 0, nullptr, kfac16);
 }
@@ -137,6 +141,7 @@ rbq_status rbq_score_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
                         float* scores, hipStream_t stream) {
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes8, qscal, scores);
   if (s != RBQ_OK) return s;
+  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes8, qscal, scores, nullptr, nullptr,
                       stream, nullptr, nullptr, 0, nullptr, nullptr, 8);
 }
@@ -147,6 +152,7 @@ rbq_status rbq_score_ints_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, i
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, ip_out, qplanes8, pc_out,
                                    ip_out);
   if (s != RBQ_OK) return s;
+  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes8, nullptr, nullptr, ip_out, pc_out,
                       stream, nullptr, nullptr, 0, nullptr, nullptr, 8);
 }
@@ -158,7 +164,7 @@ rbq_status rbq_score_ints(int32_t batch, int32_t heads_q, int32_t heads_kv, int3
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, ip_out, qplanes, pc_out, ip_out);
   if (s != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, nullptr, nullptr, ip_out, pc_out,
-                      stream);
+                      stream, nullptr, nullptr, 0, nullptr, nullptr, 4, head_dim);
 }
 
 rbq_status rbq_topp_select(int32_t batch, int32_t heads_q, int32_t n, const float* scores, float p, float sm_scale,
@@ -177,7 +183,7 @@ rbq_status rbq_sparse_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, i
                                     sel_count, K_loc, V_loc, loc_ld, w, sm_scale, out, ws, ws_bytes);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, loc_ld,
-                       w, sm_scale, out, lse, ws, true, stream);
+                       w, sm_scale, out, lse, ws, true, stream, nullptr, 0, nullptr, nullptr, head_dim);
 }
 
 rbq_status rbq_dense_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
@@ -188,7 +194,7 @@ rbq_status rbq_dense_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, in
                                     nullptr, K_loc, V_loc, loc_ld, w, sm_scale, out, ws, ws_bytes);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, nullptr, nullptr, K_loc, V_loc, loc_ld, w,
-                       sm_scale, out, lse, ws, false, stream);
+                       sm_scale, out, lse, ws, false, stream, nullptr, 0, nullptr, nullptr, head_dim);
 }
 
 rbq_status rbq_decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
@@ -233,6 +239,7 @@ rbq_status decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32
                          hipStream_t stream) {
   rbq_status s = check_ragged(n, w, cap, seq_n, seq_w);
   if (s != RBQ_OK) return s;
+  if (head_dim == 64) return RBQ_EUNSUPPORTED;   // (ragged batches: D = 128)
   s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, sparse, sel_idx, sel_count, K, V,
                    cap, w, sm_scale, out, ws, ws_bytes);
   if (s != RBQ_OK) return s;
@@ -253,6 +260,7 @@ rbq_status decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, 
   rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, w, cap, seq_n, seq_w)) != RBQ_OK) return s;
+  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   if (seq_p == nullptr || (reinterpret_cast<uintptr_t>(seq_p) & 15u) != 0) return RBQ_EINVAL;
   const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
   if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
@@ -299,6 +307,7 @@ rbq_status rbq_score_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, in
   rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores);
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, 0, cap, seq_n, nullptr)) != RBQ_OK) return s;
+  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr,
                       stream, nullptr, nullptr, 0, seq_n);
 }
@@ -309,6 +318,7 @@ rbq_status rbq_score_varlen_f16(int32_t batch, int32_t heads_q, int32_t heads_kv
   rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac16, qplanes, qscal, scores);
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, 0, cap, seq_n, nullptr)) != RBQ_OK) return s;
+  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, qscal, scores, nullptr, nullptr,
                       stream, nullptr, nullptr, 0, seq_n, kfac16);
 }

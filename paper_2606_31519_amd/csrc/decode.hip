@@ -240,15 +240,15 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// dot products of one K row (bf16 or fp32) with the G scaled queries in LDS
-template <int DT, int G>
-__device__ __forceinline__ void row_dots(const void* rowp, const float (*qs)[kHeadDim], float* dot) {
+// dot products of one K row (bf16 or fp32, D dimensions) with the G scaled queries in LDS
+template <int DT, int G, int D>
+__device__ __forceinline__ void row_dots(const void* rowp, const float (*qs)[D], float* dot) {
 #pragma unroll
   for (int g = 0; g < G; ++g) dot[g] = 0.f;
   if (DT == RBQ_BF16) {
     const u32x4* r = static_cast<const u32x4*>(rowp);
 #pragma unroll 4
-    for (int c = 0; c < kHeadDim / 8; ++c) {
+    for (int c = 0; c < D / 8; ++c) {
       const u32x4 v = r[c];
       const float k0 = bf16_lo(v.x), k1 = bf16_hi(v.x), k2 = bf16_lo(v.y), k3 = bf16_hi(v.y);
       const float k4 = bf16_lo(v.z), k5 = bf16_hi(v.z), k6 = bf16_lo(v.w), k7 = bf16_hi(v.w);
@@ -265,7 +265,7 @@ __device__ __forceinline__ void row_dots(const void* rowp, const float (*qs)[kHe
   } else {
     const f32x4* r = static_cast<const f32x4*>(rowp);
 #pragma unroll 4
-    for (int c = 0; c < kHeadDim / 4; ++c) {
+    for (int c = 0; c < D / 4; ++c) {
       const f32x4 v = r[c];
 #pragma unroll
       for (int g = 0; g < G; ++g) {
@@ -278,8 +278,14 @@ __device__ __forceinline__ void row_dots(const void* rowp, const float (*qs)[kHe
   }
 }
 
-template <int DT>
+// the V values of this lane's output dimensions: 2 lane, 2 lane + 1 at D = 128;
+// dimension `lane` (and a zero) at D = 64
+template <int DT, int D>
 __device__ __forceinline__ f32x2 load_v2(const void* rowp, int lane) {
+  if constexpr (D == 64) {
+    if (DT == RBQ_BF16) return f32x2{bf16_lo(uint32_t(static_cast<const uint16_t*>(rowp)[lane])), 0.f};
+    return f32x2{static_cast<const float*>(rowp)[lane], 0.f};
+  }
   if (DT == RBQ_BF16) {
     const uint32_t v = static_cast<const uint32_t*>(rowp)[lane];
     return f32x2{bf16_lo(v), bf16_hi(v)};
@@ -287,7 +293,8 @@ __device__ __forceinline__ f32x2 load_v2(const void* rowp, int lane) {
   return static_cast<const f32x2*>(rowp)[lane];
 }
 
-template <int DT, bool SPARSE, int G, bool RAGGED>
+// D: head dimension, 128 or 64 (at 64 this kernel also serves bf16 K/V)
+template <int DT, bool SPARSE, int G, bool RAGGED, int D = kHeadDim>
 __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     const float* __restrict__ q, const void* __restrict__ K, const void* __restrict__ V, int cap, int n,
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
@@ -296,7 +303,7 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     int fold_wq, float scale_log2e, float* __restrict__ part, int Hq, int Hkv, const int32_t* __restrict__ seq_n,
     const int32_t* __restrict__ seq_w) {
   constexpr int kElem = DT == RBQ_BF16 ? 2 : 4;
-  __shared__ float qs[G][kHeadDim];
+  __shared__ float qs[G][D];
   __shared__ uint32_t bm[G][kBmAll];
   __shared__ int32_t lst[SPARSE ? kListCap : 1];
   __shared__ uint16_t hmask[SPARSE ? kListCap : 1];
@@ -305,7 +312,7 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   __shared__ int ucount;
   __shared__ float ps[kDWaves][G][kWave];
   __shared__ float sm[kDWaves][G], sl[kDWaves][G];
-  __shared__ float sacc[kDWaves][G][kHeadDim];
+  __shared__ float sacc[kDWaves][G][D];
 
   // (ragged grids are split-major, so the empty splits past short sequences come last)
   const int split = RAGGED ? blockIdx.y : blockIdx.x;
@@ -339,19 +346,19 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     c1 = RAGGED ? max(c0, min(wb, c0 + kDecodeWinChunk)) : min(w, c0 + kDecodeWinChunk);
   }
   if (RAGGED && c1 == c0 && nwin == 0) {   // block-uniform: past this sequence's rows, an empty partial state
-    if (int(threadIdx.x) < G) part[(int64_t(row0 + threadIdx.x) * total_splits + split) * (kHeadDim + 2)] = -INFINITY;
+    if (int(threadIdx.x) < G) part[(int64_t(row0 + threadIdx.x) * total_splits + split) * (D + 2)] = -INFINITY;
     return;
   }
-  const char* Kbase = window ? static_cast<const char*>(K_loc) + (int64_t(bh) * loc_ld + wbase) * kHeadDim * kElem
-                             : static_cast<const char*>(K) + int64_t(bh) * cap * kHeadDim * kElem;
-  const char* Vbase = window ? static_cast<const char*>(V_loc) + (int64_t(bh) * loc_ld + wbase) * kHeadDim * kElem
-                             : static_cast<const char*>(V) + int64_t(bh) * cap * kHeadDim * kElem;
+  const char* Kbase = window ? static_cast<const char*>(K_loc) + (int64_t(bh) * loc_ld + wbase) * D * kElem
+                             : static_cast<const char*>(K) + int64_t(bh) * cap * D * kElem;
+  const char* Vbase = window ? static_cast<const char*>(V_loc) + (int64_t(bh) * loc_ld + wbase) * D * kElem
+                             : static_cast<const char*>(V) + int64_t(bh) * cap * D * kElem;
 
   constexpr bool kPreMask = G <= 4;   // (for larger groups the early load costs registers)
   const unsigned long long mword =
       kPreMask && SPARSE && !window ? load_mask_word<G>(sel_mask, mask_words, row0, c0, c1) : 0ull;
-  for (int e = threadIdx.x; e < G * kHeadDim; e += kDThreads)
-    qs[e / kHeadDim][e % kHeadDim] = q[int64_t(row0) * kHeadDim + e] * scale_log2e;
+  for (int e = threadIdx.x; e < G * D; e += kDThreads)
+    qs[e / D][e % D] = q[int64_t(row0) * D + e] * scale_log2e;
 
   // ---- the list of rows to visit in this split
   const bool use_list = SPARSE && !window;
@@ -390,7 +397,7 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     }
     float dot[G];
     if (valid) {
-      row_dots<DT, G>(Kbase + int64_t(pos) * kHeadDim * kElem, qs, dot);
+      row_dots<DT, G, D>(Kbase + int64_t(pos) * D * kElem, qs, dot);
     } else {
 #pragma unroll
       for (int g = 0; g < G; ++g) dot[g] = 0.f;
@@ -414,7 +421,7 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     const int rows = min(kWave, U - tt * kWave);
     for (int t = 0; t < rows; ++t) {
       const int pt = use_list ? lst[tt * kWave + t] : c0 + tt * kWave + t;
-      const f32x2 v = load_v2<DT>(Vbase + int64_t(pt) * kHeadDim * kElem, lane);
+      const f32x2 v = load_v2<DT, D>(Vbase + int64_t(pt) * D * kElem, lane);
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         const float pr = ps[wave][g][t];
@@ -431,13 +438,17 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
       sm[wave][g] = m[g];
       sl[wave][g] = l[g];
     }
-    sacc[wave][g][2 * lane] = acc[g].x;
-    sacc[wave][g][2 * lane + 1] = acc[g].y;
+    if constexpr (D == 64) {
+      sacc[wave][g][lane] = acc[g].x;
+    } else {
+      sacc[wave][g][2 * lane] = acc[g].x;
+      sacc[wave][g][2 * lane + 1] = acc[g].y;
+    }
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < G * (kHeadDim + 2); e += kDThreads) {
-    const int g = e / (kHeadDim + 2);
-    const int k = e - g * (kHeadDim + 2);
+  for (int e = threadIdx.x; e < G * (D + 2); e += kDThreads) {
+    const int g = e / (D + 2);
+    const int k = e - g * (D + 2);
     float M = -INFINITY;
 #pragma unroll
     for (int v = 0; v < kDWaves; ++v) M = fmaxf(M, sm[v][g]);
@@ -456,7 +467,7 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
         }
       }
     }
-    part[(int64_t(row0 + g) * total_splits + split) * (kHeadDim + 2) + k] = r;
+    part[(int64_t(row0 + g) * total_splits + split) * (D + 2) + k] = r;
   }
 }
 
@@ -798,8 +809,6 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
 // splits with running (max, sum, acc) rescaling, all of a group's loads issued
 // together; the 8 groups are then merged in order (bitwise deterministic).
 constexpr int kCombThreads = 256;
-constexpr int kSliceDims = kHeadDim / kCombSlices;               // 32
-constexpr int kCombGroups = kCombThreads / kSliceDims;           // 8
 constexpr int kCombBatch = 16;                                   // splits per thread per round
 
 __device__ __forceinline__ void lse_merge(float& m, float& l, float& o, float ms, float ls, float os) {
@@ -812,14 +821,18 @@ __device__ __forceinline__ void lse_merge(float& m, float& l, float& o, float ms
   m = mn;
 }
 
+// (D = 128: 32 dimensions per block, 8 groups; D = 64: 16 dimensions, 16 groups)
+template <int D = kHeadDim>
 __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(const float* __restrict__ part, int splits,
                                                                       float* __restrict__ out,
                                                                       float* __restrict__ lse) {
+  constexpr int kSliceDims = D / kCombSlices;
+  constexpr int kCombGroups = kCombThreads / kSliceDims;
   __shared__ float gm[kCombGroups][kSliceDims], gl[kCombGroups][kSliceDims], go[kCombGroups][kSliceDims];
   const int row = blockIdx.x, slice = blockIdx.y;
   const int dl = threadIdx.x % kSliceDims, grp = threadIdx.x / kSliceDims;
   const int d = slice * kSliceDims + dl;
-  const float* pr = part + int64_t(row) * splits * (kHeadDim + 2);
+  const float* pr = part + int64_t(row) * splits * (D + 2);
   float m = -INFINITY, l = 0.f, o = 0.f;
   for (int s0 = grp; s0 < splits; s0 += kCombGroups * kCombBatch) {
     float ms[kCombBatch], ls[kCombBatch], os[kCombBatch];
@@ -827,7 +840,7 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(const floa
     for (int k = 0; k < kCombBatch; ++k) {
       const int s = s0 + kCombGroups * k;
       const bool ok = s < splits;
-      const float* ps = pr + int64_t(ok ? s : 0) * (kHeadDim + 2);
+      const float* ps = pr + int64_t(ok ? s : 0) * (D + 2);
       ms[k] = ok ? ps[0] : -INFINITY;
       ls[k] = ps[1];
       os[k] = ps[2 + d];
@@ -842,12 +855,12 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(const floa
   if (grp == 0) {
 #pragma unroll
     for (int g = 1; g < kCombGroups; ++g) lse_merge(m, l, o, gm[g][dl], gl[g][dl], go[g][dl]);
-    out[int64_t(row) * kHeadDim + d] = l > 0.f ? o / l : 0.f;
+    out[int64_t(row) * D + d] = l > 0.f ? o / l : 0.f;
     if (lse && slice == 0 && dl == 0) lse[row] = l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY;
   }
 }
 
-template <int DT, bool SPARSE, bool RAGGED>
+template <int DT, bool SPARSE, bool RAGGED, int D = kHeadDim>
 rbq_status launch_g(int G, dim3 grid, hipStream_t stream, const float* q, const void* K, const void* V, int cap,
                     int n, const int32_t* sel_idx, const int32_t* sel_count, const unsigned long long* sel_mask,
                     int mask_words, const void* K_loc, const void* V_loc, int64_t loc_ld, int w, int chunk,
@@ -855,13 +868,13 @@ rbq_status launch_g(int G, dim3 grid, hipStream_t stream, const float* q, const 
                     int Hkv, const int32_t* seq_n, const int32_t* seq_w) {
 #define RBQ_DECODE_CASE(GG)                                                                                       \
   case GG:                                                                                                        \
-    if constexpr (DT == RBQ_BF16)                                                                                 \
+    if constexpr (DT == RBQ_BF16 && D == kHeadDim)                                                                \
       decode_mfma_kernel<SPARSE, GG, RAGGED><<<grid, kDThreads, 0, stream>>>(                                     \
           q, static_cast<const uint16_t*>(K), static_cast<const uint16_t*>(V), cap, n, sel_idx, sel_count,        \
           sel_mask, mask_words, static_cast<const uint16_t*>(K_loc), static_cast<const uint16_t*>(V_loc), loc_ld, \
           w, chunk, idx_splits, total, fold_s0, fold_wq, scale_log2e, part, Hq, Hkv, seq_n, seq_w);               \
     else                                                                                                          \
-      decode_vec_kernel<DT, SPARSE, GG, RAGGED><<<grid, kDThreads, 0, stream>>>(                                  \
+      decode_vec_kernel<DT, SPARSE, GG, RAGGED, D><<<grid, kDThreads, 0, stream>>>(                               \
           q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, loc_ld, w, chunk, idx_splits,  \
           total, fold_s0, fold_wq, scale_log2e, part, Hq, Hkv, seq_n, seq_w);                                     \
     break;
@@ -885,8 +898,9 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                          const int32_t* sel_count, const void* K_loc, const void* V_loc, int64_t loc_ld, int32_t w,
                          float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream,
                          const unsigned long long* sel_mask, int32_t mask_words, const int32_t* seq_n,
-                         const int32_t* seq_w) {
+                         const int32_t* seq_w, int32_t head_dim) {
   const int G = heads_q / heads_kv;
+  const int D = head_dim;
   const size_t elem = kv_dtype == RBQ_BF16 ? 2 : 4;
   if (seq_n) {   // ragged: every sequence's window is its own cache tail
     K_loc = K;
@@ -898,9 +912,9 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
   // the window rows are the cache tail when they sit right after the indexed rows of every (b, kv-head)
   const bool tail = n > 0 && w > 0 && loc_ld == cap &&
                     (seq_n != nullptr ||
-                     (static_cast<const char*>(K_loc) == static_cast<const char*>(K) + size_t(n) * kHeadDim * elem &&
-                      static_cast<const char*>(V_loc) == static_cast<const char*>(V) + size_t(n) * kHeadDim * elem)) &&
-                    (int64_t(n) + w) * kHeadDim * int64_t(elem) < (int64_t(1) << 31);
+                     (static_cast<const char*>(K_loc) == static_cast<const char*>(K) + size_t(n) * D * elem &&
+                      static_cast<const char*>(V_loc) == static_cast<const char*>(V) + size_t(n) * D * elem)) &&
+                    (int64_t(n) + w) * D * int64_t(elem) < (int64_t(1) << 31);
   const DecodeSplits sp = decode_splits(batch, heads_kv, n, w, tail, sparse, seq_n != nullptr);
   const dim3 grid = seq_n ? dim3(batch * heads_kv, sp.total()) : dim3(sp.total(), batch * heads_kv);
   float* part = static_cast<float*>(ws);
@@ -911,6 +925,21 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                    w, sp.chunk, sp.idx_splits, sp.total(), sp.fold_s0, sp.fold_wq, scale_log2e, part, heads_q,      \
                    heads_kv, seq_n, seq_w)
   const bool rg = seq_n != nullptr;
+  if (D == 64) {   // uniform batches: the vector kernel for both dtypes
+#define RBQ_DECODE_LAUNCH64(DT, SP)                                                                                 \
+  launch_g<DT, SP, false, 64>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc,    \
+                              V_loc, loc_ld, w, sp.chunk, sp.idx_splits, sp.total(), sp.fold_s0, sp.fold_wq,        \
+                              scale_log2e, part, heads_q, heads_kv, seq_n, seq_w)
+    if (kv_dtype == RBQ_BF16)
+      st = sparse ? RBQ_DECODE_LAUNCH64(RBQ_BF16, true) : RBQ_DECODE_LAUNCH64(RBQ_BF16, false);
+    else
+      st = sparse ? RBQ_DECODE_LAUNCH64(RBQ_F32, true) : RBQ_DECODE_LAUNCH64(RBQ_F32, false);
+#undef RBQ_DECODE_LAUNCH64
+    if (st != RBQ_OK) return st;
+    decode_combine_kernel<64><<<dim3(batch * heads_q, kCombSlices), kCombThreads, 0, stream>>>(part, sp.total(),
+                                                                                                 out, lse);
+    return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
+  }
   if (kv_dtype == RBQ_BF16) {
     if (rg)
       st = sparse ? RBQ_DECODE_LAUNCH(RBQ_BF16, true, true) : RBQ_DECODE_LAUNCH(RBQ_BF16, false, true);
@@ -924,8 +953,8 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
   }
 #undef RBQ_DECODE_LAUNCH
   if (st != RBQ_OK) return st;
-  decode_combine_kernel<<<dim3(batch * heads_q, kCombSlices), kCombThreads, 0, stream>>>(part, sp.total(), out,
-                                                                                           lse);
+  decode_combine_kernel<kHeadDim><<<dim3(batch * heads_q, kCombSlices), kCombThreads, 0, stream>>>(part, sp.total(),
+                                                                                                     out, lse);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

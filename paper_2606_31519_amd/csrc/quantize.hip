@@ -20,12 +20,19 @@
 namespace rbq {
 namespace {
 
-constexpr int kQThreads = kHeadDim;   // one thread per output dimension in the epilogue
-constexpr int kQWaves = kQThreads / kWave;
-constexpr int kQParts = 2;            // the matrix-vector product is split over 2 thread groups
-constexpr int kQAll = kQParts * kQThreads;
+constexpr int kQAll = 256;            // threads per block
+// For head dimension D: one thread per output dimension in the epilogue (the
+// first D threads, the lead group), and the matrix-vector product split over
+// kQAll / D thread groups (2 at D = 128, 4 at D = 64).
+template <int D>
+struct QShape {
+  static constexpr int kQWaves = D / kWave;      // waves of the lead group
+  static constexpr int kQParts = kQAll / D;
+};
+constexpr int kQWavesMax = kHeadDim / kWave;
 
 // reductions over the first kQWaves waves (the other waves take part in the barriers only)
+template <int kQWaves>
 __device__ __forceinline__ float block_sum(float v, float* red) {
   v = wave_sum(v);
   const int w = threadIdx.x / kWave;
@@ -51,6 +58,7 @@ __device__ __forceinline__ float block_sum_all(float v, float* red) {
   return s;
 }
 
+template <int kQWaves>
 __device__ __forceinline__ float block_min(float v, float* red) {
   v = wave_min(v);
   const int w = threadIdx.x / kWave;
@@ -63,6 +71,7 @@ __device__ __forceinline__ float block_min(float v, float* red) {
   return s;
 }
 
+template <int kQWaves>
 __device__ __forceinline__ float block_max(float v, float* red) {
   v = wave_max(v);
   const int w = threadIdx.x / kWave;
@@ -99,7 +108,10 @@ struct QuantArgs {
 };
 
 // query head `row` (= b * Hq + h), by the kQAll threads of the calling block
+template <int D>
 __device__ __forceinline__ void quantize_row(const QuantArgs& qa, int row) {
+  constexpr int kQWaves = QShape<D>::kQWaves, kQParts = QShape<D>::kQParts;
+  constexpr int W = D / 32;                    // words per bit-plane
   const float* __restrict__ q = qa.q;
   const float* __restrict__ P = qa.P;
   const float* __restrict__ c_q = qa.c_q;
@@ -108,26 +120,26 @@ __device__ __forceinline__ void quantize_row(const QuantArgs& qa, int row) {
   float* __restrict__ qscal = qa.qscal;
   float* __restrict__ qrot_out = qa.qrot_out;
   const int Hq = qa.Hq, Hkv = qa.Hkv;
-  __shared__ float u_s[kHeadDim];
-  __shared__ float part_s[kQParts][kHeadDim];
-  __shared__ float red[2 * (kQAll / kWave) + 2 * kQWaves];
+  __shared__ float u_s[D];
+  __shared__ float part_s[kQParts][D];
+  __shared__ float red[2 * (kQAll / kWave) + 2 * kQWavesMax];
   const int b = row / Hq;
   const int h = row - b * Hq;
   const int grp = b * Hkv + h / (Hq / Hkv);    // (b, kv head)
-  const int j = threadIdx.x % kHeadDim;        // output dimension
-  const int part = threadIdx.x / kHeadDim;     // which quarter of the input dimensions
+  const int j = threadIdx.x % D;               // output dimension
+  const int part = threadIdx.x / D;            // which share of the input dimensions
 
-  // this group's 64 rows of P, requested before anything else (they do not depend on q)
-  constexpr int kRows = kHeadDim / kQParts;
+  // this group's D / kQParts rows of P, requested before anything else (they do not depend on q)
+  constexpr int kRows = D / kQParts;
   float pv[kRows];
 #pragma unroll
-  for (int k = 0; k < kRows; ++k) pv[k] = P[(part * kRows + k) * kHeadDim + j];
+  for (int k = 0; k < kRows; ++k) pv[k] = P[(part * kRows + k) * D + j];
 
   float qj = 0.f, y = 0.f, ck = 0.f;
   if (part == 0) {
-    qj = q[int64_t(row) * kHeadDim + j];
-    const float cq = c_q ? c_q[int64_t(grp) * kHeadDim + j] : 0.f;
-    ck = c_k[int64_t(grp) * kHeadDim + j];
+    qj = q[int64_t(row) * D + j];
+    const float cq = c_q ? c_q[int64_t(grp) * D + j] : 0.f;
+    ck = c_k[int64_t(grp) * D + j];
     y = qj - cq;
   }
   // the first two waves hold the vector; the block sums include zeros from the others
@@ -136,37 +148,39 @@ __device__ __forceinline__ void quantize_row(const QuantArgs& qa, int row) {
   if (part == 0) u_s[j] = A > 0.f ? y / A : 0.f;
   __syncthreads();
 
-  // q'[j] = sum_d P[d][j] u[d]: each group takes 64 rows of P (loaded above)
+  // q'[j] = sum_d P[d][j] u[d]: each group takes kRows rows of P (loaded above)
   float acc = 0.f;
 #pragma unroll
   for (int k = 0; k < kRows; ++k) acc = fmaf(pv[k], u_s[part * kRows + k], acc);
   part_s[part][j] = acc;
   __syncthreads();
-  // every thread computes the sum; only the first 128 (two waves) use it
-  acc = part_s[0][j] + part_s[1][j];
+  // every thread computes the sum (in a fixed order); only the lead group uses it
+  acc = part_s[0][j];
+#pragma unroll
+  for (int t = 1; t < kQParts; ++t) acc += part_s[t][j];
   const bool lead = part == 0;
-  if (qrot_out && lead) qrot_out[int64_t(row) * kHeadDim + j] = acc;
+  if (qrot_out && lead) qrot_out[int64_t(row) * D + j] = acc;
 
-  const float ql = block_min(acc, red + 2 * (kQAll / kWave));
-  const float qr = block_max(acc, red + 2 * (kQAll / kWave) + kQWaves);
+  const float ql = block_min<kQWaves>(acc, red + 2 * (kQAll / kWave));
+  const float qr = block_max<kQWaves>(acc, red + 2 * (kQAll / kWave) + kQWavesMax);
   float delta;
   {
 #pragma clang fp contract(off)
     delta = __fdiv_rn(__fsub_rn(qr, ql), float(qa.levels));
   }
   const int code = quant_code(acc, ql, delta, float(qa.levels));
-  const float su = block_sum(float(code), red);   // exact: integers below 2^24
+  const float su = block_sum<kQWaves>(float(code), red);   // exact: integers below 2^24
 
   // bit-plane m, 64 dimensions per wave: low 32 lanes -> word 2w, high -> 2w + 1
   const int w = j / kWave;
-  uint32_t* planes = qplanes + int64_t(row) * qa.planes * kWords;
+  uint32_t* planes = qplanes + int64_t(row) * qa.planes * W;
 #pragma unroll
   for (int m = 0; m < 8; ++m) {
     if (m >= qa.planes) break;
     const uint64_t bal = __ballot((code >> m) & 1);
     if (lead && lane_id() == 0) {
-      planes[m * kWords + 2 * w] = uint32_t(bal);
-      planes[m * kWords + 2 * w + 1] = uint32_t(bal >> 32);
+      planes[m * W + 2 * w] = uint32_t(bal);
+      planes[m * W + 2 * w + 1] = uint32_t(bal >> 32);
     }
   }
   if (lead && j < RBQ_QSCAL_STRIDE) {
@@ -181,20 +195,21 @@ __device__ __forceinline__ void quantize_row(const QuantArgs& qa, int row) {
   }
 }
 
-__global__ __launch_bounds__(kQAll) void quantize_kernel(QuantArgs qa) { quantize_row(qa, blockIdx.x); }
+template <int D>
+__global__ __launch_bounds__(kQAll) void quantize_kernel(QuantArgs qa) { quantize_row<D>(qa, blockIdx.x); }
 
 // One launch for the query quantisation and the lazy index update of the
 // decode step (they are independent): blocks [0, rows) quantise one query
 // head each, the others encode the window keys as encode_kernel would.
 static_assert(kQAll == kEncThreads, "both roles run on blocks of the same size");
-template <int DT, bool RAGGED>
+template <int DT, bool RAGGED, int D = kHeadDim>
 __global__ __launch_bounds__(kQAll) void quantize_flush_kernel(QuantArgs qa, EncodeArgs ea, int rows, int per_head) {
   const int blk = blockIdx.x;
   if (blk < rows) {
-    quantize_row(qa, blk);
+    quantize_row<D>(qa, blk);
   } else {
     const int e = blk - rows;
-    encode_tiles<DT, false, RAGGED>(ea, e / per_head, e % per_head, per_head);
+    encode_tiles<DT, false, RAGGED, D>(ea, e / per_head, e % per_head, per_head);
   }
 }
 
@@ -202,9 +217,12 @@ __global__ __launch_bounds__(kQAll) void quantize_flush_kernel(QuantArgs qa, Enc
 
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
-                           hipStream_t stream, int32_t bits) {
+                           hipStream_t stream, int32_t bits, int32_t head_dim) {
   const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, qrot_out, heads_q, heads_kv, (1 << bits) - 1, bits > 4 ? 8 : 4};
-  quantize_kernel<<<batch * heads_q, kQAll, 0, stream>>>(qa);
+  if (head_dim == 64)
+    quantize_kernel<64><<<batch * heads_q, kQAll, 0, stream>>>(qa);
+  else
+    quantize_kernel<kHeadDim><<<batch * heads_q, kQAll, 0, stream>>>(qa);
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 
@@ -212,9 +230,9 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
                                  const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal,
                                  const void* keys, int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset,
                                  int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream, const int32_t* seq_off,
-                                 const int32_t* seq_cnt, int32_t off_max, uint16_t* kfac16) {
+                                 const int32_t* seq_cnt, int32_t off_max, uint16_t* kfac16, int32_t head_dim) {
   if (n_new == 0)
-    return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
+    return launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, 4, head_dim);
   const QuantArgs qa{q, P, c_q, c_k, qplanes, qscal, nullptr, heads_q, heads_kv, 15, 4};
   const EncodeArgs ea{keys,  keys_ld, n_new,   offset,  cap,     P,       c_q,     c_k,     codes,
                       kfac,  nullptr, nullptr, seq_off, seq_cnt, off_max, heads_kv, kfac16};
@@ -222,6 +240,13 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
   const int per_head = encode_blocks_per_head(n_new, bhs);
   const int blocks = rows + per_head * bhs;
   const bool rg = seq_off != nullptr;
+  if (head_dim == 64) {   // (uniform batches only)
+    if (keys_dtype == RBQ_BF16)
+      quantize_flush_kernel<RBQ_BF16, false, 64><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+    else
+      quantize_flush_kernel<RBQ_F32, false, 64><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+    return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
+  }
   if (keys_dtype == RBQ_BF16) {
     if (rg)
       quantize_flush_kernel<RBQ_BF16, true><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);

@@ -109,12 +109,13 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 rbq_status launch_encode(int32_t batch, int32_t heads_kv, const void* keys, int32_t keys_dtype, int64_t keys_ld,
                          int32_t n_new, int32_t offset, int32_t cap, const float* P, const float* c_q, float* c_k,
                          uint32_t* codes, float* kfac, uint32_t flags, float* alpha_out, void* ws,
-                         float* rot_out, hipStream_t stream, uint16_t* kfac16 = nullptr);
+                         float* rot_out, hipStream_t stream, uint16_t* kfac16 = nullptr,
+                         int32_t head_dim = kHeadDim);
 // (kfac16: the compact index's fp16 factors, written instead of kfac when non-NULL)
 // bits: B_q, the query's quantisation bits (1..8; 4 bit-planes per head up to 4 bits, 8 above)
 rbq_status launch_quantize(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const float* P,
                            const float* c_q, const float* c_k, uint32_t* qplanes, float* qscal, float* qrot_out,
-                           hipStream_t stream, int32_t bits = 4);
+                           hipStream_t stream, int32_t bits = 4, int32_t head_dim = kHeadDim);
 // query quantisation and, in the same launch, the lazy encode of n_new window
 // keys into index rows [offset, offset + n_new) with the existing c_k (ragged,
 // seq_off != NULL: sequence b encodes min(seq_cnt[b], n_new) keys (n_new without
@@ -125,7 +126,7 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
                                  const void* keys, int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset,
                                  int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream,
                                  const int32_t* seq_off = nullptr, const int32_t* seq_cnt = nullptr,
-                                 int32_t off_max = 0, uint16_t* kfac16 = nullptr);
+                                 int32_t off_max = 0, uint16_t* kfac16 = nullptr, int32_t head_dim = kHeadDim);
 // slot_max (fused decode step): [B * Hq][score_blocks_per_row()] block maxima of the
 // scores, with hist[0, hist_words) zeroed by the same launch; NULL otherwise.
 // seq_n (ragged batches): [B] indexed keys per sequence, clamped to [0, n]; n is the row stride
@@ -133,7 +134,8 @@ rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream,
                         float* slot_max = nullptr, unsigned long long* hist = nullptr, int64_t hist_words = 0,
-                        const int32_t* seq_n = nullptr, const uint16_t* kfac16 = nullptr, int32_t planes = 4);
+                        const int32_t* seq_n = nullptr, const uint16_t* kfac16 = nullptr, int32_t planes = 4,
+                        int32_t head_dim = kHeadDim);
 // (kfac16: the compact index's fp16 factors [B][Hkv][cap], read instead of kfac when non-NULL; g = 0.
 //  planes: query bit-planes per head, 4 or 8 (8: B_q up to 8; uniform, unfused calls only))
 // slot_max / nslots: per-row partial maxima written by launch_score together with
@@ -149,7 +151,8 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                          const int32_t* sel_count, const void* K_loc, const void* V_loc, int64_t loc_ld, int32_t w,
                          float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream,
                          const unsigned long long* sel_mask = nullptr, int32_t mask_words = 0,
-                         const int32_t* seq_n = nullptr, const int32_t* seq_w = nullptr);
+                         const int32_t* seq_n = nullptr, const int32_t* seq_w = nullptr,
+                         int32_t head_dim = kHeadDim);
 // (ragged: seq_n / seq_w [B] indexed and window rows per sequence, the window
 // being the sequence's cache tail; K_loc, V_loc and loc_ld are then ignored)
 

@@ -102,9 +102,11 @@ struct ScoreSlots {
 // FAC16: the compact index, one fp16 factor f per key (g = 0) instead of (f, g) in fp32.
 // QB: bit-planes per query head, 4 (B_q <= 4) or 8 (B_q <= 8: the code is split
 // into its low and high nibbles, ip = ip_lo + 16 ip_hi, two dot8 chains).
-template <int KPT, bool INTS, bool SLOTS, bool RAGGED, bool FAC16, int QB = 4>
+// D: head dimension, 128 or 64 (64: the two code words per key and per query
+// plane are padded with zero words, which add nothing to ip or pc).
+template <int KPT, bool INTS, bool SLOTS, bool RAGGED, bool FAC16, int QB = 4, int D = kHeadDim>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(
-    const u32x4* __restrict__ codes, const f32x2* __restrict__ kfac, const uint16_t* __restrict__ kfac16,
+    const uint32_t* __restrict__ codes, const f32x2* __restrict__ kfac, const uint16_t* __restrict__ kfac16,
     const uint32_t* __restrict__ qplanes, const float* __restrict__ qscal, float* __restrict__ scores,
     int32_t* __restrict__ ip_out, int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G,
     ScoreSlots sl, const int32_t* __restrict__ seq_n) {
@@ -138,7 +140,12 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
 #pragma unroll
   for (int u = 0; u < KPT; ++u) {
     const int i = min(i0 + u * kScoreThreads, nb - 1);    // keys past nb are computed but never stored
-    c[u] = __builtin_nontemporal_load(codes + kbase + i);
+    if (D == 128) {
+      c[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(codes) + kbase + i);
+    } else {
+      const u32x2 c2 = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(codes) + kbase + i);
+      c[u] = u32x4{c2.x, c2.y, 0u, 0u};
+    }
     if (!INTS && FAC16) fh[u] = __builtin_nontemporal_load(kfac16 + kbase + i);
     if (!INTS && !FAC16) fg[u] = __builtin_nontemporal_load(kfac + kbase + i);
   }
@@ -150,13 +157,15 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   clear_counters();
   const bool full = (blockIdx.x + 1) * (kScoreThreads * KPT) <= nb;   // block-uniform: no key past nb
   if (threadIdx.x < 4 * G) {                  // one lane per (head, word)
+    constexpr int W = D / 32;                   // code words per key
     const int h = threadIdx.x >> 2, w = threadIdx.x & 3;
-    const uint32_t* Q = qplanes + int64_t(row0 + h) * QW + w;   // [plane][word]
+    const uint32_t* Q = qplanes + int64_t(row0 + h) * (QB * W) + w;   // [plane][word]
+    const bool in = w < W;                      // (D = 64: words 2 and 3 are zero padding)
     uint32_t o[4];
-    planes_to_nibbles(Q[0], Q[4], Q[8], Q[12], o);
+    planes_to_nibbles(in ? Q[0] : 0u, in ? Q[W] : 0u, in ? Q[2 * W] : 0u, in ? Q[3 * W] : 0u, o);
     *reinterpret_cast<u32x4*>(&qn_s[h][4 * w]) = u32x4{o[0], o[1], o[2], o[3]};
     if (QB == 8) {                              // planes 4..7: the high nibbles
-      planes_to_nibbles(Q[16], Q[20], Q[24], Q[28], o);
+      planes_to_nibbles(in ? Q[4 * W] : 0u, in ? Q[5 * W] : 0u, in ? Q[6 * W] : 0u, in ? Q[7 * W] : 0u, o);
       *reinterpret_cast<u32x4*>(&qn_s[h][16 + 4 * w]) = u32x4{o[0], o[1], o[2], o[3]};
     }
   }
@@ -165,7 +174,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
 #pragma unroll
   for (int u = 0; u < KPT; ++u) {
     const int pc = __popc(c[u].x) + __popc(c[u].y) + __popc(c[u].z) + __popc(c[u].w);
-    pcm[u] = 2 * pc - kHeadDim;
+    pcm[u] = 2 * pc - D;
     e[u] = spread_code(c[u]);
     if (INTS) {
       const int i = i0 + u * kScoreThreads;
@@ -240,24 +249,24 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
 }
 
-template <bool INTS, bool SLOTS, bool RAGGED, bool FAC16 = false, int QB = 4>
+template <bool INTS, bool SLOTS, bool RAGGED, bool FAC16 = false, int QB = 4, int D = kHeadDim>
 rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
                       const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal, float* scores,
                       int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
                       const int32_t* seq_n) {
-  const u32x4* c4 = reinterpret_cast<const u32x4*>(codes);
+  const uint32_t* c4 = codes;
   const f32x2* f2 = reinterpret_cast<const f32x2*>(kfac);
   switch (kpt) {
     case 4:
-      score_kernel<4, INTS, SLOTS, RAGGED, FAC16, QB><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
+      score_kernel<4, INTS, SLOTS, RAGGED, FAC16, QB, D><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
                                                                        n, cap, Hq, Hkv, G, sl, seq_n);
       break;
     case 2:
-      score_kernel<2, INTS, SLOTS, RAGGED, FAC16, QB><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
+      score_kernel<2, INTS, SLOTS, RAGGED, FAC16, QB, D><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
                                                                        n, cap, Hq, Hkv, G, sl, seq_n);
       break;
     default:
-      score_kernel<1, INTS, SLOTS, RAGGED, FAC16, QB><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
+      score_kernel<1, INTS, SLOTS, RAGGED, FAC16, QB, D><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
                                                                        n, cap, Hq, Hkv, G, sl, seq_n);
       break;
   }
@@ -270,7 +279,7 @@ rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, float* slot_max,
                         unsigned long long* hist, int64_t hist_words, const int32_t* seq_n,
-                        const uint16_t* kfac16, int32_t planes) {
+                        const uint16_t* kfac16, int32_t planes, int32_t head_dim) {
   if (n == 0) return RBQ_OK;
   const int G = heads_q / heads_kv;
   const int kpt = score_keys_per_lane(batch, heads_kv, n);
@@ -280,6 +289,19 @@ rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
   launch_kpt<I, S, R, F>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, cap, \
                          heads_q, heads_kv, G, sl, seq_n)
 #define RBQ_SCORE_FAC(S, R) (kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, S, R, true) : RBQ_SCORE_LAUNCH(false, S, R, false))
+  if (head_dim == 64) {   // D = 64: the uniform calls (integer hook, standalone, fused step), fp32 factors
+    if (ip_out != nullptr)
+      return launch_kpt<true, false, false, false, 4, 64>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal,
+                                                          scores, ip_out, pc_out, n, cap, heads_q, heads_kv, G, sl,
+                                                          seq_n);
+    return slot_max != nullptr
+               ? launch_kpt<false, true, false, false, 4, 64>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal,
+                                                              scores, ip_out, pc_out, n, cap, heads_q, heads_kv, G,
+                                                              sl, seq_n)
+               : launch_kpt<false, false, false, false, 4, 64>(kpt, grid, stream, codes, kfac, kfac16, qplanes,
+                                                               qscal, scores, ip_out, pc_out, n, cap, heads_q,
+                                                               heads_kv, G, sl, seq_n);
+  }
   if (planes == 8) {   // 8-plane queries: the standalone call only (integer hook included)
     if (ip_out != nullptr)
       return launch_kpt<true, false, false, false, 8>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores,

@@ -20,7 +20,7 @@ rbq_status check_heads(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
   if (int64_t(batch) * heads_q > 65535 * int64_t(1024)) return RBQ_EINVAL;
   if (int64_t(batch) * heads_kv > 65535) return RBQ_EINVAL;   // grid.y of the per-(b, kv-head) kernels
   if (heads_q / heads_kv > 16) return RBQ_EUNSUPPORTED;       // GQA group size handled by the kernels
-  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
+  if (head_dim != kHeadDim && head_dim != 64) return RBQ_EUNSUPPORTED;   // D = 128, and 64 for the uniform calls
   return RBQ_OK;
 }
 

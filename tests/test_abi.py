@@ -86,7 +86,7 @@ def test_invalid_arguments_are_rejected_on_the_host(lib):
     assert enc(flags=1, ws=None) == EINVAL
     assert enc(flags=1, wsb=16) == EINVAL
     assert enc(dt=7) == EUNSUP
-    assert enc(D=64) == EUNSUP
+    assert enc(D=96) == EUNSUP
     assert enc(D=100) == EINVAL
     assert enc(ld=5) == EINVAL
     assert enc(B=0) == EINVAL
@@ -205,3 +205,30 @@ def test_compact_index_calls_reject_invalid_arguments_on_the_host(lib):
                                        FAKE, None, 1, FAKE, 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
                                        1 << 30, 0)
     assert stv == EINVAL                             # no factor array
+
+
+def test_head_dim_64_is_rejected_where_it_is_not_built(lib):
+    """D = 64 runs the uniform calls; the ragged, compact-index and 8-plane calls
+    return RBQ_EUNSUPPORTED for it, before anything is launched."""
+    L = lib.lib
+    EUNSUP = lib.RBQ_EUNSUPPORTED
+    assert L.rbq_score_varlen(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
+    assert L.rbq_score_varlen_f16(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
+    assert L.rbq_sparse_decode_varlen(1, 8, 4, 64, FAKE, FAKE, FAKE, 1, 200, 100, 10, FAKE, None, FAKE, FAKE, 0.1,
+                                      FAKE, None, FAKE, 1 << 30, 0) == EUNSUP
+    assert L.rbq_dense_decode_varlen(1, 8, 4, 64, FAKE, FAKE, FAKE, 1, 200, 100, 10, FAKE, None, 0.1, FAKE, None,
+                                     FAKE, 1 << 30, 0) == EUNSUP
+    assert L.rbq_decode_step_varlen(1, 8, 4, 64, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1, 200, 100, 10, FAKE, None,
+                                    FAKE, FAKE, 1, FAKE, 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+                                    1 << 30, 0) == EUNSUP
+    assert L.rbq_encode_keys_f16(1, 1, 64, FAKE, 1, 10, 10, 0, 10, FAKE, FAKE, FAKE, FAKE, 0, FAKE, 1 << 20,
+                                 0) == EUNSUP
+    assert L.rbq_score_f16(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
+    assert L.rbq_decode_step_f16(1, 8, 4, 64, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 200, 100, 10, FAKE, FAKE, 1, 0.9,
+                                 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, 0) == EUNSUP
+    assert L.rbq_score_q8(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
+    assert L.rbq_score_ints_q8(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
+    # and the uniform calls still validate their arguments at D = 64
+    assert L.rbq_score(1, 8, 4, 64, 11, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == lib.RBQ_EINVAL
+    assert lib.rbq_workspace_bytes(lib.RBQ_OP_DECODE_STEP, 1, 8, 4, 64, 1000, 16) < \
+        lib.rbq_workspace_bytes(lib.RBQ_OP_DECODE_STEP, 1, 8, 4, 128, 1000, 16)

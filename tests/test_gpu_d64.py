@@ -1,0 +1,167 @@
+"""Head dimension 64 (the D = 64 shape of the paper's kernel ablation) through
+the C ABI, uniform batches: every stage against the oracle, and the fused step
+against the separate calls.
+
+  * rbq_encode_keys (debug form): the codes are the signs of the GPU's fp32
+    rotation (bit-exact), which is within 1e-5 ||x|| of the oracle's; factors,
+    alpha and the centroid within 1e-5 relative;
+  * rbq_quantize_query (debug form): INT4 codes decided from the GPU's rotated
+    query, bit-exact; the integer dot products of rbq_score_ints bit-exact;
+    the scores within the score tolerance;
+  * rbq_sparse_decode / rbq_dense_decode (bf16 and fp32 K/V, G = 1, 4, 8, with a
+    window) against the oracle's attention;
+  * rbq_decode_step against the five calls, bitwise, and its Top-p sets against
+    the oracle on the same scores.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import rbq_oracle as orc
+from workloads import gen
+import parity_util as pu
+
+pytestmark = pytest.mark.gpu
+D = 64
+
+
+@pytest.fixture(scope="module")
+def R():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2606_31519_amd import rbq
+    return rbq
+
+
+@pytest.fixture(scope="module")
+def pipeline(R):
+    from paper_2606_31519_amd import pipeline as pl
+    return pl
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+@pytest.mark.parametrize("kv_dtype,n", [("bf16", 1000), ("f32", 257), ("bf16", 1)])
+def test_d64_encode_stagewise(R, pipeline, kv_dtype, n):
+    print("d64 encode", kv_dtype, n, flush=True)
+    wl = gen.random_case(2, 4, 2, n, D=D, seed=n + 64, kv_dtype=kv_dtype, c_q_scale=0.5, key_offset=2.0)
+    st = pipeline.DecodeState.from_workload(wl)
+    rot = torch.empty(2, 2, n, D, device="cuda")
+    alpha = torch.empty(2, 2, n, device="cuda")
+    st.build_index(rot_out=rot, alpha_out=alpha)
+    torch.cuda.synchronize()
+    for b in range(2):
+        for hk in range(2):
+            K = wl.K_f32(b, hk, slice(0, n)).astype(np.float64)
+            ck = _np(st.c_k[b, hk]).astype(np.float64)
+            assert np.abs(ck - orc.key_centroid(K)).max() <= 1e-5 * (np.abs(K).mean() + 1.0)
+            enc = orc.encode_keys(K, wl.P, c_k=ck, c_q=wl.c_q[b, hk])
+            codes = pu.u32(st.codes[b, hk, :n])
+            r = _np(rot[b, hk]).astype(np.float64)
+            assert np.array_equal(codes, orc.pack_bits(orc.sign_bits(r)))
+            nrm = enc["norm"]
+            assert np.all(np.abs(r - enc["R"]) <= 1e-5 * nrm[:, None] + 1e-30)
+            kfac = _np(st.kfac[b, hk, :n]).astype(np.float64)
+            assert np.all(np.abs(kfac[:, 0] - enc["f"]) <= 1e-5 * np.abs(enc["f"]) + 1e-6)
+            gscale = np.abs(wl.c_q[b, hk]).sum() * np.abs(enc["X"]).max(axis=1)
+            assert np.all(np.abs(kfac[:, 1] - enc["g"]) <= 1e-5 * gscale + 1e-6)
+            a = _np(alpha[b, hk]).astype(np.float64)
+            assert np.all(np.abs(a - enc["alpha"]) <= 1e-5 * enc["alpha"] + 1e-7)
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n", [(1, 4, 1, 4097), (2, 8, 2, 31), (1, 32, 8, 1000)])
+def test_d64_quantize_and_score(R, pipeline, B, Hq, Hkv, n):
+    print("d64 score", B, Hq, Hkv, n, flush=True)
+    wl = gen.random_case(B, Hq, Hkv, n, D=D, seed=Hq + n, kv_dtype="bf16", c_q_scale=0.3, key_offset=1.0)
+    st = pipeline.DecodeState.from_workload(wl)
+    st.build_index()
+    qrot = torch.empty(B, Hq, D, device="cuda")
+    st.quantize(qrot_out=qrot)
+    st.score()
+    ip = torch.zeros(B, Hq, n, dtype=torch.int32, device="cuda")
+    pc = torch.zeros(B, Hkv, n, dtype=torch.int32, device="cuda")
+    R.rbq_score_ints(B, Hq, Hkv, D, n, st.cap, st.codes, st.qplanes, ip, pc)
+    torch.cuda.synchronize()
+    planes, qs, qr = pu.u32(st.qplanes), _np(st.qscal), _np(qrot)
+    codes, kfac, S = pu.u32(st.codes), _np(st.kfac), _np(st.scores)
+    G = Hq // Hkv
+    for b in range(B):
+        for h in range(Hq):
+            z = orc.uniform_quantize(qr[b, h], dtype=np.float32)
+            qc = pu.planes_to_codes(planes[b, h])
+            assert np.array_equal(qc, z["codes"])
+            assert qs[b, h, 0] == np.float32(z["ql"]) and qs[b, h, 1] == np.float32(z["delta"])
+            assert qs[b, h, 2] == z["s_u"]
+            ref = orc.quantize_query(wl.q[b, h], wl.P, wl.c_q[b, h // G], _np(st.c_k[b, h // G]).astype(np.float64))
+            assert abs(qs[b, h, 3] - ref["A"]) <= 1e-5 * ref["A"]
+            bits = orc.unpack_bits(codes[b, h // G, :n], D)
+            ip_or, pc_or = orc.int_dot(bits, qc)
+            assert np.array_equal(_np(ip)[b, h], ip_or) and np.array_equal(_np(pc)[b, h // G], pc_or)
+            pu.check_scores(S[b, h, :n], codes[b, h // G, :n], kfac[b, h // G, :n].astype(np.float64),
+                            planes[b, h], qs[b, h], D=D)
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("G", [1, 4, 8])
+def test_d64_sparse_and_dense_decode(R, pipeline, kv_dtype, G):
+    Hkv, n, w = 2, 3000, 40
+    print("d64 decode", kv_dtype, G, flush=True)
+    wl = gen.random_case(2, G * Hkv, Hkv, n, D=D, seed=G + 5, kv_dtype=kv_dtype, w=w, q_scale=4.0)
+    st = pipeline.DecodeState.from_workload(wl)
+    rng = np.random.default_rng(G)
+    sel = np.zeros((2, G * Hkv, n), np.int32)
+    cnt = np.zeros((2, G * Hkv), np.int32)
+    for b in range(2):
+        for h in range(G * Hkv):
+            k = int(rng.integers(0, n // 3))
+            s = np.sort(rng.choice(n, k, replace=False)).astype(np.int32)
+            sel[b, h, :k], cnt[b, h] = s, k
+    st.sel_idx.copy_(torch.from_numpy(sel))
+    st.sel_count.copy_(torch.from_numpy(cnt))
+    st.sparse_decode()
+    d_out, d_lse = torch.empty_like(st.out), torch.empty_like(st.lse)
+    st.dense_decode(d_out, d_lse)
+    torch.cuda.synchronize()
+    out, lse, dout, dlse = _np(st.out), _np(st.lse), _np(d_out), _np(d_lse)
+    tau = 1.0 / math.sqrt(D)
+    for b in range(2):
+        for h in range(G * Hkv):
+            K = wl.K_f32(b, h // G).astype(np.float64)
+            V = wl.V_f32(b, h // G).astype(np.float64)
+            win = np.arange(n, n + w)
+            q = wl.q[b, h].astype(np.float64)
+            pu.check_attention(out[b, h], float(lse[b, h]), q, K, V, sel[b, h, :cnt[b, h]], K[win], V[win], tau)
+            pu.check_attention(dout[b, h], float(dlse[b, h]), q, K, V, np.arange(n), K[win], V[win], tau)
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "f32"])
+def test_d64_step_matches_calls_and_oracle(R, pipeline, kv_dtype):
+    print("d64 step", kv_dtype, flush=True)
+    wl = gen.random_case(2, 8, 2, 6000, D=D, seed=91, kv_dtype=kv_dtype, w=64, c_q_scale=0.3, q_scale=6.0)
+    a = pipeline.DecodeState.from_workload(wl)
+    b = pipeline.DecodeState.from_workload(wl)
+    p = 0.9
+    for st in (a, b):
+        st.build_index()
+    a.step(p)
+    b.step_calls(p)
+    torch.cuda.synchronize()
+    for name in ("qplanes", "qscal", "scores", "sel_count", "out", "lse", "codes", "kfac"):
+        x, y = _np(getattr(a, name)), _np(getattr(b, name))
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8)), name
+    cnt, sel_a, sel_b, S = _np(a.sel_count), _np(a.sel_idx), _np(b.sel_idx), _np(a.scores)
+    tau = 1.0 / math.sqrt(D)
+    G = wl.Hq // wl.Hkv
+    for bb in range(wl.B):
+        for h in range(wl.Hq):
+            s = sel_a[bb, h, :cnt[bb, h]]
+            assert np.array_equal(s, sel_b[bb, h, :cnt[bb, h]])
+            pu.check_topp(S[bb, h, :wl.n_index], p, tau, s)
+            K = wl.K_f32(bb, h // G).astype(np.float64)
+            V = wl.V_f32(bb, h // G).astype(np.float64)
+            win = np.arange(wl.n_index, wl.n_index + wl.w)
+            pu.check_attention(_np(a.out[bb, h]), float(_np(a.lse[bb, h])), wl.q[bb, h].astype(np.float64),
+                               K, V, s, K[win], V[win], tau)
