@@ -20,6 +20,7 @@ sweep (p = 0.8 / 0.9 / 0.95 / 0.99: step time, budget, KV-group union), the
 standalone score scan of the wide-head workload, a ragged serving batch (16
 sequences of mixed length, window and p) against its dense decode, the
 attention recall of the selections against exact and fixed-budget Top-k, the
+same step on the compact fp16-factor index and at head dimension 64, the
 same step with the K/V cache in host memory (read over PCIe), the
 time-to-first-token cost of the index build beside a prefill attention, and
 the oracle's CPU rate.
@@ -408,6 +409,42 @@ def quality(pipeline, torch, st, p_list, seed=20261):
     return out
 
 
+def time_d64(pipeline, gen, torch, steps, warmup, replicas=4):
+    """The 128K step at head dimension 64 (config 3's generator at D = 64):
+    rbq_decode_step per p against the dense decode of the same rows, and the
+    score call alone. At D = 64 the attention runs on the vector split-K kernel."""
+    wl = gen.config3_d64()
+    st = pipeline.DecodeState.from_workload(wl)
+    st.build_index()
+    torch.cuda.synchronize()
+    reps = [st] + [_clone_state(st, pipeline) for _ in range(replicas - 1)]
+    d_out, d_lse = torch.empty_like(st.out), torch.empty_like(st.lse)
+    gs = [_graph(torch, lambda r=r: r.dense_decode(d_out, d_lse)) for r in reps]
+    ms_dense = _time_graphs(torch, gs, steps, warmup)
+    del gs
+    out = {}
+    for p in wl.p_sweep:
+        gs = [_graph(torch, lambda r=r, p=p: r.step(p)) for r in reps]
+        ms = _time_graphs(torch, gs, steps, warmup)
+        del gs
+        st.step(p)
+        torch.cuda.synchronize()
+        cnt = st.sel_count.cpu().numpy()
+        out[str(p)] = {"ms_per_step": ms, "speedup_vs_dense": ms_dense / ms, "budget_frac": float(cnt.mean()) / st.n}
+    REPS = 16
+    for r in reps:
+        r.quantize()
+    g = _graph(torch, lambda: [reps[i % len(reps)].score() for i in range(REPS)])
+    ms_score = _time_graphs(torch, [g], max(2, steps // 4), 2) / REPS
+    del g
+    B, Hq, Hkv, D, n = st.B, st.Hq, st.Hkv, st.D, st.n
+    nbytes = B * Hkv * n * (D // 8 + 8) + B * Hq * n * 4
+    dense_bytes = B * Hkv * (n + st.w) * 2 * D * 2
+    return {"workload": wl.name, "head_dim": D, "dense_decode_ms": ms_dense,
+            "dense_GBps": dense_bytes / (ms_dense * 1e-3) / 1e9, "p": out, "score_ms": ms_score,
+            "score_GBps": nbytes / (ms_score * 1e-3) / 1e9}
+
+
 def compact_index(pipeline, torch, reps, p_list, steps, warmup, dense_ms):
     """The 128K step on the compact index (one fp16 factor per key, no query
     centroid; rbq_decode_step_f16) over the same replicas of the cache: step
@@ -555,6 +592,7 @@ def main():
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-overlap (time to first token) report")
     ap.add_argument("--no-offload", action="store_true", help="skip the step with the K/V cache in host memory")
     ap.add_argument("--no-compact", action="store_true", help="skip the step on the compact (fp16-factor) index")
+    ap.add_argument("--no-d64", action="store_true", help="skip the step at head dimension 64")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
@@ -703,6 +741,9 @@ def main():
         scan["frac_of_copy"] = scan["GBps"] / copy["GBps"]
         torch.cuda.empty_cache()
     ragged = None if args.no_ragged else time_ragged(pipeline, gen, torch, args.steps, args.warmup)
+    torch.cuda.empty_cache()
+    d64 = None if args.no_d64 else time_d64(pipeline, gen, torch, args.steps, args.warmup)
+    torch.cuda.empty_cache()
 
     cpu = None if args.no_cpu else cpu_baseline(wl)
 
@@ -747,6 +788,7 @@ def main():
         "prefill_overlap": prefill,
         "kv_in_host_memory": offloaded,
         "compact_index": compact,
+        "head_dim_64": d64,
         "cpu_baseline": cpu,
         "gen_s": t_gen,
         "git": _git_sha(),

@@ -265,6 +265,13 @@ def config3(seed: int = DATA_SEED_BASE + 3, N: int = 131072, w: int = 256) -> Wo
                         _lowrank_keys, lambda rng, b: 0.01, p_sweep=(0.8, 0.9, 0.95, 0.99))
 
 
+def config3_d64(seed: int = DATA_SEED_BASE + 3, N: int = 131072, w: int = 256) -> Workload:
+    """Config 3 at head dimension 64 (the D = 64 shape of the kernel ablation):
+    the same generator, 32 / 8 heads, 128K context, bf16, 256-key window."""
+    return _planted_gqa("gqa 32q/8kv ctx=128K b=1 bf16 window=256 D=64", 1, 32, 8, 64, N, N - w, w, seed, 0.95,
+                        _lowrank_keys, lambda rng, b: 0.01, p_sweep=(0.8, 0.9, 0.95, 0.99))
+
+
 def config4(seed: int = DATA_SEED_BASE + 4, B: int = 16, N: int = 32768) -> Workload:
     """Batch 16 x 32K, 32/8 heads, bf16; per-sequence planted fraction ~ U(0.1 %, 10 %)."""
     return _planted_gqa("gqa 32q/8kv ctx=32K b=16 bf16 varied sparsity", B, 32, 8, 128, N, N, 0, seed, 0.95,
