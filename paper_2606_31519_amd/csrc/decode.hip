@@ -485,14 +485,18 @@ __device__ __forceinline__ uint32_t bf16_bits(float x) {
 }
 __device__ __forceinline__ float bf16_val(uint32_t b) { return __uint_as_float(b << 16); }
 
-// The loads of one group of 16 rows, as one lane sees them (lane = 16 * j + x):
-//   k[kb]: K row x of the group, dimensions 32kb + 8j .. +8 (A operand of kb);
-//          the four lanes of a row read 64 contiguous bytes per instruction
-//   v[i] : V row 4j + i of the group, dimensions 8x .. 8x + 8
+// The loads of one group of 16 rows, as one lane sees them (lane = 16 * j + x),
+// for head dimension D (128 or 64):
+//   k[kb]: K row x of the group, dimensions 32kb + 8j .. +8 (A operand of kb,
+//          kb < D / 32); the four lanes of a row read 64 contiguous bytes per instruction
+//   v[i] : V row 4j + i of the group, dimensions (D / 16) x .. + D / 16
 //   mk   : bit i set when row 4j + i is valid and selected by head x
+template <int D> struct VSeg { using T = u32x4; };   // 8 bf16 per lane and row
+template <> struct VSeg<64> { using T = u32x2; };    // 4 bf16
+template <int D>
 struct GroupLoads {
-  u32x4 k[4];
-  u32x4 v[4];
+  u32x4 k[D / 32];
+  typename VSeg<D>::T v[4];
   uint32_t mk;
 };
 
@@ -511,19 +515,19 @@ __device__ __forceinline__ int row_at(int e, bool list, const RowMap& rm, const 
   return rm.at(e);
 }
 
-template <bool SPARSE>
-__device__ __forceinline__ void load_group_k(GroupLoads& d, int grp, bool skip, int U, const RowMap& rm, bool list,
+template <bool SPARSE, int D>
+__device__ __forceinline__ void load_group_k(GroupLoads<D>& d, int grp, bool skip, int U, const RowMap& rm, bool list,
                                              const int32_t* lst, __amdgpu_buffer_rsrc_t Kr, int x, int j) {
   const int e0 = grp * kGroupRows;
   const int ek = e0 + x < U ? e0 + x : e0;
   const int pk = row_at<SPARSE>(ek, list, rm, lst);
-  const int off = skip ? kSkipOffset : pk * (kHeadDim * 2) + 16 * j;
+  const int off = skip ? kSkipOffset : pk * (D * 2) + 16 * j;
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 64 * kb, 0, 0);
+  for (int kb = 0; kb < D / 32; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 64 * kb, 0, 0);
 }
 
-template <bool SPARSE, int G>
-__device__ __forceinline__ void load_group_v(GroupLoads& d, int grp, bool skip, int U, const RowMap& rm, bool list,
+template <bool SPARSE, int G, int D>
+__device__ __forceinline__ void load_group_v(GroupLoads<D>& d, int grp, bool skip, int U, const RowMap& rm, bool list,
                                              const int32_t* lst, const uint16_t* hmask,
                                              __amdgpu_buffer_rsrc_t Vr, int x, int j) {
   const int e0 = grp * kGroupRows;
@@ -534,8 +538,11 @@ __device__ __forceinline__ void load_group_v(GroupLoads& d, int grp, bool skip, 
     const bool valid = e < U;
     const int ev = valid ? e : e0;
     const int pv = row_at<SPARSE>(ev, list, rm, lst);
-    const int off = skip ? kSkipOffset : pv * (kHeadDim * 2) + 16 * x;
-    d.v[i] = __builtin_amdgcn_raw_buffer_load_b128(Vr, off, 0, 0);
+    const int off = skip ? kSkipOffset : pv * (D * 2) + (D / 8) * x;
+    if constexpr (D == 64)
+      d.v[i] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(Vr, off, 0, 0));
+    else
+      d.v[i] = __builtin_amdgcn_raw_buffer_load_b128(Vr, off, 0, 0);
     bool on = valid && x < G;
     if constexpr (SPARSE) on = on & (!list | bool((hmask[ev] >> x) & 1u));
     mk |= uint32_t(on) << i;
@@ -543,7 +550,7 @@ __device__ __forceinline__ void load_group_v(GroupLoads& d, int grp, bool skip, 
   d.mk = mk;
 }
 
-template <bool SPARSE, int G, bool RAGGED>
+template <bool SPARSE, int G, bool RAGGED, int D = kHeadDim>
 __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     const float* __restrict__ q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V, int cap, int n,
     const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
@@ -554,7 +561,9 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   static_assert(G >= 1 && G <= 16, "the MFMA tiles hold at most 16 heads");
   constexpr bool kPackedQ = kQParts * G <= 16;
   constexpr int kQOps = kPackedQ ? 1 : kQParts;
-  __shared__ u32x4 qB[4][kQOps][kWave];           // B operands of the logits product
+  constexpr int KB = D / 32;                      // k-blocks of the logits product
+  constexpr int VB = D / 32;                      // value blocks per parity (D / 16 columns per lane)
+  __shared__ u32x4 qB[KB][kQOps][kWave];          // B operands of the logits product
   __shared__ uint32_t bm[G][kBmAll];
   __shared__ int32_t lst[SPARSE ? kListCap : 1];
   __shared__ uint16_t hmask[SPARSE ? kListCap : 1];
@@ -562,7 +571,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   __shared__ int wcnt[kBmAll];
   __shared__ int ucount;
   __shared__ float sm[kDWaves][G], sl[kDWaves][G];
-  __shared__ float sacc[kDWaves][G][kHeadDim];
+  __shared__ float sacc[kDWaves][G][D];
 
   const int split = RAGGED ? blockIdx.y : blockIdx.x;   // (ragged grids are split-major)
   const int bh = RAGGED ? blockIdx.x : blockIdx.y;
@@ -596,12 +605,12 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     c1 = RAGGED ? max(c0, min(wb, c0 + kDecodeWinChunk)) : min(w, c0 + kDecodeWinChunk);
   }
   if (RAGGED && c1 == c0 && nwin == 0) {   // block-uniform: past this sequence's rows, an empty partial state
-    if (int(threadIdx.x) < G) part[(int64_t(row0 + threadIdx.x) * total_splits + split) * (kHeadDim + 2)] = -INFINITY;
+    if (int(threadIdx.x) < G) part[(int64_t(row0 + threadIdx.x) * total_splits + split) * (D + 2)] = -INFINITY;
     return;
   }
-  const uint16_t* Kb = window ? K_loc + (int64_t(bh) * loc_ld + wbase) * kHeadDim : K + int64_t(bh) * cap * kHeadDim;
-  const uint16_t* Vb = window ? V_loc + (int64_t(bh) * loc_ld + wbase) * kHeadDim : V + int64_t(bh) * cap * kHeadDim;
-  const uint32_t region = uint32_t(window ? wb : nb + (fold_wq > 0 ? wb : 0)) * uint32_t(kHeadDim * 2);   // < 2^31
+  const uint16_t* Kb = window ? K_loc + (int64_t(bh) * loc_ld + wbase) * D : K + int64_t(bh) * cap * D;
+  const uint16_t* Vb = window ? V_loc + (int64_t(bh) * loc_ld + wbase) * D : V + int64_t(bh) * cap * D;
+  const uint32_t region = uint32_t(window ? wb : nb + (fold_wq > 0 ? wb : 0)) * uint32_t(D * 2);   // < 2^31
   const __amdgpu_buffer_rsrc_t Kr = make_rsrc(Kb, region);
   const __amdgpu_buffer_rsrc_t Vr = make_rsrc(Vb, region);
   constexpr bool kPreMask = kPackedQ;   // (for larger groups the early load costs registers)
@@ -611,7 +620,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   // query operands, lane (column c, quarter jj) of k-block kb = dims 32 kb + 8 jj .. +8.
   // G <= 4: one operand per k-block, column c = part * G + head; otherwise one
   // operand per (k-block, part), column c = head.
-  for (int e = threadIdx.x; e < 4 * kQOps * kWave; e += kDThreads) {
+  for (int e = threadIdx.x; e < KB * kQOps * kWave; e += kDThreads) {
     const int kb = e / (kQOps * kWave), op = (e / kWave) % kQOps, ln = e % kWave;
     const int c = ln & 15, jj = ln >> 4;
     const int h = kPackedQ ? c % G : c;
@@ -620,7 +629,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     if (h < G && prt < kQParts) {
       // both 16-byte loads are issued before any use (a loop over the part index
       // with a run-time bound otherwise serialises one load per element)
-      const f32x4* qp = reinterpret_cast<const f32x4*>(q + int64_t(row0 + h) * kHeadDim + 32 * kb + 8 * jj);
+      const f32x4* qp = reinterpret_cast<const f32x4*>(q + int64_t(row0 + h) * D + 32 * kb + 8 * jj);
       const f32x4 qa = qp[0], qb = qp[1];
       const float qv[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
 #pragma unroll
@@ -652,18 +661,18 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   const RowMap rm{c0, c1 - c0, RAGGED && nwin > 0 ? wrow0 - c1 : 0};
 
   float m = -INFINITY, lsum = 0.f;      // head x's running max (uniform over j) and this lane's partial sum
-  f32x4 acc[4][2];                      // lane (x, j), reg i: head 4j + i, dimension 8x + 2t + par
+  f32x4 acc[VB][2];                     // lane (x, j), reg i: head 4j + i, dimension (D / 16) x + 2t + par
 #pragma unroll
-  for (int t = 0; t < 4; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < VB; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int ngroups = (U + kGroupRows - 1) / kGroupRows;
   // One group's registers are reused for the next: its K rows are requested
   // as soon as the logits are done, its V rows as soon as the values are.
-  GroupLoads cur;
+  GroupLoads<D> cur;
   int grp = wave;
   if (grp < ngroups) {
-    load_group_k<SPARSE>(cur, grp, false, U, rm, list, lst, Kr, x, j);
-    load_group_v<SPARSE, G>(cur, grp, false, U, rm, list, lst, hmask, Vr, x, j);
+    load_group_k<SPARSE, D>(cur, grp, false, U, rm, list, lst, Kr, x, j);
+    load_group_v<SPARSE, G, D>(cur, grp, false, U, rm, list, lst, hmask, Vr, x, j);
   }
   while (grp < ngroups) {
     const int nxt = grp + kDWaves;
@@ -676,14 +685,14 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     const u32x4* qp = &qB[0][0][0] + qoff;
     f32x4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
+    for (int kb = 0; kb < KB; ++kb) {
       const bf16x8 a = __builtin_bit_cast(bf16x8, cur.k[kb]);
 #pragma unroll
       for (int op = 0; op < kQOps; ++op)
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, qp[(kb * kQOps + op) * kWave]), s,
                                                     0, 0, 0);
     }
-    load_group_k<SPARSE>(cur, last ? grp : nxt, last, U, rm, list, lst, Kr, x, j);
+    load_group_k<SPARSE, D>(cur, last ? grp : nxt, last, U, rm, list, lst, Kr, x, j);
     if constexpr (kPackedQ) {
       // column h + G and h + 2G hold the mid and lo parts of head h's logits
       // (each element goes through an opaque copy first: hipcc 7.2 miscompiles
@@ -726,7 +735,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
 #pragma unroll
       for (int i = 0; i < 4; ++i) cr[i] = __shfl(corr, 4 * j + i, kWave);
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
+      for (int t = 0; t < VB; ++t) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           acc[t][0][i] *= cr[i];
@@ -743,9 +752,9 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     }
     const s16x4 a_hi = __builtin_bit_cast(s16x4, u32x2{ph[0] | (ph[1] << 16), ph[2] | (ph[3] << 16)});
     const s16x4 a_lo = __builtin_bit_cast(s16x4, u32x2{pl[0] | (pl[1] << 16), pl[2] | (pl[3] << 16)});
-    // values: column x of block (t, par) is dimension 8x + 2t + par; k = rows 4j .. 4j + 3
+    // values: column x of block (t, par) is dimension (D / 16) x + 2t + par; k = rows 4j .. 4j + 3
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < VB; ++t) {
 #pragma unroll
       for (int par = 0; par < 2; ++par) {
         const uint32_t sel = par ? 0x07060302u : 0x05040100u;
@@ -756,7 +765,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
         acc[t][par] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a_lo, bv, acc[t][par], 0, 0, 0);
       }
     }
-    load_group_v<SPARSE, G>(cur, last ? grp : nxt, last, U, rm, list, lst, hmask, Vr, x, j);
+    load_group_v<SPARSE, G, D>(cur, last ? grp : nxt, last, U, rm, list, lst, hmask, Vr, x, j);
     grp = nxt;
   }
 
@@ -772,16 +781,16 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
     const int h = 4 * j + i;
     if (h < G) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        sacc[wave][h][8 * x + 2 * t] = acc[t][0][i];
-        sacc[wave][h][8 * x + 2 * t + 1] = acc[t][1][i];
+      for (int t = 0; t < VB; ++t) {
+        sacc[wave][h][(D / 16) * x + 2 * t] = acc[t][0][i];
+        sacc[wave][h][(D / 16) * x + 2 * t + 1] = acc[t][1][i];
       }
     }
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < G * (kHeadDim + 2); e += kDThreads) {
-    const int g = e / (kHeadDim + 2);
-    const int k = e - g * (kHeadDim + 2);
+  for (int e = threadIdx.x; e < G * (D + 2); e += kDThreads) {
+    const int g = e / (D + 2);
+    const int k = e - g * (D + 2);
     float M = -INFINITY;
 #pragma unroll
     for (int v = 0; v < kDWaves; ++v) M = fmaxf(M, sm[v][g]);
@@ -800,7 +809,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
         }
       }
     }
-    part[(int64_t(row0 + g) * total_splits + split) * (kHeadDim + 2) + k] = r;
+    part[(int64_t(row0 + g) * total_splits + split) * (D + 2) + k] = r;
   }
 }
 
@@ -868,8 +877,8 @@ rbq_status launch_g(int G, dim3 grid, hipStream_t stream, const float* q, const 
                     int Hkv, const int32_t* seq_n, const int32_t* seq_w) {
 #define RBQ_DECODE_CASE(GG)                                                                                       \
   case GG:                                                                                                        \
-    if constexpr (DT == RBQ_BF16 && D == kHeadDim)                                                                \
-      decode_mfma_kernel<SPARSE, GG, RAGGED><<<grid, kDThreads, 0, stream>>>(                                     \
+    if constexpr (DT == RBQ_BF16)                                                                                 \
+      decode_mfma_kernel<SPARSE, GG, RAGGED, D><<<grid, kDThreads, 0, stream>>>(                                  \
           q, static_cast<const uint16_t*>(K), static_cast<const uint16_t*>(V), cap, n, sel_idx, sel_count,        \
           sel_mask, mask_words, static_cast<const uint16_t*>(K_loc), static_cast<const uint16_t*>(V_loc), loc_ld, \
           w, chunk, idx_splits, total, fold_s0, fold_wq, scale_log2e, part, Hq, Hkv, seq_n, seq_w);               \
@@ -925,7 +934,7 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                    w, sp.chunk, sp.idx_splits, sp.total(), sp.fold_s0, sp.fold_wq, scale_log2e, part, heads_q,      \
                    heads_kv, seq_n, seq_w)
   const bool rg = seq_n != nullptr;
-  if (D == 64) {   // uniform batches: the vector kernel for both dtypes
+  if (D == 64) {   // uniform batches (bf16 on the matrix cores, fp32 on the vector kernel)
 #define RBQ_DECODE_LAUNCH64(DT, SP)                                                                                 \
   launch_g<DT, SP, false, 64>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc,    \
                               V_loc, loc_ld, w, sp.chunk, sp.idx_splits, sp.total(), sp.fold_s0, sp.fold_wq,        \
