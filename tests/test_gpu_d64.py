@@ -8,8 +8,8 @@ against the separate calls.
   * rbq_quantize_query (debug form): INT4 codes decided from the GPU's rotated
     query, bit-exact; the integer dot products of rbq_score_ints bit-exact;
     the scores within the score tolerance;
-  * rbq_sparse_decode / rbq_dense_decode (bf16 and fp32 K/V, G = 1, 4, 8, with a
-    window) against the oracle's attention;
+  * rbq_sparse_decode / rbq_dense_decode (bf16 K/V on the matrix cores, fp32 on
+    the vector kernel; G = 1 to 16, with a window) against the oracle's attention;
   * rbq_decode_step against the five calls, bitwise, and its Top-p sets against
     the oracle on the same scores.
 """
@@ -105,7 +105,7 @@ def test_d64_quantize_and_score(R, pipeline, B, Hq, Hkv, n):
 
 
 @pytest.mark.parametrize("kv_dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("G", [1, 4, 8])
+@pytest.mark.parametrize("G", [1, 2, 4, 8, 16])
 def test_d64_sparse_and_dense_decode(R, pipeline, kv_dtype, G):
     Hkv, n, w = 2, 3000, 40
     print("d64 decode", kv_dtype, G, flush=True)
