@@ -723,7 +723,7 @@ def main():
         offloaded = offload(pipeline, torch, st0, [0.8, 0.9, 0.95], args.steps, args.warmup)
         torch.cuda.empty_cache()
 
-    # the box's own streaming rate (elementwise copy), a second reference beside the 8 TB/s peak
+    # the GPU's measured streaming rate (elementwise copy), a second reference beside the 8 TB/s peak
     copy = _copy_rate(torch, 5)
 
     # roofline of the dominant call of the step: rbq_sparse_decode (split pass + combine),

@@ -14,8 +14,10 @@
  *     The library never allocates, frees or synchronises: each call checks
  *     its arguments on the host, enqueues kernels on `stream` and returns.
  *   - Shapes: B = batch, Hq = query heads, Hkv = KV heads (Hq % Hkv == 0,
- *     G = Hq / Hkv; query head h reads KV head h / G), D = head_dim. This
- *     build supports D = 128 (RBQ_EUNSUPPORTED otherwise).
+ *     G = Hq / Hkv; query head h reads KV head h / G), D = head_dim.
+ *     D = 128 for every call; D = 64 for the uniform calls and the fused
+ *     step (the ragged, compact-index and 8-plane calls return
+ *     RBQ_EUNSUPPORTED for it); any other D: RBQ_EUNSUPPORTED.
  *   - Layouts are row-major and contiguous:
  *       codes [B][Hkv][cap][D/32] uint32: dimension d of a key's sign code is
  *             bit d % 32 of word d / 32; the bit is 1 iff the d-th component

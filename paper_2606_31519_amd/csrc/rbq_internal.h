@@ -10,7 +10,7 @@
 
 namespace rbq {
 
-constexpr int kHeadDim = 128;        // the head_dim this build's kernels are written for
+constexpr int kHeadDim = 128;        // the head dimension of every call (64: the uniform calls, a template argument)
 constexpr int kWords = kHeadDim / 32;
 
 // ---------------------------------------------------------------- validation
