@@ -15,9 +15,7 @@
  *     its arguments on the host, enqueues kernels on `stream` and returns.
  *   - Shapes: B = batch, Hq = query heads, Hkv = KV heads (Hq % Hkv == 0,
  *     G = Hq / Hkv; query head h reads KV head h / G), D = head_dim.
- *     D = 128 for every call; D = 64 for the uniform calls and the fused
- *     step (the ragged, compact-index and 8-plane calls return
- *     RBQ_EUNSUPPORTED for it); any other D: RBQ_EUNSUPPORTED.
+ *     Every call takes D = 128 or D = 64; any other D: RBQ_EUNSUPPORTED.
  *   - Layouts are row-major and contiguous:
  *       codes [B][Hkv][cap][D/32] uint32: dimension d of a key's sign code is
  *             bit d % 32 of word d / 32; the bit is 1 iff the d-th component

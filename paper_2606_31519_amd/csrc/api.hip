@@ -17,7 +17,6 @@ rbq_status decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
   const void* fac = kfac16 != nullptr ? static_cast<const void*>(kfac16) : kfac;
   rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
   if (s != RBQ_OK) return s;
-  if (head_dim != kHeadDim && kfac16 != nullptr) return RBQ_EUNSUPPORTED;   // (the compact index is D = 128 only)
   if (n < 0 || w < 0 || cap < 0 || int64_t(n) + w > cap) return RBQ_EINVAL;
   const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
   if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
@@ -121,9 +120,8 @@ rbq_status rbq_encode_keys_f16(int32_t batch, int32_t heads_kv, int32_t head_dim
   const rbq_status s = check_encode(batch, heads_kv, head_dim, keys, keys_dtype, keys_ld, n_new, offset, cap, P, c_k,
                                     codes, kfac16, flags, ws, ws_bytes);
   if (s != RBQ_OK) return s;
-  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_encode(batch, heads_kv, keys, keys_dtype, keys_ld, n_new, offset, cap, P, nullptr, c_k, codes,
-                       nullptr, flags, nullptr, ws, nullptr, stream, kfac16);
+                       nullptr, flags, nullptr, ws, nullptr, stream, kfac16, head_dim);
 }
 
 rbq_status rbq_score_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
@@ -131,9 +129,8 @@ rbq_status rbq_score_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32
                          float* scores, hipStream_t stream) {
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac16, qplanes, qscal, scores);
   if (s != RBQ_OK) return s;
-  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, qscal, scores, nullptr, nullptr,
-                      stream, nullptr, nullptr, 0, nullptr, kfac16);
+                      stream, nullptr, nullptr, 0, nullptr, kfac16, 4, head_dim);
 }
 
 rbq_status rbq_score_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
@@ -141,9 +138,8 @@ rbq_status rbq_score_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
                         float* scores, hipStream_t stream) {
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes8, qscal, scores);
   if (s != RBQ_OK) return s;
-  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes8, qscal, scores, nullptr, nullptr,
-                      stream, nullptr, nullptr, 0, nullptr, nullptr, 8);
+                      stream, nullptr, nullptr, 0, nullptr, nullptr, 8, head_dim);
 }
 
 rbq_status rbq_score_ints_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
@@ -152,9 +148,8 @@ rbq_status rbq_score_ints_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, i
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, ip_out, qplanes8, pc_out,
                                    ip_out);
   if (s != RBQ_OK) return s;
-  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes8, nullptr, nullptr, ip_out, pc_out,
-                      stream, nullptr, nullptr, 0, nullptr, nullptr, 8);
+                      stream, nullptr, nullptr, 0, nullptr, nullptr, 8, head_dim);
 }
 
 rbq_status rbq_score_ints(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
@@ -239,12 +234,11 @@ rbq_status decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32
                          hipStream_t stream) {
   rbq_status s = check_ragged(n, w, cap, seq_n, seq_w);
   if (s != RBQ_OK) return s;
-  if (head_dim == 64) return RBQ_EUNSUPPORTED;   // (ragged batches: D = 128)
   s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, sparse, sel_idx, sel_count, K, V,
                    cap, w, sm_scale, out, ws, ws_bytes);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K, V, cap, w,
-                       sm_scale, out, lse, ws, sparse, stream, nullptr, 0, seq_n, seq_w);
+                       sm_scale, out, lse, ws, sparse, stream, nullptr, 0, seq_n, seq_w, head_dim);
 }
 
 
@@ -260,7 +254,6 @@ rbq_status decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, 
   rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, w, cap, seq_n, seq_w)) != RBQ_OK) return s;
-  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   if (seq_p == nullptr || (reinterpret_cast<uintptr_t>(seq_p) & 15u) != 0) return RBQ_EINVAL;
   const StepWorkspace sw = step_workspace(ws, batch, heads_q, heads_kv, head_dim, n, w);
   if (ws == nullptr || ws_bytes < sw.bytes) return RBQ_EINVAL;
@@ -282,19 +275,20 @@ rbq_status decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, 
   const int64_t rows = int64_t(batch) * heads_q;
   if (do_flush)   // window rows [seq_n[b], + seq_w[b]) of K into the same index rows
     s = launch_quantize_flush(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, K, kv_dtype, cap, w, 0, cap,
-                              codes, kfac, stream, seq_n, seq_w, n, kfac16);
+                              codes, kfac, stream, seq_n, seq_w, n, kfac16, head_dim);
   else
-    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream);
+    s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, 4, head_dim);
   if (s != RBQ_OK) return s;
   const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
   s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   sw.slot_max, tw.hist, rows * kHistPerRow, seq_n, kfac16);
+                   sw.slot_max, tw.hist, rows * kHistPerRow, seq_n, kfac16, 4, head_dim);
   if (s != RBQ_OK) return s;
   s = launch_topp(int32_t(rows), n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
                   score_blocks_per_row(batch, heads_kv, n), sw.masks, seq_n, seq_p, heads_q);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K, V, cap, w,
-                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), seq_n, seq_w);
+                       sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), seq_n, seq_w,
+                       head_dim);
 }
 
 }  // namespace
@@ -307,9 +301,8 @@ rbq_status rbq_score_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, in
   rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores);
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, 0, cap, seq_n, nullptr)) != RBQ_OK) return s;
-  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr,
-                      stream, nullptr, nullptr, 0, seq_n);
+                      stream, nullptr, nullptr, 0, seq_n, nullptr, 4, head_dim);
 }
 
 rbq_status rbq_score_varlen_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
@@ -318,9 +311,8 @@ rbq_status rbq_score_varlen_f16(int32_t batch, int32_t heads_q, int32_t heads_kv
   rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac16, qplanes, qscal, scores);
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, 0, cap, seq_n, nullptr)) != RBQ_OK) return s;
-  if (head_dim != kHeadDim) return RBQ_EUNSUPPORTED;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, qscal, scores, nullptr, nullptr,
-                      stream, nullptr, nullptr, 0, seq_n, kfac16);
+                      stream, nullptr, nullptr, 0, seq_n, kfac16, 4, head_dim);
 }
 
 rbq_status rbq_topp_select_varlen(int32_t batch, int32_t heads_q, int32_t n, const int32_t* seq_n,

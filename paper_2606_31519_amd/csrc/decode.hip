@@ -934,15 +934,22 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                    w, sp.chunk, sp.idx_splits, sp.total(), sp.fold_s0, sp.fold_wq, scale_log2e, part, heads_q,      \
                    heads_kv, seq_n, seq_w)
   const bool rg = seq_n != nullptr;
-  if (D == 64) {   // uniform batches (bf16 on the matrix cores, fp32 on the vector kernel)
-#define RBQ_DECODE_LAUNCH64(DT, SP)                                                                                 \
-  launch_g<DT, SP, false, 64>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc,    \
-                              V_loc, loc_ld, w, sp.chunk, sp.idx_splits, sp.total(), sp.fold_s0, sp.fold_wq,        \
-                              scale_log2e, part, heads_q, heads_kv, seq_n, seq_w)
-    if (kv_dtype == RBQ_BF16)
-      st = sparse ? RBQ_DECODE_LAUNCH64(RBQ_BF16, true) : RBQ_DECODE_LAUNCH64(RBQ_BF16, false);
-    else
-      st = sparse ? RBQ_DECODE_LAUNCH64(RBQ_F32, true) : RBQ_DECODE_LAUNCH64(RBQ_F32, false);
+  if (D == 64) {   // bf16 on the matrix cores, fp32 on the vector kernel
+#define RBQ_DECODE_LAUNCH64(DT, SP, RG)                                                                             \
+  launch_g<DT, SP, RG, 64>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, \
+                           loc_ld, w, sp.chunk, sp.idx_splits, sp.total(), sp.fold_s0, sp.fold_wq, scale_log2e, part,  \
+                           heads_q, heads_kv, seq_n, seq_w)
+    if (kv_dtype == RBQ_BF16) {
+      if (rg)
+        st = sparse ? RBQ_DECODE_LAUNCH64(RBQ_BF16, true, true) : RBQ_DECODE_LAUNCH64(RBQ_BF16, false, true);
+      else
+        st = sparse ? RBQ_DECODE_LAUNCH64(RBQ_BF16, true, false) : RBQ_DECODE_LAUNCH64(RBQ_BF16, false, false);
+    } else {
+      if (rg)
+        st = sparse ? RBQ_DECODE_LAUNCH64(RBQ_F32, true, true) : RBQ_DECODE_LAUNCH64(RBQ_F32, false, true);
+      else
+        st = sparse ? RBQ_DECODE_LAUNCH64(RBQ_F32, true, false) : RBQ_DECODE_LAUNCH64(RBQ_F32, false, false);
+    }
 #undef RBQ_DECODE_LAUNCH64
     if (st != RBQ_OK) return st;
     decode_combine_kernel<64><<<dim3(batch * heads_q, kCombSlices), kCombThreads, 0, stream>>>(part, sp.total(),

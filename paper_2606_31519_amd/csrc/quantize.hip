@@ -240,11 +240,18 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
   const int per_head = encode_blocks_per_head(n_new, bhs);
   const int blocks = rows + per_head * bhs;
   const bool rg = seq_off != nullptr;
-  if (head_dim == 64) {   // (uniform batches only)
-    if (keys_dtype == RBQ_BF16)
-      quantize_flush_kernel<RBQ_BF16, false, 64><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
-    else
-      quantize_flush_kernel<RBQ_F32, false, 64><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+  if (head_dim == 64) {
+    if (keys_dtype == RBQ_BF16) {
+      if (rg)
+        quantize_flush_kernel<RBQ_BF16, true, 64><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+      else
+        quantize_flush_kernel<RBQ_BF16, false, 64><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+    } else {
+      if (rg)
+        quantize_flush_kernel<RBQ_F32, true, 64><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+      else
+        quantize_flush_kernel<RBQ_F32, false, 64><<<blocks, kQAll, 0, stream>>>(qa, ea, rows, per_head);
+    }
     return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
   }
   if (keys_dtype == RBQ_BF16) {

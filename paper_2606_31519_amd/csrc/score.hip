@@ -275,6 +275,33 @@ rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* co
 
 }  // namespace
 
+namespace {
+
+// every form of the scan at head dimension D
+template <int D>
+rbq_status launch_score_d(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
+                          const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal, float* scores,
+                          int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
+                          const int32_t* seq_n, bool slots, int32_t planes) {
+#define RBQ_SCORE_LAUNCH(I, S, R, F, QB)                                                                      \
+  launch_kpt<I, S, R, F, QB, D>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, \
+                                cap, Hq, Hkv, G, sl, seq_n)
+#define RBQ_SCORE_FAC(S, R) \
+  (kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, S, R, true, 4) : RBQ_SCORE_LAUNCH(false, S, R, false, 4))
+  if (planes == 8) {   // 8-plane queries: the standalone call only (integer hook included)
+    if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, false, 8);
+    return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, false, false, true, 8)
+                             : RBQ_SCORE_LAUNCH(false, false, false, false, 8);
+  }
+  if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, false, 4);   // (the integer hook is never ragged)
+  if (seq_n != nullptr) return slots ? RBQ_SCORE_FAC(true, true) : RBQ_SCORE_FAC(false, true);
+  return slots ? RBQ_SCORE_FAC(true, false) : RBQ_SCORE_FAC(false, false);
+#undef RBQ_SCORE_FAC
+#undef RBQ_SCORE_LAUNCH
+}
+
+}  // namespace
+
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, float* slot_max,
@@ -285,40 +312,11 @@ rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
   const int kpt = score_keys_per_lane(batch, heads_kv, n);
   dim3 grid(score_blocks_per_row(batch, heads_kv, n), batch * heads_kv);
   const ScoreSlots sl{slot_max, hist, hist_words};
-#define RBQ_SCORE_LAUNCH(I, S, R, F)                                                                    \
-  launch_kpt<I, S, R, F>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, cap, \
-                         heads_q, heads_kv, G, sl, seq_n)
-#define RBQ_SCORE_FAC(S, R) (kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, S, R, true) : RBQ_SCORE_LAUNCH(false, S, R, false))
-  if (head_dim == 64) {   // D = 64: the uniform calls (integer hook, standalone, fused step), fp32 factors
-    if (ip_out != nullptr)
-      return launch_kpt<true, false, false, false, 4, 64>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal,
-                                                          scores, ip_out, pc_out, n, cap, heads_q, heads_kv, G, sl,
-                                                          seq_n);
-    return slot_max != nullptr
-               ? launch_kpt<false, true, false, false, 4, 64>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal,
-                                                              scores, ip_out, pc_out, n, cap, heads_q, heads_kv, G,
-                                                              sl, seq_n)
-               : launch_kpt<false, false, false, false, 4, 64>(kpt, grid, stream, codes, kfac, kfac16, qplanes,
-                                                               qscal, scores, ip_out, pc_out, n, cap, heads_q,
-                                                               heads_kv, G, sl, seq_n);
-  }
-  if (planes == 8) {   // 8-plane queries: the standalone call only (integer hook included)
-    if (ip_out != nullptr)
-      return launch_kpt<true, false, false, false, 8>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores,
-                                                      ip_out, pc_out, n, cap, heads_q, heads_kv, G, sl, seq_n);
-    return kfac16 != nullptr
-               ? launch_kpt<false, false, false, true, 8>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal,
-                                                          scores, ip_out, pc_out, n, cap, heads_q, heads_kv, G, sl,
-                                                          seq_n)
-               : launch_kpt<false, false, false, false, 8>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal,
-                                                           scores, ip_out, pc_out, n, cap, heads_q, heads_kv, G, sl,
-                                                           seq_n);
-  }
-  if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, false);   // (the integer hook is never ragged)
-  if (seq_n != nullptr) return slot_max != nullptr ? RBQ_SCORE_FAC(true, true) : RBQ_SCORE_FAC(false, true);
-  return slot_max != nullptr ? RBQ_SCORE_FAC(true, false) : RBQ_SCORE_FAC(false, false);
-#undef RBQ_SCORE_FAC
-#undef RBQ_SCORE_LAUNCH
+  if (head_dim == 64)
+    return launch_score_d<64>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, cap,
+                              heads_q, heads_kv, G, sl, seq_n, slot_max != nullptr, planes);
+  return launch_score_d<kHeadDim>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n,
+                                  cap, heads_q, heads_kv, G, sl, seq_n, slot_max != nullptr, planes);
 }
 
 }  // namespace rbq

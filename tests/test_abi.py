@@ -187,7 +187,7 @@ def test_compact_index_calls_reject_invalid_arguments_on_the_host(lib):
     assert enc(kf=FAKE + 2) == EINVAL
     assert enc(off=1) == EINVAL
     assert enc(flags=4) == EINVAL
-    assert enc(D=64) == EUNSUP
+    assert enc(D=96) == EUNSUP
     sc = lambda n=10, kf=FAKE: L.rbq_score_f16(1, 8, 4, 128, n, 10, FAKE, kf, FAKE, FAKE, FAKE, 0)
     assert sc(n=11) == EINVAL
     assert sc(kf=None) == EINVAL
@@ -207,28 +207,30 @@ def test_compact_index_calls_reject_invalid_arguments_on_the_host(lib):
     assert stv == EINVAL                             # no factor array
 
 
-def test_head_dim_64_is_rejected_where_it_is_not_built(lib):
-    """D = 64 runs the uniform calls; the ragged, compact-index and 8-plane calls
-    return RBQ_EUNSUPPORTED for it, before anything is launched."""
+def test_every_call_validates_at_head_dim_64(lib):
+    """D = 64 runs every call; invalid arguments are still rejected on the host
+    (nothing here reaches a launch), and an unsupported D gives RBQ_EUNSUPPORTED."""
     L = lib.lib
-    EUNSUP = lib.RBQ_EUNSUPPORTED
-    assert L.rbq_score_varlen(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
-    assert L.rbq_score_varlen_f16(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
-    assert L.rbq_sparse_decode_varlen(1, 8, 4, 64, FAKE, FAKE, FAKE, 1, 200, 100, 10, FAKE, None, FAKE, FAKE, 0.1,
-                                      FAKE, None, FAKE, 1 << 30, 0) == EUNSUP
-    assert L.rbq_dense_decode_varlen(1, 8, 4, 64, FAKE, FAKE, FAKE, 1, 200, 100, 10, FAKE, None, 0.1, FAKE, None,
-                                     FAKE, 1 << 30, 0) == EUNSUP
+    EINVAL, EUNSUP = lib.RBQ_EINVAL, lib.RBQ_EUNSUPPORTED
+    assert L.rbq_score_varlen(1, 8, 4, 64, 10, 10, None, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EINVAL   # no seq_n
+    assert L.rbq_score_varlen(1, 8, 4, 96, 10, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
+    assert L.rbq_score_varlen_f16(1, 8, 4, 64, 11, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EINVAL
+    assert L.rbq_sparse_decode_varlen(1, 8, 4, 64, FAKE, FAKE, FAKE, 1, 105, 100, 10, FAKE, None, FAKE, FAKE, 0.1,
+                                      FAKE, None, FAKE, 1 << 30, 0) == EINVAL      # n + w > cap
+    assert L.rbq_dense_decode_varlen(1, 8, 4, 64, FAKE, FAKE, FAKE, 1, 200, 100, 10, None, None, 0.1, FAKE, None,
+                                     FAKE, 1 << 30, 0) == EINVAL                    # no seq_n
     assert L.rbq_decode_step_varlen(1, 8, 4, 64, FAKE, FAKE, None, FAKE, FAKE, FAKE, 1, 200, 100, 10, FAKE, None,
                                     FAKE, FAKE, 1, FAKE, 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
-                                    1 << 30, 0) == EUNSUP
-    assert L.rbq_encode_keys_f16(1, 1, 64, FAKE, 1, 10, 10, 0, 10, FAKE, FAKE, FAKE, FAKE, 0, FAKE, 1 << 20,
+                                    64, 0) == EINVAL                                # short workspace
+    assert L.rbq_encode_keys_f16(1, 1, 64, FAKE, 1, 10, 10, 1, 10, FAKE, FAKE, FAKE, FAKE, 0, FAKE, 1 << 20,
+                                 0) == EINVAL                                       # offset + n_new > cap
+    assert L.rbq_encode_keys_f16(1, 1, 96, FAKE, 1, 10, 10, 0, 10, FAKE, FAKE, FAKE, FAKE, 0, FAKE, 1 << 20,
                                  0) == EUNSUP
-    assert L.rbq_score_f16(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
-    assert L.rbq_decode_step_f16(1, 8, 4, 64, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 200, 100, 10, FAKE, FAKE, 1, 0.9,
-                                 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, 0) == EUNSUP
-    assert L.rbq_score_q8(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
-    assert L.rbq_score_ints_q8(1, 8, 4, 64, 10, 10, FAKE, FAKE, FAKE, FAKE, 0) == EUNSUP
-    # and the uniform calls still validate their arguments at D = 64
-    assert L.rbq_score(1, 8, 4, 64, 11, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == lib.RBQ_EINVAL
+    assert L.rbq_score_f16(1, 8, 4, 64, 10, 10, FAKE, None, FAKE, FAKE, FAKE, 0) == EINVAL
+    assert L.rbq_decode_step_f16(1, 8, 4, 64, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 105, 100, 10, FAKE, FAKE, 1, 0.9,
+                                 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, 0) == EINVAL
+    assert L.rbq_score_q8(1, 8, 4, 64, 11, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EINVAL
+    assert L.rbq_score_ints_q8(1, 8, 4, 64, 10, 10, FAKE, None, FAKE, FAKE, 0) == EINVAL
+    assert L.rbq_score(1, 8, 4, 64, 11, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EINVAL
     assert lib.rbq_workspace_bytes(lib.RBQ_OP_DECODE_STEP, 1, 8, 4, 64, 1000, 16) < \
         lib.rbq_workspace_bytes(lib.RBQ_OP_DECODE_STEP, 1, 8, 4, 128, 1000, 16)

@@ -165,3 +165,112 @@ def test_d64_step_matches_calls_and_oracle(R, pipeline, kv_dtype):
             win = np.arange(wl.n_index, wl.n_index + wl.w)
             pu.check_attention(_np(a.out[bb, h]), float(_np(a.lse[bb, h])), wl.q[bb, h].astype(np.float64),
                                K, V, s, K[win], V[win], tau)
+
+
+def test_d64_ragged_step_matches_ragged_calls_and_each_sequence(R, pipeline):
+    """rbq_decode_step_varlen at D = 64 against the separate ragged calls plus
+    each sequence's window encode (bitwise), its scores against each sequence's
+    uniform score call (bitwise) and its Top-p sets against the oracle."""
+    seq_n, seq_w, seq_p = [6000, 0, 4097, 1234], [48, 17, 0, 33], [0.9, 0.7, 1.0, 0.95]
+    Hq, Hkv, n = 8, 2, 6000
+    print("d64 ragged", seq_n, seq_w, seq_p, flush=True)
+    B, w = len(seq_n), max(seq_w)
+    wl = gen.random_case(B, Hq, Hkv, n, D=D, seed=23, kv_dtype="bf16", w=w, c_q_scale=0.3)
+    a = pipeline.DecodeState.from_workload(wl)
+    b = pipeline.DecodeState.from_workload(wl)
+    for st in (a, b):
+        st.build_index_ragged(seq_n)
+    dev = dict(device="cuda")
+    sn = torch.tensor(seq_n, dtype=torch.int32, **dev)
+    sw = torch.tensor(seq_w, dtype=torch.int32, **dev)
+    sp = torch.tensor(seq_p, dtype=torch.float32, **dev)
+    a.step_ragged(sn, sw, sp)
+    cap = b.cap
+    R.rbq_quantize_query(B, Hq, Hkv, D, b.q, b.P, b.c_q, b.c_k, b.qplanes, b.qscal)
+    R.rbq_score_varlen(B, Hq, Hkv, D, n, cap, sn, b.codes, b.kfac, b.qplanes, b.qscal, b.scores)
+    R.rbq_topp_select_varlen(B, Hq, n, sn, b.scores, sp, b.sm_scale, b.sel_idx, b.sel_count, b.ws_topp)
+    R.rbq_sparse_decode_varlen(B, Hq, Hkv, D, b.q, b.K, b.V, cap, n, w, sn, sw, b.sel_idx, b.sel_count,
+                               b.sm_scale, b.out, b.lse, b.ws_decode)
+    for s in range(B):
+        if seq_w[s]:
+            R.rbq_encode_keys(1, Hkv, D, b.K[s:s + 1, :, seq_n[s]:], cap, seq_w[s], seq_n[s], cap, b.P,
+                              b.c_q[s:s + 1], b.c_k[s:s + 1], b.codes[s:s + 1], b.kfac[s:s + 1], 0, None, None)
+    torch.cuda.synchronize()
+    cnt = _np(a.sel_count)
+    assert np.array_equal(cnt, _np(b.sel_count))
+    tau = 1.0 / math.sqrt(D)
+    G = Hq // Hkv
+    for s in range(B):
+        for name in ("out", "lse"):
+            x, y = _np(getattr(a, name))[s], _np(getattr(b, name))[s]
+            assert np.array_equal(x.view(np.uint8), y.view(np.uint8)), (name, s)
+        rows = slice(0, seq_n[s] + seq_w[s])
+        assert np.array_equal(pu.u32(a.codes[s, :, rows]), pu.u32(b.codes[s, :, rows]))
+        assert np.array_equal(_np(a.kfac[s, :, rows]).view(np.uint32), _np(b.kfac[s, :, rows]).view(np.uint32))
+        if not seq_n[s]:
+            continue
+        x = _np(a.scores)[s, :, :seq_n[s]]
+        S1 = torch.zeros(1, Hq, seq_n[s], dtype=torch.float32, **dev)
+        R.rbq_score(1, Hq, Hkv, D, seq_n[s], cap, b.codes[s:s + 1], b.kfac[s:s + 1], b.qplanes[s:s + 1],
+                    b.qscal[s:s + 1], S1)
+        torch.cuda.synchronize()
+        assert np.array_equal(_np(S1)[0].view(np.uint8), x.view(np.uint8))
+        for h in range(Hq):
+            sel = _np(a.sel_idx)[s, h, :cnt[s, h]]
+            assert np.array_equal(sel, _np(b.sel_idx)[s, h, :cnt[s, h]])
+            p = min(float(np.float32(seq_p[s])), 1.0)   # the device's fp32 p
+            if p < 1.0:
+                pu.check_topp(x[h], p, tau, sel)
+            else:
+                assert cnt[s, h] == seq_n[s]
+            K = wl.K_f32(s, h // G).astype(np.float64)
+            V = wl.V_f32(s, h // G).astype(np.float64)
+            win = np.arange(seq_n[s], seq_n[s] + seq_w[s])
+            pu.check_attention(_np(a.out[s, h]), float(_np(a.lse[s, h])), wl.q[s, h].astype(np.float64), K, V,
+                               sel, K[win], V[win], tau)
+
+
+def test_d64_compact_index_and_eight_bit_queries(R, pipeline):
+    """The compact index at D = 64: codes bitwise those of the full index,
+    factors its fp32 f rounded to fp16, the fused step bitwise the separate
+    calls; and 8-bit queries at D = 64: integer dots bit-exact, scores within
+    the score tolerance."""
+    print("d64 compact + q8", flush=True)
+    wl = gen.random_case(2, 8, 2, 5000, D=D, seed=29, kv_dtype="bf16", w=32, c_q_scale=0.0, q_scale=6.0)
+    full = pipeline.DecodeState.from_workload(wl, c_q=False)
+    a = pipeline.DecodeState.from_workload(wl, compact=True)
+    b = pipeline.DecodeState.from_workload(wl, compact=True)
+    for st in (full, a, b):
+        st.build_index()
+    torch.cuda.synchronize()
+    assert np.array_equal(pu.u32(full.codes), pu.u32(a.codes))
+    n = wl.n_index
+    f32 = _np(full.kfac)[..., 0][..., :n]
+    assert np.array_equal(np.minimum(f32, 65504.0).astype(np.float16).view(np.uint16),
+                          _np(a.kfac16)[..., :n].view(np.uint16))
+    a.step(0.9)
+    b.step_calls(0.9)
+    torch.cuda.synchronize()
+    for name in ("scores", "sel_count", "out", "lse", "codes", "kfac16"):
+        x, y = _np(getattr(a, name)), _np(getattr(b, name))
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8)), name
+    # eight-bit queries on the full index
+    qp = torch.zeros(2, 8, 8, D // 32, dtype=torch.int32, device="cuda")
+    qs = torch.zeros_like(full.qscal)
+    R.rbq_quantize_query_bits(2, 8, 2, D, full.q, full.P, None, full.c_k, 8, qp, qs)
+    S = torch.zeros_like(full.scores)
+    R.rbq_score_q8(2, 8, 2, D, n, full.cap, full.codes, full.kfac, qp, qs, S)
+    ip = torch.zeros(2, 8, n, dtype=torch.int32, device="cuda")
+    pc = torch.zeros(2, 2, n, dtype=torch.int32, device="cuda")
+    R.rbq_score_ints_q8(2, 8, 2, D, n, full.cap, full.codes, qp, ip, pc)
+    torch.cuda.synchronize()
+    planes, qsn, Sn = pu.u32(qp), _np(qs), _np(S)
+    codes, kfac = pu.u32(full.codes), _np(full.kfac)
+    for bb in range(2):
+        for h in range(8):
+            qc = pu.planes_to_codes(planes[bb, h])
+            assert qc.max() <= 255
+            ip_or, pc_or = orc.int_dot(orc.unpack_bits(codes[bb, h // 4, :n], D), qc)
+            assert np.array_equal(_np(ip)[bb, h], ip_or) and np.array_equal(_np(pc)[bb, h // 4], pc_or)
+            pu.check_scores(Sn[bb, h, :n], codes[bb, h // 4, :n], kfac[bb, h // 4, :n].astype(np.float64),
+                            planes[bb, h], qsn[bb, h], D=D)
