@@ -197,3 +197,35 @@ def test_compact_ragged_step_matches_ragged_calls(R, pipeline):
                             b.qscal[s:s + 1], S1)
             torch.cuda.synchronize()
             assert np.array_equal(_np(S1)[0].view(np.uint8), x.view(np.uint8))
+
+
+def test_compact_config3_full_size_sampled(R, pipeline):
+    """Config 3's 128K workload on the compact index (the bench's compact_index
+    launch shape) through the fused step with the flush: sampled KV groups and
+    heads against the oracle (codes, fp16 factors, scores with g = 0, the Top-p
+    set, attention)."""
+    wl = gen.config3()
+    st = pipeline.DecodeState.from_workload(wl, compact=True)
+    st.build_index()
+    n, w, G = wl.n_index, wl.w, wl.G
+    tau = 1.0 / math.sqrt(wl.D)
+    for p in (0.9, 0.95):
+        print("compact config3 p", p, flush=True)
+        st.step(p)
+        torch.cuda.synchronize()
+        S, codes, f16 = _np(st.scores), pu.u32(st.codes), _np(st.kfac16).astype(np.float64)
+        planes, qs, ck = pu.u32(st.qplanes), _np(st.qscal), _np(st.c_k)
+        sel, cnt, out, lse = _np(st.sel_idx), _np(st.sel_count), _np(st.out), _np(st.lse)
+        for hk in (0, 5):
+            K, V = wl.K_f32(0, hk).astype(np.float64), wl.V_f32(0, hk).astype(np.float64)
+            enc = orc.encode_keys(K[:n + w], wl.P, c_k=ck[0, hk].astype(np.float64))
+            diff = orc.unpack_bits(codes[0, hk, :n + w], wl.D) != enc["bits"]
+            assert np.all(np.abs(enc["R"][diff]) <= 1e-5 * np.broadcast_to(enc["norm"][:, None], diff.shape)[diff])
+            off = f16[0, hk, :n + w] != orc.compact_factor(enc["f"])
+            assert np.all(_near_binary16_tie(enc["f"])[off])
+            for h in (hk * G, hk * G + 3):
+                fac = np.stack([f16[0, hk, :n], np.zeros(n)], axis=1)
+                pu.check_scores(S[0, h, :n], codes[0, hk, :n], fac, planes[0, h], qs[0, h])
+                got = sel[0, h, :cnt[0, h]]
+                pu.check_topp(S[0, h, :n], p, tau, got)
+                pu.check_attention(out[0, h], lse[0, h], wl.q[0, h], K[:n], V[:n], got, K[n:n + w], V[n:n + w], tau)

@@ -274,3 +274,33 @@ def test_d64_compact_index_and_eight_bit_queries(R, pipeline):
             assert np.array_equal(_np(ip)[bb, h], ip_or) and np.array_equal(_np(pc)[bb, h // 4], pc_or)
             pu.check_scores(Sn[bb, h, :n], codes[bb, h // 4, :n], kfac[bb, h // 4, :n].astype(np.float64),
                             planes[bb, h], qsn[bb, h], D=D)
+
+
+def test_d64_config3_full_size_sampled(R, pipeline):
+    """Config 3's 128K workload at D = 64 (the bench's head_dim_64 launch shape)
+    through the fused step with the flush: sampled KV groups and heads checked
+    against the oracle (codes and factors, scores, the Top-p set, attention)."""
+    wl = gen.config3_d64()
+    st = pipeline.DecodeState.from_workload(wl)
+    st.build_index()
+    n, w, G = wl.n_index, wl.w, wl.G
+    tau = 1.0 / math.sqrt(D)
+    for p in (0.9, 0.95):
+        print("d64 config3 p", p, flush=True)
+        st.step(p)
+        torch.cuda.synchronize()
+        S, codes, kfac = _np(st.scores), pu.u32(st.codes), _np(st.kfac)
+        planes, qs, ck = pu.u32(st.qplanes), _np(st.qscal), _np(st.c_k)
+        sel, cnt, out, lse = _np(st.sel_idx), _np(st.sel_count), _np(st.out), _np(st.lse)
+        for hk in (0, 5):
+            K, V = wl.K_f32(0, hk).astype(np.float64), wl.V_f32(0, hk).astype(np.float64)
+            enc = orc.encode_keys(K[:n + w], wl.P, c_k=ck[0, hk].astype(np.float64), c_q=wl.c_q[0, hk])
+            diff = orc.unpack_bits(codes[0, hk, :n + w], D) != enc["bits"]
+            assert np.all(np.abs(enc["R"][diff]) <= 1e-5 * np.broadcast_to(enc["norm"][:, None], diff.shape)[diff])
+            assert np.all(np.abs(kfac[0, hk, :n + w, 0] - enc["f"]) <= 1e-5 * np.abs(enc["f"]) + 1e-6)
+            for h in (hk * G, hk * G + 3):
+                pu.check_scores(S[0, h, :n], codes[0, hk, :n], kfac[0, hk, :n].astype(np.float64), planes[0, h],
+                                qs[0, h], D=D)
+                got = sel[0, h, :cnt[0, h]]
+                pu.check_topp(S[0, h, :n], p, tau, got)
+                pu.check_attention(out[0, h], lse[0, h], wl.q[0, h], K[:n], V[:n], got, K[n:n + w], V[n:n + w], tau)
