@@ -349,6 +349,19 @@ rbq_status rbq_decode_step_varlen_f16(int32_t batch, int32_t heads_q, int32_t he
                                       int32_t* sel_idx, int32_t* sel_count, float* out, float* lse,
                                       void* ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * rbq_mapped_device_pointer -- the device address of pinned host memory
+ * (hipHostGetDevicePointer), for a K/V cache kept in host memory while the
+ * index stays in HBM (Appendix C: the small index on the GPU, the full cache
+ * offloaded). Every call that takes K / V (or K_loc / V_loc) accepts such an
+ * address; the kernels then read the rows they touch over PCIe.
+ *   host_ptr (host): memory allocated pinned (hipHostMalloc, or a pinned
+ *     allocator); device_ptr (host) out: its device address, NULL on error.
+ * RBQ_EINVAL for a NULL argument; RBQ_EDEVICE when the runtime cannot map the
+ * pointer (not pinned, or not visible to the current device).
+ */
+rbq_status rbq_mapped_device_pointer(const void* host_ptr, void** device_ptr);
+
 /* Workspace bytes needed by `op` (one of RBQ_OP_*) for these sizes; 0 for an
  * unknown op or invalid sizes. Host-only, never touches the device. */
 size_t rbq_workspace_bytes(int32_t op, int32_t batch, int32_t heads_q, int32_t heads_kv,

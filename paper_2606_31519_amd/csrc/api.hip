@@ -60,6 +60,18 @@ rbq_status decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
 
 extern "C" {
 
+rbq_status rbq_mapped_device_pointer(const void* host_ptr, void** device_ptr) {
+  if (host_ptr == nullptr || device_ptr == nullptr) return RBQ_EINVAL;
+  *device_ptr = nullptr;
+  void* d = nullptr;
+  if (hipHostGetDevicePointer(&d, const_cast<void*>(host_ptr), 0) != hipSuccess || d == nullptr) {
+    (void)hipGetLastError();   // leave no error behind for the next call
+    return RBQ_EDEVICE;
+  }
+  *device_ptr = d;
+  return RBQ_OK;
+}
+
 rbq_status rbq_encode_keys_debug(int32_t batch, int32_t heads_kv, int32_t head_dim, const void* keys,
                                  int32_t keys_dtype, int64_t keys_ld, int32_t n_new, int32_t offset, int32_t cap,
                                  const float* P, const float* c_q, float* c_k, uint32_t* codes, float* kfac,

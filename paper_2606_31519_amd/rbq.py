@@ -27,7 +27,7 @@ EXPORTED = [
     "rbq_encode_keys_debug", "rbq_quantize_query_debug", "rbq_score_ints",
     "rbq_score_varlen", "rbq_topp_select_varlen", "rbq_sparse_decode_varlen", "rbq_dense_decode_varlen",
     "rbq_decode_step_varlen", "rbq_quantize_query_bits",
-    "rbq_score_q8", "rbq_score_ints_q8",
+    "rbq_score_q8", "rbq_score_ints_q8", "rbq_mapped_device_pointer",
     "rbq_encode_keys_f16", "rbq_score_f16", "rbq_decode_step_f16", "rbq_score_varlen_f16", "rbq_decode_step_varlen_f16",
 ]
 
@@ -69,6 +69,7 @@ def _load():
         "rbq_decode_step_varlen": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp,
                                    i32, vp, f32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
         "rbq_score_q8": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp],
+        "rbq_mapped_device_pointer": [vp, ctypes.POINTER(vp)],
         "rbq_score_ints_q8": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp],
         # the compact index (fp16 factors, no c_q)
         "rbq_encode_keys_f16": [i32, i32, i32, vp, i32, i64, i32, i32, i32, vp, vp, vp, vp, u32, vp, sz, vp],
@@ -132,14 +133,9 @@ class MappedHost:
         if t.device.type != "cpu" or not t.is_pinned() or not t.is_contiguous():
             raise ValueError("a host K/V buffer must be a contiguous pinned CPU tensor (pin_memory=True)")
         if _base is None:
-            # the HIP runtime of this process (torch and librbq.so load the same one)
-            hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | ctypes.RTLD_GLOBAL)
-            hip.hipHostGetDevicePointer.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_void_p, ctypes.c_uint]
-            hip.hipHostGetDevicePointer.restype = ctypes.c_int
             dev = ctypes.c_void_p()
-            st = hip.hipHostGetDevicePointer(ctypes.byref(dev), ctypes.c_void_p(t.data_ptr()), 0)
-            if st != 0 or not dev.value:
-                raise RuntimeError(f"hipHostGetDevicePointer failed ({st}): the buffer is not mapped for the device")
+            _check("rbq_mapped_device_pointer", lib.rbq_mapped_device_pointer(ctypes.c_void_p(t.data_ptr()),
+                                                                              ctypes.byref(dev)))
             _base = dev.value
         self.tensor, self.dtype, self._base, self._offset = t, t.dtype, _base, _offset
 

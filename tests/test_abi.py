@@ -234,3 +234,9 @@ def test_every_call_validates_at_head_dim_64(lib):
     assert L.rbq_score(1, 8, 4, 64, 11, 10, FAKE, FAKE, FAKE, FAKE, FAKE, 0) == EINVAL
     assert lib.rbq_workspace_bytes(lib.RBQ_OP_DECODE_STEP, 1, 8, 4, 64, 1000, 16) < \
         lib.rbq_workspace_bytes(lib.RBQ_OP_DECODE_STEP, 1, 8, 4, 128, 1000, 16)
+
+
+def test_mapped_device_pointer_rejects_null_arguments(lib):
+    out = ctypes.c_void_p(123)
+    assert lib.lib.rbq_mapped_device_pointer(None, ctypes.byref(out)) == lib.RBQ_EINVAL
+    assert lib.lib.rbq_mapped_device_pointer(ctypes.c_void_p(FAKE), None) == lib.RBQ_EINVAL
