@@ -194,3 +194,63 @@ class DecodeState:
         rbq.rbq_dense_decode_varlen(self.B, self.Hq, self.Hkv, self.D, self.q, self.K, self.V, self.cap, self.n,
                                     self.w, seq_n, seq_w, self.sm_scale, self.out if out is None else out,
                                     self.lse if lse is None else lse, self.ws_decode, stream)
+
+
+class DecodeSession:
+    """A decode loop over one growing cache: the lazy index update of Section
+    3.4 as a serving loop would run it. The cache holds `cap` rows per (sequence,
+    KV head). The prefill rows [0, n) are indexed once (with their centroid);
+    each generated token's key and value are appended to the window after the
+    indexed rows, each step attends over the Top-p selection of the index plus
+    the whole window (one rbq_decode_step), and the step that finds the window
+    full also flushes it into the index (encoded with the prefill centroid), so
+    the next step scores n + window keys. Buffers and workspaces are sized once,
+    for the largest index the cache can hold.
+
+    K, V: [B][Hkv][cap][D] device tensors holding the prefill rows; P: the
+    rotation; c_q: query centroids or None."""
+
+    def __init__(self, B, Hq, Hkv, D, cap, n_prefill, window, K, V, P, c_q=None, device="cuda"):
+        if not 0 < window <= rbq.RBQ_MAX_WINDOW or n_prefill + window > cap:
+            raise ValueError("the window must fit after the prefill rows (n_prefill + window <= cap)")
+        q = torch.zeros(B, Hq, D, dtype=torch.float32, device=device)
+        # sized for the largest index: every buffer and workspace grows with n
+        self.state = DecodeState(B, Hq, Hkv, D, cap, cap - window, window, K, V, q, P, c_q, device)
+        self.n, self.w, self.window = n_prefill, 0, window
+        st = self.state
+        # the step workspace is not monotonic in n (smaller indexes may take more,
+        # shorter decode splits): size it for every index size the loop will pass
+        need = max(rbq.rbq_workspace_bytes(rbq.RBQ_OP_DECODE_STEP, B, Hq, Hkv, D, m, window)
+                   for m in range(n_prefill, cap - window + 1, window))
+        if need > st.ws_step.numel():
+            st.ws_step = torch.empty(need, dtype=torch.uint8, device=device)
+        rbq.rbq_encode_keys(B, Hkv, D, K, cap, n_prefill, 0, cap, P, c_q, st.c_k, st.codes, st.kfac,
+                            rbq.RBQ_ENCODE_SET_CENTROID, None, st.ws_encode)
+
+    def append(self, k: torch.Tensor, v: torch.Tensor):
+        """Append one token's key and value ([B][Hkv][D]) to the window."""
+        if self.w == self.window:
+            raise RuntimeError("the window is full: run step() first (it flushes the window)")
+        if self.n + self.w >= self.state.cap:
+            raise RuntimeError("the cache is full")
+        r = self.n + self.w
+        self.state.K[:, :, r].copy_(k)
+        self.state.V[:, :, r].copy_(v)
+        self.w += 1
+
+    def step(self, q: torch.Tensor, p: float, stream=None) -> bool:
+        """One decode step for the query q [B][Hq][D] at Top-p p; returns whether
+        the window was flushed into the index. The outputs are state.out and
+        state.lse; the selection is state.sel_idx / state.sel_count (row stride:
+        the n of this step, self.n before a flush)."""
+        st = self.state
+        st.q.copy_(q)
+        flush = self.w == self.window
+        rbq.rbq_decode_step(st.B, st.Hq, st.Hkv, st.D, st.q, st.P, st.c_q, st.c_k, st.K, st.V, st.cap, self.n, self.w,
+                            st.codes, st.kfac, flush, p, st.sm_scale, st.qplanes, st.qscal, st.scores, st.sel_idx,
+                            st.sel_count, st.out, st.lse, st.ws_step, stream)
+        self.last_n, self.last_w = self.n, self.w
+        if flush:
+            self.n += self.w
+            self.w = 0
+        return flush

@@ -20,6 +20,7 @@ RBQ_F32, RBQ_BF16 = 0, 1
 RBQ_ENCODE_SET_CENTROID = 1
 RBQ_OP_ENCODE, RBQ_OP_TOPP, RBQ_OP_SPARSE_DECODE, RBQ_OP_DENSE_DECODE, RBQ_OP_DECODE_STEP = 1, 2, 3, 4, 5
 QSCAL_STRIDE = 8
+RBQ_MAX_WINDOW = 4096   # largest local window accepted by the decode calls
 
 EXPORTED = [
     "rbq_encode_keys", "rbq_quantize_query", "rbq_score", "rbq_topp_select", "rbq_sparse_decode",

@@ -1,0 +1,82 @@
+"""A decode loop over a growing cache (pipeline.DecodeSession, the lazy index
+update of Section 3.4): one token appended per step, the window flushed into
+the index by the step that finds it full. Across three flushes the index rows
+of the flushed tokens are the oracle's encoding with the prefill centroid, the
+index grows by the window each time, and each checked step's Top-p set and
+attention (selection of the current index plus the current window) match the
+oracle."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import rbq_oracle as orc
+from workloads import gen
+import parity_util as pu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def pipeline():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2606_31519_amd import pipeline as pl
+    return pl
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def test_session_grows_the_index_through_lazy_flushes(pipeline):
+    B, Hq, Hkv, D = 1, 8, 2, 128
+    n0, window, steps = 3000, 32, 100          # the 32nd, 64th and 96th steps flush (their window is full)
+    cap = n0 + 4 * window
+    wl = gen.random_case(B, Hq, Hkv, cap, seed=71, kv_dtype="bf16", q_scale=5.0)
+    K = pipeline.to_device_kv(wl.K, wl.kv_dtype, "cuda")
+    V = pipeline.to_device_kv(wl.V, wl.kv_dtype, "cuda")
+    P = torch.from_numpy(np.ascontiguousarray(wl.P)).cuda()
+    # the "generated" tokens are the rows after the prefill, appended one per step
+    K_new, V_new = K[:, :, n0:].clone(), V[:, :, n0:].clone()
+    K[:, :, n0:] = 0
+    V[:, :, n0:] = 0
+    ses = pipeline.DecodeSession(B, Hq, Hkv, D, cap, n0, window, K, V, P)
+    rng = np.random.default_rng(3)
+    tau = 1.0 / math.sqrt(D)
+    G = Hq // Hkv
+    Kf = np.stack([wl.K_f32(0, hk) for hk in range(Hkv)]).astype(np.float64)   # [Hkv][cap][D]
+    Vf = np.stack([wl.V_f32(0, hk) for hk in range(Hkv)]).astype(np.float64)
+    ck = None
+    flushes = 0
+    for t in range(steps):
+        ses.append(K_new[:, :, t], V_new[:, :, t])
+        q = torch.from_numpy((5.0 * rng.standard_normal((B, Hq, D))).astype(np.float32)).cuda()
+        n_before, w_before = ses.n, ses.w
+        flushed = ses.step(q, 0.9)
+        torch.cuda.synchronize()
+        if ck is None:
+            ck = _np(ses.state.c_k[0]).astype(np.float64)
+        if flushed:
+            flushes += 1
+            assert ses.n == n_before + window and ses.w == 0
+            codes, kfac = pu.u32(ses.state.codes[0]), _np(ses.state.kfac[0]).astype(np.float64)
+            for hk in range(Hkv):
+                rows = slice(n_before, n_before + window)
+                enc = orc.encode_keys(Kf[hk, rows], wl.P, c_k=ck[hk])
+                diff = orc.unpack_bits(codes[hk, rows], D) != enc["bits"]
+                assert np.all(np.abs(enc["R"][diff]) <= 1e-5 * np.broadcast_to(enc["norm"][:, None], diff.shape)[diff])
+                assert np.all(np.abs(kfac[hk, rows, 0] - enc["f"]) <= 1e-5 * enc["f"] + 1e-6)
+        if flushed or t in (0, 50):
+            n, w = n_before, w_before
+            S = _np(ses.state.scores).reshape(-1)[:B * Hq * n].reshape(B, Hq, n)
+            cnt = _np(ses.state.sel_count)
+            sel = _np(ses.state.sel_idx).reshape(-1)[:B * Hq * n].reshape(B, Hq, n)
+            out, lse = _np(ses.state.out), _np(ses.state.lse)
+            for h in (0, Hq - 1):
+                hk = h // G
+                got = sel[0, h, :cnt[0, h]]
+                pu.check_topp(S[0, h], 0.9, tau, got)
+                pu.check_attention(out[0, h], lse[0, h], _np(q)[0, h].astype(np.float64), Kf[hk, :n], Vf[hk, :n],
+                                   got, Kf[hk, n:n + w], Vf[hk, n:n + w], tau)
+    assert flushes == 3 and ses.n == n0 + 3 * window
