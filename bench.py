@@ -642,6 +642,10 @@ def main():
     call_graphs = [_graph(torch, lambda r=r: r.step_calls(p)) for r in reps]
     ms_step_calls = _time_graphs(torch, call_graphs, args.steps, args.warmup)
     del call_graphs
+    # the step without the flush: a serving loop flushes the window once per `w` tokens
+    nf_graphs = [_graph(torch, lambda r=r: r.step(p, flush=False)) for r in reps]
+    ms_step_noflush = _time_graphs(torch, nf_graphs, args.steps, args.warmup)
+    del nf_graphs
     # each stage on its own: one graph runs it REPS times back-to-back over the replicas, so the
     # graph launch is amortised and the time per run is that of the stage's kernels plus launch gaps
     REPS = 16
@@ -771,6 +775,10 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms_step,
         "ms_per_step_five_calls": ms_step_calls,
+        # a serving loop's per-token cost: the step without the flush plus the
+        # flush of the window (stages.flush) spread over the w tokens it holds
+        "ms_per_step_flush_amortized": ms_step_noflush + stage_ms["flush"] / max(st0.w, 1),
+        "ms_per_step_no_flush": ms_step_noflush,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
