@@ -212,6 +212,23 @@ def _time_graphs(torch, graphs, steps, warmup):
     return a.elapsed_time(b) / steps
 
 
+def _replay_distribution(torch, graphs, reps=50, warmup=10):
+    """Per-replay durations (HIP events around each replay, the replicas in turn):
+    p10 / median / p90 in ms."""
+    for i in range(warmup):
+        graphs[i % len(graphs)].replay()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record()
+    for i in range(reps):
+        graphs[i % len(graphs)].replay()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    d = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)])
+    return {"reps": reps, "warmup": warmup, "p10_ms": float(np.percentile(d, 10)), "median_ms": float(np.median(d)),
+            "p90_ms": float(np.percentile(d, 90))}
+
+
 def time_scan_c5(pipeline, gen, torch, steps, warmup, replicas=4):
     """Standalone rbq_score scan on the wide-head workload (batch 4 x 128K, 64/8 heads)."""
     wl = gen.config5()
@@ -639,6 +656,7 @@ def main():
     # as the five separate calls, for reference
     step_graphs = [_graph(torch, lambda r=r: r.step(p)) for r in reps]
     ms_step = _time_graphs(torch, step_graphs, args.steps, args.warmup)
+    step_dist = _replay_distribution(torch, step_graphs)
     call_graphs = [_graph(torch, lambda r=r: r.step_calls(p)) for r in reps]
     ms_step_calls = _time_graphs(torch, call_graphs, args.steps, args.warmup)
     del call_graphs
@@ -775,6 +793,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms_step,
         "ms_per_step_five_calls": ms_step_calls,
+        "step_distribution": step_dist,
         # a serving loop's per-token cost: the step without the flush plus the
         # flush of the window (stages.flush) spread over the w tokens it holds
         "ms_per_step_flush_amortized": ms_step_noflush + stage_ms["flush"] / max(st0.w, 1),
