@@ -324,6 +324,15 @@ def time_ragged(pipeline, gen, torch, steps, warmup, seed=20260):
     sparse_bytes = (union + win_rows) * row_bytes + int(cnt.sum()) * 4 + B * st.Hq * st.D * 4
     dense_bytes = (idx_rows + win_rows) * row_bytes
     frac = cnt / np.repeat(seq_n, st.Hq).reshape(B, st.Hq)
+    hist_edges = [0.0, 0.005, 0.01, 0.02, 0.05, 0.1, 0.2, 0.5, 1.0]
+    hist = np.histogram(frac.reshape(-1), bins=hist_edges)[0]
+    # the batch's standalone score scan at the uniform length (every sequence at n = 32512, the
+    # 16 x 32K scan of 160 MiB): rbq_score over the whole batch, 8 calls per graph
+    calls = 8
+    g = _graph(torch, lambda: [st.score() for _ in range(calls)])
+    ms_scan = _time_graphs(torch, [g], max(2, steps // 2), warmup) / calls
+    del g
+    scan_bytes = B * st.Hkv * st.n * (st.D // 8 + 8) + B * st.Hq * st.n * 4
     return {"workload": "gqa 32q/8kv b=16 bf16 ragged: indexed keys ~ U(2048, 32512), window ~ U(0, 256), "
                         "p ~ U(0.80, 0.95) per sequence; planted fraction ~ U(0.1 %, 10 %)",
             "seq_n": seq_n.tolist(), "seq_w": seq_w.tolist(), "seq_p": [float(x) for x in seq_p],
@@ -333,7 +342,11 @@ def time_ragged(pipeline, gen, torch, steps, warmup, seed=20260):
             "sparse_decode": {"ms": ms_sparse, "bytes": float(sparse_bytes),
                               "GBps": sparse_bytes / (ms_sparse * 1e-3) / 1e9,
                               "frac_hbm": sparse_bytes / (ms_sparse * 1e-3) / 1e9 / HBM_PEAK_GBS},
-            "budget_frac_mean": float(frac.mean()), "union_frac": union / idx_rows}
+            "budget_frac_mean": float(frac.mean()), "union_frac": union / idx_rows,
+            "budget_frac_per_sequence": [float(x) for x in frac.mean(axis=1)],
+            "budget_frac_histogram": {"edges": hist_edges, "heads": [int(x) for x in hist]},
+            "scan_uniform_16x32k": {"ms": ms_scan, "bytes": scan_bytes, "GBps": scan_bytes / (ms_scan * 1e-3) / 1e9,
+                                    "frac_hbm": scan_bytes / (ms_scan * 1e-3) / 1e9 / HBM_PEAK_GBS}}
 
 
 def quality(pipeline, torch, st, p_list, seed=20261):
