@@ -445,6 +445,30 @@ def quality(pipeline, torch, st, p_list, seed=20261):
     return out
 
 
+# (batch, keys, heads, head_dim): the shapes of the paper's score-kernel ablation (Table kernel_ablation)
+ABLATION_SHAPES = [(1, 1024, 8, 128), (1, 4096, 8, 128), (1, 8192, 8, 128), (1, 16384, 8, 128), (4, 4096, 8, 128),
+                   (8, 4096, 8, 128), (1, 4096, 32, 128), (1, 8192, 8, 64)]
+
+
+def time_ablation_shapes(pipeline, gen, torch, steps, warmup):
+    """rbq_score on the shapes of Table kernel_ablation, each head its own KV head
+    (G = 1): mean time per call in a graph of 16 calls (the launch gaps included)."""
+    out = []
+    for (b, n, h, d) in ABLATION_SHAPES:
+        wl = gen.random_case(b, h, h, n, D=d, seed=n + h + d, kv_dtype="bf16")
+        st = pipeline.DecodeState.from_workload(wl)
+        st.build_index()
+        st.quantize()
+        torch.cuda.synchronize()
+        calls = 16
+        g = _graph(torch, lambda: [st.score() for _ in range(calls)])
+        ms = _time_graphs(torch, [g], max(4, steps), warmup) / calls
+        del g
+        nbytes = b * h * n * (d // 8 + 8) + b * h * n * 4
+        out.append({"shape": [b, n, h, d], "us": ms * 1e3, "GBps": nbytes / (ms * 1e-3) / 1e9})
+    return out
+
+
 def time_d64(pipeline, gen, torch, steps, warmup, replicas=4):
     """The 128K step at head dimension 64 (config 3's generator at D = 64):
     rbq_decode_step per p against the dense decode of the same rows, and the
@@ -629,6 +653,7 @@ def main():
     ap.add_argument("--no-offload", action="store_true", help="skip the step with the K/V cache in host memory")
     ap.add_argument("--no-compact", action="store_true", help="skip the step on the compact (fp16-factor) index")
     ap.add_argument("--no-d64", action="store_true", help="skip the step at head dimension 64")
+    ap.add_argument("--no-ablation", action="store_true", help="skip the score call on the kernel-ablation shapes")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
@@ -785,6 +810,7 @@ def main():
     torch.cuda.empty_cache()
     d64 = None if args.no_d64 else time_d64(pipeline, gen, torch, args.steps, args.warmup)
     torch.cuda.empty_cache()
+    ablation = None if args.no_ablation else time_ablation_shapes(pipeline, gen, torch, args.steps, args.warmup)
 
     cpu = None if args.no_cpu else cpu_baseline(wl)
 
@@ -835,6 +861,7 @@ def main():
         "kv_in_host_memory": offloaded,
         "compact_index": compact,
         "head_dim_64": d64,
+        "score_ablation_shapes": ablation,
         "cpu_baseline": cpu,
         "gen_s": t_gen,
         "git": _git_sha(),
