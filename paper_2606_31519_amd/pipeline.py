@@ -208,14 +208,15 @@ class DecodeSession:
     for the largest index the cache can hold.
 
     K, V: [B][Hkv][cap][D] device tensors holding the prefill rows; P: the
-    rotation; c_q: query centroids or None."""
+    rotation; c_q: query centroids or None; compact: the fp16-factor index
+    (then without c_q)."""
 
-    def __init__(self, B, Hq, Hkv, D, cap, n_prefill, window, K, V, P, c_q=None, device="cuda"):
+    def __init__(self, B, Hq, Hkv, D, cap, n_prefill, window, K, V, P, c_q=None, device="cuda", compact=False):
         if not 0 < window <= rbq.RBQ_MAX_WINDOW or n_prefill + window > cap:
             raise ValueError("the window must fit after the prefill rows (n_prefill + window <= cap)")
         q = torch.zeros(B, Hq, D, dtype=torch.float32, device=device)
         # sized for the largest index: every buffer and workspace grows with n
-        self.state = DecodeState(B, Hq, Hkv, D, cap, cap - window, window, K, V, q, P, c_q, device)
+        self.state = DecodeState(B, Hq, Hkv, D, cap, cap - window, window, K, V, q, P, c_q, device, compact)
         self.n, self.w, self.window = n_prefill, 0, window
         st = self.state
         # the step workspace is not monotonic in n (smaller indexes may take more,
@@ -224,8 +225,12 @@ class DecodeSession:
                    for m in range(n_prefill, cap - window + 1, window))
         if need > st.ws_step.numel():
             st.ws_step = torch.empty(need, dtype=torch.uint8, device=device)
-        rbq.rbq_encode_keys(B, Hkv, D, K, cap, n_prefill, 0, cap, P, c_q, st.c_k, st.codes, st.kfac,
-                            rbq.RBQ_ENCODE_SET_CENTROID, None, st.ws_encode)
+        if compact:
+            rbq.rbq_encode_keys_f16(B, Hkv, D, K, cap, n_prefill, 0, cap, P, st.c_k, st.codes, st.kfac16,
+                                    rbq.RBQ_ENCODE_SET_CENTROID, st.ws_encode)
+        else:
+            rbq.rbq_encode_keys(B, Hkv, D, K, cap, n_prefill, 0, cap, P, c_q, st.c_k, st.codes, st.kfac,
+                                rbq.RBQ_ENCODE_SET_CENTROID, None, st.ws_encode)
 
     def append(self, k: torch.Tensor, v: torch.Tensor):
         """Append one token's key and value ([B][Hkv][D]) to the window."""
@@ -246,9 +251,14 @@ class DecodeSession:
         st = self.state
         st.q.copy_(q)
         flush = self.w == self.window
-        rbq.rbq_decode_step(st.B, st.Hq, st.Hkv, st.D, st.q, st.P, st.c_q, st.c_k, st.K, st.V, st.cap, self.n, self.w,
-                            st.codes, st.kfac, flush, p, st.sm_scale, st.qplanes, st.qscal, st.scores, st.sel_idx,
-                            st.sel_count, st.out, st.lse, st.ws_step, stream)
+        if st.compact:
+            rbq.rbq_decode_step_f16(st.B, st.Hq, st.Hkv, st.D, st.q, st.P, st.c_k, st.K, st.V, st.cap, self.n,
+                                    self.w, st.codes, st.kfac16, flush, p, st.sm_scale, st.qplanes, st.qscal,
+                                    st.scores, st.sel_idx, st.sel_count, st.out, st.lse, st.ws_step, stream)
+        else:
+            rbq.rbq_decode_step(st.B, st.Hq, st.Hkv, st.D, st.q, st.P, st.c_q, st.c_k, st.K, st.V, st.cap, self.n,
+                                self.w, st.codes, st.kfac, flush, p, st.sm_scale, st.qplanes, st.qscal, st.scores,
+                                st.sel_idx, st.sel_count, st.out, st.lse, st.ws_step, stream)
         self.last_n, self.last_w = self.n, self.w
         if flush:
             self.n += self.w

@@ -4,7 +4,7 @@ the index by the step that finds it full. Across three flushes the index rows
 of the flushed tokens are the oracle's encoding with the prefill centroid, the
 index grows by the window each time, and each checked step's Top-p set and
 attention (selection of the current index plus the current window) match the
-oracle."""
+oracle. Run at D = 128 and 64 on the full index and on the compact index."""
 import math
 
 import numpy as np
@@ -29,11 +29,13 @@ def _np(t):
     return t.detach().cpu().numpy()
 
 
-def test_session_grows_the_index_through_lazy_flushes(pipeline):
-    B, Hq, Hkv, D = 1, 8, 2, 128
+@pytest.mark.parametrize("D,compact", [(128, False), (64, False), (128, True)])
+def test_session_grows_the_index_through_lazy_flushes(pipeline, D, compact):
+    print("session D", D, "compact", compact, flush=True)
+    B, Hq, Hkv = 1, 8, 2
     n0, window, steps = 3000, 32, 100          # the 32nd, 64th and 96th steps flush (their window is full)
     cap = n0 + 4 * window
-    wl = gen.random_case(B, Hq, Hkv, cap, seed=71, kv_dtype="bf16", q_scale=5.0)
+    wl = gen.random_case(B, Hq, Hkv, cap, D=D, seed=71, kv_dtype="bf16", q_scale=5.0)
     K = pipeline.to_device_kv(wl.K, wl.kv_dtype, "cuda")
     V = pipeline.to_device_kv(wl.V, wl.kv_dtype, "cuda")
     P = torch.from_numpy(np.ascontiguousarray(wl.P)).cuda()
@@ -41,7 +43,7 @@ def test_session_grows_the_index_through_lazy_flushes(pipeline):
     K_new, V_new = K[:, :, n0:].clone(), V[:, :, n0:].clone()
     K[:, :, n0:] = 0
     V[:, :, n0:] = 0
-    ses = pipeline.DecodeSession(B, Hq, Hkv, D, cap, n0, window, K, V, P)
+    ses = pipeline.DecodeSession(B, Hq, Hkv, D, cap, n0, window, K, V, P, compact=compact)
     rng = np.random.default_rng(3)
     tau = 1.0 / math.sqrt(D)
     G = Hq // Hkv
@@ -60,13 +62,18 @@ def test_session_grows_the_index_through_lazy_flushes(pipeline):
         if flushed:
             flushes += 1
             assert ses.n == n_before + window and ses.w == 0
-            codes, kfac = pu.u32(ses.state.codes[0]), _np(ses.state.kfac[0]).astype(np.float64)
+            codes = pu.u32(ses.state.codes[0])
+            fac = _np(ses.state.kfac16[0] if compact else ses.state.kfac[0][..., 0]).astype(np.float64)
             for hk in range(Hkv):
                 rows = slice(n_before, n_before + window)
                 enc = orc.encode_keys(Kf[hk, rows], wl.P, c_k=ck[hk])
                 diff = orc.unpack_bits(codes[hk, rows], D) != enc["bits"]
                 assert np.all(np.abs(enc["R"][diff]) <= 1e-5 * np.broadcast_to(enc["norm"][:, None], diff.shape)[diff])
-                assert np.all(np.abs(kfac[hk, rows, 0] - enc["f"]) <= 1e-5 * enc["f"] + 1e-6)
+                if compact:   # the fp16 factor: the oracle's rounding, or one step off at a near-tie
+                    want = orc.compact_factor(enc["f"])
+                    assert np.all((fac[hk, rows] == want) | (np.abs(fac[hk, rows] - want) <= 2.0 ** -10 * want))
+                else:
+                    assert np.all(np.abs(fac[hk, rows] - enc["f"]) <= 1e-5 * enc["f"] + 1e-6)
         if flushed or t in (0, 50):
             n, w = n_before, w_before
             S = _np(ses.state.scores).reshape(-1)[:B * Hq * n].reshape(B, Hq, n)
