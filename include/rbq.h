@@ -172,6 +172,8 @@ rbq_status rbq_score_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
  * fp32 exponentials, so the set may differ from an exact-arithmetic one only
  * where the cumulative mass passes p within ~1e-6.
  *   p (host) in (0, 1]; sm_scale (host) > 0, usually 1/sqrt(D).
+ *   n < 2^24 (16,777,216) keys per row: the masses of a row are summed as
+ *     64-bit integers of up to 2^40 each; a longer row gives RBQ_EUNSUPPORTED.
  *   sel_idx   [B][Hq][n] int32 out: the first sel_count[r] entries of row r are
  *             the selected key indices in ascending order; the rest is unspecified.
  *   sel_count [B][Hq] int32 out.
@@ -373,36 +375,6 @@ size_t rbq_index_bytes(int32_t batch, int32_t heads_kv, int32_t head_dim, int32_
 
 const char* rbq_status_string(rbq_status s);
 int32_t rbq_version(void);
-
-/*
- * Test hooks. They run the same kernels as the calls above and additionally
- * expose intermediate values, so that integer and sign decisions can be
- * checked exactly against the oracle given the same floating-point inputs.
- *   rbq_encode_keys_debug: as rbq_encode_keys, plus rot_out [B][Hkv][n_new][D]
- *     float = the fp32 rotated centred keys whose signs became the codes.
- *   rbq_quantize_query_debug: as rbq_quantize_query, plus qrot_out [B][Hq][D]
- *     float = the fp32 rotated unit query that was quantised.
- *   rbq_score_ints: ip_out [B][Hq][n] int32 = <c_b, q_u>, pc_out [B][Hkv][n]
- *     int32 = popcount(c_b), computed by the score kernel's integer path;
- *     rbq_score_ints_q8 the same from 8-plane queries (rbq_score_q8's path).
- */
-rbq_status rbq_encode_keys_debug(int32_t batch, int32_t heads_kv, int32_t head_dim,
-                                 const void* keys, int32_t keys_dtype, int64_t keys_ld,
-                                 int32_t n_new, int32_t offset, int32_t cap,
-                                 const float* P, const float* c_q, float* c_k,
-                                 uint32_t* codes, float* kfac, uint32_t flags,
-                                 float* alpha_out, void* ws, size_t ws_bytes,
-                                 float* rot_out, hipStream_t stream);
-rbq_status rbq_quantize_query_debug(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
-                                    const float* q, const float* P, const float* c_q, const float* c_k,
-                                    uint32_t* qplanes, float* qscal, float* qrot_out,
-                                    hipStream_t stream);
-rbq_status rbq_score_ints(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
-                          int32_t n, int32_t cap, const uint32_t* codes, const uint32_t* qplanes,
-                          int32_t* ip_out, int32_t* pc_out, hipStream_t stream);
-rbq_status rbq_score_ints_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
-                             int32_t n, int32_t cap, const uint32_t* codes, const uint32_t* qplanes8,
-                             int32_t* ip_out, int32_t* pc_out, hipStream_t stream);
 
 #ifdef __cplusplus
 }

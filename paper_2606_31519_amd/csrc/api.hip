@@ -44,12 +44,11 @@ rbq_status decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
   else
     s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, 4, head_dim);
   if (s != RBQ_OK) return s;
-  const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
   s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   sw.slot_max, tw.hist, rows * kHistPerRow, nullptr, kfac16, 4, head_dim);
+                   nullptr, kfac16, 4, head_dim);
   if (s != RBQ_OK) return s;
-  s = launch_topp(int32_t(rows), n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
-                  score_blocks_per_row(batch, heads_kv, n), sw.masks);
+  s = launch_topp(int32_t(rows), n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, stream, heads_q / heads_kv,
+                  sw.masks);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, cap, w,
                        sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), nullptr, nullptr,
@@ -122,7 +121,7 @@ rbq_status rbq_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t h
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores);
   if (s != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr,
-                      stream, nullptr, nullptr, 0, nullptr, nullptr, 4, head_dim);
+                      stream, nullptr, nullptr, 4, head_dim);
 }
 
 rbq_status rbq_encode_keys_f16(int32_t batch, int32_t heads_kv, int32_t head_dim, const void* keys,
@@ -142,7 +141,7 @@ rbq_status rbq_score_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac16, qplanes, qscal, scores);
   if (s != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, qscal, scores, nullptr, nullptr,
-                      stream, nullptr, nullptr, 0, nullptr, kfac16, 4, head_dim);
+                      stream, nullptr, kfac16, 4, head_dim);
 }
 
 rbq_status rbq_score_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
@@ -151,7 +150,7 @@ rbq_status rbq_score_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes8, qscal, scores);
   if (s != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes8, qscal, scores, nullptr, nullptr,
-                      stream, nullptr, nullptr, 0, nullptr, nullptr, 8, head_dim);
+                      stream, nullptr, nullptr, 8, head_dim);
 }
 
 rbq_status rbq_score_ints_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
@@ -161,7 +160,7 @@ rbq_status rbq_score_ints_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, i
                                    ip_out);
   if (s != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes8, nullptr, nullptr, ip_out, pc_out,
-                      stream, nullptr, nullptr, 0, nullptr, nullptr, 8, head_dim);
+                      stream, nullptr, nullptr, 8, head_dim);
 }
 
 rbq_status rbq_score_ints(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n, int32_t cap,
@@ -171,7 +170,7 @@ rbq_status rbq_score_ints(int32_t batch, int32_t heads_q, int32_t heads_kv, int3
   const rbq_status s = check_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, ip_out, qplanes, pc_out, ip_out);
   if (s != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, nullptr, nullptr, ip_out, pc_out,
-                      stream, nullptr, nullptr, 0, nullptr, nullptr, 4, head_dim);
+                      stream, nullptr, nullptr, 4, head_dim);
 }
 
 rbq_status rbq_topp_select(int32_t batch, int32_t heads_q, int32_t n, const float* scores, float p, float sm_scale,
@@ -291,12 +290,11 @@ rbq_status decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, 
   else
     s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, 4, head_dim);
   if (s != RBQ_OK) return s;
-  const ToppWorkspace tw = topp_workspace(sw.topp, rows, n);
   s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   sw.slot_max, tw.hist, rows * kHistPerRow, seq_n, kfac16, 4, head_dim);
+                   seq_n, kfac16, 4, head_dim);
   if (s != RBQ_OK) return s;
-  s = launch_topp(int32_t(rows), n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.slot_max,
-                  score_blocks_per_row(batch, heads_kv, n), sw.masks, seq_n, seq_p, heads_q);
+  s = launch_topp(int32_t(rows), n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, stream, heads_q / heads_kv,
+                  sw.masks, seq_n, seq_p, heads_q);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K, V, cap, w,
                        sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), seq_n, seq_w,
@@ -314,7 +312,7 @@ rbq_status rbq_score_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, in
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, 0, cap, seq_n, nullptr)) != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr,
-                      stream, nullptr, nullptr, 0, seq_n, nullptr, 4, head_dim);
+                      stream, seq_n, nullptr, 4, head_dim);
 }
 
 rbq_status rbq_score_varlen_f16(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
@@ -324,7 +322,7 @@ rbq_status rbq_score_varlen_f16(int32_t batch, int32_t heads_q, int32_t heads_kv
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, 0, cap, seq_n, nullptr)) != RBQ_OK) return s;
   return launch_score(batch, heads_q, heads_kv, n, cap, codes, nullptr, qplanes, qscal, scores, nullptr, nullptr,
-                      stream, nullptr, nullptr, 0, seq_n, kfac16, 4, head_dim);
+                      stream, seq_n, kfac16, 4, head_dim);
 }
 
 rbq_status rbq_topp_select_varlen(int32_t batch, int32_t heads_q, int32_t n, const int32_t* seq_n,
@@ -335,8 +333,8 @@ rbq_status rbq_topp_select_varlen(int32_t batch, int32_t heads_q, int32_t n, con
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, 0, n, seq_n, nullptr)) != RBQ_OK) return s;
   if (seq_p == nullptr || (reinterpret_cast<uintptr_t>(seq_p) & 15u) != 0) return RBQ_EINVAL;
-  return launch_topp(batch * heads_q, n, scores, 0.5f, sm_scale, sel_idx, sel_count, ws, stream, nullptr, 0, nullptr,
-                     seq_n, seq_p, heads_q);
+  return launch_topp(batch * heads_q, n, scores, 0.5f, sm_scale, sel_idx, sel_count, ws, stream, 1, nullptr, seq_n,
+                     seq_p, heads_q);
 }
 
 rbq_status rbq_sparse_decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,

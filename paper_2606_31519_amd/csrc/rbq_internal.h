@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "../../include/rbq.h"
+#include "../../include/rbq_testing.h"
 
 namespace rbq {
 
@@ -33,22 +34,37 @@ rbq_status check_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
                         size_t ws_bytes);
 
 // ---------------------------------------------------------------- workspace layouts
-// Top-p: per row, the scores are cut into chunks of kToppChunk; three radix
-// levels of 12, 12 and 8 bits of the order-preserving score key.
-constexpr int kToppThreads = 256;
-constexpr int kToppPerThread = 16;
-constexpr int kToppChunk = kToppThreads * kToppPerThread;   // 4096 scores per block
-constexpr int kBins1 = 4096, kBins2 = 4096, kBins3 = 256;
-constexpr int kCoarse = 64;                                   // coarse bins (of 64 fine bins) of levels 1 and 2
-constexpr int kHistPerRow = kBins1 + kBins2 + kBins3 + 2 * kCoarse;   // uint64 counters per row
-constexpr int kToppStateWords = 8;                          // per-row uint32 state
+// Top-p: each row of scores is cut into parts of spb sub-chunks of kSelSub
+// keys; one block of kSelThreads threads per (row, part) in each of three
+// passes (per-part histograms, candidate gathering, final select + write).
+constexpr int kSelThreads = 1024;
+constexpr int kSelPerThread = 16;
+constexpr int kSelSub = kSelThreads * kSelPerThread;   // 16384 keys per sub-chunk
+constexpr int kSelMaxParts = 64;                       // parts per row (longer rows take more sub-chunks per part)
+constexpr int kSelBins = 4096;                         // 12-bit radix levels (key bits 31..20, then 19..8)
+constexpr int kSelBins3 = 256;                         // last level (key bits 7..0)
+constexpr int kSelCoarse = 64;                         // coarse bins of 64 first-level bins each
+constexpr int kSelCandCap = 4096;                      // candidate keys one part hands to the final pass
+constexpr int kSelCandLds = 16384;                     // candidate keys of a row the final pass holds in LDS
+constexpr int32_t kToppMaxKeys = int32_t(1) << 24;     // keys per row the fixed-point sums hold
+// per-part records (bytes): the first pass's histogram (block max, 64 coarse
+// sums, the directory of non-empty coarse bins, their 64-bin sections) and the
+// second pass's sums and candidate keys
+constexpr size_t kSelP1Coarse = 16, kSelP1Dir = 16 + 8 * kSelCoarse, kSelP1Sec = 1024;
+constexpr size_t kSelPart1Bytes = kSelP1Sec + size_t(8) * kSelCoarse * 64;
+constexpr size_t kSelP2Cand = 64;
+constexpr size_t kSelPart2Bytes = kSelP2Cand + size_t(4) * kSelCandCap;
+constexpr int kSelStateWords = 4;                      // per row: row max (bits), first-level crossing bin
 
+struct ToppPlan {
+  int32_t spb;     // sub-chunks per part
+  int32_t parts;   // parts per row
+};
+ToppPlan topp_plan(int32_t n);
 struct ToppWorkspace {
-  float* chunk_max;             // [rows][chunks]
-  unsigned long long* hist;     // [rows][kHistPerRow]
-  int32_t* chunk_cnt;           // [rows][chunks][1 + kBins3]: keys above the final bin, then
-                                // suffix counts of the final bin's 256 sub-bins
-  uint32_t* state;              // [rows][kToppStateWords]
+  unsigned char* part1;   // [rows][parts] kSelPart1Bytes
+  unsigned char* part2;   // [rows][parts] kSelPart2Bytes
+  uint32_t* state;        // [rows][kSelStateWords]
   size_t bytes;
 };
 ToppWorkspace topp_workspace(void* base, int64_t rows, int32_t n);
@@ -84,14 +100,22 @@ size_t decode_workspace_bytes(int32_t batch, int32_t heads_q, int32_t heads_kv, 
 // Score: blocks of kScoreThreads lanes, 1, 2 or 4 keys per lane.
 constexpr int kScoreThreads = 256;
 int score_keys_per_lane(int32_t batch, int32_t heads_kv, int32_t n);
-int score_blocks_per_row(int32_t batch, int32_t heads_kv, int32_t n);
 int topp_mask_words(int32_t n);   // 64-key words of a row's selection bitmap
+
+// Placement of blocks on the 8 XCDs (each with its own L2). A launch hands
+// workgroup id p to XCD p % 8. Every kernel that touches the scores of
+// (KV group g, part j) -- the score scan that writes them and the Top-p passes
+// that read them -- places that work on XCD (g * parts + j) % 8, so the
+// passes find the scores in their own L2. Work item (tile q, slot s) of a
+// launch with `slots` blocks per tile gets workgroup id
+// ((q / 8) * slots + s) * 8 + q % 8; the grid is xcd_grid(tiles, slots).
+constexpr int kXcds = 8;
+inline int64_t xcd_grid(int64_t tiles, int64_t slots) { return (tiles + kXcds - 1) / kXcds * kXcds * slots; }
 
 // Fused decode step: the workspaces of its stages side by side.
 struct StepWorkspace {
   void* decode;                     // decode_workspace_bytes()
   void* topp;                       // topp_workspace().bytes
-  float* slot_max;                  // [B * Hq][score_blocks_per_row()]
   unsigned long long* masks;        // [B * Hq][topp_mask_words(n)]
   size_t topp_bytes;
   size_t bytes;
@@ -127,24 +151,22 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
                                  int32_t cap, uint32_t* codes, float* kfac, hipStream_t stream,
                                  const int32_t* seq_off = nullptr, const int32_t* seq_cnt = nullptr,
                                  int32_t off_max = 0, uint16_t* kfac16 = nullptr, int32_t head_dim = kHeadDim);
-// slot_max (fused decode step): [B * Hq][score_blocks_per_row()] block maxima of the
-// scores, with hist[0, hist_words) zeroed by the same launch; NULL otherwise.
 // seq_n (ragged batches): [B] indexed keys per sequence, clamped to [0, n]; n is the row stride
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream,
-                        float* slot_max = nullptr, unsigned long long* hist = nullptr, int64_t hist_words = 0,
                         const int32_t* seq_n = nullptr, const uint16_t* kfac16 = nullptr, int32_t planes = 4,
                         int32_t head_dim = kHeadDim);
 // (kfac16: the compact index's fp16 factors [B][Hkv][cap], read instead of kfac when non-NULL; g = 0.
 //  planes: query bit-planes per head, 4 or 8 (8: B_q up to 8; uniform, unfused calls only))
-// slot_max / nslots: per-row partial maxima written by launch_score together with
-// the zeroing of the workspace's counters (the max pass is skipped); masks:
-// optional [rows][topp_mask_words(n)] selection bitmaps (bit i of word k = key 64 k + i);
-// seq_n / seq_p (ragged batches): [B] keys and p per sequence, row r of sequence r / heads_q
+// group: rows per KV group (heads_q / heads_kv when the scores come from
+// launch_score of the same step, 1 when unknown): only the placement of the
+// blocks on the XCDs depends on it. masks: optional [rows][topp_mask_words(n)]
+// selection bitmaps (bit i of word k = key 64 k + i); seq_n / seq_p (ragged
+// batches): [B] keys and p per sequence, row r of sequence r / heads_q
 rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,
-                       int32_t* sel_count, void* ws, hipStream_t stream, const float* slot_max = nullptr,
-                       int32_t nslots = 0, unsigned long long* masks = nullptr, const int32_t* seq_n = nullptr,
+                       int32_t* sel_count, void* ws, hipStream_t stream, int32_t group = 1,
+                       unsigned long long* masks = nullptr, const int32_t* seq_n = nullptr,
                        const float* seq_p = nullptr, int32_t heads_q = 1);
 rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const void* K,
                          const void* V, int32_t kv_dtype, int32_t cap, int32_t n, const int32_t* sel_idx,

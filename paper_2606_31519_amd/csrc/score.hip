@@ -18,10 +18,12 @@
 //   S = A f X + B0 + g,
 // which avoids the cancellation between 2 Delta ip and Delta S_u in fp32. The
 // kernel streams codes + factors once (24 B per KV key, non-temporal) and
-// writes 4 B per (key, head) with non-temporal stores (measured faster for the
-// whole decode step too, although the Top-p passes read the scores next).
-// Blocks that lie wholly inside [0, n) take a path without per-key guards.
-// The scan is HBM-bound at G = 4 and at G = 8.
+// writes 4 B per (key, head). Blocks that lie wholly inside [0, n) take a path
+// without per-key guards. The scan is HBM-bound at G = 4 and at G = 8.
+// Placement: the blocks of (KV group g, Top-p part j) -- the keys
+// [j * span, (j + 1) * span), span = the Top-p part length -- all run on XCD
+// (g * parts + j) % 8, where the Top-p passes that read these scores run too,
+// so those passes find them in that XCD's L2.
 // Ragged batches (RAGGED, seq_n != NULL): sequence b has seq_n[b] indexed keys
 // (clamped to [0, n]); n is the row stride of the scores and bounds the grid.
 // A block reads its sequence's count first and leaves at once when it lies
@@ -77,26 +79,12 @@ __device__ __forceinline__ uint32_t query_dot(const Spread& e, const uint32_t* q
   return binary_int4_dot(e, qn);
 }
 
-// block maximum of each of the G heads from the per-wave maxima
-// (maxima of every 32-lane half-wave, reduced by DPP in the head loop)
-constexpr int kHalfWaves = 2 * kScoreThreads / kWave;
-__device__ __forceinline__ void write_slots(float (*mx_s)[kHalfWaves], int row0, int G, float* slot_max) {
-  __syncthreads();
-  if (int(threadIdx.x) < G) {
-    float m = mx_s[threadIdx.x][0];
-#pragma unroll
-    for (int w = 1; w < kHalfWaves; ++w) m = fmaxf(m, mx_s[threadIdx.x][w]);
-    slot_max[int64_t(row0 + threadIdx.x) * gridDim.x + blockIdx.x] = m;
-  }
-}
-
-// Extra outputs of the fused decode step: the maximum score of every (query
-// head, block) in slot_max[row][blockIdx.x], and the zeroing of the Top-p
-// histogram counters that the selection accumulates into next.
-struct ScoreSlots {
-  float* slot_max;                 // [B * Hq][gridDim.x] or NULL
-  unsigned long long* hist;        // counters to zero
-  int64_t hist_words;
+// The launch: tiles q = g * parts + j (KV group g, Top-p part j), `slots`
+// blocks of kScoreThreads * KPT keys per tile, tile q on XCD q % 8.
+struct ScoreGrid {
+  int tiles;   // B * Hkv * parts
+  int parts;   // Top-p parts per row
+  int slots;   // score blocks per part
 };
 
 // FAC16: the compact index, one fp16 factor f per key (g = 0) instead of (f, g) in fp32.
@@ -104,36 +92,27 @@ struct ScoreSlots {
 // into its low and high nibbles, ip = ip_lo + 16 ip_hi, two dot8 chains).
 // D: head dimension, 128 or 64 (64: the two code words per key and per query
 // plane are padded with zero words, which add nothing to ip or pc).
-template <int KPT, bool INTS, bool SLOTS, bool RAGGED, bool FAC16, int QB = 4, int D = kHeadDim>
+template <int KPT, bool INTS, bool RAGGED, bool FAC16, int QB = 4, int D = kHeadDim>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const uint32_t* __restrict__ codes, const f32x2* __restrict__ kfac, const uint16_t* __restrict__ kfac16,
     const uint32_t* __restrict__ qplanes, const float* __restrict__ qscal, float* __restrict__ scores,
     int32_t* __restrict__ ip_out, int32_t* __restrict__ pc_out, int n, int cap, int Hq, int Hkv, int G,
-    ScoreSlots sl, const int32_t* __restrict__ seq_n) {
+    ScoreGrid sg, const int32_t* __restrict__ seq_n) {
   constexpr int QW = 4 * QB;                 // nibble words per head
   __shared__ uint32_t qn_s[kMaxGroup][QW];
-  __shared__ float mx_s[SLOTS ? kMaxGroup : 1][kHalfWaves];
-  const int bh = blockIdx.y;                 // b * Hkv + kv head
+  const int x = blockIdx.x % kXcds, r = blockIdx.x / kXcds;
+  const int q = (r / sg.slots) * kXcds + x;  // tile: (KV group, Top-p part)
+  if (q >= sg.tiles) return;                 // block-uniform: past the last tile
+  const int bh = q / sg.parts;               // b * Hkv + kv head
+  const int blk = (q % sg.parts) * sg.slots + r % sg.slots;   // block of the row
   const int b = bh / Hkv;
   const int hk = bh - b * Hkv;
   const int64_t kbase = int64_t(bh) * cap;
-  const int i0 = blockIdx.x * (kScoreThreads * KPT) + threadIdx.x;
+  const int i0 = blk * (kScoreThreads * KPT) + threadIdx.x;
   const int row0 = b * Hq + hk * G;
 
-  auto clear_counters = [&]() {   // (fused step) this block's share of the counters
-    if (SLOTS) {
-      const int64_t nblk = int64_t(gridDim.x) * gridDim.y, lb = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
-      const int64_t per = (sl.hist_words + nblk - 1) / nblk;
-      const int64_t e1 = min(sl.hist_words, (lb + 1) * per);
-      for (int64_t e = lb * per + threadIdx.x; e < e1; e += kScoreThreads) sl.hist[e] = 0ull;
-    }
-  };
   const int nb = RAGGED ? min(max(seq_n[b], 0), n) : n;   // this sequence's indexed keys
-  if (RAGGED && int(blockIdx.x) * (kScoreThreads * KPT) >= nb) {   // block-uniform: no key of this block is indexed
-    clear_counters();
-    if (SLOTS && int(threadIdx.x) < G) sl.slot_max[int64_t(row0 + threadIdx.x) * gridDim.x + blockIdx.x] = -INFINITY;
-    return;
-  }
+  if (blk * (kScoreThreads * KPT) >= nb) return;   // block-uniform: no key of this block is indexed
   u32x4 c[KPT];
   f32x2 fg[KPT];
   uint16_t fh[KPT];
@@ -154,8 +133,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     if (FAC16) return fmaf(float(__builtin_bit_cast(_Float16, fh[u])), y, B0);
     return fmaf(fg[u].x, y, B0 + fg[u].y);
   };
-  clear_counters();
-  const bool full = (blockIdx.x + 1) * (kScoreThreads * KPT) <= nb;   // block-uniform: no key past nb
+  const bool full = (blk + 1) * (kScoreThreads * KPT) <= nb;   // block-uniform: no key past nb
   if (threadIdx.x < 4 * G) {                  // one lane per (head, word)
     constexpr int W = D / 32;                   // code words per key
     const int h = threadIdx.x >> 2, w = threadIdx.x & 3;
@@ -197,21 +175,13 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       const int su = int(qs[2]);
       const float a_delta = A * delta, a_ql = A * ql;
       float* out = scores + int64_t(row) * n;
-      float mx = -INFINITY;
 #pragma unroll
       for (int u = 0; u < KPT; ++u) {
         const int ip = int(query_dot<QB>(e[u], qn));
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
-        const float sc = assemble(u, y, B0);
-        if (SLOTS) mx = fmaxf(mx, sc);
-        __builtin_nontemporal_store(sc, out + i0 + u * kScoreThreads);
-      }
-      if (SLOTS) {
-        mx = max32(mx);
-        if ((lane_id() & 31) == 0) mx_s[g][threadIdx.x / 32] = mx;
+        out[i0 + u * kScoreThreads] = assemble(u, y, B0);
       }
     }
-    if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
     return;
   }
   for (int g = 0; g < G; ++g) {
@@ -224,7 +194,6 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const int su = int(qs[2]);
     const float a_delta = A * delta, a_ql = A * ql;
     float* out = scores + int64_t(row) * n;
-    float mx = -INFINITY;
 #pragma unroll
     for (int u = 0; u < KPT; ++u) {
       const int i = i0 + u * kScoreThreads;
@@ -235,68 +204,47 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         const float sc = assemble(u, y, B0);
-        if (i < nb) {
-          if (SLOTS) mx = fmaxf(mx, sc);
-          __builtin_nontemporal_store(sc, out + i);
-        }
+        if (i < nb) out[i] = sc;
       }
     }
-    if (SLOTS) {
-      mx = max32(mx);
-      if ((lane_id() & 31) == 0) mx_s[g][threadIdx.x / 32] = mx;
-    }
   }
-  if (SLOTS) write_slots(mx_s, row0, G, sl.slot_max);
 }
 
-template <bool INTS, bool SLOTS, bool RAGGED, bool FAC16 = false, int QB = 4, int D = kHeadDim>
+template <bool INTS, bool RAGGED, bool FAC16 = false, int QB = 4, int D = kHeadDim>
 rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
                       const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal, float* scores,
-                      int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
+                      int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreGrid sg,
                       const int32_t* seq_n) {
-  const uint32_t* c4 = codes;
   const f32x2* f2 = reinterpret_cast<const f32x2*>(kfac);
+#define RBQ_SCORE_KPT(K)                                                                                    \
+  score_kernel<K, INTS, RAGGED, FAC16, QB, D><<<grid, kScoreThreads, 0, stream>>>(                          \
+      codes, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, cap, Hq, Hkv, G, sg, seq_n)
   switch (kpt) {
-    case 4:
-      score_kernel<4, INTS, SLOTS, RAGGED, FAC16, QB, D><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
-                                                                       n, cap, Hq, Hkv, G, sl, seq_n);
-      break;
-    case 2:
-      score_kernel<2, INTS, SLOTS, RAGGED, FAC16, QB, D><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
-                                                                       n, cap, Hq, Hkv, G, sl, seq_n);
-      break;
-    default:
-      score_kernel<1, INTS, SLOTS, RAGGED, FAC16, QB, D><<<grid, kScoreThreads, 0, stream>>>(c4, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out,
-                                                                       n, cap, Hq, Hkv, G, sl, seq_n);
-      break;
+    case 4: RBQ_SCORE_KPT(4); break;
+    case 2: RBQ_SCORE_KPT(2); break;
+    default: RBQ_SCORE_KPT(1); break;
   }
+#undef RBQ_SCORE_KPT
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
-
-}  // namespace
-
-namespace {
 
 // every form of the scan at head dimension D
 template <int D>
 rbq_status launch_score_d(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
                           const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal, float* scores,
-                          int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreSlots sl,
-                          const int32_t* seq_n, bool slots, int32_t planes) {
-#define RBQ_SCORE_LAUNCH(I, S, R, F, QB)                                                                      \
-  launch_kpt<I, S, R, F, QB, D>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, \
-                                cap, Hq, Hkv, G, sl, seq_n)
-#define RBQ_SCORE_FAC(S, R) \
-  (kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, S, R, true, 4) : RBQ_SCORE_LAUNCH(false, S, R, false, 4))
+                          int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreGrid sg,
+                          const int32_t* seq_n, int32_t planes) {
+#define RBQ_SCORE_LAUNCH(I, R, F, QB)                                                                         \
+  launch_kpt<I, R, F, QB, D>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, \
+                             cap, Hq, Hkv, G, sg, seq_n)
   if (planes == 8) {   // 8-plane queries: the standalone call only (integer hook included)
-    if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, false, 8);
-    return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, false, false, true, 8)
-                             : RBQ_SCORE_LAUNCH(false, false, false, false, 8);
+    if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, 8);
+    return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, false, true, 8) : RBQ_SCORE_LAUNCH(false, false, false, 8);
   }
-  if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, false, 4);   // (the integer hook is never ragged)
-  if (seq_n != nullptr) return slots ? RBQ_SCORE_FAC(true, true) : RBQ_SCORE_FAC(false, true);
-  return slots ? RBQ_SCORE_FAC(true, false) : RBQ_SCORE_FAC(false, false);
-#undef RBQ_SCORE_FAC
+  if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, 4);   // (the integer hook is never ragged)
+  if (seq_n != nullptr)
+    return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, true, true, 4) : RBQ_SCORE_LAUNCH(false, true, false, 4);
+  return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, false, true, 4) : RBQ_SCORE_LAUNCH(false, false, false, 4);
 #undef RBQ_SCORE_LAUNCH
 }
 
@@ -304,19 +252,24 @@ rbq_status launch_score_d(int kpt, dim3 grid, hipStream_t stream, const uint32_t
 
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
-                        float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, float* slot_max,
-                        unsigned long long* hist, int64_t hist_words, const int32_t* seq_n,
+                        float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, const int32_t* seq_n,
                         const uint16_t* kfac16, int32_t planes, int32_t head_dim) {
   if (n == 0) return RBQ_OK;
   const int G = heads_q / heads_kv;
   const int kpt = score_keys_per_lane(batch, heads_kv, n);
-  dim3 grid(score_blocks_per_row(batch, heads_kv, n), batch * heads_kv);
-  const ScoreSlots sl{slot_max, hist, hist_words};
+  const ToppPlan pl = topp_plan(n);
+  ScoreGrid sg;
+  sg.parts = pl.parts;
+  sg.tiles = batch * heads_kv * pl.parts;
+  sg.slots = pl.spb * kSelSub / (kScoreThreads * kpt);
+  const int64_t blocks = xcd_grid(sg.tiles, sg.slots);
+  if (blocks * kScoreThreads >= (int64_t(1) << 32)) return RBQ_EUNSUPPORTED;   // beyond one launch's grid
+  const dim3 grid{unsigned(blocks)};
   if (head_dim == 64)
     return launch_score_d<64>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, cap,
-                              heads_q, heads_kv, G, sl, seq_n, slot_max != nullptr, planes);
+                              heads_q, heads_kv, G, sg, seq_n, planes);
   return launch_score_d<kHeadDim>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, n,
-                                  cap, heads_q, heads_kv, G, sl, seq_n, slot_max != nullptr, planes);
+                                  cap, heads_q, heads_kv, G, sg, seq_n, planes);
 }
 
 }  // namespace rbq

@@ -2,44 +2,49 @@
 //
 // The selected set is { i : S_i >= s* } where s* is the largest score value
 // whose "mass at or above" reaches p of the softmax total. Instead of a sort
-// (O(n log n)) or Algorithm 3's ternary search over values, s* is found by a
-// radix select over the order-preserving 32-bit key of the fp32 score, with
-// histogram bins weighted by softmax mass: levels of 12, 12 and 8 key bits,
-// each pass keeping only the keys inside the bin where the cumulative mass
-// (counted from the top) crosses the target.
+// (O(n log n)) or Algorithm 3's ternary search over values, s* is found as the
+// boundary key K* of a radix select over the order-preserving 32-bit key of
+// the fp32 score, with bins weighted by softmax mass: levels of 12, 12 and 8
+// key bits.
 //
-// Masses are exp((S - max) * sm_scale) in fp32, converted to 2^-40 fixed point
-// and summed with 64-bit integer atomics (LDS first, then one global atomic
-// per non-empty bin per block), so every sum is exact and order-independent:
-// the result is bitwise deterministic. The per-element mass rounding (< 2^-40
-// each) and fp32 exp (~1 ulp) leave the decision within ~1e-6 of the exact
-// cumulative mass.
+// Masses. A key's mass is exp2((S - M) * sm_scale * log2(e)) in fp32 with M
+// the row maximum, as a 2^-40 fixed-point integer; sums are 64-bit integer
+// sums, so they are exact and do not depend on the order of the additions:
+// the selection is bitwise deterministic. The target is T = ceil(p * Z) with Z
+// the row's total, and K* is the largest key such that the keys >= K* hold at
+// least T. The per-key rounding (< 2^-40 each) and the fp32 exponential keep
+// the cumulative mass within ~1e-6 of the exact one.
 //
-// Kernels, each over grid (blocks, rows); a block takes spb consecutive
-// sub-chunks of 4096 scores of its row (spb = 1 unless the batch has more than
-// about a wave of sub-chunks). The crossing searches
-// are repeated by every block of a row, which costs less than an extra launch
-// and needs neither cross-block waiting nor device-wide fences; levels 1 and 2
-// also keep 64 coarse bins (sums of 64 fine bins), so a search reads 64 coarse
-// then 64 fine counters (one wave, two dependent loads) instead of 4096:
-//   1 max        per-block max; clears the row's histograms
-//   2 level 1    row max; 4096-bin histogram of key bits 31..20
-//   3 level 2    total mass Z, target T = ceil(p Z), crossing bin b1;
-//                histogram of bits 19..8 inside b1
-//   4 level 3    crossing b2; histogram of bits 7..0 inside (b1, b2); per
-//                block: the count of keys above that 24-bit bin and the suffix
-//                counts of its 256 sub-bins
-//   5 write      crossing b3 and K*; offset = sum over the earlier blocks of
-//                (count above + suffix count at b3); ascending compaction
-// Every pass issues its 16 loads per thread up front (indices clamped, the
-// out-of-range values masked) and those of the next sub-chunk before working
-// on the current one, so a pass costs one memory round trip per block.
+// Three passes over a row, one block of 1024 threads per (row, part), a part
+// being spb consecutive sub-chunks of 16384 keys:
+//   1 hist   per part: its own maximum m_j and a 4096-bin histogram of the
+//            first level (key bits 31..20) with masses relative to m_j, stored
+//            as 64 coarse sums plus the 64-bin sections of the non-empty
+//            coarse bins (plain stores: no atomics outside LDS).
+//   2 cand   every block of a row merges the row's part histograms, each
+//            rescaled by exp2((m_j - M) ...) in fp64, and takes the first-level
+//            bin b1 where the mass from the top crosses p of the total (an
+//            estimate: the exact check comes next). Then, with exact masses
+//            relative to M, it sums its part's total mass, the mass and count
+//            of its keys above b1, and the mass of its keys inside b1, and
+//            hands the keys inside b1 (the candidates) to the last pass.
+//   3 final  from the exact sums, T = ceil(p Z). If b1 holds the crossing
+//            (mass above b1 < T <= mass above b1 + mass in b1), the rest of K*
+//            (key bits 19..0) is resolved from the row's candidates in LDS: a
+//            12-bit and an 8-bit histogram with block barriers only. Otherwise
+//            (b1 missed by the estimate, or more candidates than the buffers
+//            hold) every block of the row runs an exact three-level select over
+//            all of the row's keys. Each block then writes its keys >= K* in
+//            ascending order at the offset given by the selected counts of the
+//            parts before it (above-b1 counts plus candidates >= K*).
+// Every pass reads the row's scores; all three and the score scan that wrote
+// them run the work of (KV group, part) on the same XCD, so the scores are
+// read from that XCD's L2.
 //
 // Ragged batches (seq_n / seq_p != NULL): row r of sequence b = r / Hq has
 // seq_n[b] keys (clamped to [0, n]; n stays the row stride and sizes the grid)
 // and its own p = seq_p[b]. Blocks past a row's keys leave at once; rows whose
-// p is >= 1 (or that have no keys) skip the histogram passes, and the write
-// pass selects every key of them.
+// p is >= 1 skip the first two passes, and the last pass selects every key.
 #include <algorithm>
 #include <cmath>
 
@@ -50,23 +55,39 @@ namespace rbq {
 namespace {
 
 typedef unsigned long long u64;
-constexpr int kT = kToppThreads;
-constexpr int kPT = kToppPerThread;
-constexpr int kChunk = kToppChunk;
+constexpr int kT = kSelThreads;
+constexpr int kPT = kSelPerThread;
+constexpr int kSub = kSelSub;
 constexpr int kTW = kT / kWave;            // waves per block
 constexpr float kFix = 1099511627776.0f;   // 2^40
 
-// softmax mass of one score in 2^-40 units; every pass evaluates it with the
-// same instructions, so the same score always gets the same mass
+// softmax mass of one score in 2^-40 units relative to m (s <= m); every pass
+// evaluates it with the same instructions, so the same score always gets the
+// same mass
 __device__ __forceinline__ u64 fixed_mass(float s, float m, float scale_log2e) {
   const float e = __builtin_amdgcn_exp2f(__fmul_rn(__fsub_rn(s, m), scale_log2e));
   return u64(__fmul_rn(e, kFix));
+}
+
+// inverse of score_key (-0 comes back as +0, which has the same mass)
+__device__ __forceinline__ float key_score(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
 }
 
 __device__ __forceinline__ u64 shfl_down_u64(u64 v, int o) {
   const uint32_t lo = __shfl_down(uint32_t(v), o, kWave);
   const uint32_t hi = __shfl_down(uint32_t(v >> 32), o, kWave);
   return (u64(hi) << 32) | lo;
+}
+__device__ __forceinline__ u64 shfl_u64(u64 v, int src) {
+  const uint32_t lo = __shfl(uint32_t(v), src, kWave);
+  const uint32_t hi = __shfl(uint32_t(v >> 32), src, kWave);
+  return (u64(hi) << 32) | lo;
+}
+__device__ __forceinline__ u64 wave_sum_u64(u64 v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += shfl_down_u64(v, o);
+  return shfl_u64(v, 0);
 }
 
 __device__ __forceinline__ float block_max(float m, float* red) {
@@ -80,110 +101,68 @@ __device__ __forceinline__ float block_max(float m, float* red) {
   return r;
 }
 
-// Crossing search over `nbins` counters of one row (bins ordered by key): the
-// highest bin b with sum_{b' >= b} hist[b'] >= T. With `frac` > 0 the target
-// is T = ceil(frac * total). Returns b and the mass needed inside it,
-// T - sum_{b' > b}, in *out (valid after the trailing barrier). Exactly one
-// thread matches, because the suffix sums grow monotonically from 0 to the
-// total and 1 <= T <= total.
+// block-wide sum of one u64 per thread (every thread gets the total)
+__device__ __forceinline__ u64 block_sum_u64(u64 v, u64* red) {
+  v = wave_sum_u64(v);
+  __syncthreads();
+  if (lane_id() == 0) red[threadIdx.x / kWave] = v;
+  __syncthreads();
+  u64 r = 0;
+#pragma unroll
+  for (int w = 0; w < kTW; ++w) r += red[w];
+  return r;
+}
+
 struct Crossing {
   uint32_t bin;
   uint32_t pad;
   u64 need;
 };
-template <int BPT>
-__device__ void find_crossing(const u64* h, u64 T, float frac, u64* wtot, Crossing* out) {
+
+// Crossing search over NB counters of one row held in LDS (bins ordered by
+// key): the highest bin b with sum_{b' >= b} h[b'] >= need, and the mass still
+// needed inside it, need - sum_{b' > b} h[b'], in *out (valid after the
+// trailing barrier). Requires 1 <= need <= the total: then exactly one thread
+// matches, since the suffix sums grow monotonically from 0 to the total.
+template <int NB>
+__device__ void lds_crossing(const u64* h, u64 need, u64* wtot, Crossing* out) {
+  constexpr int BPT = NB >= kT ? NB / kT : 1;   // bins per thread
+  constexpr int NT = NB / BPT;                  // threads holding bins
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
+  u64 hv[BPT];
   u64 s = 0;
 #pragma unroll
-  for (int k = 0; k < BPT; ++k) s += h[k];
-  // inclusive suffix sum inside the wave (higher lanes hold higher bins)
-  u64 x = s;
+  for (int k = 0; k < BPT; ++k) {
+    hv[k] = t < NT ? h[t * BPT + k] : 0ull;
+    s += hv[k];
+  }
+  u64 x = s;   // inclusive suffix sum inside the wave (higher lanes hold higher bins)
 #pragma unroll
   for (int o = 1; o < kWave; o <<= 1) {
     const u64 y = shfl_down_u64(x, o);
     if (lane + o < kWave) x += y;
   }
-  __syncthreads();   // wtot may still be read by a previous search
+  __syncthreads();   // wtot and *out may still be read after a previous search
   if (lane == 0) wtot[w] = x;
-  __syncthreads();
-  u64 above = x - s;                        // strictly above this thread's bins, inside the wave
-  u64 total = 0;
-#pragma unroll
-  for (int v = 0; v < kTW; ++v) {
-    total += wtot[v];
-    if (v > w) above += wtot[v];
+  if (t == 0) {      // (defined even if no bin matched)
+    out->bin = 0;
+    out->need = need;
   }
-  if (frac > 0.f) T = u64(ceil(double(frac) * double(total)));
-  u64 cum = above;
+  __syncthreads();
+  u64 cum = x - s;   // strictly above this thread's bins
+#pragma unroll
+  for (int v = 0; v < kTW; ++v)
+    if (v > w) cum += wtot[v];
 #pragma unroll
   for (int k = BPT - 1; k >= 0; --k) {
-    if (cum < T && cum + h[k] >= T) {
+    if (t < NT && cum < need && cum + hv[k] >= need) {
       out->bin = uint32_t(t * BPT + k);
-      out->need = T - cum;
+      out->need = need - cum;
     }
-    cum += h[k];
+    cum += hv[k];
   }
   __syncthreads();
 }
-
-// The same search over 4096 fine bins with their 64 coarse sums, by wave 0:
-// the coarse crossing first, then the fine crossing inside it.
-// `c` is coarse[lane] for the threads of wave 0 (loaded by the caller together
-// with its other independent loads, so the search costs one more round trip).
-__device__ void find_crossing_2lvl(const u64* __restrict__ fine, u64 c, u64 T, float frac, Crossing* out) {
-  static_assert(kCoarse == kWave && kBins1 == kCoarse * kWave && kBins2 == kBins1, "one coarse bin per lane");
-  if (threadIdx.x < kWave) {
-    const int lane = lane_id();
-    u64 x = c;                                   // inclusive suffix sum (higher lanes hold higher bins)
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const u64 y = shfl_down_u64(x, o);
-      if (lane + o < kWave) x += y;
-    }
-    const uint32_t tlo = __shfl(uint32_t(x), 0, kWave), thi = __shfl(uint32_t(x >> 32), 0, kWave);
-    const u64 total = (u64(thi) << 32) | tlo;
-    if (frac > 0.f) T = u64(ceil(double(frac) * double(total)));
-    const u64 above = x - c;
-    const uint64_t hit = __ballot(above < T && x >= T);
-    const int g = __builtin_ctzll(hit);          // exactly one lane: suffix sums grow from 0 to total >= T >= 1
-    const uint32_t nlo = __shfl(uint32_t(T - above), g, kWave), nhi = __shfl(uint32_t((T - above) >> 32), g, kWave);
-    const u64 need = (u64(nhi) << 32) | nlo;
-    const u64 f = fine[g * kWave + lane];
-    u64 z = f;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const u64 y = shfl_down_u64(z, o);
-      if (lane + o < kWave) z += y;
-    }
-    const u64 above2 = z - f;
-    if (above2 < need && z >= need) {
-      out->bin = uint32_t(g * kWave + lane);
-      out->need = need - above2;
-    }
-  }
-  __syncthreads();
-}
-
-// Coarse sums of a block's LDS histogram of 4096 bins, added to the row's
-// 64 global coarse counters (one atomic per non-empty coarse bin).
-__device__ __forceinline__ void flush_coarse(const u64* h, u64* __restrict__ gcoarse) {
-  constexpr int kPer = kBins1 / kT;             // 16 fine bins per thread, 4 threads per coarse bin
-  u64 s = 0;
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) s += h[threadIdx.x * kPer + k];
-  s += shfl_down_u64(s, 1);
-  s += shfl_down_u64(s, 2);
-  if ((threadIdx.x & 3) == 0 && s) atomicAdd(&gcoarse[threadIdx.x / 4], s);
-}
-
-// the thread's kPT scores of sub-chunk cs (element cs * kChunk + k * kT + tid), all
-// loads in flight; indices past the row's n keys are clamped (the values are masked)
-__device__ __forceinline__ void load_chunk(const float* __restrict__ s, int n, int cs, float* v) {
-#pragma unroll
-  for (int k = 0; k < kPT; ++k) v[k] = s[min(cs * kChunk + k * kT + int(threadIdx.x), n - 1)];
-}
-__device__ __forceinline__ bool in_row(int n, int cs, int k) { return cs * kChunk + k * kT + int(threadIdx.x) < n; }
 
 // A row's key count and p: the call's, or its sequence's in a ragged batch. A
 // p outside (0, 1] is clamped into it (<= 0 or NaN: the smallest positive p,
@@ -204,249 +183,484 @@ __device__ __forceinline__ RowSel row_sel(const int32_t* __restrict__ seq_n, con
   return r;
 }
 
-// Block c of a row takes the sub-chunks [c * spb, c * spb + spb) that hold keys
-// of the row (none for a block past a short row of a ragged batch). The host
-// sets spb so that a pass is about one wave of blocks whatever the batch: the
-// per-block work of a pass (clearing and flushing the LDS histogram, the
-// crossing searches, the launch) is then paid once per spb sub-chunks.
-// (MULTI = false: spb == 1, the kernels compile to a single sub-chunk per block)
-struct Span {
-  int cs0, cs1;
+// The (row, part) of this block: tile q = (row / group) * parts + part runs on
+// XCD q % 8, the group's rows of a tile in consecutive slots.
+struct SelWork {
+  int row, part;
+  bool ok;
 };
-template <bool MULTI>
-__device__ __forceinline__ Span block_span(int c, int spb, int chunks, int nr) {
-  if (!MULTI) return Span{c, c * kChunk < nr ? c + 1 : c};
-  return Span{c * spb, min(min(c * spb + spb, chunks), (nr + kChunk - 1) / kChunk)};
+__device__ __forceinline__ SelWork sel_work(int parts, int group, int rows) {
+  const int p = blockIdx.x, x = p % kXcds, r = p / kXcds;
+  const int s = r % group, q = (r / group) * kXcds + x;
+  SelWork w;
+  w.ok = q < (rows / group) * parts;
+  w.row = (q / parts) * group + s;
+  w.part = q % parts;
+  return w;
 }
 
-__device__ __forceinline__ float row_max(const float* __restrict__ part_max, int nmax, float* red) {
-  float m = -INFINITY;
-  for (int k = threadIdx.x; k < nmax; k += kT) m = fmaxf(m, part_max[k]);
-  return block_max(m, red);
-}
-
-template <bool RAGGED, bool MULTI>
-__global__ __launch_bounds__(kT) void topp_max_kernel(const float* __restrict__ scores, int n, int chunks, int spb,
-                                                      float* __restrict__ chunk_max, u64* __restrict__ hist,
-                                                      const int32_t* __restrict__ seq_n, int hq) {
-  __shared__ float red[kTW];
-  const int row = blockIdx.y, c = blockIdx.x;
-  const int nr = RAGGED ? row_sel(seq_n, nullptr, hq, row, n, 1.f).n : n;
-  const Span sp = block_span<MULTI>(c, spb, chunks, nr);
-  const float* srow = scores + int64_t(row) * n;
-  float m = -INFINITY;
-  float v[kPT], vn[kPT];
-  if (sp.cs0 < sp.cs1) load_chunk(srow, nr, sp.cs0, v);
-  for (int cs = sp.cs0; cs < sp.cs1; ++cs) {
-    if (MULTI && cs + 1 < sp.cs1) load_chunk(srow, nr, cs + 1, vn);   // the next sub-chunk lands meanwhile
+// the thread's kPT scores of the sub-chunk at `base` (element base + k * kT + tid),
+// all loads in flight; indices at or past `end` are clamped (the values are masked)
+__device__ __forceinline__ void load_sub(const float* __restrict__ s, int base, int end, float* v) {
 #pragma unroll
-    for (int k = 0; k < kPT; ++k) {
-      if (in_row(nr, cs, k)) m = fmaxf(m, v[k]);
-      if (MULTI) v[k] = vn[k];
-    }
+  for (int k = 0; k < kPT; ++k) v[k] = s[min(base + k * kT + int(threadIdx.x), end - 1)];
+}
+__device__ __forceinline__ bool in_range(int base, int end, int k) { return base + k * kT + int(threadIdx.x) < end; }
+
+// ---------------------------------------------------------------- pass 1: part histograms
+template <bool RAGGED, bool MULTI>
+__global__ __launch_bounds__(kT) void sel_hist_kernel(const float* __restrict__ scores, int n, int spb, int parts,
+                                                      int group, int rows, float scale_log2e,
+                                                      unsigned char* __restrict__ part1,
+                                                      const int32_t* __restrict__ seq_n,
+                                                      const float* __restrict__ seq_p, int hq) {
+  __shared__ u64 h[kSelBins];
+  __shared__ u64 cs[kSelCoarse];
+  __shared__ int dir_s[kSelCoarse];
+  __shared__ float red[kTW];
+  const SelWork wk = sel_work(parts, group, rows);
+  if (!wk.ok) return;
+  const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, wk.row, n, 0.5f) : RowSel{n, 0.5f};
+  const int k0 = wk.part * spb * kSub;
+  if (k0 >= rs.n || (RAGGED && rs.p >= 1.f)) return;   // block-uniform: no histogram needed here
+  const int k1 = min(rs.n, k0 + spb * kSub);
+  const float* srow = scores + int64_t(wk.row) * n;
+  float v[kPT];
+  load_sub(srow, k0, k1, v);
+  for (int b = threadIdx.x; b < kSelBins; b += kT) h[b] = 0;
+  // the part's maximum
+  float m = -INFINITY;
+  for (int base = k0; base < k1; base += kSub) {
+    if (MULTI && base > k0) load_sub(srow, base, k1, v);
+#pragma unroll
+    for (int k = 0; k < kPT; ++k)
+      if (in_range(base, k1, k)) m = fmaxf(m, v[k]);
+    if (!MULTI) break;
   }
-  m = block_max(m, red);
-  if (threadIdx.x == 0) chunk_max[int64_t(row) * gridDim.x + c] = m;
-  // this block's share of the row's histogram counters
-  const int per = (kHistPerRow + gridDim.x - 1) / gridDim.x;
-  const int e0 = c * per, e1 = min(kHistPerRow, e0 + per);
-  u64* h = hist + int64_t(row) * kHistPerRow;
-  for (int e = e0 + threadIdx.x; e < e1; e += kT) h[e] = 0;
-}
-
-// The row maximum comes from nmax partial maxima per row: the max kernel's per
-// block, or (fused decode step) the score kernel's per block.
-template <bool RAGGED, bool MULTI>
-__global__ __launch_bounds__(kT) void topp_level1_kernel(const float* __restrict__ scores, int n, int chunks, int spb,
-                                                         const float* __restrict__ rmax, int nmax, float scale_log2e,
-                                                         float p, u64* __restrict__ hist, uint32_t* __restrict__ state,
-                                                         const int32_t* __restrict__ seq_n,
-                                                         const float* __restrict__ seq_p, int hq) {
-  __shared__ u64 h[kBins1];
-  __shared__ float red[kTW];
-  const int row = blockIdx.y, c = blockIdx.x;
-  const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, row, n, p) : RowSel{n, p};
-  const Span sp = block_span<MULTI>(c, spb, chunks, rs.n);
-  if (RAGGED && (sp.cs1 <= sp.cs0 || rs.p >= 1.f)) return;   // block-uniform: nothing of this row to histogram here
-  for (int b = threadIdx.x; b < kBins1; b += kT) h[b] = 0;
-  const float* srow = scores + int64_t(row) * n;
-  float v[kPT], vn[kPT];
-  load_chunk(srow, rs.n, sp.cs0, v);
-  const float m = row_max(rmax + int64_t(row) * nmax, nmax, red);   // barriers: h is clear after it
-  if (c == 0 && threadIdx.x == 0) state[int64_t(row) * kToppStateWords + 6] = __float_as_uint(m);   // for the next passes
-  for (int cs = sp.cs0; cs < (MULTI ? sp.cs1 : sp.cs0 + 1); ++cs) {
-    if (MULTI && cs + 1 < sp.cs1) load_chunk(srow, rs.n, cs + 1, vn);
+  m = block_max(m, red);   // (its barriers also order the clearing of h before the adds)
+  for (int base = k0; base < k1; base += kSub) {
+    if (MULTI) load_sub(srow, base, k1, v);   // (read again: from L2)
 #pragma unroll
     for (int k = 0; k < kPT; ++k) {
-      const u64 ms = fixed_mass(v[k], m, scale_log2e);
-      if (in_row(rs.n, cs, k) && ms) atomicAdd(&h[score_key(v[k]) >> 20], ms);
-      if (MULTI) v[k] = vn[k];
+      const u64 e = fixed_mass(v[k], m, scale_log2e);
+      if (in_range(base, k1, k) && e) atomicAdd(&h[score_key(v[k]) >> 20], e);
+    }
+    if (!MULTI) break;
+  }
+  __syncthreads();
+  // coarse sums: 4 fine bins per thread, 16 threads per coarse bin
+  const int t = threadIdx.x;
+  u64 s4 = h[4 * t] + h[4 * t + 1] + h[4 * t + 2] + h[4 * t + 3];
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) s4 += shfl_down_u64(s4, o);
+  if ((t & 15) == 0) cs[t >> 4] = s4;
+  __syncthreads();
+  unsigned char* P1 = part1 + (int64_t(wk.row) * parts + wk.part) * kSelPart1Bytes;
+  if (t < kSelCoarse) {   // wave 0: the directory of non-empty coarse bins
+    const bool nz = cs[t] != 0ull;
+    const u64 bal = __ballot(nz);
+    const int d = nz ? __popcll(bal & ((1ull << t) - 1ull)) : -1;
+    dir_s[t] = d;
+    reinterpret_cast<u64*>(P1 + kSelP1Coarse)[t] = cs[t];
+    reinterpret_cast<int32_t*>(P1 + kSelP1Dir)[t] = d;
+    if (t == 0) {
+      reinterpret_cast<float*>(P1)[0] = m;
+      reinterpret_cast<uint32_t*>(P1)[1] = uint32_t(__popcll(bal));
     }
   }
   __syncthreads();
-  u64* g = hist + int64_t(row) * kHistPerRow;
-  for (int b = threadIdx.x; b < kBins1; b += kT)
-    if (h[b]) atomicAdd(&g[b], h[b]);
-  flush_coarse(h, g + kBins1 + kBins2 + kBins3);
+  const int d = dir_s[t >> 4];
+  if (d >= 0) {
+    u64* sec = reinterpret_cast<u64*>(P1 + kSelP1Sec) + d * 64 + (t & 15) * 4;
+    sec[0] = h[4 * t];
+    sec[1] = h[4 * t + 1];
+    sec[2] = h[4 * t + 2];
+    sec[3] = h[4 * t + 3];
+  }
 }
 
-// Level 2 (LEVEL == 2) or level 3 (LEVEL == 3): find the previous level's
-// crossing, then histogram the keys inside it.
-template <int LEVEL, bool RAGGED, bool MULTI>
-__global__ __launch_bounds__(kT) void topp_level_kernel(const float* __restrict__ scores, int n, int chunks, int spb,
-                                                        float scale_log2e, float p, u64* __restrict__ hist,
-                                                        uint32_t* __restrict__ state,
-                                                        int32_t* __restrict__ chunk_cnt,
-                                                        const int32_t* __restrict__ seq_n,
-                                                        const float* __restrict__ seq_p, int hq) {
-  constexpr int kBins = LEVEL == 2 ? kBins2 : kBins3;
-  __shared__ u64 h[kBins];
-  __shared__ uint32_t cnt_s[LEVEL == 3 ? kBins3 + 1 : 1];
-  __shared__ int red2[kTW];
-  if (LEVEL == 3)
-    for (int b = threadIdx.x; b <= kBins3; b += kT) cnt_s[b] = 0;
-  __shared__ Crossing cr;
-  const int row = blockIdx.y, c = blockIdx.x;
-  u64* rh = hist + int64_t(row) * kHistPerRow;
-  uint32_t* st = state + int64_t(row) * kToppStateWords;
-  for (int b = threadIdx.x; b < kBins; b += kT) h[b] = 0;
-  u64* coarse = rh + kBins1 + kBins2 + kBins3;
-  const u64 cpre = threadIdx.x < kWave ? coarse[(LEVEL == 2 ? 0 : kCoarse) + threadIdx.x] : 0;
-  const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, row, n, p) : RowSel{n, p};
-  const Span sp = block_span<MULTI>(c, spb, chunks, rs.n);
-  if (RAGGED && (sp.cs1 <= sp.cs0 || rs.p >= 1.f)) return;   // block-uniform (the write pass handles p >= 1)
-  const float* srow = scores + int64_t(row) * n;
-  float v[kPT], vn[kPT];
-  load_chunk(srow, rs.n, sp.cs0, v);
-  const float m = __uint_as_float(st[6]);   // the row max, from level 1 (h is clear after the search's barrier)
-  uint32_t prefix;
-  if (LEVEL == 2) {
-    find_crossing_2lvl(rh, cpre, 0, rs.p, &cr);
-    prefix = cr.bin;
-  } else {
-    const u64 T = (u64(st[2]) << 32) | st[1];
-    find_crossing_2lvl(rh + kBins1, cpre, T, 0.f, &cr);
-    prefix = (st[0] << 12) | cr.bin;
+// ---------------------------------------------------------------- pass 2: candidates
+// per-part record of pass 2 (at the start of its kSelPart2Bytes slot)
+struct P2Head {
+  u64 total;        // exact mass of the part's keys
+  u64 above_mass;   // ... of its keys above the first-level bin b1
+  u64 cand_mass;    // ... of its keys inside b1
+  uint32_t above_cnt;
+  uint32_t cand_cnt;   // keys inside b1 (only the first kSelCandCap are stored)
+};
+
+template <bool RAGGED, bool MULTI>
+__global__ __launch_bounds__(kT) void sel_cand_kernel(const float* __restrict__ scores, int n, int spb, int parts,
+                                                      int group, int rows, float p, float scale_log2e,
+                                                      const unsigned char* __restrict__ part1,
+                                                      unsigned char* __restrict__ part2, uint32_t* __restrict__ state,
+                                                      const int32_t* __restrict__ seq_n,
+                                                      const float* __restrict__ seq_p, int hq) {
+  __shared__ int dir_s[kSelMaxParts][kSelCoarse];
+  __shared__ u64 cval_s[kSelMaxParts][kSelCoarse];
+  __shared__ float mp_s[kSelMaxParts];
+  __shared__ double fac_s[kSelMaxParts];
+  __shared__ u64 crow[kSelCoarse], frow[kSelCoarse];
+  __shared__ u64 red[kTW];
+  __shared__ uint32_t cand_n, above_n;
+  __shared__ float M_s;
+  __shared__ uint32_t b1_s;
+  const SelWork wk = sel_work(parts, group, rows);
+  if (!wk.ok) return;
+  const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, wk.row, n, p) : RowSel{n, p};
+  const int k0 = wk.part * spb * kSub;
+  if (k0 >= rs.n || (RAGGED && rs.p >= 1.f)) return;   // block-uniform
+  const int k1 = min(rs.n, k0 + spb * kSub);
+  const int parts_r = (rs.n + spb * kSub - 1) / (spb * kSub);   // parts holding keys of this row
+  const float* srow = scores + int64_t(wk.row) * n;
+  float v[kPT];
+  load_sub(srow, k0, k1, v);   // lands while the histograms are merged
+  const int t = threadIdx.x;
+  const unsigned char* P1row = part1 + int64_t(wk.row) * parts * kSelPart1Bytes;
+  // merge 1: each part's maximum, coarse sums and directory (parts_r * 64 entries, all loads in flight)
+  const int nent = parts_r * kSelCoarse;
+  for (int e = t; e < nent; e += kT) {
+    const int j = e / kSelCoarse, cb = e % kSelCoarse;
+    const unsigned char* P1 = P1row + int64_t(j) * kSelPart1Bytes;
+    if (cb == 0) mp_s[j] = reinterpret_cast<const float*>(P1)[0];
+    cval_s[j][cb] = reinterpret_cast<const u64*>(P1 + kSelP1Coarse)[cb];
+    dir_s[j][cb] = reinterpret_cast<const int32_t*>(P1 + kSelP1Dir)[cb];
   }
-  // state words: [0..2] = level-1 bin and the mass still needed inside it
-  // (written by level 2), [3..5] = the same for level 2 (written by level 3),
-  // [6] = the row max (written by level 1); a kernel never rewrites what it reads
-  if (c == 0 && threadIdx.x == 0) {
-    const int o = LEVEL == 2 ? 0 : 3;
-    st[o] = prefix;
-    st[o + 1] = uint32_t(cr.need);
-    st[o + 2] = uint32_t(cr.need >> 32);
+  if (t < kSelCoarse) {
+    crow[t] = 0;
+    frow[t] = 0;
   }
-  const int shift_hi = LEVEL == 2 ? 20 : 8;
-  int above = 0;   // level 3: keys above the 24-bit bin, certainly selected
-  for (int cs = sp.cs0; cs < (MULTI ? sp.cs1 : sp.cs0 + 1); ++cs) {
-    if (MULTI && cs + 1 < sp.cs1) load_chunk(srow, rs.n, cs + 1, vn);
+  if (t == 0) {
+    cand_n = 0;
+    above_n = 0;
+  }
+  __syncthreads();
+  if (t < kWave) {   // wave 0: the row maximum and each part's rescale factor
+    float m = t < parts_r ? mp_s[t] : -INFINITY;
+    m = wave_max(m);
+    if (t < parts_r) fac_s[t] = exp2((double(mp_s[t]) - double(m)) * double(scale_log2e));
+    if (t == 0) M_s = m;
+  }
+  __syncthreads();
+  for (int e = t; e < nent; e += kT) {
+    const int j = e / kSelCoarse, cb = e % kSelCoarse;
+    const u64 cval = cval_s[j][cb];
+    if (cval) atomicAdd(&crow[cb], u64(double(cval) * fac_s[j] + 0.5));
+  }
+  __syncthreads();
+  // the coarse crossing of the estimated target (wave 0, one coarse bin per lane)
+  __shared__ uint32_t c1_s;
+  __shared__ u64 needc_s;
+  if (t < kWave) {
+    const u64 c = crow[t];
+    u64 x = c;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const u64 y = shfl_down_u64(x, o);
+      if (t + o < kWave) x += y;
+    }
+    const u64 total = shfl_u64(x, 0);
+    u64 T = u64(ceil(double(rs.p) * double(total)));
+    T = T < 1 ? 1 : (T > total ? total : T);
+    const u64 above = x - c;
+    const u64 hit = __ballot(above < T && x >= T);
+    const int g = hit ? __builtin_ctzll(hit) : 0;
+    if (t == g) {
+      c1_s = uint32_t(g);
+      needc_s = T - above;
+    }
+  }
+  __syncthreads();
+  const uint32_t c1 = c1_s;
+  // merge 2: the 64 first-level bins of the coarse crossing bin, from every part
+  for (int e = t; e < nent; e += kT) {
+    const int j = e / kSelCoarse, fb = e % kSelCoarse;
+    const int d = dir_s[j][c1];
+    if (d >= 0) {
+      const u64 f = reinterpret_cast<const u64*>(P1row + int64_t(j) * kSelPart1Bytes + kSelP1Sec)[d * 64 + fb];
+      if (f) atomicAdd(&frow[fb], u64(double(f) * fac_s[j] + 0.5));
+    }
+  }
+  __syncthreads();
+  if (t < kWave) {
+    const u64 f = frow[t];
+    u64 x = f;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const u64 y = shfl_down_u64(x, o);
+      if (t + o < kWave) x += y;
+    }
+    const u64 total = shfl_u64(x, 0);
+    // (the rescaled sums are estimates: keep the target inside this bin's total)
+    u64 need = needc_s > total ? total : needc_s;
+    need = need < 1 ? 1 : need;
+    const u64 above = x - f;
+    const u64 hit = __ballot(above < need && x >= need);
+    const int g = hit ? __builtin_ctzll(hit) : 0;
+    if (t == g) b1_s = c1 * kSelCoarse + uint32_t(g);
+  }
+  __syncthreads();
+  const uint32_t b1 = b1_s;
+  const float M = M_s;
+  // exact masses relative to the row maximum: totals, keys above b1, candidates in b1
+  uint32_t* cand = reinterpret_cast<uint32_t*>(part2 + (int64_t(wk.row) * parts + wk.part) * kSelPart2Bytes +
+                                               kSelP2Cand);
+  u64 tot = 0, am = 0, cm = 0;
+  uint32_t ac = 0;
+  const int lane = lane_id();
+  for (int base = k0; base < k1; base += kSub) {
+    if (MULTI && base > k0) load_sub(srow, base, k1, v);
 #pragma unroll
     for (int k = 0; k < kPT; ++k) {
+      const bool in = in_range(base, k1, k);
       const uint32_t key = score_key(v[k]);
-      if (in_row(rs.n, cs, k)) {
-        if ((key >> shift_hi) == prefix) {
-          const uint32_t bin = LEVEL == 2 ? ((key >> 8) & 0xfffu) : (key & 0xffu);
-          const u64 ms = fixed_mass(v[k], m, scale_log2e);
-          if (ms) atomicAdd(&h[bin], ms);
-          if (LEVEL == 3) atomicAdd(&cnt_s[bin], 1u);
-        } else if (LEVEL == 3 && (key >> 8) > prefix) {
-          ++above;
+      const u64 e = in ? fixed_mass(v[k], M, scale_log2e) : 0ull;
+      const uint32_t bin = key >> 20;
+      tot += e;
+      const bool up = in && bin > b1, mid = in && bin == b1;
+      am += up ? e : 0ull;
+      ac += up ? 1u : 0u;
+      cm += mid ? e : 0ull;
+      const u64 bal = __ballot(mid);
+      if (bal) {
+        uint32_t base_pos = 0;
+        if (lane == 0) base_pos = atomicAdd(&cand_n, uint32_t(__popcll(bal)));
+        base_pos = __shfl(base_pos, 0, kWave);
+        const uint32_t pos =
+            base_pos + __builtin_amdgcn_mbcnt_hi(uint32_t(bal >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal), 0u));
+        if (mid && pos < uint32_t(kSelCandCap)) cand[pos] = key;
+      }
+    }
+    if (!MULTI) break;
+  }
+  ac = uint32_t(wave_sum_int(int(ac)));
+  if (lane == 0) atomicAdd(&above_n, ac);
+  tot = block_sum_u64(tot, red);
+  am = block_sum_u64(am, red);
+  cm = block_sum_u64(cm, red);   // (its barriers also complete the LDS counters)
+  if (t == 0) {
+    P2Head* hd = reinterpret_cast<P2Head*>(part2 + (int64_t(wk.row) * parts + wk.part) * kSelPart2Bytes);
+    hd->total = tot;
+    hd->above_mass = am;
+    hd->cand_mass = cm;
+    hd->above_cnt = above_n;
+    hd->cand_cnt = cand_n;
+    if (wk.part == 0) {
+      state[int64_t(wk.row) * kSelStateWords] = __float_as_uint(M);
+      state[int64_t(wk.row) * kSelStateWords + 1] = b1;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- pass 3: resolve K* and write
+// Exact three-level select over every key of the row (the fallback): K* and,
+// per part, the number of its keys >= K* in cnt[].
+template <bool MULTI>
+__device__ uint32_t exact_select_row(const float* __restrict__ srow, int nr, int spb, int parts_r, float M,
+                                     float scale_log2e, u64 T, u64* h, u64* wtot, Crossing* cr, uint32_t* cnt) {
+  const int t = threadIdx.x;
+  uint32_t prefix = 0;
+  u64 need = T;
+  // levels: bits 31..20 (all keys), 19..8 (keys in the first bin), 7..0 (keys in both)
+#pragma unroll 1
+  for (int level = 0; level < 3; ++level) {
+    const int shift = level == 0 ? 20 : level == 1 ? 8 : 0;
+    const uint32_t mask = level == 2 ? 0xffu : 0xfffu;
+    const int hshift = level == 0 ? 32 : level == 1 ? 20 : 8;   // bits that must match the prefix
+    for (int b = t; b < kSelBins; b += kT) h[b] = 0;
+    __syncthreads();
+    float v[kPT];
+    for (int base = 0; base < nr; base += kSub) {
+      load_sub(srow, base, nr, v);
+#pragma unroll
+      for (int k = 0; k < kPT; ++k) {
+        const uint32_t key = score_key(v[k]);
+        const bool match = hshift == 32 || (key >> hshift) == prefix;
+        if (in_range(base, nr, k) && match) {
+          const u64 e = fixed_mass(v[k], M, scale_log2e);
+          if (e) atomicAdd(&h[(key >> shift) & mask], e);
         }
       }
-      if (MULTI) v[k] = vn[k];
     }
+    __syncthreads();
+    if (level < 2) lds_crossing<kSelBins>(h, need, wtot, cr);
+    else lds_crossing<kSelBins3>(h, need, wtot, cr);
+    prefix = (prefix << (level == 2 ? 8 : 12)) | cr->bin;   // b1, then (b1, b2), then K*
+    need = cr->need;
   }
-  if (LEVEL == 3) {
-    above = wave_sum_int(above);
-    if (lane_id() == 0) atomicAdd(&cnt_s[kBins3], uint32_t(above));
+  const uint32_t kstar = prefix;
+  // per part: keys >= K*
+  for (int j = t; j < parts_r; j += kT) cnt[j] = 0;
+  __syncthreads();
+  float v[kPT];
+  for (int base = 0; base < nr; base += kSub) {
+    load_sub(srow, base, nr, v);
+    int c = 0;
+#pragma unroll
+    for (int k = 0; k < kPT; ++k) c += (in_range(base, nr, k) && score_key(v[k]) >= kstar) ? 1 : 0;
+    c = wave_sum_int(c);
+    if (lane_id() == 0 && c) atomicAdd(&cnt[base / (spb * kSub)], uint32_t(c));
   }
   __syncthreads();
-  u64* g = rh + (LEVEL == 2 ? kBins1 : kBins1 + kBins2);
-  for (int b = threadIdx.x; b < kBins; b += kT)
-    if (h[b]) atomicAdd(&g[b], h[b]);
-  if (LEVEL == 2) flush_coarse(h, coarse + kCoarse);
-  if (LEVEL == 3) {
-    // this block's count above the bin, then suffix counts of the 256 sub-bins
-    static_assert(kBins3 == kT, "one sub-bin per thread");
-    int32_t* cc = chunk_cnt + (int64_t(row) * gridDim.x + c) * (1 + kBins3);
-    const int t = threadIdx.x, ln = lane_id(), wv = t / kWave;
-    int x = int(cnt_s[t]);
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {   // inclusive suffix sum inside the wave
-      const int y = __shfl_down(x, o, kWave);
-      if (ln + o < kWave) x += y;
-    }
-    if (ln == 0) red2[wv] = x;
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < kTW; ++u)
-      if (u > wv) x += red2[u];
-    cc[1 + t] = x;
-    if (t == 0) cc[0] = int32_t(cnt_s[kBins3]);
-  }
+  return kstar;
 }
 
 template <bool RAGGED, bool MULTI>
-__global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict__ scores, int n, int chunks, int spb,
-                                                        float p, const u64* __restrict__ hist,
-                                                        uint32_t* __restrict__ state,
-                                                        const int32_t* __restrict__ chunk_cnt,
-                                                        int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_count,
-                                                        u64* __restrict__ masks, const int32_t* __restrict__ seq_n,
-                                                        const float* __restrict__ seq_p, int hq) {
+__global__ __launch_bounds__(kT) void sel_final_kernel(const float* __restrict__ scores, int n, int spb, int parts,
+                                                       int group, int rows, float p, float scale_log2e,
+                                                       const unsigned char* __restrict__ part2,
+                                                       const uint32_t* __restrict__ state,
+                                                       int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_count,
+                                                       u64* __restrict__ masks, int mask_words,
+                                                       const int32_t* __restrict__ seq_n,
+                                                       const float* __restrict__ seq_p, int hq) {
+  __shared__ uint32_t ck[kSelCandLds];     // the row's candidate keys
+  __shared__ u64 h[kSelBins];
   __shared__ u64 wtot[kTW];
-  __shared__ int red[kTW];
-  __shared__ int kcnt[kPT][kTW];
   __shared__ Crossing cr;
-  const int row = blockIdx.y, c = blockIdx.x;
-  const int wave = threadIdx.x / kWave, lane = lane_id();
-  uint32_t* st = state + int64_t(row) * kToppStateWords;
-  static_assert(kBins3 == kT, "one final-level bin per thread");
-  const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, row, n, p) : RowSel{n, p};
-  const Span sp = block_span<MULTI>(c, spb, chunks, rs.n);
-  if (RAGGED && sp.cs1 <= sp.cs0) {   // block-uniform: no key of this row here (a row without keys selects none)
-    if (c == 0 && threadIdx.x == 0) sel_count[row] = 0;
+  __shared__ P2Head ph[kSelMaxParts];
+  __shared__ int pstart[kSelMaxParts + 1];
+  __shared__ uint32_t pcnt[kSelMaxParts];
+  __shared__ int kcnt[kPT][kTW];
+  __shared__ int red[kTW];
+  __shared__ int fast_s;
+  __shared__ u64 T_s, A_s;
+  const SelWork wk = sel_work(parts, group, rows);
+  if (!wk.ok) return;
+  const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, wk.row, n, p) : RowSel{n, p};
+  const int k0 = wk.part * spb * kSub;
+  if (k0 >= rs.n) {   // block-uniform: no key of this row here (a row without keys selects none)
+    if (RAGGED && rs.n == 0 && wk.part == 0 && threadIdx.x == 0) sel_count[wk.row] = 0;
     return;
   }
-  const u64 hv = hist[int64_t(row) * kHistPerRow + kBins1 + kBins2 + threadIdx.x];
-  const float* srow = scores + int64_t(row) * n;
-  float v[kPT], vn[kPT];
-  load_chunk(srow, rs.n, sp.cs0, v);
-  const bool all = RAGGED && rs.p >= 1.f;   // every key of the row (the histogram passes skipped it)
+  const int k1 = min(rs.n, k0 + spb * kSub);
+  const int span = spb * kSub;
+  const int parts_r = (rs.n + span - 1) / span;
+  const int t = threadIdx.x, lane = lane_id(), wave = t / kWave;
+  const float* srow = scores + int64_t(wk.row) * n;
+  float v[kPT];
+  load_sub(srow, k0, k1, v);
+  const bool all = RAGGED && rs.p >= 1.f;   // every key of the row (the first two passes skipped it)
   uint32_t kstar = 0u;                      // keys >= kstar are selected (every key is >= 0)
-  int offset = sp.cs0 * kChunk;
+  int offset = k0, total_sel = rs.n;
   if (!all) {
-    const u64 T = (u64(st[5]) << 32) | st[4];
-    find_crossing<1>(&hv, T, 0.f, wtot, &cr);
-    kstar = (st[3] << 8) | cr.bin;
-    // offset of this block = selected keys of the blocks before it
-    const int32_t* cc = chunk_cnt + int64_t(row) * gridDim.x * (1 + kBins3);
-    int before = 0;
-    for (int k = threadIdx.x; k < c; k += kT) before += cc[k * (1 + kBins3)] + cc[k * (1 + kBins3) + 1 + cr.bin];
-    before = wave_sum_int(before);
-    if (lane == 0) red[wave] = before;
+    const unsigned char* P2row = part2 + int64_t(wk.row) * parts * kSelPart2Bytes;
+    if (t < parts_r) ph[t] = *reinterpret_cast<const P2Head*>(P2row + int64_t(t) * kSelPart2Bytes);
+    const float M = __uint_as_float(state[int64_t(wk.row) * kSelStateWords]);
+    const uint32_t b1 = state[int64_t(wk.row) * kSelStateWords + 1];
     __syncthreads();
-    offset = 0;
+    if (t < kWave) {   // wave 0: the exact target and whether b1 holds the crossing
+      const bool in = t < parts_r;
+      const u64 Z = wave_sum_u64(in ? ph[t].total : 0ull);
+      const u64 A = wave_sum_u64(in ? ph[t].above_mass : 0ull);
+      const u64 C = wave_sum_u64(in ? ph[t].cand_mass : 0ull);
+      const uint32_t cc = in ? ph[t].cand_cnt : 0u;
+      const bool over = __ballot(cc > uint32_t(kSelCandCap)) != 0ull;
+      // candidate start positions (exclusive prefix over the parts)
+      int x = int(cc);
 #pragma unroll
-    for (int w = 0; w < kTW; ++w) offset += red[w];
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(x, o, kWave);
+        if (t >= o) x += y;
+      }
+      if (in) pstart[t + 1] = x;
+      if (t == 0) pstart[0] = 0;
+      const int ncand = __shfl(x, kWave - 1, kWave);
+      const u64 T = u64(ceil(double(rs.p) * double(Z)));
+      if (t == 0) {
+        T_s = T;
+        A_s = A;
+        fast_s = !over && ncand <= kSelCandLds && A < T && T <= A + C;
+      }
+    }
+    __syncthreads();
+    const u64 T = T_s;
+    if (fast_s) {
+      // the row's candidates into LDS (all loads in flight), the histogram cleared meanwhile
+      const int ncand = pstart[parts_r];
+      for (int b = t; b < kSelBins; b += kT) h[b] = 0;
+      for (int i = t; i < ncand; i += kT) {
+        int lo = 0, hi = parts_r - 1;   // the part holding candidate i
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (pstart[mid] <= i) lo = mid;
+          else hi = mid - 1;
+        }
+        ck[i] = reinterpret_cast<const uint32_t*>(P2row + int64_t(lo) * kSelPart2Bytes + kSelP2Cand)[i - pstart[lo]];
+      }
+      if (t < parts_r) pcnt[t] = 0;
+      __syncthreads();
+      // level 2: key bits 19..8 of the candidates
+      for (int i = t; i < ncand; i += kT) {
+        const uint32_t key = ck[i];
+        const u64 e = fixed_mass(key_score(key), M, scale_log2e);
+        if (e) atomicAdd(&h[(key >> 8) & 0xfffu], e);
+      }
+      __syncthreads();
+      lds_crossing<kSelBins>(h, T - A_s, wtot, &cr);
+      const uint32_t b2 = cr.bin;
+      const u64 need2 = cr.need;
+      const uint32_t pre = (b1 << 12) | b2;
+      for (int b = t; b < kSelBins3; b += kT) h[b] = 0;
+      __syncthreads();
+      // level 3: key bits 7..0 of the candidates inside (b1, b2)
+      for (int i = t; i < ncand; i += kT) {
+        const uint32_t key = ck[i];
+        if ((key >> 8) == pre) {
+          const u64 e = fixed_mass(key_score(key), M, scale_log2e);
+          if (e) atomicAdd(&h[key & 0xffu], e);
+        }
+      }
+      __syncthreads();
+      lds_crossing<kSelBins3>(h, need2, wtot, &cr);
+      kstar = (pre << 8) | cr.bin;
+      // per part: candidates >= K*
+      for (int i = t; i < ncand; i += kT) {
+        if (ck[i] >= kstar) {
+          int lo = 0, hi = parts_r - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (pstart[mid] <= i) lo = mid;
+            else hi = mid - 1;
+          }
+          atomicAdd(&pcnt[lo], 1u);
+        }
+      }
+      __syncthreads();
+      if (t < parts_r) pcnt[t] += ph[t].above_cnt;
+      __syncthreads();
+    } else {
+      kstar = exact_select_row<MULTI>(srow, rs.n, spb, parts_r, M, scale_log2e, T, h, wtot, &cr, pcnt);
+    }
+    // offset of this part = selected keys of the parts before it
+    if (t < kWave) {
+      const int c = t < parts_r ? int(pcnt[t]) : 0;
+      const int before = wave_sum_int(t < wk.part ? c : 0);
+      const int tot = wave_sum_int(c);
+      if (t == 0) {
+        red[0] = before;
+        red[1] = tot;
+      }
+    }
+    __syncthreads();
+    offset = red[0];
+    total_sel = red[1];
   }
 
-  // ascending compaction, sub-chunk by sub-chunk: element (k, thread) of sub-chunk cs has
-  // index cs*kChunk + k*kT + thread, so the order is k-major, then wave, then lane
-  int32_t* out = sel_idx + int64_t(row) * n;
-  for (int cs = sp.cs0; cs < (MULTI ? sp.cs1 : sp.cs0 + 1); ++cs) {
-    if (MULTI && cs + 1 < sp.cs1) load_chunk(srow, rs.n, cs + 1, vn);
+  // ascending compaction, sub-chunk by sub-chunk: element (k, thread) of a sub-chunk
+  // has index base + k*kT + thread, so the order is k-major, then wave, then lane
+  int32_t* out = sel_idx + int64_t(wk.row) * n;
+  for (int base = k0; base < k1; base += kSub) {
+    if (MULTI && base > k0) load_sub(srow, base, k1, v);
     uint64_t bal[kPT];
 #pragma unroll
     for (int k = 0; k < kPT; ++k) {
-      bal[k] = __ballot(in_row(rs.n, cs, k) && score_key(v[k]) >= kstar);
+      bal[k] = __ballot(in_range(base, k1, k) && score_key(v[k]) >= kstar);
       if (lane == 0) {
         kcnt[k][wave] = __popcll(bal[k]);
-        // keys cs*kChunk + k*kT + 64 wave + [0, 64) of the row's selection bitmap
-        if (masks) masks[int64_t(row) * chunks * (kChunk / 64) + cs * (kChunk / 64) + k * kTW + wave] = bal[k];
+        // keys base + k*kT + 64 wave + [0, 64) of the row's selection bitmap
+        if (masks) masks[int64_t(wk.row) * mask_words + (base + k * kT) / 64 + wave] = bal[k];
       }
-      if (MULTI) v[k] = vn[k];
     }
     __syncthreads();
 #pragma unroll
@@ -460,22 +674,23 @@ __global__ __launch_bounds__(kT) void topp_write_kernel(const float* __restrict_
       if ((bal[k] >> lane) & 1u) {
         const int pre =
             __builtin_amdgcn_mbcnt_hi(uint32_t(bal[k] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal[k]), 0u));
-        out[offset + woff + pre] = cs * kChunk + k * kT + int(threadIdx.x);
+        out[offset + woff + pre] = base + k * kT + t;
       }
       offset += tot;
     }
-    if (MULTI && cs + 1 < sp.cs1) __syncthreads();   // kcnt is rewritten for the next sub-chunk
+    if (!MULTI) break;
+    __syncthreads();   // kcnt is rewritten for the next sub-chunk
   }
-  // the block holding the row's last key writes the count
-  const int last = RAGGED ? ((rs.n - 1) / kChunk) / spb : int(gridDim.x) - 1;
-  if (c == last && threadIdx.x == 0) sel_count[row] = offset;
+  // the part holding the row's last key writes the count
+  if (wk.part == parts_r - 1 && t == 0) sel_count[wk.row] = total_sel;
 }
 
-__global__ __launch_bounds__(kT) void topp_all_kernel(int n, int32_t* __restrict__ sel_idx,
-                                                      int32_t* __restrict__ sel_count, u64* __restrict__ masks,
-                                                      int mask_words) {
+constexpr int kAllThreads = 256;
+__global__ __launch_bounds__(kAllThreads) void topp_all_kernel(int n, int32_t* __restrict__ sel_idx,
+                                                               int32_t* __restrict__ sel_count,
+                                                               u64* __restrict__ masks, int mask_words) {
   const int row = blockIdx.y;
-  const int i = blockIdx.x * kT + threadIdx.x;
+  const int i = blockIdx.x * kAllThreads + threadIdx.x;
   if (i < n) sel_idx[int64_t(row) * n + i] = i;
   if (blockIdx.x == 0 && threadIdx.x == 0) sel_count[row] = n;
   if (masks && (i & 63) == 0 && i / 64 < mask_words) {
@@ -484,58 +699,47 @@ __global__ __launch_bounds__(kT) void topp_all_kernel(int n, int32_t* __restrict
   }
 }
 
-constexpr int kToppWaveBlocks = 1024;   // blocks per pass the sub-chunks are shared out to (about one wave)
-
 template <bool RAGGED, bool MULTI>
-void topp_passes(int rows, hipStream_t stream, int n, int chunks, int spb, const float* scores, float p,
-                 float scale_log2e, const ToppWorkspace& w, int32_t* sel_idx, int32_t* sel_count,
-                 const float* slot_max, int nslots, u64* masks, const int32_t* seq_n, const float* seq_p,
-                 int heads_q) {
-  const dim3 grid((chunks + spb - 1) / spb, rows);
-  const float* rmax = slot_max;
-  int nmax = nslots;
-  if (slot_max == nullptr) {   // otherwise the score launch has written the maxima and cleared the counters
-    topp_max_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, w.chunk_max, w.hist, seq_n, heads_q);
-    rmax = w.chunk_max;
-    nmax = int(grid.x);
-  }
-  topp_level1_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, rmax, nmax, scale_log2e, p, w.hist,
-                                                      w.state, seq_n, seq_p, heads_q);
-  topp_level_kernel<2, RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, scale_log2e, p, w.hist, w.state,
-                                                        w.chunk_cnt, seq_n, seq_p, heads_q);
-  topp_level_kernel<3, RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, scale_log2e, p, w.hist, w.state,
-                                                        w.chunk_cnt, seq_n, seq_p, heads_q);
-  topp_write_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, chunks, spb, p, w.hist, w.state, w.chunk_cnt, sel_idx,
-                                                     sel_count, masks, seq_n, seq_p, heads_q);
+void sel_passes(int rows, int group, hipStream_t stream, int n, const ToppPlan& pl, const float* scores, float p,
+                float scale_log2e, const ToppWorkspace& w, int32_t* sel_idx, int32_t* sel_count, u64* masks,
+                int mask_words, const int32_t* seq_n, const float* seq_p, int heads_q) {
+  const dim3 grid(unsigned(xcd_grid(int64_t(rows / group) * pl.parts, group)));
+  sel_hist_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, pl.spb, pl.parts, group, rows, scale_log2e,
+                                                          w.part1, seq_n, seq_p, heads_q);
+  sel_cand_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, pl.spb, pl.parts, group, rows, p, scale_log2e,
+                                                          w.part1, w.part2, w.state, seq_n, seq_p, heads_q);
+  sel_final_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, pl.spb, pl.parts, group, rows, p, scale_log2e,
+                                                           w.part2, w.state, sel_idx, sel_count, masks, mask_words,
+                                                           seq_n, seq_p, heads_q);
 }
 
 }  // namespace
 
 rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,
-                       int32_t* sel_count, void* ws, hipStream_t stream, const float* slot_max, int32_t nslots,
+                       int32_t* sel_count, void* ws, hipStream_t stream, int32_t group,
                        unsigned long long* masks, const int32_t* seq_n, const float* seq_p, int32_t heads_q) {
   const int mask_words = topp_mask_words(n);
   const bool ragged = seq_n != nullptr || seq_p != nullptr;   // per-row counts / p: decided on the device
   if (n == 0 || (p >= 1.0f && !ragged)) {
     // every key (or none) is selected
     const int cover = masks ? mask_words * 64 : n;
-    const dim3 grid(cover > 0 ? (cover + kT - 1) / kT : 1, rows);
-    topp_all_kernel<<<grid, kT, 0, stream>>>(n, sel_idx, sel_count, masks, mask_words);
+    const dim3 grid(cover > 0 ? (cover + kAllThreads - 1) / kAllThreads : 1, rows);
+    topp_all_kernel<<<grid, kAllThreads, 0, stream>>>(n, sel_idx, sel_count, masks, mask_words);
     return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
   }
-  const int chunks = (n + kChunk - 1) / kChunk;
-  ToppWorkspace w = topp_workspace(ws, rows, n);
+  if (group < 1 || rows % group != 0) group = 1;
+  const ToppPlan pl = topp_plan(n);
+  const ToppWorkspace w = topp_workspace(ws, rows, n);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
-  const int spb = int(std::min<int64_t>(chunks, std::max<int64_t>(1, int64_t(rows) * chunks / kToppWaveBlocks)));
-#define RBQ_TOPP_PASSES(RG, MU)                                                                                  \
-  topp_passes<RG, MU>(rows, stream, n, chunks, spb, scores, p, scale_log2e, w, sel_idx, sel_count, slot_max,   \
-                      nslots, masks, RG ? seq_n : nullptr, RG ? seq_p : nullptr, heads_q)
+#define RBQ_SEL_PASSES(RG, MU)                                                                                  \
+  sel_passes<RG, MU>(rows, group, stream, n, pl, scores, p, scale_log2e, w, sel_idx, sel_count, masks, mask_words, \
+                     RG ? seq_n : nullptr, RG ? seq_p : nullptr, heads_q)
   if (ragged) {
-    if (spb > 1) RBQ_TOPP_PASSES(true, true); else RBQ_TOPP_PASSES(true, false);
+    if (pl.spb > 1) RBQ_SEL_PASSES(true, true); else RBQ_SEL_PASSES(true, false);
   } else {
-    if (spb > 1) RBQ_TOPP_PASSES(false, true); else RBQ_TOPP_PASSES(false, false);
+    if (pl.spb > 1) RBQ_SEL_PASSES(false, true); else RBQ_SEL_PASSES(false, false);
   }
-#undef RBQ_TOPP_PASSES
+#undef RBQ_SEL_PASSES
   return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
 }
 

@@ -68,19 +68,25 @@ rbq_status check_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
   return RBQ_OK;
 }
 
+ToppPlan topp_plan(int32_t n) {
+  const int64_t subs = n > 0 ? (int64_t(n) + kSelSub - 1) / kSelSub : 1;
+  ToppPlan pl;
+  pl.spb = int32_t((subs + kSelMaxParts - 1) / kSelMaxParts);
+  pl.parts = int32_t((subs + pl.spb - 1) / pl.spb);
+  return pl;
+}
+
 ToppWorkspace topp_workspace(void* base, int64_t rows, int32_t n) {
-  const int64_t chunks = n > 0 ? (int64_t(n) + kToppChunk - 1) / kToppChunk : 1;
+  const ToppPlan pl = topp_plan(n);
   ToppWorkspace w{};
   size_t off = 0;
   char* b = static_cast<char*>(base);
-  w.hist = reinterpret_cast<unsigned long long*>(b + off);
-  off = align_up(off + size_t(rows) * kHistPerRow * sizeof(unsigned long long), 256);
-  w.chunk_max = reinterpret_cast<float*>(b + off);
-  off = align_up(off + size_t(rows) * chunks * sizeof(float), 256);
-  w.chunk_cnt = reinterpret_cast<int32_t*>(b + off);
-  off = align_up(off + size_t(rows) * chunks * (1 + kBins3) * sizeof(int32_t), 256);
+  w.part1 = reinterpret_cast<unsigned char*>(b + off);
+  off = align_up(off + size_t(rows) * pl.parts * kSelPart1Bytes, 256);
+  w.part2 = reinterpret_cast<unsigned char*>(b + off);
+  off = align_up(off + size_t(rows) * pl.parts * kSelPart2Bytes, 256);
   w.state = reinterpret_cast<uint32_t*>(b + off);
-  off = align_up(off + size_t(rows) * kToppStateWords * sizeof(uint32_t), 256);
+  off = align_up(off + size_t(rows) * kSelStateWords * sizeof(uint32_t), 256);
   w.bytes = off;
   return w;
 }
@@ -89,6 +95,9 @@ rbq_status check_topp(int32_t batch, int32_t heads_q, int32_t n, const float* sc
                       const int32_t* sel_idx, const int32_t* sel_count, const void* ws, size_t ws_bytes) {
   if (batch <= 0 || heads_q <= 0 || n < 0) return RBQ_EINVAL;
   if (int64_t(batch) * heads_q > 65535) return RBQ_EINVAL;
+  // a row's softmax masses are summed as 2^-40 fixed-point integers of at most
+  // 2^40 each in 64 bits: exact only below 2^24 keys per row
+  if (n >= kToppMaxKeys) return RBQ_EUNSUPPORTED;
   if (!(p > 0.0f) || !(p <= 1.0f)) return RBQ_EINVAL;                  // also rejects NaN
   if (!std::isfinite(sm_scale) || !(sm_scale > 0.0f)) return RBQ_EINVAL;
   if (bad_ptr(sel_count)) return RBQ_EINVAL;
@@ -108,22 +117,22 @@ DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w
   const int64_t groups = int64_t(batch) * heads_kv;
   s.chunk = kDecodeChunk;
   while (s.chunk > 256 && groups * ((int64_t(n) + s.chunk - 1) / s.chunk) < kDecodeMinBlocks) s.chunk /= 2;
-  s.idx_splits = n > 0 ? (n + s.chunk - 1) / s.chunk : 0;
-  s.win_splits = w > 0 ? (w + kDecodeWinChunk - 1) / kDecodeWinChunk : 0;
+  s.idx_splits = n > 0 ? int32_t((int64_t(n) + s.chunk - 1) / s.chunk) : 0;
+  s.win_splits = w > 0 ? int32_t((int64_t(w) + kDecodeWinChunk - 1) / kDecodeWinChunk) : 0;
   if (tail_window && s.idx_splits > 0 && w > 0) {
     if (ragged) {
       const int cap = kDecodeListCap - s.chunk;   // window rows a split's list can still take
-      if ((w + cap - 1) / cap <= s.idx_splits) {
+      if ((int64_t(w) + cap - 1) / cap <= s.idx_splits) {
         s.fold_wq = cap;
         s.win_splits = 0;
       }
     } else if (sparse) {
-      const int wq = (w + s.idx_splits - 1) / s.idx_splits;
+      const int64_t wq = (int64_t(w) + s.idx_splits - 1) / s.idx_splits;
       if (wq <= kDecodeFoldMax) {
-        s.fold_wq = wq;
+        s.fold_wq = int32_t(wq);
         s.win_splits = 0;
       }
-    } else if (n - (s.idx_splits - 1) * s.chunk + w <= s.chunk) {
+    } else if (int64_t(n) - int64_t(s.idx_splits - 1) * s.chunk + w <= s.chunk) {
       s.fold_s0 = s.idx_splits - 1;
       s.fold_wq = w;
       s.win_splits = 0;
@@ -171,11 +180,9 @@ int score_keys_per_lane(int32_t batch, int32_t heads_kv, int32_t n) {
   if (kv_keys >= int64_t(kScoreThreads) * 2 * 1024) return 2;
   return 1;
 }
-int score_blocks_per_row(int32_t batch, int32_t heads_kv, int32_t n) {
-  const int per_block = kScoreThreads * score_keys_per_lane(batch, heads_kv, n);
-  return (n + per_block - 1) / per_block;
+int topp_mask_words(int32_t n) {
+  return n > 0 ? int((int64_t(n) + kSelSub - 1) / kSelSub * (kSelSub / 64)) : 0;
 }
-int topp_mask_words(int32_t n) { return n > 0 ? (n + kToppChunk - 1) / kToppChunk * (kToppChunk / 64) : 0; }
 
 StepWorkspace step_workspace(void* base, int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
                              int32_t n, int32_t w) {
@@ -188,8 +195,6 @@ StepWorkspace step_workspace(void* base, int32_t batch, int32_t heads_q, int32_t
   s.topp = b + off;
   s.topp_bytes = topp_workspace(nullptr, rows, n).bytes;
   off = align_up(off + s.topp_bytes, 256);
-  s.slot_max = reinterpret_cast<float*>(b + off);
-  off = align_up(off + size_t(rows) * score_blocks_per_row(batch, heads_kv, n) * sizeof(float), 256);
   s.masks = reinterpret_cast<unsigned long long*>(b + off);
   off = align_up(off + size_t(rows) * topp_mask_words(n) * sizeof(unsigned long long), 256);
   s.bytes = off;

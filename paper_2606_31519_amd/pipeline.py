@@ -215,14 +215,21 @@ class DecodeSession:
         if not 0 < window <= rbq.RBQ_MAX_WINDOW or n_prefill + window > cap:
             raise ValueError("the window must fit after the prefill rows (n_prefill + window <= cap)")
         q = torch.zeros(B, Hq, D, dtype=torch.float32, device=device)
-        # sized for the largest index: every buffer and workspace grows with n
-        self.state = DecodeState(B, Hq, Hkv, D, cap, cap - window, window, K, V, q, P, c_q, device, compact)
+        # Every flush adds a whole window to the index, and append() keeps
+        # n + w <= cap, so the index sizes a step can see are n_prefill + k * window
+        # up to cap (the last one may leave less than a window of room, and the
+        # steps after it run with that index and a partial window).
+        self.n_sizes = list(range(n_prefill, cap + 1, window))
+        self.n_max = self.n_sizes[-1]
+        # sized for the largest index: the scores, selections and per-row workspaces grow with n
+        self.state = DecodeState(B, Hq, Hkv, D, cap, self.n_max, window, K, V, q, P, c_q, device, compact)
         self.n, self.w, self.window = n_prefill, 0, window
         st = self.state
         # the step workspace is not monotonic in n (smaller indexes may take more,
-        # shorter decode splits): size it for every index size the loop will pass
+        # shorter decode splits): size it for every index size the loop will pass;
+        # for a given n it grows with the window rows, so the full window bounds it
         need = max(rbq.rbq_workspace_bytes(rbq.RBQ_OP_DECODE_STEP, B, Hq, Hkv, D, m, window)
-                   for m in range(n_prefill, cap - window + 1, window))
+                   for m in self.n_sizes)
         if need > st.ws_step.numel():
             st.ws_step = torch.empty(need, dtype=torch.uint8, device=device)
         if compact:
@@ -249,6 +256,9 @@ class DecodeSession:
         state.lse; the selection is state.sel_idx / state.sel_count (row stride:
         the n of this step, self.n before a flush)."""
         st = self.state
+        if self.n > self.n_max or self.n + self.w > st.cap:
+            raise RuntimeError(f"index of {self.n} keys + {self.w} window rows exceeds the session's buffers "
+                               f"({self.n_max} keys, cap {st.cap})")
         st.q.copy_(q)
         flush = self.w == self.window
         if st.compact:

@@ -122,6 +122,15 @@ def _check(name, st):
         raise RbqError(name, st)
 
 
+def _need(name, **sizes):
+    """Refuse a tensor smaller than what the call reads or writes through it:
+    the C ABI takes bare pointers and cannot see buffer sizes. Each keyword is
+    name=(tensor or None, elements needed)."""
+    for arg, (t, count) in sizes.items():
+        if isinstance(t, torch.Tensor) and t.numel() < count:
+            raise ValueError(f"{name}: {arg} holds {t.numel()} elements, the call needs {count}")
+
+
 class MappedHost:
     """A pinned host tensor handed to the kernels by its device address
     (hipHostGetDevicePointer), so that they read it over PCIe: a K/V cache kept
@@ -187,6 +196,8 @@ def rbq_encode_keys(batch, heads_kv, head_dim, keys, keys_ld, n_new, offset, cap
 
 def rbq_quantize_query(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, qplanes, qscal, stream=None,
                        qrot_out=None):
+    _need("rbq_quantize_query", qplanes=(qplanes, batch * heads_q * 4 * (head_dim // 32)),
+          qscal=(qscal, batch * heads_q * QSCAL_STRIDE))
     args = (batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_q), _ptr(c_k), _ptr(qplanes), _ptr(qscal))
     if qrot_out is None:
         _check("rbq_quantize_query", lib.rbq_quantize_query(*args, _stream(stream)))
@@ -201,27 +212,33 @@ def rbq_quantize_query_bits(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, 
 
 
 def rbq_score(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes, qscal, scores, stream=None):
+    _need("rbq_score", scores=(scores, batch * heads_q * n))
     _check("rbq_score", lib.rbq_score(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(codes), _ptr(kfac),
                                       _ptr(qplanes), _ptr(qscal), _ptr(scores), _stream(stream)))
 
 
 def rbq_score_q8(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac, qplanes8, qscal, scores, stream=None):
     """rbq_score for queries of up to 8 bits (eight bit-planes per head)."""
+    _need("rbq_score_q8", scores=(scores, batch * heads_q * n))
     _check("rbq_score_q8", lib.rbq_score_q8(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(codes), _ptr(kfac),
                                             _ptr(qplanes8), _ptr(qscal), _ptr(scores), _stream(stream)))
 
 
 def rbq_score_ints_q8(batch, heads_q, heads_kv, head_dim, n, cap, codes, qplanes8, ip_out, pc_out, stream=None):
+    _need("rbq_score_ints_q8", ip_out=(ip_out, batch * heads_q * n), pc_out=(pc_out, batch * heads_kv * n))
     _check("rbq_score_ints_q8", lib.rbq_score_ints_q8(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(codes),
                                                       _ptr(qplanes8), _ptr(ip_out), _ptr(pc_out), _stream(stream)))
 
 
 def rbq_score_ints(batch, heads_q, heads_kv, head_dim, n, cap, codes, qplanes, ip_out, pc_out, stream=None):
+    _need("rbq_score_ints", ip_out=(ip_out, batch * heads_q * n), pc_out=(pc_out, batch * heads_kv * n))
     _check("rbq_score_ints", lib.rbq_score_ints(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(codes),
                                                 _ptr(qplanes), _ptr(ip_out), _ptr(pc_out), _stream(stream)))
 
 
 def rbq_topp_select(batch, heads_q, n, scores, p, sm_scale, sel_idx, sel_count, ws, stream=None):
+    _need("rbq_topp_select", scores=(scores, batch * heads_q * n), sel_idx=(sel_idx, batch * heads_q * n),
+          sel_count=(sel_count, batch * heads_q))
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check("rbq_topp_select", lib.rbq_topp_select(batch, heads_q, n, _ptr(scores), p, sm_scale, _ptr(sel_idx),
                                                   _ptr(sel_count), _ptr(ws), ws_bytes, _stream(stream)))
@@ -229,6 +246,8 @@ def rbq_topp_select(batch, heads_q, n, scores, p, sm_scale, sel_idx, sel_count, 
 
 def rbq_sparse_decode(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, sel_idx, sel_count, K_loc, V_loc,
                       loc_ld, w, sm_scale, out, lse, ws, stream=None):
+    _need("rbq_sparse_decode", sel_idx=(sel_idx, batch * heads_q * n), sel_count=(sel_count, batch * heads_q),
+          out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q))
     ws_bytes = ws.numel() * ws.element_size()
     _check("rbq_sparse_decode", lib.rbq_sparse_decode(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n, _ptr(sel_idx),
@@ -238,6 +257,7 @@ def rbq_sparse_decode(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, sel_i
 
 def rbq_dense_decode(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, K_loc, V_loc, loc_ld, w, sm_scale, out,
                      lse, ws, stream=None):
+    _need("rbq_dense_decode", out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q))
     ws_bytes = ws.numel() * ws.element_size()
     _check("rbq_dense_decode", lib.rbq_dense_decode(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n, _ptr(K_loc),
@@ -246,6 +266,10 @@ def rbq_dense_decode(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, K_loc,
 
 def rbq_decode_step(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, cap, n, w, codes, kfac, flush, p,
                     sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws, stream=None):
+    _need("rbq_decode_step", qplanes=(qplanes, batch * heads_q * 4 * (head_dim // 32)),
+          qscal=(qscal, batch * heads_q * QSCAL_STRIDE), scores=(scores, batch * heads_q * n),
+          sel_idx=(sel_idx, batch * heads_q * n), sel_count=(sel_count, batch * heads_q),
+          out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q))
     ws_bytes = ws.numel() * ws.element_size()
     _check("rbq_decode_step", lib.rbq_decode_step(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_q), _ptr(c_k), _ptr(K), _ptr(V),
@@ -259,12 +283,15 @@ def rbq_decode_step(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, ca
 
 def rbq_score_varlen(batch, heads_q, heads_kv, head_dim, n, cap, seq_n, codes, kfac, qplanes, qscal, scores,
                      stream=None):
+    _need("rbq_score_varlen", scores=(scores, batch * heads_q * n), seq_n=(seq_n, batch))
     _check("rbq_score_varlen", lib.rbq_score_varlen(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(seq_n),
                                                     _ptr(codes), _ptr(kfac), _ptr(qplanes), _ptr(qscal),
                                                     _ptr(scores), _stream(stream)))
 
 
 def rbq_topp_select_varlen(batch, heads_q, n, seq_n, scores, seq_p, sm_scale, sel_idx, sel_count, ws, stream=None):
+    _need("rbq_topp_select_varlen", scores=(scores, batch * heads_q * n), sel_idx=(sel_idx, batch * heads_q * n),
+          sel_count=(sel_count, batch * heads_q), seq_n=(seq_n, batch), seq_p=(seq_p, batch))
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check("rbq_topp_select_varlen", lib.rbq_topp_select_varlen(
         batch, heads_q, n, _ptr(seq_n), _ptr(scores), _ptr(seq_p), sm_scale, _ptr(sel_idx), _ptr(sel_count),
@@ -273,6 +300,9 @@ def rbq_topp_select_varlen(batch, heads_q, n, seq_n, scores, seq_p, sm_scale, se
 
 def rbq_sparse_decode_varlen(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, w, seq_n, seq_w, sel_idx,
                              sel_count, sm_scale, out, lse, ws, stream=None):
+    _need("rbq_sparse_decode_varlen", sel_idx=(sel_idx, batch * heads_q * n), sel_count=(sel_count, batch * heads_q),
+          out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q), seq_n=(seq_n, batch),
+          seq_w=(seq_w, batch))
     ws_bytes = ws.numel() * ws.element_size()
     _check("rbq_sparse_decode_varlen", lib.rbq_sparse_decode_varlen(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n, w, _ptr(seq_n),
@@ -282,6 +312,8 @@ def rbq_sparse_decode_varlen(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n
 
 def rbq_dense_decode_varlen(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, w, seq_n, seq_w, sm_scale, out,
                             lse, ws, stream=None):
+    _need("rbq_dense_decode_varlen", out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q),
+          seq_n=(seq_n, batch), seq_w=(seq_w, batch))
     ws_bytes = ws.numel() * ws.element_size()
     _check("rbq_dense_decode_varlen", lib.rbq_dense_decode_varlen(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n, w, _ptr(seq_n),
@@ -291,6 +323,11 @@ def rbq_dense_decode_varlen(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n,
 def rbq_decode_step_varlen(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, cap, n, w, seq_n, seq_w, codes,
                            kfac, flush, seq_p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws,
                            stream=None):
+    _need("rbq_decode_step_varlen", qplanes=(qplanes, batch * heads_q * 4 * (head_dim // 32)),
+          qscal=(qscal, batch * heads_q * QSCAL_STRIDE), scores=(scores, batch * heads_q * n),
+          sel_idx=(sel_idx, batch * heads_q * n), sel_count=(sel_count, batch * heads_q),
+          out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q),
+          seq_n=(seq_n, batch), seq_w=(seq_w, batch), seq_p=(seq_p, batch))
     ws_bytes = ws.numel() * ws.element_size()
     _check("rbq_decode_step_varlen", lib.rbq_decode_step_varlen(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_q), _ptr(c_k), _ptr(K), _ptr(V),
@@ -311,12 +348,17 @@ def rbq_encode_keys_f16(batch, heads_kv, head_dim, keys, keys_ld, n_new, offset,
 
 
 def rbq_score_f16(batch, heads_q, heads_kv, head_dim, n, cap, codes, kfac16, qplanes, qscal, scores, stream=None):
+    _need("rbq_score_f16", scores=(scores, batch * heads_q * n))
     _check("rbq_score_f16", lib.rbq_score_f16(batch, heads_q, heads_kv, head_dim, n, cap, _ptr(codes), _ptr(kfac16),
                                               _ptr(qplanes), _ptr(qscal), _ptr(scores), _stream(stream)))
 
 
 def rbq_decode_step_f16(batch, heads_q, heads_kv, head_dim, q, P, c_k, K, V, cap, n, w, codes, kfac16, flush, p,
                         sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws, stream=None):
+    _need("rbq_decode_step_f16", qplanes=(qplanes, batch * heads_q * 4 * (head_dim // 32)),
+          qscal=(qscal, batch * heads_q * QSCAL_STRIDE), scores=(scores, batch * heads_q * n),
+          sel_idx=(sel_idx, batch * heads_q * n), sel_count=(sel_count, batch * heads_q),
+          out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q))
     ws_bytes = ws.numel() * ws.element_size()
     _check("rbq_decode_step_f16", lib.rbq_decode_step_f16(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_k), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n,
@@ -326,6 +368,7 @@ def rbq_decode_step_f16(batch, heads_q, heads_kv, head_dim, q, P, c_k, K, V, cap
 
 def rbq_score_varlen_f16(batch, heads_q, heads_kv, head_dim, n, cap, seq_n, codes, kfac16, qplanes, qscal, scores,
                          stream=None):
+    _need("rbq_score_varlen_f16", scores=(scores, batch * heads_q * n), seq_n=(seq_n, batch))
     _check("rbq_score_varlen_f16", lib.rbq_score_varlen_f16(
         batch, heads_q, heads_kv, head_dim, n, cap, _ptr(seq_n), _ptr(codes), _ptr(kfac16), _ptr(qplanes),
         _ptr(qscal), _ptr(scores), _stream(stream)))
@@ -334,6 +377,11 @@ def rbq_score_varlen_f16(batch, heads_q, heads_kv, head_dim, n, cap, seq_n, code
 def rbq_decode_step_varlen_f16(batch, heads_q, heads_kv, head_dim, q, P, c_k, K, V, cap, n, w, seq_n, seq_w, codes,
                                kfac16, flush, seq_p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse,
                                ws, stream=None):
+    _need("rbq_decode_step_varlen_f16", qplanes=(qplanes, batch * heads_q * 4 * (head_dim // 32)),
+          qscal=(qscal, batch * heads_q * QSCAL_STRIDE), scores=(scores, batch * heads_q * n),
+          sel_idx=(sel_idx, batch * heads_q * n), sel_count=(sel_count, batch * heads_q),
+          out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q),
+          seq_n=(seq_n, batch), seq_w=(seq_w, batch), seq_p=(seq_p, batch))
     ws_bytes = ws.numel() * ws.element_size()
     _check("rbq_decode_step_varlen_f16", lib.rbq_decode_step_varlen_f16(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_k), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n,

@@ -41,6 +41,63 @@ def planes_to_codes(planes: np.ndarray) -> np.ndarray:
     return sum(orc.unpack_bits(planes[j], D).astype(np.int64) << j for j in range(planes.shape[0]))
 
 
+# The GPU rotates the unit query in fp32: each component is a D-term dot product
+# of a column of P with u, whose fp32 rounding is at most D * 2^-24 * sum_j |P_jd u_j|
+# <= D * 2^-24 (Cauchy-Schwarz, unit vectors): 7.6e-6 at D = 128. q_l and q_r are
+# the minimum and maximum of those components, so each is within that of the
+# oracle's, and Delta = (q_r - q_l) / 15 within 2/15 of it plus its own rounding.
+ROT_ATOL = 1e-5
+
+
+def check_qscal(qs, planes, q, P, c_q, c_k, D=128):
+    """The per-head constants rbq_quantize_query wrote ({q_l, Delta, S_u, A, B0,
+    q_r}) against the oracle's Algorithm 2 step 1 for the same query and
+    centroids: A and B0 within fp32 rounding of their sums, q_l / q_r / Delta
+    within the rotation bound above, and S_u exactly the sum of the GPU's codes."""
+    ref = orc.quantize_query(np.asarray(q, np.float64), P, None if c_q is None else np.asarray(c_q, np.float64),
+                             np.asarray(c_k, np.float64))
+    qs = np.asarray(qs, np.float64)
+    assert abs(qs[3] - ref["A"]) <= 1e-5 * ref["A"] + 1e-6, ("A", qs[3], ref["A"])
+    assert abs(qs[4] - ref["B0"]) <= 1e-5 * float(np.abs(q) @ np.abs(c_k)) + 1e-6, ("B0", qs[4], ref["B0"])
+    assert abs(qs[0] - ref["ql"]) <= ROT_ATOL, ("q_l", qs[0], ref["ql"])
+    assert abs(qs[5] - ref["qr"]) <= ROT_ATOL, ("q_r", qs[5], ref["qr"])
+    assert abs(qs[1] - ref["delta"]) <= 2 * ROT_ATOL / 15 + 2.0 ** -23 * abs(ref["delta"]), ("Delta", qs[1], ref["delta"])
+    assert qs[2] == planes_to_codes(planes).sum(), ("S_u", qs[2])
+    assert qs[6] == 0.0 and qs[7] == 0.0
+    return ref
+
+
+def check_encode_group(codes, kfac, c_k, K, P, c_q, rot=None, alpha=None, c_k_given=False):
+    """Index rows of one (sequence, KV head) against the oracle's Algorithm 1 on
+    the same keys: the centroid (unless it was given), the sign codes (bit-exact
+    given the GPU's rotated values when `rot` is passed; end to end, every
+    flipped bit lies within 1e-5 * ||x|| of zero), f and g to 1e-5 relative.
+    codes [n][D/32] uint32, kfac [n][2], c_k [D], K [n][D] float64; returns the
+    number of flipped bits."""
+    K = np.asarray(K, np.float64)
+    ck = np.asarray(c_k, np.float64)
+    D = K.shape[1]
+    if not c_k_given:
+        assert np.abs(ck - orc.key_centroid(K)).max() <= 1e-5 * (np.abs(K).mean() + 1.0)
+    enc = orc.encode_keys(K, P, c_k=ck, c_q=c_q)
+    kfac = np.asarray(kfac, np.float64)
+    nrm = enc["norm"]
+    if rot is not None:
+        r = np.asarray(rot, np.float64)
+        assert np.array_equal(codes, orc.pack_bits(orc.sign_bits(r)))        # stage-wise exact
+        assert np.all(np.abs(r - enc["R"]) <= 1e-5 * nrm[:, None] + 1e-30)
+    diff = orc.unpack_bits(codes, D) != enc["bits"]
+    assert np.all(np.abs(enc["R"][diff]) <= 1e-5 * np.broadcast_to(nrm[:, None], diff.shape)[diff])
+    assert np.all(np.abs(kfac[:, 0] - enc["f"]) <= 1e-5 * np.abs(enc["f"]) + 1e-6)
+    cq = np.zeros(D) if c_q is None else np.asarray(c_q, np.float64)
+    gscale = np.abs(cq).sum() * np.abs(enc["X"]).max(axis=1)
+    assert np.all(np.abs(kfac[:, 1] - enc["g"]) <= 1e-5 * gscale + 1e-6)
+    if alpha is not None:
+        a = np.asarray(alpha, np.float64)
+        assert np.all(np.abs(a - enc["alpha"]) <= 1e-5 * enc["alpha"] + 1e-7)
+    return int(diff.sum())
+
+
 def score_tolerance(codes, f, g, qcodes, qs, D=128):
     bits = orc.unpack_bits(codes, D)
     ip, pc = orc.int_dot(bits, qcodes)

@@ -8,6 +8,8 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "rbq.h")
+HEADERS = sorted(os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))
+                 if f.endswith(".h"))
 LIB = os.path.join(ROOT, "paper_2606_31519_amd", "librbq.so")
 
 
@@ -20,9 +22,16 @@ def lib():
     return rbq
 
 
-def declared_symbols():
-    text = open(HEADER).read()
+def declared_symbols(headers=None):
+    text = "".join(open(h).read() for h in (headers or HEADERS))
     return sorted(set(re.findall(r"^(?:rbq_status|size_t|const char\*|int32_t)\s+(rbq_\w+)\(", text, re.M)))
+
+
+def test_test_hooks_are_not_in_the_product_header():
+    product = declared_symbols([HEADER])
+    testing = declared_symbols([os.path.join(ROOT, "include", "rbq_testing.h")])
+    assert testing and not set(testing) & set(product)
+    assert all(n.endswith(("_debug", "_ints", "_ints_q8")) for n in testing)
 
 
 def test_header_declares_the_five_calls():
@@ -104,6 +113,11 @@ def test_invalid_arguments_are_rejected_on_the_host(lib):
     assert tp(s=float("inf")) == EINVAL
     assert tp(s=-1.0) == EINVAL
     assert tp(wsb=8) == EINVAL
+    # rows of 2^24 keys or more would overflow the 64-bit fixed-point mass sums
+    big = lambda n: L.rbq_topp_select(1, 1, n, FAKE, 0.9, 0.1, FAKE, FAKE, FAKE, 1 << 40, 0)
+    assert big(1 << 24) == EUNSUP
+    assert big((1 << 31) - 1) == EUNSUP
+    assert L.rbq_topp_select_varlen(1, 1, 1 << 24, FAKE, FAKE, FAKE, 0.1, FAKE, FAKE, FAKE, 1 << 40, 0) == EUNSUP
     # decode: window above the limit, window without buffers, G not a power of two, n > cap
     dec = lambda **k: L.rbq_sparse_decode(1, k.get("Hq", 8), 4 if k.get("Hq", 8) % 4 == 0 else 3, 128, FAKE, FAKE,
                                           FAKE, 1, k.get("cap", 100), k.get("n", 100), FAKE, FAKE,

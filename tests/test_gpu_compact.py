@@ -224,6 +224,7 @@ def test_compact_config3_full_size_sampled(R, pipeline):
             off = f16[0, hk, :n + w] != orc.compact_factor(enc["f"])
             assert np.all(_near_binary16_tie(enc["f"])[off])
             for h in (hk * G, hk * G + 3):
+                pu.check_qscal(qs[0, h], planes[0, h], wl.q[0, h], wl.P, None, ck[0, hk])   # (built without c_q)
                 fac = np.stack([f16[0, hk, :n], np.zeros(n)], axis=1)
                 pu.check_scores(S[0, h, :n], codes[0, hk, :n], fac, planes[0, h], qs[0, h])
                 got = sel[0, h, :cnt[0, h]]

@@ -95,8 +95,7 @@ def test_d64_quantize_and_score(R, pipeline, B, Hq, Hkv, n):
             assert np.array_equal(qc, z["codes"])
             assert qs[b, h, 0] == np.float32(z["ql"]) and qs[b, h, 1] == np.float32(z["delta"])
             assert qs[b, h, 2] == z["s_u"]
-            ref = orc.quantize_query(wl.q[b, h], wl.P, wl.c_q[b, h // G], _np(st.c_k[b, h // G]).astype(np.float64))
-            assert abs(qs[b, h, 3] - ref["A"]) <= 1e-5 * ref["A"]
+            pu.check_qscal(qs[b, h], planes[b, h], wl.q[b, h], wl.P, wl.c_q[b, h // G], _np(st.c_k[b, h // G]), D=D)
             bits = orc.unpack_bits(codes[b, h // G, :n], D)
             ip_or, pc_or = orc.int_dot(bits, qc)
             assert np.array_equal(_np(ip)[b, h], ip_or) and np.array_equal(_np(pc)[b, h // G], pc_or)
@@ -299,6 +298,7 @@ def test_d64_config3_full_size_sampled(R, pipeline):
             assert np.all(np.abs(enc["R"][diff]) <= 1e-5 * np.broadcast_to(enc["norm"][:, None], diff.shape)[diff])
             assert np.all(np.abs(kfac[0, hk, :n + w, 0] - enc["f"]) <= 1e-5 * np.abs(enc["f"]) + 1e-6)
             for h in (hk * G, hk * G + 3):
+                pu.check_qscal(qs[0, h], planes[0, h], wl.q[0, h], wl.P, wl.c_q[0, hk], ck[0, hk], D=D)
                 pu.check_scores(S[0, h, :n], codes[0, hk, :n], kfac[0, hk, :n].astype(np.float64), planes[0, h],
                                 qs[0, h], D=D)
                 got = sel[0, h, :cnt[0, h]]

@@ -1,7 +1,8 @@
 """One sequence near the path's size limits: 4,193,792 indexed keys of one KV
 head (4 query heads) plus a 512-row window, bf16, through rbq_decode_step.
-The selection then spans 1024 sub-chunks of 4096 keys per row, its bitmaps
-65,536 words per row, and the decode's 32-bit byte offsets reach 1 GiB.
+The selection then spans 256 sub-chunks of 16384 keys per row (64 parts of
+4 sub-chunks), its bitmaps 65,536 words per row, and the decode's 32-bit byte
+offsets reach 1 GiB.
 
 Inputs are seeded on the device (Gaussian keys with four outlier channels
 x8, Gaussian values, a scaled Gaussian query). The oracle checks the
@@ -78,7 +79,9 @@ def test_largest_sequence_end_to_end(pipeline):
     planes, qs = pu.u32(st.qplanes[0]), st.qscal[0].cpu().numpy()
     out, lse = st.out[0].cpu().numpy(), st.lse[0].cpu().numpy()
     ix = idx[idx < N]
+    P64 = st.P.cpu().numpy().astype(np.float64)
     for h in range(HQ):
+        pu.check_qscal(qs[h], planes[h], q[0, h].double().cpu().numpy(), P64, None, ck)
         pu.check_scores(S[h, ix], codes[idx < N], kfac[idx < N], planes[h], qs[h])
         s_h = sel[h, :cnt[h]]
         res = pu.check_topp(S[h, :N], p, tau, s_h)

@@ -2,13 +2,17 @@
 cache over PCIe through its device address (rbq.MappedHost). The index build,
 the fused decode step (whose sparse attention gathers only the selected and
 window rows), the same step as separate calls and the dense decode must give
-bitwise the results they give with the cache in HBM: the same kernels read the
-same bytes."""
+bitwise the results they give with the cache in HBM (the same kernels read the
+same bytes), and the mapped run is checked against the oracle as well: the
+index, the scores, every head's Top-p set and the sparse and dense attention."""
+import math
+
 import numpy as np
 import pytest
 import torch
 
 from workloads import gen
+import parity_util as pu
 
 pytestmark = pytest.mark.gpu
 
@@ -54,3 +58,24 @@ def test_step_calls_and_dense_decode_with_kv_in_host_memory(env, kv_dtype):
         for h in range(ref.Hq):
             assert np.array_equal(sel[0][b_, h, :cnt[b_, h]], sel[1][b_, h, :cnt[b_, h]])
     assert cnt.min() >= 1
+    # the mapped run against the oracle: index (prefill rows and the flushed window),
+    # scores on the GPU's codes, Top-p sets, sparse and dense attention
+    c_k, codes, kfac, planes, S = outs[1][0], outs[1][1].view(np.uint32), outs[1][2], outs[1][3].view(np.uint32), outs[1][4]
+    qs = st.qscal.cpu().numpy()
+    out, lse, dout, dlse = outs[1][6], outs[1][7], outs[1][8], outs[1][9]
+    n, w, G, tau = wl.n_index, wl.w, wl.G, 1.0 / math.sqrt(wl.D)
+    for b_ in range(wl.B):
+        for hk in range(wl.Hkv):
+            K, V = wl.K_f32(b_, hk).astype(np.float64), wl.V_f32(b_, hk).astype(np.float64)
+            pu.check_encode_group(codes[b_, hk, :n], kfac[b_, hk, :n], c_k[b_, hk], K[:n], wl.P, wl.c_q[b_, hk])
+            pu.check_encode_group(codes[b_, hk, n:n + w], kfac[b_, hk, n:n + w], c_k[b_, hk], K[n:n + w], wl.P,
+                                  wl.c_q[b_, hk], c_k_given=True)
+            for h in range(hk * G, (hk + 1) * G):
+                pu.check_qscal(qs[b_, h], planes[b_, h], wl.q[b_, h], wl.P, wl.c_q[b_, hk], c_k[b_, hk])
+                pu.check_scores(S[b_, h, :n], codes[b_, hk, :n], kfac[b_, hk, :n], planes[b_, h], qs[b_, h])
+                got = sel[1][b_, h, :cnt[b_, h]]
+                pu.check_topp(S[b_, h, :n], 0.9, tau, got)
+                pu.check_attention(out[b_, h], lse[b_, h], wl.q[b_, h], K[:n], V[:n], got, K[n:n + w], V[n:n + w],
+                                   tau)
+                pu.check_attention(dout[b_, h], dlse[b_, h], wl.q[b_, h], K[:n], V[:n], np.arange(n), K[n:n + w],
+                                   V[n:n + w], tau)

@@ -61,30 +61,34 @@ def test_score_integers_bit_exact(R, B, Hkv, G, cap, n):
 
 
 # ---------------------------------------------------------------- query quantisation
-@pytest.mark.parametrize("case", ["plain", "centred", "degenerate"])
-def test_quantize_query_stagewise(R, pipeline, case):
-    w = gen.random_case(2, 8, 2, 64, seed=11, kv_dtype="f32", c_q_scale=0.0 if case == "plain" else 0.7)
+@pytest.mark.parametrize("case,Hq,Hkv", [("plain", 8, 2), ("centred", 8, 2), ("degenerate", 8, 2),
+                                          ("centred", 4, 4), ("centred", 8, 4), ("centred", 64, 8),
+                                          ("centred", 16, 1)])
+def test_quantize_query_stagewise(R, pipeline, case, Hq, Hkv):
+    """Every query head's planes and constants against the oracle, at group
+    sizes 1 to 16 with a non-zero query centroid per KV group: head h reads
+    c_q and c_k of KV group h / G."""
+    w = gen.random_case(2, Hq, Hkv, 64, seed=11, kv_dtype="f32", c_q_scale=0.0 if case == "plain" else 0.7)
     if case == "degenerate":
         w.q[0, 0] = w.c_q[0, 0]          # q == c_q: A = 0
         w.q[1, 3] = 0.0
+    G = Hq // Hkv
     st = pipeline.DecodeState.from_workload(w)
-    st.c_k.copy_(torch.randn(2, 2, 128, generator=torch.Generator().manual_seed(1)).cuda())
-    qrot = torch.empty(2, 8, 128, device="cuda")
+    st.c_k.copy_(torch.randn(2, Hkv, 128, generator=torch.Generator().manual_seed(1)).cuda())
+    qrot = torch.empty(2, Hq, 128, device="cuda")
     st.quantize(qrot_out=qrot)
     torch.cuda.synchronize()
     planes = pu.u32(st.qplanes)
     qs, qr, ck = _np(st.qscal), _np(qrot), _np(st.c_k)
     for b in range(2):
-        for h in range(8):
-            hk = h // 4
+        for h in range(Hq):
+            hk = h // G
             z = orc.uniform_quantize(qr[b, h], dtype=np.float32)      # the decision in fp32, from the GPU's q'
             assert np.array_equal(pu.planes_to_codes(planes[b, h]), z["codes"])
             assert qs[b, h, 0] == np.float32(z["ql"]) and qs[b, h, 1] == np.float32(z["delta"])
             assert qs[b, h, 2] == z["s_u"]
-            ref = orc.quantize_query(w.q[b, h], w.P, w.c_q[b, hk], ck[b, hk])
-            assert abs(qs[b, h, 3] - ref["A"]) <= 1e-5 * ref["A"] + 1e-6
-            assert abs(qs[b, h, 4] - ref["B0"]) <= 1e-5 * (np.abs(w.q[b, h]) @ np.abs(ck[b, hk])) + 1e-6
-            assert np.abs(qr[b, h] - ref["qrot"]).max() <= 1e-5
+            ref = pu.check_qscal(qs[b, h], planes[b, h], w.q[b, h], w.P, w.c_q[b, hk], ck[b, hk])
+            assert np.abs(qr[b, h] - ref["qrot"]).max() <= pu.ROT_ATOL
             # end to end the codes may differ only where the oracle's value sits on a rounding edge
             t = (ref["qrot"] - ref["ql"]) / ref["delta"] if ref["delta"] > 0 else np.zeros(128)
             off = np.nonzero(pu.planes_to_codes(planes[b, h]) != ref["codes"])[0]
@@ -136,28 +140,10 @@ def test_quantize_query_bits_and_scores(R, pipeline, bits):
 
 # ---------------------------------------------------------------- index construction
 def _check_encode_group(st, w, b, hk, n, rot, alpha, c_k_given=None):
-    K = w.K_f32(b, hk, slice(0, n)).astype(np.float64)
-    ck_gpu = _np(st.c_k[b, hk]).astype(np.float64)
-    if c_k_given is None:
-        ck_ref = orc.key_centroid(K)
-        assert np.abs(ck_gpu - ck_ref).max() <= 1e-5 * (np.abs(K).mean() + 1.0)
-    enc = orc.encode_keys(K, w.P, c_k=ck_gpu, c_q=w.c_q[b, hk])
-    codes = pu.u32(st.codes[b, hk, :n])
-    kfac = _np(st.kfac[b, hk, :n]).astype(np.float64)
-    nrm = enc["norm"]
-    if rot is not None:
-        r = _np(rot[b, hk]).astype(np.float64)
-        assert np.array_equal(codes, orc.pack_bits(orc.sign_bits(r)))        # stage-wise exact
-        assert np.all(np.abs(r - enc["R"]) <= 1e-5 * nrm[:, None] + 1e-30)
-    diff = orc.unpack_bits(codes, 128) != enc["bits"]
-    assert np.all(np.abs(enc["R"][diff]) <= 1e-5 * np.broadcast_to(nrm[:, None], diff.shape)[diff])
-    assert np.all(np.abs(kfac[:, 0] - enc["f"]) <= 1e-5 * np.abs(enc["f"]) + 1e-6)
-    gscale = np.abs(w.c_q[b, hk]).sum() * np.abs(enc["X"]).max(axis=1)
-    assert np.all(np.abs(kfac[:, 1] - enc["g"]) <= 1e-5 * gscale + 1e-6)
-    if alpha is not None:
-        a = _np(alpha[b, hk]).astype(np.float64)
-        assert np.all(np.abs(a - enc["alpha"]) <= 1e-5 * enc["alpha"] + 1e-7)
-    return int(diff.sum())
+    return pu.check_encode_group(pu.u32(st.codes[b, hk, :n]), _np(st.kfac[b, hk, :n]), _np(st.c_k[b, hk]),
+                                 w.K_f32(b, hk, slice(0, n)), w.P, w.c_q[b, hk],
+                                 rot=None if rot is None else _np(rot[b, hk]),
+                                 alpha=None if alpha is None else _np(alpha[b, hk]), c_k_given=c_k_given is not None)
 
 
 @pytest.mark.parametrize("kv_dtype,n", [("bf16", 1000), ("f32", 257), ("bf16", 1), ("f32", 128)])
@@ -276,6 +262,38 @@ def test_topp_large_crossing_bin(R):
             pu.check_topp(S[r].astype(np.float32), p, 1.0, sel[r, :cnt[r]])
 
 
+def test_topp_rows_past_a_million_keys(R):
+    """Rows of more than 64 sub-chunks of 16384 keys: each selection block takes
+    several consecutive sub-chunks (the multi-sub-chunk kernels), with a row
+    that ends inside a block's span, one with a dense tie at the boundary, and
+    one whose first-level crossing bin holds more keys than the candidate
+    buffers (the exact full-row fallback)."""
+    n = 1_100_001
+    rng = np.random.default_rng(9)
+    S = np.stack([rng.standard_normal(n) * 5.0,
+                  np.where(rng.random(n) < 0.02, 25.0, 0.0) + rng.standard_normal(n),
+                  np.round(rng.standard_normal(n) * 2.0) / 4.0])
+    for p in (0.5, 0.95):
+        sel, cnt = _topp_rows(R, S, p, 1 / math.sqrt(128) * 8)
+        for r in range(S.shape[0]):
+            pu.check_topp(S[r].astype(np.float32), p, 1 / math.sqrt(128) * 8, sel[r, :cnt[r]])
+
+
+def test_topp_many_candidates_without_overflow(R):
+    """A row whose first-level crossing bin holds more candidates than the final
+    pass keeps in LDS, although no single part exceeds its candidate buffer
+    (the fallback taken for the row as a whole), beside an ordinary row."""
+    n = 131072
+    rng = np.random.default_rng(10)
+    band = 3.0 + rng.random(n) * 1e-3                     # 20 % of the keys in one narrow band
+    S = np.stack([np.where(rng.random(n) < 0.2, band, rng.standard_normal(n) - 4.0),
+                  rng.standard_normal(n) * 3.0])
+    for p in (0.3, 0.9):
+        sel, cnt = _topp_rows(R, S, p, 1.0)
+        for r in range(S.shape[0]):
+            pu.check_topp(S[r].astype(np.float32), p, 1.0, sel[r, :cnt[r]])
+
+
 # ---------------------------------------------------------------- attention
 def _rand_sel(rng, n, frac, Hq):
     out = []
@@ -342,7 +360,7 @@ def _end_to_end(R, pipeline, wl, p, groups, rows_per_group=None, flush=False):
         _check_encode_group(st, wl, b, hk, n, None, None)
         heads = range(hk * G, (hk + 1) * G) if rows_per_group is None else [hk * G + g for g in rows_per_group]
         for h in heads:
-            ref = orc.quantize_query(wl.q[b, h], wl.P, wl.c_q[b, hk], ck[b, hk])
+            ref = pu.check_qscal(qs[b, h], planes[b, h], wl.q[b, h], wl.P, wl.c_q[b, hk], ck[b, hk])
             qc = pu.planes_to_codes(planes[b, h])
             t = (ref["qrot"] - ref["ql"]) / ref["delta"]
             off = np.nonzero(qc != ref["codes"])[0]

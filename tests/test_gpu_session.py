@@ -87,3 +87,48 @@ def test_session_grows_the_index_through_lazy_flushes(pipeline, D, compact):
                 pu.check_attention(out[0, h], lse[0, h], _np(q)[0, h].astype(np.float64), Kf[hk, :n], Vf[hk, :n],
                                    got, Kf[hk, n:n + w], Vf[hk, n:n + w], tau)
     assert flushes == 3 and ses.n == n0 + 3 * window
+
+
+def test_session_steps_after_the_last_flush_with_a_partial_window(pipeline):
+    """A capacity that is not the prefill plus a whole number of windows: the
+    third flush takes the index to 3096 keys, past cap - window = 3068, and the
+    steps after it run with that index and a window that can only grow to the
+    4 rows left. The session's buffers must hold every index size it reaches;
+    the last steps are checked against the oracle."""
+    B, Hq, Hkv, D = 1, 8, 2, 128
+    n0, window, cap = 3000, 32, 3100
+    wl = gen.random_case(B, Hq, Hkv, cap, D=D, seed=72, kv_dtype="bf16", q_scale=5.0)
+    K = pipeline.to_device_kv(wl.K, wl.kv_dtype, "cuda")
+    V = pipeline.to_device_kv(wl.V, wl.kv_dtype, "cuda")
+    P = torch.from_numpy(np.ascontiguousarray(wl.P)).cuda()
+    K_new, V_new = K[:, :, n0:].clone(), V[:, :, n0:].clone()
+    K[:, :, n0:] = 0
+    V[:, :, n0:] = 0
+    ses = pipeline.DecodeSession(B, Hq, Hkv, D, cap, n0, window, K, V, P)
+    assert ses.n_max == 3096 and ses.state.scores.numel() >= B * Hq * 3096
+    rng = np.random.default_rng(4)
+    tau = 1.0 / math.sqrt(D)
+    G = Hq // Hkv
+    Kf = np.stack([wl.K_f32(0, hk) for hk in range(Hkv)]).astype(np.float64)
+    Vf = np.stack([wl.V_f32(0, hk) for hk in range(Hkv)]).astype(np.float64)
+    for t in range(cap - n0):
+        ses.append(K_new[:, :, t], V_new[:, :, t])
+        q = torch.from_numpy((5.0 * rng.standard_normal((B, Hq, D))).astype(np.float32)).cuda()
+        n, w = ses.n, ses.w
+        ses.step(q, 0.9)
+        torch.cuda.synchronize()
+        if n < 3096:
+            continue
+        S = _np(ses.state.scores).reshape(-1)[:B * Hq * n].reshape(B, Hq, n)
+        cnt = _np(ses.state.sel_count)
+        sel = _np(ses.state.sel_idx).reshape(-1)[:B * Hq * n].reshape(B, Hq, n)
+        out, lse = _np(ses.state.out), _np(ses.state.lse)
+        for h in range(Hq):
+            hk = h // G
+            got = sel[0, h, :cnt[0, h]]
+            pu.check_topp(S[0, h], 0.9, tau, got)
+            pu.check_attention(out[0, h], lse[0, h], _np(q)[0, h].astype(np.float64), Kf[hk, :n], Vf[hk, :n], got,
+                               Kf[hk, n:n + w], Vf[hk, n:n + w], tau)
+    assert ses.n == 3096 and ses.w == 4
+    with pytest.raises(RuntimeError):
+        ses.append(K_new[:, :, 0], V_new[:, :, 0])   # the cache is full

@@ -8,6 +8,7 @@ import pytest
 import torch
 
 from workloads import gen
+import parity_util as pu
 
 pytestmark = pytest.mark.gpu
 
@@ -107,7 +108,8 @@ def test_fused_step_graph_replays(pipeline):
 def test_index_build_beside_prefill_attention(pipeline):
     """The prefill index build on a second stream, started together with a
     causal attention over the same context (as bench.py times it), writes the
-    same centroid, codes and factors as a build alone."""
+    same centroid, codes and factors as a build alone, and those match the
+    oracle's encoding of the same keys."""
     from torch.nn.attention import SDPBackend, sdpa_kernel
     case = (1, 8, 2, 4096, 0, "bf16", 0.9, False, 8)
     ref = _state(pipeline, case)
@@ -128,3 +130,10 @@ def test_index_build_beside_prefill_attention(pipeline):
     torch.cuda.synchronize()
     for a, b in zip(want, (st.c_k, st.codes, st.kfac)):
         assert np.array_equal(a.view(np.uint8), b.cpu().numpy().view(np.uint8))
+    # and the build itself against the oracle's Algorithm 1 on the same keys
+    B, Hq, Hkv, n, w, dt, p, flush, seed = case
+    wl = gen.random_case(B, Hq, Hkv, n, seed=seed, kv_dtype=dt, w=w, c_q_scale=0.5)
+    codes, kfac, ck = st.codes.cpu().numpy().view(np.uint32), st.kfac.cpu().numpy(), st.c_k.cpu().numpy()
+    for hk in range(Hkv):
+        pu.check_encode_group(codes[0, hk, :n], kfac[0, hk, :n], ck[0, hk], wl.K_f32(0, hk, slice(0, n)), wl.P,
+                              wl.c_q[0, hk])
