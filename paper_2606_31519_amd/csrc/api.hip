@@ -45,7 +45,7 @@ rbq_status decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
     s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, 4, head_dim);
   if (s != RBQ_OK) return s;
   s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   nullptr, kfac16, 4, head_dim);
+                   nullptr, kfac16, 4, head_dim, kPlaceGroup);
   if (s != RBQ_OK) return s;
   s = launch_topp(int32_t(rows), n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, stream, heads_q / heads_kv,
                   sw.masks);
@@ -291,7 +291,7 @@ rbq_status decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, 
     s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, 4, head_dim);
   if (s != RBQ_OK) return s;
   s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   seq_n, kfac16, 4, head_dim);
+                   seq_n, kfac16, 4, head_dim, kPlaceGroup);
   if (s != RBQ_OK) return s;
   s = launch_topp(int32_t(rows), n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, stream, heads_q / heads_kv,
                   sw.masks, seq_n, seq_p, heads_q);

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "rbq_internal.h"
+
 namespace rbq {
 
 constexpr int kWave = 64;
@@ -71,6 +73,67 @@ __device__ __forceinline__ uint32_t score_key(float s) {
 }
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// The tile (KV group g, Top-p part j) and slot s of workgroup p of a launch
+// placed by tile_place() with `slots` workgroups per tile; false for a
+// workgroup past the last tile.
+__device__ __forceinline__ bool tile_of(const TilePlace& t, int slots, int p, int& g, int& j, int& s) {
+  if (t.mode == kPlaceStream) {
+    const int q = p / slots;
+    s = p % slots;
+    g = q / t.parts;
+    j = q % t.parts;
+    return g < t.groups;
+  }
+  const int x = p % kXcds, r = p / kXcds;
+  s = r % slots;
+  const int k = r / slots;   // the tile's rank on its XCD
+  if (t.spread == 1) {
+    g = (k / t.parts) * kXcds + x;
+    j = k % t.parts;
+    return g < t.groups;
+  }
+  g = x % t.groups;
+  const int u = x / t.groups;   // which of the group's XCDs
+  j = k * t.spread + u;
+  return u < t.spread && j < t.parts;
+}
+
+// Wave reductions on the DPP / swizzle paths (no LDS permutes): sums of 64-bit
+// integers and maxima over all 64 lanes, the result in every lane.
+#define RBQ_DPP_U32(v, ctrl) uint32_t(__builtin_amdgcn_update_dpp(0, int(v), (ctrl), 0xF, 0xF, false))
+#define RBQ_DPP_U64(v, ctrl) ((uint64_t(RBQ_DPP_U32(uint32_t((v) >> 32), ctrl)) << 32) | RBQ_DPP_U32(uint32_t(v), ctrl))
+__device__ __forceinline__ uint64_t swap16_u64(uint64_t v) {
+  const uint32_t lo = uint32_t(__builtin_amdgcn_ds_swizzle(int(uint32_t(v)), 0x401F));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_ds_swizzle(int(uint32_t(v >> 32)), 0x401F));
+  return (uint64_t(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l) {
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), l));
+  const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v >> 32)), l));
+  return (uint64_t(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+  v += RBQ_DPP_U64(v, 0xB1);    // quad_perm [1,0,3,2]
+  v += RBQ_DPP_U64(v, 0x4E);    // quad_perm [2,3,0,1]
+  v += RBQ_DPP_U64(v, 0x141);   // row_half_mirror
+  v += RBQ_DPP_U64(v, 0x140);   // row_mirror: each 16-lane row holds its sum
+  v += swap16_u64(v);           // each 32-lane half holds its sum
+  return readlane_u64(v, 0) + readlane_u64(v, 32);
+}
+__device__ __forceinline__ float wave_max_dpp(float v) {
+  v = max32(v);
+  return fmaxf(__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0)),
+               __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32)));
+}
+__device__ __forceinline__ int wave_sum_i32(int v) {
+  v += int(RBQ_DPP_U32(uint32_t(v), 0xB1));
+  v += int(RBQ_DPP_U32(uint32_t(v), 0x4E));
+  v += int(RBQ_DPP_U32(uint32_t(v), 0x141));
+  v += int(RBQ_DPP_U32(uint32_t(v), 0x140));
+  v += __builtin_amdgcn_ds_swizzle(v, 0x401F);
+  return __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 32);
+}
 
 // Raw buffer resource over `bytes` bytes from `base` (gfx9 descriptor word 3):
 // loads through it are range-checked by the hardware and return 0 past the end.

@@ -48,10 +48,10 @@ constexpr int kSelCandCap = 4096;                      // candidate keys one par
 constexpr int kSelCandLds = 16384;                     // candidate keys of a row the final pass holds in LDS
 constexpr int32_t kToppMaxKeys = int32_t(1) << 24;     // keys per row the fixed-point sums hold
 // per-part records (bytes): the first pass's histogram (block max, 64 coarse
-// sums, the directory of non-empty coarse bins, their 64-bin sections) and the
-// second pass's sums and candidate keys
-constexpr size_t kSelP1Coarse = 16, kSelP1Dir = 16 + 8 * kSelCoarse, kSelP1Sec = 1024;
-constexpr size_t kSelPart1Bytes = kSelP1Sec + size_t(8) * kSelCoarse * 64;
+// sums, the directory of non-empty coarse bins, their 64-bin sections, in
+// fp32) and the second pass's sums and candidate keys
+constexpr size_t kSelP1Coarse = 16, kSelP1Dir = 16 + 4 * kSelCoarse, kSelP1Sec = 1024;
+constexpr size_t kSelPart1Bytes = kSelP1Sec + size_t(4) * kSelCoarse * 64;
 constexpr size_t kSelP2Cand = 64;
 constexpr size_t kSelPart2Bytes = kSelP2Cand + size_t(4) * kSelCandCap;
 constexpr int kSelStateWords = 4;                      // per row: row max (bits), first-level crossing bin
@@ -103,14 +103,43 @@ int score_keys_per_lane(int32_t batch, int32_t heads_kv, int32_t n);
 int topp_mask_words(int32_t n);   // 64-key words of a row's selection bitmap
 
 // Placement of blocks on the 8 XCDs (each with its own L2). A launch hands
-// workgroup id p to XCD p % 8. Every kernel that touches the scores of
-// (KV group g, part j) -- the score scan that writes them and the Top-p passes
-// that read them -- places that work on XCD (g * parts + j) % 8, so the
-// passes find the scores in their own L2. Work item (tile q, slot s) of a
-// launch with `slots` blocks per tile gets workgroup id
-// ((q / 8) * slots + s) * 8 + q % 8; the grid is xcd_grid(tiles, slots).
+// workgroup id p to XCD p % 8. The work of a launch is a set of tiles (KV group
+// g, Top-p part j) of `slots` workgroups each, placed in one of two ways:
+//   kPlaceStream: tile after tile in workgroup order, so the whole GPU streams
+//     neighbouring keys at any moment (the fastest order for a scan alone);
+//   kPlaceGroup: every kernel that touches the scores of a tile -- the scan
+//     that writes them and the Top-p passes that read them and each other's
+//     per-part records -- runs that tile on the same XCD: all the parts of a
+//     group on XCD g % 8 when there are at least 8 groups, otherwise each group
+//     spread over 8 / groups XCDs (part j on the (j % spread)-th of them) so
+//     that every XCD still gets work. The passes then read the scores and a
+//     row's records from their own L2.
+// tile_grid() is the launch size.
 constexpr int kXcds = 8;
-inline int64_t xcd_grid(int64_t tiles, int64_t slots) { return (tiles + kXcds - 1) / kXcds * kXcds * slots; }
+enum TileMode : int32_t { kPlaceStream = 0, kPlaceGroup = 1 };
+struct TilePlace {
+  int32_t groups;    // KV groups (B * Hkv; for a call without groups, its rows)
+  int32_t parts;     // Top-p parts per row
+  int32_t spread;    // XCDs per group (kPlaceGroup)
+  int32_t per_xcd;   // tiles per XCD (kPlaceGroup), all tiles (kPlaceStream)
+  int32_t mode;
+};
+inline TilePlace tile_place(int32_t groups, int32_t parts, int32_t mode) {
+  TilePlace t;
+  t.groups = groups;
+  t.parts = parts;
+  t.mode = mode;
+  t.spread = groups >= kXcds ? 1 : kXcds / groups;
+  if (mode == kPlaceStream)
+    t.per_xcd = groups * parts;
+  else
+    t.per_xcd =
+        t.spread == 1 ? int32_t((int64_t(groups) + kXcds - 1) / kXcds * parts) : (parts + t.spread - 1) / t.spread;
+  return t;
+}
+inline int64_t tile_grid(const TilePlace& t, int64_t slots) {
+  return t.mode == kPlaceStream ? int64_t(t.per_xcd) * slots : int64_t(t.per_xcd) * slots * kXcds;
+}
 
 // Fused decode step: the workspaces of its stages side by side.
 struct StepWorkspace {
@@ -152,16 +181,18 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
                                  const int32_t* seq_off = nullptr, const int32_t* seq_cnt = nullptr,
                                  int32_t off_max = 0, uint16_t* kfac16 = nullptr, int32_t head_dim = kHeadDim);
 // seq_n (ragged batches): [B] indexed keys per sequence, clamped to [0, n]; n is the row stride
+// place: kPlaceGroup when the Top-p passes of the same step read the scores
+// next (their blocks then find them in their own L2), kPlaceStream otherwise
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream,
                         const int32_t* seq_n = nullptr, const uint16_t* kfac16 = nullptr, int32_t planes = 4,
-                        int32_t head_dim = kHeadDim);
+                        int32_t head_dim = kHeadDim, int32_t place = kPlaceStream);
 // (kfac16: the compact index's fp16 factors [B][Hkv][cap], read instead of kfac when non-NULL; g = 0.
 //  planes: query bit-planes per head, 4 or 8 (8: B_q up to 8; uniform, unfused calls only))
 // group: rows per KV group (heads_q / heads_kv when the scores come from
-// launch_score of the same step, 1 when unknown): only the placement of the
-// blocks on the XCDs depends on it. masks: optional [rows][topp_mask_words(n)]
+// launch_score of the same step with kPlaceGroup, 1 when unknown): only the
+// placement of the blocks on the XCDs depends on it. masks: optional [rows][topp_mask_words(n)]
 // selection bitmaps (bit i of word k = key 64 k + i); seq_n / seq_p (ragged
 // batches): [B] keys and p per sequence, row r of sequence r / heads_q
 rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,

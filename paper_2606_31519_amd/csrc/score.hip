@@ -18,14 +18,14 @@
 //   S = A f X + B0 + g,
 // which avoids the cancellation between 2 Delta ip and Delta S_u in fp32. The
 // kernel streams codes + factors once (24 B per KV key, non-temporal) and
-// writes 4 B per (key, head). Blocks that lie wholly inside [0, n) take a path
+// writes 4 B per (key, head) with non-temporal stores. Blocks that lie wholly inside [0, n) take a path
 // without per-key guards. The scan is HBM-bound at G = 4 and at G = 8.
 // Placement: the blocks of (KV group g, Top-p part j) -- the keys
-// [j * span, (j + 1) * span), span = the Top-p part length -- all run on XCD
-// (g * parts + j) % 8, where the Top-p passes that read these scores run too,
-// so those passes find them in that XCD's L2.
+// [j * span, (j + 1) * span), span = the Top-p part length -- run on the XCD
+// tile_place() gives that tile, where the Top-p passes that read these scores
+// run too, so those passes find them in that XCD's L2.
 // Ragged batches (RAGGED, seq_n != NULL): sequence b has seq_n[b] indexed keys
-// (clamped to [0, n]); n is the row stride of the scores and bounds the grid.
+// (clamped to [0, n]; n is the row stride of the scores and bounds the grid).
 // A block reads its sequence's count first and leaves at once when it lies
 // past it; loads are clamped to the sequence's last key.
 #include "rbq_device.h"
@@ -79,11 +79,10 @@ __device__ __forceinline__ uint32_t query_dot(const Spread& e, const uint32_t* q
   return binary_int4_dot(e, qn);
 }
 
-// The launch: tiles q = g * parts + j (KV group g, Top-p part j), `slots`
-// blocks of kScoreThreads * KPT keys per tile, tile q on XCD q % 8.
+// The launch: tiles (KV group, Top-p part) placed by tile_place(), `slots`
+// blocks of kScoreThreads * KPT keys per tile.
 struct ScoreGrid {
-  int tiles;   // B * Hkv * parts
-  int parts;   // Top-p parts per row
+  TilePlace tp;
   int slots;   // score blocks per part
 };
 
@@ -100,11 +99,9 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     ScoreGrid sg, const int32_t* __restrict__ seq_n) {
   constexpr int QW = 4 * QB;                 // nibble words per head
   __shared__ uint32_t qn_s[kMaxGroup][QW];
-  const int x = blockIdx.x % kXcds, r = blockIdx.x / kXcds;
-  const int q = (r / sg.slots) * kXcds + x;  // tile: (KV group, Top-p part)
-  if (q >= sg.tiles) return;                 // block-uniform: past the last tile
-  const int bh = q / sg.parts;               // b * Hkv + kv head
-  const int blk = (q % sg.parts) * sg.slots + r % sg.slots;   // block of the row
+  int bh, part, slot;                        // KV group b * Hkv + kv head, Top-p part, block in the part
+  if (!tile_of(sg.tp, sg.slots, int(blockIdx.x), bh, part, slot)) return;   // block-uniform: past the last tile
+  const int blk = part * sg.slots + slot;    // block of the row
   const int b = bh / Hkv;
   const int hk = bh - b * Hkv;
   const int64_t kbase = int64_t(bh) * cap;
@@ -179,7 +176,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       for (int u = 0; u < KPT; ++u) {
         const int ip = int(query_dot<QB>(e[u], qn));
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
-        out[i0 + u * kScoreThreads] = assemble(u, y, B0);
+        __builtin_nontemporal_store(assemble(u, y, B0), out + i0 + u * kScoreThreads);
       }
     }
     return;
@@ -204,7 +201,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         const float sc = assemble(u, y, B0);
-        if (i < nb) out[i] = sc;
+        if (i < nb) __builtin_nontemporal_store(sc, out + i);
       }
     }
   }
@@ -253,16 +250,15 @@ rbq_status launch_score_d(int kpt, dim3 grid, hipStream_t stream, const uint32_t
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, const int32_t* seq_n,
-                        const uint16_t* kfac16, int32_t planes, int32_t head_dim) {
+                        const uint16_t* kfac16, int32_t planes, int32_t head_dim, int32_t place) {
   if (n == 0) return RBQ_OK;
   const int G = heads_q / heads_kv;
   const int kpt = score_keys_per_lane(batch, heads_kv, n);
   const ToppPlan pl = topp_plan(n);
   ScoreGrid sg;
-  sg.parts = pl.parts;
-  sg.tiles = batch * heads_kv * pl.parts;
+  sg.tp = tile_place(batch * heads_kv, pl.parts, place);
   sg.slots = pl.spb * kSelSub / (kScoreThreads * kpt);
-  const int64_t blocks = xcd_grid(sg.tiles, sg.slots);
+  const int64_t blocks = tile_grid(sg.tp, sg.slots);
   if (blocks * kScoreThreads >= (int64_t(1) << 32)) return RBQ_EUNSUPPORTED;   // beyond one launch's grid
   const dim3 grid{unsigned(blocks)};
   if (head_dim == 64)

@@ -18,9 +18,11 @@
 // Three passes over a row, one block of 1024 threads per (row, part), a part
 // being spb consecutive sub-chunks of 16384 keys:
 //   1 hist   per part: its own maximum m_j and a 4096-bin histogram of the
-//            first level (key bits 31..20) with masses relative to m_j, stored
-//            as 64 coarse sums plus the 64-bin sections of the non-empty
-//            coarse bins (plain stores: no atomics outside LDS).
+//            first level (key bits 31..20) with masses relative to m_j,
+//            stored in fp32 as 64 coarse sums plus the 64-bin sections of the
+//            non-empty coarse bins (plain stores: no atomics outside LDS).
+//            It is only an estimate: nothing downstream depends on its
+//            rounding except which bin the next pass gathers.
 //   2 cand   every block of a row merges the row's part histograms, each
 //            rescaled by exp2((m_j - M) ...) in fp64, and takes the first-level
 //            bin b1 where the mass from the top crosses p of the total (an
@@ -38,7 +40,8 @@
 //            ascending order at the offset given by the selected counts of the
 //            parts before it (above-b1 counts plus candidates >= K*).
 // Every pass reads the row's scores; all three and the score scan that wrote
-// them run the work of (KV group, part) on the same XCD, so the scores are
+// them run the work of (KV group, part) on the same XCD (tile_place), so the
+// scores, and with at least 8 KV groups every per-part record of a row, are
 // read from that XCD's L2.
 //
 // Ragged batches (seq_n / seq_p != NULL): row r of sequence b = r / Hq has
@@ -79,40 +82,6 @@ __device__ __forceinline__ u64 shfl_down_u64(u64 v, int o) {
   const uint32_t hi = __shfl_down(uint32_t(v >> 32), o, kWave);
   return (u64(hi) << 32) | lo;
 }
-__device__ __forceinline__ u64 shfl_u64(u64 v, int src) {
-  const uint32_t lo = __shfl(uint32_t(v), src, kWave);
-  const uint32_t hi = __shfl(uint32_t(v >> 32), src, kWave);
-  return (u64(hi) << 32) | lo;
-}
-__device__ __forceinline__ u64 wave_sum_u64(u64 v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += shfl_down_u64(v, o);
-  return shfl_u64(v, 0);
-}
-
-__device__ __forceinline__ float block_max(float m, float* red) {
-  m = wave_max(m);
-  __syncthreads();
-  if (lane_id() == 0) red[threadIdx.x / kWave] = m;
-  __syncthreads();
-  float r = red[0];
-#pragma unroll
-  for (int w = 1; w < kTW; ++w) r = fmaxf(r, red[w]);
-  return r;
-}
-
-// block-wide sum of one u64 per thread (every thread gets the total)
-__device__ __forceinline__ u64 block_sum_u64(u64 v, u64* red) {
-  v = wave_sum_u64(v);
-  __syncthreads();
-  if (lane_id() == 0) red[threadIdx.x / kWave] = v;
-  __syncthreads();
-  u64 r = 0;
-#pragma unroll
-  for (int w = 0; w < kTW; ++w) r += red[w];
-  return r;
-}
-
 struct Crossing {
   uint32_t bin;
   uint32_t pad;
@@ -125,7 +94,7 @@ struct Crossing {
 // trailing barrier). Requires 1 <= need <= the total: then exactly one thread
 // matches, since the suffix sums grow monotonically from 0 to the total.
 template <int NB>
-__device__ void lds_crossing(const u64* h, u64 need, u64* wtot, Crossing* out) {
+__device__ __forceinline__ void lds_crossing(const u64* h, u64 need, u64* wtot, Crossing* out) {
   constexpr int BPT = NB >= kT ? NB / kT : 1;   // bins per thread
   constexpr int NT = NB / BPT;                  // threads holding bins
   const int t = threadIdx.x, lane = lane_id(), w = t / kWave;
@@ -183,20 +152,100 @@ __device__ __forceinline__ RowSel row_sel(const int32_t* __restrict__ seq_n, con
   return r;
 }
 
-// The (row, part) of this block: tile q = (row / group) * parts + part runs on
-// XCD q % 8, the group's rows of a tile in consecutive slots.
+// The (row, part) of this block: tile (KV group, part), the group's rows in
+// the tile's consecutive slots (group = rows per KV group, 1 when unknown).
 struct SelWork {
   int row, part;
   bool ok;
 };
-__device__ __forceinline__ SelWork sel_work(int parts, int group, int rows) {
-  const int p = blockIdx.x, x = p % kXcds, r = p / kXcds;
-  const int s = r % group, q = (r / group) * kXcds + x;
+__device__ __forceinline__ SelWork sel_work(const TilePlace& tp, int group) {
+  int g, j, s;
   SelWork w;
-  w.ok = q < (rows / group) * parts;
-  w.row = (q / parts) * group + s;
-  w.part = q % parts;
+  w.ok = tile_of(tp, group, int(blockIdx.x), g, j, s);
+  w.row = g * group + s;
+  w.part = j;
   return w;
+}
+
+// Exclusive prefix of one u32 per lane over the wave (row shifts and row
+// broadcasts), and the wave's total.
+__device__ __forceinline__ uint32_t wave_excl_scan_u32(uint32_t v, uint32_t* total) {
+  uint32_t x = v;
+  x += RBQ_DPP_U32(x, 0x111);   // row_shr:1
+  x += RBQ_DPP_U32(x, 0x112);   // row_shr:2
+  x += RBQ_DPP_U32(x, 0x114);   // row_shr:4
+  x += RBQ_DPP_U32(x, 0x118);   // row_shr:8: inclusive within each row of 16
+  x += uint32_t(__builtin_amdgcn_update_dpp(0, int(x), 0x142, 0xA, 0xF, false));   // row_bcast:15 into rows 1, 3
+  x += uint32_t(__builtin_amdgcn_update_dpp(0, int(x), 0x143, 0xC, 0xF, false));   // row_bcast:31 into rows 2, 3
+  *total = uint32_t(__builtin_amdgcn_readlane(int(x), 63));
+  return x - v;
+}
+
+// Crossing search over 4096 u64 bins in LDS by wave 0 alone (call from every
+// thread; valid in *out after the trailing barrier): the coarse sums of 64
+// bins, the coarse crossing, then the crossing among that coarse bin's 64
+// bins. Same result as lds_crossing<4096>. 1 <= need <= the total.
+__device__ __forceinline__ void lds_crossing_4096(const u64* h, u64 need, u64* coarse, Crossing* out) {
+  const int t = threadIdx.x, lane = lane_id();
+  u64 s4 = h[4 * t] + h[4 * t + 1] + h[4 * t + 2] + h[4 * t + 3];
+  s4 += RBQ_DPP_U64(s4, 0xB1);
+  s4 += RBQ_DPP_U64(s4, 0x4E);
+  s4 += RBQ_DPP_U64(s4, 0x141);
+  s4 += RBQ_DPP_U64(s4, 0x140);   // each 16-lane row: the sum of its 64 bins
+  if ((t & 15) == 0) coarse[t >> 4] = s4;
+  __syncthreads();
+  if (t < kWave) {
+    u64 suf = 0;   // coarse bins lane..63 (a short LDS walk; no cross-lane traffic)
+    for (int q = kWave - 1; q >= lane; --q) suf += coarse[q];
+    const u64 above = suf - coarse[lane];
+    const u64 hit = __ballot(above < need && suf >= need);
+    const int c = hit ? __builtin_ctzll(hit) : 0;
+    const u64 need_c = need - readlane_u64(above, c);
+    const u64* f = h + c * kWave;
+    u64 fs = 0;
+    for (int q = kWave - 1; q >= lane; --q) fs += f[q];
+    const u64 fa = fs - f[lane];
+    const u64 fhit = __ballot(fa < need_c && fs >= need_c);
+    const int b = fhit ? __builtin_ctzll(fhit) : 0;
+    if (lane == b) {
+      out->bin = uint32_t(c * kWave + b);
+      out->need = need_c - fa;
+    }
+  }
+  __syncthreads();
+}
+
+// The same over 256 bins (4 per lane of wave 0).
+__device__ __forceinline__ void lds_crossing_256(const u64* h, u64 need, u64* scratch, Crossing* out) {
+  const int t = threadIdx.x, lane = lane_id();
+  if (t < kWave) {
+    const u64 s4 = h[4 * lane] + h[4 * lane + 1] + h[4 * lane + 2] + h[4 * lane + 3];
+    scratch[lane] = s4;
+  }
+  __syncthreads();
+  if (t < kWave) {
+    u64 suf = 0;
+    for (int q = kWave - 1; q >= lane; --q) suf += scratch[q];
+    const u64 above = suf - scratch[lane];
+    const u64 hit = __ballot(above < need && suf >= need);
+    const int l = hit ? __builtin_ctzll(hit) : 0;
+    if (lane == l) {
+      u64 cum = above;
+      uint32_t bin = 4u * l;
+      u64 rest = need - above;
+      for (int k = 3; k >= 0; --k) {   // inside the lane's 4 bins, from the top
+        const u64 v = h[4 * l + k];
+        if (cum < need && cum + v >= need) {
+          bin = uint32_t(4 * l + k);
+          rest = need - cum;
+        }
+        cum += v;
+      }
+      out->bin = bin;
+      out->need = rest;
+    }
+  }
+  __syncthreads();
 }
 
 // the thread's kPT scores of the sub-chunk at `base` (element base + k * kT + tid),
@@ -209,25 +258,28 @@ __device__ __forceinline__ bool in_range(int base, int end, int k) { return base
 
 // ---------------------------------------------------------------- pass 1: part histograms
 template <bool RAGGED, bool MULTI>
-__global__ __launch_bounds__(kT) void sel_hist_kernel(const float* __restrict__ scores, int n, int spb, int parts,
-                                                      int group, int rows, float scale_log2e,
+__global__ __launch_bounds__(kT) void sel_hist_kernel(const float* __restrict__ scores, int n, int spb, TilePlace tp,
+                                                      int group, float scale_log2e,
                                                       unsigned char* __restrict__ part1,
                                                       const int32_t* __restrict__ seq_n,
                                                       const float* __restrict__ seq_p, int hq) {
   __shared__ u64 h[kSelBins];
-  __shared__ u64 cs[kSelCoarse];
+  __shared__ float cs[kSelCoarse];
   __shared__ int dir_s[kSelCoarse];
   __shared__ float red[kTW];
-  const SelWork wk = sel_work(parts, group, rows);
+  const SelWork wk = sel_work(tp, group);
   if (!wk.ok) return;
+  const int parts = tp.parts;
   const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, wk.row, n, 0.5f) : RowSel{n, 0.5f};
   const int k0 = wk.part * spb * kSub;
   if (k0 >= rs.n || (RAGGED && rs.p >= 1.f)) return;   // block-uniform: no histogram needed here
   const int k1 = min(rs.n, k0 + spb * kSub);
   const float* srow = scores + int64_t(wk.row) * n;
+  const int t = threadIdx.x;
   float v[kPT];
   load_sub(srow, k0, k1, v);
-  for (int b = threadIdx.x; b < kSelBins; b += kT) h[b] = 0;
+#pragma unroll
+  for (int k = 0; k < kSelBins / kT; ++k) h[k * kT + t] = 0ull;
   // the part's maximum
   float m = -INFINITY;
   for (int base = k0; base < k1; base += kSub) {
@@ -237,31 +289,42 @@ __global__ __launch_bounds__(kT) void sel_hist_kernel(const float* __restrict__ 
       if (in_range(base, k1, k)) m = fmaxf(m, v[k]);
     if (!MULTI) break;
   }
-  m = block_max(m, red);   // (its barriers also order the clearing of h before the adds)
+  m = wave_max_dpp(m);
+  if (lane_id() == 0) red[t / kWave] = m;
+  __syncthreads();   // (also orders the clearing of h before the adds)
+#pragma unroll
+  for (int w = 0; w < kTW; ++w) m = fmaxf(m, red[w]);
   for (int base = k0; base < k1; base += kSub) {
     if (MULTI) load_sub(srow, base, k1, v);   // (read again: from L2)
 #pragma unroll
     for (int k = 0; k < kPT; ++k) {
+      // (64-bit integer LDS atomics: under the contention of a few popular bins
+      // they run several times faster than fp32 ones)
       const u64 e = fixed_mass(v[k], m, scale_log2e);
       if (in_range(base, k1, k) && e) atomicAdd(&h[score_key(v[k]) >> 20], e);
     }
     if (!MULTI) break;
   }
   __syncthreads();
-  // coarse sums: 4 fine bins per thread, 16 threads per coarse bin
-  const int t = threadIdx.x;
-  u64 s4 = h[4 * t] + h[4 * t + 1] + h[4 * t + 2] + h[4 * t + 3];
-#pragma unroll
-  for (int o = 8; o > 0; o >>= 1) s4 += shfl_down_u64(s4, o);
+  // the record in fp32, in units of the part's top mass: coarse sums of 4 bins per
+  // thread, a 16-lane row per coarse bin
+  constexpr float kUnit = 1.0f / kFix;
+  const float f0 = float(h[4 * t]) * kUnit, f1 = float(h[4 * t + 1]) * kUnit, f2 = float(h[4 * t + 2]) * kUnit,
+              f3 = float(h[4 * t + 3]) * kUnit;
+  float s4 = (f0 + f1) + (f2 + f3);
+  s4 += RBQ_DPP(s4, 0xB1);
+  s4 += RBQ_DPP(s4, 0x4E);
+  s4 += RBQ_DPP(s4, 0x141);
+  s4 += RBQ_DPP(s4, 0x140);
   if ((t & 15) == 0) cs[t >> 4] = s4;
   __syncthreads();
   unsigned char* P1 = part1 + (int64_t(wk.row) * parts + wk.part) * kSelPart1Bytes;
   if (t < kSelCoarse) {   // wave 0: the directory of non-empty coarse bins
-    const bool nz = cs[t] != 0ull;
+    const bool nz = cs[t] > 0.f;
     const u64 bal = __ballot(nz);
     const int d = nz ? __popcll(bal & ((1ull << t) - 1ull)) : -1;
     dir_s[t] = d;
-    reinterpret_cast<u64*>(P1 + kSelP1Coarse)[t] = cs[t];
+    reinterpret_cast<float*>(P1 + kSelP1Coarse)[t] = cs[t];
     reinterpret_cast<int32_t*>(P1 + kSelP1Dir)[t] = d;
     if (t == 0) {
       reinterpret_cast<float*>(P1)[0] = m;
@@ -270,13 +333,7 @@ __global__ __launch_bounds__(kT) void sel_hist_kernel(const float* __restrict__ 
   }
   __syncthreads();
   const int d = dir_s[t >> 4];
-  if (d >= 0) {
-    u64* sec = reinterpret_cast<u64*>(P1 + kSelP1Sec) + d * 64 + (t & 15) * 4;
-    sec[0] = h[4 * t];
-    sec[1] = h[4 * t + 1];
-    sec[2] = h[4 * t + 2];
-    sec[3] = h[4 * t + 3];
-  }
+  if (d >= 0) *reinterpret_cast<f32x4*>(P1 + kSelP1Sec + size_t(4) * (d * 64 + (t & 15) * 4)) = f32x4{f0, f1, f2, f3};
 }
 
 // ---------------------------------------------------------------- pass 2: candidates
@@ -290,114 +347,95 @@ struct P2Head {
 };
 
 template <bool RAGGED, bool MULTI>
-__global__ __launch_bounds__(kT) void sel_cand_kernel(const float* __restrict__ scores, int n, int spb, int parts,
-                                                      int group, int rows, float p, float scale_log2e,
+__global__ __launch_bounds__(kT) void sel_cand_kernel(const float* __restrict__ scores, int n, int spb, TilePlace tp,
+                                                      int group, float p, float scale_log2e,
                                                       const unsigned char* __restrict__ part1,
                                                       unsigned char* __restrict__ part2, uint32_t* __restrict__ state,
                                                       const int32_t* __restrict__ seq_n,
                                                       const float* __restrict__ seq_p, int hq) {
+  __shared__ float val_s[kSelMaxParts][kSelCoarse];   // coarse sums, then the crossing coarse bin's sections
   __shared__ int dir_s[kSelMaxParts][kSelCoarse];
-  __shared__ u64 cval_s[kSelMaxParts][kSelCoarse];
   __shared__ float mp_s[kSelMaxParts];
   __shared__ double fac_s[kSelMaxParts];
-  __shared__ u64 crow[kSelCoarse], frow[kSelCoarse];
-  __shared__ u64 red[kTW];
-  __shared__ uint32_t cand_n, above_n;
+  __shared__ u64 red[kTW][4];
+  __shared__ uint32_t cand_n;
+  __shared__ uint32_t c1_s, b1_s;
+  __shared__ double needc_s;
   __shared__ float M_s;
-  __shared__ uint32_t b1_s;
-  const SelWork wk = sel_work(parts, group, rows);
+  const SelWork wk = sel_work(tp, group);
   if (!wk.ok) return;
+  const int parts = tp.parts;
   const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, wk.row, n, p) : RowSel{n, p};
   const int k0 = wk.part * spb * kSub;
   if (k0 >= rs.n || (RAGGED && rs.p >= 1.f)) return;   // block-uniform
   const int k1 = min(rs.n, k0 + spb * kSub);
   const int parts_r = (rs.n + spb * kSub - 1) / (spb * kSub);   // parts holding keys of this row
   const float* srow = scores + int64_t(wk.row) * n;
+  const int t = threadIdx.x, lane = lane_id(), wave = t / kWave;
   float v[kPT];
   load_sub(srow, k0, k1, v);   // lands while the histograms are merged
-  const int t = threadIdx.x;
   const unsigned char* P1row = part1 + int64_t(wk.row) * parts * kSelPart1Bytes;
-  // merge 1: each part's maximum, coarse sums and directory (parts_r * 64 entries, all loads in flight)
+  // merge 1: each part's maximum, coarse sums and directory (all loads in flight)
   const int nent = parts_r * kSelCoarse;
   for (int e = t; e < nent; e += kT) {
     const int j = e / kSelCoarse, cb = e % kSelCoarse;
     const unsigned char* P1 = P1row + int64_t(j) * kSelPart1Bytes;
     if (cb == 0) mp_s[j] = reinterpret_cast<const float*>(P1)[0];
-    cval_s[j][cb] = reinterpret_cast<const u64*>(P1 + kSelP1Coarse)[cb];
+    val_s[j][cb] = reinterpret_cast<const float*>(P1 + kSelP1Coarse)[cb];
     dir_s[j][cb] = reinterpret_cast<const int32_t*>(P1 + kSelP1Dir)[cb];
   }
-  if (t < kSelCoarse) {
-    crow[t] = 0;
-    frow[t] = 0;
-  }
-  if (t == 0) {
-    cand_n = 0;
-    above_n = 0;
-  }
+  if (t == 0) cand_n = 0;
   __syncthreads();
-  if (t < kWave) {   // wave 0: the row maximum and each part's rescale factor
-    float m = t < parts_r ? mp_s[t] : -INFINITY;
-    m = wave_max(m);
-    if (t < parts_r) fac_s[t] = exp2((double(mp_s[t]) - double(m)) * double(scale_log2e));
-    if (t == 0) M_s = m;
-  }
-  __syncthreads();
-  for (int e = t; e < nent; e += kT) {
-    const int j = e / kSelCoarse, cb = e % kSelCoarse;
-    const u64 cval = cval_s[j][cb];
-    if (cval) atomicAdd(&crow[cb], u64(double(cval) * fac_s[j] + 0.5));
-  }
-  __syncthreads();
-  // the coarse crossing of the estimated target (wave 0, one coarse bin per lane)
-  __shared__ uint32_t c1_s;
-  __shared__ u64 needc_s;
-  if (t < kWave) {
-    const u64 c = crow[t];
-    u64 x = c;
+  if (t < kWave) {   // wave 0: the row maximum, each part's rescale factor, the coarse crossing
+    const float mj = lane < parts_r ? mp_s[lane] : -INFINITY;
+    const float M = wave_max_dpp(mj);
+    const double fac = lane < parts_r ? exp2((double(mj) - double(M)) * double(scale_log2e)) : 0.0;
+    fac_s[lane] = fac;
+    double c = 0.0;   // the row's coarse bin `lane`, summed over the parts in order
+    for (int j = 0; j < parts_r; ++j) c += double(val_s[j][lane]) * __shfl(fac, j, kWave);
+    double x = c;     // inclusive suffix sum (higher lanes hold higher bins)
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
-      const u64 y = shfl_down_u64(x, o);
-      if (t + o < kWave) x += y;
+      const double y = __shfl_down(x, o, kWave);
+      if (lane + o < kWave) x += y;
     }
-    const u64 total = shfl_u64(x, 0);
-    u64 T = u64(ceil(double(rs.p) * double(total)));
-    T = T < 1 ? 1 : (T > total ? total : T);
-    const u64 above = x - c;
+    const double total = __shfl(x, 0, kWave);
+    const double T = double(rs.p) * total;   // (fp32 masses: the target needs no rounding up)
+    const double above = x - c;
     const u64 hit = __ballot(above < T && x >= T);
     const int g = hit ? __builtin_ctzll(hit) : 0;
-    if (t == g) {
+    if (lane == g) {
       c1_s = uint32_t(g);
       needc_s = T - above;
     }
+    if (lane == 0) M_s = M;
   }
   __syncthreads();
   const uint32_t c1 = c1_s;
-  // merge 2: the 64 first-level bins of the coarse crossing bin, from every part
+  // merge 2: the crossing coarse bin's 64 first-level bins, from every part
   for (int e = t; e < nent; e += kT) {
     const int j = e / kSelCoarse, fb = e % kSelCoarse;
     const int d = dir_s[j][c1];
-    if (d >= 0) {
-      const u64 f = reinterpret_cast<const u64*>(P1row + int64_t(j) * kSelPart1Bytes + kSelP1Sec)[d * 64 + fb];
-      if (f) atomicAdd(&frow[fb], u64(double(f) * fac_s[j] + 0.5));
-    }
+    val_s[j][fb] = d >= 0 ? reinterpret_cast<const float*>(P1row + int64_t(j) * kSelPart1Bytes + kSelP1Sec)[d * 64 + fb]
+                          : 0.f;
   }
   __syncthreads();
   if (t < kWave) {
-    const u64 f = frow[t];
-    u64 x = f;
+    double f = 0.0;
+    for (int j = 0; j < parts_r; ++j) f += double(val_s[j][lane]) * fac_s[j];
+    double x = f;
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
-      const u64 y = shfl_down_u64(x, o);
-      if (t + o < kWave) x += y;
+      const double y = __shfl_down(x, o, kWave);
+      if (lane + o < kWave) x += y;
     }
-    const u64 total = shfl_u64(x, 0);
+    const double total = __shfl(x, 0, kWave);
     // (the rescaled sums are estimates: keep the target inside this bin's total)
-    u64 need = needc_s > total ? total : needc_s;
-    need = need < 1 ? 1 : need;
-    const u64 above = x - f;
-    const u64 hit = __ballot(above < need && x >= need);
-    const int g = hit ? __builtin_ctzll(hit) : 0;
-    if (t == g) b1_s = c1 * kSelCoarse + uint32_t(g);
+    const double need = fmax(fmin(needc_s, total), 0.0);
+    const double above = x - f;
+    const u64 hit = __ballot(above < need && x >= need && f > 0.0);
+    const int g = hit ? __builtin_ctzll(hit) : __builtin_ctzll(__ballot(f > 0.0) | (1ull << 63));
+    if (lane == g) b1_s = c1 * kSelCoarse + uint32_t(g);
   }
   __syncthreads();
   const uint32_t b1 = b1_s;
@@ -407,43 +445,59 @@ __global__ __launch_bounds__(kT) void sel_cand_kernel(const float* __restrict__ 
                                                kSelP2Cand);
   u64 tot = 0, am = 0, cm = 0;
   uint32_t ac = 0;
-  const int lane = lane_id();
   for (int base = k0; base < k1; base += kSub) {
     if (MULTI && base > k0) load_sub(srow, base, k1, v);
+    uint64_t bal[kPT];
+    uint32_t wcnt = 0;
 #pragma unroll
     for (int k = 0; k < kPT; ++k) {
       const bool in = in_range(base, k1, k);
-      const uint32_t key = score_key(v[k]);
+      const uint32_t bin = score_key(v[k]) >> 20;
       const u64 e = in ? fixed_mass(v[k], M, scale_log2e) : 0ull;
-      const uint32_t bin = key >> 20;
       tot += e;
       const bool up = in && bin > b1, mid = in && bin == b1;
       am += up ? e : 0ull;
       ac += up ? 1u : 0u;
       cm += mid ? e : 0ull;
-      const u64 bal = __ballot(mid);
-      if (bal) {
-        uint32_t base_pos = 0;
-        if (lane == 0) base_pos = atomicAdd(&cand_n, uint32_t(__popcll(bal)));
-        base_pos = __shfl(base_pos, 0, kWave);
+      bal[k] = __ballot(mid);
+      wcnt += uint32_t(__popcll(bal[k]));
+    }
+    if (wcnt) {   // wave-uniform: one slot reservation per wave, then the keys in order
+      uint32_t pos0 = 0;
+      if (lane == 0) pos0 = atomicAdd(&cand_n, wcnt);
+      pos0 = uint32_t(__builtin_amdgcn_readfirstlane(int(pos0)));
+#pragma unroll
+      for (int k = 0; k < kPT; ++k) {
         const uint32_t pos =
-            base_pos + __builtin_amdgcn_mbcnt_hi(uint32_t(bal >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal), 0u));
-        if (mid && pos < uint32_t(kSelCandCap)) cand[pos] = key;
+            pos0 + __builtin_amdgcn_mbcnt_hi(uint32_t(bal[k] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal[k]), 0u));
+        if (((bal[k] >> lane) & 1u) && pos < uint32_t(kSelCandCap)) cand[pos] = score_key(v[k]);
+        pos0 += uint32_t(__popcll(bal[k]));
       }
     }
     if (!MULTI) break;
   }
-  ac = uint32_t(wave_sum_int(int(ac)));
-  if (lane == 0) atomicAdd(&above_n, ac);
-  tot = block_sum_u64(tot, red);
-  am = block_sum_u64(am, red);
-  cm = block_sum_u64(cm, red);   // (its barriers also complete the LDS counters)
+  tot = wave_sum_u64(tot);
+  am = wave_sum_u64(am);
+  cm = wave_sum_u64(cm);
+  const int acw = wave_sum_i32(int(ac));
+  if (lane == 0) {
+    red[wave][0] = tot;
+    red[wave][1] = am;
+    red[wave][2] = cm;
+    red[wave][3] = u64(acw);
+  }
+  __syncthreads();   // (also completes the candidate count)
   if (t == 0) {
+    u64 r[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int w = 0; w < kTW; ++w)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r[q] += red[w][q];
     P2Head* hd = reinterpret_cast<P2Head*>(part2 + (int64_t(wk.row) * parts + wk.part) * kSelPart2Bytes);
-    hd->total = tot;
-    hd->above_mass = am;
-    hd->cand_mass = cm;
-    hd->above_cnt = above_n;
+    hd->total = r[0];
+    hd->above_mass = r[1];
+    hd->cand_mass = r[2];
+    hd->above_cnt = uint32_t(r[3]);
     hd->cand_cnt = cand_n;
     if (wk.part == 0) {
       state[int64_t(wk.row) * kSelStateWords] = __float_as_uint(M);
@@ -456,7 +510,7 @@ __global__ __launch_bounds__(kT) void sel_cand_kernel(const float* __restrict__ 
 // Exact three-level select over every key of the row (the fallback): K* and,
 // per part, the number of its keys >= K* in cnt[].
 template <bool MULTI>
-__device__ uint32_t exact_select_row(const float* __restrict__ srow, int nr, int spb, int parts_r, float M,
+__device__ __forceinline__ uint32_t exact_select_row(const float* __restrict__ srow, int nr, int spb, int parts_r, float M,
                                      float scale_log2e, u64 T, u64* h, u64* wtot, Crossing* cr, uint32_t* cnt) {
   const int t = threadIdx.x;
   uint32_t prefix = 0;
@@ -505,28 +559,43 @@ __device__ uint32_t exact_select_row(const float* __restrict__ srow, int nr, int
   return kstar;
 }
 
+// the part holding candidate i of a row (pstart: exclusive prefix of the parts' counts)
+__device__ __forceinline__ int cand_part(const int* pstart, int parts_r, int i) {
+  int lo = 0, hi = parts_r - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (pstart[mid] <= i) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+constexpr int kCandPT = kSelCandLds / kT;   // candidates per thread when the LDS buffer is full
+
 template <bool RAGGED, bool MULTI>
-__global__ __launch_bounds__(kT) void sel_final_kernel(const float* __restrict__ scores, int n, int spb, int parts,
-                                                       int group, int rows, float p, float scale_log2e,
+__global__ __launch_bounds__(kT) void sel_final_kernel(const float* __restrict__ scores, int n, int spb, TilePlace tp,
+                                                       int group, float p, float scale_log2e,
                                                        const unsigned char* __restrict__ part2,
                                                        const uint32_t* __restrict__ state,
                                                        int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_count,
                                                        u64* __restrict__ masks, int mask_words,
                                                        const int32_t* __restrict__ seq_n,
                                                        const float* __restrict__ seq_p, int hq) {
-  __shared__ uint32_t ck[kSelCandLds];     // the row's candidate keys
+  __shared__ uint32_t ck[kSelCandLds];     // the row's candidate keys, part by part
   __shared__ u64 h[kSelBins];
+  __shared__ u64 h3[kSelBins3];
   __shared__ u64 wtot[kTW];
+  __shared__ u64 coarse[kWave];
   __shared__ Crossing cr;
   __shared__ P2Head ph[kSelMaxParts];
   __shared__ int pstart[kSelMaxParts + 1];
   __shared__ uint32_t pcnt[kSelMaxParts];
-  __shared__ int kcnt[kPT][kTW];
-  __shared__ int red[kTW];
-  __shared__ int fast_s;
+  __shared__ uint32_t kbase[kPT * kTW];    // exclusive prefix of the (step, wave) counts of a sub-chunk
+  __shared__ int fast_s, off_s, tot_s;
   __shared__ u64 T_s, A_s;
-  const SelWork wk = sel_work(parts, group, rows);
+  const SelWork wk = sel_work(tp, group);
   if (!wk.ok) return;
+  const int parts = tp.parts;
   const RowSel rs = RAGGED ? row_sel(seq_n, seq_p, hq, wk.row, n, p) : RowSel{n, p};
   const int k0 = wk.part * spb * kSub;
   if (k0 >= rs.n) {   // block-uniform: no key of this row here (a row without keys selects none)
@@ -548,103 +617,89 @@ __global__ __launch_bounds__(kT) void sel_final_kernel(const float* __restrict__
     if (t < parts_r) ph[t] = *reinterpret_cast<const P2Head*>(P2row + int64_t(t) * kSelPart2Bytes);
     const float M = __uint_as_float(state[int64_t(wk.row) * kSelStateWords]);
     const uint32_t b1 = state[int64_t(wk.row) * kSelStateWords + 1];
+#pragma unroll
+    for (int k = 0; k < kSelBins / kT; ++k) h[k * kT + t] = 0ull;
+    if (t < kSelBins3) h3[t] = 0ull;
     __syncthreads();
     if (t < kWave) {   // wave 0: the exact target and whether b1 holds the crossing
-      const bool in = t < parts_r;
-      const u64 Z = wave_sum_u64(in ? ph[t].total : 0ull);
-      const u64 A = wave_sum_u64(in ? ph[t].above_mass : 0ull);
-      const u64 C = wave_sum_u64(in ? ph[t].cand_mass : 0ull);
-      const uint32_t cc = in ? ph[t].cand_cnt : 0u;
+      const bool in = lane < parts_r;
+      const u64 Z = wave_sum_u64(in ? ph[lane].total : 0ull);
+      const u64 A = wave_sum_u64(in ? ph[lane].above_mass : 0ull);
+      const u64 C = wave_sum_u64(in ? ph[lane].cand_mass : 0ull);
+      const uint32_t cc = in ? ph[lane].cand_cnt : 0u;
       const bool over = __ballot(cc > uint32_t(kSelCandCap)) != 0ull;
-      // candidate start positions (exclusive prefix over the parts)
-      int x = int(cc);
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const int y = __shfl_up(x, o, kWave);
-        if (t >= o) x += y;
-      }
-      if (in) pstart[t + 1] = x;
-      if (t == 0) pstart[0] = 0;
-      const int ncand = __shfl(x, kWave - 1, kWave);
+      uint32_t ncand;
+      const uint32_t before = wave_excl_scan_u32(cc, &ncand);
+      if (in) pstart[lane] = int(before);
+      if (lane == 0) pstart[parts_r] = int(ncand);
       const u64 T = u64(ceil(double(rs.p) * double(Z)));
-      if (t == 0) {
+      if (lane == 0) {
         T_s = T;
         A_s = A;
-        fast_s = !over && ncand <= kSelCandLds && A < T && T <= A + C;
+        fast_s = !over && ncand <= uint32_t(kSelCandLds) && A < T && T <= A + C;
       }
     }
     __syncthreads();
     const u64 T = T_s;
     if (fast_s) {
-      // the row's candidates into LDS (all loads in flight), the histogram cleared meanwhile
       const int ncand = pstart[parts_r];
-      for (int b = t; b < kSelBins; b += kT) h[b] = 0;
-      for (int i = t; i < ncand; i += kT) {
-        int lo = 0, hi = parts_r - 1;   // the part holding candidate i
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if (pstart[mid] <= i) lo = mid;
-          else hi = mid - 1;
+      // the row's candidates into LDS: every thread's loads in flight together
+      uint32_t kv[kCandPT];
+#pragma unroll
+      for (int u = 0; u < kCandPT; ++u) {
+        const int i = t + u * kT;
+        if (i < ncand) {
+          const int j = cand_part(pstart, parts_r, i);
+          kv[u] = reinterpret_cast<const uint32_t*>(P2row + int64_t(j) * kSelPart2Bytes + kSelP2Cand)[i - pstart[j]];
         }
-        ck[i] = reinterpret_cast<const uint32_t*>(P2row + int64_t(lo) * kSelPart2Bytes + kSelP2Cand)[i - pstart[lo]];
       }
-      if (t < parts_r) pcnt[t] = 0;
-      __syncthreads();
-      // level 2: key bits 19..8 of the candidates
-      for (int i = t; i < ncand; i += kT) {
-        const uint32_t key = ck[i];
-        const u64 e = fixed_mass(key_score(key), M, scale_log2e);
-        if (e) atomicAdd(&h[(key >> 8) & 0xfffu], e);
+#pragma unroll
+      for (int u = 0; u < kCandPT; ++u) {
+        const int i = t + u * kT;
+        if (i < ncand) {
+          ck[i] = kv[u];
+          const u64 e = fixed_mass(key_score(kv[u]), M, scale_log2e);   // level 2: key bits 19..8
+          if (e) atomicAdd(&h[(kv[u] >> 8) & 0xfffu], e);
+        }
       }
       __syncthreads();
-      lds_crossing<kSelBins>(h, T - A_s, wtot, &cr);
+      lds_crossing_4096(h, T - A_s, coarse, &cr);
       const uint32_t b2 = cr.bin;
       const u64 need2 = cr.need;
       const uint32_t pre = (b1 << 12) | b2;
-      for (int b = t; b < kSelBins3; b += kT) h[b] = 0;
-      __syncthreads();
       // level 3: key bits 7..0 of the candidates inside (b1, b2)
       for (int i = t; i < ncand; i += kT) {
         const uint32_t key = ck[i];
         if ((key >> 8) == pre) {
           const u64 e = fixed_mass(key_score(key), M, scale_log2e);
-          if (e) atomicAdd(&h[key & 0xffu], e);
+          if (e) atomicAdd(&h3[key & 0xffu], e);
         }
       }
       __syncthreads();
-      lds_crossing<kSelBins3>(h, need2, wtot, &cr);
+      lds_crossing_256(h3, need2, coarse, &cr);
       kstar = (pre << 8) | cr.bin;
-      // per part: candidates >= K*
-      for (int i = t; i < ncand; i += kT) {
-        if (ck[i] >= kstar) {
-          int lo = 0, hi = parts_r - 1;
-          while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (pstart[mid] <= i) lo = mid;
-            else hi = mid - 1;
-          }
-          atomicAdd(&pcnt[lo], 1u);
-        }
+      // per part: its keys above b1 plus its candidates >= K* (a wave per part)
+      for (int j = wave; j < parts_r; j += kTW) {
+        int c = 0;
+        for (int i = pstart[j] + lane; i < pstart[j + 1]; i += kWave) c += ck[i] >= kstar ? 1 : 0;
+        c = wave_sum_i32(c);
+        if (lane == 0) pcnt[j] = ph[j].above_cnt + uint32_t(c);
       }
-      __syncthreads();
-      if (t < parts_r) pcnt[t] += ph[t].above_cnt;
       __syncthreads();
     } else {
       kstar = exact_select_row<MULTI>(srow, rs.n, spb, parts_r, M, scale_log2e, T, h, wtot, &cr, pcnt);
     }
     // offset of this part = selected keys of the parts before it
     if (t < kWave) {
-      const int c = t < parts_r ? int(pcnt[t]) : 0;
-      const int before = wave_sum_int(t < wk.part ? c : 0);
-      const int tot = wave_sum_int(c);
-      if (t == 0) {
-        red[0] = before;
-        red[1] = tot;
-      }
+      const uint32_t c = lane < parts_r ? pcnt[lane] : 0u;
+      uint32_t tot;
+      const uint32_t before = wave_excl_scan_u32(c, &tot);
+      if (lane == wk.part) off_s = int(before);
+      if (lane == 0) tot_s = int(tot);
     }
     __syncthreads();
-    offset = red[0];
-    total_sel = red[1];
+    offset = off_s;
+    total_sel = tot_s;
   }
 
   // ascending compaction, sub-chunk by sub-chunk: element (k, thread) of a sub-chunk
@@ -657,29 +712,35 @@ __global__ __launch_bounds__(kT) void sel_final_kernel(const float* __restrict__
     for (int k = 0; k < kPT; ++k) {
       bal[k] = __ballot(in_range(base, k1, k) && score_key(v[k]) >= kstar);
       if (lane == 0) {
-        kcnt[k][wave] = __popcll(bal[k]);
+        kbase[k * kTW + wave] = uint32_t(__popcll(bal[k]));
         // keys base + k*kT + 64 wave + [0, 64) of the row's selection bitmap
         if (masks) masks[int64_t(wk.row) * mask_words + (base + k * kT) / 64 + wave] = bal[k];
       }
     }
     __syncthreads();
+    if (t < kWave) {   // wave 0: exclusive prefix over the 256 (step, wave) counts, 4 per lane
+      const uint32_t c0 = kbase[4 * lane], c1 = kbase[4 * lane + 1], c2 = kbase[4 * lane + 2],
+                     c3 = kbase[4 * lane + 3];
+      uint32_t tot;
+      const uint32_t b0 = wave_excl_scan_u32(c0 + c1 + c2 + c3, &tot);
+      kbase[4 * lane] = b0;
+      kbase[4 * lane + 1] = b0 + c0;
+      kbase[4 * lane + 2] = b0 + c0 + c1;
+      kbase[4 * lane + 3] = b0 + c0 + c1 + c2;
+      if (lane == 0) tot_s = int(tot);   // (reused: the sub-chunk's selected keys)
+    }
+    __syncthreads();
 #pragma unroll
     for (int k = 0; k < kPT; ++k) {
-      int woff = 0, tot = 0;
-#pragma unroll
-      for (int w = 0; w < kTW; ++w) {
-        woff += w < wave ? kcnt[k][w] : 0;
-        tot += kcnt[k][w];
-      }
       if ((bal[k] >> lane) & 1u) {
         const int pre =
             __builtin_amdgcn_mbcnt_hi(uint32_t(bal[k] >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal[k]), 0u));
-        out[offset + woff + pre] = base + k * kT + t;
+        out[offset + int(kbase[k * kTW + wave]) + pre] = base + k * kT + t;
       }
-      offset += tot;
     }
     if (!MULTI) break;
-    __syncthreads();   // kcnt is rewritten for the next sub-chunk
+    offset += tot_s;
+    __syncthreads();   // kbase and tot_s are rewritten for the next sub-chunk
   }
   // the part holding the row's last key writes the count
   if (wk.part == parts_r - 1 && t == 0) sel_count[wk.row] = total_sel;
@@ -703,14 +764,15 @@ template <bool RAGGED, bool MULTI>
 void sel_passes(int rows, int group, hipStream_t stream, int n, const ToppPlan& pl, const float* scores, float p,
                 float scale_log2e, const ToppWorkspace& w, int32_t* sel_idx, int32_t* sel_count, u64* masks,
                 int mask_words, const int32_t* seq_n, const float* seq_p, int heads_q) {
-  const dim3 grid(unsigned(xcd_grid(int64_t(rows / group) * pl.parts, group)));
-  sel_hist_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, pl.spb, pl.parts, group, rows, scale_log2e,
-                                                          w.part1, seq_n, seq_p, heads_q);
-  sel_cand_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, pl.spb, pl.parts, group, rows, p, scale_log2e,
-                                                          w.part1, w.part2, w.state, seq_n, seq_p, heads_q);
-  sel_final_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, pl.spb, pl.parts, group, rows, p, scale_log2e,
-                                                           w.part2, w.state, sel_idx, sel_count, masks, mask_words,
-                                                           seq_n, seq_p, heads_q);
+  const TilePlace tp = tile_place(rows / group, pl.parts, kPlaceGroup);
+  const dim3 grid(unsigned(tile_grid(tp, group)));
+  sel_hist_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, pl.spb, tp, group, scale_log2e, w.part1, seq_n,
+                                                          seq_p, heads_q);
+  sel_cand_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, pl.spb, tp, group, p, scale_log2e, w.part1,
+                                                          w.part2, w.state, seq_n, seq_p, heads_q);
+  sel_final_kernel<RAGGED, MULTI><<<grid, kT, 0, stream>>>(scores, n, pl.spb, tp, group, p, scale_log2e, w.part2,
+                                                           w.state, sel_idx, sel_count, masks, mask_words, seq_n,
+                                                           seq_p, heads_q);
 }
 
 }  // namespace
