@@ -352,6 +352,32 @@ rbq_status rbq_decode_step_varlen_f16(int32_t batch, int32_t heads_q, int32_t he
                                       void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * rbq_decode_step_noalloc -- rbq_decode_step without a workspace argument, for
+ * callers that cannot allocate device memory: code under stream capture,
+ * serving loops with a fixed memory plan, harnesses that forbid allocation.
+ * The step's scratch memory is a static device array of
+ * RBQ_NOALLOC_SCRATCH_BYTES bytes inside the library, one per GPU, held until
+ * the process ends; the address of the current device's copy is looked up on
+ * the first call made with that device current. Arguments, layouts, results
+ * (bitwise) and errors are those of rbq_decode_step, plus:
+ *   RBQ_EUNSUPPORTED when rbq_workspace_bytes(RBQ_OP_DECODE_STEP, B, Hq, Hkv,
+ *     D, n, w) exceeds RBQ_NOALLOC_SCRATCH_BYTES (one sequence of 32 query
+ *     heads over 8 KV heads at D = 128 fits up to n = 128K, w = 256);
+ *   RBQ_EDEVICE when the array's address cannot be looked up.
+ * No kernel depends on what an earlier call left in the array, but every call
+ * on one GPU uses the same array: calls that may overlap in time on one GPU
+ * (other streams, other host threads) race, and the caller must order them.
+ */
+#define RBQ_NOALLOC_SCRATCH_BYTES (16u << 20)
+rbq_status rbq_decode_step_noalloc(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                   const float* q, const float* P, const float* c_q, const float* c_k,
+                                   const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n,
+                                   int32_t w, uint32_t* codes, float* kfac, int32_t flush, float p,
+                                   float sm_scale, uint32_t* qplanes, float* qscal, float* scores,
+                                   int32_t* sel_idx, int32_t* sel_count, float* out, float* lse,
+                                   hipStream_t stream);
+
+/*
  * rbq_mapped_device_pointer -- the device address of pinned host memory
  * (hipHostGetDevicePointer), for a K/V cache kept in host memory while the
  * index stays in HBM (Appendix C: the small index on the GPU, the full cache

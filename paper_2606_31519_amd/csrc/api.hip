@@ -1,6 +1,8 @@
 // Exported C entry points: validate on the host, then enqueue on `stream`.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "rbq_internal.h"
 
 using namespace rbq;
@@ -53,6 +55,34 @@ rbq_status decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, cap, w,
                        sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), nullptr, nullptr,
                        head_dim);
+}
+
+// The scratch memory of rbq_decode_step_noalloc: a static device array, one
+// copy per GPU at its own address. Host code never passes `scratch` itself (on
+// the host the name is only a stand-in for the symbol): the address of the
+// current device's copy is looked up once per device and kept in scratch_ptr.
+__device__ __align__(256) unsigned char scratch[RBQ_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices];
+
+rbq_status scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return RBQ_EDEVICE;
+  }
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) {
+      (void)hipGetLastError();   // leave no error behind for the next call
+      return RBQ_EDEVICE;
+    }
+    scratch_ptr[dev] = ptr;
+  }
+  *out = scratch_ptr[dev];
+  return RBQ_OK;
 }
 
 }  // namespace
@@ -223,6 +253,22 @@ rbq_status rbq_decode_step_f16(int32_t batch, int32_t heads_q, int32_t heads_kv,
   return decode_step(batch, heads_q, heads_kv, head_dim, q, P, nullptr, c_k, K, V, kv_dtype, cap, n, w, codes,
                      nullptr, kfac16, flush, p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws,
                      ws_bytes, stream);
+}
+
+rbq_status rbq_decode_step_noalloc(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
+                                   const float* q, const float* P, const float* c_q, const float* c_k, const void* K,
+                                   const void* V, int32_t kv_dtype, int32_t cap, int32_t n, int32_t w,
+                                   uint32_t* codes, float* kfac, int32_t flush, float p, float sm_scale,
+                                   uint32_t* qplanes, float* qscal, float* scores, int32_t* sel_idx,
+                                   int32_t* sel_count, float* out, float* lse, hipStream_t stream) {
+  const size_t need = rbq_workspace_bytes(RBQ_OP_DECODE_STEP, batch, heads_q, heads_kv, head_dim, n, w);
+  if (need > size_t(RBQ_NOALLOC_SCRATCH_BYTES)) return RBQ_EUNSUPPORTED;   // (0: invalid sizes, rejected below)
+  void* ws = nullptr;
+  const rbq_status s = scratch_address(&ws);
+  if (s != RBQ_OK) return s;
+  return decode_step(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, kv_dtype, cap, n, w, codes, kfac,
+                     nullptr, flush, p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, ws,
+                     size_t(RBQ_NOALLOC_SCRATCH_BYTES), stream);
 }
 
 }  // extern "C"

@@ -233,7 +233,7 @@ const char* rbq_status_string(rbq_status s) {
   switch (s) {
     case RBQ_OK: return "ok";
     case RBQ_EINVAL: return "invalid argument";
-    case RBQ_EUNSUPPORTED: return "unsupported shape or dtype";
+    case RBQ_EUNSUPPORTED: return "unsupported shape, dtype or size";
     case RBQ_EDEVICE: return "HIP runtime error";
     default: return "unknown status";
   }

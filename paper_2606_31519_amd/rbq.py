@@ -21,6 +21,7 @@ RBQ_ENCODE_SET_CENTROID = 1
 RBQ_OP_ENCODE, RBQ_OP_TOPP, RBQ_OP_SPARSE_DECODE, RBQ_OP_DENSE_DECODE, RBQ_OP_DECODE_STEP = 1, 2, 3, 4, 5
 QSCAL_STRIDE = 8
 RBQ_MAX_WINDOW = 4096   # largest local window accepted by the decode calls
+RBQ_NOALLOC_SCRATCH_BYTES = 16 << 20   # the static scratch of rbq_decode_step_noalloc
 
 EXPORTED = [
     "rbq_encode_keys", "rbq_quantize_query", "rbq_score", "rbq_topp_select", "rbq_sparse_decode",
@@ -30,6 +31,7 @@ EXPORTED = [
     "rbq_decode_step_varlen", "rbq_quantize_query_bits",
     "rbq_score_q8", "rbq_score_ints_q8", "rbq_mapped_device_pointer",
     "rbq_encode_keys_f16", "rbq_score_f16", "rbq_decode_step_f16", "rbq_score_varlen_f16", "rbq_decode_step_varlen_f16",
+    "rbq_decode_step_noalloc",
 ]
 
 
@@ -60,6 +62,8 @@ def _load():
                              vp],
         "rbq_decode_step": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, i32, f32, f32,
                             vp, vp, vp, vp, vp, vp, vp, vp, sz, vp],
+        "rbq_decode_step_noalloc": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, i32, f32,
+                                    f32, vp, vp, vp, vp, vp, vp, vp, vp],
         "rbq_quantize_query_bits": [i32, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp],
         "rbq_score_varlen": [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp],
         "rbq_topp_select_varlen": [i32, i32, i32, vp, vp, vp, f32, vp, vp, vp, sz, vp],
@@ -277,6 +281,17 @@ def rbq_decode_step(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, ca
         _ptr(qscal), _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _ptr(out), _ptr(lse), _ptr(ws), ws_bytes,
         _stream(stream)))
 
+
+def rbq_decode_step_noalloc(batch, heads_q, heads_kv, head_dim, q, P, c_q, c_k, K, V, cap, n, w, codes, kfac, flush,
+                            p, sm_scale, qplanes, qscal, scores, sel_idx, sel_count, out, lse, stream=None):
+    _need("rbq_decode_step_noalloc", qplanes=(qplanes, batch * heads_q * 4 * (head_dim // 32)),
+          qscal=(qscal, batch * heads_q * QSCAL_STRIDE), scores=(scores, batch * heads_q * n),
+          sel_idx=(sel_idx, batch * heads_q * n), sel_count=(sel_count, batch * heads_q),
+          out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q))
+    _check("rbq_decode_step_noalloc", lib.rbq_decode_step_noalloc(
+        batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(P), _ptr(c_q), _ptr(c_k), _ptr(K), _ptr(V),
+        kv_dtype_code(K), cap, n, w, _ptr(codes), _ptr(kfac), int(bool(flush)), p, sm_scale, _ptr(qplanes),
+        _ptr(qscal), _ptr(scores), _ptr(sel_idx), _ptr(sel_count), _ptr(out), _ptr(lse), _stream(stream)))
 
 # ---- ragged batches: per-sequence key counts (seq_n), window rows (seq_w) and p (seq_p), device tensors
 

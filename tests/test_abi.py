@@ -254,3 +254,14 @@ def test_mapped_device_pointer_rejects_null_arguments(lib):
     out = ctypes.c_void_p(123)
     assert lib.lib.rbq_mapped_device_pointer(None, ctypes.byref(out)) == lib.RBQ_EINVAL
     assert lib.lib.rbq_mapped_device_pointer(ctypes.c_void_p(FAKE), None) == lib.RBQ_EINVAL
+
+
+def test_noalloc_step_rejects_sizes_beyond_its_scratch_on_the_host(lib):
+    """rbq_decode_step_noalloc returns RBQ_EUNSUPPORTED for sizes whose step
+    workspace exceeds its static scratch, before any pointer is read or any
+    device call is made (so it runs without a GPU)."""
+    B, Hq, Hkv, D, n, w = 4, 64, 8, 128, 131072, 256
+    assert lib.rbq_workspace_bytes(lib.RBQ_OP_DECODE_STEP, B, Hq, Hkv, D, n, w) > lib.RBQ_NOALLOC_SCRATCH_BYTES
+    st = lib.lib.rbq_decode_step_noalloc(B, Hq, Hkv, D, *([None] * 6), lib.RBQ_BF16, n + w, n, w, None, None, 1,
+                                         0.9, 0.1, *([None] * 7), None)
+    assert st == lib.RBQ_EUNSUPPORTED
