@@ -47,14 +47,15 @@ constexpr int kSelCoarse = 64;                         // coarse bins of 64 firs
 constexpr int kSelCandCap = 4096;                      // candidate keys one part hands to the final pass
 constexpr int kSelCandLds = 16384;                     // candidate keys of a row the final pass holds in LDS
 constexpr int32_t kToppMaxKeys = int32_t(1) << 24;     // keys per row the fixed-point sums hold
-// per-part records (bytes): the first pass's histogram (block max, 64 coarse
-// sums, the directory of non-empty coarse bins, their 64-bin sections, in
-// fp32) and the second pass's sums and candidate keys
-constexpr size_t kSelP1Coarse = 16, kSelP1Dir = 16 + 4 * kSelCoarse, kSelP1Sec = 1024;
-constexpr size_t kSelPart1Bytes = kSelP1Sec + size_t(4) * kSelCoarse * 64;
+// per-part records (bytes): the first pass's exact histogram (the part's
+// maximum and total, 64 coarse sums, the directory of non-empty coarse bins
+// and their 64-bin sections; 64-bit fixed-point masses relative to the part's
+// maximum) and the second pass's counts and candidate keys
+constexpr size_t kSelP1Coarse = 16, kSelP1Dir = 16 + 8 * kSelCoarse, kSelP1Sec = 1024;
+constexpr size_t kSelPart1Bytes = kSelP1Sec + size_t(8) * kSelCoarse * 64;
 constexpr size_t kSelP2Cand = 64;
 constexpr size_t kSelPart2Bytes = kSelP2Cand + size_t(4) * kSelCandCap;
-constexpr int kSelStateWords = 4;                      // per row: row max (bits), first-level crossing bin
+constexpr int kSelStateWords = 8;   // per row: row maximum, b1, mass needed inside b1, target (fp64)
 
 struct ToppPlan {
   int32_t spb;     // sub-chunks per part

@@ -81,6 +81,13 @@ __device__ __forceinline__ uint32_t query_dot(const Spread& e, const uint32_t* q
 
 // The launch: tiles (KV group, Top-p part) placed by tile_place(), `slots`
 // blocks of kScoreThreads * KPT keys per tile.
+// Scores of a standalone scan (stream placement) are written past the caches;
+// those of a step's scan (group placement) stay in the XCD's L2, where the
+// Top-p passes that run the same tiles read them next.
+__device__ __forceinline__ void put_score(float v, float* p, bool keep) {
+  if (keep) *p = v;
+  else __builtin_nontemporal_store(v, p);
+}
 struct ScoreGrid {
   TilePlace tp;
   int slots;   // score blocks per part
@@ -107,6 +114,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   const int64_t kbase = int64_t(bh) * cap;
   const int i0 = blk * (kScoreThreads * KPT) + threadIdx.x;
   const int row0 = b * Hq + hk * G;
+  const bool keep = sg.tp.mode == kPlaceGroup;
 
   const int nb = RAGGED ? min(max(seq_n[b], 0), n) : n;   // this sequence's indexed keys
   if (blk * (kScoreThreads * KPT) >= nb) return;   // block-uniform: no key of this block is indexed
@@ -176,7 +184,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       for (int u = 0; u < KPT; ++u) {
         const int ip = int(query_dot<QB>(e[u], qn));
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
-        __builtin_nontemporal_store(assemble(u, y, B0), out + i0 + u * kScoreThreads);
+        put_score(assemble(u, y, B0), out + i0 + u * kScoreThreads, keep);
       }
     }
     return;
@@ -201,7 +209,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         const float sc = assemble(u, y, B0);
-        if (i < nb) __builtin_nontemporal_store(sc, out + i);
+        if (i < nb) put_score(sc, out + i, keep);
       }
     }
   }
