@@ -97,12 +97,40 @@ def copy_probe(torch, steps):
     print(json.dumps({"copy_probe": _copy_rate(torch, steps)}), flush=True)
 
 
-def _git_sha():
+BUILD_INFO = os.path.join(ROOT, "paper_2606_31519_amd", "librbq.build.json")
+
+
+def _build_info():
+    """What the build wrote beside librbq.so: its commit (git may be absent where
+    the bench runs), whether the sources differed from it, and their hash."""
     try:
-        return subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"], capture_output=True,
-                              text=True).stdout.strip() or None
+        with open(BUILD_INFO) as f:
+            return json.load(f)
     except Exception:
         return None
+
+
+def _git_sha():
+    try:
+        sha = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short=12", "HEAD"], capture_output=True,
+                             text=True).stdout.strip()
+        if sha:
+            return sha
+    except Exception:
+        pass
+    info = _build_info()
+    return info.get("git") if info else None
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    return None
 
 
 def _clone_state(st, pipeline):
@@ -148,11 +176,12 @@ def cpu_baseline(wl, budget_s: float = 10.0, max_steps: int = 20) -> dict:
     each (quantise, score, Top-p, sparse attention, flush), group after group,
     repeating whole steps of the workload until ~budget_s of CPU work."""
     from oracle import rbq_oracle as orc
-    try:
+    cores = len(os.sched_getaffinity(0))   # the CPUs this process may run on
+    try:   # the BLAS pool the oracle's matrix products use (everything else is one thread)
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
-        cores = 1
+        blas_threads = None
     n, w, G, D = wl.n_index, wl.w, wl.G, wl.D
     tau = 1.0 / math.sqrt(D)
     groups = []
@@ -180,7 +209,8 @@ def cpu_baseline(wl, budget_s: float = 10.0, max_steps: int = 20) -> dict:
             break
     return {"value": done_keys / t_total, "unit": "keys/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{done_groups} KV-group decode steps of the 128K workload ({wl.Hkv} groups per step, "
-                      f"{G} query heads x {n} keys per group; index build excluded), {t_total:.1f} s"}
+                      f"{G} query heads x {n} keys per group; index build excluded), {t_total:.1f} s",
+            "blas_threads": blas_threads, "cpu_model": _cpu_model()}
 
 
 def _graph(torch, fn):
@@ -229,12 +259,9 @@ def _replay_distribution(torch, graphs, reps=50, warmup=10):
             "p90_ms": float(np.percentile(d, 90))}
 
 
-def time_scan_c5(pipeline, gen, torch, steps, warmup, replicas=4):
-    """Standalone rbq_score scan on the wide-head workload (batch 4 x 128K, 64/8 heads)."""
-    wl = gen.config5()
-    st = pipeline.DecodeState.from_workload(wl)
-    del wl
-    st.build_index()
+def time_scan_c5(pipeline, torch, st, steps, warmup, replicas=4):
+    """Standalone rbq_score scan on the wide-head workload (batch 4 x 128K, 64/8
+    heads; st: its state with the index built)."""
     st.quantize()
     torch.cuda.synchronize()
     reps = [st]
@@ -276,6 +303,79 @@ def time_scan_c5(pipeline, gen, torch, steps, warmup, replicas=4):
             "traffic": _measured_traffic(SCAN_TRAFFIC_FILE, SCORE_SRC, "score_source_sha256"),
             "compact_index": {"ms": ms16, "keys_per_s": B * Hq * n / (ms16 * 1e-3), "bytes": nbytes16,
                               "GBps": gbs16, "frac_hbm": gbs16 / HBM_PEAK_GBS}}
+
+
+def time_gqa_step(pipeline, torch, wl, steps, warmup, replicas=4, st0=None):
+    """The fused step (rbq_decode_step) of a GQA workload at its p against this
+    library's dense decode of the same rows, over `replicas` copies of the cache
+    (so a step does not find the previous one's K/V in the Infinity Cache), with
+    the selected budget and the KV-group union of the selected rows."""
+    p = wl.p
+    if st0 is None:
+        st0 = pipeline.DecodeState.from_workload(wl)
+        st0.build_index()
+        torch.cuda.synchronize()
+    reps = [st0] + [_clone_state(st0, pipeline) for _ in range(replicas - 1)]
+    gs = [_graph(torch, lambda r=r: r.step(p)) for r in reps]
+    ms = _time_graphs(torch, gs, steps, warmup)
+    del gs
+    d_out, d_lse = torch.empty_like(st0.out), torch.empty_like(st0.lse)
+    gs = [_graph(torch, lambda r=r: r.dense_decode(d_out, d_lse)) for r in reps]
+    dense = _time_graphs(torch, gs, steps, warmup)
+    del gs, reps
+    st0.step(p)
+    torch.cuda.synchronize()
+    u_rows, _ = _union_rows(st0)
+    cnt = st0.sel_count.cpu().numpy()
+    B, Hq, Hkv, n = st0.B, st0.Hq, st0.Hkv, st0.n
+    return {"workload": wl.name, "p": p, "ms_per_step": ms, "dense_decode_ms": dense,
+            "speedup_vs_dense": dense / ms, "keys_per_s": B * Hq * n / (ms * 1e-3),
+            "budget_frac": float(cnt.mean()) / n, "union_frac": u_rows / (B * Hkv * n)}
+
+
+def time_config1(pipeline, gen, torch, steps):
+    """Config 1 (one head, 4096 fp32 keys, p = 0.9): each call's time on the GPU
+    (a graph of 16 calls) beside the oracle's time for the same call on the host
+    (best of 3), on the same inputs."""
+    from oracle import rbq_oracle as orc
+    wl = gen.config1()
+    st = pipeline.DecodeState.from_workload(wl)
+    st.build_index()
+    st.quantize()
+    st.score()
+    st.select(wl.p)
+    torch.cuda.synchronize()
+    calls = {"encode": lambda: st.build_index(), "quantize": lambda: st.quantize(), "score": lambda: st.score(),
+             "topp": lambda: st.select(wl.p), "sparse_decode": lambda: st.sparse_decode()}
+    gpu = {}
+    for name, f in calls.items():
+        g = _graph(torch, lambda f=f: [f() for _ in range(16)])
+        gpu[name] = _time_graphs(torch, [g], max(2, steps // 4), 2) / 16
+        del g
+    K = wl.K_f32(0, 0).astype(np.float64)
+    V = wl.V_f32(0, 0).astype(np.float64)
+    q, P, cq = wl.q[0, 0], wl.P, wl.c_q[0, 0]
+    tau = 1.0 / math.sqrt(wl.D)
+    box = {}
+
+    def best(name, fn):
+        ts = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            r = fn()
+            ts.append(time.perf_counter() - t0)
+        box[name] = r
+        return min(ts)
+
+    cpu = {"encode": best("enc", lambda: orc.encode_keys(K, P, c_q=cq))}
+    cpu["quantize"] = best("qq", lambda: orc.quantize_query(q, P, cq, box["enc"]["c_k"]))
+    cpu["score"] = best("est", lambda: orc.estimate_scores(box["enc"], box["qq"]))
+    cpu["topp"] = best("sel", lambda: orc.topp_select(box["est"]["S"], wl.p, tau))
+    cpu["sparse_decode"] = best("out", lambda: orc.sparse_decode(q, K, V, box["sel"]["idx"], K[:0], V[:0], tau))
+    return {"workload": wl.name, "p": wl.p,
+            "calls": {k: {"gpu_ms": gpu[k], "oracle_s": cpu[k], "oracle_over_gpu": cpu[k] * 1e3 / gpu[k]}
+                      for k in calls},
+            "step_gpu_ms": sum(gpu.values()), "step_oracle_s": sum(cpu.values())}
 
 
 def time_ragged(pipeline, gen, torch, steps, warmup, seed=20260):
@@ -654,6 +754,8 @@ def main():
     ap.add_argument("--no-compact", action="store_true", help="skip the step on the compact (fp16-factor) index")
     ap.add_argument("--no-d64", action="store_true", help="skip the step at head dimension 64")
     ap.add_argument("--no-ablation", action="store_true", help="skip the score call on the kernel-ablation shapes")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip config 1 (per call, GPU vs oracle), config 2 (32K step) and the config-5 step")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB copy used to calibrate the HBM byte counters")
     args = ap.parse_args()
@@ -801,10 +903,23 @@ def main():
 
     del reps, step_graphs
     torch.cuda.empty_cache()
-    scan = None
-    if not args.no_scan:
-        scan = time_scan_c5(pipeline, gen, torch, args.steps, args.warmup)
-        scan["frac_of_copy"] = scan["GBps"] / copy["GBps"]
+    scan = c5_step = None
+    if not (args.no_scan and args.no_configs):
+        wl5 = gen.config5()
+        st5 = pipeline.DecodeState.from_workload(wl5)
+        st5.build_index()
+        torch.cuda.synchronize()
+        if not args.no_scan:
+            scan = time_scan_c5(pipeline, torch, st5, args.steps, args.warmup)
+            scan["frac_of_copy"] = scan["GBps"] / copy["GBps"]
+        if not args.no_configs:
+            c5_step = time_gqa_step(pipeline, torch, wl5, args.steps, args.warmup, st0=st5)
+        del wl5, st5
+        torch.cuda.empty_cache()
+    c1 = c2 = None
+    if not args.no_configs:
+        c1 = time_config1(pipeline, gen, torch, args.steps)
+        c2 = time_gqa_step(pipeline, torch, gen.config2(), args.steps, args.warmup)
         torch.cuda.empty_cache()
     ragged = None if args.no_ragged else time_ragged(pipeline, gen, torch, args.steps, args.warmup)
     torch.cuda.empty_cache()
@@ -823,6 +938,13 @@ def main():
             print(f"prefill co-runner unavailable: {e}", file=sys.stderr)
     cnt = st0.sel_count.cpu().numpy()
     keys_scored = st0.B * st0.Hq * st0.n
+    if scan is not None:   # the scan's own roofline (the other half of the headline metric)
+        roofline["scan"] = {"kernel": "score_kernel", "workload": scan["workload"], "bound": "hbm",
+                            "achieved": scan["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": scan["frac_hbm"], "traffic": scan["traffic"],
+                            "algorithmic_bytes_per_launch": float(scan["bytes"]), "ms_per_launch": scan["ms"],
+                            "keys_per_s": scan["keys_per_s"]}
+    # (the driver keeps the end of the output: the detailed reports first, the summary last)
     line = {
         "metric": "proxy-scored keys/s of the Top-p sparse decode step at 128K context",
         "value": keys_scored / (ms_step * 1e-3),
@@ -831,12 +953,6 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
-        "ms_per_step_five_calls": ms_step_calls,
-        "step_distribution": step_dist,
-        # a serving loop's per-token cost: the step without the flush plus the
-        # flush of the window (stages.flush) spread over the w tokens it holds
-        "ms_per_step_flush_amortized": ms_step_noflush + stage_ms["flush"] / max(st0.w, 1),
-        "ms_per_step_no_flush": ms_step_noflush,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -845,26 +961,36 @@ def main():
         "config": {"workload": "gqa 32q/8kv ctx=128K (130816 indexed + 256 window) b=1 bf16, lazy flush of 256 keys",
                    "p": p, "batch": st0.B, "heads_q": st0.Hq, "heads_kv": st0.Hkv, "head_dim": st0.D,
                    "context": st0.n + st0.w, "replicas": args.replicas},
-        "dense_decode_ms": dense_ms,
-        "sdpa_decode_ms": sdpa_ms,
-        "speedup_vs_dense": dense_best / ms_step,
-        "dense_GBps": dense_bytes / (dense_ms * 1e-3) / 1e9,
-        "budget": {"mean": float(cnt.mean()), "min": int(cnt.min()), "max": int(cnt.max()),
-                   "union_rows_per_kv_head": union_rows / (st0.B * st0.Hkv)},
-        "stages": kern,
-        "roofline": roofline,
-        "scan_wide_heads": scan,
-        "p_sweep": sweep or None,
-        "ragged": ragged,
         "recall": recall,
+        "ragged": ragged,
         "prefill_overlap": prefill,
         "kv_in_host_memory": offloaded,
         "compact_index": compact,
         "head_dim_64": d64,
         "score_ablation_shapes": ablation,
-        "cpu_baseline": cpu,
+        "step_distribution": step_dist,
+        "stages": kern,
         "gen_s": t_gen,
+        "sdpa_decode_ms": sdpa_ms,
+        "dense_GBps": dense_bytes / (dense_ms * 1e-3) / 1e9,
+        "budget": {"mean": float(cnt.mean()), "min": int(cnt.min()), "max": int(cnt.max()),
+                   "union_rows_per_kv_head": union_rows / (st0.B * st0.Hkv)},
+        "ms_per_step_five_calls": ms_step_calls,
+        # a serving loop's per-token cost: the step without the flush plus the
+        # flush of the window (stages.flush) spread over the w tokens it holds
+        "ms_per_step_flush_amortized": ms_step_noflush + stage_ms["flush"] / max(st0.w, 1),
+        "ms_per_step_no_flush": ms_step_noflush,
+        "config1_per_call": c1,
+        "config2_step": c2,
+        "config5_step": c5_step,
+        "scan_wide_heads": scan,
+        "p_sweep": sweep or None,
         "git": _git_sha(),
+        "build": _build_info(),
+        "dense_decode_ms": dense_ms,
+        "speedup_vs_dense": dense_best / ms_step,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
 

@@ -68,7 +68,40 @@ def build(verbose: bool = False) -> str:
     tmp = LIB_PATH + ".tmp"
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
     os.replace(tmp, LIB_PATH)
+    _write_build_info()
     return LIB_PATH
+
+
+BUILD_INFO = os.path.join(HERE, "librbq.build.json")
+
+
+def _write_build_info() -> None:
+    """Beside the library: the commit it was built from (with whether the tree
+    had uncommitted changes) and a hash of its sources, so that a run on a
+    machine without the repository's history can still name what it ran."""
+    import datetime
+    import hashlib
+    import json
+
+    def git(*args):
+        try:
+            r = subprocess.run(["git", "-C", HERE, *args], capture_output=True, text=True, timeout=10)
+            return r.stdout.strip() if r.returncode == 0 else None
+        except Exception:
+            return None
+
+    h = hashlib.sha256()
+    inc = os.path.join(os.path.dirname(HERE), "include")
+    for d in (CSRC, inc):
+        for name in sorted(os.listdir(d)):
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    status = git("status", "--porcelain", "--", CSRC, inc)
+    info = {"git": git("rev-parse", "--short=12", "HEAD"), "sources_dirty": bool(status) if status is not None else None,
+            "sources_sha256": h.hexdigest(), "arch": ARCH,
+            "built_utc": datetime.datetime.now(datetime.timezone.utc).strftime("%Y-%m-%dT%H:%M:%SZ")}
+    with open(BUILD_INFO, "w") as f:
+        json.dump(info, f)
 
 
 if __name__ == "__main__":

@@ -84,8 +84,11 @@ __device__ __forceinline__ uint32_t query_dot(const Spread& e, const uint32_t* q
 // Scores of a standalone scan (stream placement) are written past the caches;
 // those of a step's scan (group placement) stay in the XCD's L2, where the
 // Top-p passes that run the same tiles read them next.
-__device__ __forceinline__ void put_score(float v, float* p, bool keep) {
-  if (keep) *p = v;
+// (a compile-time choice: the two stores in one run-time branch get merged into
+// a plain store, dropping the streaming hint)
+template <bool KEEP>
+__device__ __forceinline__ void put_score(float v, float* p) {
+  if constexpr (KEEP) *p = v;
   else __builtin_nontemporal_store(v, p);
 }
 struct ScoreGrid {
@@ -98,7 +101,8 @@ struct ScoreGrid {
 // into its low and high nibbles, ip = ip_lo + 16 ip_hi, two dot8 chains).
 // D: head dimension, 128 or 64 (64: the two code words per key and per query
 // plane are padded with zero words, which add nothing to ip or pc).
-template <int KPT, bool INTS, bool RAGGED, bool FAC16, int QB = 4, int D = kHeadDim>
+// KEEP: the scores stay in L2 (group placement: a step's scan), else they stream past it.
+template <int KPT, bool INTS, bool RAGGED, bool FAC16, int QB = 4, int D = kHeadDim, bool KEEP = false>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const uint32_t* __restrict__ codes, const f32x2* __restrict__ kfac, const uint16_t* __restrict__ kfac16,
     const uint32_t* __restrict__ qplanes, const float* __restrict__ qscal, float* __restrict__ scores,
@@ -114,7 +118,6 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
   const int64_t kbase = int64_t(bh) * cap;
   const int i0 = blk * (kScoreThreads * KPT) + threadIdx.x;
   const int row0 = b * Hq + hk * G;
-  const bool keep = sg.tp.mode == kPlaceGroup;
 
   const int nb = RAGGED ? min(max(seq_n[b], 0), n) : n;   // this sequence's indexed keys
   if (blk * (kScoreThreads * KPT) >= nb) return;   // block-uniform: no key of this block is indexed
@@ -184,7 +187,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       for (int u = 0; u < KPT; ++u) {
         const int ip = int(query_dot<QB>(e[u], qn));
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
-        put_score(assemble(u, y, B0), out + i0 + u * kScoreThreads, keep);
+        put_score<KEEP>(assemble(u, y, B0), out + i0 + u * kScoreThreads);
       }
     }
     return;
@@ -209,20 +212,20 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         const float sc = assemble(u, y, B0);
-        if (i < nb) put_score(sc, out + i, keep);
+        if (i < nb) put_score<KEEP>(sc, out + i);
       }
     }
   }
 }
 
-template <bool INTS, bool RAGGED, bool FAC16 = false, int QB = 4, int D = kHeadDim>
+template <bool INTS, bool RAGGED, bool FAC16 = false, int QB = 4, int D = kHeadDim, bool KEEP = false>
 rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
                       const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal, float* scores,
                       int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreGrid sg,
                       const int32_t* seq_n) {
   const f32x2* f2 = reinterpret_cast<const f32x2*>(kfac);
 #define RBQ_SCORE_KPT(K)                                                                                    \
-  score_kernel<K, INTS, RAGGED, FAC16, QB, D><<<grid, kScoreThreads, 0, stream>>>(                          \
+  score_kernel<K, INTS, RAGGED, FAC16, QB, D, KEEP><<<grid, kScoreThreads, 0, stream>>>(                          \
       codes, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, cap, Hq, Hkv, G, sg, seq_n)
   switch (kpt) {
     case 4: RBQ_SCORE_KPT(4); break;
@@ -247,6 +250,14 @@ rbq_status launch_score_d(int kpt, dim3 grid, hipStream_t stream, const uint32_t
     return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, false, true, 8) : RBQ_SCORE_LAUNCH(false, false, false, 8);
   }
   if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, 4);   // (the integer hook is never ragged)
+  if (sg.tp.mode == kPlaceGroup) {   // a step's scan: the scores stay in L2 for the Top-p passes
+#define RBQ_SCORE_KEEP(R, F)                                                                                      \
+  launch_kpt<false, R, F, 4, D, true>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, \
+                                      n, cap, Hq, Hkv, G, sg, seq_n)
+    if (seq_n != nullptr) return kfac16 != nullptr ? RBQ_SCORE_KEEP(true, true) : RBQ_SCORE_KEEP(true, false);
+    return kfac16 != nullptr ? RBQ_SCORE_KEEP(false, true) : RBQ_SCORE_KEEP(false, false);
+#undef RBQ_SCORE_KEEP
+  }
   if (seq_n != nullptr)
     return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, true, true, 4) : RBQ_SCORE_LAUNCH(false, true, false, 4);
   return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, false, true, 4) : RBQ_SCORE_LAUNCH(false, false, false, 4);
