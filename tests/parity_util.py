@@ -20,6 +20,13 @@ import numpy as np
 
 from oracle import rbq_oracle as orc
 
+# The GPU's cumulative softmax mass differs from the fp64 one by the 2^-40
+# truncation of each mass (<= n 2^-40 of the top mass: 1.2e-7 at n = 2^17), the
+# hardware exp2's ~1 ulp (1.2e-7 relative), and above all the fp32 rounding of
+# the exponent's argument x = (S - m) tau log2(e): each of its two roundings is
+# 2^-24 |x|, which moves a mass by ln2 2^-23 |x| relative, so the total moves by
+# ln2 2^-23 times the mass-weighted mean of |x| (up to ~20 on the flat rows of
+# the tests): ~2e-6 in all. The band is that with a margin for the exp2's ulps.
 MASS_BAND = 5e-6
 OUT_ATOL = 2e-3
 LSE_ATOL = 1e-3
