@@ -234,11 +234,9 @@ rbq_status rbq_dense_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, in
  * (K + n*D: row n of every (b, kv-head) block, rows `cap` apart), with fewer
  * launches: the query quantisation and the window encode share one launch
  * (the encode writes index rows [n, n + w), which nothing else in the step
- * reads); the score pass also writes per-block maxima of every query head
- * and clears the selection's counters, so the selection starts from the
- * histogram; the selection also writes per-head bitmaps of the selected keys,
- * from which the sparse attention builds its row lists without searching
- * sel_idx. Every argument means what it means in those calls; qplanes, qscal,
+ * reads), and the selection also writes per-head bitmaps of the selected
+ * keys, from which the sparse attention builds its row lists without
+ * searching sel_idx. Every argument means what it means in those calls; qplanes, qscal,
  * scores, sel_idx and sel_count are written as they would be.
  *   flush: nonzero to run the window encode (codes / kfac rows [n, n + w)).
  *   ws: at least rbq_workspace_bytes(RBQ_OP_DECODE_STEP, B, Hq, Hkv, D, n, w) bytes.

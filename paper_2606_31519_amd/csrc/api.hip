@@ -47,10 +47,9 @@ rbq_status decode_step(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t
     s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, 4, head_dim);
   if (s != RBQ_OK) return s;
   s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   nullptr, kfac16, 4, head_dim, kPlaceGroup);
+                   nullptr, kfac16, 4, head_dim);
   if (s != RBQ_OK) return s;
-  s = launch_topp(int32_t(rows), n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, stream, heads_q / heads_kv,
-                  sw.masks);
+  s = launch_topp(int32_t(rows), n, scores, p, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.masks);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, cap, w,
                        sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), nullptr, nullptr,
@@ -337,10 +336,10 @@ rbq_status decode_step_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, 
     s = launch_quantize(batch, heads_q, heads_kv, q, P, c_q, c_k, qplanes, qscal, nullptr, stream, 4, head_dim);
   if (s != RBQ_OK) return s;
   s = launch_score(batch, heads_q, heads_kv, n, cap, codes, kfac, qplanes, qscal, scores, nullptr, nullptr, stream,
-                   seq_n, kfac16, 4, head_dim, kPlaceGroup);
+                   seq_n, kfac16, 4, head_dim);
   if (s != RBQ_OK) return s;
-  s = launch_topp(int32_t(rows), n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, stream, heads_q / heads_kv,
-                  sw.masks, seq_n, seq_p, heads_q);
+  s = launch_topp(int32_t(rows), n, scores, 0.5f, sm_scale, sel_idx, sel_count, sw.topp, stream, sw.masks,
+                  seq_n, seq_p, heads_q);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K, V, cap, w,
                        sm_scale, out, lse, sw.decode, true, stream, sw.masks, topp_mask_words(n), seq_n, seq_w,
@@ -379,7 +378,7 @@ rbq_status rbq_topp_select_varlen(int32_t batch, int32_t heads_q, int32_t n, con
   if (s != RBQ_OK) return s;
   if ((s = check_ragged(n, 0, n, seq_n, nullptr)) != RBQ_OK) return s;
   if (seq_p == nullptr || (reinterpret_cast<uintptr_t>(seq_p) & 15u) != 0) return RBQ_EINVAL;
-  return launch_topp(batch * heads_q, n, scores, 0.5f, sm_scale, sel_idx, sel_count, ws, stream, 1, nullptr, seq_n,
+  return launch_topp(batch * heads_q, n, scores, 0.5f, sm_scale, sel_idx, sel_count, ws, stream, nullptr, seq_n,
                      seq_p, heads_q);
 }
 

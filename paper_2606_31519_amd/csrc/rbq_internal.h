@@ -182,23 +182,17 @@ rbq_status launch_quantize_flush(int32_t batch, int32_t heads_q, int32_t heads_k
                                  const int32_t* seq_off = nullptr, const int32_t* seq_cnt = nullptr,
                                  int32_t off_max = 0, uint16_t* kfac16 = nullptr, int32_t head_dim = kHeadDim);
 // seq_n (ragged batches): [B] indexed keys per sequence, clamped to [0, n]; n is the row stride
-// place: kPlaceGroup when the Top-p passes of the same step read the scores
-// next (their blocks then find them in their own L2), kPlaceStream otherwise
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream,
                         const int32_t* seq_n = nullptr, const uint16_t* kfac16 = nullptr, int32_t planes = 4,
-                        int32_t head_dim = kHeadDim, int32_t place = kPlaceStream);
+                        int32_t head_dim = kHeadDim);
 // (kfac16: the compact index's fp16 factors [B][Hkv][cap], read instead of kfac when non-NULL; g = 0.
 //  planes: query bit-planes per head, 4 or 8 (8: B_q up to 8; uniform, unfused calls only))
-// group: rows per KV group (heads_q / heads_kv when the scores come from
-// launch_score of the same step with kPlaceGroup, 1 when unknown): only the
-// placement of the blocks on the XCDs depends on it. masks: optional [rows][topp_mask_words(n)]
-// selection bitmaps (bit i of word k = key 64 k + i); seq_n / seq_p (ragged
+// masks: optional [rows][topp_mask_words(n)] selection bitmaps (bit i of word k = key 64 k + i); seq_n / seq_p (ragged
 // batches): [B] keys and p per sequence, row r of sequence r / heads_q
 rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,
-                       int32_t* sel_count, void* ws, hipStream_t stream, int32_t group = 1,
-                       unsigned long long* masks = nullptr, const int32_t* seq_n = nullptr,
+                       int32_t* sel_count, void* ws, hipStream_t stream, unsigned long long* masks = nullptr, const int32_t* seq_n = nullptr,
                        const float* seq_p = nullptr, int32_t heads_q = 1);
 rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const float* q, const void* K,
                          const void* V, int32_t kv_dtype, int32_t cap, int32_t n, const int32_t* sel_idx,

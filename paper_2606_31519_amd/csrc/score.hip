@@ -24,10 +24,8 @@
 // runs on the matrix cores instead (score_mfma_kernel: one mixed e4m3 x e2m1
 // product per 16 keys and all heads), which halves the vector-ALU work per key;
 // the integers, and so the scores, are bitwise those of the dot8 form.
-// Placement: the blocks of (KV group g, Top-p part j) -- the keys
-// [j * span, (j + 1) * span), span = the Top-p part length -- run on the XCD
-// tile_place() gives that tile, where the Top-p passes that read these scores
-// run too, so those passes find them in that XCD's L2.
+// Blocks run in key order (tile_place() stream placement over (KV group, Top-p
+// part) tiles), so the GPU streams neighbouring keys at any moment.
 // Ragged batches (RAGGED, seq_n != NULL): sequence b has seq_n[b] indexed keys
 // (clamped to [0, n]; n is the row stride of the scores and bounds the grid).
 // A block reads its sequence's count first and leaves at once when it lies
@@ -85,18 +83,13 @@ __device__ __forceinline__ uint32_t query_dot(const Spread& e, const uint32_t* q
   return binary_int4_dot(e, qn);
 }
 
-// The launch: tiles (KV group, Top-p part) placed by tile_place(), `slots`
-// blocks of kScoreThreads * KPT keys per tile.
-// Scores of a standalone scan (stream placement) are written past the caches;
-// those of a step's scan (group placement) stay in the XCD's L2, where the
-// Top-p passes that run the same tiles read them next.
-// (a compile-time choice: the two stores in one run-time branch get merged into
-// a plain store, dropping the streaming hint)
-template <bool KEEP>
-__device__ __forceinline__ void put_score(float v, float* p) {
-  if constexpr (KEEP) *p = v;
-  else __builtin_nontemporal_store(v, p);
-}
+// The launch: tiles (KV group, Top-p part) in workgroup order (stream
+// placement, so the whole GPU streams neighbouring keys at any moment), `slots`
+// blocks of kScoreThreads * KPT keys per tile. Scores are written past the
+// caches: the selection kernels that read them next fetch them from the memory
+// side in any case (a kernel boundary does not leave them in the L2), and
+// plain stores that keep them there cost the scan their write-back.
+__device__ __forceinline__ void put_score(float v, float* p) { __builtin_nontemporal_store(v, p); }
 struct ScoreGrid {
   TilePlace tp;
   int slots;   // score blocks per part
@@ -107,8 +100,7 @@ struct ScoreGrid {
 // into its low and high nibbles, ip = ip_lo + 16 ip_hi, two dot8 chains).
 // D: head dimension, 128 or 64 (64: the two code words per key and per query
 // plane are padded with zero words, which add nothing to ip or pc).
-// KEEP: the scores stay in L2 (group placement: a step's scan), else they stream past it.
-template <int KPT, bool INTS, bool RAGGED, bool FAC16, int QB = 4, int D = kHeadDim, bool KEEP = false>
+template <int KPT, bool INTS, bool RAGGED, bool FAC16, int QB = 4, int D = kHeadDim>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(
     const uint32_t* __restrict__ codes, const f32x2* __restrict__ kfac, const uint16_t* __restrict__ kfac16,
     const uint32_t* __restrict__ qplanes, const float* __restrict__ qscal, float* __restrict__ scores,
@@ -207,7 +199,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       for (int u = 0; u < KPT; ++u) {
         const int ip = int(query_dot<QB>(e[u], qn));
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
-        put_score<KEEP>(assemble(u, y, B0), out + i0 + u * kScoreThreads);
+        put_score(assemble(u, y, B0), out + i0 + u * kScoreThreads);
       }
     }
     return;
@@ -235,7 +227,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
         // A f X with X = Delta (2 ip - S_u) + q_l (2 pc - D)
         const float y = fmaf(a_delta, float(2 * ip - su), a_ql * float(pcm[u]));
         const float sc = assemble(u, y, B0);
-        if (i < nb) put_score<KEEP>(sc, out + i);
+        if (i < nb) put_score(sc, out + i);
       }
     }
   }
@@ -284,7 +276,7 @@ __device__ __forceinline__ float fsum16(float x, float y) {
 }
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 
-template <int G, int KPT, bool RAGGED, bool FAC16, bool KEEP>
+template <int G, int KPT, bool RAGGED, bool FAC16>
 __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
     const uint32_t* __restrict__ codes, const f32x2* __restrict__ kfac, const uint16_t* __restrict__ kfac16,
     const uint32_t* __restrict__ qplanes, const float* __restrict__ qscal, float* __restrict__ scores, int n,
@@ -452,13 +444,11 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
         }
         float* o = scores + int64_t(row0 + hl0 + t) * n + i4;
         if (whole) {
-          const f32x4 v = {sc[0], sc[1], sc[2], sc[3]};
-          if constexpr (KEEP) *reinterpret_cast<f32x4*>(o) = v;
-          else __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(o));
+          __builtin_nontemporal_store(f32x4{sc[0], sc[1], sc[2], sc[3]}, reinterpret_cast<f32x4*>(o));
         } else {
 #pragma unroll
           for (int m = 0; m < 4; ++m)
-            if (i4 + m < nb) put_score<KEEP>(sc[m], o + m);
+            if (i4 + m < nb) put_score(sc[m], o + m);
         }
       }
     }
@@ -467,14 +457,14 @@ __global__ __launch_bounds__(kScoreThreads) void score_mfma_kernel(
   else body(std::integral_constant<bool, false>{});
 }
 
-template <bool INTS, bool RAGGED, bool FAC16 = false, int QB = 4, int D = kHeadDim, bool KEEP = false>
+template <bool INTS, bool RAGGED, bool FAC16 = false, int QB = 4, int D = kHeadDim>
 rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
                       const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal, float* scores,
                       int32_t* ip_out, int32_t* pc_out, int n, int cap, int Hq, int Hkv, int G, ScoreGrid sg,
                       const int32_t* seq_n) {
   const f32x2* f2 = reinterpret_cast<const f32x2*>(kfac);
 #define RBQ_SCORE_KPT(K)                                                                                    \
-  score_kernel<K, INTS, RAGGED, FAC16, QB, D, KEEP><<<grid, kScoreThreads, 0, stream>>>(                          \
+  score_kernel<K, INTS, RAGGED, FAC16, QB, D><<<grid, kScoreThreads, 0, stream>>>(                          \
       codes, f2, kfac16, qplanes, qscal, scores, ip_out, pc_out, n, cap, Hq, Hkv, G, sg, seq_n)
   switch (kpt) {
     case 4: RBQ_SCORE_KPT(4); break;
@@ -486,13 +476,13 @@ rbq_status launch_kpt(int kpt, dim3 grid, hipStream_t stream, const uint32_t* co
 }
 
 // the matrix-core form (G = 4 or 8)
-template <bool RAGGED, bool FAC16, bool KEEP>
+template <bool RAGGED, bool FAC16>
 rbq_status launch_mfma(int kpt, dim3 grid, hipStream_t stream, const uint32_t* codes, const float* kfac,
                        const uint16_t* kfac16, const uint32_t* qplanes, const float* qscal, float* scores, int n,
                        int cap, int Hq, int Hkv, int G, ScoreGrid sg, const int32_t* seq_n) {
   const f32x2* f2 = reinterpret_cast<const f32x2*>(kfac);
 #define RBQ_MFMA(GG, K)                                                                                   \
-  score_mfma_kernel<GG, K, RAGGED, FAC16, KEEP><<<grid, kScoreThreads, 0, stream>>>(codes, f2, kfac16, qplanes, \
+  score_mfma_kernel<GG, K, RAGGED, FAC16><<<grid, kScoreThreads, 0, stream>>>(codes, f2, kfac16, qplanes, \
                                                                                    qscal, scores, n, cap, Hq,  \
                                                                                    Hkv, sg, seq_n)
   if (G == 8) {
@@ -521,24 +511,11 @@ rbq_status launch_score_d(int kpt, dim3 grid, hipStream_t stream, const uint32_t
   // the matrix-core form where it measured faster: G = 8, and G = 4 at four rounds per wave
   if (D == kHeadDim && (G == 8 || (G == 4 && kpt == 4)) && n % 4 == 0 && cap % 4 == 0) {
     const bool R = seq_n != nullptr, F = kfac16 != nullptr;
-#define RBQ_MFMA_LAUNCH(RR, FF, KK)                                                                         \
-  launch_mfma<RR, FF, KK>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, n, cap, Hq, Hkv, G, sg, \
-                          seq_n)
-    if (sg.tp.mode == kPlaceGroup) {
-      if (R) return F ? RBQ_MFMA_LAUNCH(true, true, true) : RBQ_MFMA_LAUNCH(true, false, true);
-      return F ? RBQ_MFMA_LAUNCH(false, true, true) : RBQ_MFMA_LAUNCH(false, false, true);
-    }
-    if (R) return F ? RBQ_MFMA_LAUNCH(true, true, false) : RBQ_MFMA_LAUNCH(true, false, false);
-    return F ? RBQ_MFMA_LAUNCH(false, true, false) : RBQ_MFMA_LAUNCH(false, false, false);
+#define RBQ_MFMA_LAUNCH(RR, FF)                                                                               \
+  launch_mfma<RR, FF>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, n, cap, Hq, Hkv, G, sg, seq_n)
+    if (R) return F ? RBQ_MFMA_LAUNCH(true, true) : RBQ_MFMA_LAUNCH(true, false);
+    return F ? RBQ_MFMA_LAUNCH(false, true) : RBQ_MFMA_LAUNCH(false, false);
 #undef RBQ_MFMA_LAUNCH
-  }
-  if (sg.tp.mode == kPlaceGroup) {   // a step's scan: the scores stay in L2 for the Top-p passes
-#define RBQ_SCORE_KEEP(R, F)                                                                                      \
-  launch_kpt<false, R, F, 4, D, true>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, ip_out, pc_out, \
-                                      n, cap, Hq, Hkv, G, sg, seq_n)
-    if (seq_n != nullptr) return kfac16 != nullptr ? RBQ_SCORE_KEEP(true, true) : RBQ_SCORE_KEEP(true, false);
-    return kfac16 != nullptr ? RBQ_SCORE_KEEP(false, true) : RBQ_SCORE_KEEP(false, false);
-#undef RBQ_SCORE_KEEP
   }
   if (seq_n != nullptr)
     return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, true, true, 4) : RBQ_SCORE_LAUNCH(false, true, false, 4);
@@ -551,13 +528,13 @@ rbq_status launch_score_d(int kpt, dim3 grid, hipStream_t stream, const uint32_t
 rbq_status launch_score(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t n, int32_t cap,
                         const uint32_t* codes, const float* kfac, const uint32_t* qplanes, const float* qscal,
                         float* scores, int32_t* ip_out, int32_t* pc_out, hipStream_t stream, const int32_t* seq_n,
-                        const uint16_t* kfac16, int32_t planes, int32_t head_dim, int32_t place) {
+                        const uint16_t* kfac16, int32_t planes, int32_t head_dim) {
   if (n == 0) return RBQ_OK;
   const int G = heads_q / heads_kv;
   const int kpt = score_keys_per_lane(batch, heads_kv, n);
   const ToppPlan pl = topp_plan(n);
   ScoreGrid sg;
-  sg.tp = tile_place(batch * heads_kv, pl.parts, place);
+  sg.tp = tile_place(batch * heads_kv, pl.parts, kPlaceStream);
   sg.slots = pl.spb * kSelSub / (kScoreThreads * kpt);
   const int64_t blocks = tile_grid(sg.tp, sg.slots);
   if (blocks * kScoreThreads >= (int64_t(1) << 32)) return RBQ_EUNSUPPORTED;   // beyond one launch's grid

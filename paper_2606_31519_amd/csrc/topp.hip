@@ -39,10 +39,9 @@
 //            its keys >= K* in ascending order at the offset given by the
 //            selected counts of the parts before it (above-b1 counts plus
 //            candidates >= K*).
-// Every pass reads the row's scores; all three and the score scan that wrote
-// them run the work of (KV group, part) on the same XCD (tile_place), so the
-// scores, and with at least 8 KV groups every per-part record of a row, are
-// read from that XCD's L2.
+// Every pass reads the row's scores (from the memory side: a kernel boundary
+// does not leave them in the L2). The parts of a row run on one XCD
+// (tile_place, one row per tile group).
 //
 // Ragged batches (seq_n / seq_p != NULL): row r of sequence b = r / Hq has
 // seq_n[b] keys (clamped to [0, n]; n stays the row stride and sizes the grid)
@@ -867,8 +866,8 @@ void sel_passes(int rows, int group, hipStream_t stream, int n, const ToppPlan& 
 }  // namespace
 
 rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, float sm_scale, int32_t* sel_idx,
-                       int32_t* sel_count, void* ws, hipStream_t stream, int32_t group,
-                       unsigned long long* masks, const int32_t* seq_n, const float* seq_p, int32_t heads_q) {
+                       int32_t* sel_count, void* ws, hipStream_t stream, unsigned long long* masks,
+                       const int32_t* seq_n, const float* seq_p, int32_t heads_q) {
   const int mask_words = topp_mask_words(n);
   const bool ragged = seq_n != nullptr || seq_p != nullptr;   // per-row counts / p: decided on the device
   if (n == 0 || (p >= 1.0f && !ragged)) {
@@ -878,12 +877,11 @@ rbq_status launch_topp(int32_t rows, int32_t n, const float* scores, float p, fl
     topp_all_kernel<<<grid, kAllThreads, 0, stream>>>(n, sel_idx, sel_count, masks, mask_words);
     return hipGetLastError() == hipSuccess ? RBQ_OK : RBQ_EDEVICE;
   }
-  if (group < 1 || rows % group != 0) group = 1;
   const ToppPlan pl = topp_plan(n);
   const ToppWorkspace w = topp_workspace(ws, rows, n);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
 #define RBQ_SEL_PASSES(RG, MU)                                                                                  \
-  sel_passes<RG, MU>(rows, group, stream, n, pl, scores, p, scale_log2e, w, sel_idx, sel_count, masks, mask_words, \
+  sel_passes<RG, MU>(rows, 1, stream, n, pl, scores, p, scale_log2e, w, sel_idx, sel_count, masks, mask_words, \
                      RG ? seq_n : nullptr, RG ? seq_p : nullptr, heads_q)
   if (ragged) {
     if (pl.spb > 1) RBQ_SEL_PASSES(true, true); else RBQ_SEL_PASSES(true, false);
