@@ -297,7 +297,7 @@ def time_scan_c5(pipeline, torch, st, steps, warmup, replicas=4):
     del g
     nbytes16 = B * Hkv * n * (D // 8 + 2) + B * Hq * n * 4
     gbs16 = nbytes16 / (ms16 * 1e-3) / 1e9
-    return {"workload": "gqa 64q/8kv ctx=128K b=4 bf16 student-t", "kernel": "score_kernel",
+    return {"workload": "gqa 64q/8kv ctx=128K b=4 bf16 student-t", "kernel": "score_mfma_kernel",
             "ms": ms, "keys_per_s": B * Hq * n / (ms * 1e-3), "kv_keys_per_s": B * Hkv * n / (ms * 1e-3),
             "bytes": nbytes, "GBps": gbs, "frac_hbm": gbs / HBM_PEAK_GBS,
             "traffic": _measured_traffic(SCAN_TRAFFIC_FILE, SCORE_SRC, "score_source_sha256"),
@@ -939,7 +939,7 @@ def main():
     cnt = st0.sel_count.cpu().numpy()
     keys_scored = st0.B * st0.Hq * st0.n
     if scan is not None:   # the scan's own roofline (the other half of the headline metric)
-        roofline["scan"] = {"kernel": "score_kernel", "workload": scan["workload"], "bound": "hbm",
+        roofline["scan"] = {"kernel": "score_mfma_kernel", "workload": scan["workload"], "bound": "hbm",
                             "achieved": scan["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                             "frac": scan["frac_hbm"], "traffic": scan["traffic"],
                             "algorithmic_bytes_per_launch": float(scan["bytes"]), "ms_per_launch": scan["ms"],
