@@ -47,7 +47,8 @@ def _two_forms(R, st, n, compact, seq_n=None):
         S = torch.full((B, Hq, m), float("nan"), device="cuda")
         if seq_n is not None:
             sn = torch.tensor([min(s, m) for s in seq_n], dtype=torch.int32, device="cuda")
-            R.rbq_score_varlen(B, Hq, Hkv, 128, m, st.cap, sn, st.codes, fac, st.qplanes, st.qscal, S)
+            call = R.rbq_score_varlen_f16 if compact else R.rbq_score_varlen
+            call(B, Hq, Hkv, 128, m, st.cap, sn, st.codes, fac, st.qplanes, st.qscal, S)
         elif compact:
             R.rbq_score_f16(B, Hq, Hkv, 128, m, st.cap, st.codes, fac, st.qplanes, st.qscal, S)
         else:
@@ -84,23 +85,31 @@ def test_matrix_core_scan_is_bitwise_the_dot8_scan(R, pipeline, B, Hq, Hkv, n, c
         pu.check_scores(S4[b, h, :n], codes[b, h // G, :n], fac, planes[b, h], qs[b, h])
 
 
-def test_matrix_core_scan_ragged(R, pipeline):
-    B, Hq, Hkv, n = 4, 64, 8, 5000
-    seq = [n - 1, 1234, 0, 7]
-    print("score forms ragged", seq, flush=True)
-    wl = gen.random_case(B, Hq, Hkv, n, seed=91, kv_dtype="bf16", c_q_scale=0.0, key_offset=1.0)
-    st = pipeline.DecodeState.from_workload(wl, c_q=False)
+@pytest.mark.parametrize("B,Hq,Hkv,n,seq,compact", [
+    (4, 64, 8, 5000, [4999, 1234, 0, 7], False),                        # G = 8, one round per wave
+    (4, 64, 8, 5000, [4999, 1234, 0, 7], True),                         # compact index
+    (16, 32, 8, 16384, [16383, 9000, 0, 4097, 1, 16000, 777, 12345,     # G = 4, four rounds per wave
+                        16383, 3, 8191, 8192, 100, 15000, 2048, 64], False),
+])
+def test_matrix_core_scan_ragged(R, pipeline, B, Hq, Hkv, n, seq, compact):
+    print("score forms ragged", B, Hq, Hkv, n, "compact" if compact else "full", flush=True)
+    wl = gen.random_case(B, Hq, Hkv, n, seed=91 + B, kv_dtype="bf16", c_q_scale=0.0, key_offset=1.0)
+    st = pipeline.DecodeState.from_workload(wl, c_q=False, compact=compact)
     st.build_index()
     st.quantize()
-    S4, S3 = _two_forms(R, st, n, False, seq_n=seq)
-    codes, kfac, planes, qs = pu.u32(st.codes), _np(st.kfac), pu.u32(st.qplanes), _np(st.qscal)
+    S4, S3 = _two_forms(R, st, n, compact, seq_n=seq)
+    codes, planes, qs = pu.u32(st.codes), pu.u32(st.qplanes), _np(st.qscal)
     G = Hq // Hkv
     for b in range(B):
         m = seq[b]   # entries past a sequence's count are unspecified
         assert np.array_equal(S4[b, :, :m].view(np.uint32), S3[b, :, :m].view(np.uint32))
-        if m:
+        if m and b < 4:
             for h in (0, Hq - 1):
-                pu.check_scores(S4[b, h, :m], codes[b, h // G, :m], kfac[b, h // G, :m], planes[b, h], qs[b, h])
+                if compact:
+                    fac = np.stack([_np(st.kfac16)[b, h // G, :m].astype(np.float64), np.zeros(m)], axis=1)
+                else:
+                    fac = _np(st.kfac)[b, h // G, :m]
+                pu.check_scores(S4[b, h, :m], codes[b, h // G, :m], fac, planes[b, h], qs[b, h])
 
 
 def test_matrix_core_scan_integers_are_exact(R, pipeline):
