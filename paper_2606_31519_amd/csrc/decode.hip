@@ -96,18 +96,29 @@ __device__ __forceinline__ void wave_lower_bounds(const int32_t* __restrict__ a,
   r1 = lo1;
 }
 
-// This thread's word of the split's selection bitmaps (thread t < G * 16: head
-// t / 16, 64-key word t % 16); for small groups it is requested at the start
-// of the kernel so that the load overlaps the query staging.
+// This lane's words of the split's selection bitmaps: word l % 16 (keys
+// c0 + 64 (l % 16) .. + 64) of heads l / 16 + 4k. Every wave of the block reads
+// the same words; for small groups they are requested at the start of the
+// kernel so that the loads overlap the query staging. (Bits past the split's
+// last position are cleared where the words are used, so that no wait for the
+// loads is placed here.)
 template <int G>
-__device__ __forceinline__ unsigned long long load_mask_word(const unsigned long long* __restrict__ sel_mask,
-                                                             int mask_words, int row0, int c0, int c1) {
-  constexpr int kMw = kBmWords / 2;   // 64-key words per split
-  static_assert(G * kMw <= kDThreads, "one word per thread");
-  const int t = threadIdx.x;
-  if (sel_mask == nullptr || t >= G * kMw) return 0ull;
-  const int g = t / kMw, wd = t % kMw;
-  return c0 + 64 * wd < c1 ? sel_mask[int64_t(row0 + g) * mask_words + c0 / 64 + wd] : 0ull;
+struct MaskWords {
+  unsigned long long w[(G + 3) / 4];
+};
+template <int G>
+__device__ __forceinline__ MaskWords<G> load_mask_words(const unsigned long long* __restrict__ sel_mask,
+                                                        int mask_words, int row0, int c0, int c1) {
+  MaskWords<G> m;
+  const int lane = lane_id(), wd = lane & 15;
+#pragma unroll
+  for (int k = 0; k < (G + 3) / 4; ++k) {
+    const int g = lane / 16 + 4 * k;
+    m.w[k] = sel_mask != nullptr && g < G && c0 + 64 * wd < c1
+                 ? sel_mask[int64_t(row0 + g) * mask_words + c0 / 64 + wd]
+                 : 0ull;
+  }
+  return m;
 }
 
 // Per-block row list of a sparse split: the union over the G heads of the
@@ -127,21 +138,57 @@ __device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32
                                 const unsigned long long* __restrict__ sel_mask, int mask_words, int row0,
                                 int n, int c0, int c1, int nwin, int wshift, uint32_t (*bm)[kBmAll], int32_t* lst,
                                 uint16_t* hmask, int* rng_lo, int* rng_hi, int* wcnt, int* ucount,
-                                unsigned long long mword) {
+                                MaskWords<G> mw) {
   constexpr int kWaves = kThreads / kWave;
   const int t = threadIdx.x, wave = t / kWave, lane = lane_id();
-  if (sel_mask) {   // mword: this thread's word, from load_mask_word (when preloaded)
-    constexpr int kMw = kBmWords / 2;
-    static_assert(kThreads == kDThreads, "load_mask_word assigns the words");
-    if (!PRE) mword = load_mask_word<G>(sel_mask, mask_words, row0, c0, c1);
-    if (t < G * kMw) {
-      const int g = t / kMw, wd = t % kMw;
-      bm[g][2 * wd] = uint32_t(mword);
-      bm[g][2 * wd + 1] = uint32_t(mword >> 32);
+  if (sel_mask) {
+    // Every wave ranks the split's 16 union words itself (no LDS bitmaps): lane l
+    // holds word l % 16 of heads l / 16 + 4k (mw, from load_mask_words when
+    // preloaded), the heads' words are ORed across the rows of 16 lanes, and an
+    // exclusive prefix of their popcounts gives each word's first list entry.
+    // Wave v then writes the entries of words v, v + kWaves, ... and the last
+    // wave the folded window rows; one barrier publishes the list.
+    if (!PRE) mw = load_mask_words<G>(sel_mask, mask_words, row0, c0, c1);
+    const int wd = lane & 15;
+    const int lim = c1 - c0 - 64 * wd;   // positions of word wd inside the split
+    const unsigned long long keep = lim >= 64 ? ~0ull : lim > 0 ? (1ull << lim) - 1ull : 0ull;
+    unsigned long long u = 0ull;
+#pragma unroll
+    for (int k = 0; k < (G + 3) / 4; ++k) {
+      mw.w[k] &= keep;
+      u |= mw.w[k];
     }
-    constexpr int kExtra = kBmAll - kBmWords;   // the folded window's words
-    for (int e = t; e < G * kExtra; e += kThreads) bm[e / kExtra][kBmWords + e % kExtra] = 0u;
+    u |= swap16_u64(u);   // lanes l and l ^ 16
+    u |= (uint64_t(uint32_t(__shfl_xor(int(uint32_t(u >> 32)), 32, kWave))) << 32) |
+         uint32_t(__shfl_xor(int(uint32_t(u)), 32, kWave));
+    const uint32_t c = uint32_t(__popcll(u));
+    uint32_t inc = c;   // inclusive prefix over the 16 words of each row of lanes
+    inc += RBQ_DPP_U32(inc, 0x111);   // row_shr:1
+    inc += RBQ_DPP_U32(inc, 0x112);   // row_shr:2
+    inc += RBQ_DPP_U32(inc, 0x114);   // row_shr:4
+    inc += RBQ_DPP_U32(inc, 0x118);   // row_shr:8
+    const uint32_t excl = inc - c;
+    const int nidx = __builtin_amdgcn_readlane(int(inc), 15);
+    for (int v = wave; v < kBmWords / 2; v += kWaves) {   // (wave-uniform)
+      const unsigned long long uw = readlane_u64(u, v);
+      const int off = __builtin_amdgcn_readlane(int(excl), v);
+      uint32_t mk = 0u;
+#pragma unroll
+      for (int g = 0; g < G; ++g) mk |= uint32_t((readlane_u64(mw.w[g / 4], (g % 4) * 16 + v) >> lane) & 1ull) << g;
+      if ((uw >> lane) & 1ull) {
+        const int o = off + int(__builtin_amdgcn_mbcnt_hi(uint32_t(uw >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(uw), 0u)));
+        lst[o] = c0 + 64 * v + lane;
+        hmask[o] = uint16_t(mk);
+      }
+    }
+    if (wave == kWaves - 1) {
+      for (int i = lane; i < nwin; i += kWave) {   // the folded window rows, every head
+        lst[nidx + i] = c1 + wshift + i;
+        hmask[nidx + i] = uint16_t((1u << G) - 1u);
+      }
+    }
     __syncthreads();
+    return nidx + nwin;
   } else {
   for (int g = wave; g < G; g += kWaves) {
     const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
@@ -355,8 +402,8 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
                              : static_cast<const char*>(V) + int64_t(bh) * cap * D * kElem;
 
   constexpr bool kPreMask = G <= 4;   // (for larger groups the early load costs registers)
-  const unsigned long long mword =
-      kPreMask && SPARSE && !window ? load_mask_word<G>(sel_mask, mask_words, row0, c0, c1) : 0ull;
+  MaskWords<G> mword{};
+  if (kPreMask && SPARSE && !window) mword = load_mask_words<G>(sel_mask, mask_words, row0, c0, c1);
   for (int e = threadIdx.x; e < G * D; e += kDThreads)
     qs[e / D][e % D] = q[int64_t(row0) * D + e] * scale_log2e;
 
@@ -614,8 +661,8 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   const __amdgpu_buffer_rsrc_t Kr = make_rsrc(Kb, region);
   const __amdgpu_buffer_rsrc_t Vr = make_rsrc(Vb, region);
   constexpr bool kPreMask = kPackedQ;   // (for larger groups the early load costs registers)
-  const unsigned long long mword =
-      kPreMask && SPARSE && !window ? load_mask_word<G>(sel_mask, mask_words, row0, c0, c1) : 0ull;
+  MaskWords<G> mword{};
+  if (kPreMask && SPARSE && !window) mword = load_mask_words<G>(sel_mask, mask_words, row0, c0, c1);
 
   // query operands, lane (column c, quarter jj) of k-block kb = dims 32 kb + 8 jj .. +8.
   // G <= 4: one operand per k-block, column c = part * G + head; otherwise one
