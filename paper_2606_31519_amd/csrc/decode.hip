@@ -134,7 +134,7 @@ __device__ __forceinline__ MaskWords<G> load_mask_words(const unsigned long long
 // With selection bitmaps (sel_mask != NULL, [rows][mask_words] words of 64
 // keys, c0 a multiple of 64) the per-head bitmaps are loaded directly instead.
 template <int G, int kThreads, bool PRE>
-__device__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
+__device__ __forceinline__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
                                 const unsigned long long* __restrict__ sel_mask, int mask_words, int row0,
                                 int n, int c0, int c1, int nwin, int wshift, uint32_t (*bm)[kBmAll], int32_t* lst,
                                 uint16_t* hmask, int* rng_lo, int* rng_hi, int* wcnt, int* ucount,
