@@ -20,8 +20,8 @@
 // kernel streams codes + factors once (24 B per KV key, non-temporal) and
 // writes 4 B per (key, head) with non-temporal stores. Blocks that lie wholly inside [0, n) take a path
 // without per-key guards. The scan is HBM-bound at G = 4 and at G = 8.
-// At G = 8 (and at G = 4 with four 64-key rounds per wave) the integer part
-// runs on the matrix cores instead (score_mfma_kernel: one mixed e4m3 x e2m1
+// At G = 8, and at G = 4 with two or four 64-key rounds per wave, the integer
+// part runs on the matrix cores instead (score_mfma_kernel: one mixed e4m3 x e2m1
 // product per 16 keys and all heads), which halves the vector-ALU work per key;
 // the integers, and so the scores, are bitwise those of the dot8 form.
 // Blocks run in key order (tile_place() stream placement over (KV group, Top-p
@@ -508,8 +508,8 @@ rbq_status launch_score_d(int kpt, dim3 grid, hipStream_t stream, const uint32_t
     return kfac16 != nullptr ? RBQ_SCORE_LAUNCH(false, false, true, 8) : RBQ_SCORE_LAUNCH(false, false, false, 8);
   }
   if (ip_out != nullptr) return RBQ_SCORE_LAUNCH(true, false, false, 4);   // (the integer hook is never ragged)
-  // the matrix-core form where it measured faster: G = 8, and G = 4 at four rounds per wave
-  if (D == kHeadDim && (G == 8 || (G == 4 && kpt == 4)) && n % 4 == 0 && cap % 4 == 0) {
+  // the matrix-core form where it measured faster: G = 8, and G = 4 at two or four rounds per wave
+  if (D == kHeadDim && (G == 8 || (G == 4 && kpt >= 2)) && n % 4 == 0 && cap % 4 == 0) {
     const bool R = seq_n != nullptr, F = kfac16 != nullptr;
 #define RBQ_MFMA_LAUNCH(RR, FF)                                                                               \
   launch_mfma<RR, FF>(kpt, grid, stream, codes, kfac, kfac16, qplanes, qscal, scores, n, cap, Hq, Hkv, G, sg, seq_n)

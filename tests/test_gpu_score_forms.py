@@ -2,8 +2,8 @@
 
 The scan computes the integer part ip = sum_d bit_d q_d either with v_dot8
 (one lane per key) or on the matrix cores (one e4m3 x e2m1 product per 16 keys,
-taken at G = 8, at G = 4 with four 64-key rounds per wave, when n and cap are
-multiples of 4). Each key's score depends on its own code, factors and query
+taken at G = 8, and at G = 4 with two or four 64-key rounds per wave, when n
+and cap are multiples of 4). Each key's score depends on its own code, factors and query
 only, so a call over n keys (matrix-core form) and one over n - 1 keys (n - 1
 not a multiple of 4: the dot8 form) must give the same bits for the first
 n - 1 keys. The matrix-core results are also checked against the oracle's
@@ -62,7 +62,9 @@ def _two_forms(R, st, n, compact, seq_n=None):
     (2, 64, 8, 3000, False),     # G = 8, one round per wave, ragged block tails
     (4, 64, 8, 65536, False),    # G = 8, four rounds per wave
     (16, 32, 8, 16384, False),   # G = 4, four rounds per wave
+    (1, 32, 8, 65536, False),    # G = 4, two rounds per wave (the shape of the 128K step's scan)
     (2, 64, 8, 3000, True),      # compact index (fp16 factor)
+    (1, 32, 8, 65536, True),
     (4, 64, 8, 65536, True),
 ])
 def test_matrix_core_scan_is_bitwise_the_dot8_scan(R, pipeline, B, Hq, Hkv, n, compact):
