@@ -5,9 +5,10 @@
 // indexed positions (or of window rows) for all G query heads of the KV group.
 // For the sparse call it finds each head's part of its ascending selection list
 // (a 64-way search per wave: three dependent loads for 128K entries), marks the
-// selected positions in per-head LDS bitmaps and compacts their union: every
-// K/V row selected by any head of the group is gathered from HBM once and used
-// by the heads that selected it (a per-entry head mask keeps each head's
+// selected positions in per-head LDS bitmaps and compacts their union (or,
+// given the selection's bitmaps, ranks the chunk's union words in every wave):
+// every K/V row selected by any head of the group is gathered from HBM once and
+// used by the heads that selected it (a per-entry head mask keeps each head's
 // softmax over its own set only).
 //
 // bf16 K/V (decode_mfma_kernel): each wave takes groups of 16 gathered rows and
@@ -132,7 +133,8 @@ __device__ __forceinline__ MaskWords<G> load_mask_words(const unsigned long long
 // in per-head LDS bitmaps, and the union is compacted with wave ballots.
 //
 // With selection bitmaps (sel_mask != NULL, [rows][mask_words] words of 64
-// keys, c0 a multiple of 64) the per-head bitmaps are loaded directly instead.
+// keys, c0 a multiple of 64) the list is built from the words themselves,
+// without the searches, the LDS bitmaps and their compaction (below).
 template <int G, int kThreads, bool PRE>
 __device__ __forceinline__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
                                 const unsigned long long* __restrict__ sel_mask, int mask_words, int row0,
