@@ -552,8 +552,12 @@ struct GroupLoads {
 // Loads go through buffer resources over the (sequence, KV head)'s rows: a
 // load that has nothing to fetch (no next group) gets an offset past the end
 // and is dropped by the hardware, so every path issues the same instructions
-// and the compiler's wait counts stay exact.
+// and the compiler's wait counts stay exact. Each K / V row is read once per
+// call, so the loads carry the non-temporal policy: allocated normally, the
+// gathered rows displace the lines that are read again (the scores, the index,
+// the partial states) from the L2 and the Infinity Cache.
 constexpr int kSkipOffset = 0x7FFFFF00;
+constexpr int kStream = 2;   // cache-policy bits of the K / V buffer loads: nt
 
 template <bool SPARSE>
 __device__ __forceinline__ int row_at(int e, bool list, const RowMap& rm, const int32_t* lst) {
@@ -572,7 +576,7 @@ __device__ __forceinline__ void load_group_k(GroupLoads<D>& d, int grp, bool ski
   const int pk = row_at<SPARSE>(ek, list, rm, lst);
   const int off = skip ? kSkipOffset : pk * (D * 2) + 16 * j;
 #pragma unroll
-  for (int kb = 0; kb < D / 32; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 64 * kb, 0, 0);
+  for (int kb = 0; kb < D / 32; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 64 * kb, 0, kStream);
 }
 
 template <bool SPARSE, int G, int D>
@@ -589,9 +593,9 @@ __device__ __forceinline__ void load_group_v(GroupLoads<D>& d, int grp, bool ski
     const int pv = row_at<SPARSE>(ev, list, rm, lst);
     const int off = skip ? kSkipOffset : pv * (D * 2) + (D / 8) * x;
     if constexpr (D == 64)
-      d.v[i] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(Vr, off, 0, 0));
+      d.v[i] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(Vr, off, 0, kStream));
     else
-      d.v[i] = __builtin_amdgcn_raw_buffer_load_b128(Vr, off, 0, 0);
+      d.v[i] = __builtin_amdgcn_raw_buffer_load_b128(Vr, off, 0, kStream);
     bool on = valid && x < G;
     if constexpr (SPARSE) on = on & (!list | bool((hmask[ev] >> x) & 1u));
     mk |= uint32_t(on) << i;
