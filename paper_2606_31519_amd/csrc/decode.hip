@@ -37,6 +37,7 @@
 // and launched split-major; a sequence's window is spread over its own splits,
 // and a split past its rows writes an empty partial state and leaves.
 #include <cmath>
+#include <type_traits>
 
 #include "rbq_device.h"
 #include "rbq_internal.h"
@@ -553,11 +554,18 @@ struct GroupLoads {
 // load that has nothing to fetch (no next group) gets an offset past the end
 // and is dropped by the hardware, so every path issues the same instructions
 // and the compiler's wait counts stay exact. Each K / V row is read once per
-// call, so the loads carry the non-temporal policy: allocated normally, the
-// gathered rows displace the lines that are read again (the scores, the index,
-// the partial states) from the L2 and the Infinity Cache.
+// call. Where the gather is bound by bandwidth -- the dense call, and sparse
+// blocks of groups of at most 4 query heads whose rows cover at least a third
+// of their positions -- the loads carry the non-temporal policy: allocated
+// normally, the gathered rows displace the lines that are read again (the
+// scores, the index, the partial states) from the L2 and the Infinity Cache
+// (128K, 32 / 8 heads: the sparse call at p = 0.95 and the dense call ~12 %
+// faster). Sparser blocks, and groups of 8 or 16 heads (three products per
+// 16 rows for the logits instead of one), are bound by latency and compute;
+// there the policy measured slower.
 constexpr int kSkipOffset = 0x7FFFFF00;
 constexpr int kStream = 2;   // cache-policy bits of the K / V buffer loads: nt
+constexpr int kStreamDenNum = 1, kStreamDenDen = 3;   // a third of the block's positions
 
 template <bool SPARSE>
 __device__ __forceinline__ int row_at(int e, bool list, const RowMap& rm, const int32_t* lst) {
@@ -568,7 +576,7 @@ __device__ __forceinline__ int row_at(int e, bool list, const RowMap& rm, const 
   return rm.at(e);
 }
 
-template <bool SPARSE, int D>
+template <bool SPARSE, int D, int CP>
 __device__ __forceinline__ void load_group_k(GroupLoads<D>& d, int grp, bool skip, int U, const RowMap& rm, bool list,
                                              const int32_t* lst, __amdgpu_buffer_rsrc_t Kr, int x, int j) {
   const int e0 = grp * kGroupRows;
@@ -576,10 +584,10 @@ __device__ __forceinline__ void load_group_k(GroupLoads<D>& d, int grp, bool ski
   const int pk = row_at<SPARSE>(ek, list, rm, lst);
   const int off = skip ? kSkipOffset : pk * (D * 2) + 16 * j;
 #pragma unroll
-  for (int kb = 0; kb < D / 32; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 64 * kb, 0, kStream);
+  for (int kb = 0; kb < D / 32; ++kb) d.k[kb] = __builtin_amdgcn_raw_buffer_load_b128(Kr, off + 64 * kb, 0, CP);
 }
 
-template <bool SPARSE, int G, int D>
+template <bool SPARSE, int G, int D, int CP>
 __device__ __forceinline__ void load_group_v(GroupLoads<D>& d, int grp, bool skip, int U, const RowMap& rm, bool list,
                                              const int32_t* lst, const uint16_t* hmask,
                                              __amdgpu_buffer_rsrc_t Vr, int x, int j) {
@@ -593,9 +601,9 @@ __device__ __forceinline__ void load_group_v(GroupLoads<D>& d, int grp, bool ski
     const int pv = row_at<SPARSE>(ev, list, rm, lst);
     const int off = skip ? kSkipOffset : pv * (D * 2) + (D / 8) * x;
     if constexpr (D == 64)
-      d.v[i] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(Vr, off, 0, kStream));
+      d.v[i] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(Vr, off, 0, CP));
     else
-      d.v[i] = __builtin_amdgcn_raw_buffer_load_b128(Vr, off, 0, kStream);
+      d.v[i] = __builtin_amdgcn_raw_buffer_load_b128(Vr, off, 0, CP);
     bool on = valid && x < G;
     if constexpr (SPARSE) on = on & (!list | bool((hmask[ev] >> x) & 1u));
     mk |= uint32_t(on) << i;
@@ -719,13 +727,18 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   for (int t = 0; t < VB; ++t) acc[t][0] = acc[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int ngroups = (U + kGroupRows - 1) / kGroupRows;
+  // the loads' cache policy (block-uniform): streaming where the gather is bound by bandwidth
+  const bool stream =
+      !SPARSE || (G <= 4 && int64_t(U) * kStreamDenDen >= int64_t(c1 - c0 + nwin) * kStreamDenNum);
+  auto gather = [&](auto cp_tag) {
+  constexpr int CP = decltype(cp_tag)::value;
   // One group's registers are reused for the next: its K rows are requested
   // as soon as the logits are done, its V rows as soon as the values are.
   GroupLoads<D> cur;
   int grp = wave;
   if (grp < ngroups) {
-    load_group_k<SPARSE, D>(cur, grp, false, U, rm, list, lst, Kr, x, j);
-    load_group_v<SPARSE, G, D>(cur, grp, false, U, rm, list, lst, hmask, Vr, x, j);
+    load_group_k<SPARSE, D, CP>(cur, grp, false, U, rm, list, lst, Kr, x, j);
+    load_group_v<SPARSE, G, D, CP>(cur, grp, false, U, rm, list, lst, hmask, Vr, x, j);
   }
   while (grp < ngroups) {
     const int nxt = grp + kDWaves;
@@ -745,7 +758,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
         s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, qp[(kb * kQOps + op) * kWave]), s,
                                                     0, 0, 0);
     }
-    load_group_k<SPARSE, D>(cur, last ? grp : nxt, last, U, rm, list, lst, Kr, x, j);
+    load_group_k<SPARSE, D, CP>(cur, last ? grp : nxt, last, U, rm, list, lst, Kr, x, j);
     if constexpr (kPackedQ) {
       // column h + G and h + 2G hold the mid and lo parts of head h's logits
       // (each element goes through an opaque copy first: hipcc 7.2 miscompiles
@@ -818,9 +831,12 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
         acc[t][par] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a_lo, bv, acc[t][par], 0, 0, 0);
       }
     }
-    load_group_v<SPARSE, G, D>(cur, last ? grp : nxt, last, U, rm, list, lst, hmask, Vr, x, j);
+    load_group_v<SPARSE, G, D, CP>(cur, last ? grp : nxt, last, U, rm, list, lst, hmask, Vr, x, j);
     grp = nxt;
   }
+  };
+  if (stream) gather(std::integral_constant<int, kStream>{});
+  else gather(std::integral_constant<int, 0>{});
 
   // ---- merge the waves, write this split's partial state per head
   lsum += __shfl_xor(lsum, 16, kWave);
