@@ -18,12 +18,6 @@
  *   rbq_score_ints: ip_out [B][Hq][n] int32 = <c_b, q_u>, pc_out [B][Hkv][n]
  *     int32 = popcount(c_b), computed by the score kernel's integer path;
  *     rbq_score_ints_q8 the same from 8-plane queries (rbq_score_q8's path).
- *   rbq_sparse_decode_debug: as rbq_sparse_decode, but the row lists of the
- *     attention are always built from the index lists (a search of each head's
- *     list per split) instead of from the selection bitmaps that
- *     rbq_sparse_decode builds first for rows of up to 2^20 keys; the two must
- *     agree bitwise. ws: rbq_workspace_bytes(RBQ_OP_DENSE_DECODE, ...) bytes
- *     suffice.
  */
 #ifndef RBQ_TESTING_H
 #define RBQ_TESTING_H
@@ -48,12 +42,6 @@ rbq_status rbq_quantize_query_debug(int32_t batch, int32_t heads_q, int32_t head
 rbq_status rbq_score_ints(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
                           int32_t n, int32_t cap, const uint32_t* codes, const uint32_t* qplanes,
                           int32_t* ip_out, int32_t* pc_out, hipStream_t stream);
-rbq_status rbq_sparse_decode_debug(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
-                                   const float* q, const void* K, const void* V, int32_t kv_dtype,
-                                   int32_t cap, int32_t n, const int32_t* sel_idx, const int32_t* sel_count,
-                                   const void* K_loc, const void* V_loc, int64_t loc_ld, int32_t w,
-                                   float sm_scale, float* out, float* lse, void* ws, size_t ws_bytes,
-                                   hipStream_t stream);
 rbq_status rbq_score_ints_q8(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim,
                              int32_t n, int32_t cap, const uint32_t* codes, const uint32_t* qplanes8,
                              int32_t* ip_out, int32_t* pc_out, hipStream_t stream);

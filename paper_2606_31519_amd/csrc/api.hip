@@ -215,22 +215,10 @@ rbq_status rbq_sparse_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, i
                              int64_t loc_ld, int32_t w, float sm_scale, float* out, float* lse, void* ws,
                              size_t ws_bytes, hipStream_t stream) {
   const rbq_status s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, true, sel_idx,
-                                    sel_count, K_loc, V_loc, loc_ld, w, sm_scale, out, ws, ws_bytes, true);
-  if (s != RBQ_OK) return s;
-  return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, loc_ld,
-                       w, sm_scale, out, lse, ws, true, stream, nullptr, 0, nullptr, nullptr, head_dim);
-}
-
-rbq_status rbq_sparse_decode_debug(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
-                                   const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n,
-                                   const int32_t* sel_idx, const int32_t* sel_count, const void* K_loc,
-                                   const void* V_loc, int64_t loc_ld, int32_t w, float sm_scale, float* out,
-                                   float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
-  const rbq_status s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, true, sel_idx,
                                     sel_count, K_loc, V_loc, loc_ld, w, sm_scale, out, ws, ws_bytes);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K_loc, V_loc, loc_ld,
-                       w, sm_scale, out, lse, ws, true, stream, nullptr, 0, nullptr, nullptr, head_dim, true);
+                       w, sm_scale, out, lse, ws, true, stream, nullptr, 0, nullptr, nullptr, head_dim);
 }
 
 rbq_status rbq_dense_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
@@ -303,7 +291,7 @@ rbq_status decode_varlen(int32_t batch, int32_t heads_q, int32_t heads_kv, int32
   rbq_status s = check_ragged(n, w, cap, seq_n, seq_w);
   if (s != RBQ_OK) return s;
   s = check_decode(batch, heads_q, heads_kv, head_dim, q, K, V, kv_dtype, cap, n, sparse, sel_idx, sel_count, K, V,
-                   cap, w, sm_scale, out, ws, ws_bytes, true);
+                   cap, w, sm_scale, out, ws, ws_bytes);
   if (s != RBQ_OK) return s;
   return launch_decode(batch, heads_q, heads_kv, q, K, V, kv_dtype, cap, n, sel_idx, sel_count, K, V, cap, w,
                        sm_scale, out, lse, ws, sparse, stream, nullptr, 0, seq_n, seq_w, head_dim);

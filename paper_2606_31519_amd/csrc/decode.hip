@@ -938,39 +938,6 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(const floa
   }
 }
 
-// The selection of each row as bitmaps (bit i of word k: key 64 k + i), from
-// its index list: one block per row ORs the entries into the row's words in
-// LDS and then writes every word, so that the attention builds its row lists
-// from the words, as in the fused step (one pass instead of a search of every
-// head's list per split). Entries outside [0, n) are ignored.
-constexpr int kBmThreads = 1024;
-constexpr int kBmBatch = 16;   // entries per thread in flight
-constexpr int kBmMaxWords = kDecodeBitmapMaxKeys / 64;
-__global__ __launch_bounds__(kBmThreads) void sel_bitmap_kernel(const int32_t* __restrict__ sel_idx,
-                                                                const int32_t* __restrict__ sel_count, int n,
-                                                                int words, unsigned long long* __restrict__ masks) {
-  __shared__ unsigned long long bw[kBmMaxWords];
-  const int row = blockIdx.x, t = threadIdx.x;
-  for (int k = t; k < words; k += kBmThreads) bw[k] = 0ull;
-  const int cnt = min(max(sel_count[row], 0), n);
-  const int32_t* sel = sel_idx + int64_t(row) * n;
-  __syncthreads();
-  for (int e0 = 0; e0 < cnt; e0 += kBmThreads * kBmBatch) {
-    int v[kBmBatch];
-#pragma unroll
-    for (int u = 0; u < kBmBatch; ++u) {
-      const int e = e0 + u * kBmThreads + t;
-      v[u] = e < cnt ? sel[e] : -1;
-    }
-#pragma unroll
-    for (int u = 0; u < kBmBatch; ++u)
-      if (v[u] >= 0 && v[u] < n) atomicOr(&bw[v[u] >> 6], 1ull << (v[u] & 63));
-  }
-  __syncthreads();
-  unsigned long long* out = masks + int64_t(row) * words;
-  for (int k = t; k < words; k += kBmThreads) out[k] = bw[k];
-}
-
 template <int DT, bool SPARSE, bool RAGGED, int D = kHeadDim>
 rbq_status launch_g(int G, dim3 grid, hipStream_t stream, const float* q, const void* K, const void* V, int cap,
                     int n, const int32_t* sel_idx, const int32_t* sel_count, const unsigned long long* sel_mask,
@@ -1009,7 +976,7 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                          const int32_t* sel_count, const void* K_loc, const void* V_loc, int64_t loc_ld, int32_t w,
                          float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream,
                          const unsigned long long* sel_mask, int32_t mask_words, const int32_t* seq_n,
-                         const int32_t* seq_w, int32_t head_dim, bool lists) {
+                         const int32_t* seq_w, int32_t head_dim) {
   const int G = heads_q / heads_kv;
   const int D = head_dim;
   const size_t elem = kv_dtype == RBQ_BF16 ? 2 : 4;
@@ -1030,14 +997,6 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
   const dim3 grid = seq_n ? dim3(batch * heads_kv, sp.total()) : dim3(sp.total(), batch * heads_kv);
   float* part = static_cast<float*>(ws);
   const float scale_log2e = float(double(sm_scale) * 1.4426950408889634);
-  if (sparse && sel_mask == nullptr && !lists && n > 0 && n <= kDecodeBitmapMaxKeys) {
-    // the selection bitmaps, after the partial states in ws
-    auto* bm = reinterpret_cast<unsigned long long*>(static_cast<char*>(ws) +
-                                                     decode_workspace_bytes(batch, heads_q, heads_kv, D, n, w));
-    mask_words = topp_mask_words(n);
-    sel_bitmap_kernel<<<batch * heads_q, kBmThreads, 0, stream>>>(sel_idx, sel_count, n, mask_words, bm);
-    sel_mask = bm;
-  }
   rbq_status st;
 #define RBQ_DECODE_LAUNCH(DT, SP, RG)                                                                              \
   launch_g<DT, SP, RG>(G, grid, stream, q, K, V, cap, n, sel_idx, sel_count, sel_mask, mask_words, K_loc, V_loc, loc_ld, \

@@ -31,7 +31,7 @@ rbq_status check_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
                         const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n, bool sparse,
                         const int32_t* sel_idx, const int32_t* sel_count, const void* K_loc, const void* V_loc,
                         int64_t loc_ld, int32_t w, float sm_scale, const float* out, const void* ws,
-                        size_t ws_bytes, bool bitmaps = false);
+                        size_t ws_bytes);
 
 // ---------------------------------------------------------------- workspace layouts
 // Top-p: each row of scores is cut into parts of spb sub-chunks of kSelSub
@@ -95,11 +95,8 @@ constexpr int kDecodeListCap = 1280;      // row-list positions of a sparse spli
 // by the chunk), provided every sequence's window fits its splits that way.
 DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w, bool tail_window = false,
                            bool sparse = false, bool ragged = false);
-// bitmaps: room for the selection bitmaps a sparse call builds from index
-// lists ([B * Hq][topp_mask_words(n)] words, rows of at most kDecodeBitmapMaxKeys keys)
-constexpr int32_t kDecodeBitmapMaxKeys = int32_t(1) << 20;
 size_t decode_workspace_bytes(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
-                              int32_t w, bool bitmaps = false);
+                              int32_t w);
 
 // Score: blocks of kScoreThreads lanes, 1, 2 or 4 keys per lane.
 constexpr int kScoreThreads = 256;
@@ -203,10 +200,7 @@ rbq_status launch_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, const
                          float sm_scale, float* out, float* lse, void* ws, bool sparse, hipStream_t stream,
                          const unsigned long long* sel_mask = nullptr, int32_t mask_words = 0,
                          const int32_t* seq_n = nullptr, const int32_t* seq_w = nullptr,
-                         int32_t head_dim = kHeadDim, bool lists = false);
-// (a sparse call given index lists and no bitmaps first builds the bitmaps in
-// ws (decode_workspace_bytes(..., true)) for rows of at most
-// kDecodeBitmapMaxKeys keys; lists: keep the index lists (a test hook))
+                         int32_t head_dim = kHeadDim);
 // (ragged: seq_n / seq_w [B] indexed and window rows per sequence, the window
 // being the sequence's cache tail; K_loc, V_loc and loc_ld are then ignored)
 

@@ -143,20 +143,17 @@ DecodeSplits decode_splits(int32_t batch, int32_t heads_kv, int32_t n, int32_t w
 }
 
 size_t decode_workspace_bytes(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, int32_t n,
-                              int32_t w, bool bitmaps) {
+                              int32_t w) {
   if (batch <= 0 || heads_q <= 0 || heads_kv <= 0 || head_dim <= 0 || n < 0 || w < 0) return 0;
   const DecodeSplits s = decode_splits(batch, heads_kv, n, w);
-  size_t bytes = align_up(size_t(batch) * heads_q * s.total() * (head_dim + 2) * sizeof(float), 256);
-  if (bitmaps && n > 0 && n <= kDecodeBitmapMaxKeys)
-    bytes += align_up(size_t(batch) * heads_q * topp_mask_words(n) * sizeof(unsigned long long), 256);
-  return bytes;
+  return align_up(size_t(batch) * heads_q * s.total() * (head_dim + 2) * sizeof(float), 256);
 }
 
 rbq_status check_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_t head_dim, const float* q,
                         const void* K, const void* V, int32_t kv_dtype, int32_t cap, int32_t n, bool sparse,
                         const int32_t* sel_idx, const int32_t* sel_count, const void* K_loc, const void* V_loc,
                         int64_t loc_ld, int32_t w, float sm_scale, const float* out, const void* ws,
-                        size_t ws_bytes, bool bitmaps) {
+                        size_t ws_bytes) {
   rbq_status s = check_heads(batch, heads_q, heads_kv, head_dim);
   if (s != RBQ_OK) return s;
   if (kv_dtype != RBQ_F32 && kv_dtype != RBQ_BF16) return RBQ_EUNSUPPORTED;
@@ -171,8 +168,7 @@ rbq_status check_decode(int32_t batch, int32_t heads_q, int32_t heads_kv, int32_
   // rows of one (sequence, KV head) are addressed with 32-bit byte offsets
   const int64_t row_bytes = int64_t(head_dim) * (kv_dtype == RBQ_BF16 ? 2 : 4);
   if (int64_t(n) * row_bytes >= (int64_t(1) << 31) || int64_t(w) * row_bytes >= (int64_t(1) << 31)) return RBQ_EINVAL;
-  if (bad_ptr(ws) || ws_bytes < decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w, sparse && bitmaps))
-    return RBQ_EINVAL;
+  if (bad_ptr(ws) || ws_bytes < decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w)) return RBQ_EINVAL;
   return RBQ_OK;
 }
 
@@ -218,7 +214,6 @@ size_t rbq_workspace_bytes(int32_t op, int32_t batch, int32_t heads_q, int32_t h
     case RBQ_OP_TOPP:
       return rbq::topp_workspace(nullptr, int64_t(batch) * heads_q, n).bytes;
     case RBQ_OP_SPARSE_DECODE:
-      return rbq::decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w, true);
     case RBQ_OP_DENSE_DECODE:
       return rbq::decode_workspace_bytes(batch, heads_q, heads_kv, head_dim, n, w);
     case RBQ_OP_DECODE_STEP:

@@ -31,7 +31,7 @@ EXPORTED = [
     "rbq_decode_step_varlen", "rbq_quantize_query_bits",
     "rbq_score_q8", "rbq_score_ints_q8", "rbq_mapped_device_pointer",
     "rbq_encode_keys_f16", "rbq_score_f16", "rbq_decode_step_f16", "rbq_score_varlen_f16", "rbq_decode_step_varlen_f16",
-    "rbq_decode_step_noalloc", "rbq_sparse_decode_debug",
+    "rbq_decode_step_noalloc",
 ]
 
 
@@ -58,8 +58,6 @@ def _load():
         "rbq_topp_select": [i32, i32, i32, vp, f32, f32, vp, vp, vp, sz, vp],
         "rbq_sparse_decode": [i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, i64, i32, f32, vp, vp,
                               vp, sz, vp],
-        "rbq_sparse_decode_debug": [i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, i64, i32, f32, vp,
-                                    vp, vp, sz, vp],
         "rbq_dense_decode": [i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, i64, i32, f32, vp, vp, vp, sz,
                              vp],
         "rbq_decode_step": [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, i32, f32, f32,
@@ -256,18 +254,6 @@ def rbq_sparse_decode(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, sel_i
           out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q))
     ws_bytes = ws.numel() * ws.element_size()
     _check("rbq_sparse_decode", lib.rbq_sparse_decode(
-        batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n, _ptr(sel_idx),
-        _ptr(sel_count), _ptr(K_loc), _ptr(V_loc), loc_ld, w, sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws_bytes,
-        _stream(stream)))
-
-
-def rbq_sparse_decode_debug(batch, heads_q, heads_kv, head_dim, q, K, V, cap, n, sel_idx, sel_count, K_loc, V_loc,
-                            loc_ld, w, sm_scale, out, lse, ws, stream=None):
-    """Test hook: rbq_sparse_decode with the row lists built from the index lists."""
-    _need("rbq_sparse_decode_debug", sel_idx=(sel_idx, batch * heads_q * n), sel_count=(sel_count, batch * heads_q),
-          out=(out, batch * heads_q * head_dim), lse=(lse, batch * heads_q))
-    ws_bytes = ws.numel() * ws.element_size()
-    _check("rbq_sparse_decode_debug", lib.rbq_sparse_decode_debug(
         batch, heads_q, heads_kv, head_dim, _ptr(q), _ptr(K), _ptr(V), kv_dtype_code(K), cap, n, _ptr(sel_idx),
         _ptr(sel_count), _ptr(K_loc), _ptr(V_loc), loc_ld, w, sm_scale, _ptr(out), _ptr(lse), _ptr(ws), ws_bytes,
         _stream(stream)))
