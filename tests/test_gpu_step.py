@@ -21,6 +21,8 @@ CASES = [
     (2, 8, 8, 4100, 300, "bf16", 1.0, True, 5),       # p = 1 selects every key
     (1, 8, 2, 0, 64, "bf16", 0.9, True, 6),           # no indexed key: the window only
     (1, 4, 1, 10000, 17, "bf16", 0.5, True, 7),
+    (1, 16, 2, 6000, 64, "bf16", 0.9, True, 8),       # G = 8: the matrix-core scan
+    (1, 32, 8, 65536, 64, "bf16", 0.9, True, 9),      # G = 4, two keys per lane: the matrix-core scan
 ]
 
 
@@ -137,3 +139,59 @@ def test_index_build_beside_prefill_attention(pipeline):
     for hk in range(Hkv):
         pu.check_encode_group(codes[0, hk, :n], kfac[0, hk, :n], ck[0, hk], wl.K_f32(0, hk, slice(0, n)), wl.P,
                               wl.c_q[0, hk])
+
+
+def test_fused_step_any_workspace_contents(pipeline):
+    """The step's workspace needs no initialisation and carries nothing from
+    one call to the next: filled with ones, zeros or random bytes before the
+    call, it gives the outputs of the separate calls."""
+    case = CASES[0]
+    p = case[6]
+    ref = _state(pipeline, case)
+    ref.step_calls(p)
+    want = _outputs(ref)
+    st = _state(pipeline, case)
+    g = torch.Generator(device="cpu").manual_seed(5)
+    for fill in (0xFF, 0x00, None):
+        print("workspace fill", fill, flush=True)
+        if fill is None:
+            st.ws_step.copy_(torch.randint(0, 256, st.ws_step.shape, generator=g, dtype=torch.uint8))
+        else:
+            st.ws_step.fill_(fill)
+        st.step(p)
+        _same(_outputs(st), want)
+
+
+@pytest.mark.parametrize("ci", [0, 4, 7, 8])
+def test_fused_step_graph_replays_new_queries(pipeline, ci):
+    """Each replay of a captured step quantises the query it finds in the
+    buffer: with a new query before every replay (and eager steps between
+    the replays) every replay matches the separate calls on that query."""
+    case = CASES[ci]
+    p = case[6]
+    ref = _state(pipeline, case)
+    st = _state(pipeline, case)
+    q0 = st.q.clone()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        st.step(p)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            st.step(p)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    gen_q = torch.Generator(device="cpu").manual_seed(17 + ci)
+    for i in range(4):
+        print("replay", i, flush=True)
+        qn = (q0.cpu() + 0.5 * torch.randn(q0.shape, generator=gen_q)).to(q0.device)
+        st.q.copy_(qn)
+        ref.q.copy_(qn)
+        ref.step_calls(p)
+        want = _outputs(ref)
+        torch.cuda.synchronize()
+        g.replay()
+        _same(_outputs(st), want)
+        st.step(p)            # eager work between the replays
+        _same(_outputs(st), want)
