@@ -51,7 +51,6 @@ constexpr int kBmWords = kDecodeChunk / 32;                       // words of th
 constexpr int kListRounds = (kDecodeChunk + kDecodeFoldMax + kDThreads - 1) / kDThreads;
 constexpr int kListCap = kListRounds * kDThreads;                 // list positions (indexed + folded window)
 static_assert(kListCap == kDecodeListCap, "the split sizing on the host assumes this list capacity");
-constexpr int kBmAll = kListCap / 32;
 constexpr float kLn2 = 0.69314718055994531f;
 __device__ __forceinline__ float wmax64(float v) { v = max32(v); return fmaxf(v, __shfl_xor(v, 32, kWave)); }
 __device__ __forceinline__ float wsum64(float v) { v = sum32(v); return v + __shfl_xor(v, 32, kWave); }
@@ -129,159 +128,113 @@ __device__ __forceinline__ MaskWords<G> load_mask_words(const unsigned long long
 // the nwin window rows folded into the split (every head; list positions
 // c1 - c0 + i, rows c1 + wshift + i). Returns the
 // number of entries (block-uniform). All threads of the block must call it.
-// Each wave finds the part [lower bound of c0, lower bound of c1) of its
-// heads' selection lists; the entries are then loaded all at once and marked
-// in per-head LDS bitmaps, and the union is compacted with wave ballots.
-//
-// With selection bitmaps (sel_mask != NULL, [rows][mask_words] words of 64
-// keys, c0 a multiple of 64) the list is built from the words themselves,
-// without the searches, the LDS bitmaps and their compaction (below).
+// The list is ranked from the split's 16 words of 64 positions per head
+// (c0 a multiple of 64): the selection's bitmaps themselves when given
+// (sel_mask != NULL, [rows][mask_words] words of 64 keys); otherwise each wave
+// finds the part [lower bound of c0, lower bound of c1) of its heads'
+// selection lists, and the entries, loaded all at once, are marked in
+// per-head LDS bitmaps that then serve as the words.
 template <int G, int kThreads, bool PRE>
 __device__ __forceinline__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
                                 const unsigned long long* __restrict__ sel_mask, int mask_words, int row0,
-                                int n, int c0, int c1, int nwin, int wshift, uint32_t (*bm)[kBmAll], int32_t* lst,
-                                uint16_t* hmask, int* rng_lo, int* rng_hi, int* wcnt, int* ucount,
-                                MaskWords<G> mw) {
+                                int n, int c0, int c1, int nwin, int wshift, uint32_t (*bm)[kBmWords], int32_t* lst,
+                                uint16_t* hmask, int* rng_lo, int* rng_hi, MaskWords<G> mw) {
   constexpr int kWaves = kThreads / kWave;
   const int t = threadIdx.x, wave = t / kWave, lane = lane_id();
-  if (sel_mask) {
-    // Every wave ranks the split's 16 union words itself (no LDS bitmaps): lane l
-    // holds word l % 16 of heads l / 16 + 4k (mw, from load_mask_words when
-    // preloaded), the heads' words are ORed across the rows of 16 lanes, and an
-    // exclusive prefix of their popcounts gives each word's first list entry.
-    // Wave v then writes the entries of words v, v + kWaves, ... and the last
-    // wave the folded window rows; one barrier publishes the list.
-    if (!PRE) mw = load_mask_words<G>(sel_mask, mask_words, row0, c0, c1);
-    const int wd = lane & 15;
-    const int lim = c1 - c0 - 64 * wd;   // positions of word wd inside the split
-    const unsigned long long keep = lim >= 64 ? ~0ull : lim > 0 ? (1ull << lim) - 1ull : 0ull;
-    unsigned long long u = 0ull;
+  const int wd = lane & 15;
+  if (sel_mask == nullptr) {
+    for (int g = wave; g < G; g += kWaves) {
+      const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
+      const int cnt = min(max(sel_count[row0 + g], 0), n);
+      int lo, hi;
+      wave_lower_bounds(sel, cnt, c0, c1, lo, hi);
+      if (lane == 0) {
+        rng_lo[g] = lo;
+        rng_hi[g] = hi;
+      }
+    }
+    for (int e = t; e < G * kBmWords; e += kThreads) bm[e / kBmWords][e % kBmWords] = 0u;
+    __syncthreads();
+    // mark the selected positions: every entry's load first, then the LDS bit sets
+    constexpr int kPer = kDecodeChunk / kThreads;            // entries per thread per head (a split has <= chunk)
+    constexpr int kHB = G < 4 ? G : 4;                      // heads per batch of loads
+#pragma unroll
+    for (int g0 = 0; g0 < G; g0 += kHB) {
+      int pv[kHB][kPer];
+#pragma unroll
+      for (int gg = 0; gg < kHB; ++gg) {
+        const int g = g0 + gg;
+        const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
+        const int lo = rng_lo[g], hi = rng_hi[g];
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {   // (loaded unconditionally, the index clamped into the row, so
+          const int e = lo + u * kThreads + t;   // that every load is in flight at once)
+          const int v = sel[max(min(e, hi - 1), 0)];
+          pv[gg][u] = e < hi ? v - c0 : -1;
+        }
+      }
+#pragma unroll
+      for (int gg = 0; gg < kHB; ++gg)
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+          const int pos = pv[gg][u];
+          if (pos >= 0 && pos < c1 - c0) atomicOr(&bm[g0 + gg][pos >> 5], 1u << (pos & 31));
+        }
+    }
+    __syncthreads();
+    // this lane's words, laid out as load_mask_words gives them
 #pragma unroll
     for (int k = 0; k < (G + 3) / 4; ++k) {
-      mw.w[k] &= keep;
-      u |= mw.w[k];
+      const int g = lane / 16 + 4 * k;
+      mw.w[k] = g < G ? (uint64_t(bm[g][2 * wd + 1]) << 32) | bm[g][2 * wd] : 0ull;
     }
-    u |= swap16_u64(u);   // lanes l and l ^ 16
-    u |= (uint64_t(uint32_t(__shfl_xor(int(uint32_t(u >> 32)), 32, kWave))) << 32) |
-         uint32_t(__shfl_xor(int(uint32_t(u)), 32, kWave));
-    const uint32_t c = uint32_t(__popcll(u));
-    uint32_t inc = c;   // inclusive prefix over the 16 words of each row of lanes
-    inc += RBQ_DPP_U32(inc, 0x111);   // row_shr:1
-    inc += RBQ_DPP_U32(inc, 0x112);   // row_shr:2
-    inc += RBQ_DPP_U32(inc, 0x114);   // row_shr:4
-    inc += RBQ_DPP_U32(inc, 0x118);   // row_shr:8
-    const uint32_t excl = inc - c;
-    const int nidx = __builtin_amdgcn_readlane(int(inc), 15);
-    for (int v = wave; v < kBmWords / 2; v += kWaves) {   // (wave-uniform)
-      const unsigned long long uw = readlane_u64(u, v);
-      const int off = __builtin_amdgcn_readlane(int(excl), v);
-      uint32_t mk = 0u;
+  } else if (!PRE) {
+    mw = load_mask_words<G>(sel_mask, mask_words, row0, c0, c1);
+  }
+  // Every wave ranks the split's 16 union words itself: lane l holds word
+  // l % 16 of heads l / 16 + 4k, the heads' words are ORed across the rows of
+  // 16 lanes, and an exclusive prefix of their popcounts gives each word's
+  // first list entry. Wave v then writes the entries of words v, v + kWaves,
+  // ... and the last wave the folded window rows; one barrier publishes the list.
+  const int lim = c1 - c0 - 64 * wd;   // positions of word wd inside the split
+  const unsigned long long keep = lim >= 64 ? ~0ull : lim > 0 ? (1ull << lim) - 1ull : 0ull;
+  unsigned long long u = 0ull;
 #pragma unroll
-      for (int g = 0; g < G; ++g) mk |= uint32_t((readlane_u64(mw.w[g / 4], (g % 4) * 16 + v) >> lane) & 1ull) << g;
-      if ((uw >> lane) & 1ull) {
-        const int o = off + int(__builtin_amdgcn_mbcnt_hi(uint32_t(uw >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(uw), 0u)));
-        lst[o] = c0 + 64 * v + lane;
-        hmask[o] = uint16_t(mk);
-      }
-    }
-    if (wave == kWaves - 1) {
-      for (int i = lane; i < nwin; i += kWave) {   // the folded window rows, every head
-        lst[nidx + i] = c1 + wshift + i;
-        hmask[nidx + i] = uint16_t((1u << G) - 1u);
-      }
-    }
-    __syncthreads();
-    return nidx + nwin;
-  } else {
-  for (int g = wave; g < G; g += kWaves) {
-    const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
-    const int cnt = min(max(sel_count[row0 + g], 0), n);
-    int lo, hi;
-    wave_lower_bounds(sel, cnt, c0, c1, lo, hi);
-    if (lane == 0) {
-      rng_lo[g] = lo;
-      rng_hi[g] = hi;
+  for (int k = 0; k < (G + 3) / 4; ++k) {
+    mw.w[k] &= keep;
+    u |= mw.w[k];
+  }
+  u |= swap16_u64(u);   // lanes l and l ^ 16
+  u |= (uint64_t(uint32_t(__shfl_xor(int(uint32_t(u >> 32)), 32, kWave))) << 32) |
+       uint32_t(__shfl_xor(int(uint32_t(u)), 32, kWave));
+  const uint32_t c = uint32_t(__popcll(u));
+  uint32_t inc = c;   // inclusive prefix over the 16 words of each row of lanes
+  inc += RBQ_DPP_U32(inc, 0x111);   // row_shr:1
+  inc += RBQ_DPP_U32(inc, 0x112);   // row_shr:2
+  inc += RBQ_DPP_U32(inc, 0x114);   // row_shr:4
+  inc += RBQ_DPP_U32(inc, 0x118);   // row_shr:8
+  const uint32_t excl = inc - c;
+  const int nidx = __builtin_amdgcn_readlane(int(inc), 15);
+  for (int v = wave; v < kBmWords / 2; v += kWaves) {   // (wave-uniform)
+    const unsigned long long uw = readlane_u64(u, v);
+    const int off = __builtin_amdgcn_readlane(int(excl), v);
+    uint32_t mk = 0u;
+#pragma unroll
+    for (int g = 0; g < G; ++g) mk |= uint32_t((readlane_u64(mw.w[g / 4], (g % 4) * 16 + v) >> lane) & 1ull) << g;
+    if ((uw >> lane) & 1ull) {
+      const int o = off + int(__builtin_amdgcn_mbcnt_hi(uint32_t(uw >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(uw), 0u)));
+      lst[o] = c0 + 64 * v + lane;
+      hmask[o] = uint16_t(mk);
     }
   }
-  for (int e = t; e < G * kBmAll; e += kThreads) bm[e / kBmAll][e % kBmAll] = 0u;
-  __syncthreads();
-  // mark the selected positions: every entry's load first, then the LDS bit sets
-  constexpr int kPer = kDecodeChunk / kThreads;            // entries per thread per head (a split has <= chunk)
-  constexpr int kHB = G < 4 ? G : 4;                      // heads per batch of loads
-#pragma unroll
-  for (int g0 = 0; g0 < G; g0 += kHB) {
-    int pv[kHB][kPer];
-#pragma unroll
-    for (int gg = 0; gg < kHB; ++gg) {
-      const int g = g0 + gg;
-      const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
-      const int lo = rng_lo[g], hi = rng_hi[g];
-#pragma unroll
-      for (int u = 0; u < kPer; ++u) {
-        const int e = lo + u * kThreads + t;
-        pv[gg][u] = e < hi ? sel[e] - c0 : -1;
-      }
+  if (wave == kWaves - 1) {
+    for (int i = lane; i < nwin; i += kWave) {   // the folded window rows, every head
+      lst[nidx + i] = c1 + wshift + i;
+      hmask[nidx + i] = uint16_t((1u << G) - 1u);
     }
-#pragma unroll
-    for (int gg = 0; gg < kHB; ++gg)
-#pragma unroll
-      for (int u = 0; u < kPer; ++u) {
-        const int pos = pv[gg][u];
-        if (pos >= 0 && pos < c1 - c0) atomicOr(&bm[g0 + gg][pos >> 5], 1u << (pos & 31));
-      }
   }
   __syncthreads();
-  }
-  // the folded window rows are marked in the first head's bitmap
-  // (their head masks are set to every head below)
-  const int ce = c1 + nwin;   // list positions end at ce - c0
-  if (nwin > 0) {
-    for (int e = c1 - c0 + t; e < ce - c0; e += kThreads) atomicOr(&bm[0][e >> 5], 1u << (e & 31));
-    __syncthreads();
-  }
-  // union of the G bitmaps, compacted in ascending position order: position
-  // r * kThreads + t in round r, ranked by wave ballots
-  constexpr int kRounds = kListRounds;
-  static_assert(kThreads == kDThreads, "list sizes assume the decode block");
-  bool f[kRounds];
-  uint64_t bal[kRounds];
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const int pos = r * kThreads + t;
-    uint32_t any = 0u;
-#pragma unroll
-    for (int g = 0; g < G; ++g) any |= bm[g][pos >> 5];
-    f[r] = pos < ce - c0 && ((any >> (pos & 31)) & 1u);
-    bal[r] = __ballot(f[r]);
-    if (lane == 0) wcnt[r * kWaves + wave] = __popcll(bal[r]);
-  }
-  __syncthreads();
-  int base = 0;
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    int woff = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const int cw = wcnt[r * kWaves + w];
-      woff += w < wave ? cw : 0;
-      tot += cw;
-    }
-    if (f[r]) {
-      const int pos = r * kThreads + t;
-      const int o = base + woff + __builtin_amdgcn_mbcnt_hi(uint32_t(bal[r] >> 32),
-                                                            __builtin_amdgcn_mbcnt_lo(uint32_t(bal[r]), 0u));
-      uint32_t mk32 = 0u;
-#pragma unroll
-      for (int g = 0; g < G; ++g) mk32 |= ((bm[g][pos >> 5] >> (pos & 31)) & 1u) << g;
-      const uint16_t mk = uint16_t(pos >= c1 - c0 ? (1u << G) - 1u : mk32);   // window rows: every head
-      lst[o] = c0 + pos + (pos >= c1 - c0 ? wshift : 0);
-      hmask[o] = mk;
-    }
-    base += tot;
-  }
-  if (t == 0) *ucount = base;
-  __syncthreads();
-  return *ucount;
+  return nidx + nwin;
 }
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -354,12 +307,10 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
     const int32_t* __restrict__ seq_w) {
   constexpr int kElem = DT == RBQ_BF16 ? 2 : 4;
   __shared__ float qs[G][D];
-  __shared__ uint32_t bm[G][kBmAll];
+  __shared__ uint32_t bm[SPARSE ? G : 1][kBmWords];
   __shared__ int32_t lst[SPARSE ? kListCap : 1];
   __shared__ uint16_t hmask[SPARSE ? kListCap : 1];
   __shared__ int rng_lo[G], rng_hi[G];
-  __shared__ int wcnt[kBmAll];
-  __shared__ int ucount;
   __shared__ float ps[kDWaves][G][kWave];
   __shared__ float sm[kDWaves][G], sl[kDWaves][G];
   __shared__ float sacc[kDWaves][G][D];
@@ -414,8 +365,8 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   const bool use_list = SPARSE && !window;
   int U;
   if (use_list) {
-    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
-                                       &ucount, mword);
+    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi,
+                                       mword);
   } else {
     __syncthreads();
     U = (c1 - c0) + nwin;
@@ -625,12 +576,10 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   constexpr int KB = D / 32;                      // k-blocks of the logits product
   constexpr int VB = D / 32;                      // value blocks per parity (D / 16 columns per lane)
   __shared__ u32x4 qB[KB][kQOps][kWave];          // B operands of the logits product
-  __shared__ uint32_t bm[G][kBmAll];
+  __shared__ uint32_t bm[SPARSE ? G : 1][kBmWords];
   __shared__ int32_t lst[SPARSE ? kListCap : 1];
   __shared__ uint16_t hmask[SPARSE ? kListCap : 1];
   __shared__ int rng_lo[G], rng_hi[G];
-  __shared__ int wcnt[kBmAll];
-  __shared__ int ucount;
   __shared__ float sm[kDWaves][G], sl[kDWaves][G];
   __shared__ float sacc[kDWaves][G][D];
 
@@ -712,8 +661,8 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
 
   int U;
   if (SPARSE && !window) {
-    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi, wcnt,
-                                       &ucount, mword);
+    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi,
+                                       mword);
   } else {
     __syncthreads();
     U = (c1 - c0) + nwin;
