@@ -73,8 +73,11 @@ __device__ __forceinline__ void wave_lower_bounds(const int32_t* __restrict__ a,
   while (hi0 > lo0 || hi1 > lo1) {
     const int st0 = (hi0 - lo0 + kWave - 1) / kWave, st1 = (hi1 - lo1 + kWave - 1) / kWave;
     const int p0 = lo0 + lane * st0, p1 = lo1 + lane * st1;
-    const bool lt0 = p0 < hi0 && a[p0] < x0;
-    const bool lt1 = p1 < hi1 && a[p1] < x1;
+    // both probes' loads unconditionally, the indices clamped into the list
+    // (which holds an entry here: cnt > lo >= 0), so that they are in flight together
+    const int v0 = a[min(p0, cnt - 1)], v1 = a[min(p1, cnt - 1)];
+    const bool lt0 = p0 < hi0 && v0 < x0;
+    const bool lt1 = p1 < hi1 && v1 < x1;
     const int k0 = __popcll(__ballot(lt0)), k1 = __popcll(__ballot(lt1));   // the first k probes are below x
     if (hi0 > lo0) {
       if (k0 == 0) {
@@ -122,6 +125,25 @@ __device__ __forceinline__ MaskWords<G> load_mask_words(const unsigned long long
   return m;
 }
 
+// The selection counts of this wave's heads (wave, wave + kDWaves, ...) for
+// the searches of the separate sparse call, requested at the start of the
+// kernel so that the load overlaps the query staging.
+template <int G>
+struct HeadCounts {
+  int c[(G + kDWaves - 1) / kDWaves];
+};
+template <int G>
+__device__ __forceinline__ HeadCounts<G> load_head_counts(const int32_t* __restrict__ sel_count, int row0) {
+  HeadCounts<G> h;
+  const int wave = threadIdx.x / kWave;
+#pragma unroll
+  for (int i = 0; i < (G + kDWaves - 1) / kDWaves; ++i) {
+    const int g = min(wave + kDWaves * i, G - 1);   // (a wave past the heads loads the last one's, unused)
+    h.c[i] = sel_count[row0 + g];                    // (clamped where it is used: no wait here)
+  }
+  return h;
+}
+
 // Per-block row list of a sparse split: the union over the G heads of the
 // group of the positions in [c0, c1) that each head selected, in ascending
 // order, with a bit mask of the heads that selected each entry, followed by
@@ -138,14 +160,19 @@ template <int G, int kThreads, bool PRE>
 __device__ __forceinline__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
                                 const unsigned long long* __restrict__ sel_mask, int mask_words, int row0,
                                 int n, int c0, int c1, int nwin, int wshift, uint32_t (*bm)[kBmWords], int32_t* lst,
-                                uint16_t* hmask, int* rng_lo, int* rng_hi, MaskWords<G> mw) {
+                                uint16_t* hmask, int* rng_lo, int* rng_hi, MaskWords<G> mw,
+                                const HeadCounts<G>& hc) {
   constexpr int kWaves = kThreads / kWave;
   const int t = threadIdx.x, wave = t / kWave, lane = lane_id();
   const int wd = lane & 15;
   if (sel_mask == nullptr) {
-    for (int g = wave; g < G; g += kWaves) {
+    static_assert(kWaves == kDWaves, "the preloaded counts assume the decode block");
+#pragma unroll
+    for (int i = 0; i < (G + kWaves - 1) / kWaves; ++i) {
+      const int g = wave + kWaves * i;
+      if (g >= G) break;   // (wave-uniform)
       const int32_t* sel = sel_idx + int64_t(row0 + g) * n;
-      const int cnt = min(max(sel_count[row0 + g], 0), n);
+      const int cnt = min(max(hc.c[i], 0), n);
       int lo, hi;
       wave_lower_bounds(sel, cnt, c0, c1, lo, hi);
       if (lane == 0) {
@@ -358,6 +385,8 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   constexpr bool kPreMask = G <= 4;   // (for larger groups the early load costs registers)
   MaskWords<G> mword{};
   if (kPreMask && SPARSE && !window) mword = load_mask_words<G>(sel_mask, mask_words, row0, c0, c1);
+  HeadCounts<G> hcount{};   // (loaded in every sparse block, used by the search only: no branch, no early wait)
+  if constexpr (SPARSE) hcount = load_head_counts<G>(sel_count, row0);
   for (int e = threadIdx.x; e < G * D; e += kDThreads)
     qs[e / D][e % D] = q[int64_t(row0) * D + e] * scale_log2e;
 
@@ -366,7 +395,7 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   int U;
   if (use_list) {
     U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi,
-                                       mword);
+                                       mword, hcount);
   } else {
     __syncthreads();
     U = (c1 - c0) + nwin;
@@ -626,6 +655,8 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   constexpr bool kPreMask = kPackedQ;   // (for larger groups the early load costs registers)
   MaskWords<G> mword{};
   if (kPreMask && SPARSE && !window) mword = load_mask_words<G>(sel_mask, mask_words, row0, c0, c1);
+  HeadCounts<G> hcount{};   // (loaded in every sparse block, used by the search only: no branch, no early wait)
+  if constexpr (SPARSE) hcount = load_head_counts<G>(sel_count, row0);
 
   // query operands, lane (column c, quarter jj) of k-block kb = dims 32 kb + 8 jj .. +8.
   // G <= 4: one operand per k-block, column c = part * G + head; otherwise one
@@ -662,7 +693,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
   int U;
   if (SPARSE && !window) {
     U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi,
-                                       mword);
+                                       mword, hcount);
   } else {
     __syncthreads();
     U = (c1 - c0) + nwin;
