@@ -228,18 +228,25 @@ def _graph(torch, fn):
     return g
 
 
-def _time_graphs(torch, graphs, steps, warmup):
-    """Replay the graphs round-robin; mean ms per replay between two HIP events."""
+def _time_graphs(torch, graphs, steps, warmup, windows=3):
+    """Replay the graphs round-robin: `warmup` untimed replays, then the mean ms
+    per replay between two HIP events around `steps` replays, the median over
+    `windows` such windows (a stall of the GPU in one window then moves no
+    figure). The bench line's own step and dense times take one window of
+    exactly `steps` replays."""
     for i in range(warmup):
         graphs[i % len(graphs)].replay()
     torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for i in range(steps):
-        graphs[i % len(graphs)].replay()
-    b.record()
-    torch.cuda.synchronize()
-    return a.elapsed_time(b) / steps
+    times = []
+    for _ in range(windows):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(steps):
+            graphs[i % len(graphs)].replay()
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b) / steps)
+    return float(np.median(times))
 
 
 def _replay_distribution(torch, graphs, reps=50, warmup=10):
@@ -739,8 +746,10 @@ def prefill_overlap(torch, st, steps=3):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # (100 timed replays of a ~0.1 ms step: a window of ~10 ms, so that one stall of the
+    # GPU does not move the line; 30 warm-up replays settle the clocks after the set-up)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--p", type=float, default=0.95)
     ap.add_argument("--replicas", type=int, default=4)
     ap.add_argument("--no-scan", action="store_true", help="skip the standalone wide-head scan")
@@ -795,7 +804,7 @@ def main():
     # the whole step (rbq_decode_step), one HIP graph per replica; then the same step
     # as the five separate calls, for reference
     step_graphs = [_graph(torch, lambda r=r: r.step(p)) for r in reps]
-    ms_step = _time_graphs(torch, step_graphs, args.steps, args.warmup)
+    ms_step = _time_graphs(torch, step_graphs, args.steps, args.warmup, windows=1)
     step_dist = _replay_distribution(torch, step_graphs)
     call_graphs = [_graph(torch, lambda r=r: r.step_calls(p)) for r in reps]
     ms_step_calls = _time_graphs(torch, call_graphs, args.steps, args.warmup)
@@ -824,7 +833,7 @@ def main():
     dense_out = torch.empty_like(st0.out)
     dense_lse = torch.empty_like(st0.lse)
     dense_graphs = [_graph(torch, lambda r=r: r.dense_decode(dense_out, dense_lse)) for r in reps]
-    dense_ms = _time_graphs(torch, dense_graphs, args.steps, args.warmup)
+    dense_ms = _time_graphs(torch, dense_graphs, args.steps, args.warmup, windows=1)
     del dense_graphs
     sdpa_ms = None
     try:
