@@ -150,14 +150,14 @@ __device__ __forceinline__ HeadCounts<G> load_head_counts(const int32_t* __restr
 // the nwin window rows folded into the split (every head; list positions
 // c1 - c0 + i, rows c1 + wshift + i). Returns the
 // number of entries (block-uniform). All threads of the block must call it.
-// The list is ranked from the split's 16 words of 64 positions per head
-// (c0 a multiple of 64): the selection's bitmaps themselves when given
-// (sel_mask != NULL, [rows][mask_words] words of 64 keys); otherwise each wave
-// finds the part [lower bound of c0, lower bound of c1) of its heads'
-// selection lists, and the entries, loaded all at once, are marked in
-// per-head LDS bitmaps that then serve as the words.
+// The list is ranked from the split's 16 words of 64 positions per head: the
+// selection's bitmaps themselves when given (sel_mask != NULL, [rows][mask_words]
+// words of 64 keys, c0 a multiple of 64); otherwise each wave finds the part
+// [lower bound of c0, lower bound of c1) of its heads' selection lists (their
+// counts in hc), and the entries, loaded all at once, are marked in per-head
+// LDS bitmaps that then serve as the words.
 template <int G, int kThreads, bool PRE>
-__device__ __forceinline__ int build_union_list(const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_count,
+__device__ __forceinline__ int build_union_list(const int32_t* __restrict__ sel_idx,
                                 const unsigned long long* __restrict__ sel_mask, int mask_words, int row0,
                                 int n, int c0, int c1, int nwin, int wshift, uint32_t (*bm)[kBmWords], int32_t* lst,
                                 uint16_t* hmask, int* rng_lo, int* rng_hi, MaskWords<G> mw,
@@ -394,7 +394,7 @@ __global__ __launch_bounds__(kDThreads) void decode_vec_kernel(
   const bool use_list = SPARSE && !window;
   int U;
   if (use_list) {
-    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi,
+    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi,
                                        mword, hcount);
   } else {
     __syncthreads();
@@ -692,7 +692,7 @@ __global__ __launch_bounds__(kDThreads) void decode_mfma_kernel(
 
   int U;
   if (SPARSE && !window) {
-    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_count, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi,
+    U = build_union_list<G, kDThreads, kPreMask>(sel_idx, sel_mask, mask_words, row0, n, c0, c1, nwin, wrow0 - c1, bm, lst, hmask, rng_lo, rng_hi,
                                        mword, hcount);
   } else {
     __syncthreads();
